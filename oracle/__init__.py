@@ -1,0 +1,210 @@
+"""TEST INFRASTRUCTURE ONLY: Python access to the CPU reference ("oracle").
+
+The oracle is a plain double-precision C implementation of BUDDY's
+budget-routed decode step (arXiv 2606.09514; Sec. 3.1 Eq. 1, Sec. 4.2 Eq. 2,
+Sec. 4.3, App. C.1, Sec. 6 limitations).  Only the tests, the smoke check and
+the benchmark's CPU-baseline leg may import this package; the product path
+never does, and nothing here imports the product package.
+
+Storage arrays are numpy: bf16 as ``np.uint16`` bit patterns, fp32 as
+``np.float32``.  A sequence's cache for one layer is ``[n_kv][max_ctx][hd]``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SO = os.path.join(_HERE, "liboracle.so")
+_SRC = os.path.join(_HERE, "buddy_oracle.c")
+
+ACTS = {"silu": 0, "gelu": 1}
+DTYPES = {"f32": 0, "bf16": 1}
+
+
+def build() -> str:
+    """Compile the oracle with gcc (no fast-math, no FP contraction)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-ffp-contract=off", "-fopenmp",
+           "-fPIC", "-shared", _SRC, "-o", _SO + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_SO + ".tmp", _SO)
+    return _SO
+
+
+class _Config(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ffn", C.c_int32),
+                ("dm_hidden", C.c_int32), ("dm_act", C.c_int32), ("dtype", C.c_int32),
+                ("max_ctx", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double)]
+
+
+class _Layer(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in
+                ("attn_norm", "wqkv", "wo", "mlp_norm", "wgate_up", "wdown")]
+
+
+class _DM(C.Structure):
+    _fields_ = [("w1", C.c_void_p), ("b1", C.c_void_p), ("w2", C.c_void_p),
+                ("b2", C.c_void_p), ("prior", C.c_void_p), ("omega", C.c_double)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO):
+            build()
+        L = C.CDLL(_SO)
+        vp, i32, dp = C.c_void_p, C.c_int32, C.POINTER(C.c_double)
+        L.orc_bf16_from_double.argtypes = [C.c_double]
+        L.orc_bf16_from_double.restype = C.c_uint16
+        L.orc_rmsnorm.argtypes = [C.POINTER(_Config), vp, vp, vp]
+        L.orc_rope.argtypes = [C.POINTER(_Config), vp, i32]
+        L.orc_block.argtypes = [C.POINTER(_Config), C.POINTER(_Layer), vp, vp, i32, vp]
+        L.orc_pool.argtypes = [C.POINTER(_Config), vp, vp, i32, vp]
+        L.orc_dm_scores.argtypes = [C.POINTER(_Config), C.POINTER(_DM), vp, vp]
+        L.orc_topk.argtypes = [vp, i32, i32, vp, dp]
+        L.orc_topk.restype = C.c_int
+        L.orc_decode_seq.argtypes = [C.POINTER(_Config), C.POINTER(_Layer), C.POINTER(_DM),
+                                     vp, vp, i32, i32, vp, vp, vp, vp, vp, dp,
+                                     C.POINTER(C.c_int32)]
+        L.orc_decode_seq.restype = C.c_int
+        L.orc_num_threads.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _need(a, dtype, name):
+    if not (isinstance(a, np.ndarray) and a.dtype == dtype and a.flags.c_contiguous):
+        raise TypeError(f"{name}: expected a C-contiguous {np.dtype(dtype).name} array")
+    return a
+
+
+def bf16_from_double(x: float) -> int:
+    return int(lib().orc_bf16_from_double(float(x)))
+
+
+def num_threads() -> int:
+    return int(lib().orc_num_threads())
+
+
+class Oracle:
+    """Holds a model (weights as numpy storage arrays) for the C oracle.
+
+    cfg keys: n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn,
+    dm_hidden, dm_act ('silu'|'gelu'), dtype ('f32'|'bf16'), max_ctx,
+    rms_eps, rope_theta.  layers: list of dicts with attn_norm, wqkv, wo,
+    mlp_norm, wgate_up, wdown.  dm: dict with w1, b1, w2, b2, prior (float32
+    or None) and omega.
+    """
+
+    def __init__(self, cfg: dict, layers: list, dm: dict | None):
+        self.cfg = dict(cfg)
+        self.sdt = np.uint16 if cfg["dtype"] == "bf16" else np.float32
+        self._c = _Config(cfg["n_layers"], cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"],
+                          cfg["head_dim"], cfg["d_ffn"], cfg.get("dm_hidden", 0),
+                          ACTS[cfg.get("dm_act", "silu")], DTYPES[cfg["dtype"]],
+                          cfg["max_ctx"], float(cfg["rms_eps"]), float(cfg["rope_theta"]))
+        self._keep = []
+        arr = (_Layer * len(layers))()
+        for i, lw in enumerate(layers):
+            for n in _Layer._fields_:
+                a = _need(lw[n[0]], self.sdt, n[0])
+                self._keep.append(a)
+                setattr(arr[i], n[0], a.ctypes.data)
+        self._layers = arr
+        self._dm = None
+        if dm is not None:
+            d = _DM()
+            for n in ("w1", "b1", "w2", "b2"):
+                a = _need(dm[n], self.sdt, n)
+                self._keep.append(a)
+                setattr(d, n, a.ctypes.data)
+            pr = dm.get("prior")
+            if pr is not None:
+                pr = _need(pr, np.float32, "prior")
+                self._keep.append(pr)
+                d.prior = pr.ctypes.data
+            d.omega = float(dm.get("omega", 0.0))
+            self._dm = d
+
+    @property
+    def L_mid(self) -> int:
+        return self.cfg["n_layers"] - 2
+
+    # -- pieces ---------------------------------------------------------
+    def rmsnorm(self, h, g):
+        h = np.ascontiguousarray(h, dtype=np.float64)
+        out = np.empty_like(h)
+        lib().orc_rmsnorm(C.byref(self._c), _ptr(h), _ptr(_need(g, self.sdt, "g")), _ptr(out))
+        return out
+
+    def rope(self, x, pos: int):
+        x = np.array(x, dtype=np.float64, copy=True)
+        lib().orc_rope(C.byref(self._c), _ptr(x), int(pos))
+        return x
+
+    def block(self, layer: int, kc, vc, pos: int, h):
+        h = np.array(h, dtype=np.float64, copy=True)
+        lib().orc_block(C.byref(self._c), C.byref(self._layers[layer]),
+                        _ptr(_need(kc, self.sdt, "kc")), _ptr(_need(vc, self.sdt, "vc")),
+                        int(pos), _ptr(h))
+        return h
+
+    def pool(self, kc, vc, pos: int):
+        n = self.cfg["n_kv_heads"] * self.cfg["head_dim"]
+        z = np.empty(2 * n, dtype=np.float64)
+        lib().orc_pool(C.byref(self._c), _ptr(_need(kc, self.sdt, "kc")),
+                       _ptr(_need(vc, self.sdt, "vc")), int(pos), _ptr(z))
+        return z
+
+    def dm_scores(self, z):
+        z = np.ascontiguousarray(z, dtype=np.float64)
+        s = np.empty(self.L_mid, dtype=np.float32)
+        lib().orc_dm_scores(C.byref(self._c), C.byref(self._dm), _ptr(z), _ptr(s))
+        return s
+
+    @staticmethod
+    def topk(scores, k: int):
+        s = np.ascontiguousarray(scores, dtype=np.float32)
+        m = np.zeros(s.shape[0], dtype=np.uint8)
+        margin = C.c_double(0.0)
+        rc = lib().orc_topk(_ptr(s), s.shape[0], int(k), _ptr(m), C.byref(margin))
+        if rc != 0:
+            raise ValueError("k out of range")
+        return m, margin.value
+
+    # -- the whole step --------------------------------------------------
+    def decode_seq(self, kcs, vcs, pos: int, k: int, x, route=None):
+        """One decode step of one sequence.  kcs/vcs: per-layer cache arrays
+        (modified in place).  Returns (h, mask, scores, margin, n_exec)."""
+        L = self.cfg["n_layers"]
+        assert len(kcs) == L and len(vcs) == L
+        kp = (C.c_void_p * L)(*[_need(a, self.sdt, "kc").ctypes.data for a in kcs])
+        vp = (C.c_void_p * L)(*[_need(a, self.sdt, "vc").ctypes.data for a in vcs])
+        x = np.ascontiguousarray(x, dtype=np.float32)
+        h = np.empty(self.cfg["d_model"], dtype=np.float64)
+        mask = np.zeros(self.L_mid, dtype=np.uint8)
+        scores = np.zeros(self.L_mid, dtype=np.float32)
+        margin = C.c_double(0.0)
+        n_exec = C.c_int32(0)
+        r = None
+        if route is not None:
+            r = np.ascontiguousarray(route, dtype=np.uint8)
+            mask[:] = r
+        rc = lib().orc_decode_seq(C.byref(self._c), self._layers,
+                                  C.byref(self._dm) if self._dm is not None else None,
+                                  kp, vp, int(pos), int(k), _ptr(r), _ptr(x), _ptr(h),
+                                  _ptr(mask), _ptr(scores), C.byref(margin), C.byref(n_exec))
+        if rc != 0:
+            raise ValueError("oracle rejected the arguments")
+        return h, mask, scores, margin.value, n_exec.value

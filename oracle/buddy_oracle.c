@@ -1,0 +1,353 @@
+/*
+ * buddy_oracle.c -- TEST INFRASTRUCTURE ONLY: the CPU reference ("oracle")
+ * of BUDDY's budget-routed decode step (arXiv 2606.09514).
+ *
+ * Only tests, the smoke check and the benchmark's CPU-baseline leg may load
+ * this file's library.  It shares no code, header or table with the GPU
+ * library.  Everything is computed in IEEE double with plain loops in the
+ * order the method states it; OpenMP only splits independent output rows, so
+ * results do not depend on the thread count.
+ *
+ * Paper passages followed (section / equation of the paper):
+ *   - layer skipping, Sec. 3.1 Eq. (1): a skipped block is the identity on H;
+ *   - first and last blocks always run, k = round(b L) - 2 routable blocks,
+ *     Sec. 4.2.1 and Eq. (2);
+ *   - score fusion s' = s + omega p~ and top-k selection, Eq. (2);
+ *   - two-layer MLP scorer over pooled context, Sec. 4.2.3 and App. C.1;
+ *   - KV-aware planner: the first layer's KV cache plus the newest token as
+ *     the router context, Sec. 4.3;
+ *   - skipped layers store zero-filled K/V, Sec. 6 (limitations);
+ *   - decode attention over the cache with the new token appended,
+ *     App. "Background" (prefill vs decode, KV-cache equation);
+ *   - the Llama-style block (Q/K/V/O projections, attention, d -> d_c -> d
+ *     MLP), App. C.2.
+ * Readings where the paper is silent are listed at each function.
+ */
+#include "buddy_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ---------------------------------------------------------------- storage */
+
+static double ld(const void* p, size_t i, int dtype)
+{
+    if (dtype == ORC_BF16) {
+        uint32_t bits = (uint32_t)((const uint16_t*)p)[i] << 16;
+        float f;
+        memcpy(&f, &bits, 4);
+        return (double)f;
+    }
+    return (double)((const float*)p)[i];
+}
+
+uint16_t orc_bf16_from_double(double x)
+{
+    if (isnan(x)) return 0x7FC0;
+    /* bf16 keeps 8 significant bits; exponent range as fp32.  Round the
+     * exact value to the nearest representable value, ties to even, by
+     * scaling onto an integer grid and using the current (nearest-even)
+     * rounding mode of nearbyint. */
+    double ax = fabs(x), r;
+    if (ax == 0.0 || isinf(x)) {
+        r = ax;
+    } else {
+        int e;
+        frexp(ax, &e);                 /* ax = m 2^e, 0.5 <= m < 1 */
+        int q = e - 8;                 /* quantum of the 8-bit significand */
+        if (q < -133) q = -133;        /* subnormal bf16 quantum is 2^-133 */
+        r = ldexp(nearbyint(ldexp(ax, -q)), q);
+        if (r > 3.3895313892515355e38) r = INFINITY; /* beyond max finite */
+    }
+    float f = (float)r;                /* exact: r is a bf16 value */
+    uint32_t bits;
+    memcpy(&bits, &f, 4);
+    bits >>= 16;
+    if (x < 0 || (x == 0 && signbit(x))) bits |= 0x8000;
+    return (uint16_t)bits;
+}
+
+static void st(void* p, size_t i, int dtype, double v)
+{
+    if (dtype == ORC_BF16)
+        ((uint16_t*)p)[i] = orc_bf16_from_double(v);
+    else
+        ((float*)p)[i] = (float)v;
+}
+
+int orc_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* y[o] = sum_k W[row0 + o][k] x[k], o < rows; W row-major with `cols` columns. */
+static void matvec(const void* W, int dtype, int64_t row0, int64_t rows,
+                   int64_t cols, const double* x, double* y)
+{
+#pragma omp parallel for schedule(static) if (rows * cols > 65536)
+    for (int64_t o = 0; o < rows; ++o) {
+        double acc = 0.0;
+        size_t base = (size_t)(row0 + o) * (size_t)cols;
+        for (int64_t k = 0; k < cols; ++k) acc += ld(W, base + k, dtype) * x[k];
+        y[o] = acc;
+    }
+}
+
+/* ------------------------------------------------------------------ block */
+
+/* RMSNorm as used by Llama-style blocks (App. C.2 names the block layout;
+ * the normalisation itself follows the Llama convention). */
+void orc_rmsnorm(const orc_config* c, const double* h, const void* g, double* out)
+{
+    int d = c->d_model;
+    double ss = 0.0;
+    for (int i = 0; i < d; ++i) ss += h[i] * h[i];
+    double inv = 1.0 / sqrt(ss / d + c->rms_eps);
+    for (int i = 0; i < d; ++i) out[i] = h[i] * inv * ld(g, i, c->dtype);
+}
+
+/* Rotary position embedding, rotate-half pairing (i, i + hd/2) with angle
+ * pos * theta^(-2i/hd).  The paper only names a Llama-style block; this is
+ * the Llama convention. */
+void orc_rope(const orc_config* c, double* x, int32_t pos)
+{
+    int half = c->head_dim / 2;
+    for (int i = 0; i < half; ++i) {
+        double inv_freq = pow(c->rope_theta, -2.0 * i / c->head_dim);
+        double ang = (double)pos * inv_freq;
+        double cs = cos(ang), sn = sin(ang);
+        double a = x[i], b = x[i + half];
+        x[i] = a * cs - b * sn;
+        x[i + half] = b * cs + a * sn;
+    }
+}
+
+static double act_silu(double x) { return x / (1.0 + exp(-x)); }
+static double act_gelu(double x) { return 0.5 * x * (1.0 + erf(x / sqrt(2.0))); }
+
+void orc_block(const orc_config* c, const orc_layer* w, void* kc, void* vc,
+               int32_t pos, double* h)
+{
+    const int d = c->d_model, nq = c->n_heads, nkv = c->n_kv_heads;
+    const int hd = c->head_dim, f = c->d_ffn, T = c->max_ctx, dt = c->dtype;
+    const int nqkv = (nq + 2 * nkv) * hd;
+    double* u = malloc(sizeof(double) * d);
+    double* qkv = malloc(sizeof(double) * nqkv);
+    double* o = malloc(sizeof(double) * nq * hd);
+    double* y = malloc(sizeof(double) * (d > 2 * f ? d : 2 * f));
+    double* m = malloc(sizeof(double) * f);
+    double* p = malloc(sizeof(double) * (pos + 1));
+
+    /* attention half: u = RMSNorm(h); [q;k;v] = Wqkv u; RoPE on q and k */
+    orc_rmsnorm(c, h, w->attn_norm, u);
+    matvec(w->wqkv, dt, 0, nqkv, d, u, qkv);
+    double* q = qkv;
+    double* kn = qkv + nq * hd;
+    double* vn = qkv + (nq + nkv) * hd;
+    for (int hh = 0; hh < nq; ++hh) orc_rope(c, q + hh * hd, pos);
+    for (int g = 0; g < nkv; ++g) orc_rope(c, kn + g * hd, pos);
+
+    /* KV-cache update: the new row is stored at pos in storage precision */
+    for (int g = 0; g < nkv; ++g)
+        for (int i = 0; i < hd; ++i) {
+            size_t at = ((size_t)g * T + pos) * hd + i;
+            st(kc, at, dt, kn[g * hd + i]);
+            st(vc, at, dt, vn[g * hd + i]);
+        }
+
+    /* decode attention of each query head over positions 0..pos of its KV
+     * group g = floor(h / (nq / nkv)), scale 1/sqrt(hd), softmax, sum p V */
+    const double scale = 1.0 / sqrt((double)hd);
+    const int grp = nq / nkv;
+    for (int hh = 0; hh < nq; ++hh) {
+        int g = hh / grp;
+        double mx = -INFINITY;
+        for (int j = 0; j <= pos; ++j) {
+            double s = 0.0;
+            for (int i = 0; i < hd; ++i)
+                s += q[hh * hd + i] * ld(kc, ((size_t)g * T + j) * hd + i, dt);
+            p[j] = s * scale;
+            if (p[j] > mx) mx = p[j];
+        }
+        double den = 0.0;
+        for (int j = 0; j <= pos; ++j) {
+            p[j] = exp(p[j] - mx);
+            den += p[j];
+        }
+        for (int i = 0; i < hd; ++i) {
+            double acc = 0.0;
+            for (int j = 0; j <= pos; ++j)
+                acc += p[j] * ld(vc, ((size_t)g * T + j) * hd + i, dt);
+            o[hh * hd + i] = acc / den;
+        }
+    }
+
+    /* h <- h + Wo o */
+    matvec(w->wo, dt, 0, d, nq * hd, o, y);
+    for (int i = 0; i < d; ++i) h[i] += y[i];
+
+    /* MLP half: h <- h + Wdown (SiLU(Wgate u2) * (Wup u2)), u2 = RMSNorm(h) */
+    orc_rmsnorm(c, h, w->mlp_norm, u);
+    matvec(w->wgate_up, dt, 0, 2 * (int64_t)f, d, u, y);
+    for (int i = 0; i < f; ++i) m[i] = act_silu(y[i]) * y[f + i];
+    matvec(w->wdown, dt, 0, d, f, m, y);
+    for (int i = 0; i < d; ++i) h[i] += y[i];
+
+    free(u); free(qkv); free(o); free(y); free(m); free(p);
+}
+
+/* ----------------------------------------------------------------- router */
+
+/* KV-aware planner (Sec. 4.3): the first layer's cache, with the newest
+ * token's row already appended, is averaged over positions 0..pos. */
+void orc_pool(const orc_config* c, const void* kc, const void* vc, int32_t pos,
+              double* z)
+{
+    const int nkv = c->n_kv_heads, hd = c->head_dim, T = c->max_ctx;
+    const int n = nkv * hd;
+    for (int g = 0; g < nkv; ++g)
+        for (int i = 0; i < hd; ++i) {
+            double sk = 0.0, sv = 0.0;
+            for (int j = 0; j <= pos; ++j) {
+                size_t at = ((size_t)g * T + j) * hd + i;
+                sk += ld(kc, at, c->dtype);
+                sv += ld(vc, at, c->dtype);
+            }
+            z[g * hd + i] = sk / (pos + 1);
+            z[n + g * hd + i] = sv / (pos + 1);
+        }
+}
+
+/* Decision Module scorer (Sec. 4.2.3, App. C.1): Linear - act - Linear, then
+ * the prior fusion of Eq. (2).  The softmax of Eq. (2) is monotone and is not
+ * needed to select the top k. */
+void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
+                   float* scores)
+{
+    const int H = c->dm_hidden, Lm = c->n_layers - 2;
+    const int din = 2 * c->n_kv_heads * c->head_dim + c->d_model;
+    double* a = malloc(sizeof(double) * H);
+    double* s = malloc(sizeof(double) * Lm);
+    matvec(dm->w1, c->dtype, 0, H, din, z, a);
+    for (int j = 0; j < H; ++j) {
+        double x = a[j] + ld(dm->b1, j, c->dtype);
+        a[j] = c->dm_act == ORC_ACT_GELU_ERF ? act_gelu(x) : act_silu(x);
+    }
+    matvec(dm->w2, c->dtype, 0, Lm, H, a, s);
+    for (int i = 0; i < Lm; ++i) {
+        double v = s[i] + ld(dm->b2, i, c->dtype);
+        if (dm->prior) v += dm->omega * (double)dm->prior[i];
+        scores[i] = (float)v;
+    }
+    free(a); free(s);
+}
+
+/* Deterministic ordering for the hard top-k (Eq. 2): larger score first,
+ * equal scores by lower layer index, NaN after every number. */
+static const float* g_cmp_scores;  /* set only under the single-threaded qsort below */
+
+static int cmp_rank(const void* pa, const void* pb)
+{
+    int32_t a = *(const int32_t*)pa, b = *(const int32_t*)pb;
+    float sa = g_cmp_scores[a], sb = g_cmp_scores[b];
+    int na = isnan(sa), nb = isnan(sb);
+    if (na != nb) return na ? 1 : -1;
+    if (!na && sa != sb) return sa > sb ? -1 : 1;
+    return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+int orc_topk(const float* scores, int32_t n, int32_t k, uint8_t* mask,
+             double* margin)
+{
+    if (n < 0 || k < 0 || k > n) return -1;
+    int32_t* order = malloc(sizeof(int32_t) * (n > 0 ? n : 1));
+    for (int32_t i = 0; i < n; ++i) order[i] = i;
+#pragma omp critical(orc_topk_sort)
+    {
+        g_cmp_scores = scores;
+        qsort(order, (size_t)n, sizeof(int32_t), cmp_rank);
+    }
+    for (int32_t i = 0; i < n; ++i) mask[i] = 0;
+    for (int32_t r = 0; r < k; ++r) mask[order[r]] = 1;
+    if (margin) {
+        if (k == 0 || k == n) *margin = INFINITY;
+        else {
+            double m = (double)scores[order[k - 1]] - (double)scores[order[k]];
+            *margin = isnan(m) ? 0.0 : m;
+        }
+    }
+    free(order);
+    return 0;
+}
+
+/* ------------------------------------------------------------- decode step */
+
+int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                   void* const* kc, void* const* vc, int32_t pos, int32_t k_budget,
+                   const uint8_t* route, const float* x, double* h_out,
+                   uint8_t* mask_out, float* scores_out, double* margin_out,
+                   int32_t* n_exec_out)
+{
+    const int L = c->n_layers, Lm = L - 2, d = c->d_model, dt = c->dtype;
+    const int nkv = c->n_kv_heads, hd = c->head_dim, T = c->max_ctx;
+    if (L < 2 || pos < 0 || pos >= T || k_budget < 0 || k_budget > Lm) return -1;
+    if (!route && !dm) return -1;
+
+    double* h = malloc(sizeof(double) * d);
+    uint8_t* mask = malloc((size_t)(Lm > 0 ? Lm : 1));
+    float* sc = malloc(sizeof(float) * (Lm > 0 ? Lm : 1));
+    double margin = INFINITY;
+    for (int i = 0; i < d; ++i) h[i] = (double)x[i];
+
+    /* first block always runs (Sec. 4.2.1); it appends the newest token's
+     * first-layer K/V, which the planner then sees */
+    orc_block(c, &layers[0], kc[0], vc[0], pos, h);
+
+    if (route) {
+        for (int i = 0; i < Lm; ++i) mask[i] = route[i] ? 1 : 0;
+    } else {
+        /* router context: [mean K | mean V | newest hidden after block 0] */
+        const int din = 2 * nkv * hd + d;
+        double* z = malloc(sizeof(double) * din);
+        orc_pool(c, kc[0], vc[0], pos, z);
+        for (int i = 0; i < d; ++i) z[2 * nkv * hd + i] = h[i];
+        orc_dm_scores(c, dm, z, sc);
+        orc_topk(sc, Lm, k_budget, mask, &margin);
+        free(z);
+        if (scores_out) memcpy(scores_out, sc, sizeof(float) * Lm);
+        if (mask_out) memcpy(mask_out, mask, (size_t)Lm);
+    }
+
+    /* routable blocks 1..L-2, Eq. (1): run when selected; when skipped, h is
+     * unchanged and the layer's K/V slot at pos is zero-filled (Sec. 6) */
+    int n_exec = 1;
+    for (int l = 1; l <= Lm; ++l) {
+        if (mask[l - 1]) {
+            orc_block(c, &layers[l], kc[l], vc[l], pos, h);
+            ++n_exec;
+        } else {
+            for (int g = 0; g < nkv; ++g)
+                for (int i = 0; i < hd; ++i) {
+                    size_t at = ((size_t)g * T + pos) * hd + i;
+                    st(kc[l], at, dt, 0.0);
+                    st(vc[l], at, dt, 0.0);
+                }
+        }
+    }
+    orc_block(c, &layers[L - 1], kc[L - 1], vc[L - 1], pos, h);
+    ++n_exec;
+
+    memcpy(h_out, h, sizeof(double) * d);
+    if (margin_out) *margin_out = margin;
+    if (n_exec_out) *n_exec_out = n_exec;
+    free(h); free(mask); free(sc);
+    return 0;
+}

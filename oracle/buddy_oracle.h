@@ -1,0 +1,107 @@
+/*
+ * buddy_oracle.h -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow CPU reference ("oracle") of one budget-routed decode step of
+ * BUDDY (Budget-Driven Dynamic depth routing, arXiv 2606.09514).  Only the
+ * test suite, the smoke check and the benchmark's CPU-baseline leg may load
+ * this library.  The GPU library never links, includes or calls it, and it
+ * shares no code with the GPU library.
+ *
+ * Arithmetic is IEEE double throughout.  Values held in storage precision
+ * (weights, the KV cache) are read by exact up-conversion; newly produced K/V
+ * rows are rounded to the storage precision when stored, because the model
+ * keeps its cache in that precision and later steps read the rounded values.
+ * Layer scores are rounded to fp32 before the top-k decision, so both sides
+ * take that integer decision on fp32 values.
+ *
+ * Layouts (all row-major):
+ *   wqkv     [(n_heads + 2 n_kv_heads) * head_dim][d_model]  rows: q | k | v
+ *   wo       [d_model][n_heads * head_dim]
+ *   wgate_up [2 d_ffn][d_model]                                rows: gate | up
+ *   wdown    [d_model][d_ffn]
+ *   attn_norm, mlp_norm [d_model]
+ *   dm w1 [dm_hidden][din], b1 [dm_hidden], w2 [L_mid][dm_hidden], b2 [L_mid]
+ *      din = 2 * n_kv_heads * head_dim + d_model
+ *   one sequence's cache for one layer: [n_kv_heads][max_ctx][head_dim]
+ * Every weight array and the cache are in the storage dtype (fp32 or bf16).
+ */
+#ifndef BUDDY_ORACLE_H
+#define BUDDY_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORC_F32 = 0, ORC_BF16 = 1 };
+enum { ORC_ACT_SILU = 0, ORC_ACT_GELU_ERF = 1 };
+
+typedef struct {
+    int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn;
+    int32_t dm_hidden, dm_act, dtype, max_ctx;
+    double rms_eps, rope_theta;
+} orc_config;
+
+typedef struct {
+    const void *attn_norm, *wqkv, *wo, *mlp_norm, *wgate_up, *wdown;
+} orc_layer;
+
+typedef struct {
+    const void *w1, *b1, *w2, *b2;
+    const float *prior;   /* normalized prior p~ [L_mid], or NULL */
+    double omega;         /* prior weight; 0 disables the fusion */
+} orc_dm;
+
+/* bf16 bits nearest to x (round to nearest, ties to even; NaN -> quiet NaN). */
+uint16_t orc_bf16_from_double(double x);
+
+/* RMSNorm: out = h / sqrt(mean(h^2) + eps) * g (g in storage dtype). */
+void orc_rmsnorm(const orc_config* c, const double* h, const void* g, double* out);
+
+/* Rotary embedding (rotate-half pairing) of one head vector x[head_dim] at pos. */
+void orc_rope(const orc_config* c, double* x, int32_t pos);
+
+/* One decoder block (Eq. 1 with M=1) for one sequence at position pos:
+ * appends K/V (rounded to storage) at pos of this layer's cache and updates h. */
+void orc_block(const orc_config* c, const orc_layer* w, void* kc, void* vc,
+               int32_t pos, double* h);
+
+/* Mean of the cached K and V rows at positions 0..pos (inclusive), each
+ * flattened head-major to n_kv_heads*head_dim: z = [mean K | mean V]. */
+void orc_pool(const orc_config* c, const void* kc, const void* vc, int32_t pos,
+              double* z);
+
+/* Decision Module: s' = W2 act(W1 z + b1) + b2 + omega * prior, rounded to fp32. */
+void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
+                   float* scores);
+
+/* Deterministic top-k over n scores: order by (score desc, index asc, NaN last).
+ * mask[i] = 1 for the first k.  *margin = s(k-th) - s(k+1-th) in that order,
+ * +inf when k == 0 or k == n.  Returns 0, or -1 for k outside [0, n]. */
+int orc_topk(const float* scores, int32_t n, int32_t k, uint8_t* mask,
+             double* margin);
+
+/* One full decode step for one sequence.
+ *   kc[l], vc[l]: this sequence's cache of layer l ([n_kv][max_ctx][hd]).
+ *   pos: cached positions before the step (the new token is written at pos).
+ *   k_budget: number of routable layers to run (0..L-2).
+ *   route: optional fixed mask over the L-2 routable layers (skips the
+ *          Decision Module); NULL routes with the Decision Module.
+ *   x: input hidden [d]; h_out: output hidden [d].
+ *   mask_out[L-2], scores_out[L-2] (left untouched when route != NULL),
+ *   margin_out, n_exec_out (blocks executed, including first and last):
+ *   all optional.
+ * Returns 0, or -1 on invalid arguments (nothing written). */
+int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                   void* const* kc, void* const* vc, int32_t pos, int32_t k_budget,
+                   const uint8_t* route, const float* x, double* h_out,
+                   uint8_t* mask_out, float* scores_out, double* margin_out,
+                   int32_t* n_exec_out);
+
+/* Number of OpenMP threads the oracle uses. */
+int orc_num_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,88 @@
+"""Analytic cost model of the routed decode step (host logic).
+
+- Budget to layer count: k = round(b L) - 2 (Sec. 4.2.1, Eq. 2); the App. C.2
+  variant k = b L - I clamped to [1, L - I].
+- FLOP model of App. C.2: F_DM = 2BTdr + 2BTr(L - I),
+  F_layer = 8Td^2 + 4T^2 d + 4T d d_c, F_model(b) = b L F_layer and
+  rho(b) = F_DM / F_model(b).
+- Algorithmic bytes of one decode step, which the benchmark divides by the
+  measured step time to get the fraction of the HBM roofline: the weights of
+  every block some sequence executes (read once per step), the KV rows each
+  executed (sequence, block) pair attends, the first-layer KV scan of the
+  router context, the Decision Module weights, and the new K/V rows written.
+"""
+from __future__ import annotations
+
+import math
+
+
+def budget_to_k(b: float, n_layers: int, clamp: bool = False, ignored: int = 2) -> int:
+    """Eq. 2: k = round(b L) - 2, rounding halves away from zero.  With
+    clamp=True the App. C.2 form k = b L - I limited to [1, L - I]."""
+    if not (0.0 < b <= 1.0):
+        raise ValueError("budget must lie in (0, 1]")
+    k = int(math.floor(b * n_layers + 0.5)) - ignored
+    if clamp:
+        k = min(max(k, 1), n_layers - ignored)
+    return max(k, 0)
+
+
+def k_to_budget(k: int, n_layers: int) -> float:
+    """Budget Predictor inverse map b = (k + 2) / L (Sec. 4.4)."""
+    return (k + 2) / n_layers
+
+
+def dm_flops(B: int, T: int, d: int, r: int, L: int, I: int = 2) -> int:
+    return 2 * B * T * d * r + 2 * B * T * r * (L - I)
+
+
+def layer_flops(T: int, d: int, d_c: int) -> int:
+    return 8 * T * d * d + 4 * T * T * d + 4 * T * d * d_c
+
+
+def model_flops(b: float, L: int, T: int, d: int, d_c: int) -> float:
+    return b * L * layer_flops(T, d, d_c)
+
+
+def dm_overhead(b: float, B: int, T: int, d: int, d_c: int, r: int, L: int, I: int = 2) -> float:
+    return dm_flops(B, T, d, r, L, I) / model_flops(b, L, T, d, d_c)
+
+
+# ------------------------------------------------------------ bytes per step
+
+def _s(dtype: str) -> int:
+    return 2 if dtype == "bf16" else 4
+
+
+def layer_weight_bytes(cfg: dict) -> int:
+    d, nq, nkv, hd, f = (cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"],
+                         cfg["head_dim"], cfg["d_ffn"])
+    elems = d * (nq + 2 * nkv) * hd + nq * hd * d + 3 * d * f + 2 * d
+    return elems * _s(cfg["dtype"])
+
+
+def dm_weight_bytes(cfg: dict) -> int:
+    H, Lm = cfg["dm_hidden"], cfg["n_layers"] - 2
+    din = 2 * cfg["n_kv_heads"] * cfg["head_dim"] + cfg["d_model"]
+    return (H * din + H + Lm * H + Lm) * _s(cfg["dtype"])
+
+
+def step_bytes(cfg: dict, masks, positions) -> dict:
+    """Algorithmic bytes of one step given the realised per-sequence masks
+    (each a sequence of L-2 zeros/ones) and the positions written this step.
+    Attention of a sequence at position p reads p + 1 cached rows."""
+    L = cfg["n_layers"]
+    s = _s(cfg["dtype"])
+    row = 2 * cfg["n_kv_heads"] * cfg["head_dim"] * s          # one K row + one V row
+    used = {0, L - 1}
+    kv = 0
+    for m, p in zip(masks, positions):
+        n_exec = 2 + sum(int(v) for v in m)
+        kv += n_exec * row * (p + 1)
+        used.update(l + 1 for l, v in enumerate(m) if v)
+    weights = len(used) * layer_weight_bytes(cfg)
+    pool = sum(row * (p + 1) for p in positions)
+    dmw = dm_weight_bytes(cfg)
+    writes = len(positions) * L * row
+    return dict(weights=weights, kv=kv, pool=pool, dm=dmw, kv_writes=writes,
+                total=weights + kv + pool + dmw + writes, layers_used=len(used))

@@ -1,0 +1,310 @@
+"""Pins of the CPU oracle against facts fixed outside it.
+
+Each test checks the oracle against something other than itself: library
+routines (torch, Hugging Face's Llama), brute force on tiny inputs, closed
+forms, and the structural invariants the paper states (exact budget, dense
+equivalence, identity of skipped blocks, zero-filled skipped KV).
+"""
+import math
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import Oracle, bf16_from_double
+from paper_2606_09514_amd import synth
+
+from _hf import hf_forward, hf_model
+
+SMALL = dict(n_layers=6, d_model=64, n_heads=4, n_kv_heads=2, head_dim=16, d_ffn=96,
+             dm_hidden=32, dm_act="gelu", rope_theta=1e4, rms_eps=1e-5)
+
+
+def make(shape=SMALL, dtype="f32", max_ctx=24, seed=0, omega=0.0):
+    cfg = synth.model_config(shape, dtype, max_ctx)
+    W = synth.model_weights(cfg, seed, "cpu", omega=omega)
+    layers = [{k: synth.storage_numpy(v) for k, v in lw.items()} for lw in W["layers"]]
+    dm = {k: (synth.storage_numpy(v) if torch.is_tensor(v) else v) for k, v in W["dm"].items()}
+    return cfg, layers, dm, Oracle(cfg, layers, dm)
+
+
+def empty_cache(cfg, orc):
+    shp = (cfg["n_kv_heads"], cfg["max_ctx"], cfg["head_dim"])
+    kc = [np.zeros(shp, dtype=orc.sdt) for _ in range(cfg["n_layers"])]
+    vc = [np.zeros(shp, dtype=orc.sdt) for _ in range(cfg["n_layers"])]
+    return kc, vc
+
+
+def relerr(a, b):
+    return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-30))
+
+
+# ----------------------------------------------------------- storage rounding
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(1)
+    vals = np.concatenate([
+        rng.standard_normal(20000).astype(np.float32),
+        (rng.standard_normal(2000) * 1e-39).astype(np.float32),      # fp32 subnormals
+        (rng.standard_normal(2000) * 1e37).astype(np.float32),
+        np.array([0.0, -0.0, 1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, 3.4028235e38,
+                  -3.4028235e38, np.inf, -np.inf], dtype=np.float32),
+    ])
+    ref = torch.from_numpy(vals).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = np.array([bf16_from_double(float(v)) for v in vals], dtype=np.uint16)
+    assert np.array_equal(got, ref)
+    assert bf16_from_double(float("nan")) & 0x7F80 == 0x7F80
+
+
+# ------------------------------------------------------------ block pieces
+
+def test_rmsnorm_matches_torch_and_closed_form():
+    cfg, layers, dm, orc = make()
+    rng = np.random.default_rng(2)
+    h = rng.standard_normal(cfg["d_model"]) * 3.0
+    g = layers[0]["attn_norm"]
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(h)[None], (cfg["d_model"],),
+                                       torch.from_numpy(g.astype(np.float64)),
+                                       eps=cfg["rms_eps"])[0].numpy()
+    assert relerr(orc.rmsnorm(h, g), ref) < 1e-13
+    # constant input c: every output is c / sqrt(c^2 + eps) * g
+    c = 0.37
+    one = np.ones(cfg["d_model"], dtype=np.float32)
+    out = orc.rmsnorm(np.full(cfg["d_model"], c), one)
+    assert np.allclose(out, c / math.sqrt(c * c + cfg["rms_eps"]), rtol=0, atol=1e-15)
+
+
+def test_rope_pins():
+    from transformers.models.llama.modeling_llama import apply_rotary_pos_emb
+    cfg, _, _, orc = make()
+    hd = cfg["head_dim"]
+    rng = np.random.default_rng(3)
+    q, k = rng.standard_normal(hd), rng.standard_normal(hd)
+    # identity at position 0, norm preserved everywhere
+    assert np.array_equal(orc.rope(q, 0), q)
+    for p in (1, 7, 300, 8191):
+        assert abs(np.linalg.norm(orc.rope(q, p)) - np.linalg.norm(q)) < 1e-12
+    # relative position: <R_m q, R_n k> depends only on m - n
+    a = orc.rope(q, 9) @ orc.rope(k, 4)
+    b = orc.rope(q, 105) @ orc.rope(k, 100)
+    assert abs(a - b) < 1e-12
+    # the library rotary embedding (angles in fp32 there, hence the tolerance)
+    inv = 1.0 / (cfg["rope_theta"] ** (torch.arange(0, hd, 2, dtype=torch.float64) / hd))
+    for p in (1, 5, 17):
+        ang = p * inv
+        emb = torch.cat([ang, ang])
+        qe, _ = apply_rotary_pos_emb(torch.from_numpy(q)[None, None, None],
+                                     torch.from_numpy(k)[None, None, None],
+                                     emb.cos()[None], emb.sin()[None])
+        assert np.max(np.abs(qe[0, 0, 0].numpy() - orc.rope(q, p))) < 1e-12
+
+
+# ------------------------------------------------- dense equivalence and routes
+
+def run_sequence(cfg, orc, xs, k, route=None):
+    kc, vc = empty_cache(cfg, orc)
+    outs, execs, masks = [], [], []
+    for t, x in enumerate(xs):
+        h, mask, _, _, n_exec = orc.decode_seq(kc, vc, t, k, x, route=route)
+        outs.append(h)
+        execs.append(n_exec)
+        masks.append(mask)
+    return np.array(outs), execs, masks, (kc, vc)
+
+
+def test_all_layers_equals_dense_forward():
+    """k = L_mid: the routed decode is the dense causal forward (Eq. 1, M = 1)."""
+    cfg, layers, dm, orc = make()
+    xs = synth.hidden_inputs(12, cfg["d_model"], seed=5).numpy()
+    got, execs, _, _ = run_sequence(cfg, orc, xs, k=orc.L_mid)
+    ref = hf_forward(hf_model(cfg, layers, list(range(cfg["n_layers"]))), xs)
+    assert relerr(got, ref) < 1e-5, relerr(got, ref)
+    assert all(e == cfg["n_layers"] for e in execs)
+
+
+def test_k0_equals_first_and_last_block_model():
+    cfg, layers, dm, orc = make()
+    xs = synth.hidden_inputs(9, cfg["d_model"], seed=6).numpy()
+    got, execs, masks, _ = run_sequence(cfg, orc, xs, k=0)
+    ref = hf_forward(hf_model(cfg, layers, [0, cfg["n_layers"] - 1]), xs)
+    assert relerr(got, ref) < 1e-5
+    assert all(e == 2 for e in execs) and all(m.sum() == 0 for m in masks)
+
+
+def test_constant_route_equals_sub_model():
+    """Skipped blocks are never read under a fixed route: the result is the
+    dense forward of {first} + S + {last}."""
+    cfg, layers, dm, orc = make()
+    route = np.array([0, 1, 0, 1], dtype=np.uint8)       # routable layers 2 and 4
+    xs = synth.hidden_inputs(10, cfg["d_model"], seed=7).numpy()
+    got, execs, _, _ = run_sequence(cfg, orc, xs, k=2, route=route)
+    ref = hf_forward(hf_model(cfg, layers, [0, 2, 4, 5]), xs)
+    assert relerr(got, ref) < 1e-5
+    assert all(e == 4 for e in execs)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_exact_budget_every_k(dtype):
+    """Every sequence executes exactly k + 2 blocks and selects k layers."""
+    cfg, layers, dm, orc = make(dtype=dtype, omega=0.1)
+    xs = synth.hidden_inputs(6, cfg["d_model"], seed=8).numpy()
+    for k in range(orc.L_mid + 1):
+        _, execs, masks, _ = run_sequence(cfg, orc, xs, k=k)
+        assert all(e == k + 2 for e in execs)
+        assert all(int(m.sum()) == k for m in masks)
+
+
+def test_routes_deterministic_under_seed():
+    outs = []
+    for _ in range(2):
+        cfg, layers, dm, orc = make(omega=0.1, seed=11)
+        xs = synth.hidden_inputs(8, cfg["d_model"], seed=12).numpy()
+        h, _, masks, _ = run_sequence(cfg, orc, xs, k=2)
+        outs.append((h.tobytes(), np.array(masks).tobytes()))
+    assert outs[0] == outs[1]
+
+
+def test_thread_count_does_not_change_results():
+    code = ("import sys; sys.path.insert(0, %r); sys.path.insert(0, %r)\n"
+            "import hashlib, numpy as np\n"
+            "from test_oracle_pins import make, run_sequence\n"
+            "from paper_2606_09514_amd import synth\n"
+            "cfg, l, d, o = make(shape=dict(n_layers=4, d_model=256, n_heads=4, n_kv_heads=2,"
+            " head_dim=64, d_ffn=512, dm_hidden=64, dm_act='silu', rope_theta=1e4,"
+            " rms_eps=1e-5), omega=0.1)\n"
+            "xs = synth.hidden_inputs(4, 256, seed=1).numpy()\n"
+            "h, _, m, _ = run_sequence(cfg, o, xs, k=1)\n"
+            "print(hashlib.sha256(h.tobytes() + np.array(m).tobytes()).hexdigest())\n"
+            % (os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+               os.path.dirname(os.path.abspath(__file__))))
+    digests = []
+    for n in ("1", "4"):
+        env = dict(os.environ, OMP_NUM_THREADS=n)
+        r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True,
+                           text=True, check=True)
+        digests.append(r.stdout.strip().splitlines()[-1])
+    assert digests[0] == digests[1]
+
+
+# -------------------------------------------------------------------- router
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_pool_brute_force(dtype):
+    cfg, layers, dm, orc = make(dtype=dtype)
+    rng = np.random.default_rng(4)
+    shp = (cfg["n_kv_heads"], cfg["max_ctx"], cfg["head_dim"])
+    if dtype == "bf16":
+        mk = lambda: torch.from_numpy(rng.standard_normal(shp).astype(np.float32)).to(
+            torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        up = lambda a: (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    else:
+        mk = lambda: rng.standard_normal(shp).astype(np.float32)
+        up = lambda a: a.astype(np.float64)
+    kc, vc = mk(), mk()
+    for pos in (0, 1, 2):
+        z = orc.pool(kc, vc, pos)
+        n = cfg["n_kv_heads"] * cfg["head_dim"]
+        for g in range(cfg["n_kv_heads"]):
+            for i in range(cfg["head_dim"]):
+                sk = sum(up(kc[g, j, i]) for j in range(pos + 1)) / (pos + 1)
+                sv = sum(up(vc[g, j, i]) for j in range(pos + 1)) / (pos + 1)
+                assert z[g * cfg["head_dim"] + i] == pytest.approx(sk, rel=1e-15, abs=1e-300)
+                assert z[n + g * cfg["head_dim"] + i] == pytest.approx(sv, rel=1e-15, abs=1e-300)
+    # constant rows pool to that constant
+    kc[...] = kc[0, 0, 0]
+    vc[...] = vc[1, 0, 3]
+    z = orc.pool(kc, vc, 15)
+    assert np.all(z[:n] == up(kc[0, 0, 0])) and np.all(z[n:] == up(vc[1, 0, 3]))
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+def test_dm_scores_match_torch(act):
+    shape = dict(SMALL, dm_act=act)
+    cfg, layers, dm, orc = make(shape=shape, omega=0.1)
+    din = 2 * cfg["n_kv_heads"] * cfg["head_dim"] + cfg["d_model"]
+    z = np.random.default_rng(9).standard_normal(din)
+    T = lambda a: torch.from_numpy(a.astype(np.float64))
+    a = torch.nn.functional.linear(T(z), T(dm["w1"]), T(dm["b1"]))
+    a = torch.nn.functional.gelu(a) if act == "gelu" else torch.nn.functional.silu(a)
+    s = torch.nn.functional.linear(a, T(dm["w2"]), T(dm["b2"])) + 0.1 * T(dm["prior"])
+    got = orc.dm_scores(z)
+    assert np.array_equal(got, s.numpy().astype(np.float32)) or \
+        np.max(np.abs(got - s.numpy())) < 1e-7
+
+
+def test_dm_constant_scores_select_lowest_indices():
+    cfg, layers, dm, _ = make()
+    dm2 = dict(dm, w2=np.zeros_like(dm["w2"]), b2=np.full_like(dm["b2"], 0.25), prior=None)
+    orc = Oracle(cfg, layers, dm2)
+    kc, vc = empty_cache(cfg, orc)
+    for k in range(orc.L_mid + 1):
+        _, mask, scores, margin, _ = orc.decode_seq(kc, vc, 0, k, np.ones(cfg["d_model"]))
+        assert np.all(scores == np.float32(0.25))
+        assert list(mask) == [1] * k + [0] * (orc.L_mid - k)
+        assert margin == (math.inf if k in (0, orc.L_mid) else 0.0)
+
+
+def test_omega_zero_ignores_prior():
+    cfg, layers, dm, _ = make(omega=0.1)
+    z = np.random.default_rng(10).standard_normal(2 * 2 * 16 + 64)
+    with_prior_w0 = Oracle(cfg, layers, dict(dm, omega=0.0)).dm_scores(z)
+    without = Oracle(cfg, layers, dict(dm, prior=None)).dm_scores(z)
+    assert np.array_equal(with_prior_w0, without)
+
+
+def test_topk_matches_stable_sort():
+    rng = np.random.default_rng(11)
+    for trial in range(300):
+        n = int(rng.integers(1, 40))
+        s = rng.integers(-3, 4, size=n).astype(np.float32) * 0.5   # many ties
+        if trial % 5 == 0:
+            s[rng.integers(0, n)] = np.nan
+        if trial % 7 == 0:
+            s[rng.integers(0, n)] = -0.0
+        k = int(rng.integers(0, n + 1))
+        key = lambda i: (1, 0.0, i) if np.isnan(s[i]) else (0, -float(s[i]), i)
+        order = sorted(range(n), key=key)
+        mask, margin = Oracle.topk(s, k)
+        assert sorted(np.nonzero(mask)[0].tolist()) == sorted(order[:k])
+        if 0 < k < n:
+            m = float(s[order[k - 1]]) - float(s[order[k]])
+            assert margin == (0.0 if math.isnan(m) else m)
+        else:
+            assert margin == math.inf
+    with pytest.raises(ValueError):
+        Oracle.topk(np.zeros(3, np.float32), 4)
+
+
+# --------------------------------------------------------- skipped-layer KV
+
+def test_skipped_layer_kv_is_zero_and_attended_as_zero():
+    """Sec. 6: skipped layers keep zero-filled K/V, which later steps attend
+    as ordinary entries.  Built so the routable block adds exactly the mean
+    of its V cache over positions 0..pos (W_q = 0 gives uniform attention,
+    W_o = I, no MLP); the outer blocks are identities (W_o = W_down = 0)."""
+    shape = dict(n_layers=3, d_model=4, n_heads=1, n_kv_heads=1, head_dim=4, d_ffn=4,
+                 dm_hidden=4, dm_act="silu", rope_theta=1e4, rms_eps=1e-5)
+    cfg, layers, dm, _ = make(shape=shape, max_ctx=4)
+    for lw in layers:
+        lw["wo"][...] = 0
+        lw["wdown"][...] = 0
+    layers[1]["wqkv"][:4] = 0                      # q rows
+    layers[1]["wo"][...] = np.eye(4, dtype=np.float32)
+    orc = Oracle(cfg, layers, dm)
+    kc, vc = empty_cache(cfg, orc)
+    for a in kc + vc:            # stale contents: every slot read must be written first
+        a[...] = 7.0
+    rng = np.random.default_rng(12)
+    x0, x1 = rng.standard_normal(4).astype(np.float32), rng.standard_normal(4).astype(np.float32)
+    h0, *_ = orc.decode_seq(kc, vc, 0, 0, x0, route=np.array([0], np.uint8))
+    assert np.array_equal(h0, x0.astype(np.float64))          # blocks 0 and 2 are identities
+    assert np.all(kc[1][:, 0] == 0) and np.all(vc[1][:, 0] == 0)
+    assert np.any(kc[0][:, 0] != 0)
+    h1, *_ = orc.decode_seq(kc, vc, 1, 1, x1, route=np.array([1], np.uint8))
+    v1 = vc[1][0, 1].astype(np.float64)
+    assert np.any(v1 != 0)
+    # literal zero-fill: the skipped slot counts in the softmax with value 0
+    assert np.allclose(h1, x1 + (0.0 + v1) / 2.0, rtol=0, atol=1e-14)
