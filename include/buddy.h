@@ -1,0 +1,174 @@
+/*
+ * buddy.h -- C ABI of the MI355X (gfx950) budget-routed decode step of
+ * BUDDY (Budget-Driven Dynamic depth routing, arXiv 2606.09514).
+ *
+ * One call of buddy_decode_step advances every sequence of a batch by one
+ * token:
+ *   1. the first block runs for every sequence and appends its K/V row;
+ *   2. the KV-aware planner (Sec. 4.3) averages the first layer's K and V
+ *      cache rows 0..pos (the new row included) and joins them with the new
+ *      token's hidden state after the first block:
+ *          z = [mean K | mean V | h]          (din = 2 n_kv hd + d)
+ *   3. the Decision Module (Sec. 4.2.3, App. C.1) scores the L-2 routable
+ *      blocks, s = W2 act(W1 z + b1) + b2, and fuses the prior,
+ *      s' = s + omega p~ (Eq. 2);
+ *   4. a deterministic top-k keeps the k_b best blocks of sequence b
+ *      (Eq. 2; ties go to the lower block index, NaN ranks last);
+ *   5. each routable block runs only on the sequences that selected it
+ *      (grouping by mask, App. C.1); a skipped block leaves h unchanged
+ *      (Eq. 1) and gets a zero-filled K/V row at pos (Sec. 6, limitations);
+ *   6. the last block runs for every sequence.
+ * The decoder block is Llama-style (App. C.2): RMSNorm, Q/K/V projection,
+ * rotary embedding (rotate-half pairing, angle pos * theta^(-2i/hd)), grouped
+ * query attention over the cache including the new row (App. "Background",
+ * KV-cache equation), output projection, residual, RMSNorm, SwiGLU MLP,
+ * residual.  Projections are bias-free.
+ *
+ * Conventions shared by every entry point:
+ *   - Memory: every pointer marked "device" is memory the caller allocated on
+ *     the current HIP device; the caller owns it and keeps it alive until the
+ *     enqueued work has finished.  The library never frees caller memory.
+ *     A model handle owns only its workspace.
+ *   - Precision: weights and the KV cache are stored in the configured dtype
+ *     (fp32 or bf16); hidden states, scores and all accumulation are fp32.
+ *     New K/V rows are rounded to the storage dtype (nearest, ties to even).
+ *   - Layouts are row-major.  Weight matrices are [out][in]:
+ *       wqkv     [(n_heads + 2 n_kv_heads) hd][d]    rows q | k | v
+ *       wo       [d][n_heads hd]
+ *       wgate_up [2 d_ffn][d]                        rows gate | up
+ *       wdown    [d][d_ffn]
+ *       attn_norm, mlp_norm [d]
+ *       Decision Module: w1 [dm_hidden][din], b1 [dm_hidden],
+ *                        w2 [L-2][dm_hidden], b2 [L-2]  (storage dtype),
+ *                        prior [L-2] fp32 (already normalised p~) or NULL.
+ *     KV cache: K and V each [n_layers][max_batch][n_kv_heads][max_ctx][hd].
+ *   - Positions: pos[b] (host array) is the number of cached rows of
+ *     sequence b before the step; the step writes row pos[b] of every layer
+ *     and attends rows 0..pos[b].  The caller advances pos.
+ *   - Streams: `stream` is a hipStream_t (NULL = the null stream).  All work
+ *     is enqueued on it without host synchronisation; outputs are valid once
+ *     the stream reaches the enqueued work.
+ *   - Errors: arguments are validated on the host before anything is
+ *     enqueued; on a validation failure nothing is written and a status is
+ *     returned.  BUDDY_EDEVICE reports a HIP launch error; its text is
+ *     available from buddy_last_error.  Handles are not thread-safe; calls
+ *     on one handle must not overlap (they share its workspace).
+ */
+#ifndef BUDDY_H
+#define BUDDY_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BUDDY_OK = 0,
+    BUDDY_EINVAL = 1,       /* null pointer, bad enum, k or pos out of range */
+    BUDDY_ESHAPE = 2,       /* configuration shape the kernels do not support */
+    BUDDY_ECAPACITY = 3,    /* batch above max_batch */
+    BUDDY_ENOMEM = 4,       /* workspace allocation failed */
+    BUDDY_EDEVICE = 5,      /* HIP error (see buddy_last_error) */
+    BUDDY_EUNSUPPORTED = 6  /* valid request this build does not implement */
+} buddy_status;
+
+typedef enum { BUDDY_F32 = 0, BUDDY_BF16 = 1 } buddy_dtype;
+
+/* Decision Module activation: SiLU (App. C.1) or exact GELU (erf form). */
+typedef enum { BUDDY_ACT_SILU = 0, BUDDY_ACT_GELU_ERF = 1 } buddy_dm_act;
+
+/* KV treatment of a skipped block: zero-filled rows (Sec. 6) are the only
+ * treatment the paper fixes; BUDDY_SKIP_KV_MASK returns BUDDY_EUNSUPPORTED. */
+typedef enum { BUDDY_SKIP_KV_ZERO = 0, BUDDY_SKIP_KV_MASK = 1 } buddy_skip_kv;
+
+typedef struct {
+    int32_t n_layers;     /* L >= 2; blocks 0 and L-1 always run          */
+    int32_t d_model;      /* multiple of 8                                 */
+    int32_t n_heads;      /* query heads, multiple of n_kv_heads           */
+    int32_t n_kv_heads;   /* n_heads / n_kv_heads <= 8                     */
+    int32_t head_dim;     /* 64 or 128                                     */
+    int32_t d_ffn;        /* multiple of 8                                 */
+    int32_t dm_hidden;    /* Decision Module hidden width, multiple of 2   */
+    int32_t dm_act;       /* buddy_dm_act                                  */
+    int32_t dtype;        /* buddy_dtype of weights and KV cache           */
+    int32_t max_batch;    /* 1..256: workspace and KV cache batch capacity */
+    int32_t max_ctx;      /* rows per sequence in the KV cache             */
+    float rms_eps;        /* RMSNorm epsilon                               */
+    float rope_theta;     /* rotary base                                   */
+} buddy_config;
+
+typedef struct {
+    const void *attn_norm, *wqkv, *wo, *mlp_norm, *wgate_up, *wdown; /* device */
+} buddy_layer_weights;
+
+typedef struct {
+    const void *w1, *b1, *w2, *b2;  /* device, storage dtype              */
+    const float* prior;             /* device [L-2] fp32, or NULL         */
+    float omega;                    /* prior weight of Eq. 2 (paper: 0.1) */
+} buddy_dm_weights;
+
+typedef struct {
+    void* k;  /* device [L][max_batch][n_kv][max_ctx][hd], storage dtype */
+    void* v;  /* same layout as k                                         */
+} buddy_kv;
+
+typedef struct buddy_model buddy_model;
+
+/* Creates a model handle on the current HIP device.  `layers` holds
+ * n_layers entries; the weight pointers are copied, the weights are not.
+ * Allocates the handle's workspace (sized by max_batch and max_ctx).
+ * Returns BUDDY_OK and *out, or an error status with *out = NULL. */
+buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weights* layers,
+                                const buddy_dm_weights* dm, buddy_model** out);
+
+/* Waits for the device, then frees the handle's workspace.  NULL is a no-op. */
+void buddy_model_destroy(buddy_model* m);
+
+/* KV-aware planner plus Decision Module (Sec. 4.3, Sec. 4.2.3, Eq. 2 fusion)
+ * without routing: for b < B, pools the first layer's K/V rows 0..pos[b] of
+ * kv (the newest token's row already written) with h_new[b] (device
+ * [B][d] fp32) and writes s' to scores_out (device [B][L-2] fp32).
+ * pos: host [B].  B = 0 is a no-op. */
+buddy_status buddy_pool_route(buddy_model* m, const buddy_kv* kv, const int32_t* pos,
+                              const float* h_new, int32_t B, float* scores_out,
+                              void* stream);
+
+/* Deterministic per-row top-k (Eq. 2): mask_out[b][i] = 1 iff layer i is
+ * among the k[b] largest of scores[b][0..n) under (score desc, index asc,
+ * NaN last).  scores: device [B][n] fp32; k: host [B], 0 <= k[b] <= n;
+ * mask_out: device [B][n] uint8; 1 <= n <= 255; B <= 65535.  Needs no
+ * model handle. */
+buddy_status buddy_select_topk(const float* scores, const int32_t* k, int32_t B, int32_t n,
+                               uint8_t* mask_out, void* stream);
+
+/* One budget-routed decode step for B sequences (steps 1-6 above).
+ *   hidden: device [B][d] fp32; input H_0 of the new token, overwritten
+ *           with the last block's output H_L (no final norm).
+ *   pos:    host [B]; 0 <= pos[b] < max_ctx.
+ *   k:      host [B]; 0 <= k[b] <= L-2 routable blocks to run.
+ *   skip_kv: buddy_skip_kv.
+ *   route_override: device [B][L-2] uint8 (nonzero = run) or NULL; when
+ *           given, the planner and Decision Module are not run, k is
+ *           ignored and scores_out is left untouched.
+ *   mask_out: device [B][L-2] uint8 or NULL: the mask that was executed.
+ *   scores_out: device [B][L-2] fp32 or NULL: s' of step 3.
+ * B = 0 is a no-op; B > max_batch gives BUDDY_ECAPACITY. */
+buddy_status buddy_decode_step(buddy_model* m, const buddy_kv* kv, float* hidden,
+                               const int32_t* pos, const int32_t* k, int32_t B,
+                               int32_t skip_kv, const uint8_t* route_override,
+                               uint8_t* mask_out, float* scores_out, void* stream);
+
+/* Budget to routable-block count, k = round(b L) - 2 (Eq. 2), halves away
+ * from zero, limited to [0, L-2]; -1 when b is outside (0, 1]. */
+int32_t buddy_budget_to_k(float b, int32_t n_layers);
+
+const char* buddy_status_string(buddy_status s);
+
+/* Text of the last HIP error seen by this handle ("" if none). */
+const char* buddy_last_error(const buddy_model* m);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

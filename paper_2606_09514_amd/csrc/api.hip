@@ -1,0 +1,342 @@
+// Host side of the C ABI declared in include/buddy.h: argument validation,
+// the model handle and its workspace, and the order of kernel launches of
+// one budget-routed decode step.  Every launch goes to the caller's stream;
+// nothing here synchronises with the device except buddy_model_destroy.
+#include <math.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+
+#include "buddy_internal.h"
+
+using namespace buddy;
+
+struct buddy_model {
+    Model M;
+};
+
+namespace {
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+buddy_status fail_device(Model& M, hipError_t e, const char* where) {
+    snprintf(M.last_error, sizeof(M.last_error), "%s: %s", where, hipGetErrorString(e));
+    return BUDDY_EDEVICE;
+}
+
+buddy_status check_config(const buddy_config* c) {
+    if (!c) return BUDDY_EINVAL;
+    if (c->n_layers < 2 || c->n_layers - 2 > 255) return BUDDY_ESHAPE;
+    if (c->d_model <= 0 || c->d_model % 8) return BUDDY_ESHAPE;
+    if (c->n_kv_heads <= 0 || c->n_heads <= 0 || c->n_heads % c->n_kv_heads) return BUDDY_ESHAPE;
+    if (c->n_heads / c->n_kv_heads > kMaxGroup) return BUDDY_ESHAPE;
+    if (c->head_dim != 64 && c->head_dim != 128) return BUDDY_ESHAPE;
+    if (c->d_ffn <= 0 || c->d_ffn % 8) return BUDDY_ESHAPE;
+    if (c->dm_hidden <= 0 || c->dm_hidden % 2) return BUDDY_ESHAPE;
+    if (c->dm_act != BUDDY_ACT_SILU && c->dm_act != BUDDY_ACT_GELU_ERF) return BUDDY_EINVAL;
+    if (c->dtype != BUDDY_F32 && c->dtype != BUDDY_BF16) return BUDDY_EINVAL;
+    if (c->max_batch < 1 || c->max_batch > kMaxBatch) return BUDDY_ECAPACITY;
+    if (c->max_ctx < 1) return BUDDY_EINVAL;
+    if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return BUDDY_EINVAL;
+    // the activation rows of one GEMV pass must fit in LDS
+    const int kmax = c->d_ffn > c->d_model ? c->d_ffn : c->d_model;
+    if ((size_t)kmax * sizeof(float) > 80 * 1024) return BUDDY_ESHAPE;
+    const int din = 2 * c->n_kv_heads * c->head_dim + c->d_model;
+    if ((size_t)din * sizeof(float) > 80 * 1024) return BUDDY_ESHAPE;
+    return BUDDY_OK;
+}
+
+size_t elem_size(const buddy_config& c) { return c.dtype == BUDDY_BF16 ? 2 : 4; }
+
+// Cache base of block l (elements of the storage dtype, as bytes).
+const char* layer_base(const Model& M, const void* kv, int l) {
+    const buddy_config& c = M.cfg;
+    const size_t per_layer = (size_t)c.max_batch * c.n_kv_heads * c.max_ctx * c.head_dim;
+    return (const char*)kv + (size_t)l * per_layer * elem_size(c);
+}
+
+int attn_chunks(const Model& M, int B, int max_pos) {
+    const buddy_config& c = M.cfg;
+    // about 2048 workgroups over the step's (sequence, KV head) pairs, each
+    // chunk at least 32 rows
+    const int pairs = B * c.n_kv_heads;
+    int want = (2048 + pairs - 1) / pairs;
+    const int by_len = (max_pos + 1 + 31) / 32;
+    if (want > by_len) want = by_len;
+    if (want < 1) want = 1;
+    if (want > M.ws.max_chunks) want = M.ws.max_chunks;
+    return want;
+}
+
+buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows rows,
+                       int max_pos, hipStream_t s) {
+    const buddy_config& c = M.cfg;
+    const buddy_layer_weights& w = M.layers[l];
+    const int qdim = c.n_heads * c.head_dim;
+    hipError_t e;
+
+    GemvArgs g;
+    memset(&g, 0, sizeof(g));
+    g.rows = rows;
+    g.eps = c.rms_eps;
+    g.T = c.max_ctx; g.hd = c.head_dim; g.nq = c.n_heads; g.nkv = c.n_kv_heads;
+    g.bcap = c.max_batch; g.pos = M.ws.pos; g.inv_freq = M.ws.inv_freq;
+    g.kc = (void*)layer_base(M, kv->k, l);
+    g.vc = (void*)layer_base(M, kv->v, l);
+
+    // RMSNorm + QKV projection + rotary + KV append
+    g.W = w.wqkv; g.N = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; g.K = c.d_model;
+    g.X = hidden; g.ldx = c.d_model; g.gain = w.attn_norm;
+    g.Y = M.ws.q; g.ldy = qdim;
+    if ((e = launch_gemv(c.dtype, PRO_RMSNORM, EPI_QKV, g, s)) != hipSuccess)
+        return fail_device(M, e, "qkv");
+
+    // attention over rows 0..pos
+    AttnArgs a;
+    a.q = M.ws.q; a.o = M.ws.o; a.kc = g.kc; a.vc = g.vc;
+    a.T = c.max_ctx; a.hd = c.head_dim; a.nq = c.n_heads; a.nkv = c.n_kv_heads;
+    a.bcap = c.max_batch; a.pos = M.ws.pos; a.rows = rows;
+    a.chunks = attn_chunks(M, rows.n_max, max_pos);
+    a.chunk_len = (max_pos + 1 + a.chunks - 1) / a.chunks;
+    a.part = M.ws.part; a.counters = M.ws.attn_cnt; a.max_chunks = M.ws.max_chunks;
+    if ((e = launch_attention(c.dtype, a, s)) != hipSuccess) return fail_device(M, e, "attention");
+
+    // h += Wo o
+    g.W = w.wo; g.N = c.d_model; g.K = qdim; g.X = M.ws.o; g.ldx = qdim; g.gain = nullptr;
+    g.Y = hidden; g.ldy = c.d_model;
+    if ((e = launch_gemv(c.dtype, PRO_NONE, EPI_ADD, g, s)) != hipSuccess)
+        return fail_device(M, e, "o_proj");
+
+    // m = SiLU(Wg u2) * (Wu u2), u2 = RMSNorm(h)
+    g.W = w.wgate_up; g.N = 2 * c.d_ffn; g.K = c.d_model; g.X = hidden; g.ldx = c.d_model;
+    g.gain = w.mlp_norm; g.f = c.d_ffn; g.Y = M.ws.m; g.ldy = c.d_ffn;
+    if ((e = launch_gemv(c.dtype, PRO_RMSNORM, EPI_SWIGLU, g, s)) != hipSuccess)
+        return fail_device(M, e, "gate_up");
+
+    // h += Wdown m
+    g.W = w.wdown; g.N = c.d_model; g.K = c.d_ffn; g.X = M.ws.m; g.ldx = c.d_ffn;
+    g.gain = nullptr; g.Y = hidden; g.ldy = c.d_model;
+    if ((e = launch_gemv(c.dtype, PRO_NONE, EPI_ADD, g, s)) != hipSuccess)
+        return fail_device(M, e, "down");
+    return BUDDY_OK;
+}
+
+// Router context and the Decision Module's hidden layer for every sequence.
+buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, int max_pos,
+                         hipStream_t s) {
+    const buddy_config& c = M.cfg;
+    hipError_t e;
+    if ((e = launch_pool(M, kv->k, kv->v, h, B, max_pos, s)) != hipSuccess)
+        return fail_device(M, e, "pool");
+    GemvArgs g;
+    memset(&g, 0, sizeof(g));
+    g.W = M.dm.w1; g.N = c.dm_hidden; g.K = 2 * c.n_kv_heads * c.head_dim + c.d_model;
+    g.X = M.ws.z; g.ldx = g.K;
+    g.rows = Rows{M.ws.idx_all, M.ws.n_all, B};
+    g.Y = M.ws.a; g.ldy = c.dm_hidden;
+    g.bias = M.dm.b1; g.act = c.dm_act;
+    if ((e = launch_gemv(c.dtype, PRO_NONE, EPI_BIAS_ACT, g, s)) != hipSuccess)
+        return fail_device(M, e, "dm_hidden");
+    return BUDDY_OK;
+}
+
+buddy_status check_step_host(const Model& M, const int32_t* pos, int B, int* max_pos) {
+    *max_pos = 0;
+    for (int b = 0; b < B; ++b) {
+        if (pos[b] < 0 || pos[b] >= M.cfg.max_ctx) return BUDDY_EINVAL;
+        if (pos[b] > *max_pos) *max_pos = pos[b];
+    }
+    return BUDDY_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weights* layers,
+                                const buddy_dm_weights* dm, buddy_model** out) {
+    if (!out) return BUDDY_EINVAL;
+    *out = nullptr;
+    buddy_status st = check_config(cfg);
+    if (st != BUDDY_OK) return st;
+    if (!layers || !dm) return BUDDY_EINVAL;
+    for (int l = 0; l < cfg->n_layers; ++l) {
+        const buddy_layer_weights& w = layers[l];
+        if (!w.attn_norm || !w.wqkv || !w.wo || !w.mlp_norm || !w.wgate_up || !w.wdown)
+            return BUDDY_EINVAL;
+    }
+    if (!dm->w1 || !dm->b1 || !dm->w2 || !dm->b2) return BUDDY_EINVAL;
+
+    buddy_model* h = new (std::nothrow) buddy_model;
+    if (!h) return BUDDY_ENOMEM;
+    memset(&h->M, 0, sizeof(h->M));
+    Model& M = h->M;
+    M.cfg = *cfg;
+    M.dm = *dm;
+    M.layers = (buddy_layer_weights*)malloc(sizeof(buddy_layer_weights) * cfg->n_layers);
+    if (!M.layers) { delete h; return BUDDY_ENOMEM; }
+    memcpy(M.layers, layers, sizeof(buddy_layer_weights) * cfg->n_layers);
+    (void)hipGetDevice(&M.device);
+
+    const buddy_config& c = M.cfg;
+    const size_t Bc = c.max_batch, Lm = c.n_layers - 2, hd = c.head_dim;
+    const size_t din = 2 * c.n_kv_heads * hd + c.d_model;
+    const size_t qdim = (size_t)c.n_heads * hd;
+    int max_chunks = (c.max_ctx + 31) / 32;
+    if (max_chunks > 256) max_chunks = 256;
+    int max_splits = (c.max_ctx + 63) / 64;
+    if (max_splits > 64) max_splits = 64;
+    M.ws.max_chunks = max_chunks;
+    M.ws.max_pool_splits = max_splits;
+
+    struct Piece { void** dst; size_t bytes; };
+    Workspace& W = M.ws;
+    Piece pieces[] = {
+        {(void**)&W.pos, Bc * 4}, {(void**)&W.kb, Bc * 4}, {(void**)&W.idx_all, Bc * 4},
+        {(void**)&W.n_all, 4}, {(void**)&W.idx, Lm * Bc * 4 + 4}, {(void**)&W.cnt, Lm * 4 + 4},
+        {(void**)&W.mask, Bc * Lm + 1}, {(void**)&W.scores, Bc * Lm * 4 + 4},
+        {(void**)&W.z, Bc * din * 4}, {(void**)&W.a, Bc * c.dm_hidden * 4},
+        {(void**)&W.q, Bc * qdim * 4}, {(void**)&W.o, Bc * qdim * 4},
+        {(void**)&W.m, Bc * c.d_ffn * 4},
+        {(void**)&W.part, Bc * c.n_heads * max_chunks * (hd + 2) * 4},
+        {(void**)&W.pool_part, Bc * c.n_kv_heads * max_splits * 2 * hd * 4},
+        {(void**)&W.attn_cnt, Bc * c.n_kv_heads * 4}, {(void**)&W.pool_cnt, Bc * c.n_kv_heads * 4},
+        {(void**)&W.route_cnt, 4}, {(void**)&W.inv_freq, hd / 2 * 8},
+    };
+    size_t total = 0;
+    for (const Piece& p : pieces) total += align_up(p.bytes);
+    if (hipMalloc(&M.ws_base, total) != hipSuccess) {
+        free(M.layers); delete h; return BUDDY_ENOMEM;
+    }
+    size_t off = 0;
+    for (const Piece& p : pieces) { *p.dst = (char*)M.ws_base + off; off += align_up(p.bytes); }
+    hipError_t e = hipMemset(M.ws_base, 0, total);
+    double* inv = (double*)malloc(hd / 2 * sizeof(double));
+    for (size_t i = 0; i < hd / 2; ++i) inv[i] = pow((double)c.rope_theta, -2.0 * i / (double)hd);
+    if (e == hipSuccess) e = hipMemcpy(W.inv_freq, inv, hd / 2 * sizeof(double), hipMemcpyHostToDevice);
+    free(inv);
+    if (e != hipSuccess) {
+        (void)hipFree(M.ws_base); free(M.layers); delete h; return BUDDY_EDEVICE;
+    }
+    *out = h;
+    return BUDDY_OK;
+}
+
+void buddy_model_destroy(buddy_model* h) {
+    if (!h) return;
+    (void)hipDeviceSynchronize();
+    (void)hipFree(h->M.ws_base);
+    free(h->M.layers);
+    delete h;
+}
+
+buddy_status buddy_pool_route(buddy_model* h, const buddy_kv* kv, const int32_t* pos,
+                              const float* h_new, int32_t B, float* scores_out, void* stream) {
+    if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
+    if (B == 0) return BUDDY_OK;
+    if (B < 0) return BUDDY_EINVAL;
+    Model& M = h->M;
+    if (B > M.cfg.max_batch) return BUDDY_ECAPACITY;
+    if (!pos || !h_new || !scores_out) return BUDDY_EINVAL;
+    int max_pos;
+    buddy_status st = check_step_host(M, pos, B, &max_pos);
+    if (st != BUDDY_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    StepArgs a;
+    memset(&a, 0, sizeof(a));
+    a.B = B;
+    for (int b = 0; b < B; ++b) a.pos[b] = pos[b];
+    hipError_t e = launch_setup(a, M.ws, s);
+    if (e != hipSuccess) return fail_device(M, e, "setup");
+    if ((st = run_planner(M, kv, h_new, B, max_pos, s)) != BUDDY_OK) return st;
+    if ((e = launch_route(M, kv->k, kv->v, B, nullptr, nullptr, scores_out, true, s)) != hipSuccess)
+        return fail_device(M, e, "scores");
+    return BUDDY_OK;
+}
+
+buddy_status buddy_select_topk(const float* scores, const int32_t* k, int32_t B, int32_t n,
+                               uint8_t* mask_out, void* stream) {
+    if (B == 0) return BUDDY_OK;
+    if (!scores || !k || !mask_out || B < 0 || B > 65535 || n < 1 || n > 255) return BUDDY_EINVAL;
+    for (int b = 0; b < B; ++b)
+        if (k[b] < 0 || k[b] > n) return BUDDY_EINVAL;
+    hipError_t e = launch_select_topk(scores, k, B, n, mask_out, (hipStream_t)stream);
+    return e == hipSuccess ? BUDDY_OK : BUDDY_EDEVICE;
+}
+
+buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden,
+                               const int32_t* pos, const int32_t* k, int32_t B,
+                               int32_t skip_kv, const uint8_t* route_override,
+                               uint8_t* mask_out, float* scores_out, void* stream) {
+    if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
+    if (skip_kv != BUDDY_SKIP_KV_ZERO && skip_kv != BUDDY_SKIP_KV_MASK) return BUDDY_EINVAL;
+    if (B == 0) return BUDDY_OK;
+    if (B < 0) return BUDDY_EINVAL;
+    Model& M = h->M;
+    const buddy_config& c = M.cfg;
+    if (B > c.max_batch) return BUDDY_ECAPACITY;
+    if (!hidden || !pos || (!k && !route_override)) return BUDDY_EINVAL;
+    int max_pos;
+    buddy_status st = check_step_host(M, pos, B, &max_pos);
+    if (st != BUDDY_OK) return st;
+    const int Lm = c.n_layers - 2;
+    if (!route_override)
+        for (int b = 0; b < B; ++b)
+            if (k[b] < 0 || k[b] > Lm) return BUDDY_EINVAL;
+    if (skip_kv == BUDDY_SKIP_KV_MASK) return BUDDY_EUNSUPPORTED;
+
+    hipStream_t s = (hipStream_t)stream;
+    StepArgs a;
+    memset(&a, 0, sizeof(a));
+    a.B = B;
+    for (int b = 0; b < B; ++b) {
+        a.pos[b] = pos[b];
+        a.k[b] = route_override ? 0 : (uint8_t)k[b];
+    }
+    hipError_t e = launch_setup(a, M.ws, s);
+    if (e != hipSuccess) return fail_device(M, e, "setup");
+
+    const Rows all{M.ws.idx_all, M.ws.n_all, B};
+    // first block on every sequence (appends the first-layer K/V row)
+    if ((st = run_block(M, kv, hidden, 0, all, max_pos, s)) != BUDDY_OK) return st;
+    // KV-aware planner and Decision Module, unless the route is given
+    if (!route_override)
+        if ((st = run_planner(M, kv, hidden, B, max_pos, s)) != BUDDY_OK) return st;
+    if ((e = launch_route(M, kv->k, kv->v, B, route_override, mask_out, scores_out, false, s)) !=
+        hipSuccess)
+        return fail_device(M, e, "route");
+    // routable blocks on their compacted sub-batches
+    for (int l = 1; l <= Lm; ++l) {
+        const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), B};
+        if ((st = run_block(M, kv, hidden, l, r, max_pos, s)) != BUDDY_OK) return st;
+    }
+    // last block on every sequence
+    return run_block(M, kv, hidden, c.n_layers - 1, all, max_pos, s);
+}
+
+int32_t buddy_budget_to_k(float b, int32_t n_layers) {
+    if (!(b > 0.f && b <= 1.f) || n_layers < 2) return -1;
+    int32_t k = (int32_t)floor((double)b * n_layers + 0.5) - 2;
+    if (k < 0) k = 0;
+    if (k > n_layers - 2) k = n_layers - 2;
+    return k;
+}
+
+const char* buddy_status_string(buddy_status s) {
+    switch (s) {
+        case BUDDY_OK: return "ok";
+        case BUDDY_EINVAL: return "invalid argument";
+        case BUDDY_ESHAPE: return "unsupported shape";
+        case BUDDY_ECAPACITY: return "batch above capacity";
+        case BUDDY_ENOMEM: return "out of device memory";
+        case BUDDY_EDEVICE: return "HIP error";
+        case BUDDY_EUNSUPPORTED: return "not implemented";
+    }
+    return "unknown status";
+}
+
+const char* buddy_last_error(const buddy_model* h) { return h ? h->M.last_error : ""; }
+
+}  // extern "C"

@@ -1,0 +1,177 @@
+// Internal declarations shared by the HIP translation units of libbuddy.
+// Device helpers, the workspace layout and the launcher entry points that
+// the host API (api.hip) calls.  gfx950 only: 64-lane wavefronts.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/buddy.h"
+
+namespace buddy {
+
+typedef uint16_t bf16_t;
+
+constexpr int kMaxBatch = 256;     // batch capacity limit (one WG scans a column)
+constexpr int kMaxGroup = 8;       // query heads per KV head held in registers
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- storage
+
+__device__ __forceinline__ float bf2f(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+// fp32 -> bf16, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ bf16_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)(((u >> 16) & 0x8000u) | 0x7fc0u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+template <typename T> struct St;
+template <> struct St<float> {
+    static constexpr int V = 4;  // elements per 16-byte vector
+    __device__ static float get(const float* p, size_t i) { return p[i]; }
+    __device__ static void put(float* p, size_t i, float v) { p[i] = v; }
+    __device__ static void vec(const float* p, float* out) {
+        float4 w = *reinterpret_cast<const float4*>(p);
+        out[0] = w.x; out[1] = w.y; out[2] = w.z; out[3] = w.w;
+    }
+};
+template <> struct St<bf16_t> {
+    static constexpr int V = 8;
+    __device__ static float get(const bf16_t* p, size_t i) { return bf2f(p[i]); }
+    __device__ static void put(bf16_t* p, size_t i, float v) { p[i] = f2bf(v); }
+    __device__ static void vec(const bf16_t* p, float* out) {
+        uint4 w = *reinterpret_cast<const uint4*>(p);
+        out[0] = __uint_as_float(w.x << 16); out[1] = __uint_as_float(w.x & 0xffff0000u);
+        out[2] = __uint_as_float(w.y << 16); out[3] = __uint_as_float(w.y & 0xffff0000u);
+        out[4] = __uint_as_float(w.z << 16); out[5] = __uint_as_float(w.z & 0xffff0000u);
+        out[6] = __uint_as_float(w.w << 16); out[7] = __uint_as_float(w.w & 0xffff0000u);
+    }
+};
+
+// ------------------------------------------------------------- reductions
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+// Arrival counter for "last workgroup finishes the reduction".  Every
+// thread's global writes are made visible device-wide before the arrival;
+// the workgroup that arrives last (count == expected) sees all of them and
+// re-arms the counter for the next launch.  No workgroup ever waits.
+__device__ __forceinline__ bool arrive_last(int* counter, int expected) {
+    __shared__ int s_last;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int prev = atomicAdd(counter, 1);
+        s_last = (prev == expected - 1);
+        if (s_last) atomicExch(counter, 0);
+    }
+    __syncthreads();
+    bool last = s_last != 0;
+    if (last) __threadfence();
+    return last;
+}
+
+// --------------------------------------------------------------- workspace
+
+struct Workspace {
+    int32_t* pos;        // [max_batch]   positions of this step
+    int32_t* kb;         // [max_batch]   budgets
+    int32_t* idx_all;    // [max_batch]   identity row list for blocks 0 and L-1
+    int32_t* n_all;      // [1]           = B
+    int32_t* idx;        // [L-2][max_batch] per-block routed rows, ascending
+    int32_t* cnt;        // [L-2]         routed row count per block
+    uint8_t* mask;       // [max_batch][L-2] executed mask
+    float* scores;       // [max_batch][L-2]
+    float* z;            // [max_batch][din]  router context
+    float* a;            // [max_batch][dm_hidden]
+    float* q;            // [max_batch][n_heads hd]  rotated queries
+    float* o;            // [max_batch][n_heads hd]  attention output
+    float* m;            // [max_batch][d_ffn]       SwiGLU output
+    float* part;         // attention partials [max_batch][n_heads][max_chunks][hd + 2]
+    float* pool_part;    // pool partials [max_batch][n_kv][max_pool_splits][2 hd]
+    int32_t* attn_cnt;   // [max_batch][n_kv] arrival counters
+    int32_t* pool_cnt;   // [max_batch][n_kv]
+    int32_t* route_cnt;  // [1]
+    double* inv_freq;    // [hd/2] rotary inverse frequencies
+    int max_chunks;
+    int max_pool_splits;
+};
+
+struct Model {
+    buddy_config cfg;
+    buddy_layer_weights* layers;  // host array of device pointers
+    buddy_dm_weights dm;
+    Workspace ws;
+    void* ws_base;                // one allocation holding the workspace
+    int device;
+    char last_error[256];
+};
+
+// Per-step host values handed to the device through kernel arguments.
+struct StepArgs {
+    int32_t B;
+    int32_t pos[kMaxBatch];
+    uint8_t k[kMaxBatch];
+};
+
+// --------------------------------------------------------------- launchers
+
+// Row set of one routed launch: rows i < *cnt map to sequences idx[i]; the
+// grid is sized for at most n_max rows.
+struct Rows {
+    const int32_t* idx;
+    const int32_t* cnt;
+    int n_max;
+};
+
+hipError_t launch_setup(const StepArgs& a, const Workspace& ws, hipStream_t s);
+
+// Mean of K/V rows 0..pos of the first layer, joined with h: z = [mK | mV | h].
+hipError_t launch_pool(const Model& M, const void* k0, const void* v0, const float* h,
+                       int B, int max_pos, hipStream_t s);
+
+// Decision Module second layer + prior + top-k (or the override mask), then
+// zero-fill of skipped K/V rows and per-block compaction.
+hipError_t launch_route(const Model& M, const void* kc, const void* vc, int B,
+                        const uint8_t* route_override, uint8_t* mask_out,
+                        float* scores_out, bool scores_only, hipStream_t s);
+
+hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B, int n,
+                              uint8_t* mask_out, hipStream_t s);
+
+enum Pro { PRO_NONE = 0, PRO_RMSNORM = 1 };
+enum Epi { EPI_ADD = 0, EPI_BIAS_ACT = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+
+struct GemvArgs {
+    const void* W; int N; int K;       // weight [N][K]
+    const float* X; int ldx;           // activation rows, indexed by sequence
+    const void* gain; float eps;       // PRO_RMSNORM
+    Rows rows;
+    float* Y; int ldy;                 // output rows, indexed by sequence
+    const void* bias; int act;         // EPI_BIAS_ACT
+    int f;                             // EPI_SWIGLU: rows j and f + j
+    // EPI_QKV: rotary + cache append of this block
+    void* kc; void* vc; int T; int hd; int nq; int nkv; int bcap;
+    const int32_t* pos; const double* inv_freq;
+};
+hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream_t s);
+
+struct AttnArgs {
+    const float* q; float* o;
+    const void* kc; const void* vc;    // this block's cache base
+    int T, hd, nq, nkv, bcap;
+    const int32_t* pos;
+    Rows rows;
+    int chunks, chunk_len;
+    float* part; int32_t* counters; int max_chunks;
+};
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
+
+}  // namespace buddy

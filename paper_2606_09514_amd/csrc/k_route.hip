@@ -1,0 +1,277 @@
+// Router-side kernels of the budget-routed decode step (gfx950).
+//
+//  setup_kernel   publishes the step's positions and budgets to device memory
+//                 and the identity row list used by the always-run blocks.
+//  pool_kernel    KV-aware planner (Sec. 4.3): mean of the first layer's K
+//                 and V rows 0..pos per KV head, joined with the newest hidden
+//                 state: z = [mean K | mean V | h].  Positions are split over
+//                 workgroups; the last workgroup of each (sequence, head)
+//                 folds the split partials (no atomics on data).
+//  route_kernel   Decision Module output layer plus prior fusion (Eq. 2),
+//                 deterministic top-k by rank counting, zero-fill of the K/V
+//                 row of every skipped block (Sec. 6), and -- in the last
+//                 workgroup -- grouping by mask (App. C.1): for every routable
+//                 block the ascending list of sequences that run it.
+//  topk_kernel    the standalone top-k entry point.
+#include "buddy_internal.h"
+
+namespace buddy {
+
+// ------------------------------------------------------------------ setup
+
+__global__ __launch_bounds__(256) void setup_kernel(StepArgs a, Workspace ws) {
+    const int t = threadIdx.x;
+    if (t < a.B) {
+        ws.pos[t] = a.pos[t];
+        ws.kb[t] = a.k[t];
+        ws.idx_all[t] = t;
+    }
+    if (t == 0) ws.n_all[0] = a.B;
+}
+
+hipError_t launch_setup(const StepArgs& a, const Workspace& ws, hipStream_t s) {
+    setup_kernel<<<1, 256, 0, s>>>(a, ws);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------- pool
+
+struct PoolParams {
+    const void* k0; const void* v0;  // first layer's cache base
+    const float* h; int d;           // newest hidden [B][d]
+    const int32_t* pos;
+    float* z; int din;
+    float* part; int32_t* counters;
+    int T, hd, nkv, splits, max_splits;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void pool_kernel(PoolParams p) {
+    constexpr int V = St<T>::V;
+    __shared__ float red[2][256 * V];   // [K|V][row slot][hd] partial sums
+    const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x;
+    const int n = p.pos[b] + 1;
+    const int cpr = p.hd / V;           // threads per cache row
+    const int rpp = 256 / cpr;          // rows per pass
+    const int col = tid % cpr, slot = tid / cpr;
+    const int len = (n + p.splits - 1) / p.splits;
+    const int j0 = s * len, j1 = min(j0 + len, n);
+    const size_t base = ((size_t)b * p.nkv + g) * p.T * p.hd;
+    const T* K = (const T*)p.k0 + base;
+    const T* Vc = (const T*)p.v0 + base;
+
+    float ak[V], av[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) ak[e] = av[e] = 0.f;
+    for (int j = j0 + slot; j < j1; j += rpp) {
+        float kr[V], vr[V];
+        St<T>::vec(K + (size_t)j * p.hd + col * V, kr);
+        St<T>::vec(Vc + (size_t)j * p.hd + col * V, vr);
+#pragma unroll
+        for (int e = 0; e < V; ++e) { ak[e] += kr[e]; av[e] += vr[e]; }
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+        red[0][slot * p.hd + col * V + e] = ak[e];
+        red[1][slot * p.hd + col * V + e] = av[e];
+    }
+    __syncthreads();
+    float* part = p.part + (((size_t)b * p.nkv + g) * p.max_splits) * 2 * p.hd;
+    for (int t = tid; t < 2 * p.hd; t += 256) {
+        const int which = t / p.hd, e = t % p.hd;
+        float acc = 0.f;
+        for (int r = 0; r < rpp; ++r) acc += red[which][r * p.hd + e];
+        part[(size_t)s * 2 * p.hd + t] = acc;
+    }
+    // the newest hidden state is the last part of z
+    if (s == 0 && g == 0)
+        for (int t = tid; t < p.d; t += 256)
+            p.z[(size_t)b * p.din + 2 * p.nkv * p.hd + t] = p.h[(size_t)b * p.d + t];
+
+    if (arrive_last(&p.counters[b * p.nkv + g], p.splits)) {
+        const float inv_n = 1.0f / (float)n;
+        for (int t = tid; t < 2 * p.hd; t += 256) {
+            float acc = 0.f;
+            for (int q = 0; q < p.splits; ++q) acc += part[(size_t)q * 2 * p.hd + t];
+            const int which = t / p.hd, e = t % p.hd;
+            p.z[(size_t)b * p.din + which * p.nkv * p.hd + g * p.hd + e] = acc * inv_n;
+        }
+    }
+}
+
+hipError_t launch_pool(const Model& M, const void* k0, const void* v0, const float* h,
+                       int B, int max_pos, hipStream_t s) {
+    const buddy_config& c = M.cfg;
+    PoolParams p;
+    p.k0 = k0; p.v0 = v0; p.h = h; p.d = c.d_model;
+    p.pos = M.ws.pos; p.z = M.ws.z; p.din = 2 * c.n_kv_heads * c.head_dim + c.d_model;
+    p.part = M.ws.pool_part; p.counters = M.ws.pool_cnt;
+    p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.max_splits = M.ws.max_pool_splits;
+    // enough workgroups to stream the first-layer cache with the whole chip,
+    // at least 64 rows per workgroup
+    int want = (512 + B * c.n_kv_heads - 1) / (B * c.n_kv_heads);
+    int by_len = (max_pos + 1 + 63) / 64;
+    int splits = want < by_len ? want : by_len;
+    if (splits < 1) splits = 1;
+    if (splits > p.max_splits) splits = p.max_splits;
+    p.splits = splits;
+    dim3 grid(splits, c.n_kv_heads, B);
+    if (c.dtype == BUDDY_BF16) pool_kernel<bf16_t><<<grid, 256, 0, s>>>(p);
+    else pool_kernel<float><<<grid, 256, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ route
+
+// Strict total order of the top-k: a number beats NaN, larger beats smaller,
+// equal values go to the lower layer index.
+__device__ __forceinline__ bool beats(float sj, int j, float si, int i) {
+    const bool nj = isnan(sj), ni = isnan(si);
+    if (nj != ni) return ni;
+    if (!nj && sj != si) return sj > si;
+    return j < i;
+}
+
+struct RouteParams {
+    const float* a; int H;
+    const void* w2; const void* b2; const float* prior; float omega;
+    int Lm, B;
+    const int32_t* kb; const int32_t* pos;
+    const uint8_t* route_override;
+    uint8_t* mask; uint8_t* mask_out;
+    float* scores; float* scores_out;
+    void* kc; void* vc;               // cache bases (layer 0)
+    int T, hd, nkv, bcap;
+    int32_t* idx; int32_t* cnt; int32_t* counter;
+    int scores_only;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
+    __shared__ float s_sc[256];
+    __shared__ uint8_t s_mask[256];
+    const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int Lm = p.Lm;
+
+    if (p.route_override) {
+        if (tid < Lm) s_mask[tid] = p.route_override[(size_t)b * Lm + tid] != 0;
+    } else {
+        const T* w2 = (const T*)p.w2;
+        const float* a = p.a + (size_t)b * p.H;
+        for (int i = wave; i < Lm; i += 4) {
+            float acc = 0.f;
+            for (int h = lane; h < p.H; h += kWave) acc += St<T>::get(w2, (size_t)i * p.H + h) * a[h];
+            acc = wave_sum(acc);
+            if (lane == 0) {
+                float v = acc + St<T>::get((const T*)p.b2, i);
+                if (p.prior) v += p.omega * p.prior[i];
+                s_sc[i] = v;
+            }
+        }
+        __syncthreads();
+        if (tid < Lm) {
+            p.scores[(size_t)b * Lm + tid] = s_sc[tid];
+            if (p.scores_out) p.scores_out[(size_t)b * Lm + tid] = s_sc[tid];
+        }
+        if (p.scores_only) return;
+        if (tid < Lm) {
+            const float si = s_sc[tid];
+            int rank = 0;
+            for (int j = 0; j < Lm; ++j) rank += (j != tid) && beats(s_sc[j], j, si, tid);
+            s_mask[tid] = rank < p.kb[b];
+        }
+    }
+    __syncthreads();
+    if (tid < Lm) {
+        p.mask[(size_t)b * Lm + tid] = s_mask[tid];
+        if (p.mask_out) p.mask_out[(size_t)b * Lm + tid] = s_mask[tid];
+    }
+
+    // zero-filled K/V row at this step's position for every skipped block
+    const int pos = p.pos[b];
+    const size_t layer_stride = (size_t)p.bcap * p.nkv * p.T * p.hd;
+    const int per_layer = p.nkv * p.hd;
+    for (int t = tid; t < Lm * per_layer; t += 256) {
+        const int i = t / per_layer, r = t % per_layer;
+        if (s_mask[i]) continue;
+        const int g = r / p.hd, e = r % p.hd;
+        const size_t at = (size_t)(i + 1) * layer_stride +
+                          (((size_t)b * p.nkv + g) * p.T + pos) * p.hd + e;
+        ((T*)p.kc)[at] = (T)0;
+        ((T*)p.vc)[at] = (T)0;
+    }
+
+    // grouping by mask, done once every sequence's mask is written
+    if (arrive_last(p.counter, gridDim.x)) {
+        for (int i = wave; i < Lm; i += 4) {
+            int base = 0;
+            for (int b0 = 0; b0 < p.B; b0 += kWave) {
+                const int bb = b0 + lane;
+                const bool sel = bb < p.B && p.mask[(size_t)bb * Lm + i];
+                const uint64_t bal = __ballot(sel);
+                const int before = __popcll(bal & ((1ull << lane) - 1ull));
+                if (sel) p.idx[(size_t)i * p.bcap + base + before] = bb;
+                base += __popcll(bal);
+            }
+            if (lane == 0) p.cnt[i] = base;
+        }
+    }
+}
+
+hipError_t launch_route(const Model& M, const void* kc, const void* vc, int B,
+                        const uint8_t* route_override, uint8_t* mask_out,
+                        float* scores_out, bool scores_only, hipStream_t s) {
+    const buddy_config& c = M.cfg;
+    RouteParams p;
+    p.a = M.ws.a; p.H = c.dm_hidden;
+    p.w2 = M.dm.w2; p.b2 = M.dm.b2; p.prior = M.dm.prior; p.omega = M.dm.omega;
+    p.Lm = c.n_layers - 2; p.B = B;
+    p.kb = M.ws.kb; p.pos = M.ws.pos;
+    p.route_override = route_override;
+    p.mask = M.ws.mask; p.mask_out = mask_out;
+    p.scores = M.ws.scores; p.scores_out = scores_out;
+    p.kc = (void*)kc; p.vc = (void*)vc;
+    p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.bcap = c.max_batch;
+    p.idx = M.ws.idx; p.cnt = M.ws.cnt; p.counter = M.ws.route_cnt;
+    p.scores_only = scores_only ? 1 : 0;
+    if (c.dtype == BUDDY_BF16) route_kernel<bf16_t><<<B, 256, 0, s>>>(p);
+    else route_kernel<float><<<B, 256, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+// ----------------------------------------------------------- select_topk
+
+struct TopkArgs {
+    int n, rows;
+    uint8_t k[kMaxBatch];
+};
+
+__global__ __launch_bounds__(256) void topk_kernel(const float* scores, uint8_t* mask, TopkArgs a) {
+    __shared__ float s_sc[256];
+    const int r = blockIdx.x, tid = threadIdx.x;
+    if (tid < a.n) s_sc[tid] = scores[(size_t)r * a.n + tid];
+    __syncthreads();
+    if (tid < a.n) {
+        const float si = s_sc[tid];
+        int rank = 0;
+        for (int j = 0; j < a.n; ++j) rank += (j != tid) && beats(s_sc[j], j, si, tid);
+        mask[(size_t)r * a.n + tid] = rank < (int)a.k[r];
+    }
+}
+
+hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B, int n,
+                              uint8_t* mask_out, hipStream_t s) {
+    for (int r0 = 0; r0 < B; r0 += kMaxBatch) {
+        TopkArgs a;
+        a.n = n;
+        a.rows = B - r0 < kMaxBatch ? B - r0 : kMaxBatch;
+        for (int r = 0; r < a.rows; ++r) a.k[r] = (uint8_t)k_host[r0 + r];
+        topk_kernel<<<a.rows, 256, 0, s>>>(scores + (size_t)r0 * n, mask_out + (size_t)r0 * n, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace buddy

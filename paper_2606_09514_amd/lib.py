@@ -1,0 +1,200 @@
+"""ctypes binding of libbuddy.so, the C ABI declared in include/buddy.h.
+
+Argument marshalling only: torch tensors are passed as device pointers and
+torch's current HIP stream as the stream; every step of the decode path runs
+in the library's HIP kernels.  Importing this module does not load the
+library; the first call does, and fails loudly when it has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+_SO = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbuddy.so")
+
+OK, EINVAL, ESHAPE, ECAPACITY, ENOMEM, EDEVICE, EUNSUPPORTED = range(7)
+F32, BF16 = 0, 1
+ACT_SILU, ACT_GELU_ERF = 0, 1
+SKIP_KV_ZERO, SKIP_KV_MASK = 0, 1
+
+
+class Config(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ffn", C.c_int32),
+                ("dm_hidden", C.c_int32), ("dm_act", C.c_int32), ("dtype", C.c_int32),
+                ("max_batch", C.c_int32), ("max_ctx", C.c_int32),
+                ("rms_eps", C.c_float), ("rope_theta", C.c_float)]
+
+
+class LayerWeights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in
+                ("attn_norm", "wqkv", "wo", "mlp_norm", "wgate_up", "wdown")]
+
+
+class DMWeights(C.Structure):
+    _fields_ = [("w1", C.c_void_p), ("b1", C.c_void_p), ("w2", C.c_void_p),
+                ("b2", C.c_void_p), ("prior", C.c_void_p), ("omega", C.c_float)]
+
+
+class KV(C.Structure):
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p)]
+
+
+class BuddyError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(msg)
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises when the HIP extension is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO):
+            raise RuntimeError(f"libbuddy.so is not built ({_SO}); run "
+                               "`python -m paper_2606_09514_amd.build` or __graft_entry__.build()")
+        L = C.CDLL(_SO)
+        vp, i32, P = C.c_void_p, C.c_int32, C.POINTER
+        L.buddy_model_create.argtypes = [P(Config), P(LayerWeights), P(DMWeights), P(vp)]
+        L.buddy_model_create.restype = C.c_int
+        L.buddy_model_destroy.argtypes = [vp]
+        L.buddy_model_destroy.restype = None
+        L.buddy_pool_route.argtypes = [vp, P(KV), vp, vp, i32, vp, vp]
+        L.buddy_pool_route.restype = C.c_int
+        L.buddy_select_topk.argtypes = [vp, vp, i32, i32, vp, vp]
+        L.buddy_select_topk.restype = C.c_int
+        L.buddy_decode_step.argtypes = [vp, P(KV), vp, vp, vp, i32, i32, vp, vp, vp, vp]
+        L.buddy_decode_step.restype = C.c_int
+        L.buddy_budget_to_k.argtypes = [C.c_float, i32]
+        L.buddy_budget_to_k.restype = i32
+        L.buddy_status_string.argtypes = [C.c_int]
+        L.buddy_status_string.restype = C.c_char_p
+        L.buddy_last_error.argtypes = [vp]
+        L.buddy_last_error.restype = C.c_char_p
+        _lib = L
+    return _lib
+
+
+def _dev(t, name, dtype=None):
+    if t is None:
+        return None
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.is_contiguous()):
+        raise TypeError(f"{name}: expected a contiguous device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _host_i32(values):
+    arr = (C.c_int32 * max(len(values), 1))(*[int(v) for v in values])
+    return arr
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _raise(rc: int, handle=None):
+    if rc != OK:
+        L = lib()
+        msg = L.buddy_status_string(rc).decode()
+        if handle is not None:
+            extra = L.buddy_last_error(handle).decode()
+            if extra:
+                msg += f" ({extra})"
+        raise BuddyError(rc, msg)
+
+
+def budget_to_k(b: float, n_layers: int) -> int:
+    return int(lib().buddy_budget_to_k(float(b), int(n_layers)))
+
+
+def select_topk(scores: torch.Tensor, k, mask_out: torch.Tensor, stream=None,
+                check: bool = True) -> int:
+    B, n = (scores.shape[0], scores.shape[1]) if scores.dim() == 2 else (0, 0)
+    rc = lib().buddy_select_topk(_dev(scores, "scores", torch.float32), _host_i32(k), B, n,
+                                 _dev(mask_out, "mask_out", torch.uint8), _stream(stream))
+    if check:
+        _raise(rc)
+    return rc
+
+
+class Model:
+    """A model handle over caller-owned device weights.
+
+    cfg: dict with the buddy_config fields (dm_act 'silu'|'gelu', dtype
+    'f32'|'bf16').  weights: {'layers': [dict of tensors], 'dm': {...}} as
+    produced by paper_2606_09514_amd.synth.model_weights on the device.
+    """
+
+    def __init__(self, cfg: dict, weights: dict, max_batch: int):
+        self.cfg = dict(cfg)
+        self.dtype = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
+        c = Config(cfg["n_layers"], cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"],
+                   cfg["head_dim"], cfg["d_ffn"], cfg["dm_hidden"],
+                   ACT_GELU_ERF if cfg["dm_act"] == "gelu" else ACT_SILU,
+                   BF16 if cfg["dtype"] == "bf16" else F32, int(max_batch), cfg["max_ctx"],
+                   float(cfg["rms_eps"]), float(cfg["rope_theta"]))
+        self._c = c
+        self._keep = weights
+        L = cfg["n_layers"]
+        arr = (LayerWeights * L)()
+        for i, lw in enumerate(weights["layers"]):
+            for n, _ in LayerWeights._fields_:
+                setattr(arr[i], n, _dev(lw[n], n, self.dtype))
+        dm = weights["dm"]
+        d = DMWeights(_dev(dm["w1"], "w1", self.dtype), _dev(dm["b1"], "b1", self.dtype),
+                      _dev(dm["w2"], "w2", self.dtype), _dev(dm["b2"], "b2", self.dtype),
+                      _dev(dm.get("prior"), "prior", torch.float32), float(dm.get("omega", 0.0)))
+        h = C.c_void_p()
+        rc = lib().buddy_model_create(C.byref(c), arr, C.byref(d), C.byref(h))
+        _raise(rc)
+        self._h = h
+
+    @property
+    def L_mid(self) -> int:
+        return self.cfg["n_layers"] - 2
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().buddy_model_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def decode_step(self, k_cache, v_cache, hidden, pos, k, route_override=None,
+                    mask_out=None, scores_out=None, skip_kv: int = SKIP_KV_ZERO,
+                    stream=None, check: bool = True) -> int:
+        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype))
+        B = len(pos)
+        rc = lib().buddy_decode_step(
+            self._h, C.byref(kv), _dev(hidden, "hidden", torch.float32), _host_i32(pos),
+            _host_i32(k) if k is not None else None, B, int(skip_kv),
+            _dev(route_override, "route_override", torch.uint8),
+            _dev(mask_out, "mask_out", torch.uint8),
+            _dev(scores_out, "scores_out", torch.float32), _stream(stream))
+        if check:
+            _raise(rc, self._h)
+        return rc
+
+    def pool_route(self, k_cache, v_cache, pos, h_new, scores_out, stream=None,
+                   check: bool = True) -> int:
+        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype))
+        rc = lib().buddy_pool_route(self._h, C.byref(kv), _host_i32(pos),
+                                    _dev(h_new, "h_new", torch.float32), len(pos),
+                                    _dev(scores_out, "scores_out", torch.float32),
+                                    _stream(stream))
+        if check:
+            _raise(rc, self._h)
+        return rc
