@@ -1,0 +1,251 @@
+#!/usr/bin/env python3
+"""Benchmark of the budget-routed decode step on one MI355X.
+
+Workload: a Llama-3-8B-shaped random-init model (32 blocks, d 4096, 32/8
+heads, FFN 14336, Decision Module hidden 512, bf16 weights and KV cache),
+batch 1 with 2048 cached positions, decoding with budgets k in {15, 22, 30}.
+Inputs are synthetic (seeded), resident in HBM before timing.
+
+For each k: W untimed warm-up steps, then K timed steps bracketed by a
+device synchronisation on both sides; the hidden state is fed back and the
+position advances every step.  The headline `value` is tokens/s at the first
+budget (k = 15).  The roofline object covers the dominant kernel (the
+RMSNorm + gate/up + SwiGLU GEMV of the first block, which runs every step),
+timed live with HIP events around that launch inside the timed region.  The
+CPU baseline times the oracle on the host cores on a bounded sample of the
+same workload.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0   # MI355X HBM3E peak
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """Raw hipEvent_t handles for the library's timing hook."""
+
+    def __init__(self):
+        self.h = C.CDLL("libamdhip64.so")
+        self.h.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.h.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.h.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.h.hipEventDestroy.argtypes = [C.c_void_p]
+
+    def create(self, n):
+        out = []
+        for _ in range(n):
+            e = C.c_void_p()
+            assert self.h.hipEventCreate(C.byref(e)) == 0
+            out.append(e.value)
+        return out
+
+    def elapsed_ms(self, a, b):
+        assert self.h.hipEventSynchronize(C.c_void_p(b)) == 0
+        ms = C.c_float()
+        assert self.h.hipEventElapsedTime(C.byref(ms), C.c_void_p(a), C.c_void_p(b)) == 0
+        return ms.value
+
+    def destroy(self, evs):
+        for e in evs:
+            self.h.hipEventDestroy(C.c_void_p(e))
+
+
+def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer):
+    import torch
+    from paper_2606_09514_amd import costmodel
+    from paper_2606_09514_amd import lib as blib
+
+    B, Lm = w.batch, cfg["n_layers"] - 2
+    hidden = x0.clone()
+    masks = torch.zeros((steps, B, Lm), dtype=torch.uint8, device="cuda")
+    pos = w.ctx
+    for _ in range(warmup):
+        model.decode_step(dk, dv, hidden, [pos] * B, ks)
+        pos += 1
+    starts, stops = hip.create(steps), hip.create(steps)
+    model.set_timing_events(blib.KERNEL_GATE_UP, kernel_layer, starts, stops)
+    positions = []
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for t in range(steps):
+        model.decode_step(dk, dv, hidden, [pos] * B, ks, mask_out=masks[t])
+        positions.append([pos] * B)
+        pos += 1
+    t1.record()
+    torch.cuda.synchronize()
+    model.set_timing_events(blib.KERNEL_GATE_UP, kernel_layer, [], [])
+    total_ms = t0.elapsed_time(t1)
+    kern_ms = [hip.elapsed_ms(a, b) for a, b in zip(starts, stops)]
+    hip.destroy(starts + stops)
+    m = masks.cpu().numpy()
+    step_bytes = [costmodel.step_bytes(cfg, m[t], positions[t]) for t in range(steps)]
+    total_bytes = sum(s["total"] for s in step_bytes)
+    assert all(int(m[t, b].sum()) == ks[b] for t in range(steps) for b in range(B))
+    distinct = len({m[t].tobytes() for t in range(steps)})
+    return dict(total_ms=total_ms, ms_per_step=total_ms / steps,
+                tokens_per_s=B * steps / (total_ms / 1e3),
+                bytes_per_step=total_bytes / steps,
+                step_hbm_frac=total_bytes / (total_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+                layers_used=sum(s["layers_used"] for s in step_bytes) / steps,
+                distinct_routes=distinct, kernel_ms=sum(kern_ms) / len(kern_ms),
+                hidden=hidden, end_pos=pos)
+
+
+def cpu_baseline(cfg, W, dk, dv, x0, k, ctx, budget_s=12.0):
+    """The oracle on the host cores: decode steps of sequence 0 of the same
+    workload until about budget_s seconds of CPU work (at least one)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2606_09514_amd import synth
+
+    log("cpu_baseline: copying weights and sequence 0's cache to the host")
+    layers = [{n: synth.storage_numpy(t) for n, t in lw.items()} for lw in W["layers"]]
+    dm = {n: (synth.storage_numpy(t) if torch.is_tensor(t) else t) for n, t in W["dm"].items()}
+    orc = oracle.Oracle(cfg, layers, dm)
+    hk = synth.storage_numpy(dk[:, 0]).copy()
+    hv = synth.storage_numpy(dv[:, 0]).copy()
+    x = x0[0].cpu().numpy()
+    L = cfg["n_layers"]
+    n, t0 = 0, time.perf_counter()
+    while True:
+        h, *_ = orc.decode_seq([hk[l] for l in range(L)], [hv[l] for l in range(L)],
+                               ctx + n, k, x)
+        x = h.astype(np.float32)
+        n += 1
+        el = time.perf_counter() - t0
+        log(f"cpu_baseline: oracle step {n} done, {el:.1f} s")
+        if el >= budget_s or n >= 8:
+            break
+    return dict(value=n / el, unit="tokens/s", cores=oracle.num_threads(), kind="oracle",
+                sample=f"{n} decode step(s) of sequence 0 at k={k}, ctx {ctx}, "
+                       f"same weights and cache, oracle in double precision")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=128)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="llama3_8b_b1_ctx2048")
+    ap.add_argument("--budgets", default=None, help="comma list of k (default: the workload's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--policy", default="auto", choices=["auto", "device", "host"],
+                    help="launch policy of the routable blocks")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run a 1 GiB device copy first (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs the decode step on one GPU; "
+              f"--gpus {args.gpus} is not supported (sharding is design-only)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_09514_amd import lib as blib
+    from paper_2606_09514_amd import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    blib.lib()                     # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    w = synth.WORKLOADS[args.workload]
+    budgets = [int(b) for b in args.budgets.split(",")] if args.budgets else list(w.budgets)
+    cfg = synth.model_config(w.shape, w.dtype, w.ctx + args.warmup + args.steps + 1)
+
+    if args.copy_calibration:
+        a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        log("copy calibration: 3 x 1 GiB device copies done")
+
+    log(f"generating weights and KV cache for {w.name}")
+    W = synth.model_weights(cfg, seed=0, device="cuda", omega=w.omega)
+    dk, dv = synth.kv_cache(cfg, w.batch, w.ctx, seed=1, device="cuda")
+    x0 = synth.hidden_inputs(w.batch, cfg["d_model"], seed=2, device="cuda")
+    torch.cuda.synchronize()
+    model = blib.Model(cfg, W, max_batch=w.batch)
+    model.set_launch_policy({"auto": blib.LAUNCH_AUTO, "device": blib.LAUNCH_DEVICE_ROUTED,
+                             "host": blib.LAUNCH_HOST_ROUTED}[args.policy])
+    hip = HipEvents()
+
+    runs = {}
+    for i, k in enumerate(budgets if not w.mixed else [None]):
+        ks = synth.budgets(w, seed=1) if w.mixed else [k] * w.batch
+        r = run_budget(model, cfg, w, dk, dv, x0, ks, args.steps, args.warmup, hip, 0)
+        name = "mixed" if w.mixed else str(k)
+        runs[name] = r
+        log(f"k={name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step, "
+            f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline, gate_up {r['kernel_ms'] * 1e3:.1f} us")
+
+    head = runs[next(iter(runs))]
+    head_k = budgets[0] if not w.mixed else None
+    d, f = cfg["d_model"], cfg["d_ffn"]
+    s = 2 if w.dtype == "bf16" else 4
+    # algorithmic bytes of one gate/up launch: weights, input rows, output rows
+    gate_up_bytes = 2 * f * d * s + w.batch * d * 4 + w.batch * f * 4
+    achieved = gate_up_bytes / (head["kernel_ms"] / 1e3) / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, W, dk, dv, x0, head_k if head_k is not None else 15, w.ctx)
+
+    out = {
+        "metric": "routed-decode tokens/s at budget k (1 GPU); % of HBM roofline",
+        "value": round(head["tokens_per_s"], 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(head["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "shape": w.shape, "batch": w.batch, "ctx": w.ctx,
+                   "k": head_k if head_k is not None else "mixed",
+                   "weights_kv": w.dtype, "accumulate": "f32", "omega": w.omega,
+                   "launch_policy": args.policy,
+                   "parallelism": "none (1 GPU)"},
+        "per_budget": {n: {"tokens_per_s": round(r["tokens_per_s"], 2),
+                           "ms_per_step": round(r["ms_per_step"], 4),
+                           "bytes_per_step": int(r["bytes_per_step"]),
+                           "step_hbm_frac": round(r["step_hbm_frac"], 4),
+                           "layers_used": r["layers_used"],
+                           "distinct_routes": r["distinct_routes"],
+                           "gate_up_us": round(r["kernel_ms"] * 1e3, 2)}
+                       for n, r in runs.items()},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": "gemv gate_up+SwiGLU (block 0)",
+                     "bytes_per_launch": gate_up_bytes,
+                     "launch_us": round(head["kernel_ms"] * 1e3, 2)},
+        "cpu_baseline": cpu,
+    }
+    model.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -46,8 +46,9 @@
  *     sequence b before the step; the step writes row pos[b] of every layer
  *     and attends rows 0..pos[b].  The caller advances pos.
  *   - Streams: `stream` is a hipStream_t (NULL = the null stream).  All work
- *     is enqueued on it without host synchronisation; outputs are valid once
- *     the stream reaches the enqueued work.
+ *     is enqueued on it; outputs are valid once the stream reaches the
+ *     enqueued work.  The only host wait is the optional one of the
+ *     host-routed launch policy (buddy_set_launch_policy).
  *   - Errors: arguments are validated on the host before anything is
  *     enqueued; on a validation failure nothing is written and a status is
  *     returned.  BUDDY_EDEVICE reports a HIP launch error; its text is
@@ -89,7 +90,7 @@ typedef struct {
     int32_t n_kv_heads;   /* n_heads / n_kv_heads <= 8                     */
     int32_t head_dim;     /* 64 or 128                                     */
     int32_t d_ffn;        /* multiple of 8                                 */
-    int32_t dm_hidden;    /* Decision Module hidden width, multiple of 2   */
+    int32_t dm_hidden;    /* Decision Module hidden width, multiple of 8   */
     int32_t dm_act;       /* buddy_dm_act                                  */
     int32_t dtype;        /* buddy_dtype of weights and KV cache           */
     int32_t max_batch;    /* 1..256: workspace and KV cache batch capacity */
@@ -158,6 +159,46 @@ buddy_status buddy_decode_step(buddy_model* m, const buddy_kv* kv, float* hidden
                                const int32_t* pos, const int32_t* k, int32_t B,
                                int32_t skip_kv, const uint8_t* route_override,
                                uint8_t* mask_out, float* scores_out, void* stream);
+
+/* How buddy_decode_step launches the routable blocks.
+ *   BUDDY_LAUNCH_DEVICE_ROUTED: everything is enqueued without waiting; every
+ *     routable block is launched and its kernels read the routed row count
+ *     on the device, so a block nobody selected costs only empty launches.
+ *     The call never blocks the host (suitable for stream capture).
+ *   BUDDY_LAUNCH_HOST_ROUTED: after the router, the call waits for the
+ *     per-block routed counts (written by the device to mapped pinned host
+ *     memory owned by the handle) and launches only the blocks some sequence
+ *     runs, with grids sized to the routed rows.  The host blocks until the
+ *     first block and the router have run.
+ *   BUDDY_LAUNCH_AUTO (default): host-routed when B <= 16 and not every
+ *     sequence runs every block, device-routed otherwise. */
+typedef enum {
+    BUDDY_LAUNCH_AUTO = 0,
+    BUDDY_LAUNCH_DEVICE_ROUTED = 1,
+    BUDDY_LAUNCH_HOST_ROUTED = 2
+} buddy_launch_policy;
+
+/* Sets the launch policy of a handle; BUDDY_EINVAL for an unknown policy. */
+buddy_status buddy_set_launch_policy(buddy_model* m, int32_t policy);
+
+/* Kernels of a decoder block, for buddy_set_timing_events. */
+typedef enum {
+    BUDDY_KERNEL_QKV = 0,        /* RMSNorm + QKV projection + rotary + KV append */
+    BUDDY_KERNEL_ATTENTION = 1,  /* split-K decode attention                      */
+    BUDDY_KERNEL_O_PROJ = 2,     /* output projection + residual                  */
+    BUDDY_KERNEL_GATE_UP = 3,    /* RMSNorm + gate/up projection + SwiGLU         */
+    BUDDY_KERNEL_DOWN = 4        /* down projection + residual                    */
+} buddy_kernel;
+
+/* Measurement hook.  For the next n calls of buddy_decode_step on this
+ * handle, call i records start[i] on its stream right before the launch of
+ * `kernel` in block `layer` and stop[i] right after it.  start and stop are
+ * arrays of n hipEvent_t handles that the caller created and keeps alive
+ * until the calls have run; the handle copies the arrays.  n = 0 turns the
+ * hook off.  Errors: BUDDY_EINVAL for a bad kernel, layer or n < 0, or null
+ * arrays with n > 0. */
+buddy_status buddy_set_timing_events(buddy_model* m, int32_t kernel, int32_t layer,
+                                     void* const* start, void* const* stop, int32_t n);
 
 /* Budget to routable-block count, k = round(b L) - 2 (Eq. 2), halves away
  * from zero, limited to [0, L-2]; -1 when b is outside (0, 1]. */

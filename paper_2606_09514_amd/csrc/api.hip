@@ -7,6 +7,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
+#include <chrono>
 #include <new>
 
 #include "buddy_internal.h"
@@ -34,16 +36,33 @@ buddy_status check_config(const buddy_config* c) {
     if (c->n_heads / c->n_kv_heads > kMaxGroup) return BUDDY_ESHAPE;
     if (c->head_dim != 64 && c->head_dim != 128) return BUDDY_ESHAPE;
     if (c->d_ffn <= 0 || c->d_ffn % 8) return BUDDY_ESHAPE;
-    if (c->dm_hidden <= 0 || c->dm_hidden % 2) return BUDDY_ESHAPE;
+    if (c->dm_hidden <= 0 || c->dm_hidden % 8) return BUDDY_ESHAPE;
     if (c->dm_act != BUDDY_ACT_SILU && c->dm_act != BUDDY_ACT_GELU_ERF) return BUDDY_EINVAL;
     if (c->dtype != BUDDY_F32 && c->dtype != BUDDY_BF16) return BUDDY_EINVAL;
     if (c->max_batch < 1 || c->max_batch > kMaxBatch) return BUDDY_ECAPACITY;
     if (c->max_ctx < 1) return BUDDY_EINVAL;
+    if (c->max_ctx > (1 << 20)) return BUDDY_ECAPACITY;  // keeps attention chunks <= 256
     if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return BUDDY_EINVAL;
+    // a GEMV wavefront holds at most 16 k-steps of a two-row unit (K = d_model)
+    // and a quarter of 64 k-steps of a single row
+    const int ks = 64 * (c->dtype == BUDDY_BF16 ? 8 : 4);
+    if (c->d_model > 16 * ks || c->d_ffn > 64 * ks) return BUDDY_ESHAPE;
+    // every K the GEMVs see (d_model, d_ffn, n_heads * head_dim and the
+    // router input 2 n_kv hd + d) is a whole number of k-steps of 64 lanes x
+    // 16 bytes or at most 8 k-steps; fp32 weights (small models) have rows of
+    // at most 8 k-steps
+    const int din = 2 * c->n_kv_heads * c->head_dim + c->d_model;
+    const int qdim = c->n_heads * c->head_dim;
+    auto rows_ok = [ks](int K) { return K % ks == 0 || K <= 8 * ks; };
+    if (c->dtype == BUDDY_BF16 &&
+        !(rows_ok(c->d_model) && rows_ok(c->d_ffn) && rows_ok(qdim) && rows_ok(din)))
+        return BUDDY_ESHAPE;
+    if (c->dtype == BUDDY_F32 &&
+        (c->d_model > 8 * ks || c->d_ffn > 8 * ks || qdim > 8 * ks || din > 8 * ks))
+        return BUDDY_ESHAPE;
     // the activation rows of one GEMV pass must fit in LDS
     const int kmax = c->d_ffn > c->d_model ? c->d_ffn : c->d_model;
     if ((size_t)kmax * sizeof(float) > 80 * 1024) return BUDDY_ESHAPE;
-    const int din = 2 * c->n_kv_heads * c->head_dim + c->d_model;
     if ((size_t)din * sizeof(float) > 80 * 1024) return BUDDY_ESHAPE;
     return BUDDY_OK;
 }
@@ -57,17 +76,37 @@ const char* layer_base(const Model& M, const void* kv, int l) {
     return (const char*)kv + (size_t)l * per_layer * elem_size(c);
 }
 
-int attn_chunks(const Model& M, int B, int max_pos) {
+// Position chunks per (sequence, KV head): enough workgroups to cover the
+// chip (about 2048 over the launch), chunk lengths a multiple of the rows one
+// workgroup block reads, at most kAttnMaxChunks chunks.
+void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chunk_len) {
     const buddy_config& c = M.cfg;
-    // about 2048 workgroups over the step's (sequence, KV head) pairs, each
-    // chunk at least 32 rows
-    const int pairs = B * c.n_kv_heads;
+    const int rows = attention_rows_per_wg(c.dtype, c.head_dim);
+    const int blocks = (max_pos + 1 + rows - 1) / rows;
+    const int pairs = n_rows * c.n_kv_heads;
     int want = (2048 + pairs - 1) / pairs;
-    const int by_len = (max_pos + 1 + 31) / 32;
-    if (want > by_len) want = by_len;
+    if (want > blocks) want = blocks;
+    if (want > kAttnMaxChunks) want = kAttnMaxChunks;
     if (want < 1) want = 1;
-    if (want > M.ws.max_chunks) want = M.ws.max_chunks;
-    return want;
+    // at most kAttnMaxChunks chunks (max_ctx is bounded at create so that
+    // min_chunks itself stays within it)
+    const int min_chunks = (blocks + kAttnMaxChunks - 1) / kAttnMaxChunks;
+    const int per = (blocks + (want > min_chunks ? want : min_chunks) - 1) /
+                    (want > min_chunks ? want : min_chunks);
+    *chunk_len = per * rows;
+    *chunks = (max_pos + 1 + *chunk_len - 1) / *chunk_len;
+}
+
+// Timing hook: event around kernel `kind` of block l, if asked for.
+bool timed(const Model& M, int kind, int l) {
+    const TimingHook& t = M.timing;
+    return t.n > 0 && t.next < t.n && t.kernel == kind && t.layer == l;
+}
+
+hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
+    if (!timed(M, kind, l)) return hipSuccess;
+    const TimingHook& t = M.timing;
+    return hipEventRecord(stop ? t.stop[t.next] : t.start[t.next], s);
 }
 
 buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows rows,
@@ -82,7 +121,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     g.rows = rows;
     g.eps = c.rms_eps;
     g.T = c.max_ctx; g.hd = c.head_dim; g.nq = c.n_heads; g.nkv = c.n_kv_heads;
-    g.bcap = c.max_batch; g.pos = M.ws.pos; g.inv_freq = M.ws.inv_freq;
+    g.bcap = c.max_batch; g.pos = M.ws.pos; g.rope = M.ws.rope;
     g.kc = (void*)layer_base(M, kv->k, l);
     g.vc = (void*)layer_base(M, kv->v, l);
 
@@ -90,7 +129,9 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     g.W = w.wqkv; g.N = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; g.K = c.d_model;
     g.X = hidden; g.ldx = c.d_model; g.gain = w.attn_norm;
     g.Y = M.ws.q; g.ldy = qdim;
-    if ((e = launch_gemv(c.dtype, PRO_RMSNORM, EPI_QKV, g, s)) != hipSuccess)
+    if ((e = mark(M, BUDDY_KERNEL_QKV, l, false, s)) != hipSuccess ||
+        (e = launch_gemv(c.dtype, PRO_RMSNORM, EPI_QKV, g, s)) != hipSuccess ||
+        (e = mark(M, BUDDY_KERNEL_QKV, l, true, s)) != hipSuccess)
         return fail_device(M, e, "qkv");
 
     // attention over rows 0..pos
@@ -98,27 +139,35 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     a.q = M.ws.q; a.o = M.ws.o; a.kc = g.kc; a.vc = g.vc;
     a.T = c.max_ctx; a.hd = c.head_dim; a.nq = c.n_heads; a.nkv = c.n_kv_heads;
     a.bcap = c.max_batch; a.pos = M.ws.pos; a.rows = rows;
-    a.chunks = attn_chunks(M, rows.n_max, max_pos);
-    a.chunk_len = (max_pos + 1 + a.chunks - 1) / a.chunks;
-    a.part = M.ws.part; a.counters = M.ws.attn_cnt; a.max_chunks = M.ws.max_chunks;
-    if ((e = launch_attention(c.dtype, a, s)) != hipSuccess) return fail_device(M, e, "attention");
+    attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
+    a.part = M.ws.part; a.max_chunks = M.ws.max_chunks;
+    if ((e = mark(M, BUDDY_KERNEL_ATTENTION, l, false, s)) != hipSuccess ||
+        (e = launch_attention(c.dtype, a, s)) != hipSuccess ||
+        (e = mark(M, BUDDY_KERNEL_ATTENTION, l, true, s)) != hipSuccess)
+        return fail_device(M, e, "attention");
 
     // h += Wo o
     g.W = w.wo; g.N = c.d_model; g.K = qdim; g.X = M.ws.o; g.ldx = qdim; g.gain = nullptr;
     g.Y = hidden; g.ldy = c.d_model;
-    if ((e = launch_gemv(c.dtype, PRO_NONE, EPI_ADD, g, s)) != hipSuccess)
+    if ((e = mark(M, BUDDY_KERNEL_O_PROJ, l, false, s)) != hipSuccess ||
+        (e = launch_gemv(c.dtype, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
+        (e = mark(M, BUDDY_KERNEL_O_PROJ, l, true, s)) != hipSuccess)
         return fail_device(M, e, "o_proj");
 
     // m = SiLU(Wg u2) * (Wu u2), u2 = RMSNorm(h)
     g.W = w.wgate_up; g.N = 2 * c.d_ffn; g.K = c.d_model; g.X = hidden; g.ldx = c.d_model;
     g.gain = w.mlp_norm; g.f = c.d_ffn; g.Y = M.ws.m; g.ldy = c.d_ffn;
-    if ((e = launch_gemv(c.dtype, PRO_RMSNORM, EPI_SWIGLU, g, s)) != hipSuccess)
+    if ((e = mark(M, BUDDY_KERNEL_GATE_UP, l, false, s)) != hipSuccess ||
+        (e = launch_gemv(c.dtype, PRO_RMSNORM, EPI_SWIGLU, g, s)) != hipSuccess ||
+        (e = mark(M, BUDDY_KERNEL_GATE_UP, l, true, s)) != hipSuccess)
         return fail_device(M, e, "gate_up");
 
     // h += Wdown m
     g.W = w.wdown; g.N = c.d_model; g.K = c.d_ffn; g.X = M.ws.m; g.ldx = c.d_ffn;
     g.gain = nullptr; g.Y = hidden; g.ldy = c.d_model;
-    if ((e = launch_gemv(c.dtype, PRO_NONE, EPI_ADD, g, s)) != hipSuccess)
+    if ((e = mark(M, BUDDY_KERNEL_DOWN, l, false, s)) != hipSuccess ||
+        (e = launch_gemv(c.dtype, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
+        (e = mark(M, BUDDY_KERNEL_DOWN, l, true, s)) != hipSuccess)
         return fail_device(M, e, "down");
     return BUDDY_OK;
 }
@@ -134,11 +183,32 @@ buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, in
     memset(&g, 0, sizeof(g));
     g.W = M.dm.w1; g.N = c.dm_hidden; g.K = 2 * c.n_kv_heads * c.head_dim + c.d_model;
     g.X = M.ws.z; g.ldx = g.K;
-    g.rows = Rows{M.ws.idx_all, M.ws.n_all, B};
+    g.rows = Rows{M.ws.idx_all, M.ws.n_all, B, true};
     g.Y = M.ws.a; g.ldy = c.dm_hidden;
     g.bias = M.dm.b1; g.act = c.dm_act;
     if ((e = launch_gemv(c.dtype, PRO_NONE, EPI_BIAS_ACT, g, s)) != hipSuccess)
         return fail_device(M, e, "dm_hidden");
+    return BUDDY_OK;
+}
+
+// Host-routed launches: spin until the compaction kernel has published the
+// counts of step `seq` to mapped host memory.  A device error, or no answer
+// within a minute, ends the wait with BUDDY_EDEVICE.
+buddy_status wait_route(Model& M, int32_t seq, hipStream_t s) {
+    volatile int32_t* flag = M.h_cnt + (M.cfg.n_layers - 2);
+    const auto t0 = std::chrono::steady_clock::now();
+    long spins = 0;
+    while (*flag != seq) {
+        if ((++spins & 0xfff) == 0) {
+            hipError_t e = hipStreamQuery(s);
+            if (e != hipSuccess && e != hipErrorNotReady) return fail_device(M, e, "route wait");
+            if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(60)) {
+                snprintf(M.last_error, sizeof(M.last_error), "route wait: timed out");
+                return BUDDY_EDEVICE;
+            }
+        }
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
     return BUDDY_OK;
 }
 
@@ -184,8 +254,7 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
     const size_t Bc = c.max_batch, Lm = c.n_layers - 2, hd = c.head_dim;
     const size_t din = 2 * c.n_kv_heads * hd + c.d_model;
     const size_t qdim = (size_t)c.n_heads * hd;
-    int max_chunks = (c.max_ctx + 31) / 32;
-    if (max_chunks > 256) max_chunks = 256;
+    const int max_chunks = kAttnMaxChunks;
     int max_splits = (c.max_ctx + 63) / 64;
     if (max_splits > 64) max_splits = 64;
     M.ws.max_chunks = max_chunks;
@@ -202,8 +271,7 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
         {(void**)&W.m, Bc * c.d_ffn * 4},
         {(void**)&W.part, Bc * c.n_heads * max_chunks * (hd + 2) * 4},
         {(void**)&W.pool_part, Bc * c.n_kv_heads * max_splits * 2 * hd * 4},
-        {(void**)&W.attn_cnt, Bc * c.n_kv_heads * 4}, {(void**)&W.pool_cnt, Bc * c.n_kv_heads * 4},
-        {(void**)&W.route_cnt, 4}, {(void**)&W.inv_freq, hd / 2 * 8},
+        {(void**)&W.rope, (size_t)c.max_ctx * (hd / 2) * sizeof(float2)},
     };
     size_t total = 0;
     for (const Piece& p : pieces) total += align_up(p.bytes);
@@ -213,11 +281,29 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
     size_t off = 0;
     for (const Piece& p : pieces) { *p.dst = (char*)M.ws_base + off; off += align_up(p.bytes); }
     hipError_t e = hipMemset(M.ws_base, 0, total);
-    double* inv = (double*)malloc(hd / 2 * sizeof(double));
-    for (size_t i = 0; i < hd / 2; ++i) inv[i] = pow((double)c.rope_theta, -2.0 * i / (double)hd);
-    if (e == hipSuccess) e = hipMemcpy(W.inv_freq, inv, hd / 2 * sizeof(double), hipMemcpyHostToDevice);
-    free(inv);
+    // rotary table: angle pos * theta^(-2i/hd) in double, cos and sin rounded to fp32
+    const size_t half = hd / 2;
+    float2* rope = (float2*)malloc((size_t)c.max_ctx * half * sizeof(float2));
+    if (!rope) e = hipErrorOutOfMemory;
+    for (size_t i = 0; rope && i < half; ++i) {
+        const double inv_freq = pow((double)c.rope_theta, -2.0 * (double)i / (double)hd);
+        for (int p = 0; p < c.max_ctx; ++p) {
+            const double ang = (double)p * inv_freq;
+            rope[(size_t)p * half + i] = make_float2((float)cos(ang), (float)sin(ang));
+        }
+    }
+    if (e == hipSuccess)
+        e = hipMemcpy(W.rope, rope, (size_t)c.max_ctx * half * sizeof(float2), hipMemcpyHostToDevice);
+    free(rope);
+    if (e == hipSuccess)
+        e = hipHostMalloc((void**)&M.h_cnt, (Lm + 1) * sizeof(int32_t),
+                          hipHostMallocMapped | hipHostMallocCoherent);
+    if (e == hipSuccess) {
+        memset(M.h_cnt, 0xff, (Lm + 1) * sizeof(int32_t));
+        e = hipHostGetDevicePointer((void**)&M.d_host_cnt, M.h_cnt, 0);
+    }
     if (e != hipSuccess) {
+        if (M.h_cnt) (void)hipHostFree(M.h_cnt);
         (void)hipFree(M.ws_base); free(M.layers); delete h; return BUDDY_EDEVICE;
     }
     *out = h;
@@ -228,7 +314,10 @@ void buddy_model_destroy(buddy_model* h) {
     if (!h) return;
     (void)hipDeviceSynchronize();
     (void)hipFree(h->M.ws_base);
+    (void)hipHostFree(h->M.h_cnt);
     free(h->M.layers);
+    free(h->M.timing.start);
+    free(h->M.timing.stop);
     delete h;
 }
 
@@ -251,7 +340,8 @@ buddy_status buddy_pool_route(buddy_model* h, const buddy_kv* kv, const int32_t*
     hipError_t e = launch_setup(a, M.ws, s);
     if (e != hipSuccess) return fail_device(M, e, "setup");
     if ((st = run_planner(M, kv, h_new, B, max_pos, s)) != BUDDY_OK) return st;
-    if ((e = launch_route(M, kv->k, kv->v, B, nullptr, nullptr, scores_out, true, s)) != hipSuccess)
+    if ((e = launch_route(M, kv->k, kv->v, B, nullptr, nullptr, scores_out, true, -1, s)) !=
+        hipSuccess)
         return fail_device(M, e, "scores");
     return BUDDY_OK;
 }
@@ -298,22 +388,74 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     hipError_t e = launch_setup(a, M.ws, s);
     if (e != hipSuccess) return fail_device(M, e, "setup");
 
-    const Rows all{M.ws.idx_all, M.ws.n_all, B};
+    const Rows all{M.ws.idx_all, M.ws.n_all, B, true};
     // first block on every sequence (appends the first-layer K/V row)
     if ((st = run_block(M, kv, hidden, 0, all, max_pos, s)) != BUDDY_OK) return st;
     // KV-aware planner and Decision Module, unless the route is given
     if (!route_override)
         if ((st = run_planner(M, kv, hidden, B, max_pos, s)) != BUDDY_OK) return st;
-    if ((e = launch_route(M, kv->k, kv->v, B, route_override, mask_out, scores_out, false, s)) !=
-        hipSuccess)
+    // Launch policy.  Device-routed: every routable block is launched and its
+    // kernels read the routed row count on the device (an unused block costs
+    // only empty launches).  Host-routed: the compaction kernel publishes the
+    // per-block counts to mapped host memory; the host waits for them and
+    // launches only the blocks some sequence runs, with exact grids.
+    bool all_used = !route_override;
+    for (int b = 0; all_used && b < B; ++b) all_used = k[b] == Lm;
+    bool host_routed = false;
+    if (M.policy == BUDDY_LAUNCH_HOST_ROUTED) host_routed = true;
+    else if (M.policy == BUDDY_LAUNCH_AUTO) host_routed = !all_used && B <= kHostRoutedMaxBatch;
+    host_routed = host_routed && Lm > 0;
+    const int32_t seq = host_routed ? (M.seq = (M.seq + 1) & 0x3fffffff) : -1;
+    if ((e = launch_route(M, kv->k, kv->v, B, route_override, mask_out, scores_out, false, seq,
+                          s)) != hipSuccess)
         return fail_device(M, e, "route");
+    if (host_routed && (st = wait_route(M, seq, s)) != BUDDY_OK) return st;
     // routable blocks on their compacted sub-batches
     for (int l = 1; l <= Lm; ++l) {
-        const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), B};
+        int n_max = B;
+        if (host_routed) {
+            n_max = M.h_cnt[l - 1];
+            if (n_max == 0) continue;
+        }
+        const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), n_max,
+                     host_routed};
         if ((st = run_block(M, kv, hidden, l, r, max_pos, s)) != BUDDY_OK) return st;
     }
     // last block on every sequence
-    return run_block(M, kv, hidden, c.n_layers - 1, all, max_pos, s);
+    st = run_block(M, kv, hidden, c.n_layers - 1, all, max_pos, s);
+    if (M.timing.n > 0 && M.timing.next < M.timing.n) ++M.timing.next;
+    return st;
+}
+
+buddy_status buddy_set_launch_policy(buddy_model* h, int32_t policy) {
+    if (!h || policy < BUDDY_LAUNCH_AUTO || policy > BUDDY_LAUNCH_HOST_ROUTED) return BUDDY_EINVAL;
+    h->M.policy = policy;
+    return BUDDY_OK;
+}
+
+buddy_status buddy_set_timing_events(buddy_model* h, int32_t kernel, int32_t layer,
+                                     void* const* start, void* const* stop, int32_t n) {
+    if (!h || n < 0 || kernel < BUDDY_KERNEL_QKV || kernel > BUDDY_KERNEL_DOWN) return BUDDY_EINVAL;
+    Model& M = h->M;
+    if (layer < 0 || layer >= M.cfg.n_layers) return BUDDY_EINVAL;
+    if (n > 0 && (!start || !stop)) return BUDDY_EINVAL;
+    free(M.timing.start);
+    free(M.timing.stop);
+    memset(&M.timing, 0, sizeof(M.timing));
+    if (n == 0) return BUDDY_OK;
+    M.timing.start = (hipEvent_t*)malloc(sizeof(hipEvent_t) * n);
+    M.timing.stop = (hipEvent_t*)malloc(sizeof(hipEvent_t) * n);
+    if (!M.timing.start || !M.timing.stop) {
+        free(M.timing.start); free(M.timing.stop);
+        memset(&M.timing, 0, sizeof(M.timing));
+        return BUDDY_ENOMEM;
+    }
+    memcpy(M.timing.start, start, sizeof(hipEvent_t) * n);
+    memcpy(M.timing.stop, stop, sizeof(hipEvent_t) * n);
+    M.timing.kernel = kernel;
+    M.timing.layer = layer;
+    M.timing.n = n;
+    return BUDDY_OK;
 }
 
 int32_t buddy_budget_to_k(float b, int32_t n_layers) {

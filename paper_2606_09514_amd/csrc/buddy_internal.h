@@ -15,6 +15,7 @@ typedef uint16_t bf16_t;
 constexpr int kMaxBatch = 256;     // batch capacity limit (one WG scans a column)
 constexpr int kMaxGroup = 8;       // query heads per KV head held in registers
 constexpr int kWave = 64;
+constexpr int kAttnMaxChunks = 256;  // position chunks per (sequence, KV head)
 
 // ---------------------------------------------------------------- storage
 
@@ -51,31 +52,28 @@ template <> struct St<bf16_t> {
     }
 };
 
+// Raw 16-byte weight vectors stay packed in registers until they are used.
+template <typename TW>
+__device__ __forceinline__ void unpack(const uint4& w, float* out);
+template <>
+__device__ __forceinline__ void unpack<bf16_t>(const uint4& w, float* out) {
+    out[0] = __uint_as_float(w.x << 16); out[1] = __uint_as_float(w.x & 0xffff0000u);
+    out[2] = __uint_as_float(w.y << 16); out[3] = __uint_as_float(w.y & 0xffff0000u);
+    out[4] = __uint_as_float(w.z << 16); out[5] = __uint_as_float(w.z & 0xffff0000u);
+    out[6] = __uint_as_float(w.w << 16); out[7] = __uint_as_float(w.w & 0xffff0000u);
+}
+template <>
+__device__ __forceinline__ void unpack<float>(const uint4& w, float* out) {
+    out[0] = __uint_as_float(w.x); out[1] = __uint_as_float(w.y);
+    out[2] = __uint_as_float(w.z); out[3] = __uint_as_float(w.w);
+}
+
 // ------------------------------------------------------------- reductions
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
     return v;
-}
-
-// Arrival counter for "last workgroup finishes the reduction".  Every
-// thread's global writes are made visible device-wide before the arrival;
-// the workgroup that arrives last (count == expected) sees all of them and
-// re-arms the counter for the next launch.  No workgroup ever waits.
-__device__ __forceinline__ bool arrive_last(int* counter, int expected) {
-    __shared__ int s_last;
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int prev = atomicAdd(counter, 1);
-        s_last = (prev == expected - 1);
-        if (s_last) atomicExch(counter, 0);
-    }
-    __syncthreads();
-    bool last = s_last != 0;
-    if (last) __threadfence();
-    return last;
 }
 
 // --------------------------------------------------------------- workspace
@@ -96,16 +94,30 @@ struct Workspace {
     float* m;            // [max_batch][d_ffn]       SwiGLU output
     float* part;         // attention partials [max_batch][n_heads][max_chunks][hd + 2]
     float* pool_part;    // pool partials [max_batch][n_kv][max_pool_splits][2 hd]
-    int32_t* attn_cnt;   // [max_batch][n_kv] arrival counters
-    int32_t* pool_cnt;   // [max_batch][n_kv]
-    int32_t* route_cnt;  // [1]
-    double* inv_freq;    // [hd/2] rotary inverse frequencies
+    float2* rope;        // [max_ctx][hd/2] (cos, sin) of pos * theta^(-2i/hd)
     int max_chunks;
     int max_pool_splits;
 };
 
+// Caller-owned HIP events recorded around one kernel of one block per step.
+struct TimingHook {
+    int kernel, layer, n, next;
+    hipEvent_t* start;
+    hipEvent_t* stop;
+};
+
+// Largest batch for which the automatic launch policy waits for the route
+// and launches only the blocks in use (at larger batches nearly every block
+// is used by some sequence).
+constexpr int kHostRoutedMaxBatch = 16;
+
 struct Model {
     buddy_config cfg;
+    TimingHook timing;
+    int policy;                   // buddy_launch_policy
+    int32_t* h_cnt;               // mapped pinned host memory: [L-2] counts, then a sequence number
+    int32_t* d_host_cnt;          // device address of h_cnt
+    int32_t seq;                  // sequence number of the last published route
     buddy_layer_weights* layers;  // host array of device pointers
     buddy_dm_weights dm;
     Workspace ws;
@@ -124,11 +136,13 @@ struct StepArgs {
 // --------------------------------------------------------------- launchers
 
 // Row set of one routed launch: rows i < *cnt map to sequences idx[i]; the
-// grid is sized for at most n_max rows.
+// grid is sized for at most n_max rows.  exact: the host knows that *cnt is
+// n_max (kernels then need not read the count before starting).
 struct Rows {
     const int32_t* idx;
     const int32_t* cnt;
     int n_max;
+    bool exact;
 };
 
 hipError_t launch_setup(const StepArgs& a, const Workspace& ws, hipStream_t s);
@@ -139,9 +153,12 @@ hipError_t launch_pool(const Model& M, const void* k0, const void* v0, const flo
 
 // Decision Module second layer + prior + top-k (or the override mask), then
 // zero-fill of skipped K/V rows and per-block compaction.
+// publish_seq >= 0: also publish the per-block counts and then publish_seq
+// to the mapped host buffer (host-routed launches wait for it).
 hipError_t launch_route(const Model& M, const void* kc, const void* vc, int B,
                         const uint8_t* route_override, uint8_t* mask_out,
-                        float* scores_out, bool scores_only, hipStream_t s);
+                        float* scores_out, bool scores_only, int32_t publish_seq,
+                        hipStream_t s);
 
 hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B, int n,
                               uint8_t* mask_out, hipStream_t s);
@@ -159,7 +176,7 @@ struct GemvArgs {
     int f;                             // EPI_SWIGLU: rows j and f + j
     // EPI_QKV: rotary + cache append of this block
     void* kc; void* vc; int T; int hd; int nq; int nkv; int bcap;
-    const int32_t* pos; const double* inv_freq;
+    const int32_t* pos; const float2* rope;
 };
 hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream_t s);
 
@@ -170,8 +187,11 @@ struct AttnArgs {
     const int32_t* pos;
     Rows rows;
     int chunks, chunk_len;
-    float* part; int32_t* counters; int max_chunks;
+    float* part; int max_chunks;
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
+// Cache rows one attention workgroup reads per block (chunk lengths are
+// multiples of it).
+int attention_rows_per_wg(int dtype, int hd);
 
 }  // namespace buddy

@@ -6,9 +6,11 @@
 // kernel is included, as in the KV-cache equation of the paper's background
 // appendix), keeps an online softmax (running max and sum, base 2) and the
 // weighted sum of V rows, then writes the chunk's (max, sum, acc) partial.
-// The workgroup that finishes last for (b, g) merges the chunk partials in
-// chunk order and writes o[b] for the group's heads.  Zero-filled rows of
-// skipped steps are ordinary cache rows here (logit 0, value 0).
+// A second kernel merges the chunk partials of (b, g) in chunk order and
+// writes o[b] for the group's heads (no cross-workgroup synchronisation
+// inside a kernel: device-wide fences are costly across the XCDs).
+// Zero-filled rows of skipped steps are ordinary cache rows here (logit 0,
+// value 0).
 //
 // Lane layout: a cache row of hd elements is read by hd/V lanes with 16-byte
 // loads (V = 8 bf16 or 4 fp32), so a wavefront covers 64/(hd/V) rows per
@@ -21,31 +23,56 @@ __device__ __forceinline__ float scale_of(float m, float mn) {
     return m == -INFINITY ? 0.f : exp2f(m - mn);
 }
 
+constexpr int kAttnPasses = 4;   // row passes of a workgroup, all loads issued up front
+
+// Rows of one workgroup: kAttnPasses passes of 4 wavefronts x (64 / (hd / V)) rows.
 template <typename T>
+__host__ __device__ constexpr int attn_rows_per_wg(int hd) {
+    return kAttnPasses * 4 * (kWave / (hd / St<T>::V));
+}
+
+template <typename T, int GM>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     constexpr int V = St<T>::V;
-    __shared__ float s_acc[4][kMaxGroup][256 + 2];
+    __shared__ float s_acc[4][GM][128 + 2];
     const int i = blockIdx.z;
-    const int n = *a.rows.cnt;
-    if (i >= n) return;
+    if (!a.rows.exact && i >= *a.rows.cnt) return;
     const int b = a.rows.idx[i];
     const int g = blockIdx.y, c = blockIdx.x;
     const int pos = a.pos[b];
     const int G = a.nq / a.nkv;
     const int lpr = a.hd / V;          // lanes per cache row
     const int rpw = kWave / lpr;       // rows per wavefront pass
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int col = lane % lpr, sub = lane / lpr;
     const int j0 = c * a.chunk_len;
     const int j1 = min(j0 + a.chunk_len, pos + 1);
 
+    const size_t base = ((size_t)b * a.nkv + g) * a.T * a.hd + col * V;
+    const T* Kb = (const T*)a.kc + base;
+    const T* Vb = (const T*)a.vc + base;
+    const int rows_wg = kAttnPasses * 4 * rpw;
+    uint4 kr[kAttnPasses], vr[kAttnPasses];
+    // every K/V row of a block is loaded before any arithmetic on it; rows
+    // past the end are clamped to a valid row and masked below
+    auto load_block = [&](int jb) {
+#pragma unroll
+        for (int p = 0; p < kAttnPasses; ++p) {
+            const int j = min(jb + (p * 4 + wave) * rpw + sub, max(j1 - 1, 0));
+            kr[p] = *reinterpret_cast<const uint4*>(Kb + (size_t)j * a.hd);
+            vr[p] = *reinterpret_cast<const uint4*>(Vb + (size_t)j * a.hd);
+        }
+    };
+    load_block(j0);
+
     // queries of the group, pre-scaled so that exp2 of the score is the
     // softmax weight: q * log2(e) / sqrt(hd)
     const float qs = 1.4426950408889634f / sqrtf((float)a.hd);
-    float qr[kMaxGroup][V];
+    float qr[GM][V];
     const float* qb = a.q + (size_t)b * a.nq * a.hd + (size_t)g * G * a.hd + col * V;
 #pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h) {
+    for (int h = 0; h < GM; ++h) {
 #pragma unroll
         for (int e = 0; e < V; ++e) qr[h][e] = 0.f;
         if (h < G) {
@@ -54,43 +81,47 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         }
     }
 
-    float m[kMaxGroup], l[kMaxGroup], acc[kMaxGroup][V];
+    float m[GM], l[GM], acc[GM][V];
 #pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h) {
+    for (int h = 0; h < GM; ++h) {
         m[h] = -INFINITY; l[h] = 0.f;
 #pragma unroll
         for (int e = 0; e < V; ++e) acc[h][e] = 0.f;
     }
-
-    const size_t base = ((size_t)b * a.nkv + g) * a.T * a.hd + col * V;
-    const T* Kb = (const T*)a.kc + base;
-    const T* Vb = (const T*)a.vc + base;
-    for (int j = j0 + wave * rpw + sub; j < j1; j += 4 * rpw) {
-        float kr[V], vr[V];
-        St<T>::vec(Kb + (size_t)j * a.hd, kr);
-        St<T>::vec(Vb + (size_t)j * a.hd, vr);
+    for (int jb = j0; jb < j1; jb += rows_wg) {
+    if (jb != j0) load_block(jb);
 #pragma unroll
-        for (int h = 0; h < kMaxGroup; ++h) {
+    for (int p = 0; p < kAttnPasses; ++p) {
+        const int j = jb + (p * 4 + wave) * rpw + sub;
+        const bool live = j < j1;
+        float kf[V], vf[V];
+        unpack<T>(kr[p], kf);
+        unpack<T>(vr[p], vf);
+#pragma unroll
+        for (int h = 0; h < GM; ++h) {
             if (h < G) {
                 float sc = 0.f;
 #pragma unroll
-                for (int e = 0; e < V; ++e) sc += qr[h][e] * kr[e];
+                for (int e = 0; e < V; ++e) sc += qr[h][e] * kf[e];
                 for (int o = lpr >> 1; o > 0; o >>= 1) sc += __shfl_xor(sc, o, kWave);
-                const float mn = fmaxf(m[h], sc);
-                const float al = scale_of(m[h], mn);
-                const float p = exp2f(sc - mn);
-                l[h] = l[h] * al + p;
+                if (live) {
+                    const float mn = fmaxf(m[h], sc);
+                    const float al = scale_of(m[h], mn);
+                    const float pw = exp2f(sc - mn);
+                    l[h] = l[h] * al + pw;
 #pragma unroll
-                for (int e = 0; e < V; ++e) acc[h][e] = acc[h][e] * al + p * vr[e];
-                m[h] = mn;
+                    for (int e = 0; e < V; ++e) acc[h][e] = acc[h][e] * al + pw * vf[e];
+                    m[h] = mn;
+                }
             }
         }
+    }
     }
 
     // merge the row slots of the wavefront (lanes with equal col)
     for (int o = lpr; o < kWave; o <<= 1) {
 #pragma unroll
-        for (int h = 0; h < kMaxGroup; ++h) {
+        for (int h = 0; h < GM; ++h) {
             if (h < G) {
                 const float mo = __shfl_xor(m[h], o, kWave);
                 const float lo = __shfl_xor(l[h], o, kWave);
@@ -108,7 +139,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     }
     if (sub == 0) {
 #pragma unroll
-        for (int h = 0; h < kMaxGroup; ++h) {
+        for (int h = 0; h < GM; ++h) {
             if (h < G) {
 #pragma unroll
                 for (int e = 0; e < V; ++e) s_acc[wave][h][col * V + e] = acc[h][e];
@@ -137,28 +168,63 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         pp[e] = A;
         if (e == 0) { pp[a.hd] = M; pp[a.hd + 1] = L; }
     }
+}
 
-    if (arrive_last(&a.counters[b * a.nkv + g], a.chunks)) {
-        for (int t = tid; t < G * a.hd; t += 256) {
-            const int h = t / a.hd, e = t % a.hd;
-            const float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks) * pstride;
-            float M = -INFINITY;
-            for (int q = 0; q < a.chunks; ++q) M = fmaxf(M, pp[q * pstride + a.hd]);
-            float L = 0.f, A = 0.f;
-            for (int q = 0; q < a.chunks; ++q) {
-                const float sw = scale_of(pp[q * pstride + a.hd], M);
-                L += pp[q * pstride + a.hd + 1] * sw;
-                A += pp[q * pstride + e] * sw;
-            }
-            a.o[(size_t)b * a.nq * a.hd + (size_t)(g * G + h) * a.hd + e] = A / L;
-        }
+// Merge of the chunk partials of one (routed sequence, query head): the
+// chunk maxima and sums go through LDS once, then every thread folds one
+// output element over the chunks in chunk order with coalesced reads.
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
+    __shared__ float s_w[kAttnMaxChunks];
+    __shared__ float s_red[4];
+    const int i = blockIdx.y;
+    if (!a.rows.exact && i >= *a.rows.cnt) return;
+    const int b = a.rows.idx[i];
+    const int head = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const size_t pstride = (size_t)a.hd + 2;
+    const float* pp = a.part + ((size_t)b * a.nq + head) * a.max_chunks * pstride;
+    const float mc = tid < a.chunks ? pp[tid * pstride + a.hd] : -INFINITY;
+    float M = mc;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, kWave));
+    if (lane == 0) s_red[wave] = M;
+    __syncthreads();
+    M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
+    const float wc = scale_of(mc, M);
+    if (tid < a.chunks) s_w[tid] = wc;
+    float L = tid < a.chunks ? pp[tid * pstride + a.hd + 1] * wc : 0.f;
+    L = wave_sum(L);
+    __syncthreads();                      // s_red reads above are done
+    if (lane == 0) s_red[wave] = L;
+    __syncthreads();
+    L = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
+    for (int e = tid; e < a.hd; e += 256) {
+        float A = 0.f;
+#pragma unroll 8
+        for (int q = 0; q < a.chunks; ++q) A += pp[q * pstride + e] * s_w[q];
+        a.o[(size_t)b * a.nq * a.hd + (size_t)head * a.hd + e] = A / L;
     }
+}
+
+int attention_rows_per_wg(int dtype, int hd) {
+    return dtype == BUDDY_BF16 ? attn_rows_per_wg<bf16_t>(hd) : attn_rows_per_wg<float>(hd);
 }
 
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     dim3 grid(a.chunks, a.nkv, a.rows.n_max);
-    if (dtype == BUDDY_BF16) attn_kernel<bf16_t><<<grid, 256, 0, s>>>(a);
-    else attn_kernel<float><<<grid, 256, 0, s>>>(a);
+    const int G = a.nq / a.nkv;   // query heads per KV head, held in registers
+    if (dtype == BUDDY_BF16) {
+        if (G == 1) attn_kernel<bf16_t, 1><<<grid, 256, 0, s>>>(a);
+        else if (G == 2) attn_kernel<bf16_t, 2><<<grid, 256, 0, s>>>(a);
+        else if (G <= 4) attn_kernel<bf16_t, 4><<<grid, 256, 0, s>>>(a);
+        else attn_kernel<bf16_t, 8><<<grid, 256, 0, s>>>(a);
+    } else {
+        if (G <= 2) attn_kernel<float, 2><<<grid, 256, 0, s>>>(a);
+        else attn_kernel<float, 8><<<grid, 256, 0, s>>>(a);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    attn_combine_kernel<<<dim3(a.nq, a.rows.n_max), 256, 0, s>>>(a);
     return hipGetLastError();
 }
 

@@ -2,10 +2,12 @@
 // layer (gfx950).
 //
 // Y[b] (op)= W x_b for the routed rows b = idx[i], i < cnt, with W [N][K]
-// row-major in the storage dtype and x_b fp32.  Each 64-lane wavefront owns a
-// "unit" of two weight rows and streams them once with 16-byte loads per lane
-// while the activation rows of the workgroup sit in LDS, so every weight byte
-// is read from HBM once per launch whatever the number of routed rows.
+// row-major in the storage dtype and x_b fp32.  Each 64-lane wavefront owns
+// one weight row (or a K-slice of it), issues all of its 16-byte loads at
+// once and keeps them in registers while the activation rows of the
+// workgroup pass through LDS, so every weight byte is read from HBM once per
+// launch whatever the number of routed rows.  Latency is hidden by the many
+// resident wavefronts rather than by software pipelining.
 //
 // Prologues:  PRO_NONE    x = X[b]
 //             PRO_RMSNORM x = X[b] / sqrt(mean(X[b]^2) + eps) * gain
@@ -15,6 +17,8 @@
 //             EPI_QKV      unit = rows (i, i + hd/2) of one head: rotary
 //                          embedding at pos[b] for q and k heads, q to Y,
 //                          k and v appended to the cache rounded to storage.
+#include <type_traits>
+
 #include "buddy_internal.h"
 
 namespace buddy {
@@ -36,6 +40,14 @@ __device__ __forceinline__ float act_fn(float x, int act) {
     return x / (1.0f + expf(-x));
 }
 
+// Epilogue of one finished row for the single-row kinds.
+template <typename TW, int EPI>
+__device__ __forceinline__ void epilogue1(const GemvArgs& g, int b, int row, float v) {
+    float* y = g.Y + (size_t)b * g.ldy;
+    if (EPI == EPI_ADD) y[row] += v;
+    else y[row] = act_fn(v + St<TW>::get((const TW*)g.bias, row), g.act);
+}
+
 template <typename TW, int EPI>
 __device__ __forceinline__ void epilogue(const GemvArgs& g, int b, int u, int r0, int r1,
                                          float v0, float v1) {
@@ -55,11 +67,9 @@ __device__ __forceinline__ void epilogue(const GemvArgs& g, int b, int u, int r0
         const int hg = u / half, i = u - hg * half;
         const int pos = g.pos[b];
         if (hg < g.nq + g.nkv) {
-            double sn, cs;
-            sincos((double)pos * g.inv_freq[i], &sn, &cs);
-            const float c = (float)cs, s = (float)sn;
-            const float a0 = v0 * c - v1 * s;
-            const float a1 = v1 * c + v0 * s;
+            const float2 cs = g.rope[(size_t)pos * half + i];
+            const float a0 = v0 * cs.x - v1 * cs.y;
+            const float a1 = v1 * cs.x + v0 * cs.y;
             v0 = a0; v1 = a1;
         }
         if (hg < g.nq) {
@@ -77,107 +87,268 @@ __device__ __forceinline__ void epilogue(const GemvArgs& g, int b, int u, int r0
     }
 }
 
-template <typename TW, int NR, int PRO, int EPI>
-__global__ __launch_bounds__(256) void gemv_kernel(GemvArgs g, int units) {
-    extern __shared__ float xs[];   // [NR][K] activation rows of the current group
-    __shared__ float s_red[4][NR];
-    __shared__ float s_inv[NR];
-    const int n = *g.rows.cnt;
-    if (n <= 0) return;
-    constexpr int V = St<TW>::V;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int K = g.K;
-    const TW* W = (const TW*)g.W;
+constexpr int kMaxLoads = 16;  // most 16-byte weight vectors in flight per lane
 
-    for (int i0 = 0; i0 < n; i0 += NR) {
+// Dot product of one packed 16-byte weight vector with the matching
+// activations x[0..V) (16-byte aligned in LDS).
+__device__ __forceinline__ float dot16(const uint4& w, const float* x, bf16_t) {
+    const float4 a = *reinterpret_cast<const float4*>(x);
+    const float4 b = *reinterpret_cast<const float4*>(x + 4);
+    float s = __uint_as_float(w.x << 16) * a.x;
+    s += __uint_as_float(w.x & 0xffff0000u) * a.y;
+    s += __uint_as_float(w.y << 16) * a.z;
+    s += __uint_as_float(w.y & 0xffff0000u) * a.w;
+    s += __uint_as_float(w.z << 16) * b.x;
+    s += __uint_as_float(w.z & 0xffff0000u) * b.y;
+    s += __uint_as_float(w.w << 16) * b.z;
+    s += __uint_as_float(w.w & 0xffff0000u) * b.w;
+    return s;
+}
+__device__ __forceinline__ float dot16(const uint4& w, const float* x, float) {
+    const float4 a = *reinterpret_cast<const float4*>(x);
+    float s = __uint_as_float(w.x) * a.x;
+    s += __uint_as_float(w.y) * a.y;
+    s += __uint_as_float(w.z) * a.z;
+    s += __uint_as_float(w.w) * a.w;
+    return s;
+}
+
+// Weight row of wavefront slot `slot` (0..P-1, P wavefronts per workgroup)
+// in workgroup `blk`, or -1.
+//   EPI_ADD, EPI_BIAS_ACT: P/S rows per workgroup, each split over S K-slices.
+//   EPI_SWIGLU, EPI_QKV: P/2 units per workgroup; slot s < P/2 holds the
+//   first row of unit s, slot P/2 + s its second row.
+template <int EPI, int S, int P>
+__device__ __forceinline__ int slot_row(const GemvArgs& g, int blk, int slot, int units) {
+    if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+        const int u = blk * (P / 2) + slot % (P / 2);
+        if (u >= units) return -1;
+        int r0, r1;
+        unit_rows<EPI>(g, u, r0, r1);
+        return slot < P / 2 ? r0 : r1;
+    }
+    const int row = blk * (P / S) + slot / S;
+    return row < g.N ? row : -1;
+}
+
+// GEMV with every weight load of a wavefront issued up front.  Wavefront w of
+// a workgroup of P wavefronts owns one weight row (slot w / S) and the
+// K-slice w % S of it: nsteps k-steps of 64 lanes x 16 bytes are split into S
+// slices of spw steps.  The weights stay in registers while the routed
+// activation rows pass through LDS NR at a time, so each weight byte is read
+// once per launch; wide workgroups share one staging of the activations.
+// When the host knows the routed row count (n_host >= 0) the weight loads
+// start before anything else; otherwise the device count is read first and
+// an empty launch returns without touching the weights.  PRO_RMSNORM stages
+// gain * x and applies 1/rms(x) to the finished sums.
+template <typename TW, int NR, int PRO, int EPI, int S, int ML, int P, bool TAIL, bool MULTI>
+__global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int nsteps, int spw,
+                                                    int n_host) {
+    extern __shared__ float xs[];   // [NR][K] staged activation rows
+    __shared__ float s_ss[P][NR];
+    __shared__ float s_part[P][NR];
+    constexpr int V = St<TW>::V;
+    constexpr int KS = kWave * V;   // elements per k-step
+    constexpr int NT = 64 * P;      // threads per workgroup
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wavefront
+    const int K = g.K;
+    const int slot = wave / S, slice = wave % S;
+    int n = n_host;
+    if (n < 0) {
+        n = *g.rows.cnt;
+        if (n <= 0) return;
+    }
+    const int row = slot_row<EPI, S, P>(g, blockIdx.x, wave, units);
+    const int st0 = slice * spw;
+    const int nl = row < 0 ? 0 : max(0, min(spw, nsteps - st0));
+
+    // all weight loads of this wavefront: one base address plus constant
+    // offsets; only a K that is not a whole number of k-steps (TAIL) needs
+    // clamped addresses for the partial last step
+    uint4 w[ML];
+    const TW* wr = (const TW*)g.W + (size_t)max(row, 0) * K + st0 * KS + lane * V;
+#pragma unroll
+    for (int q = 0; q < ML; ++q) {
+        if (q < nl) {
+            if (TAIL) {
+                const int k = min((st0 + q) * KS + lane * V, K - V) - st0 * KS - lane * V;
+                w[q] = *reinterpret_cast<const uint4*>(wr + k);
+            } else {
+                w[q] = *reinterpret_cast<const uint4*>(wr + q * KS);
+            }
+        }
+    }
+
+    // MULTI = false: the host guarantees n <= NR, and the single pass keeps
+    // the weight registers out of a loop (half the VGPRs, twice the waves)
+    const int groups = MULTI ? (n + NR - 1) / NR : 1;
+    for (int gi = 0; gi < groups; ++gi) {
+        const int i0 = gi * NR;
         const int nr = min(NR, n - i0);
-        __syncthreads();  // the previous group's readers are done with xs
+        if (MULTI) __syncthreads();  // the previous group is done with xs and s_part
+        const TW* gain = (const TW*)g.gain;
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
             float ss = 0.f;
             if (r < nr) {
                 const float* xr = g.X + (size_t)g.rows.idx[i0 + r] * g.ldx;
-                for (int k = tid * 4; k < K; k += 1024) {
-                    const float4 v = *reinterpret_cast<const float4*>(xr + k);
-                    *reinterpret_cast<float4*>(xs + r * K + k) = v;
-                    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+                for (int k = tid * V; k < K; k += NT * V) {
+                    float v[V];
+#pragma unroll
+                    for (int e = 0; e < V; e += 4) {
+                        const float4 t = *reinterpret_cast<const float4*>(xr + k + e);
+                        v[e] = t.x; v[e + 1] = t.y; v[e + 2] = t.z; v[e + 3] = t.w;
+                    }
+                    if (PRO == PRO_RMSNORM) {
+                        float gv[V];
+                        St<TW>::vec(gain + k, gv);
+#pragma unroll
+                        for (int e = 0; e < V; ++e) { ss += v[e] * v[e]; v[e] *= gv[e]; }
+                    }
+#pragma unroll
+                    for (int e = 0; e < V; e += 4)
+                        *reinterpret_cast<float4*>(xs + r * K + k + e) = make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
                 }
             } else {
-                for (int k = tid * 4; k < K; k += 1024)
+                for (int k = tid * 4; k < K; k += NT * 4)
                     *reinterpret_cast<float4*>(xs + r * K + k) = make_float4(0.f, 0.f, 0.f, 0.f);
             }
             if (PRO == PRO_RMSNORM) {
                 ss = wave_sum(ss);
-                if (lane == 0) s_red[wave][r] = ss;
+                if (lane == 0) s_ss[wave][r] = ss;
             }
-        }
-        if (PRO == PRO_RMSNORM) {
-            __syncthreads();
-            if (tid < NR) {
-                const float t = s_red[0][tid] + s_red[1][tid] + s_red[2][tid] + s_red[3][tid];
-                s_inv[tid] = 1.0f / sqrtf(t / (float)K + g.eps);
-            }
-            __syncthreads();
-            const TW* gain = (const TW*)g.gain;
-            for (int r = 0; r < nr; ++r)
-                for (int k = tid; k < K; k += 256) xs[r * K + k] *= s_inv[r] * St<TW>::get(gain, k);
         }
         __syncthreads();
 
-        for (int u = blockIdx.x * 4 + wave; u < units; u += gridDim.x * 4) {
-            int r0, r1;
-            unit_rows<EPI>(g, u, r0, r1);
-            const TW* w0 = W + (size_t)r0 * K;
-            const TW* w1 = W + (size_t)r1 * K;
-            float acc0[NR], acc1[NR];
+        float acc[NR];
 #pragma unroll
-            for (int r = 0; r < NR; ++r) acc0[r] = acc1[r] = 0.f;
-#pragma unroll 4
-            for (int k = lane * V; k < K; k += kWave * V) {
-                float a[V], c[V];
-                St<TW>::vec(w0 + k, a);
-                St<TW>::vec(w1 + k, c);
+        for (int r = 0; r < NR; ++r) acc[r] = 0.f;
+        const float* xw = xs + st0 * KS + lane * V;
 #pragma unroll
-                for (int r = 0; r < NR; ++r) {
-                    const float* x = xs + r * K + k;
+        for (int q = 0; q < ML; ++q) {
+            if (q < nl && (!TAIL || (st0 + q) * KS + lane * V < K)) {
 #pragma unroll
-                    for (int e = 0; e < V; ++e) {
-                        acc0[r] += a[e] * x[e];
-                        acc1[r] += c[e] * x[e];
-                    }
+                for (int r = 0; r < NR; ++r) acc[r] += dot16(w[q], xw + r * K + q * KS, TW());
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const float v = wave_sum(acc[r]);
+            if (lane == 0) s_part[wave][r] = v;
+        }
+        __syncthreads();
+
+        float inv[NR];
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            inv[r] = 1.f;
+            if (PRO == PRO_RMSNORM) {
+                float t = 0.f;
+                for (int q = 0; q < P; ++q) t += s_ss[q][r];
+                inv[r] = 1.0f / sqrtf(t / (float)K + g.eps);
+            }
+        }
+        // epilogues: one (unit or row, routed row) pair per thread
+        if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+            constexpr int UPB = P / 2;
+            if (tid < UPB * nr) {
+                const int uu = tid / nr, r = tid - uu * nr;
+                const int u = blockIdx.x * UPB + uu;
+                if (u < units) {
+                    float sc = 1.f;
+#pragma unroll
+                    for (int q = 0; q < NR; ++q) if (q == r) sc = inv[q];
+                    int r0, r1;
+                    unit_rows<EPI>(g, u, r0, r1);
+                    epilogue<TW, EPI>(g, g.rows.idx[i0 + r], u, r0, r1, s_part[uu][r] * sc,
+                                      s_part[UPB + uu][r] * sc);
                 }
             }
+        } else {
+            constexpr int RPB = P / S;
+            if (tid < RPB * nr) {
+                const int sl = tid / nr, r = tid - sl * nr;
+                const int rw = blockIdx.x * RPB + sl;
+                if (rw < g.N) {
+                    float v = 0.f, sc = 1.f;
 #pragma unroll
-            for (int r = 0; r < NR; ++r) {
-                acc0[r] = wave_sum(acc0[r]);
-                acc1[r] = wave_sum(acc1[r]);
-            }
-            if (lane < nr) {
-                // lane r finishes routed row r of the group
+                    for (int q = 0; q < S; ++q) v += s_part[sl * S + q][r];
 #pragma unroll
-                for (int r = 0; r < NR; ++r)
-                    if (r == lane) epilogue<TW, EPI>(g, g.rows.idx[i0 + r], u, r0, r1, acc0[r], acc1[r]);
+                    for (int q = 0; q < NR; ++q) if (q == r) sc = inv[q];
+                    epilogue1<TW, EPI>(g, g.rows.idx[i0 + r], rw, v * sc);
+                }
             }
         }
     }
 }
 
-template <typename TW, int NR, int PRO, int EPI>
-static hipError_t launch_one(const GemvArgs& g, int units, hipStream_t s) {
+template <typename TW, int NR, int PRO, int EPI, int S, int ML, int P, bool TAIL, bool MULTI>
+static hipError_t launch_one(const GemvArgs& g, int units, int n_host, hipStream_t s) {
     const size_t lds = (size_t)NR * g.K * sizeof(float);
     static bool attr_set = false;
     if (lds > 64 * 1024 && !attr_set) {
         // dynamic LDS above the 64 KB default; the dispatcher never asks
         // for more than kGemvLds
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_kernel<TW, NR, PRO, EPI>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, kGemvLds);
+        hipError_t e = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, kGemvLds);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    int grid = (units + 3) / 4;
-    if (grid > 2048) grid = 2048;
-    gemv_kernel<TW, NR, PRO, EPI><<<grid, 256, lds, s>>>(g, units);
+    constexpr int KS = kWave * St<TW>::V;
+    const int nsteps = (g.K + KS - 1) / KS;
+    const int spw = (nsteps + S - 1) / S;
+    const int per_wg = (EPI == EPI_SWIGLU || EPI == EPI_QKV) ? P / 2 : P / S;
+    const int items = (EPI == EPI_SWIGLU || EPI == EPI_QKV) ? units : g.N;
+    const int grid = (items + per_wg - 1) / per_wg;
+    gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI><<<grid, 64 * P, lds, s>>>(
+        g, units, nsteps, spw, n_host);
     return hipGetLastError();
+}
+
+// K-slices per weight row and loads per lane: 8 loads per lane where the row
+// (or a half or quarter of it) allows, else 16.  Two-row units keep S = 1
+// (their K is d_model).  Eight wavefronts per workgroup share one staging of
+// the activations.
+// Shape classes (k-steps of 64 lanes x 16 bytes per weight row):
+//   <= 8 steps: one wavefront per row, 8 loads per lane, 8 wavefronts per
+//   workgroup; two-row units with <= 16 steps: 16 loads per lane; single rows
+//   with <= 32 (<= 64) steps: quarter rows of <= 8 (16) loads per lane, 16
+//   wavefronts per workgroup so four rows share one activation staging.
+template <typename TW, int NR, int PRO, int EPI, bool TAIL, bool MULTI>
+static hipError_t dispatch_s(const GemvArgs& g, int units, int n_host, hipStream_t s) {
+    constexpr int KS = kWave * St<TW>::V;
+    const int nsteps = (g.K + KS - 1) / KS;
+    if (nsteps <= 8) return launch_one<TW, NR, PRO, EPI, 1, 8, 8, TAIL, MULTI>(g, units, n_host, s);
+    if constexpr (std::is_same<TW, float>::value) {
+        return hipErrorInvalidValue;   // fp32 rows are at most 8 k-steps (checked at create)
+    } else {
+        if (EPI == EPI_SWIGLU || EPI == EPI_QKV)
+            return launch_one<TW, NR, PRO, EPI, 1, 16, 8, TAIL, MULTI>(g, units, n_host, s);
+        if (nsteps <= 32) return launch_one<TW, NR, PRO, EPI, 4, 8, 16, TAIL, MULTI>(g, units, n_host, s);
+        return launch_one<TW, NR, PRO, EPI, 4, 16, 16, TAIL, MULTI>(g, units, n_host, s);
+    }
+}
+
+// A K that is not a whole number of k-steps (TAIL) only occurs for small
+// models; MULTI passes are built for one or four staged rows.
+template <typename TW, int NR, int PRO, int EPI>
+static hipError_t dispatch_tail(const GemvArgs& g, int units, int n_host, hipStream_t s) {
+    constexpr int KS = kWave * St<TW>::V;
+    constexpr bool kMultiOk = NR != 2;
+    const bool multi = g.rows.n_max > NR;
+    if constexpr (!kMultiOk) {
+        if (multi) return dispatch_tail<TW, 1, PRO, EPI>(g, units, n_host, s);
+    }
+    if (g.K % KS) {
+        // partial last k-step: only rows of at most 8 k-steps (checked at create)
+        if (g.K > 8 * KS) return hipErrorInvalidValue;
+        if (multi) return launch_one<TW, NR, PRO, EPI, 1, 8, 8, true, kMultiOk>(g, units, n_host, s);
+        return launch_one<TW, NR, PRO, EPI, 1, 8, 8, true, false>(g, units, n_host, s);
+    }
+    if (multi) return dispatch_s<TW, NR, PRO, EPI, false, kMultiOk>(g, units, n_host, s);
+    return dispatch_s<TW, NR, PRO, EPI, false, false>(g, units, n_host, s);
 }
 
 template <typename TW, int PRO, int EPI>
@@ -185,10 +356,11 @@ static hipError_t dispatch_nr(const GemvArgs& g, int units, hipStream_t s) {
     // rows staged per pass: as many as fit in kGemvLds, at most 4
     const size_t row_bytes = (size_t)g.K * sizeof(float);
     const int fit = (int)(kGemvLds / row_bytes);
-    int nr = g.rows.n_max < fit ? g.rows.n_max : fit;
-    if (nr >= 4) return launch_one<TW, 4, PRO, EPI>(g, units, s);
-    if (nr >= 2) return launch_one<TW, 2, PRO, EPI>(g, units, s);
-    return launch_one<TW, 1, PRO, EPI>(g, units, s);
+    const int nr = g.rows.n_max < fit ? g.rows.n_max : fit;
+    const int n_host = g.rows.exact ? g.rows.n_max : -1;
+    if (nr >= 4) return dispatch_tail<TW, 4, PRO, EPI>(g, units, n_host, s);
+    if (nr >= 2) return dispatch_tail<TW, 2, PRO, EPI>(g, units, n_host, s);
+    return dispatch_tail<TW, 1, PRO, EPI>(g, units, n_host, s);
 }
 
 template <typename TW>
@@ -198,9 +370,9 @@ static hipError_t dispatch_epi(int pro, int epi, const GemvArgs& g, hipStream_t 
         return dispatch_nr<TW, PRO_RMSNORM, EPI_QKV>(g, units, s);
     }
     if (epi == EPI_SWIGLU) return dispatch_nr<TW, PRO_RMSNORM, EPI_SWIGLU>(g, g.f, s);
-    if (epi == EPI_BIAS_ACT) return dispatch_nr<TW, PRO_NONE, EPI_BIAS_ACT>(g, g.N / 2, s);
-    if (pro == PRO_RMSNORM) return dispatch_nr<TW, PRO_RMSNORM, EPI_ADD>(g, g.N / 2, s);
-    return dispatch_nr<TW, PRO_NONE, EPI_ADD>(g, g.N / 2, s);
+    if (epi == EPI_BIAS_ACT) return dispatch_nr<TW, PRO_NONE, EPI_BIAS_ACT>(g, g.N, s);
+    if (pro == PRO_RMSNORM) return dispatch_nr<TW, PRO_RMSNORM, EPI_ADD>(g, g.N, s);
+    return dispatch_nr<TW, PRO_NONE, EPI_ADD>(g, g.N, s);
 }
 
 hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream_t s) {

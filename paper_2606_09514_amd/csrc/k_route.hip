@@ -2,17 +2,18 @@
 //
 //  setup_kernel   publishes the step's positions and budgets to device memory
 //                 and the identity row list used by the always-run blocks.
-//  pool_kernel    KV-aware planner (Sec. 4.3): mean of the first layer's K
-//                 and V rows 0..pos per KV head, joined with the newest hidden
-//                 state: z = [mean K | mean V | h].  Positions are split over
-//                 workgroups; the last workgroup of each (sequence, head)
-//                 folds the split partials (no atomics on data).
+//  pool_kernel    KV-aware planner (Sec. 4.3): sums of the first layer's K
+//                 and V rows 0..pos per KV head over split position ranges;
+//  pool_finish_kernel  folds the split sums in order into the means and
+//                 joins the newest hidden state: z = [mean K | mean V | h].
 //  route_kernel   Decision Module output layer plus prior fusion (Eq. 2),
-//                 deterministic top-k by rank counting, zero-fill of the K/V
-//                 row of every skipped block (Sec. 6), and -- in the last
-//                 workgroup -- grouping by mask (App. C.1): for every routable
-//                 block the ascending list of sequences that run it.
+//                 deterministic top-k by rank counting, and zero-fill of the
+//                 K/V row of every skipped block (Sec. 6).
+//  compact_kernel grouping by mask (App. C.1): for every routable block the
+//                 ascending list of sequences that run it and their count.
 //  topk_kernel    the standalone top-k entry point.
+// Partial results always travel through a kernel boundary; no kernel here
+// synchronises workgroups (device-wide fences are costly across the XCDs).
 #include "buddy_internal.h"
 
 namespace buddy {
@@ -41,7 +42,7 @@ struct PoolParams {
     const float* h; int d;           // newest hidden [B][d]
     const int32_t* pos;
     float* z; int din;
-    float* part; int32_t* counters;
+    float* part;
     int T, hd, nkv, splits, max_splits;
 };
 
@@ -84,20 +85,23 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolParams p) {
         for (int r = 0; r < rpp; ++r) acc += red[which][r * p.hd + e];
         part[(size_t)s * 2 * p.hd + t] = acc;
     }
+}
+
+__global__ __launch_bounds__(256) void pool_finish_kernel(PoolParams p) {
+    const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const float inv_n = 1.0f / (float)(p.pos[b] + 1);
+    const float* part = p.part + (((size_t)b * p.nkv + g) * p.max_splits) * 2 * p.hd;
+    for (int t = tid; t < 2 * p.hd; t += 256) {
+        float acc = 0.f;
+#pragma unroll 8
+        for (int q = 0; q < p.splits; ++q) acc += part[(size_t)q * 2 * p.hd + t];
+        const int which = t / p.hd, e = t % p.hd;
+        p.z[(size_t)b * p.din + which * p.nkv * p.hd + g * p.hd + e] = acc * inv_n;
+    }
     // the newest hidden state is the last part of z
-    if (s == 0 && g == 0)
+    if (g == 0)
         for (int t = tid; t < p.d; t += 256)
             p.z[(size_t)b * p.din + 2 * p.nkv * p.hd + t] = p.h[(size_t)b * p.d + t];
-
-    if (arrive_last(&p.counters[b * p.nkv + g], p.splits)) {
-        const float inv_n = 1.0f / (float)n;
-        for (int t = tid; t < 2 * p.hd; t += 256) {
-            float acc = 0.f;
-            for (int q = 0; q < p.splits; ++q) acc += part[(size_t)q * 2 * p.hd + t];
-            const int which = t / p.hd, e = t % p.hd;
-            p.z[(size_t)b * p.din + which * p.nkv * p.hd + g * p.hd + e] = acc * inv_n;
-        }
-    }
 }
 
 hipError_t launch_pool(const Model& M, const void* k0, const void* v0, const float* h,
@@ -106,7 +110,7 @@ hipError_t launch_pool(const Model& M, const void* k0, const void* v0, const flo
     PoolParams p;
     p.k0 = k0; p.v0 = v0; p.h = h; p.d = c.d_model;
     p.pos = M.ws.pos; p.z = M.ws.z; p.din = 2 * c.n_kv_heads * c.head_dim + c.d_model;
-    p.part = M.ws.pool_part; p.counters = M.ws.pool_cnt;
+    p.part = M.ws.pool_part;
     p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.max_splits = M.ws.max_pool_splits;
     // enough workgroups to stream the first-layer cache with the whole chip,
     // at least 64 rows per workgroup
@@ -119,6 +123,9 @@ hipError_t launch_pool(const Model& M, const void* k0, const void* v0, const flo
     dim3 grid(splits, c.n_kv_heads, B);
     if (c.dtype == BUDDY_BF16) pool_kernel<bf16_t><<<grid, 256, 0, s>>>(p);
     else pool_kernel<float><<<grid, 256, 0, s>>>(p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    pool_finish_kernel<<<dim3(c.n_kv_heads, B), 256, 0, s>>>(p);
     return hipGetLastError();
 }
 
@@ -143,7 +150,6 @@ struct RouteParams {
     float* scores; float* scores_out;
     void* kc; void* vc;               // cache bases (layer 0)
     int T, hd, nkv, bcap;
-    int32_t* idx; int32_t* cnt; int32_t* counter;
     int scores_only;
 };
 
@@ -157,11 +163,19 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
     if (p.route_override) {
         if (tid < Lm) s_mask[tid] = p.route_override[(size_t)b * Lm + tid] != 0;
     } else {
+        constexpr int V = St<T>::V;
         const T* w2 = (const T*)p.w2;
         const float* a = p.a + (size_t)b * p.H;
+        const int nv = p.H / V;        // 16-byte vectors per output-layer row
+#pragma unroll 4
         for (int i = wave; i < Lm; i += 4) {
             float acc = 0.f;
-            for (int h = lane; h < p.H; h += kWave) acc += St<T>::get(w2, (size_t)i * p.H + h) * a[h];
+            for (int v = lane; v < nv; v += kWave) {
+                float wv[V];
+                St<T>::vec(w2 + (size_t)i * p.H + v * V, wv);
+#pragma unroll
+                for (int e = 0; e < V; ++e) acc += wv[e] * a[v * V + e];
+            }
             acc = wave_sum(acc);
             if (lane == 0) {
                 float v = acc + St<T>::get((const T*)p.b2, i);
@@ -188,40 +202,60 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
         if (p.mask_out) p.mask_out[(size_t)b * Lm + tid] = s_mask[tid];
     }
 
-    // zero-filled K/V row at this step's position for every skipped block
+    // zero-filled K/V row at this step's position for every skipped block,
+    // written as 16-byte vectors
+    constexpr int VZ = St<T>::V;
     const int pos = p.pos[b];
     const size_t layer_stride = (size_t)p.bcap * p.nkv * p.T * p.hd;
-    const int per_layer = p.nkv * p.hd;
+    const int per_layer = p.nkv * (p.hd / VZ);
     for (int t = tid; t < Lm * per_layer; t += 256) {
         const int i = t / per_layer, r = t % per_layer;
         if (s_mask[i]) continue;
-        const int g = r / p.hd, e = r % p.hd;
+        const int g = r / (p.hd / VZ), e = (r % (p.hd / VZ)) * VZ;
         const size_t at = (size_t)(i + 1) * layer_stride +
                           (((size_t)b * p.nkv + g) * p.T + pos) * p.hd + e;
-        ((T*)p.kc)[at] = (T)0;
-        ((T*)p.vc)[at] = (T)0;
+        *reinterpret_cast<uint4*>((T*)p.kc + at) = make_uint4(0u, 0u, 0u, 0u);
+        *reinterpret_cast<uint4*>((T*)p.vc + at) = make_uint4(0u, 0u, 0u, 0u);
     }
 
-    // grouping by mask, done once every sequence's mask is written
-    if (arrive_last(p.counter, gridDim.x)) {
-        for (int i = wave; i < Lm; i += 4) {
-            int base = 0;
-            for (int b0 = 0; b0 < p.B; b0 += kWave) {
-                const int bb = b0 + lane;
-                const bool sel = bb < p.B && p.mask[(size_t)bb * Lm + i];
-                const uint64_t bal = __ballot(sel);
-                const int before = __popcll(bal & ((1ull << lane) - 1ull));
-                if (sel) p.idx[(size_t)i * p.bcap + base + before] = bb;
-                base += __popcll(bal);
-            }
-            if (lane == 0) p.cnt[i] = base;
+}
+
+// One workgroup: each wavefront scans the mask columns of every fourth
+// routable block over the batch.  When host_cnt (mapped pinned host memory)
+// is given, the counts are also published there, followed by the step's
+// sequence number once they are visible to the host.
+__global__ __launch_bounds__(256) void compact_kernel(const uint8_t* mask, int Lm, int B, int bcap,
+                                                      int32_t* idx, int32_t* cnt,
+                                                      volatile int32_t* host_cnt, int32_t seq) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int i = wave; i < Lm; i += 4) {
+        int base = 0;
+        for (int b0 = 0; b0 < B; b0 += kWave) {
+            const int bb = b0 + lane;
+            const bool sel = bb < B && mask[(size_t)bb * Lm + i];
+            const uint64_t bal = __ballot(sel);
+            const int before = __popcll(bal & ((1ull << lane) - 1ull));
+            if (sel) idx[(size_t)i * bcap + base + before] = bb;
+            base += __popcll(bal);
+        }
+        if (lane == 0) {
+            cnt[i] = base;
+            if (host_cnt) host_cnt[i] = base;
+        }
+    }
+    if (host_cnt) {
+        __syncthreads();
+        if (tid == 0) {
+            __threadfence_system();
+            host_cnt[Lm] = seq;
         }
     }
 }
 
 hipError_t launch_route(const Model& M, const void* kc, const void* vc, int B,
                         const uint8_t* route_override, uint8_t* mask_out,
-                        float* scores_out, bool scores_only, hipStream_t s) {
+                        float* scores_out, bool scores_only, int32_t publish_seq,
+                        hipStream_t s) {
     const buddy_config& c = M.cfg;
     RouteParams p;
     p.a = M.ws.a; p.H = c.dm_hidden;
@@ -233,10 +267,13 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, int B,
     p.scores = M.ws.scores; p.scores_out = scores_out;
     p.kc = (void*)kc; p.vc = (void*)vc;
     p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.bcap = c.max_batch;
-    p.idx = M.ws.idx; p.cnt = M.ws.cnt; p.counter = M.ws.route_cnt;
     p.scores_only = scores_only ? 1 : 0;
     if (c.dtype == BUDDY_BF16) route_kernel<bf16_t><<<B, 256, 0, s>>>(p);
     else route_kernel<float><<<B, 256, 0, s>>>(p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || scores_only || p.Lm == 0) return e;
+    compact_kernel<<<1, 256, 0, s>>>(M.ws.mask, p.Lm, B, c.max_batch, M.ws.idx, M.ws.cnt,
+                                     publish_seq >= 0 ? M.d_host_cnt : nullptr, publish_seq);
     return hipGetLastError();
 }
 

@@ -18,6 +18,8 @@ OK, EINVAL, ESHAPE, ECAPACITY, ENOMEM, EDEVICE, EUNSUPPORTED = range(7)
 F32, BF16 = 0, 1
 ACT_SILU, ACT_GELU_ERF = 0, 1
 SKIP_KV_ZERO, SKIP_KV_MASK = 0, 1
+LAUNCH_AUTO, LAUNCH_DEVICE_ROUTED, LAUNCH_HOST_ROUTED = 0, 1, 2
+KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN = range(5)
 
 
 class Config(C.Structure):
@@ -70,6 +72,10 @@ def lib():
         L.buddy_select_topk.restype = C.c_int
         L.buddy_decode_step.argtypes = [vp, P(KV), vp, vp, vp, i32, i32, vp, vp, vp, vp]
         L.buddy_decode_step.restype = C.c_int
+        L.buddy_set_launch_policy.argtypes = [vp, i32]
+        L.buddy_set_launch_policy.restype = C.c_int
+        L.buddy_set_timing_events.argtypes = [vp, i32, i32, vp, vp, i32]
+        L.buddy_set_timing_events.restype = C.c_int
         L.buddy_budget_to_k.argtypes = [C.c_float, i32]
         L.buddy_budget_to_k.restype = i32
         L.buddy_status_string.argtypes = [C.c_int]
@@ -187,6 +193,17 @@ class Model:
         if check:
             _raise(rc, self._h)
         return rc
+
+    def set_launch_policy(self, policy: int) -> None:
+        _raise(lib().buddy_set_launch_policy(self._h, int(policy)), self._h)
+
+    def set_timing_events(self, kernel: int, layer: int, starts, stops) -> None:
+        """starts/stops: sequences of raw hipEvent_t handles (ints)."""
+        n = len(starts)
+        a = (C.c_void_p * max(n, 1))(*starts)
+        b = (C.c_void_p * max(n, 1))(*stops)
+        _raise(lib().buddy_set_timing_events(self._h, int(kernel), int(layer),
+                                             a if n else None, b if n else None, n), self._h)
 
     def pool_route(self, k_cache, v_cache, pos, h_new, scores_out, stream=None,
                    check: bool = True) -> int:

@@ -29,7 +29,8 @@ def to_device(W):
 class Pair:
     """The same model for the GPU library and the oracle."""
 
-    def __init__(self, shape, dtype, max_ctx, batch, seed=0, omega=0.0, device_gen=False):
+    def __init__(self, shape, dtype, max_ctx, batch, seed=0, omega=0.0, device_gen=False,
+                 policy=blib.LAUNCH_AUTO):
         self.cfg = synth.model_config(shape, dtype, max_ctx)
         self.batch = batch
         if device_gen:
@@ -39,6 +40,7 @@ class Pair:
         layers, dm = host_weights(self.Wd)
         self.orc = Oracle(self.cfg, layers, dm)
         self.gpu = blib.Model(self.cfg, self.Wd, max_batch=batch)
+        self.gpu.set_launch_policy(policy)
         self.sdt = np.uint16 if dtype == "bf16" else np.float32
         self.tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
         L, nkv, hd = self.cfg["n_layers"], self.cfg["n_kv_heads"], self.cfg["head_dim"]

@@ -87,12 +87,16 @@ def run_teacher_forced(P, prompt, n_decode, ks, report):
     return masks
 
 
+POLICIES = [("host", blib.LAUNCH_HOST_ROUTED), ("device", blib.LAUNCH_DEVICE_ROUTED)]
+
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_tiny_workload_teacher_forced(dtype):
+def test_tiny_workload_teacher_forced(dtype, policy):
     """The tiny decoder workload: 8 layers, d 256, 4/2 heads, batch 4,
     64 prompt tokens then 16 fed-back decode steps, k = 3 of 6."""
     w = synth.WORKLOADS["tiny_b4_prompt64"]
-    P = Pair(w.shape, dtype, w.max_ctx, w.batch, seed=0, omega=w.omega)
+    P = Pair(w.shape, dtype, w.max_ctx, w.batch, seed=0, omega=w.omega, policy=policy)
     prompt = synth.hidden_inputs(w.batch * w.ctx, P.cfg["d_model"], seed=1).numpy() \
         .reshape(w.batch, w.ctx, -1)
     rep = new_report()
@@ -102,8 +106,9 @@ def test_tiny_workload_teacher_forced(dtype):
     assert len({m.tobytes() for m in masks}) > 1
 
 
-def test_prior_fusion_and_mixed_budgets():
-    P = Pair("tiny", "bf16", 24, 6, seed=7, omega=0.1)
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+def test_prior_fusion_and_mixed_budgets(policy):
+    P = Pair("tiny", "bf16", 24, 6, seed=7, omega=0.1, policy=policy)
     prompt = synth.hidden_inputs(6 * 8, P.cfg["d_model"], seed=8).numpy().reshape(6, 8, -1)
     rep = new_report()
     run_teacher_forced(P, prompt, 4, [0, 1, 2, 3, 5, 6], rep)
@@ -163,8 +168,9 @@ def test_route_override_matches_oracle_fixed_route():
 
 # ----------------------------------------- determinism and batch invariance
 
-def test_batch_permutation_and_determinism():
-    P = Pair("tiny", "bf16", 40, 6, seed=13, omega=0.1)
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+def test_batch_permutation_and_determinism(policy):
+    P = Pair("tiny", "bf16", 40, 6, seed=13, omega=0.1, policy=policy)
     g = torch.Generator().manual_seed(14)
     hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
     hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
@@ -253,3 +259,20 @@ def test_llama3_8b_b1_ctx2048_sampled(k):
         out, mg = compare_step(P, hk, hv, dk, dv, x, [w.ctx + t], [k], rep)
         x = out.astype(np.float32)
     print(rep)
+
+
+def test_launch_policies_agree_bitwise():
+    """Host-routed and device-routed launches run the same kernels on the
+    same rows: identical outputs and caches."""
+    outs = []
+    for _, policy in POLICIES:
+        P = Pair("tiny", "bf16", 40, 5, seed=17, omega=0.1, policy=policy)
+        g = torch.Generator().manual_seed(18)
+        hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        dk, dv = P.upload(hk), P.upload(hv)
+        x = synth.hidden_inputs(5, P.cfg["d_model"], seed=19).numpy()
+        h, m, s = gpu_step(P, dk, dv, x, [30, 12, 39, 0, 25], [1, 0, 6, 3, 2])
+        outs.append((h.tobytes(), m.tobytes(), s.tobytes(), P.download(dk).tobytes(),
+                     P.download(dv).tobytes()))
+    assert outs[0] == outs[1]
