@@ -31,6 +31,28 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0   # MI355X HBM3E peak
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic_llama3_8b_b1_ctx2048.md")
+KERNEL_SOURCES = ["paper_2606_09514_amd/csrc/k_gemv.hip", "paper_2606_09514_amd/csrc/buddy_internal.h"]
+
+
+def measured_traffic():
+    """Bytes per launch of the gate/up GEMV from the committed rocprofv3 PMC
+    record, or None when the record is missing or the kernel sources changed
+    since the counters were taken."""
+    import hashlib
+    import re
+    try:
+        text = open(TRAFFIC_RECORD).read()
+    except OSError:
+        return None
+    m = re.search(r"gate_up_traffic_bytes=(\d+) kernel_sources_sha256=([0-9a-f]{64})", text)
+    if not m:
+        return None
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return int(m.group(1)) if h.hexdigest() == m.group(2) else None
 
 
 def log(*a):
@@ -237,7 +259,8 @@ def main():
                            "gate_up_us": round(r["kernel_ms"] * 1e3, 2)}
                        for n, r in runs.items()},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": measured_traffic() if w.name == "llama3_8b_b1_ctx2048" else None,
                      "kernel": "gemv gate_up+SwiGLU (block 0)",
                      "bytes_per_launch": gate_up_bytes,
                      "launch_us": round(head["kernel_ms"] * 1e3, 2)},

@@ -110,7 +110,7 @@ hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
 }
 
 buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows rows,
-                       int max_pos, hipStream_t s) {
+                       int max_pos, int pos_u, hipStream_t s) {
     const buddy_config& c = M.cfg;
     const buddy_layer_weights& w = M.layers[l];
     const int qdim = c.n_heads * c.head_dim;
@@ -121,7 +121,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     g.rows = rows;
     g.eps = c.rms_eps;
     g.T = c.max_ctx; g.hd = c.head_dim; g.nq = c.n_heads; g.nkv = c.n_kv_heads;
-    g.bcap = c.max_batch; g.pos = M.ws.pos; g.rope = M.ws.rope;
+    g.bcap = c.max_batch; g.pos = M.ws.pos; g.pos_u = pos_u; g.rope = M.ws.rope;
     g.kc = (void*)layer_base(M, kv->k, l);
     g.vc = (void*)layer_base(M, kv->v, l);
 
@@ -138,7 +138,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     AttnArgs a;
     a.q = M.ws.q; a.o = M.ws.o; a.kc = g.kc; a.vc = g.vc;
     a.T = c.max_ctx; a.hd = c.head_dim; a.nq = c.n_heads; a.nkv = c.n_kv_heads;
-    a.bcap = c.max_batch; a.pos = M.ws.pos; a.rows = rows;
+    a.bcap = c.max_batch; a.pos = M.ws.pos; a.pos_u = pos_u; a.rows = rows;
     attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
     a.part = M.ws.part; a.max_chunks = M.ws.max_chunks;
     if ((e = mark(M, BUDDY_KERNEL_ATTENTION, l, false, s)) != hipSuccess ||
@@ -172,22 +172,47 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     return BUDDY_OK;
 }
 
-// Router context and the Decision Module's hidden layer for every sequence.
+// Router context and the Decision Module's hidden layer for every sequence:
+// split sums of the first-layer cache, then the first Decision Module GEMV,
+// which folds them into z = [mean K | mean V | h] while staging its input.
 buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, int max_pos,
-                         hipStream_t s) {
+                         int pos_u, hipStream_t s) {
     const buddy_config& c = M.cfg;
     hipError_t e;
-    if ((e = launch_pool(M, kv->k, kv->v, h, B, max_pos, s)) != hipSuccess)
+    int splits = 1;
+    if ((e = launch_pool(M, kv->k, kv->v, B, max_pos, pos_u, &splits, s)) != hipSuccess)
         return fail_device(M, e, "pool");
     GemvArgs g;
     memset(&g, 0, sizeof(g));
     g.W = M.dm.w1; g.N = c.dm_hidden; g.K = 2 * c.n_kv_heads * c.head_dim + c.d_model;
-    g.X = M.ws.z; g.ldx = g.K;
-    g.rows = Rows{M.ws.idx_all, M.ws.n_all, B, true};
+    g.rows = Rows{M.ws.idx_all, M.ws.n_all, B, true, true};
     g.Y = M.ws.a; g.ldy = c.dm_hidden;
     g.bias = M.dm.b1; g.act = c.dm_act;
-    if ((e = launch_gemv(c.dtype, PRO_NONE, EPI_BIAS_ACT, g, s)) != hipSuccess)
+    g.hd = c.head_dim; g.nkv = c.n_kv_heads; g.pos = M.ws.pos; g.pos_u = pos_u;
+    g.pool_part = M.ws.pool_part; g.pool_splits = splits;
+    g.pool_max_splits = M.ws.max_pool_splits; g.h = h; g.d = c.d_model;
+    if ((e = launch_gemv(c.dtype, PRO_POOL, EPI_BIAS_ACT, g, s)) != hipSuccess)
         return fail_device(M, e, "dm_hidden");
+    return BUDDY_OK;
+}
+
+// Per-step host values for the device: positions and budgets (kernel
+// arguments), the shared position when all sequences have it, and -- only
+// when they differ -- the device position array written by setup_kernel.
+buddy_status prepare_step(Model& M, const int32_t* pos, const int32_t* k, int B, StepArgs* a,
+                          int* pos_u, hipStream_t s) {
+    memset(a, 0, sizeof(*a));
+    a->B = B;
+    *pos_u = pos[0];
+    for (int b = 0; b < B; ++b) {
+        a->pos[b] = pos[b];
+        a->k[b] = k ? (uint8_t)k[b] : 0;
+        if (pos[b] != pos[0]) *pos_u = -1;
+    }
+    if (*pos_u < 0) {
+        hipError_t e = launch_setup(*a, M.ws, s);
+        if (e != hipSuccess) return fail_device(M, e, "setup");
+    }
     return BUDDY_OK;
 }
 
@@ -197,15 +222,16 @@ buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, in
 buddy_status wait_route(Model& M, int32_t seq, hipStream_t s) {
     volatile int32_t* flag = M.h_cnt + (M.cfg.n_layers - 2);
     const auto t0 = std::chrono::steady_clock::now();
-    long spins = 0;
+    auto next_check = t0 + std::chrono::milliseconds(1);
     while (*flag != seq) {
-        if ((++spins & 0xfff) == 0) {
-            hipError_t e = hipStreamQuery(s);
-            if (e != hipSuccess && e != hipErrorNotReady) return fail_device(M, e, "route wait");
-            if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(60)) {
-                snprintf(M.last_error, sizeof(M.last_error), "route wait: timed out");
-                return BUDDY_EDEVICE;
-            }
+        const auto now = std::chrono::steady_clock::now();
+        if (now < next_check) continue;
+        next_check = now + std::chrono::milliseconds(1);
+        hipError_t e = hipStreamQuery(s);
+        if (e != hipSuccess && e != hipErrorNotReady) return fail_device(M, e, "route wait");
+        if (now - t0 > std::chrono::seconds(60)) {
+            snprintf(M.last_error, sizeof(M.last_error), "route wait: timed out");
+            return BUDDY_EDEVICE;
         }
     }
     std::atomic_thread_fence(std::memory_order_acquire);
@@ -334,13 +360,11 @@ buddy_status buddy_pool_route(buddy_model* h, const buddy_kv* kv, const int32_t*
     if (st != BUDDY_OK) return st;
     hipStream_t s = (hipStream_t)stream;
     StepArgs a;
-    memset(&a, 0, sizeof(a));
-    a.B = B;
-    for (int b = 0; b < B; ++b) a.pos[b] = pos[b];
-    hipError_t e = launch_setup(a, M.ws, s);
-    if (e != hipSuccess) return fail_device(M, e, "setup");
-    if ((st = run_planner(M, kv, h_new, B, max_pos, s)) != BUDDY_OK) return st;
-    if ((e = launch_route(M, kv->k, kv->v, B, nullptr, nullptr, scores_out, true, -1, s)) !=
+    int pos_u;
+    if ((st = prepare_step(M, pos, nullptr, B, &a, &pos_u, s)) != BUDDY_OK) return st;
+    if ((st = run_planner(M, kv, h_new, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
+    hipError_t e;
+    if ((e = launch_route(M, kv->k, kv->v, a, nullptr, nullptr, scores_out, true, -1, s)) !=
         hipSuccess)
         return fail_device(M, e, "scores");
     return BUDDY_OK;
@@ -379,21 +403,17 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
 
     hipStream_t s = (hipStream_t)stream;
     StepArgs a;
-    memset(&a, 0, sizeof(a));
-    a.B = B;
-    for (int b = 0; b < B; ++b) {
-        a.pos[b] = pos[b];
-        a.k[b] = route_override ? 0 : (uint8_t)k[b];
-    }
-    hipError_t e = launch_setup(a, M.ws, s);
-    if (e != hipSuccess) return fail_device(M, e, "setup");
+    int pos_u;
+    if ((st = prepare_step(M, pos, route_override ? nullptr : k, B, &a, &pos_u, s)) != BUDDY_OK)
+        return st;
+    hipError_t e;
 
-    const Rows all{M.ws.idx_all, M.ws.n_all, B, true};
+    const Rows all{M.ws.idx_all, M.ws.n_all, B, true, true};
     // first block on every sequence (appends the first-layer K/V row)
-    if ((st = run_block(M, kv, hidden, 0, all, max_pos, s)) != BUDDY_OK) return st;
+    if ((st = run_block(M, kv, hidden, 0, all, max_pos, pos_u, s)) != BUDDY_OK) return st;
     // KV-aware planner and Decision Module, unless the route is given
     if (!route_override)
-        if ((st = run_planner(M, kv, hidden, B, max_pos, s)) != BUDDY_OK) return st;
+        if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
     // Launch policy.  Device-routed: every routable block is launched and its
     // kernels read the routed row count on the device (an unused block costs
     // only empty launches).  Host-routed: the compaction kernel publishes the
@@ -406,7 +426,7 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     else if (M.policy == BUDDY_LAUNCH_AUTO) host_routed = !all_used && B <= kHostRoutedMaxBatch;
     host_routed = host_routed && Lm > 0;
     const int32_t seq = host_routed ? (M.seq = (M.seq + 1) & 0x3fffffff) : -1;
-    if ((e = launch_route(M, kv->k, kv->v, B, route_override, mask_out, scores_out, false, seq,
+    if ((e = launch_route(M, kv->k, kv->v, a, route_override, mask_out, scores_out, false, seq,
                           s)) != hipSuccess)
         return fail_device(M, e, "route");
     if (host_routed && (st = wait_route(M, seq, s)) != BUDDY_OK) return st;
@@ -417,12 +437,13 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
             n_max = M.h_cnt[l - 1];
             if (n_max == 0) continue;
         }
+        // every sequence routed (known on the host): the rows are the batch in order
         const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), n_max,
-                     host_routed};
-        if ((st = run_block(M, kv, hidden, l, r, max_pos, s)) != BUDDY_OK) return st;
+                     host_routed, host_routed && n_max == B};
+        if ((st = run_block(M, kv, hidden, l, r, max_pos, pos_u, s)) != BUDDY_OK) return st;
     }
     // last block on every sequence
-    st = run_block(M, kv, hidden, c.n_layers - 1, all, max_pos, s);
+    st = run_block(M, kv, hidden, c.n_layers - 1, all, max_pos, pos_u, s);
     if (M.timing.n > 0 && M.timing.next < M.timing.n) ++M.timing.next;
     return st;
 }

@@ -137,25 +137,39 @@ struct StepArgs {
 
 // Row set of one routed launch: rows i < *cnt map to sequences idx[i]; the
 // grid is sized for at most n_max rows.  exact: the host knows that *cnt is
-// n_max (kernels then need not read the count before starting).
+// n_max (kernels then need not read the count before starting).  identity:
+// row i is sequence i (every sequence of the batch, in order), so kernels
+// need not read idx either.
 struct Rows {
     const int32_t* idx;
     const int32_t* cnt;
     int n_max;
     bool exact;
+    bool identity;
 };
+
+__device__ __forceinline__ int row_seq(const Rows& r, int i) { return r.identity ? i : r.idx[i]; }
+
+// Position of sequence b this step: pos_u when every sequence shares it
+// (no memory read), else the published per-sequence array.
+__device__ __forceinline__ int seq_pos(const int32_t* pos, int pos_u, int b) {
+    return pos_u >= 0 ? pos_u : pos[b];
+}
 
 hipError_t launch_setup(const StepArgs& a, const Workspace& ws, hipStream_t s);
 
-// Mean of K/V rows 0..pos of the first layer, joined with h: z = [mK | mV | h].
-hipError_t launch_pool(const Model& M, const void* k0, const void* v0, const float* h,
-                       int B, int max_pos, hipStream_t s);
+// Split sums of the first layer's K/V rows 0..pos; returns the number of
+// splits per (sequence, KV head) in *splits (the Decision Module GEMV folds
+// them, PRO_POOL).
+hipError_t launch_pool(const Model& M, const void* k0, const void* v0, int B, int max_pos,
+                       int pos_u, int* splits, hipStream_t s);
 
 // Decision Module second layer + prior + top-k (or the override mask), then
 // zero-fill of skipped K/V rows and per-block compaction.
 // publish_seq >= 0: also publish the per-block counts and then publish_seq
-// to the mapped host buffer (host-routed launches wait for it).
-hipError_t launch_route(const Model& M, const void* kc, const void* vc, int B,
+// to the mapped host buffer (host-routed launches wait for it).  Budgets and
+// positions travel in `a`.
+hipError_t launch_route(const Model& M, const void* kc, const void* vc, const StepArgs& a,
                         const uint8_t* route_override, uint8_t* mask_out,
                         float* scores_out, bool scores_only, int32_t publish_seq,
                         hipStream_t s);
@@ -163,7 +177,7 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, int B,
 hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B, int n,
                               uint8_t* mask_out, hipStream_t s);
 
-enum Pro { PRO_NONE = 0, PRO_RMSNORM = 1 };
+enum Pro { PRO_NONE = 0, PRO_RMSNORM = 1, PRO_POOL = 2 };
 enum Epi { EPI_ADD = 0, EPI_BIAS_ACT = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 
 struct GemvArgs {
@@ -176,7 +190,10 @@ struct GemvArgs {
     int f;                             // EPI_SWIGLU: rows j and f + j
     // EPI_QKV: rotary + cache append of this block
     void* kc; void* vc; int T; int hd; int nq; int nkv; int bcap;
-    const int32_t* pos; const float2* rope;
+    const int32_t* pos; int pos_u; const float2* rope;
+    // PRO_POOL: X is unused; row b of the input is the router context
+    // [sum K / n | sum V / n | h] built from the pool's split partial sums
+    const float* pool_part; int pool_splits, pool_max_splits; const float* h; int d;
 };
 hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream_t s);
 
@@ -184,7 +201,7 @@ struct AttnArgs {
     const float* q; float* o;
     const void* kc; const void* vc;    // this block's cache base
     int T, hd, nq, nkv, bcap;
-    const int32_t* pos;
+    const int32_t* pos; int pos_u;
     Rows rows;
     int chunks, chunk_len;
     float* part; int max_chunks;

@@ -23,6 +23,26 @@ __device__ __forceinline__ float scale_of(float m, float mn) {
     return m == -INFINITY ? 0.f : exp2f(m - mn);
 }
 
+// Sum over the 16 lanes of a DPP row (lanes 16r .. 16r+15), left in every
+// lane of the row: rotations by 8, 4, 2 and 1 within the row are plain VALU
+// operations, much shorter than LDS-routed shuffles.
+__device__ __forceinline__ float row_sum16(float v) {
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x122, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x121, 0xF, 0xF, false));
+    return v;
+}
+
+// Sum over the lpr lanes that share a cache row.
+template <int LPR>
+__device__ __forceinline__ float lanes_sum(float v) {
+    if (LPR == 16) return row_sum16(v);
+#pragma unroll
+    for (int o = LPR >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
 constexpr int kAttnPasses = 4;   // row passes of a workgroup, all loads issued up front
 
 // Rows of one workgroup: kAttnPasses passes of 4 wavefronts x (64 / (hd / V)) rows.
@@ -31,18 +51,18 @@ __host__ __device__ constexpr int attn_rows_per_wg(int hd) {
     return kAttnPasses * 4 * (kWave / (hd / St<T>::V));
 }
 
-template <typename T, int GM>
+template <typename T, int GM, int LPR>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     constexpr int V = St<T>::V;
     __shared__ float s_acc[4][GM][128 + 2];
     const int i = blockIdx.z;
     if (!a.rows.exact && i >= *a.rows.cnt) return;
-    const int b = a.rows.idx[i];
+    const int b = row_seq(a.rows, i);
     const int g = blockIdx.y, c = blockIdx.x;
-    const int pos = a.pos[b];
+    const int pos = seq_pos(a.pos, a.pos_u, b);
     const int G = a.nq / a.nkv;
-    const int lpr = a.hd / V;          // lanes per cache row
-    const int rpw = kWave / lpr;       // rows per wavefront pass
+    constexpr int lpr = LPR;           // lanes per cache row (hd / V)
+    constexpr int rpw = kWave / LPR;   // rows per wavefront pass
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int col = lane % lpr, sub = lane / lpr;
@@ -89,33 +109,49 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         for (int e = 0; e < V; ++e) acc[h][e] = 0.f;
     }
     for (int jb = j0; jb < j1; jb += rows_wg) {
-    if (jb != j0) load_block(jb);
+        if (jb != j0) load_block(jb);
+        // all scores of the block first: the row reductions are independent
+        float sc[kAttnPasses][GM];
 #pragma unroll
-    for (int p = 0; p < kAttnPasses; ++p) {
-        const int j = jb + (p * 4 + wave) * rpw + sub;
-        const bool live = j < j1;
-        float kf[V], vf[V];
-        unpack<T>(kr[p], kf);
-        unpack<T>(vr[p], vf);
+        for (int p = 0; p < kAttnPasses; ++p) {
+            float kf[V];
+            unpack<T>(kr[p], kf);
+            const bool live = jb + (p * 4 + wave) * rpw + sub < j1;
+#pragma unroll
+            for (int h = 0; h < GM; ++h) {
+                float d = 0.f;
+#pragma unroll
+                for (int e = 0; e < V; ++e) d += qr[h][e] * kf[e];
+                d = lanes_sum<LPR>(d);
+                sc[p][h] = live ? d : -INFINITY;
+            }
+        }
+        // one online-softmax update per block and head
 #pragma unroll
         for (int h = 0; h < GM; ++h) {
             if (h < G) {
-                float sc = 0.f;
+                float mx = sc[0][h];
 #pragma unroll
-                for (int e = 0; e < V; ++e) sc += qr[h][e] * kf[e];
-                for (int o = lpr >> 1; o > 0; o >>= 1) sc += __shfl_xor(sc, o, kWave);
-                if (live) {
-                    const float mn = fmaxf(m[h], sc);
+                for (int p = 1; p < kAttnPasses; ++p) mx = fmaxf(mx, sc[p][h]);
+                const float mn = fmaxf(m[h], mx);
+                if (mn != -INFINITY) {
                     const float al = scale_of(m[h], mn);
-                    const float pw = exp2f(sc - mn);
-                    l[h] = l[h] * al + pw;
+                    l[h] *= al;
 #pragma unroll
-                    for (int e = 0; e < V; ++e) acc[h][e] = acc[h][e] * al + pw * vf[e];
+                    for (int e = 0; e < V; ++e) acc[h][e] *= al;
+#pragma unroll
+                    for (int p = 0; p < kAttnPasses; ++p) {
+                        const float pw = scale_of(sc[p][h], mn);
+                        float vf[V];
+                        unpack<T>(vr[p], vf);
+                        l[h] += pw;
+#pragma unroll
+                        for (int e = 0; e < V; ++e) acc[h][e] += pw * vf[e];
+                    }
                     m[h] = mn;
                 }
             }
         }
-    }
     }
 
     // merge the row slots of the wavefront (lanes with equal col)
@@ -178,7 +214,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
     __shared__ float s_red[4];
     const int i = blockIdx.y;
     if (!a.rows.exact && i >= *a.rows.cnt) return;
-    const int b = a.rows.idx[i];
+    const int b = row_seq(a.rows, i);
     const int head = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const size_t pstride = (size_t)a.hd + 2;
@@ -213,14 +249,25 @@ int attention_rows_per_wg(int dtype, int hd) {
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     dim3 grid(a.chunks, a.nkv, a.rows.n_max);
     const int G = a.nq / a.nkv;   // query heads per KV head, held in registers
+    // lanes per cache row: hd / 8 (bf16) or hd / 4 (fp32); head_dim is 64 or 128
     if (dtype == BUDDY_BF16) {
-        if (G == 1) attn_kernel<bf16_t, 1><<<grid, 256, 0, s>>>(a);
-        else if (G == 2) attn_kernel<bf16_t, 2><<<grid, 256, 0, s>>>(a);
-        else if (G <= 4) attn_kernel<bf16_t, 4><<<grid, 256, 0, s>>>(a);
-        else attn_kernel<bf16_t, 8><<<grid, 256, 0, s>>>(a);
+        if (a.hd == 128) {
+            if (G == 1) attn_kernel<bf16_t, 1, 16><<<grid, 256, 0, s>>>(a);
+            else if (G == 2) attn_kernel<bf16_t, 2, 16><<<grid, 256, 0, s>>>(a);
+            else if (G <= 4) attn_kernel<bf16_t, 4, 16><<<grid, 256, 0, s>>>(a);
+            else attn_kernel<bf16_t, 8, 16><<<grid, 256, 0, s>>>(a);
+        } else {
+            if (G <= 2) attn_kernel<bf16_t, 2, 8><<<grid, 256, 0, s>>>(a);
+            else attn_kernel<bf16_t, 8, 8><<<grid, 256, 0, s>>>(a);
+        }
     } else {
-        if (G <= 2) attn_kernel<float, 2><<<grid, 256, 0, s>>>(a);
-        else attn_kernel<float, 8><<<grid, 256, 0, s>>>(a);
+        if (a.hd == 128) {
+            if (G <= 2) attn_kernel<float, 2, 32><<<grid, 256, 0, s>>>(a);
+            else attn_kernel<float, 8, 32><<<grid, 256, 0, s>>>(a);
+        } else {
+            if (G <= 2) attn_kernel<float, 2, 16><<<grid, 256, 0, s>>>(a);
+            else attn_kernel<float, 8, 16><<<grid, 256, 0, s>>>(a);
+        }
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

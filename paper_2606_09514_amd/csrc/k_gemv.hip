@@ -11,6 +11,8 @@
 //
 // Prologues:  PRO_NONE    x = X[b]
 //             PRO_RMSNORM x = X[b] / sqrt(mean(X[b]^2) + eps) * gain
+//             PRO_POOL    x = [sum K / n | sum V / n | h_b], folding the split
+//                         sums of the first-layer pool (router context)
 // Epilogues:  EPI_ADD      Y[b][r] += acc              (residual of Eq. 1)
 //             EPI_BIAS_ACT Y[b][r] = act(acc + bias)  (Decision Module layer 1)
 //             EPI_SWIGLU   unit j = rows (j, f + j): Y[b][j] = SiLU(g) * u
@@ -65,7 +67,7 @@ __device__ __forceinline__ void epilogue(const GemvArgs& g, int b, int u, int r0
     } else {  // EPI_QKV
         const int half = g.hd >> 1;
         const int hg = u / half, i = u - hg * half;
-        const int pos = g.pos[b];
+        const int pos = seq_pos(g.pos, g.pos_u, b);
         if (hg < g.nq + g.nkv) {
             const float2 cs = g.rope[(size_t)pos * half + i];
             const float a0 = v0 * cs.x - v1 * cs.y;
@@ -191,8 +193,31 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
             float ss = 0.f;
-            if (r < nr) {
-                const float* xr = g.X + (size_t)g.rows.idx[i0 + r] * g.ldx;
+            if (PRO == PRO_POOL && r < nr) {
+                // router context of sequence b: means of the pool's split sums,
+                // then the newest hidden state
+                const int b = row_seq(g.rows, i0 + r);
+                const int zdim = 2 * g.nkv * g.hd;
+                const float inv_n = 1.0f / (float)(seq_pos(g.pos, g.pos_u, b) + 1);
+                for (int k = tid * 4; k < K; k += NT * 4) {
+                    float4 v;
+                    if (k < zdim) {
+                        const int which = k / (g.nkv * g.hd), gg = (k / g.hd) % g.nkv, e = k % g.hd;
+                        const float* pp = g.pool_part +
+                            (((size_t)b * g.nkv + gg) * g.pool_max_splits) * 2 * g.hd + which * g.hd + e;
+                        v = make_float4(0.f, 0.f, 0.f, 0.f);
+                        for (int q = 0; q < g.pool_splits; ++q) {
+                            const float4 t = *reinterpret_cast<const float4*>(pp + (size_t)q * 2 * g.hd);
+                            v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
+                        }
+                        v.x *= inv_n; v.y *= inv_n; v.z *= inv_n; v.w *= inv_n;
+                    } else {
+                        v = *reinterpret_cast<const float4*>(g.h + (size_t)b * g.d + (k - zdim));
+                    }
+                    *reinterpret_cast<float4*>(xs + r * K + k) = v;
+                }
+            } else if (r < nr) {
+                const float* xr = g.X + (size_t)row_seq(g.rows, i0 + r) * g.ldx;
                 for (int k = tid * V; k < K; k += NT * V) {
                     float v[V];
 #pragma unroll
@@ -261,7 +286,7 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
                     for (int q = 0; q < NR; ++q) if (q == r) sc = inv[q];
                     int r0, r1;
                     unit_rows<EPI>(g, u, r0, r1);
-                    epilogue<TW, EPI>(g, g.rows.idx[i0 + r], u, r0, r1, s_part[uu][r] * sc,
+                    epilogue<TW, EPI>(g, row_seq(g.rows, i0 + r), u, r0, r1, s_part[uu][r] * sc,
                                       s_part[UPB + uu][r] * sc);
                 }
             }
@@ -276,7 +301,7 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
                     for (int q = 0; q < S; ++q) v += s_part[sl * S + q][r];
 #pragma unroll
                     for (int q = 0; q < NR; ++q) if (q == r) sc = inv[q];
-                    epilogue1<TW, EPI>(g, g.rows.idx[i0 + r], rw, v * sc);
+                    epilogue1<TW, EPI>(g, row_seq(g.rows, i0 + r), rw, v * sc);
                 }
             }
         }
@@ -370,7 +395,7 @@ static hipError_t dispatch_epi(int pro, int epi, const GemvArgs& g, hipStream_t 
         return dispatch_nr<TW, PRO_RMSNORM, EPI_QKV>(g, units, s);
     }
     if (epi == EPI_SWIGLU) return dispatch_nr<TW, PRO_RMSNORM, EPI_SWIGLU>(g, g.f, s);
-    if (epi == EPI_BIAS_ACT) return dispatch_nr<TW, PRO_NONE, EPI_BIAS_ACT>(g, g.N, s);
+    if (epi == EPI_BIAS_ACT) return dispatch_nr<TW, PRO_POOL, EPI_BIAS_ACT>(g, g.N, s);
     if (pro == PRO_RMSNORM) return dispatch_nr<TW, PRO_RMSNORM, EPI_ADD>(g, g.N, s);
     return dispatch_nr<TW, PRO_NONE, EPI_ADD>(g, g.N, s);
 }

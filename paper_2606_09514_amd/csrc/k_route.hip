@@ -3,12 +3,14 @@
 //  setup_kernel   publishes the step's positions and budgets to device memory
 //                 and the identity row list used by the always-run blocks.
 //  pool_kernel    KV-aware planner (Sec. 4.3): sums of the first layer's K
-//                 and V rows 0..pos per KV head over split position ranges;
-//  pool_finish_kernel  folds the split sums in order into the means and
-//                 joins the newest hidden state: z = [mean K | mean V | h].
+//                 and V rows 0..pos per KV head over a few split position
+//                 ranges; the Decision Module's first GEMV folds the splits
+//                 into the means and joins the newest hidden state,
+//                 z = [mean K | mean V | h] (PRO_POOL in k_gemv.hip).
 //  route_kernel   Decision Module output layer plus prior fusion (Eq. 2),
 //                 deterministic top-k by rank counting, and zero-fill of the
-//                 K/V row of every skipped block (Sec. 6).
+//                 K/V row of every skipped block (Sec. 6); with a single
+//                 sequence it also does the compaction below.
 //  compact_kernel grouping by mask (App. C.1): for every routable block the
 //                 ascending list of sequences that run it and their count.
 //  topk_kernel    the standalone top-k entry point.
@@ -39,9 +41,7 @@ hipError_t launch_setup(const StepArgs& a, const Workspace& ws, hipStream_t s) {
 
 struct PoolParams {
     const void* k0; const void* v0;  // first layer's cache base
-    const float* h; int d;           // newest hidden [B][d]
-    const int32_t* pos;
-    float* z; int din;
+    const int32_t* pos; int pos_u;
     float* part;
     int T, hd, nkv, splits, max_splits;
 };
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolParams p) {
     __shared__ float red[2][256 * V];   // [K|V][row slot][hd] partial sums
     const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x;
-    const int n = p.pos[b] + 1;
+    const int n = seq_pos(p.pos, p.pos_u, b) + 1;
     const int cpr = p.hd / V;           // threads per cache row
     const int rpp = 256 / cpr;          // rows per pass
     const int col = tid % cpr, slot = tid / cpr;
@@ -65,6 +65,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolParams p) {
     float ak[V], av[V];
 #pragma unroll
     for (int e = 0; e < V; ++e) ak[e] = av[e] = 0.f;
+#pragma unroll 4
     for (int j = j0 + slot; j < j1; j += rpp) {
         float kr[V], vr[V];
         St<T>::vec(K + (size_t)j * p.hd + col * V, kr);
@@ -87,45 +88,25 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolParams p) {
     }
 }
 
-__global__ __launch_bounds__(256) void pool_finish_kernel(PoolParams p) {
-    const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-    const float inv_n = 1.0f / (float)(p.pos[b] + 1);
-    const float* part = p.part + (((size_t)b * p.nkv + g) * p.max_splits) * 2 * p.hd;
-    for (int t = tid; t < 2 * p.hd; t += 256) {
-        float acc = 0.f;
-#pragma unroll 8
-        for (int q = 0; q < p.splits; ++q) acc += part[(size_t)q * 2 * p.hd + t];
-        const int which = t / p.hd, e = t % p.hd;
-        p.z[(size_t)b * p.din + which * p.nkv * p.hd + g * p.hd + e] = acc * inv_n;
-    }
-    // the newest hidden state is the last part of z
-    if (g == 0)
-        for (int t = tid; t < p.d; t += 256)
-            p.z[(size_t)b * p.din + 2 * p.nkv * p.hd + t] = p.h[(size_t)b * p.d + t];
-}
-
-hipError_t launch_pool(const Model& M, const void* k0, const void* v0, const float* h,
-                       int B, int max_pos, hipStream_t s) {
+hipError_t launch_pool(const Model& M, const void* k0, const void* v0, int B, int max_pos,
+                       int pos_u, int* splits_out, hipStream_t s) {
     const buddy_config& c = M.cfg;
     PoolParams p;
-    p.k0 = k0; p.v0 = v0; p.h = h; p.d = c.d_model;
-    p.pos = M.ws.pos; p.z = M.ws.z; p.din = 2 * c.n_kv_heads * c.head_dim + c.d_model;
+    p.k0 = k0; p.v0 = v0; p.pos = M.ws.pos; p.pos_u = pos_u;
     p.part = M.ws.pool_part;
     p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.max_splits = M.ws.max_pool_splits;
-    // enough workgroups to stream the first-layer cache with the whole chip,
-    // at least 64 rows per workgroup
-    int want = (512 + B * c.n_kv_heads - 1) / (B * c.n_kv_heads);
-    int by_len = (max_pos + 1 + 63) / 64;
+    // a few position splits per (sequence, KV head): enough workgroups to
+    // stream the first-layer cache, few enough partials for the fold
+    int want = (256 + B * c.n_kv_heads - 1) / (B * c.n_kv_heads);
+    int by_len = (max_pos + 1 + 127) / 128;
     int splits = want < by_len ? want : by_len;
     if (splits < 1) splits = 1;
     if (splits > p.max_splits) splits = p.max_splits;
     p.splits = splits;
+    *splits_out = splits;
     dim3 grid(splits, c.n_kv_heads, B);
     if (c.dtype == BUDDY_BF16) pool_kernel<bf16_t><<<grid, 256, 0, s>>>(p);
     else pool_kernel<float><<<grid, 256, 0, s>>>(p);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    pool_finish_kernel<<<dim3(c.n_kv_heads, B), 256, 0, s>>>(p);
     return hipGetLastError();
 }
 
@@ -144,20 +125,29 @@ struct RouteParams {
     const float* a; int H;
     const void* w2; const void* b2; const float* prior; float omega;
     int Lm, B;
-    const int32_t* kb; const int32_t* pos;
     const uint8_t* route_override;
     uint8_t* mask; uint8_t* mask_out;
     float* scores; float* scores_out;
     void* kc; void* vc;               // cache bases (layer 0)
     int T, hd, nkv, bcap;
     int scores_only;
+    int32_t* idx; int32_t* cnt;       // compaction outputs (single-sequence launch)
+    volatile int32_t* host_cnt; int32_t seq;
 };
 
+// Groups by mask the routed blocks of a one-sequence batch and publishes the
+// counts (shared by route_kernel at B = 1 and compact_kernel).
+__device__ __forceinline__ void publish_counts(volatile int32_t* host_cnt, int Lm, int32_t seq) {
+    __threadfence_system();
+    host_cnt[Lm] = seq;
+}
+
 template <typename T>
-__global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
+__global__ __launch_bounds__(1024) void route_kernel(RouteParams p, StepArgs sa) {
     __shared__ float s_sc[256];
     __shared__ uint8_t s_mask[256];
-    const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int Lm = p.Lm;
 
     if (p.route_override) {
@@ -167,8 +157,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
         const T* w2 = (const T*)p.w2;
         const float* a = p.a + (size_t)b * p.H;
         const int nv = p.H / V;        // 16-byte vectors per output-layer row
-#pragma unroll 4
-        for (int i = wave; i < Lm; i += 4) {
+        for (int i = wave; i < Lm; i += 16) {
             float acc = 0.f;
             for (int v = lane; v < nv; v += kWave) {
                 float wv[V];
@@ -193,22 +182,31 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
             const float si = s_sc[tid];
             int rank = 0;
             for (int j = 0; j < Lm; ++j) rank += (j != tid) && beats(s_sc[j], j, si, tid);
-            s_mask[tid] = rank < p.kb[b];
+            s_mask[tid] = rank < (int)sa.k[b];
         }
     }
     __syncthreads();
     if (tid < Lm) {
         p.mask[(size_t)b * Lm + tid] = s_mask[tid];
         if (p.mask_out) p.mask_out[(size_t)b * Lm + tid] = s_mask[tid];
+        if (gridDim.x == 1) {   // one sequence: this workgroup is the compaction
+            p.idx[(size_t)tid * p.bcap] = 0;
+            p.cnt[tid] = s_mask[tid];
+            if (p.host_cnt) p.host_cnt[tid] = s_mask[tid];
+        }
+    }
+    if (gridDim.x == 1 && p.host_cnt) {
+        __syncthreads();
+        if (tid == 0) publish_counts(p.host_cnt, Lm, p.seq);
     }
 
     // zero-filled K/V row at this step's position for every skipped block,
     // written as 16-byte vectors
     constexpr int VZ = St<T>::V;
-    const int pos = p.pos[b];
+    const int pos = sa.pos[b];
     const size_t layer_stride = (size_t)p.bcap * p.nkv * p.T * p.hd;
     const int per_layer = p.nkv * (p.hd / VZ);
-    for (int t = tid; t < Lm * per_layer; t += 256) {
+    for (int t = tid; t < Lm * per_layer; t += 1024) {
         const int i = t / per_layer, r = t % per_layer;
         if (s_mask[i]) continue;
         const int g = r / (p.hd / VZ), e = (r % (p.hd / VZ)) * VZ;
@@ -217,7 +215,6 @@ __global__ __launch_bounds__(256) void route_kernel(RouteParams p) {
         *reinterpret_cast<uint4*>((T*)p.kc + at) = make_uint4(0u, 0u, 0u, 0u);
         *reinterpret_cast<uint4*>((T*)p.vc + at) = make_uint4(0u, 0u, 0u, 0u);
     }
-
 }
 
 // One workgroup: each wavefront scans the mask columns of every fourth
@@ -245,35 +242,35 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint8_t* mask, int L
     }
     if (host_cnt) {
         __syncthreads();
-        if (tid == 0) {
-            __threadfence_system();
-            host_cnt[Lm] = seq;
-        }
+        if (tid == 0) publish_counts(host_cnt, Lm, seq);
     }
 }
 
-hipError_t launch_route(const Model& M, const void* kc, const void* vc, int B,
+hipError_t launch_route(const Model& M, const void* kc, const void* vc, const StepArgs& a,
                         const uint8_t* route_override, uint8_t* mask_out,
                         float* scores_out, bool scores_only, int32_t publish_seq,
                         hipStream_t s) {
     const buddy_config& c = M.cfg;
+    const int B = a.B;
     RouteParams p;
     p.a = M.ws.a; p.H = c.dm_hidden;
     p.w2 = M.dm.w2; p.b2 = M.dm.b2; p.prior = M.dm.prior; p.omega = M.dm.omega;
     p.Lm = c.n_layers - 2; p.B = B;
-    p.kb = M.ws.kb; p.pos = M.ws.pos;
     p.route_override = route_override;
     p.mask = M.ws.mask; p.mask_out = mask_out;
     p.scores = M.ws.scores; p.scores_out = scores_out;
     p.kc = (void*)kc; p.vc = (void*)vc;
     p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.bcap = c.max_batch;
     p.scores_only = scores_only ? 1 : 0;
-    if (c.dtype == BUDDY_BF16) route_kernel<bf16_t><<<B, 256, 0, s>>>(p);
-    else route_kernel<float><<<B, 256, 0, s>>>(p);
+    p.idx = M.ws.idx; p.cnt = M.ws.cnt;
+    p.host_cnt = publish_seq >= 0 ? M.d_host_cnt : nullptr;
+    p.seq = publish_seq;
+    if (c.dtype == BUDDY_BF16) route_kernel<bf16_t><<<B, 1024, 0, s>>>(p, a);
+    else route_kernel<float><<<B, 1024, 0, s>>>(p, a);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || scores_only || p.Lm == 0) return e;
+    if (e != hipSuccess || scores_only || p.Lm == 0 || B == 1) return e;
     compact_kernel<<<1, 256, 0, s>>>(M.ws.mask, p.Lm, B, c.max_batch, M.ws.idx, M.ws.cnt,
-                                     publish_seq >= 0 ? M.d_host_cnt : nullptr, publish_seq);
+                                     p.host_cnt, publish_seq);
     return hipGetLastError();
 }
 
