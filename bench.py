@@ -121,7 +121,7 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer):
     total_bytes = sum(s["total"] for s in step_bytes)
     assert all(int(m[t, b].sum()) == ks[b] for t in range(steps) for b in range(B))
     distinct = len({m[t].tobytes() for t in range(steps)})
-    return dict(total_ms=total_ms, ms_per_step=total_ms / steps,
+    return dict(ks=ks, total_ms=total_ms, ms_per_step=total_ms / steps,
                 tokens_per_s=B * steps / (total_ms / 1e3),
                 bytes_per_step=total_bytes / steps,
                 step_hbm_frac=total_bytes / (total_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
@@ -222,6 +222,8 @@ def main():
 
     head = runs[next(iter(runs))]
     head_k = budgets[0] if not w.mixed else None
+    for r in runs.values():
+        r.pop("hidden", None)
     d, f = cfg["d_model"], cfg["d_ffn"]
     s = 2 if w.dtype == "bf16" else 4
     # algorithmic bytes of one gate/up launch: weights, input rows, output rows
@@ -230,7 +232,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, W, dk, dv, x0, head_k if head_k is not None else 15, w.ctx)
+        cpu = cpu_baseline(cfg, W, dk, dv, x0, head["ks"][0], w.ctx)
 
     out = {
         "metric": "routed-decode tokens/s at budget k (1 GPU); % of HBM roofline",

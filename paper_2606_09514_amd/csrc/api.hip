@@ -81,7 +81,7 @@ const char* layer_base(const Model& M, const void* kv, int l) {
 // workgroup block reads, at most kAttnMaxChunks chunks.
 void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chunk_len) {
     const buddy_config& c = M.cfg;
-    const int rows = attention_rows_per_wg(c.dtype, c.head_dim);
+    const int rows = attention_rows_per_wg(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads);
     const int blocks = (max_pos + 1 + rows - 1) / rows;
     const int pairs = n_rows * c.n_kv_heads;
     int want = (2048 + pairs - 1) / pairs;
@@ -97,6 +97,19 @@ void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chun
     *chunks = (max_pos + 1 + *chunk_len - 1) / *chunk_len;
 }
 
+// A routed projection: the GEMV for batches of up to kGemvMaxRows sequences
+// (or fp32 weights), the MFMA path beyond.  The choice depends on the batch,
+// not on how many sequences a block routes, so a sequence's arithmetic does
+// not depend on the routes of the others or on the launch policy.
+hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, hipStream_t s) {
+    if (M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && g.K % 128 == 0) {
+        g.XB = M.ws.xb;
+        g.ldxb = M.ws.xb_ld;
+        return launch_mfma(pro, epi, g, s);
+    }
+    return launch_gemv(M.cfg.dtype, pro, epi, g, s);
+}
+
 // Timing hook: event around kernel `kind` of block l, if asked for.
 bool timed(const Model& M, int kind, int l) {
     const TimingHook& t = M.timing;
@@ -109,7 +122,7 @@ hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
     return hipEventRecord(stop ? t.stop[t.next] : t.start[t.next], s);
 }
 
-buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows rows,
+buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows rows, int batch,
                        int max_pos, int pos_u, hipStream_t s) {
     const buddy_config& c = M.cfg;
     const buddy_layer_weights& w = M.layers[l];
@@ -130,7 +143,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     g.X = hidden; g.ldx = c.d_model; g.gain = w.attn_norm;
     g.Y = M.ws.q; g.ldy = qdim;
     if ((e = mark(M, BUDDY_KERNEL_QKV, l, false, s)) != hipSuccess ||
-        (e = launch_gemv(c.dtype, PRO_RMSNORM, EPI_QKV, g, s)) != hipSuccess ||
+        (e = launch_proj(M, batch, PRO_RMSNORM, EPI_QKV, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_QKV, l, true, s)) != hipSuccess)
         return fail_device(M, e, "qkv");
 
@@ -150,7 +163,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     g.W = w.wo; g.N = c.d_model; g.K = qdim; g.X = M.ws.o; g.ldx = qdim; g.gain = nullptr;
     g.Y = hidden; g.ldy = c.d_model;
     if ((e = mark(M, BUDDY_KERNEL_O_PROJ, l, false, s)) != hipSuccess ||
-        (e = launch_gemv(c.dtype, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
+        (e = launch_proj(M, batch, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_O_PROJ, l, true, s)) != hipSuccess)
         return fail_device(M, e, "o_proj");
 
@@ -158,7 +171,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     g.W = w.wgate_up; g.N = 2 * c.d_ffn; g.K = c.d_model; g.X = hidden; g.ldx = c.d_model;
     g.gain = w.mlp_norm; g.f = c.d_ffn; g.Y = M.ws.m; g.ldy = c.d_ffn;
     if ((e = mark(M, BUDDY_KERNEL_GATE_UP, l, false, s)) != hipSuccess ||
-        (e = launch_gemv(c.dtype, PRO_RMSNORM, EPI_SWIGLU, g, s)) != hipSuccess ||
+        (e = launch_proj(M, batch, PRO_RMSNORM, EPI_SWIGLU, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_GATE_UP, l, true, s)) != hipSuccess)
         return fail_device(M, e, "gate_up");
 
@@ -166,7 +179,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     g.W = w.wdown; g.N = c.d_model; g.K = c.d_ffn; g.X = M.ws.m; g.ldx = c.d_ffn;
     g.gain = nullptr; g.Y = hidden; g.ldy = c.d_model;
     if ((e = mark(M, BUDDY_KERNEL_DOWN, l, false, s)) != hipSuccess ||
-        (e = launch_gemv(c.dtype, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
+        (e = launch_proj(M, batch, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_DOWN, l, true, s)) != hipSuccess)
         return fail_device(M, e, "down");
     return BUDDY_OK;
@@ -191,6 +204,8 @@ buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, in
     g.hd = c.head_dim; g.nkv = c.n_kv_heads; g.pos = M.ws.pos; g.pos_u = pos_u;
     g.pool_part = M.ws.pool_part; g.pool_splits = splits;
     g.pool_max_splits = M.ws.max_pool_splits; g.h = h; g.d = c.d_model;
+    // the Decision Module keeps fp32 activations at every batch size: routes
+    // are decided on these scores
     if ((e = launch_gemv(c.dtype, PRO_POOL, EPI_BIAS_ACT, g, s)) != hipSuccess)
         return fail_device(M, e, "dm_hidden");
     return BUDDY_OK;
@@ -285,6 +300,11 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
     if (max_splits > 64) max_splits = 64;
     M.ws.max_chunks = max_chunks;
     M.ws.max_pool_splits = max_splits;
+    size_t xb_ld = (size_t)c.d_model;
+    if ((size_t)c.d_ffn > xb_ld) xb_ld = c.d_ffn;
+    if (qdim > xb_ld) xb_ld = qdim;
+    if (din > xb_ld) xb_ld = din;
+    M.ws.xb_ld = (int)xb_ld;
 
     struct Piece { void** dst; size_t bytes; };
     Workspace& W = M.ws;
@@ -298,6 +318,7 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
         {(void**)&W.part, Bc * c.n_heads * max_chunks * (hd + 2) * 4},
         {(void**)&W.pool_part, Bc * c.n_kv_heads * max_splits * 2 * hd * 4},
         {(void**)&W.rope, (size_t)c.max_ctx * (hd / 2) * sizeof(float2)},
+        {(void**)&W.xb, ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
     };
     size_t total = 0;
     for (const Piece& p : pieces) total += align_up(p.bytes);
@@ -410,7 +431,7 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
 
     const Rows all{M.ws.idx_all, M.ws.n_all, B, true, true};
     // first block on every sequence (appends the first-layer K/V row)
-    if ((st = run_block(M, kv, hidden, 0, all, max_pos, pos_u, s)) != BUDDY_OK) return st;
+    if ((st = run_block(M, kv, hidden, 0, all, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
     // KV-aware planner and Decision Module, unless the route is given
     if (!route_override)
         if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
@@ -440,10 +461,10 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
         // every sequence routed (known on the host): the rows are the batch in order
         const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), n_max,
                      host_routed, host_routed && n_max == B};
-        if ((st = run_block(M, kv, hidden, l, r, max_pos, pos_u, s)) != BUDDY_OK) return st;
+        if ((st = run_block(M, kv, hidden, l, r, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
     }
     // last block on every sequence
-    st = run_block(M, kv, hidden, c.n_layers - 1, all, max_pos, pos_u, s);
+    st = run_block(M, kv, hidden, c.n_layers - 1, all, B, max_pos, pos_u, s);
     if (M.timing.n > 0 && M.timing.next < M.timing.n) ++M.timing.next;
     return st;
 }

@@ -95,6 +95,8 @@ struct Workspace {
     float* part;         // attention partials [max_batch][n_heads][max_chunks][hd + 2]
     float* pool_part;    // pool partials [max_batch][n_kv][max_pool_splits][2 hd]
     float2* rope;        // [max_ctx][hd/2] (cos, sin) of pos * theta^(-2i/hd)
+    bf16_t* xb;          // [round16(max_batch)][xb_ld] compact bf16 rows (MFMA path)
+    int xb_ld;
     int max_chunks;
     int max_pool_splits;
 };
@@ -194,8 +196,15 @@ struct GemvArgs {
     // PRO_POOL: X is unused; row b of the input is the router context
     // [sum K / n | sum V / n | h] built from the pool's split partial sums
     const float* pool_part; int pool_splits, pool_max_splits; const float* h; int d;
+    // MFMA path: compact bf16 activation rows [round16(max_batch)][ldxb]
+    bf16_t* XB; int ldxb;
 };
 hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream_t s);
+// MFMA path (bf16 weights, K a multiple of 128): prep of the compact bf16
+// rows, then the MFMA projection with the same epilogues.
+hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s);
+// Routed rows above which a bf16 projection takes the MFMA path.
+constexpr int kGemvMaxRows = 4;
 
 struct AttnArgs {
     const float* q; float* o;
@@ -209,6 +218,6 @@ struct AttnArgs {
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // Cache rows one attention workgroup reads per block (chunk lengths are
 // multiples of it).
-int attention_rows_per_wg(int dtype, int hd);
+int attention_rows_per_wg(int dtype, int hd, int G);
 
 }  // namespace buddy

@@ -43,17 +43,21 @@ __device__ __forceinline__ float lanes_sum(float v) {
     return v;
 }
 
-constexpr int kAttnPasses = 4;   // row passes of a workgroup, all loads issued up front
+// Row passes of a workgroup block, all of whose loads are issued up front:
+// four for up to four query heads per KV head, two for larger groups (their
+// registers hold 8 query heads and accumulators).
+__host__ __device__ constexpr int attn_passes(int G) { return G <= 4 ? 4 : 2; }
 
-// Rows of one workgroup: kAttnPasses passes of 4 wavefronts x (64 / (hd / V)) rows.
+// Rows of one workgroup block: passes x 4 wavefronts x (64 / (hd / V)) rows.
 template <typename T>
-__host__ __device__ constexpr int attn_rows_per_wg(int hd) {
-    return kAttnPasses * 4 * (kWave / (hd / St<T>::V));
+__host__ __device__ constexpr int attn_rows_per_wg(int hd, int G) {
+    return attn_passes(G) * 4 * (kWave / (hd / St<T>::V));
 }
 
 template <typename T, int GM, int LPR>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     constexpr int V = St<T>::V;
+    constexpr int kAttnPasses = attn_passes(GM);
     __shared__ float s_acc[4][GM][128 + 2];
     const int i = blockIdx.z;
     if (!a.rows.exact && i >= *a.rows.cnt) return;
@@ -242,8 +246,10 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
     }
 }
 
-int attention_rows_per_wg(int dtype, int hd) {
-    return dtype == BUDDY_BF16 ? attn_rows_per_wg<bf16_t>(hd) : attn_rows_per_wg<float>(hd);
+int attention_rows_per_wg(int dtype, int hd, int G) {
+    // G rounded up to the register class the launcher picks
+    const int gm = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8;
+    return dtype == BUDDY_BF16 ? attn_rows_per_wg<bf16_t>(hd, gm) : attn_rows_per_wg<float>(hd, gm);
 }
 
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {

@@ -123,9 +123,8 @@ def kv_cache(cfg: dict, batch: int, ctx: int, seed: int, device="cpu",
     for _ in range(2):
         t = torch.zeros((L, batch, nkv, T, hd), dtype=_tdtype(cfg["dtype"]), device=device)
         if ctx > 0:
-            for l in range(L):   # per layer keeps the float32 temporary small
-                t[l, :, :, :ctx, :] = _normal((batch, nkv, ctx, hd), fill_std, 0.0, gen,
-                                              device, cfg["dtype"])
+            for l in range(L):   # filled in place, one layer at a time
+                t[l, :, :, :ctx, :].normal_(mean=0.0, std=fill_std, generator=gen)
         out.append(t)
     return tuple(out)
 

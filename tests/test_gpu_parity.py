@@ -276,3 +276,91 @@ def test_launch_policies_agree_bitwise():
         outs.append((h.tobytes(), m.tobytes(), s.tobytes(), P.download(dk).tobytes(),
                      P.download(dv).tobytes()))
     assert outs[0] == outs[1]
+
+
+# --------------------------------------------- batched (MFMA) projections
+
+def one_step_all(P, hk, hv, pos, ks, x):
+    """One teacher-forced step of every sequence from the given host caches."""
+    dk, dv = P.upload(hk), P.upload(hv)
+    rep = new_report()
+    compare_step(P, hk, hv, dk, dv, x, pos, ks, rep)
+    return rep
+
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+@pytest.mark.parametrize("B", [40, 150])
+def test_batched_steps_mfma(B, policy):
+    """More routed rows than the GEMV stages per pass: the bf16 projections
+    run on MFMA (compact bf16 rows, fp32 accumulation).  Mixed positions and
+    budgets; B = 150 spans two 128-row column groups."""
+    T = 48
+    P = Pair("tiny", "bf16", T, B, seed=21, omega=0.1, policy=policy)
+    g = torch.Generator().manual_seed(22)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    rng = np.random.default_rng(23)
+    pos = rng.integers(0, T, size=B).tolist()
+    ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=24).numpy()
+    rep = one_step_all(P, hk, hv, pos, ks, x)
+    print(B, rep)
+
+
+def sampled_full_size(name, samples, seed=0):
+    """One step of a full-size workload on the GPU; the sampled sequences
+    are checked against the oracle (their caches and the weights are copied
+    to the host)."""
+    w = synth.WORKLOADS[name]
+    P = Pair(w.shape, w.dtype, w.ctx + 2, w.batch, seed=seed, omega=w.omega, device_gen=True)
+    dk, dv = synth.kv_cache(P.cfg, w.batch, w.ctx, seed=1, device="cuda")
+    ks = synth.budgets(w, seed=1)
+    pos = [w.ctx] * w.batch
+    x = synth.hidden_inputs(w.batch, P.cfg["d_model"], seed=2).numpy()
+    L = P.cfg["n_layers"]
+    pre = {b: (synth.storage_numpy(dk[:, b]).copy(), synth.storage_numpy(dv[:, b]).copy())
+           for b in samples}
+    hg, mg, _ = gpu_step(P, dk, dv, x, pos, ks)
+    tol = 2e-2
+    report = new_report()
+    for b in samples:
+        hk, hv = pre[b][0].copy(), pre[b][1].copy()
+        h, m, s, margin, n_exec = P.orc.decode_seq([hk[l] for l in range(L)],
+                                                   [hv[l] for l in range(L)],
+                                                   w.ctx, ks[b], x[b])
+        if not np.array_equal(m, mg[b]):
+            assert margin < 1e-3, (b, margin)
+            report["margin_mismatches"] += 1
+            hk, hv = pre[b][0].copy(), pre[b][1].copy()
+            h, *_ = P.orc.decode_seq([hk[l] for l in range(L)], [hv[l] for l in range(L)],
+                                     w.ctx, ks[b], x[b], route=mg[b])
+        assert int(mg[b].sum()) == ks[b] and n_exec == ks[b] + 2
+        err = relerr(hg[b], h)
+        report["max_hidden_err"] = max(report["max_hidden_err"], err)
+        assert err < tol, (b, err)
+        # new K/V rows of the sampled sequence against the oracle's
+        gk = synth.storage_numpy(dk[:, b, :, w.ctx])
+        gv = synth.storage_numpy(dv[:, b, :, w.ctx])
+        run = np.concatenate([[1], mg[b], [1]])
+        for l in range(L):
+            for ref, got in ((hk[l][:, w.ctx], gk[l]), (hv[l][:, w.ctx], gv[l])):
+                r, gg = f32(ref, P.sdt), f32(got, P.sdt)
+                if run[l]:
+                    e = relerr(gg, r)
+                    report["max_kv_err"] = max(report["max_kv_err"], e)
+                    assert e < tol, (b, l, e)
+                else:
+                    assert np.all(gg == 0) and np.all(r == 0)
+    print(name, report)
+
+
+def test_llama3_8b_b32_ctx4096_mixed_sampled():
+    sampled_full_size("llama3_8b_b32_ctx4096_mixed", samples=[0, 17, 31])
+
+
+def test_qwen2_7b_b64_ctx8192_sampled():
+    sampled_full_size("qwen2_7b_b64_ctx8192", samples=[0, 63])
+
+
+def test_mha_13b_b96_ctx2048_mixed_sampled():
+    sampled_full_size("mha_13b_b96_ctx2048_mixed", samples=[0, 95])
