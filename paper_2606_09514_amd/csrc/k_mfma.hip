@@ -1,23 +1,27 @@
-// MFMA path of the routed projections (gfx950, bf16 weights), used when a
-// launch has more routed rows than the GEMV stages in one pass: the
-// projection is then a real dense contraction over the routed rows.
+// MFMA path of the routed projections (gfx950, bf16 weights), used for
+// batches of more than four sequences: the projection is then a real dense
+// contraction over the routed rows.
 //
-//  prep_kernel  writes the routed rows as compact bf16 rows XB[i] (row i of
-//               the launch is sequence idx[i]): RMSNorm and gain folded in
+//  prep_kernel  writes the routed rows as bf16 in MFMA operand order (row i
+//               of the launch is sequence idx[i]): RMSNorm and gain folded in
 //               (PRO_RMSNORM), the router context built from the pool's split
 //               sums (PRO_POOL), or a plain conversion (PRO_NONE).
 //  mfma_kernel  Y = W XB^T with v_mfma_f32_16x16x32_bf16 (fp32 accumulate).
-//               A workgroup owns 16 weight rows (or 16 two-row units) and all
-//               routed rows; its four wavefronts take a quarter of K each and
-//               are reduced through LDS, then the same fused epilogues as the
-//               GEMV path run on the finished sums.
+//               A workgroup owns RT 16-row weight tiles (16 RT rows, or 8 RT
+//               two-row units) and all routed rows; its four wavefronts take
+//               a quarter of K each, their sums are reduced through LDS one
+//               epilogue group at a time, and the fused epilogues of the GEMV
+//               path run on the finished sums.
 //
 // Operand layouts of v_mfma_f32_16x16x32_bf16 (checked on the device):
 //   A[i][k] (16 x 32): lane i + 16 (k / 8), element k % 8
 //   B[k][j] (32 x 16): lane j + 16 (k / 8), element k % 8
 //   D[i][j] (16 x 16): lane j + 16 (i / 4), element i % 4
-// so one 16-byte load per lane fetches an A tile row segment from the
-// row-major weights and a B tile from a compact activation row.
+// One 16-byte load per lane fetches an A tile segment from the row-major
+// weights (16 rows x 64 bytes).  The activations are small and re-read by
+// every workgroup, so they are stored in B-operand order: the B tile of
+// column tile c and k-step s is 1 KB at ((c * K/32 + s) * 64 + lane) * 8
+// elements, one contiguous load per wavefront.
 #include "buddy_internal.h"
 #include "epilogue.h"
 
@@ -27,6 +31,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kMfmaMaxTiles = 8;   // 16-row column tiles of routed rows per pass
+
 
 // ----------------------------------------------------------------- prep
 
@@ -38,7 +43,6 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
     if (i >= n) return;
     const int b = row_seq(g.rows, i);
     const int K = g.K, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    bf16_t* out = g.XB + (size_t)i * g.ldxb;
     float inv = 1.f;
     if (PRO == PRO_RMSNORM) {
         const float* x = g.X + (size_t)b * g.ldx;
@@ -89,48 +93,55 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
         o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
         o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
         o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
-        *reinterpret_cast<uint4*>(out + k) = o;
+        // B-operand order: tile i / 16, k-step k / 32, lane (i % 16) + 16 (k / 8 % 4)
+        const size_t frag = ((size_t)(i >> 4) * (K >> 5) + (k >> 5)) * 64 + (i & 15) + 16 * ((k >> 3) & 3);
+        *reinterpret_cast<uint4*>(g.XB + frag * 8) = o;
     }
 }
 
 // ----------------------------------------------------------------- MFMA
 
-template <int EPI, int NT>
+// k-steps per load round: all loads of a round are issued before its MFMAs
+__host__ __device__ constexpr int mfma_round(int rt, int nt) {
+    return 16 / (rt + nt) < 1 ? 1 : 16 / (rt + nt) > 8 ? 8 : 16 / (rt + nt);
+}
+
+template <int EPI, int NT, int RT>
 __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_host) {
     constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
-    constexpr int RT = kPaired ? 2 : 1;       // weight row tiles per wavefront
-    __shared__ float s_red[4][RT][16][NT * 16];
+    constexpr int GT = kPaired ? 2 : 1;       // weight tiles per epilogue group
+    constexpr int NG = RT / GT;               // epilogue groups (16 units or rows each)
+    constexpr int U = mfma_round(RT, NT);
+    __shared__ float s_red[4][GT][16][NT * 16];
     const int n = n_host >= 0 ? n_host : *g.rows.cnt;
     if (n <= 0) return;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int K = g.K;
-    const int ks = K / 4;                     // this wavefront's K-slice (K % 128 == 0)
-    const int kbeg = wave * ks + 8 * (lane >> 4);
-    const int t0 = blockIdx.x * 16;           // first unit (two-row kinds) or row
+    const int S = K >> 5;                     // k-steps of a row
+    const int sw = S >> 2;                    // k-steps of a wavefront (K % 128 == 0)
+    const int u0 = blockIdx.x * 16 * NG;      // first unit (two-row kinds) or row
 
-    // A rows of this lane (lane % 16 within the tile); past the end the last
-    // valid unit is read and its results are discarded
-    const int u = min(t0 + (lane & 15), units - 1);
-    int arow[RT];
-    if (kPaired) {
-        int r0, r1;
-        unit_rows<EPI>(g, u, r0, r1);
-        arow[0] = r0;
-        arow[RT - 1] = r1;
-    } else {
-        arow[0] = u;
-    }
+    // A rows of this lane (lane % 16 within each tile); past the end the
+    // last valid unit is read and its sums are discarded
     const bf16_t* Ap[RT];
 #pragma unroll
-    for (int t = 0; t < RT; ++t) Ap[t] = (const bf16_t*)g.W + (size_t)arow[t] * K + kbeg;
+    for (int q = 0; q < NG; ++q) {
+        const int u = min(u0 + 16 * q + (lane & 15), units - 1);
+        int r0 = u, r1 = u;
+        if (kPaired) unit_rows<EPI>(g, u, r0, r1);
+        Ap[q] = (const bf16_t*)g.W + (size_t)r0 * K + wave * (K >> 2) + 8 * (lane >> 4);
+        if (kPaired) Ap[NG + q] = (const bf16_t*)g.W + (size_t)r1 * K + wave * (K >> 2) + 8 * (lane >> 4);
+    }
 
     for (int j0 = 0; j0 < n; j0 += NT * 16) {   // column groups of NT tiles
+        // tiles past the last one re-read the last tile and their sums are
+        // discarded: the load rounds stay branch-free
         const int nct = min(NT, (n - j0 + 15) / 16);
         const bf16_t* Bp[NT];
 #pragma unroll
         for (int c = 0; c < NT; ++c)
-            Bp[c] = g.XB + (size_t)(j0 + min(c, nct - 1) * 16 + (lane & 15)) * g.ldxb + kbeg;
+            Bp[c] = g.XB + (((size_t)((j0 >> 4) + min(c, nct - 1)) * S + wave * sw) * 64 + lane) * 8;
 
         f32x4_t acc[RT][NT];
 #pragma unroll
@@ -138,64 +149,111 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
 #pragma unroll
             for (int c = 0; c < NT; ++c) acc[t][c] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-#pragma unroll 2
-        for (int k = 0; k < ks; k += 32) {
+        int s = 0;
+        for (; s + U <= sw; s += U) {
+            bf16x8_t a[U][RT], bv[U][NT];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+#pragma unroll
+                for (int t = 0; t < RT; ++t)
+                    a[u][t] = *reinterpret_cast<const bf16x8_t*>(Ap[t] + 32 * (s + u));
+#pragma unroll
+                for (int c = 0; c < NT; ++c)
+                    bv[u][c] = *reinterpret_cast<const bf16x8_t*>(Bp[c] + 512 * (s + u));
+            }
+            __builtin_amdgcn_sched_barrier(0);   // keep every load of the round ahead
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int t = 0; t < RT; ++t)
+#pragma unroll
+                    for (int c = 0; c < NT; ++c)
+                        acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][t], bv[u][c],
+                                                                            acc[t][c], 0, 0, 0);
+        }
+        for (; s < sw; ++s) {
             bf16x8_t a[RT], bv[NT];
 #pragma unroll
-            for (int t = 0; t < RT; ++t) a[t] = *reinterpret_cast<const bf16x8_t*>(Ap[t] + k);
+            for (int t = 0; t < RT; ++t) a[t] = *reinterpret_cast<const bf16x8_t*>(Ap[t] + 32 * s);
 #pragma unroll
-            for (int c = 0; c < NT; ++c)
-                if (c < nct) bv[c] = *reinterpret_cast<const bf16x8_t*>(Bp[c] + k);
+            for (int c = 0; c < NT; ++c) bv[c] = *reinterpret_cast<const bf16x8_t*>(Bp[c] + 512 * s);
 #pragma unroll
             for (int t = 0; t < RT; ++t)
 #pragma unroll
                 for (int c = 0; c < NT; ++c)
-                    if (c < nct)
-                        acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[t], bv[c], acc[t][c],
-                                                                            0, 0, 0);
+                    acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[t], bv[c], acc[t][c], 0, 0, 0);
         }
 
-        // reduce the four K-slices through LDS
-        if (j0 > 0) __syncthreads();   // the previous group's epilogue is done with s_red
-#pragma unroll
-        for (int t = 0; t < RT; ++t)
-#pragma unroll
-            for (int c = 0; c < NT; ++c)
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    s_red[wave][t][4 * (lane >> 4) + v][c * 16 + (lane & 15)] = acc[t][c][v];
-        __syncthreads();
-
+        // per epilogue group: reduce the four K-slices through LDS, then the
+        // epilogue on the finished sums (wavefront order fixed: deterministic)
         const int ncols = min(NT * 16, n - j0);
-        for (int p = tid; p < 16 * ncols; p += 256) {
-            const int il = p / ncols, j = p - il * ncols;
-            const int uu = t0 + il;
-            if (uu >= units) continue;
-            const int b = row_seq(g.rows, j0 + j);
-            const float v0 = (s_red[0][0][il][j] + s_red[1][0][il][j]) +
-                             (s_red[2][0][il][j] + s_red[3][0][il][j]);
-            if (kPaired) {
-                const float v1 = (s_red[0][RT - 1][il][j] + s_red[1][RT - 1][il][j]) +
-                                 (s_red[2][RT - 1][il][j] + s_red[3][RT - 1][il][j]);
-                int r0, r1;
-                unit_rows<EPI>(g, uu, r0, r1);
-                epilogue<bf16_t, EPI>(g, b, uu, r0, r1, v0, v1);
-            } else {
-                epilogue1<bf16_t, EPI>(g, b, uu, v0);
+#pragma unroll
+        for (int q = 0; q < NG; ++q) {
+            __syncthreads();   // the previous group's epilogue is done with s_red
+#pragma unroll
+            for (int t = 0; t < GT; ++t)
+#pragma unroll
+                for (int c = 0; c < NT; ++c)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        s_red[wave][t][4 * (lane >> 4) + v][c * 16 + (lane & 15)] = acc[q + t * NG][c][v];
+            __syncthreads();
+            for (int p = tid; p < 16 * ncols; p += 256) {
+                const int il = p / ncols, j = p - il * ncols;
+                const int uu = u0 + 16 * q + il;
+                if (uu >= units) continue;
+                const int b = row_seq(g.rows, j0 + j);
+                const float v0 = (s_red[0][0][il][j] + s_red[1][0][il][j]) +
+                                 (s_red[2][0][il][j] + s_red[3][0][il][j]);
+                if (kPaired) {
+                    const float v1 = (s_red[0][GT - 1][il][j] + s_red[1][GT - 1][il][j]) +
+                                     (s_red[2][GT - 1][il][j] + s_red[3][GT - 1][il][j]);
+                    int r0, r1;
+                    unit_rows<EPI>(g, uu, r0, r1);
+                    epilogue<bf16_t, EPI>(g, b, uu, r0, r1, v0, v1);
+                } else {
+                    epilogue1<bf16_t, EPI>(g, b, uu, v0);
+                }
             }
         }
     }
 }
 
+// Workgroups below which a launch takes smaller weight tiles per workgroup
+constexpr int kMfmaMinGrid = 384;
+
+template <int EPI, int RT>
+static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, hipStream_t s) {
+    constexpr int per = 16 * (EPI == EPI_SWIGLU || EPI == EPI_QKV ? RT / 2 : RT);
+    const int grid = (units + per - 1) / per;
+    const int tiles = (g.rows.n_max + 15) / 16;
+    if (tiles <= 1) mfma_kernel<EPI, 1, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+    else if (tiles <= 2) mfma_kernel<EPI, 2, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+    else if (tiles <= 3) mfma_kernel<EPI, 3, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+    else if (tiles <= 4) mfma_kernel<EPI, 4, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+    else if (tiles <= 5) mfma_kernel<EPI, 5, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+    else if (tiles <= 6) mfma_kernel<EPI, 6, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+    else if constexpr (RT <= 2) {
+        if (tiles <= 7) mfma_kernel<EPI, 7, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+        else mfma_kernel<EPI, kMfmaMaxTiles, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+    }
+    return hipGetLastError();
+}
+
+// Largest weight tile per workgroup that still gives kMfmaMinGrid workgroups
+// (four tiles only up to six column tiles: beyond, their registers would
+// halve the occupancy)
 template <int EPI>
 static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, hipStream_t s) {
-    const int grid = (units + 15) / 16;
-    const int tiles = (g.rows.n_max + 15) / 16;
-    if (tiles <= 1) mfma_kernel<EPI, 1><<<grid, 256, 0, s>>>(g, units, n_host);
-    else if (tiles <= 2) mfma_kernel<EPI, 2><<<grid, 256, 0, s>>>(g, units, n_host);
-    else if (tiles <= 4) mfma_kernel<EPI, 4><<<grid, 256, 0, s>>>(g, units, n_host);
-    else mfma_kernel<EPI, kMfmaMaxTiles><<<grid, 256, 0, s>>>(g, units, n_host);
-    return hipGetLastError();
+    const bool wide = g.rows.n_max <= 16 * 6;
+    if constexpr (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+        if (wide && units / 32 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, s);
+        return launch_mfma_nt<EPI, 2>(g, units, n_host, s);
+    } else {
+        if (wide && units / 64 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, s);
+        if (units / 32 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 2>(g, units, n_host, s);
+        return launch_mfma_nt<EPI, 1>(g, units, n_host, s);
+    }
 }
 
 hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s) {
