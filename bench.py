@@ -59,35 +59,6 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-class HipEvents:
-    """Raw hipEvent_t handles for the library's timing hook."""
-
-    def __init__(self):
-        self.h = C.CDLL("libamdhip64.so")
-        self.h.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
-        self.h.hipEventSynchronize.argtypes = [C.c_void_p]
-        self.h.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
-        self.h.hipEventDestroy.argtypes = [C.c_void_p]
-
-    def create(self, n):
-        out = []
-        for _ in range(n):
-            e = C.c_void_p()
-            assert self.h.hipEventCreate(C.byref(e)) == 0
-            out.append(e.value)
-        return out
-
-    def elapsed_ms(self, a, b):
-        assert self.h.hipEventSynchronize(C.c_void_p(b)) == 0
-        ms = C.c_float()
-        assert self.h.hipEventElapsedTime(C.byref(ms), C.c_void_p(a), C.c_void_p(b)) == 0
-        return ms.value
-
-    def destroy(self, evs):
-        for e in evs:
-            self.h.hipEventDestroy(C.c_void_p(e))
-
-
 def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer):
     import torch
     from paper_2606_09514_amd import costmodel
@@ -209,7 +180,7 @@ def main():
     model = blib.Model(cfg, W, max_batch=w.batch)
     model.set_launch_policy({"auto": blib.LAUNCH_AUTO, "device": blib.LAUNCH_DEVICE_ROUTED,
                              "host": blib.LAUNCH_HOST_ROUTED}[args.policy])
-    hip = HipEvents()
+    hip = blib.HipEvents()
 
     runs = {}
     for i, k in enumerate(budgets if not w.mixed else [None]):

@@ -191,8 +191,12 @@ typedef enum {
 } buddy_kernel;
 
 /* Measurement hook.  For the next n calls of buddy_decode_step on this
- * handle, call i records start[i] on its stream right before the launch of
- * `kernel` in block `layer` and stop[i] right after it.  start and stop are
+ * handle, call i times `kernel` in block `layer`: start[i] and stop[i] are
+ * recorded at the dispatch begin and end of that kernel's main launch (the
+ * projection itself, not the activation staging of the batched path; the
+ * attention score kernel, not the chunk merge), the interval a kernel trace
+ * reports.  If the block does not run, both are recorded back to back on the
+ * stream at that point of the step.  start and stop are
  * arrays of n hipEvent_t handles that the caller created and keeps alive
  * until the calls have run; the handle copies the arrays.  n = 0 turns the
  * hook off.  Errors: BUDDY_EINVAL for a bad kernel, layer or n < 0, or null

@@ -15,6 +15,8 @@
 
 using namespace buddy;
 
+thread_local LaunchEvents buddy::tl_launch_events = {nullptr, nullptr};
+
 struct buddy_model {
     Model M;
 };
@@ -116,10 +118,19 @@ bool timed(const Model& M, int kind, int l) {
     return t.n > 0 && t.next < t.n && t.kernel == kind && t.layer == l;
 }
 
+// Arms the events of the timed kernel for its main launch; at the stop mark,
+// events that no launch took (no kernel of that kind ran) are recorded here.
 hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
     if (!timed(M, kind, l)) return hipSuccess;
     const TimingHook& t = M.timing;
-    return hipEventRecord(stop ? t.stop[t.next] : t.start[t.next], s);
+    if (!stop) {
+        tl_launch_events = {t.start[t.next], t.stop[t.next]};
+        return hipSuccess;
+    }
+    if (!tl_launch_events.start) return hipSuccess;
+    tl_launch_events = {nullptr, nullptr};
+    hipError_t e = hipEventRecord(t.start[t.next], s);
+    return e != hipSuccess ? e : hipEventRecord(t.stop[t.next], s);
 }
 
 buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows rows, int batch,
@@ -413,6 +424,7 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     const buddy_config& c = M.cfg;
     if (B > c.max_batch) return BUDDY_ECAPACITY;
     if (!hidden || !pos || (!k && !route_override)) return BUDDY_EINVAL;
+    tl_launch_events = {nullptr, nullptr};   // nothing armed by a failed earlier step
     int max_pos;
     buddy_status st = check_step_host(M, pos, B, &max_pos);
     if (st != BUDDY_OK) return st;
@@ -456,7 +468,14 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
         int n_max = B;
         if (host_routed) {
             n_max = M.h_cnt[l - 1];
-            if (n_max == 0) continue;
+            if (n_max == 0) {
+                // a timed kernel of a block that does not run: an empty interval
+                if (M.timing.n > 0 && M.timing.next < M.timing.n && M.timing.layer == l &&
+                    ((e = hipEventRecord(M.timing.start[M.timing.next], s)) != hipSuccess ||
+                     (e = hipEventRecord(M.timing.stop[M.timing.next], s)) != hipSuccess))
+                    return fail_device(M, e, "timing events");
+                continue;
+            }
         }
         // every sequence routed (known on the host): the rows are the batch in order
         const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), n_max,

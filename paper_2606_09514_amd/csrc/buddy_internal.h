@@ -4,6 +4,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 #include "../../include/buddy.h"
@@ -107,6 +108,25 @@ struct TimingHook {
     hipEvent_t* start;
     hipEvent_t* stop;
 };
+
+// Events that the next main kernel launch (a projection, the MFMA product,
+// an attention score kernel) records at its own dispatch begin and end, the
+// interval a profiler's kernel trace reports; armed by the timing hook for
+// one launch and cleared by that launch.
+struct LaunchEvents { hipEvent_t start, stop; };
+extern thread_local LaunchEvents tl_launch_events;
+
+template <typename... KArgs, typename... Args>
+inline void launch_main(void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_t lds,
+                        hipStream_t s, Args... args) {
+    LaunchEvents& ev = tl_launch_events;
+    if (ev.start) {
+        hipExtLaunchKernelGGL(kernel, grid, block, lds, s, ev.start, ev.stop, 0, args...);
+        ev.start = ev.stop = nullptr;
+    } else {
+        hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+    }
+}
 
 // Largest batch for which the automatic launch policy waits for the route
 // and launches only the blocks in use (at larger batches nearly every block

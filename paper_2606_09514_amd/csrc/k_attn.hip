@@ -8,13 +8,19 @@
 // weighted sum of V rows, then writes the chunk's (max, sum, acc) partial.
 // A second kernel merges the chunk partials of (b, g) in chunk order and
 // writes o[b] for the group's heads (no cross-workgroup synchronisation
-// inside a kernel: device-wide fences are costly across the XCDs).
-// Zero-filled rows of skipped steps are ordinary cache rows here (logit 0,
-// value 0).
+// inside a kernel: device-wide fences are costly across the XCDs); with a
+// single chunk the first kernel writes o itself.  Zero-filled rows of skipped
+// steps are ordinary cache rows here (logit 0, value 0).
 //
-// Lane layout: a cache row of hd elements is read by hd/V lanes with 16-byte
-// loads (V = 8 bf16 or 4 fp32), so a wavefront covers 64/(hd/V) rows per
-// pass and the row dot products finish with a short xor-shuffle tree.
+// Two score kernels:
+//  attn_kernel       vector ALUs: a cache row of hd elements is read by hd/V
+//                    lanes with 16-byte loads (V = 8 bf16 or 4 fp32), so a
+//                    wavefront covers 64/(hd/V) rows per pass and the row dot
+//                    products finish with a short DPP / shuffle tree.  Used
+//                    for fp32 caches, head_dim 64 and groups of one or two.
+//  attn_mfma_kernel  bf16, head_dim 128, three to eight query heads per KV
+//                    head: the scores of 16 rows against the group are one
+//                    MFMA product, P V stays on the vector ALUs.
 #include "buddy_internal.h"
 
 namespace buddy {
@@ -130,31 +136,30 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
                 sc[p][h] = live ? d : -INFINITY;
             }
         }
-        // one online-softmax update per block and head
+        // one online-softmax update per block and head, branch-free: a
+        // padded head (h >= G) has q = 0 and is never written, and with every
+        // score of the block masked mn stays -inf and scale_of gives 0
+        float vf[kAttnPasses][V];
+#pragma unroll
+        for (int p = 0; p < kAttnPasses; ++p) unpack<T>(vr[p], vf[p]);
 #pragma unroll
         for (int h = 0; h < GM; ++h) {
-            if (h < G) {
-                float mx = sc[0][h];
+            float mx = sc[0][h];
 #pragma unroll
-                for (int p = 1; p < kAttnPasses; ++p) mx = fmaxf(mx, sc[p][h]);
-                const float mn = fmaxf(m[h], mx);
-                if (mn != -INFINITY) {
-                    const float al = scale_of(m[h], mn);
-                    l[h] *= al;
+            for (int p = 1; p < kAttnPasses; ++p) mx = fmaxf(mx, sc[p][h]);
+            const float mn = fmaxf(m[h], mx);
+            const float al = scale_of(m[h], mn);
+            l[h] *= al;
 #pragma unroll
-                    for (int e = 0; e < V; ++e) acc[h][e] *= al;
+            for (int e = 0; e < V; ++e) acc[h][e] *= al;
 #pragma unroll
-                    for (int p = 0; p < kAttnPasses; ++p) {
-                        const float pw = scale_of(sc[p][h], mn);
-                        float vf[V];
-                        unpack<T>(vr[p], vf);
-                        l[h] += pw;
+            for (int p = 0; p < kAttnPasses; ++p) {
+                const float pw = scale_of(sc[p][h], mn);
+                l[h] += pw;
 #pragma unroll
-                        for (int e = 0; e < V; ++e) acc[h][e] += pw * vf[e];
-                    }
-                    m[h] = mn;
-                }
+                for (int e = 0; e < V; ++e) acc[h][e] += pw * vf[p][e];
             }
+            m[h] = mn;
         }
     }
 
@@ -162,7 +167,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int o = lpr; o < kWave; o <<= 1) {
 #pragma unroll
         for (int h = 0; h < GM; ++h) {
-            if (h < G) {
+            {
                 const float mo = __shfl_xor(m[h], o, kWave);
                 const float lo = __shfl_xor(l[h], o, kWave);
                 const float mn = fmaxf(m[h], mo);
@@ -204,9 +209,176 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             L += s_acc[w][h][a.hd + 1] * sw;
             A += s_acc[w][h][e] * sw;
         }
-        float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
-        pp[e] = A;
-        if (e == 0) { pp[a.hd] = M; pp[a.hd + 1] = L; }
+        if (a.chunks == 1) {
+            a.o[((size_t)b * a.nq + g * G + h) * a.hd + e] = A / L;
+        } else {
+            float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
+            pp[e] = A;
+            if (e == 0) { pp[a.hd] = M; pp[a.hd + 1] = L; }
+        }
+    }
+}
+
+// Grouped-query attention for bf16 caches with head_dim 128 and three to
+// kMaxGroup query heads per KV head: the scores of a 16-row slab against the
+// group's heads are one 16 x 16 x 128 MFMA product (v_mfma_f32_16x16x32_bf16,
+// K rows as the A operand, the queries split into bf16 high and low parts as
+// the B operand, so the scores keep about 16 bits of the fp32 query), the
+// online softmax runs on the MFMA result, and P V runs on the vector ALUs
+// with each lane owning two output columns of every head.
+//   D[i][j] (16 x 16): lane j + 16 (i / 4), element i % 4
+//   A[i][k]: lane i + 16 (k / 8), element k % 8;  B[k][j]: lane j + 16 (k / 8)
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t bf16_bits(float x) { return (uint32_t)f2bf(x); }
+
+template <int GM>
+__global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
+    constexpr int HD = 128, KS = HD / 32;
+    __shared__ float s_p[4][16][16];          // per wave: p[head][slab row]
+    __shared__ float s_al[4][16];             // per wave: rescale of each head
+    __shared__ float s_acc[4][GM][HD + 2];
+    const int i = blockIdx.z;
+    if (!a.rows.exact && i >= *a.rows.cnt) return;
+    const int b = row_seq(a.rows, i);
+    const int g = blockIdx.y, c = blockIdx.x;
+    const int pos = seq_pos(a.pos, a.pos_u, b);
+    const int G = a.nq / a.nkv;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int j0 = c * a.chunk_len;
+    const int j1 = min(j0 + a.chunk_len, pos + 1);
+    const size_t base = ((size_t)b * a.nkv + g) * a.T * HD;
+    const bf16_t* Kb = (const bf16_t*)a.kc + base;
+    const uint32_t* Vb = (const uint32_t*)((const bf16_t*)a.vc + base);   // bf16 pairs
+
+    // B operand: queries of the group, scaled so that exp2 of a score is the
+    // softmax weight, as bf16 high + low parts; heads past G are zero
+    bf16x8_t qh[KS], ql[KS];
+    {
+        const int h = lane & 15, q8 = 8 * (lane >> 4);
+        const float qs = 1.4426950408889634f / sqrtf((float)HD);
+        const float* qp = a.q + ((size_t)b * a.nq + g * G + min(h, G - 1)) * HD + q8;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            const float4 x0 = *reinterpret_cast<const float4*>(qp + 32 * s);
+            const float4 x1 = *reinterpret_cast<const float4*>(qp + 32 * s + 4);
+            const float xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+            uint32_t hi[4], lo[4];
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const float v0 = h < G ? xv[e] * qs : 0.f, v1 = h < G ? xv[e + 1] * qs : 0.f;
+                const uint32_t h0 = bf16_bits(v0), h1 = bf16_bits(v1);
+                const float r0 = v0 - __uint_as_float(h0 << 16), r1 = v1 - __uint_as_float(h1 << 16);
+                hi[e / 2] = h0 | (h1 << 16);
+                lo[e / 2] = bf16_bits(r0) | (bf16_bits(r1) << 16);
+            }
+            qh[s] = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+            ql[s] = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+        }
+    }
+
+    float mrun = -INFINITY;     // running max of head lane % 16 (same in its four lanes)
+    float lrun = 0.f;           // running sum over this lane's rows of that head
+    float acc[GM][2];           // columns 2 lane, 2 lane + 1 of every head
+#pragma unroll
+    for (int h = 0; h < GM; ++h) acc[h][0] = acc[h][1] = 0.f;
+
+    for (int jb = j0 + 16 * wave; jb < j1; jb += 64) {
+        // K fragments of the slab (rows clamped to a valid row, masked below)
+        // and its V rows, all issued before any arithmetic
+        bf16x8_t kf[KS];
+        const int jr = min(jb + (lane & 15), j1 - 1);
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            kf[s] = *reinterpret_cast<const bf16x8_t*>(Kb + (size_t)jr * HD + 32 * s + 8 * (lane >> 4));
+        uint32_t vw[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) vw[r] = Vb[(size_t)min(jb + r, j1 - 1) * (HD / 2) + lane];
+
+        f32x4_t d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qh[s], d, 0, 0, 0);
+            d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], ql[s], d, 0, 0, 0);
+        }
+        // rows of this lane: jb + 4 (lane / 16) + v; head lane % 16
+        float sc[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sc[v] = jb + 4 * (lane >> 4) + v < j1 ? d[v] : -INFINITY;
+        float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        const float mn = fmaxf(mrun, mx);
+        const float al = scale_of(mrun, mn);
+        float p[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) p[v] = scale_of(sc[v], mn);
+        lrun = lrun * al + ((p[0] + p[1]) + (p[2] + p[3]));
+        mrun = mn;
+        *reinterpret_cast<float4*>(&s_p[wave][lane & 15][4 * (lane >> 4)]) = make_float4(p[0], p[1], p[2], p[3]);
+        if (lane < 16) s_al[wave][lane] = al;
+        __builtin_amdgcn_wave_barrier();
+
+        float vf[16][2];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            vf[r][0] = __uint_as_float(vw[r] << 16);
+            vf[r][1] = __uint_as_float(vw[r] & 0xffff0000u);
+        }
+#pragma unroll
+        for (int h = 0; h < GM; ++h) {
+            const float sa = s_al[wave][h];
+            acc[h][0] *= sa;
+            acc[h][1] *= sa;
+#pragma unroll
+            for (int rq = 0; rq < 4; ++rq) {
+                const float4 p4 = *reinterpret_cast<const float4*>(&s_p[wave][h][4 * rq]);
+                const float pv[4] = {p4.x, p4.y, p4.z, p4.w};
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    acc[h][0] += pv[v] * vf[4 * rq + v][0];
+                    acc[h][1] += pv[v] * vf[4 * rq + v][1];
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();   // s_p / s_al reads done before the next slab's writes
+    }
+
+    // per wave: total of each head's running sum over its four lanes
+    lrun += __shfl_xor(lrun, 16, kWave);
+    lrun += __shfl_xor(lrun, 32, kWave);
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
+        s_acc[wave][h][2 * lane] = acc[h][0];
+        s_acc[wave][h][2 * lane + 1] = acc[h][1];
+    }
+    if (lane < GM) {
+        s_acc[wave][lane][HD] = mrun;
+        s_acc[wave][lane][HD + 1] = lrun;
+    }
+    __syncthreads();
+
+    // merge the four wavefronts and write this chunk's partial
+    const size_t pstride = (size_t)HD + 2;
+    for (int t = tid; t < G * HD; t += 256) {
+        const int h = t / HD, e = t % HD;
+        float M = -INFINITY;
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, s_acc[w][h][HD]);
+        float L = 0.f, A = 0.f;
+        for (int w = 0; w < 4; ++w) {
+            const float sw = scale_of(s_acc[w][h][HD], M);
+            L += s_acc[w][h][HD + 1] * sw;
+            A += s_acc[w][h][e] * sw;
+        }
+        if (a.chunks == 1) {
+            a.o[((size_t)b * a.nq + g * G + h) * HD + e] = A / L;
+        } else {
+            float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
+            pp[e] = A;
+            if (e == 0) { pp[HD] = M; pp[HD + 1] = L; }
+        }
     }
 }
 
@@ -246,7 +418,10 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
     }
 }
 
+static bool attn_uses_mfma(int dtype, int hd, int G) { return dtype == BUDDY_BF16 && hd == 128 && G >= 3 && G <= kMaxGroup; }
+
 int attention_rows_per_wg(int dtype, int hd, int G) {
+    if (attn_uses_mfma(dtype, hd, G)) return 64;
     // G rounded up to the register class the launcher picks
     const int gm = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8;
     return dtype == BUDDY_BF16 ? attn_rows_per_wg<bf16_t>(hd, gm) : attn_rows_per_wg<float>(hd, gm);
@@ -256,27 +431,29 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     dim3 grid(a.chunks, a.nkv, a.rows.n_max);
     const int G = a.nq / a.nkv;   // query heads per KV head, held in registers
     // lanes per cache row: hd / 8 (bf16) or hd / 4 (fp32); head_dim is 64 or 128
-    if (dtype == BUDDY_BF16) {
+    if (attn_uses_mfma(dtype, a.hd, G)) {
+        if (G <= 4) launch_main(attn_mfma_kernel<4>, grid, dim3(256), 0, s, a);
+        else launch_main(attn_mfma_kernel<kMaxGroup>, grid, dim3(256), 0, s, a);
+    } else if (dtype == BUDDY_BF16) {
         if (a.hd == 128) {
-            if (G == 1) attn_kernel<bf16_t, 1, 16><<<grid, 256, 0, s>>>(a);
-            else if (G == 2) attn_kernel<bf16_t, 2, 16><<<grid, 256, 0, s>>>(a);
-            else if (G <= 4) attn_kernel<bf16_t, 4, 16><<<grid, 256, 0, s>>>(a);
-            else attn_kernel<bf16_t, 8, 16><<<grid, 256, 0, s>>>(a);
+            if (G == 1) launch_main(attn_kernel<bf16_t, 1, 16>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_kernel<bf16_t, 2, 16>, grid, dim3(256), 0, s, a);
         } else {
-            if (G <= 2) attn_kernel<bf16_t, 2, 8><<<grid, 256, 0, s>>>(a);
-            else attn_kernel<bf16_t, 8, 8><<<grid, 256, 0, s>>>(a);
+            if (G <= 2) launch_main(attn_kernel<bf16_t, 2, 8>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_kernel<bf16_t, 8, 8>, grid, dim3(256), 0, s, a);
         }
     } else {
         if (a.hd == 128) {
-            if (G <= 2) attn_kernel<float, 2, 32><<<grid, 256, 0, s>>>(a);
-            else attn_kernel<float, 8, 32><<<grid, 256, 0, s>>>(a);
+            if (G <= 2) launch_main(attn_kernel<float, 2, 32>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_kernel<float, 8, 32>, grid, dim3(256), 0, s, a);
         } else {
-            if (G <= 2) attn_kernel<float, 2, 16><<<grid, 256, 0, s>>>(a);
-            else attn_kernel<float, 8, 16><<<grid, 256, 0, s>>>(a);
+            if (G <= 2) launch_main(attn_kernel<float, 2, 16>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_kernel<float, 8, 16>, grid, dim3(256), 0, s, a);
         }
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (a.chunks == 1) return hipSuccess;   // the score kernel wrote o
     attn_combine_kernel<<<dim3(a.nq, a.rows.n_max), 256, 0, s>>>(a);
     return hipGetLastError();
 }

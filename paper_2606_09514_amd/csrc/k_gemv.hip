@@ -266,8 +266,8 @@ static hipError_t launch_one(const GemvArgs& g, int units, int n_host, hipStream
     const int per_wg = (EPI == EPI_SWIGLU || EPI == EPI_QKV) ? P / 2 : P / S;
     const int items = (EPI == EPI_SWIGLU || EPI == EPI_QKV) ? units : g.N;
     const int grid = (items + per_wg - 1) / per_wg;
-    gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI><<<grid, 64 * P, lds, s>>>(
-        g, units, nsteps, spw, n_host);
+    launch_main(gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI>, dim3(grid), dim3(64 * P),
+                (uint32_t)lds, s, g, units, nsteps, spw, n_host);
     return hipGetLastError();
 }
 

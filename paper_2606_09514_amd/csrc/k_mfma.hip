@@ -227,15 +227,15 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, hipSt
     constexpr int per = 16 * (EPI == EPI_SWIGLU || EPI == EPI_QKV ? RT / 2 : RT);
     const int grid = (units + per - 1) / per;
     const int tiles = (g.rows.n_max + 15) / 16;
-    if (tiles <= 1) mfma_kernel<EPI, 1, RT><<<grid, 256, 0, s>>>(g, units, n_host);
-    else if (tiles <= 2) mfma_kernel<EPI, 2, RT><<<grid, 256, 0, s>>>(g, units, n_host);
-    else if (tiles <= 3) mfma_kernel<EPI, 3, RT><<<grid, 256, 0, s>>>(g, units, n_host);
-    else if (tiles <= 4) mfma_kernel<EPI, 4, RT><<<grid, 256, 0, s>>>(g, units, n_host);
-    else if (tiles <= 5) mfma_kernel<EPI, 5, RT><<<grid, 256, 0, s>>>(g, units, n_host);
-    else if (tiles <= 6) mfma_kernel<EPI, 6, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+    if (tiles <= 1) launch_main(mfma_kernel<EPI, 1, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
+    else if (tiles <= 2) launch_main(mfma_kernel<EPI, 2, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
+    else if (tiles <= 3) launch_main(mfma_kernel<EPI, 3, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
+    else if (tiles <= 4) launch_main(mfma_kernel<EPI, 4, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
+    else if (tiles <= 5) launch_main(mfma_kernel<EPI, 5, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
+    else if (tiles <= 6) launch_main(mfma_kernel<EPI, 6, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
     else if constexpr (RT <= 2) {
-        if (tiles <= 7) mfma_kernel<EPI, 7, RT><<<grid, 256, 0, s>>>(g, units, n_host);
-        else mfma_kernel<EPI, kMfmaMaxTiles, RT><<<grid, 256, 0, s>>>(g, units, n_host);
+        if (tiles <= 7) launch_main(mfma_kernel<EPI, 7, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
+        else launch_main(mfma_kernel<EPI, kMfmaMaxTiles, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
     }
     return hipGetLastError();
 }

@@ -215,3 +215,37 @@ class Model:
         if check:
             _raise(rc, self._h)
         return rc
+
+
+class HipEvents:
+    """Raw hipEvent_t handles for Model.set_timing_events (HIP runtime calls
+    through ctypes; the handles are plain ints)."""
+
+    def __init__(self):
+        self.h = C.CDLL("libamdhip64.so")
+        self.h.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.h.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.h.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.h.hipEventDestroy.argtypes = [C.c_void_p]
+
+    def create(self, n):
+        out = []
+        for _ in range(n):
+            e = C.c_void_p()
+            assert self.h.hipEventCreate(C.byref(e)) == 0
+            out.append(e.value)
+        return out
+
+    def elapsed_ms(self, a, b):
+        rc = self.h.hipEventSynchronize(C.c_void_p(b))
+        if rc != 0:
+            raise RuntimeError(f"hipEventSynchronize: HIP error {rc}")
+        ms = C.c_float()
+        rc = self.h.hipEventElapsedTime(C.byref(ms), C.c_void_p(a), C.c_void_p(b))
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime: HIP error {rc}")
+        return ms.value
+
+    def destroy(self, evs):
+        for e in evs:
+            self.h.hipEventDestroy(C.c_void_p(e))

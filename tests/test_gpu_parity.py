@@ -278,6 +278,36 @@ def test_launch_policies_agree_bitwise():
     assert outs[0] == outs[1]
 
 
+# ------------------------------------------------------- timing hook
+
+@pytest.mark.parametrize("B", [2, 40])
+def test_timing_hook_times_the_kernel(B):
+    """The timing hook's events bracket the timed kernel's own dispatch: a
+    positive interval for a kernel that runs (GEMV at B = 2, MFMA at B = 40;
+    the attention score kernel), a recorded pair for a block that does not
+    run, and the hook stops after n steps."""
+    P = Pair("tiny", "bf16", 40, B, seed=5, omega=0.1)
+    g = torch.Generator().manual_seed(6)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    dk, dv = P.upload(hk), P.upload(hv)
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=7).numpy()
+    hip = blib.HipEvents()
+    for kernel, layer, expect_run in ((blib.KERNEL_GATE_UP, 0, True),
+                                      (blib.KERNEL_ATTENTION, P.cfg["n_layers"] - 1, True),
+                                      (blib.KERNEL_DOWN, 1, False)):
+        st, sp = hip.create(2), hip.create(2)
+        P.gpu.set_timing_events(kernel, layer, st, sp)
+        for _ in range(3):   # the third step runs after the hook ran out
+            gpu_step(P, dk, dv, x, [20] * B, [0] * B)
+        ms = [hip.elapsed_ms(a, b) for a, b in zip(st, sp)]
+        hip.destroy(st + sp)
+        for v in ms:
+            assert np.isfinite(v) and v >= 0.0
+            if expect_run:
+                assert 0.0 < v < 50.0
+
+
 # --------------------------------------------- batched (MFMA) projections
 
 def one_step_all(P, hk, hv, pos, ks, x):
@@ -305,6 +335,42 @@ def test_batched_steps_mfma(B, policy):
     x = synth.hidden_inputs(B, P.cfg["d_model"], seed=24).numpy()
     rep = one_step_all(P, hk, hv, pos, ks, x)
     print(B, rep)
+
+
+# ------------------------------------- grouped-query attention on MFMA
+
+def gqa_shape(G):
+    """A small bf16 decoder with head_dim 128 and G query heads per KV head
+    (the MFMA score path of the attention kernel)."""
+    nkv = 2 if G < 8 else 1
+    return dict(n_layers=4, d_model=384, n_heads=G * nkv, n_kv_heads=nkv, head_dim=128,
+                d_ffn=512, dm_hidden=64, dm_act="silu", rope_theta=1e4, rms_eps=1e-5)
+
+
+@pytest.mark.parametrize("B", [1, 3, 7])
+@pytest.mark.parametrize("G", [3, 4, 8])
+def test_gqa_attention_mfma(G, B):
+    """Scores of 16-row slabs on MFMA (queries split into bf16 high and low
+    parts), softmax and P V on the vector ALUs.  Positions span one chunk
+    (direct output, no merge kernel), several chunks with ragged ends, and
+    rows zero-filled by skipped steps (the caches hold zeros at random
+    positions of the mid layers)."""
+    T = 700
+    P = Pair(gqa_shape(G), "bf16", T, B, seed=30 + G, omega=0.1)
+    g = torch.Generator().manual_seed(40 + G + B)
+    hk = torch.randn(P.shape5, generator=g).to(P.tdt)
+    hv = torch.randn(P.shape5, generator=g).to(P.tdt)
+    holes = torch.rand(P.shape5[:4], generator=g) < 0.2
+    holes[0] = False
+    hk[holes] = 0
+    hv[holes] = 0
+    hk, hv = synth.storage_numpy(hk), synth.storage_numpy(hv)
+    rng = np.random.default_rng(50 + G + B)
+    pos = ([699, 37, 300, 64, 63, 128, 500][:B] if B > 1 else [699])
+    ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=60 + G).numpy()
+    rep = one_step_all(P, hk, hv, pos, ks, x)
+    print(G, B, rep)
 
 
 def sampled_full_size(name, samples, seed=0):
