@@ -74,6 +74,11 @@ def lib():
                                      vp, vp, i32, i32, vp, vp, vp, vp, vp, dp,
                                      C.POINTER(C.c_int32)]
         L.orc_decode_seq.restype = C.c_int
+        L.orc_block_ex.argtypes = [C.POINTER(_Config), C.POINTER(_Layer), vp, vp, i32, vp, vp]
+        L.orc_decode_seq_ex.argtypes = [C.POINTER(_Config), C.POINTER(_Layer), C.POINTER(_DM),
+                                        vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, dp,
+                                        C.POINTER(C.c_int32)]
+        L.orc_decode_seq_ex.restype = C.c_int
         L.orc_num_threads.restype = C.c_int
         _lib = L
     return _lib
@@ -153,11 +158,14 @@ class Oracle:
         lib().orc_rope(C.byref(self._c), _ptr(x), int(pos))
         return x
 
-    def block(self, layer: int, kc, vc, pos: int, h):
+    def block(self, layer: int, kc, vc, pos: int, h, exec=None):
+        """exec: optional uint8 execution map [max_ctx] of this layer's cache
+        (positions with 0 are left out of the softmax)."""
         h = np.array(h, dtype=np.float64, copy=True)
-        lib().orc_block(C.byref(self._c), C.byref(self._layers[layer]),
-                        _ptr(_need(kc, self.sdt, "kc")), _ptr(_need(vc, self.sdt, "vc")),
-                        int(pos), _ptr(h))
+        ex = None if exec is None else _need(exec, np.uint8, "exec")
+        lib().orc_block_ex(C.byref(self._c), C.byref(self._layers[layer]),
+                           _ptr(_need(kc, self.sdt, "kc")), _ptr(_need(vc, self.sdt, "vc")),
+                           int(pos), _ptr(h), _ptr(ex))
         return h
 
     def pool(self, kc, vc, pos: int):
@@ -184,9 +192,11 @@ class Oracle:
         return m, margin.value
 
     # -- the whole step --------------------------------------------------
-    def decode_seq(self, kcs, vcs, pos: int, k: int, x, route=None):
+    def decode_seq(self, kcs, vcs, pos: int, k: int, x, route=None, execs=None):
         """One decode step of one sequence.  kcs/vcs: per-layer cache arrays
-        (modified in place).  Returns (h, mask, scores, margin, n_exec)."""
+        (modified in place); execs: optional per-layer uint8 execution maps
+        [max_ctx] for skipped-KV masking (modified in place).  Returns (h,
+        mask, scores, margin, n_exec)."""
         L = self.cfg["n_layers"]
         assert len(kcs) == L and len(vcs) == L
         kp = (C.c_void_p * L)(*[_need(a, self.sdt, "kc").ctypes.data for a in kcs])
@@ -201,10 +211,14 @@ class Oracle:
         if route is not None:
             r = np.ascontiguousarray(route, dtype=np.uint8)
             mask[:] = r
-        rc = lib().orc_decode_seq(C.byref(self._c), self._layers,
-                                  C.byref(self._dm) if self._dm is not None else None,
-                                  kp, vp, int(pos), int(k), _ptr(r), _ptr(x), _ptr(h),
-                                  _ptr(mask), _ptr(scores), C.byref(margin), C.byref(n_exec))
+        ep = None
+        if execs is not None:
+            assert len(execs) == L
+            ep = (C.c_void_p * L)(*[_need(a, np.uint8, "exec").ctypes.data for a in execs])
+        rc = lib().orc_decode_seq_ex(C.byref(self._c), self._layers,
+                                     C.byref(self._dm) if self._dm is not None else None,
+                                     kp, vp, ep, int(pos), int(k), _ptr(r), _ptr(x), _ptr(h),
+                                     _ptr(mask), _ptr(scores), C.byref(margin), C.byref(n_exec))
         if rc != 0:
             raise ValueError("oracle rejected the arguments")
         return h, mask, scores, margin.value, n_exec.value

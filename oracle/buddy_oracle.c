@@ -136,6 +136,12 @@ static double act_gelu(double x) { return 0.5 * x * (1.0 + erf(x / sqrt(2.0))); 
 void orc_block(const orc_config* c, const orc_layer* w, void* kc, void* vc,
                int32_t pos, double* h)
 {
+    orc_block_ex(c, w, kc, vc, pos, h, NULL);
+}
+
+void orc_block_ex(const orc_config* c, const orc_layer* w, void* kc, void* vc,
+                  int32_t pos, double* h, const uint8_t* exec)
+{
     const int d = c->d_model, nq = c->n_heads, nkv = c->n_kv_heads;
     const int hd = c->head_dim, f = c->d_ffn, T = c->max_ctx, dt = c->dtype;
     const int nqkv = (nq + 2 * nkv) * hd;
@@ -164,13 +170,16 @@ void orc_block(const orc_config* c, const orc_layer* w, void* kc, void* vc,
         }
 
     /* decode attention of each query head over positions 0..pos of its KV
-     * group g = floor(h / (nq / nkv)), scale 1/sqrt(hd), softmax, sum p V */
+     * group g = floor(h / (nq / nkv)), scale 1/sqrt(hd), softmax, sum p V;
+     * with an execution map, positions at which this block did not run are
+     * left out of the softmax (weight 0) */
     const double scale = 1.0 / sqrt((double)hd);
     const int grp = nq / nkv;
     for (int hh = 0; hh < nq; ++hh) {
         int g = hh / grp;
         double mx = -INFINITY;
         for (int j = 0; j <= pos; ++j) {
+            if (exec && !exec[j]) continue;
             double s = 0.0;
             for (int i = 0; i < hd; ++i)
                 s += q[hh * hd + i] * ld(kc, ((size_t)g * T + j) * hd + i, dt);
@@ -179,7 +188,7 @@ void orc_block(const orc_config* c, const orc_layer* w, void* kc, void* vc,
         }
         double den = 0.0;
         for (int j = 0; j <= pos; ++j) {
-            p[j] = exp(p[j] - mx);
+            p[j] = (exec && !exec[j]) ? 0.0 : exp(p[j] - mx);
             den += p[j];
         }
         for (int i = 0; i < hd; ++i) {
@@ -296,6 +305,16 @@ int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* d
                    uint8_t* mask_out, float* scores_out, double* margin_out,
                    int32_t* n_exec_out)
 {
+    return orc_decode_seq_ex(c, layers, dm, kc, vc, NULL, pos, k_budget, route, x, h_out,
+                             mask_out, scores_out, margin_out, n_exec_out);
+}
+
+int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                      void* const* kc, void* const* vc, uint8_t* const* exec, int32_t pos,
+                      int32_t k_budget, const uint8_t* route, const float* x, double* h_out,
+                      uint8_t* mask_out, float* scores_out, double* margin_out,
+                      int32_t* n_exec_out)
+{
     const int L = c->n_layers, Lm = L - 2, d = c->d_model, dt = c->dtype;
     const int nkv = c->n_kv_heads, hd = c->head_dim, T = c->max_ctx;
     if (L < 2 || pos < 0 || pos >= T || k_budget < 0 || k_budget > Lm) return -1;
@@ -309,7 +328,8 @@ int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* d
 
     /* first block always runs (Sec. 4.2.1); it appends the newest token's
      * first-layer K/V, which the planner then sees */
-    orc_block(c, &layers[0], kc[0], vc[0], pos, h);
+    if (exec) exec[0][pos] = 1;
+    orc_block_ex(c, &layers[0], kc[0], vc[0], pos, h, exec ? exec[0] : NULL);
 
     if (route) {
         for (int i = 0; i < Lm; ++i) mask[i] = route[i] ? 1 : 0;
@@ -330,8 +350,9 @@ int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* d
      * unchanged and the layer's K/V slot at pos is zero-filled (Sec. 6) */
     int n_exec = 1;
     for (int l = 1; l <= Lm; ++l) {
+        if (exec) exec[l][pos] = mask[l - 1] ? 1 : 0;
         if (mask[l - 1]) {
-            orc_block(c, &layers[l], kc[l], vc[l], pos, h);
+            orc_block_ex(c, &layers[l], kc[l], vc[l], pos, h, exec ? exec[l] : NULL);
             ++n_exec;
         } else {
             for (int g = 0; g < nkv; ++g)
@@ -342,7 +363,8 @@ int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* d
                 }
         }
     }
-    orc_block(c, &layers[L - 1], kc[L - 1], vc[L - 1], pos, h);
+    if (exec) exec[L - 1][pos] = 1;
+    orc_block_ex(c, &layers[L - 1], kc[L - 1], vc[L - 1], pos, h, exec ? exec[L - 1] : NULL);
     ++n_exec;
 
     memcpy(h_out, h, sizeof(double) * d);

@@ -66,6 +66,13 @@ void orc_rope(const orc_config* c, double* x, int32_t pos);
 void orc_block(const orc_config* c, const orc_layer* w, void* kc, void* vc,
                int32_t pos, double* h);
 
+/* orc_block with an execution map exec[max_ctx] of this layer's cache:
+ * positions j with exec[j] == 0 (the block did not run for that token) are
+ * left out of the attention softmax.  exec == NULL: every position counts
+ * (zero-filled slots of skipped steps are attended as ordinary entries). */
+void orc_block_ex(const orc_config* c, const orc_layer* w, void* kc, void* vc,
+                  int32_t pos, double* h, const uint8_t* exec);
+
 /* Mean of the cached K and V rows at positions 0..pos (inclusive), each
  * flattened head-major to n_kv_heads*head_dim: z = [mean K | mean V]. */
 void orc_pool(const orc_config* c, const void* kc, const void* vc, int32_t pos,
@@ -97,6 +104,17 @@ int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* d
                    const uint8_t* route, const float* x, double* h_out,
                    uint8_t* mask_out, float* scores_out, double* margin_out,
                    int32_t* n_exec_out);
+
+/* orc_decode_seq with skipped-KV masking: exec[l] is layer l's execution
+ * map of this sequence ([max_ctx] bytes).  The step writes exec[l][pos] (1
+ * for every block it runs, 0 for every block it skips; skipped slots are
+ * still zero-filled) and each block's attention leaves out the positions at
+ * which that block did not run.  exec == NULL is orc_decode_seq. */
+int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                      void* const* kc, void* const* vc, uint8_t* const* exec, int32_t pos,
+                      int32_t k_budget, const uint8_t* route, const float* x, double* h_out,
+                      uint8_t* mask_out, float* scores_out, double* margin_out,
+                      int32_t* n_exec_out);
 
 /* Number of OpenMP threads the oracle uses. */
 int orc_num_threads(void);

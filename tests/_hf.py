@@ -52,3 +52,32 @@ def hf_forward(model, x: np.ndarray) -> np.ndarray:
     with torch.no_grad():
         out = model(inputs_embeds=torch.from_numpy(x.astype(np.float64))[None])
     return out.last_hidden_state[0].numpy()
+
+
+def hf_routed_masked(model, x: np.ndarray, routes: np.ndarray) -> np.ndarray:
+    """Per-token routes with skipped-KV masking, computed without a KV cache:
+    block l (of the full stack `model`) runs causally over the subsequence of
+    tokens that execute it, each at its own position (rotary angles of the
+    original positions).  Block 0 and the last block run for every token;
+    routes [T][L-2] select the others.  Decoding is causal per block, so this
+    equals a token-by-token decode in which each block attends only to the
+    positions at which it ran.  Returns the last block's output [T][d]."""
+    T, L = x.shape[0], len(model.layers)
+    run = np.ones((T, L), dtype=bool)
+    run[:, 1:L - 1] = routes.astype(bool)
+    h = torch.from_numpy(x.astype(np.float64)).clone()
+    with torch.no_grad():
+        for li in range(L):
+            idx = np.nonzero(run[:, li])[0]
+            if idx.size == 0:
+                continue
+            sub = h[idx][None]
+            pid = torch.from_numpy(idx.astype(np.int64))[None]
+            cos_sin = model.rotary_emb(sub, pid)
+            n = idx.size
+            mask = torch.full((n, n), float("-inf"), dtype=torch.float64).triu(1)[None, None]
+            out = model.layers[li](sub, attention_mask=mask, position_ids=pid,
+                                   position_embeddings=cos_sin)
+            out = out[0] if isinstance(out, tuple) else out
+            h[idx] = out[0]
+    return h.numpy()

@@ -17,7 +17,7 @@ import torch
 from oracle import Oracle, bf16_from_double
 from paper_2606_09514_amd import synth
 
-from _hf import hf_forward, hf_model
+from _hf import hf_forward, hf_model, hf_routed_masked
 
 SMALL = dict(n_layers=6, d_model=64, n_heads=4, n_kv_heads=2, head_dim=16, d_ffn=96,
              dm_hidden=32, dm_act="gelu", rope_theta=1e4, rms_eps=1e-5)
@@ -308,3 +308,56 @@ def test_skipped_layer_kv_is_zero_and_attended_as_zero():
     assert np.any(v1 != 0)
     # literal zero-fill: the skipped slot counts in the softmax with value 0
     assert np.allclose(h1, x1 + (0.0 + v1) / 2.0, rtol=0, atol=1e-14)
+
+
+# --------------------------------------------------- skipped-KV masking
+
+def test_masked_skipped_kv_leaves_the_slot_out():
+    """Masking variant of the skipped-layer KV (the alternative to zero-fill
+    that the paper's conclusion names as future work): the hand case of the
+    zero-fill test, where the routable block adds the mean of its V rows over
+    the positions it attends; with the slot of the skipped step left out it
+    adds exactly the new row's V."""
+    shape = dict(n_layers=3, d_model=4, n_heads=1, n_kv_heads=1, head_dim=4, d_ffn=4,
+                 dm_hidden=4, dm_act="silu", rope_theta=1e4, rms_eps=1e-5)
+    cfg, layers, dm, _ = make(shape=shape, max_ctx=4)
+    for lw in layers:
+        lw["wo"][...] = 0
+        lw["wdown"][...] = 0
+    layers[1]["wqkv"][:4] = 0
+    layers[1]["wo"][...] = np.eye(4, dtype=np.float32)
+    orc = Oracle(cfg, layers, dm)
+    kc, vc = empty_cache(cfg, orc)
+    execs = [np.full(cfg["max_ctx"], 9, np.uint8) for _ in range(3)]   # stale contents
+    rng = np.random.default_rng(12)
+    x0, x1 = rng.standard_normal(4).astype(np.float32), rng.standard_normal(4).astype(np.float32)
+    orc.decode_seq(kc, vc, 0, 0, x0, route=np.array([0], np.uint8), execs=execs)
+    assert [e[0] for e in execs] == [1, 0, 1]
+    assert np.all(kc[1][:, 0] == 0) and np.all(vc[1][:, 0] == 0)   # still zero-filled
+    h1, *_ = orc.decode_seq(kc, vc, 1, 1, x1, route=np.array([1], np.uint8), execs=execs)
+    assert [e[1] for e in execs] == [1, 1, 1]
+    v1 = vc[1][0, 1].astype(np.float64)
+    assert np.allclose(h1, x1 + v1, rtol=0, atol=1e-14)
+
+
+def test_masked_routes_equal_per_block_subsequence_forward():
+    """Random per-token routes with masking equal an independent cache-free
+    forward (Hugging Face blocks, float64) in which each block runs causally
+    over the tokens that execute it, at their original positions."""
+    cfg, layers, dm, orc = make()
+    T, L = 14, cfg["n_layers"]
+    rng = np.random.default_rng(31)
+    routes = (rng.random((T, orc.L_mid)) < 0.5).astype(np.uint8)
+    xs = synth.hidden_inputs(T, cfg["d_model"], seed=32).numpy()
+    kc, vc = empty_cache(cfg, orc)
+    execs = [np.zeros(cfg["max_ctx"], np.uint8) for _ in range(L)]
+    got = np.array([orc.decode_seq(kc, vc, t, int(routes[t].sum()), xs[t], route=routes[t],
+                                   execs=execs)[0] for t in range(T)])
+    ref = hf_routed_masked(hf_model(cfg, layers, list(range(L))), xs, routes)
+    assert relerr(got, ref) < 1e-5, relerr(got, ref)
+    # and it is not the zero-fill result
+    kc2, vc2 = empty_cache(cfg, orc)
+    zf = np.array([orc.decode_seq(kc2, vc2, t, int(routes[t].sum()), xs[t], route=routes[t])[0]
+                   for t in range(T)])
+    assert relerr(zf, ref) > 1e-3
+
