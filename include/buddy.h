@@ -79,8 +79,14 @@ typedef enum { BUDDY_F32 = 0, BUDDY_BF16 = 1 } buddy_dtype;
 /* Decision Module activation: SiLU (App. C.1) or exact GELU (erf form). */
 typedef enum { BUDDY_ACT_SILU = 0, BUDDY_ACT_GELU_ERF = 1 } buddy_dm_act;
 
-/* KV treatment of a skipped block: zero-filled rows (Sec. 6) are the only
- * treatment the paper fixes; BUDDY_SKIP_KV_MASK returns BUDDY_EUNSUPPORTED. */
+/* KV treatment of a skipped block.
+ *   BUDDY_SKIP_KV_ZERO: the slot at the step's position is zero-filled and
+ *     later steps attend to it as an ordinary entry (logit 0, value 0): the
+ *     treatment the paper uses (Conclusion, limitations).
+ *   BUDDY_SKIP_KV_MASK: the slot is still zero-filled, and the step also
+ *     records which blocks ran in the caller's execution map (buddy_kv.exec);
+ *     attention leaves out the positions at which a block did not run (the
+ *     masking alternative the paper names as future work). */
 typedef enum { BUDDY_SKIP_KV_ZERO = 0, BUDDY_SKIP_KV_MASK = 1 } buddy_skip_kv;
 
 typedef struct {
@@ -110,8 +116,16 @@ typedef struct {
 } buddy_dm_weights;
 
 typedef struct {
-    void* k;  /* device [L][max_batch][n_kv][max_ctx][hd], storage dtype */
-    void* v;  /* same layout as k                                         */
+    void* k;        /* device [L][max_batch][n_kv][max_ctx][hd], storage dtype */
+    void* v;        /* same layout as k                                         */
+    uint8_t* exec;  /* device [L][max_batch][max_ctx] execution map, or NULL:
+                       exec[l][b][j] != 0 when block l ran for sequence b's
+                       token at position j.  Read and written only with
+                       BUDDY_SKIP_KV_MASK (required then); the caller fills
+                       the rows of cached positions (e.g. all ones after a
+                       dense prefill), each step writes every block's entry
+                       at its position.  Blocks 0 and L-1 run for every
+                       token, so their maps are all ones.                  */
 } buddy_kv;
 
 typedef struct buddy_model buddy_model;
@@ -148,7 +162,8 @@ buddy_status buddy_select_topk(const float* scores, const int32_t* k, int32_t B,
  *           with the last block's output H_L (no final norm).
  *   pos:    host [B]; 0 <= pos[b] < max_ctx.
  *   k:      host [B]; 0 <= k[b] <= L-2 routable blocks to run.
- *   skip_kv: buddy_skip_kv.
+ *   skip_kv: buddy_skip_kv; BUDDY_SKIP_KV_MASK needs kv->exec
+ *           (BUDDY_EINVAL otherwise).
  *   route_override: device [B][L-2] uint8 (nonzero = run) or NULL; when
  *           given, the planner and Decision Module are not run, k is
  *           ignored and scores_out is left untouched.

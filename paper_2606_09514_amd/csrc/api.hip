@@ -133,8 +133,8 @@ hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
     return e != hipSuccess ? e : hipEventRecord(t.stop[t.next], s);
 }
 
-buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows rows, int batch,
-                       int max_pos, int pos_u, hipStream_t s) {
+buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float* hidden, int l,
+                       Rows rows, int batch, int max_pos, int pos_u, hipStream_t s) {
     const buddy_config& c = M.cfg;
     const buddy_layer_weights& w = M.layers[l];
     const int qdim = c.n_heads * c.head_dim;
@@ -165,6 +165,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, float* hidden, int l, Rows 
     a.bcap = c.max_batch; a.pos = M.ws.pos; a.pos_u = pos_u; a.rows = rows;
     attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
     a.part = M.ws.part; a.max_chunks = M.ws.max_chunks;
+    a.exec = exec ? exec + (size_t)l * c.max_batch * c.max_ctx : nullptr;
     if ((e = mark(M, BUDDY_KERNEL_ATTENTION, l, false, s)) != hipSuccess ||
         (e = launch_attention(c.dtype, a, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_ATTENTION, l, true, s)) != hipSuccess)
@@ -396,7 +397,7 @@ buddy_status buddy_pool_route(buddy_model* h, const buddy_kv* kv, const int32_t*
     if ((st = prepare_step(M, pos, nullptr, B, &a, &pos_u, s)) != BUDDY_OK) return st;
     if ((st = run_planner(M, kv, h_new, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
     hipError_t e;
-    if ((e = launch_route(M, kv->k, kv->v, a, nullptr, nullptr, scores_out, true, -1, s)) !=
+    if ((e = launch_route(M, kv->k, kv->v, nullptr, a, nullptr, nullptr, scores_out, true, -1, s)) !=
         hipSuccess)
         return fail_device(M, e, "scores");
     return BUDDY_OK;
@@ -432,7 +433,9 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     if (!route_override)
         for (int b = 0; b < B; ++b)
             if (k[b] < 0 || k[b] > Lm) return BUDDY_EINVAL;
-    if (skip_kv == BUDDY_SKIP_KV_MASK) return BUDDY_EUNSUPPORTED;
+    // masking needs the caller's execution map
+    uint8_t* exec = skip_kv == BUDDY_SKIP_KV_MASK ? kv->exec : nullptr;
+    if (skip_kv == BUDDY_SKIP_KV_MASK && !exec) return BUDDY_EINVAL;
 
     hipStream_t s = (hipStream_t)stream;
     StepArgs a;
@@ -443,7 +446,7 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
 
     const Rows all{M.ws.idx_all, M.ws.n_all, B, true, true};
     // first block on every sequence (appends the first-layer K/V row)
-    if ((st = run_block(M, kv, hidden, 0, all, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
+    if ((st = run_block(M, kv, exec, hidden, 0, all, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
     // KV-aware planner and Decision Module, unless the route is given
     if (!route_override)
         if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
@@ -459,7 +462,7 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     else if (M.policy == BUDDY_LAUNCH_AUTO) host_routed = !all_used && B <= kHostRoutedMaxBatch;
     host_routed = host_routed && Lm > 0;
     const int32_t seq = host_routed ? (M.seq = (M.seq + 1) & 0x3fffffff) : -1;
-    if ((e = launch_route(M, kv->k, kv->v, a, route_override, mask_out, scores_out, false, seq,
+    if ((e = launch_route(M, kv->k, kv->v, exec, a, route_override, mask_out, scores_out, false, seq,
                           s)) != hipSuccess)
         return fail_device(M, e, "route");
     if (host_routed && (st = wait_route(M, seq, s)) != BUDDY_OK) return st;
@@ -480,10 +483,10 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
         // every sequence routed (known on the host): the rows are the batch in order
         const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), n_max,
                      host_routed, host_routed && n_max == B};
-        if ((st = run_block(M, kv, hidden, l, r, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
+        if ((st = run_block(M, kv, exec, hidden, l, r, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
     }
     // last block on every sequence
-    st = run_block(M, kv, hidden, c.n_layers - 1, all, B, max_pos, pos_u, s);
+    st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, B, max_pos, pos_u, s);
     if (M.timing.n > 0 && M.timing.next < M.timing.n) ++M.timing.next;
     return st;
 }

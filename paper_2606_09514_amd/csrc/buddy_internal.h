@@ -191,7 +191,7 @@ hipError_t launch_pool(const Model& M, const void* k0, const void* v0, int B, in
 // publish_seq >= 0: also publish the per-block counts and then publish_seq
 // to the mapped host buffer (host-routed launches wait for it).  Budgets and
 // positions travel in `a`.
-hipError_t launch_route(const Model& M, const void* kc, const void* vc, const StepArgs& a,
+hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t* exec, const StepArgs& a,
                         const uint8_t* route_override, uint8_t* mask_out,
                         float* scores_out, bool scores_only, int32_t publish_seq,
                         hipStream_t s);
@@ -234,6 +234,7 @@ struct AttnArgs {
     Rows rows;
     int chunks, chunk_len;
     float* part; int max_chunks;
+    const uint8_t* exec;                // this block's execution map [bcap][T], or null
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // Cache rows one attention workgroup reads per block (chunk lengths are

@@ -10,7 +10,10 @@
 // writes o[b] for the group's heads (no cross-workgroup synchronisation
 // inside a kernel: device-wide fences are costly across the XCDs); with a
 // single chunk the first kernel writes o itself.  Zero-filled rows of skipped
-// steps are ordinary cache rows here (logit 0, value 0).
+// steps are ordinary cache rows here (logit 0, value 0), unless the block's
+// execution map is given: then rows at which the block did not run are left
+// out of the softmax (the new row at pos always counts: the block runs for
+// it, and the first block's entry is written only after its attention).
 //
 // Two score kernels:
 //  attn_kernel       vector ALUs: a cache row of hd elements is read by hd/V
@@ -84,6 +87,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const T* Vb = (const T*)a.vc + base;
     const int rows_wg = kAttnPasses * 4 * rpw;
     uint4 kr[kAttnPasses], vr[kAttnPasses];
+    uint8_t er[kAttnPasses];
+    const uint8_t* exr = a.exec ? a.exec + (size_t)b * a.T : nullptr;
     // every K/V row of a block is loaded before any arithmetic on it; rows
     // past the end are clamped to a valid row and masked below
     auto load_block = [&](int jb) {
@@ -92,6 +97,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             const int j = min(jb + (p * 4 + wave) * rpw + sub, max(j1 - 1, 0));
             kr[p] = *reinterpret_cast<const uint4*>(Kb + (size_t)j * a.hd);
             vr[p] = *reinterpret_cast<const uint4*>(Vb + (size_t)j * a.hd);
+            er[p] = exr ? exr[j] : 1;
         }
     };
     load_block(j0);
@@ -126,7 +132,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         for (int p = 0; p < kAttnPasses; ++p) {
             float kf[V];
             unpack<T>(kr[p], kf);
-            const bool live = jb + (p * 4 + wave) * rpw + sub < j1;
+            const int jrow = jb + (p * 4 + wave) * rpw + sub;
+            const bool live = jrow < j1 && (er[p] != 0 || jrow == pos);
 #pragma unroll
             for (int h = 0; h < GM; ++h) {
                 float d = 0.f;
@@ -296,6 +303,12 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         uint32_t vw[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) vw[r] = Vb[(size_t)min(jb + r, j1 - 1) * (HD / 2) + lane];
+        uint8_t ex[4] = {1, 1, 1, 1};
+        if (a.exec) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                ex[v] = a.exec[(size_t)b * a.T + min(jb + 4 * (lane >> 4) + v, j1 - 1)];
+        }
 
         f32x4_t d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -306,7 +319,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         // rows of this lane: jb + 4 (lane / 16) + v; head lane % 16
         float sc[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) sc[v] = jb + 4 * (lane >> 4) + v < j1 ? d[v] : -INFINITY;
+        for (int v = 0; v < 4; ++v) {
+            const int jrow = jb + 4 * (lane >> 4) + v;
+            sc[v] = jrow < j1 && (ex[v] != 0 || jrow == pos) ? d[v] : -INFINITY;
+        }
         float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
         mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
         mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));

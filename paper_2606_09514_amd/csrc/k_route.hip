@@ -8,9 +8,11 @@
 //                 into the means and joins the newest hidden state,
 //                 z = [mean K | mean V | h] (PRO_POOL in k_gemv.hip).
 //  route_kernel   Decision Module output layer plus prior fusion (Eq. 2),
-//                 deterministic top-k by rank counting, and zero-fill of the
-//                 K/V row of every skipped block (Sec. 6); with a single
-//                 sequence it also does the compaction below.
+//                 deterministic top-k by rank counting, zero-fill of the K/V
+//                 row of every skipped block (Conclusion: non-executed states
+//                 are zero vectors) and, with skipped-KV masking, the step's
+//                 entries of the execution map; with a single sequence it
+//                 also does the compaction below.
 //  compact_kernel grouping by mask (App. C.1): for every routable block the
 //                 ascending list of sequences that run it and their count.
 //  topk_kernel    the standalone top-k entry point.
@@ -133,6 +135,7 @@ struct RouteParams {
     int scores_only;
     int32_t* idx; int32_t* cnt;       // compaction outputs (single-sequence launch)
     volatile int32_t* host_cnt; int32_t seq;
+    uint8_t* exec;                    // execution map [L][bcap][T] (masking), or null
 };
 
 // Groups by mask the routed blocks of a one-sequence batch and publishes the
@@ -200,10 +203,16 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteParams p, StepArgs sa)
         if (tid == 0) publish_counts(p.host_cnt, Lm, p.seq);
     }
 
+    // with masking, every block's entry of the execution map at this step's
+    // position: 1 for the first and last blocks and the selected ones
+    const int pos = sa.pos[b];
+    if (p.exec && tid < Lm + 2)
+        p.exec[((size_t)tid * p.bcap + b) * p.T + pos] =
+            (tid == 0 || tid == Lm + 1) ? 1 : s_mask[tid - 1];
+
     // zero-filled K/V row at this step's position for every skipped block,
     // written as 16-byte vectors
     constexpr int VZ = St<T>::V;
-    const int pos = sa.pos[b];
     const size_t layer_stride = (size_t)p.bcap * p.nkv * p.T * p.hd;
     const int per_layer = p.nkv * (p.hd / VZ);
     for (int t = tid; t < Lm * per_layer; t += 1024) {
@@ -246,7 +255,7 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint8_t* mask, int L
     }
 }
 
-hipError_t launch_route(const Model& M, const void* kc, const void* vc, const StepArgs& a,
+hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t* exec, const StepArgs& a,
                         const uint8_t* route_override, uint8_t* mask_out,
                         float* scores_out, bool scores_only, int32_t publish_seq,
                         hipStream_t s) {
@@ -265,6 +274,7 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, const St
     p.idx = M.ws.idx; p.cnt = M.ws.cnt;
     p.host_cnt = publish_seq >= 0 ? M.d_host_cnt : nullptr;
     p.seq = publish_seq;
+    p.exec = exec;
     if (c.dtype == BUDDY_BF16) route_kernel<bf16_t><<<B, 1024, 0, s>>>(p, a);
     else route_kernel<float><<<B, 1024, 0, s>>>(p, a);
     hipError_t e = hipGetLastError();

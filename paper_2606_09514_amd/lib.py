@@ -41,7 +41,7 @@ class DMWeights(C.Structure):
 
 
 class KV(C.Structure):
-    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p)]
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("exec", C.c_void_p)]
 
 
 class BuddyError(RuntimeError):
@@ -181,8 +181,11 @@ class Model:
 
     def decode_step(self, k_cache, v_cache, hidden, pos, k, route_override=None,
                     mask_out=None, scores_out=None, skip_kv: int = SKIP_KV_ZERO,
-                    stream=None, check: bool = True) -> int:
-        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype))
+                    stream=None, check: bool = True, exec_map=None) -> int:
+        """exec_map: device uint8 [L][max_batch][max_ctx] execution map, for
+        skip_kv = SKIP_KV_MASK."""
+        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype),
+                _dev(exec_map, "exec_map", torch.uint8))
         B = len(pos)
         rc = lib().buddy_decode_step(
             self._h, C.byref(kv), _dev(hidden, "hidden", torch.float32), _host_i32(pos),

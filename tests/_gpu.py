@@ -71,40 +71,47 @@ def relerr(got, ref):
     return float(np.max(np.abs(got - ref)) / max(float(np.max(np.abs(ref))), 1e-30))
 
 
-def oracle_step(P, hk, hv, b, pos, k, x, route=None):
-    """One oracle step of sequence b on views of the host caches (modified)."""
+def oracle_step(P, hk, hv, b, pos, k, x, route=None, hx=None):
+    """One oracle step of sequence b on views of the host caches (modified);
+    hx: host execution maps [L][B][T] for skipped-KV masking (modified)."""
     L = P.cfg["n_layers"]
     kcs = [hk[l, b] for l in range(L)]
     vcs = [hv[l, b] for l in range(L)]
-    return P.orc.decode_seq(kcs, vcs, pos, k, x, route=route)
+    execs = None if hx is None else [hx[l, b] for l in range(L)]
+    return P.orc.decode_seq(kcs, vcs, pos, k, x, route=route, execs=execs)
 
 
-def gpu_step(P, dk, dv, x, pos, ks, route=None):
+def gpu_step(P, dk, dv, x, pos, ks, route=None, dx=None):
+    """One GPU step; dx: device execution map (skipped-KV masking) or None."""
     B = len(pos)
     hidden = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
     mask = torch.zeros((B, P.L_mid), dtype=torch.uint8, device="cuda")
     scores = torch.zeros((B, P.L_mid), dtype=torch.float32, device="cuda")
     ro = None if route is None else torch.from_numpy(np.asarray(route, np.uint8)).cuda()
     P.gpu.decode_step(dk, dv, hidden, pos, ks, route_override=ro, mask_out=mask,
-                      scores_out=scores)
+                      scores_out=scores, exec_map=dx,
+                      skip_kv=blib.SKIP_KV_ZERO if dx is None else blib.SKIP_KV_MASK)
     torch.cuda.synchronize()
     return hidden.cpu().numpy(), mask.cpu().numpy(), scores.cpu().numpy()
 
 
-def compare_step(P, hk, hv, dk, dv, x, pos, ks, report):
-    """Teacher-forced step: the GPU caches hold the oracle's state on entry.
-    Runs both sides, applies the parity rules, and leaves the oracle's
-    post-step state in hk/hv (re-run with the GPU's route where the routes
-    legitimately differ).  Returns the oracle outputs [B][d]."""
+def compare_step(P, hk, hv, dk, dv, x, pos, ks, report, hx=None, dx=None):
+    """Teacher-forced step: the GPU caches (and execution maps hx/dx, with
+    masking) hold the oracle's state on entry.  Runs both sides, applies the
+    parity rules, and leaves the oracle's post-step state in hk/hv/hx (re-run
+    with the GPU's route where the routes legitimately differ).  Returns the
+    oracle outputs [B][d]."""
     B = len(pos)
     tol = TOL[P.cfg["dtype"]]
-    hg, mg, sg = gpu_step(P, dk, dv, x, pos, ks)
+    hg, mg, sg = gpu_step(P, dk, dv, x, pos, ks, dx=dx)
     gk, gv = P.download(dk), P.download(dv)
+    gx = None if dx is None else dx.cpu().numpy()
     out = np.zeros((B, P.cfg["d_model"]))
     for b in range(B):
         pre_k = [hk[l, b].copy() for l in range(P.cfg["n_layers"])]
         pre_v = [hv[l, b].copy() for l in range(P.cfg["n_layers"])]
-        h, m, s, margin, n_exec = oracle_step(P, hk, hv, b, pos[b], ks[b], x[b])
+        pre_x = None if hx is None else [hx[l, b].copy() for l in range(P.cfg["n_layers"])]
+        h, m, s, margin, n_exec = oracle_step(P, hk, hv, b, pos[b], ks[b], x[b], hx=hx)
         assert n_exec == ks[b] + 2 and int(m.sum()) == ks[b]
         if not np.array_equal(m, mg[b]):
             assert margin < MARGIN, f"route mismatch at margin {margin} (seq {b})"
@@ -112,7 +119,11 @@ def compare_step(P, hk, hv, dk, dv, x, pos, ks, report):
             for l in range(P.cfg["n_layers"]):
                 hk[l, b] = pre_k[l]
                 hv[l, b] = pre_v[l]
-            h, *_ = oracle_step(P, hk, hv, b, pos[b], ks[b], x[b], route=mg[b])
+                if hx is not None:
+                    hx[l, b] = pre_x[l]
+            h, *_ = oracle_step(P, hk, hv, b, pos[b], ks[b], x[b], route=mg[b], hx=hx)
+        if hx is not None:   # the execution map is integer data: exact
+            assert np.array_equal(gx[:, b], hx[:, b]), f"execution map differs (seq {b})"
         assert int(mg[b].sum()) == ks[b]
         err = relerr(hg[b], h)
         report["max_hidden_err"] = max(report["max_hidden_err"], err)

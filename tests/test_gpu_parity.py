@@ -212,8 +212,8 @@ def test_abi_validation_writes_nothing():
     rc = P.gpu.decode_step(dk, dv, hidden, [0, 0, 0], [1, 1, 1], mask_out=mask, check=False)
     assert rc == blib.ECAPACITY
     rc = P.gpu.decode_step(dk, dv, hidden, [0, 0], [1, 1], skip_kv=blib.SKIP_KV_MASK,
-                           mask_out=mask, check=False)
-    assert rc == blib.EUNSUPPORTED
+                           mask_out=mask, check=False)        # masking without a map
+    assert rc == blib.EINVAL
     rc = P.gpu.decode_step(dk, dv, hidden, [0, 0], [1, 1], skip_kv=7, check=False)
     assert rc == blib.EINVAL
     torch.cuda.synchronize()
@@ -370,6 +370,62 @@ def test_gqa_attention_mfma(G, B):
     ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
     x = synth.hidden_inputs(B, P.cfg["d_model"], seed=60 + G).numpy()
     rep = one_step_all(P, hk, hv, pos, ks, x)
+    print(G, B, rep)
+
+
+# ------------------------------------------------ skipped-KV masking
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_masked_skipped_kv_teacher_forced(dtype, policy):
+    """BUDDY_SKIP_KV_MASK on the tiny decoder: 24 prompt tokens then 8
+    fed-back steps, mixed budgets; every step checks the execution map
+    exactly and the hidden state / new K/V rows under the parity rules."""
+    B, T = 4, 40
+    P = Pair("tiny", dtype, T, B, seed=3, omega=0.1, policy=policy)
+    prompt = synth.hidden_inputs(B * 24, P.cfg["d_model"], seed=4).numpy().reshape(B, 24, -1)
+    hk, hv = P.empty_host_cache()
+    L = P.cfg["n_layers"]
+    hx = np.full((L, B, T), 7, np.uint8)          # stale: every entry read is written first
+    dk, dv = P.upload(hk), P.upload(hv)
+    dx = torch.from_numpy(hx).cuda()
+    ks = [1, 3, 5, 2]
+    rep = new_report()
+    x = prompt[:, 0]
+    for t in range(24 + 8):
+        dk.copy_(P.upload(hk))
+        dv.copy_(P.upload(hv))
+        dx.copy_(torch.from_numpy(hx))
+        x_t = prompt[:, t] if t < 24 else x
+        out, _ = compare_step(P, hk, hv, dk, dv, x_t, [t] * B, ks, rep, hx=hx, dx=dx)
+        x = out.astype(np.float32)
+    print(dtype, rep)
+
+
+@pytest.mark.parametrize("B", [1, 5])
+@pytest.mark.parametrize("G", [1, 4])
+def test_masked_attention_random_history(G, B):
+    """Masking with a random execution history supplied by the caller (as
+    after a routed prefill): head_dim 128, the MFMA score kernel (G = 4) and
+    the vector kernel (G = 1); positions span several chunks; one layer's
+    history is all zeros for one sequence (only the new row counts)."""
+    T = 640
+    P = Pair(gqa_shape(G), "bf16", T, B, seed=70 + G, omega=0.1)
+    g = torch.Generator().manual_seed(71 + G + B)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    L = P.cfg["n_layers"]
+    hx = (torch.rand((L, B, T), generator=g) < 0.6).numpy().astype(np.uint8)
+    hx[0] = 1
+    hx[L - 1] = 1
+    hx[1, 0] = 0
+    pos = [639, 100, 64, 350, 3][:B]
+    ks = [2, 1, 0, 2, 1][:B]
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=72).numpy()
+    dk, dv = P.upload(hk), P.upload(hv)
+    dx = torch.from_numpy(hx).cuda()
+    rep = new_report()
+    compare_step(P, hk, hv, dk, dv, x, pos, ks, rep, hx=hx, dx=dx)
     print(G, B, rep)
 
 
