@@ -79,6 +79,17 @@ typedef enum { BUDDY_F32 = 0, BUDDY_BF16 = 1 } buddy_dtype;
 /* Decision Module activation: SiLU (App. C.1) or exact GELU (erf form). */
 typedef enum { BUDDY_ACT_SILU = 0, BUDDY_ACT_GELU_ERF = 1 } buddy_dm_act;
 
+/* Router context (Sec. 4.3 and the feature ablation of Sec. 5): pooled
+ * first-layer cache features followed by the newest token's hidden state
+ * after the first block.
+ *   BUDDY_CTX_KV:   [mean K | mean V | h]  (2 n_kv hd + d values)
+ *   BUDDY_CTX_K:    [mean K | h]           (n_kv hd + d)
+ *   BUDDY_CTX_V:    [mean V | h]           (the paper's default feature)
+ *   BUDDY_CTX_K_PLUS_V: [mean K + mean V | h]
+ * Means run over positions 0..pos (the new row included); the Decision
+ * Module's first layer has this many inputs (w1 is [dm_hidden][din]). */
+typedef enum { BUDDY_CTX_KV = 0, BUDDY_CTX_K = 1, BUDDY_CTX_V = 2, BUDDY_CTX_K_PLUS_V = 3 } buddy_router_ctx;
+
 /* KV treatment of a skipped block.
  *   BUDDY_SKIP_KV_ZERO: the slot at the step's position is zero-filled and
  *     later steps attend to it as an ordinary entry (logit 0, value 0): the
@@ -103,6 +114,7 @@ typedef struct {
     int32_t max_ctx;      /* rows per sequence in the KV cache             */
     float rms_eps;        /* RMSNorm epsilon                               */
     float rope_theta;     /* rotary base                                   */
+    int32_t router_ctx;   /* buddy_router_ctx                              */
 } buddy_config;
 
 typedef struct {

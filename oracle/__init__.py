@@ -23,6 +23,7 @@ _SRC = os.path.join(_HERE, "buddy_oracle.c")
 
 ACTS = {"silu": 0, "gelu": 1}
 DTYPES = {"f32": 0, "bf16": 1}
+CTXS = {"kv": 0, "k": 1, "v": 2, "k+v": 3}
 
 
 def build() -> str:
@@ -38,7 +39,8 @@ class _Config(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ffn", C.c_int32),
                 ("dm_hidden", C.c_int32), ("dm_act", C.c_int32), ("dtype", C.c_int32),
-                ("max_ctx", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double)]
+                ("max_ctx", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
+                ("router_ctx", C.c_int32)]
 
 
 class _Layer(C.Structure):
@@ -74,6 +76,9 @@ def lib():
                                      vp, vp, i32, i32, vp, vp, vp, vp, vp, dp,
                                      C.POINTER(C.c_int32)]
         L.orc_decode_seq.restype = C.c_int
+        L.orc_context_dim.argtypes = [C.POINTER(_Config)]
+        L.orc_context_dim.restype = C.c_int
+        L.orc_router_context.argtypes = [C.POINTER(_Config), vp, vp, i32, vp, vp]
         L.orc_block_ex.argtypes = [C.POINTER(_Config), C.POINTER(_Layer), vp, vp, i32, vp, vp]
         L.orc_decode_seq_ex.argtypes = [C.POINTER(_Config), C.POINTER(_Layer), C.POINTER(_DM),
                                         vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, dp,
@@ -107,7 +112,7 @@ class Oracle:
 
     cfg keys: n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn,
     dm_hidden, dm_act ('silu'|'gelu'), dtype ('f32'|'bf16'), max_ctx,
-    rms_eps, rope_theta.  layers: list of dicts with attn_norm, wqkv, wo,
+    rms_eps, rope_theta, router_ctx ('kv'|'k'|'v'|'k+v', default 'kv').  layers: list of dicts with attn_norm, wqkv, wo,
     mlp_norm, wgate_up, wdown.  dm: dict with w1, b1, w2, b2, prior (float32
     or None) and omega.
     """
@@ -118,7 +123,8 @@ class Oracle:
         self._c = _Config(cfg["n_layers"], cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"],
                           cfg["head_dim"], cfg["d_ffn"], cfg.get("dm_hidden", 0),
                           ACTS[cfg.get("dm_act", "silu")], DTYPES[cfg["dtype"]],
-                          cfg["max_ctx"], float(cfg["rms_eps"]), float(cfg["rope_theta"]))
+                          cfg["max_ctx"], float(cfg["rms_eps"]), float(cfg["rope_theta"]),
+                          CTXS[cfg.get("router_ctx", "kv")])
         self._keep = []
         arr = (_Layer * len(layers))()
         for i, lw in enumerate(layers):
@@ -173,6 +179,15 @@ class Oracle:
         z = np.empty(2 * n, dtype=np.float64)
         lib().orc_pool(C.byref(self._c), _ptr(_need(kc, self.sdt, "kc")),
                        _ptr(_need(vc, self.sdt, "vc")), int(pos), _ptr(z))
+        return z
+
+    def context(self, kc, vc, pos: int, h):
+        """Router context z of one sequence (pooled first-layer features of
+        the configured variant, then h)."""
+        z = np.empty(int(lib().orc_context_dim(C.byref(self._c))), dtype=np.float64)
+        hh = np.ascontiguousarray(h, dtype=np.float64)
+        lib().orc_router_context(C.byref(self._c), _ptr(_need(kc, self.sdt, "kc")),
+                                 _ptr(_need(vc, self.sdt, "vc")), int(pos), _ptr(hh), _ptr(z))
         return z
 
     def dm_scores(self, z):

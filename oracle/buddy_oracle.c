@@ -235,6 +235,35 @@ void orc_pool(const orc_config* c, const void* kc, const void* vc, int32_t pos,
         }
 }
 
+
+/* Router context variants: the feature G_t of Sec. 4.3 is K, V or K + V of
+ * the first layer's cache, pooled over the prefix and the new row (the
+ * concatenation [K | V] is the default context of this implementation), and
+ * the newest token's hidden state after the first block follows it (the
+ * planner "pools it together with the newest token representation"). */
+int orc_context_dim(const orc_config* c)
+{
+    const int n = c->n_kv_heads * c->head_dim;
+    return (c->router_ctx == ORC_CTX_KV ? 2 * n : n) + c->d_model;
+}
+
+void orc_router_context(const orc_config* c, const void* kc, const void* vc, int32_t pos,
+                        const double* h, double* z)
+{
+    const int n = c->n_kv_heads * c->head_dim;
+    double* kv = malloc(sizeof(double) * 2 * n);
+    orc_pool(c, kc, vc, pos, kv);          /* [mean K | mean V] */
+    int m = 0;
+    switch (c->router_ctx) {
+    case ORC_CTX_K:        for (int i = 0; i < n; ++i) z[m++] = kv[i]; break;
+    case ORC_CTX_V:        for (int i = 0; i < n; ++i) z[m++] = kv[n + i]; break;
+    case ORC_CTX_K_PLUS_V: for (int i = 0; i < n; ++i) z[m++] = kv[i] + kv[n + i]; break;
+    default:               for (int i = 0; i < 2 * n; ++i) z[m++] = kv[i]; break;
+    }
+    for (int i = 0; i < c->d_model; ++i) z[m++] = h[i];
+    free(kv);
+}
+
 /* Decision Module scorer (Sec. 4.2.3, App. C.1): Linear - act - Linear, then
  * the prior fusion of Eq. (2).  The softmax of Eq. (2) is monotone and is not
  * needed to select the top k. */
@@ -242,7 +271,7 @@ void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
                    float* scores)
 {
     const int H = c->dm_hidden, Lm = c->n_layers - 2;
-    const int din = 2 * c->n_kv_heads * c->head_dim + c->d_model;
+    const int din = orc_context_dim(c);
     double* a = malloc(sizeof(double) * H);
     double* s = malloc(sizeof(double) * Lm);
     matvec(dm->w1, c->dtype, 0, H, din, z, a);
@@ -334,11 +363,9 @@ int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm
     if (route) {
         for (int i = 0; i < Lm; ++i) mask[i] = route[i] ? 1 : 0;
     } else {
-        /* router context: [mean K | mean V | newest hidden after block 0] */
-        const int din = 2 * nkv * hd + d;
-        double* z = malloc(sizeof(double) * din);
-        orc_pool(c, kc[0], vc[0], pos, z);
-        for (int i = 0; i < d; ++i) z[2 * nkv * hd + i] = h[i];
+        /* router context: pooled first-layer features, newest hidden after block 0 */
+        double* z = malloc(sizeof(double) * orc_context_dim(c));
+        orc_router_context(c, kc[0], vc[0], pos, h, z);
         orc_dm_scores(c, dm, z, sc);
         orc_topk(sc, Lm, k_budget, mask, &margin);
         free(z);

@@ -36,10 +36,15 @@ extern "C" {
 enum { ORC_F32 = 0, ORC_BF16 = 1 };
 enum { ORC_ACT_SILU = 0, ORC_ACT_GELU_ERF = 1 };
 
+/* Router context variants (Sec. 4.3: the features G_t in {K, V, K + V}
+ * pooled from the first layer's cache, then the newest hidden state). */
+enum { ORC_CTX_KV = 0, ORC_CTX_K = 1, ORC_CTX_V = 2, ORC_CTX_K_PLUS_V = 3 };
+
 typedef struct {
     int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn;
     int32_t dm_hidden, dm_act, dtype, max_ctx;
     double rms_eps, rope_theta;
+    int32_t router_ctx;   /* ORC_CTX_* */
 } orc_config;
 
 typedef struct {
@@ -78,7 +83,18 @@ void orc_block_ex(const orc_config* c, const orc_layer* w, void* kc, void* vc,
 void orc_pool(const orc_config* c, const void* kc, const void* vc, int32_t pos,
               double* z);
 
-/* Decision Module: s' = W2 act(W1 z + b1) + b2 + omega * prior, rounded to fp32. */
+/* Length of the router context z for the configured variant. */
+int orc_context_dim(const orc_config* c);
+
+/* Router context z of one sequence: the pooled first-layer features of the
+ * variant (ORC_CTX_KV: [mean K | mean V]; ORC_CTX_K: mean K; ORC_CTX_V:
+ * mean V; ORC_CTX_K_PLUS_V: mean K + mean V; means over 0..pos as in
+ * orc_pool), followed by the newest hidden state h[d_model]. */
+void orc_router_context(const orc_config* c, const void* kc, const void* vc, int32_t pos,
+                        const double* h, double* z);
+
+/* Decision Module: s' = W2 act(W1 z + b1) + b2 + omega * prior, rounded to fp32;
+ * z has orc_context_dim(c) values. */
 void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
                    float* scores);
 

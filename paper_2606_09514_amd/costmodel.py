@@ -63,7 +63,8 @@ def layer_weight_bytes(cfg: dict) -> int:
 
 def dm_weight_bytes(cfg: dict) -> int:
     H, Lm = cfg["dm_hidden"], cfg["n_layers"] - 2
-    din = 2 * cfg["n_kv_heads"] * cfg["head_dim"] + cfg["d_model"]
+    n = cfg["n_kv_heads"] * cfg["head_dim"]
+    din = (2 * n if cfg.get("router_ctx", "kv") == "kv" else n) + cfg["d_model"]
     return (H * din + H + Lm * H + Lm) * _s(cfg["dtype"])
 
 

@@ -45,15 +45,16 @@ buddy_status check_config(const buddy_config* c) {
     if (c->max_ctx < 1) return BUDDY_EINVAL;
     if (c->max_ctx > (1 << 20)) return BUDDY_ECAPACITY;  // keeps attention chunks <= 256
     if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return BUDDY_EINVAL;
+    if (c->router_ctx < BUDDY_CTX_KV || c->router_ctx > BUDDY_CTX_K_PLUS_V) return BUDDY_EINVAL;
     // a GEMV wavefront holds at most 16 k-steps of a two-row unit (K = d_model)
     // and a quarter of 64 k-steps of a single row
     const int ks = 64 * (c->dtype == BUDDY_BF16 ? 8 : 4);
     if (c->d_model > 16 * ks || c->d_ffn > 64 * ks) return BUDDY_ESHAPE;
     // every K the GEMVs see (d_model, d_ffn, n_heads * head_dim and the
-    // router input 2 n_kv hd + d) is a whole number of k-steps of 64 lanes x
-    // 16 bytes or at most 8 k-steps; fp32 weights (small models) have rows of
-    // at most 8 k-steps
-    const int din = 2 * c->n_kv_heads * c->head_dim + c->d_model;
+    // router input) is a whole number of k-steps of 64 lanes x 16 bytes or at
+    // most 8 k-steps; fp32 weights (small models) have rows of at most 8
+    // k-steps
+    const int din = pooled_dim(c->router_ctx, c->n_kv_heads, c->head_dim) + c->d_model;
     const int qdim = c->n_heads * c->head_dim;
     auto rows_ok = [ks](int K) { return K % ks == 0 || K <= 8 * ks; };
     if (c->dtype == BUDDY_BF16 &&
@@ -209,7 +210,9 @@ buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, in
         return fail_device(M, e, "pool");
     GemvArgs g;
     memset(&g, 0, sizeof(g));
-    g.W = M.dm.w1; g.N = c.dm_hidden; g.K = 2 * c.n_kv_heads * c.head_dim + c.d_model;
+    g.W = M.dm.w1; g.N = c.dm_hidden;
+    g.K = pooled_dim(c.router_ctx, c.n_kv_heads, c.head_dim) + c.d_model;
+    g.ctx = c.router_ctx;
     g.rows = Rows{M.ws.idx_all, M.ws.n_all, B, true, true};
     g.Y = M.ws.a; g.ldy = c.dm_hidden;
     g.bias = M.dm.b1; g.act = c.dm_act;
@@ -305,7 +308,7 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
 
     const buddy_config& c = M.cfg;
     const size_t Bc = c.max_batch, Lm = c.n_layers - 2, hd = c.head_dim;
-    const size_t din = 2 * c.n_kv_heads * hd + c.d_model;
+    const size_t din = pooled_dim(c.router_ctx, c.n_kv_heads, hd) + c.d_model;
     const size_t qdim = (size_t)c.n_heads * hd;
     const int max_chunks = kAttnMaxChunks;
     int max_splits = (c.max_ctx + 63) / 64;

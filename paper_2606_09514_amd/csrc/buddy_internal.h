@@ -213,12 +213,40 @@ struct GemvArgs {
     // EPI_QKV: rotary + cache append of this block
     void* kc; void* vc; int T; int hd; int nq; int nkv; int bcap;
     const int32_t* pos; int pos_u; const float2* rope;
-    // PRO_POOL: X is unused; row b of the input is the router context
-    // [sum K / n | sum V / n | h] built from the pool's split partial sums
-    const float* pool_part; int pool_splits, pool_max_splits; const float* h; int d;
+    // PRO_POOL: X is unused; row b of the input is the router context,
+    // pooled first-layer features of variant ctx (buddy_router_ctx) built
+    // from the pool's split partial sums, then h
+    const float* pool_part; int pool_splits, pool_max_splits; const float* h; int d; int ctx;
     // MFMA path: compact bf16 activation rows [round16(max_batch)][ldxb]
     bf16_t* XB; int ldxb;
 };
+
+// Pooled inputs of the router context: 2 n_kv hd for [mean K | mean V],
+// n_kv hd for the single-feature variants.
+__host__ __device__ inline int pooled_dim(int ctx, int nkv, int hd) {
+    return (ctx == BUDDY_CTX_KV ? 2 : 1) * nkv * hd;
+}
+
+// Router-context inputs k .. k+3 (k % 4 == 0, k < pooled_dim) of sequence b:
+// the split sums of the pool for mean K, mean V or their sum, times 1/n.
+__device__ __forceinline__ float4 pooled_feature4(const GemvArgs& g, int b, int k, float inv_n) {
+    const int nh = g.nkv * g.hd;
+    int kk = k, first = 0, last = 0;          // feature rows 0 (K) .. 1 (V) to add
+    if (g.ctx == BUDDY_CTX_KV) { first = last = k / nh; kk = k - first * nh; }
+    else if (g.ctx == BUDDY_CTX_V) { first = last = 1; }
+    else if (g.ctx == BUDDY_CTX_K_PLUS_V) { last = 1; }
+    const int gg = kk / g.hd, e = kk - gg * g.hd;
+    const float* pp = g.pool_part + ((size_t)b * g.nkv + gg) * g.pool_max_splits * 2 * g.hd + e;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int q = 0; q < g.pool_splits; ++q) {
+        for (int w = first; w <= last; ++w) {
+            const float4 t = *reinterpret_cast<const float4*>(pp + ((size_t)q * 2 + w) * g.hd);
+            v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
+        }
+    }
+    v.x *= inv_n; v.y *= inv_n; v.z *= inv_n; v.w *= inv_n;
+    return v;
+}
 hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream_t s);
 // MFMA path (bf16 weights, K a multiple of 128): prep of the compact bf16
 // rows, then the MFMA projection with the same epilogues.

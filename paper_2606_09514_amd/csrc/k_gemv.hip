@@ -136,20 +136,12 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
                 // router context of sequence b: means of the pool's split sums,
                 // then the newest hidden state
                 const int b = row_seq(g.rows, i0 + r);
-                const int zdim = 2 * g.nkv * g.hd;
+                const int zdim = pooled_dim(g.ctx, g.nkv, g.hd);
                 const float inv_n = 1.0f / (float)(seq_pos(g.pos, g.pos_u, b) + 1);
                 for (int k = tid * 4; k < K; k += NT * 4) {
                     float4 v;
                     if (k < zdim) {
-                        const int which = k / (g.nkv * g.hd), gg = (k / g.hd) % g.nkv, e = k % g.hd;
-                        const float* pp = g.pool_part +
-                            (((size_t)b * g.nkv + gg) * g.pool_max_splits) * 2 * g.hd + which * g.hd + e;
-                        v = make_float4(0.f, 0.f, 0.f, 0.f);
-                        for (int q = 0; q < g.pool_splits; ++q) {
-                            const float4 t = *reinterpret_cast<const float4*>(pp + (size_t)q * 2 * g.hd);
-                            v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
-                        }
-                        v.x *= inv_n; v.y *= inv_n; v.z *= inv_n; v.w *= inv_n;
+                        v = pooled_feature4(g, b, k, inv_n);
                     } else {
                         v = *reinterpret_cast<const float4*>(g.h + (size_t)b * g.d + (k - zdim));
                     }

@@ -57,23 +57,13 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
         inv = 1.0f / sqrtf((s_ss[0] + s_ss[1] + s_ss[2] + s_ss[3]) / (float)K + g.eps);
     }
     const float inv_n = PRO == PRO_POOL ? 1.0f / (float)(seq_pos(g.pos, g.pos_u, b) + 1) : 0.f;
-    const int zdim = 2 * g.nkv * g.hd;
+    const int zdim = pooled_dim(g.ctx, g.nkv, g.hd);
     for (int k = tid * 8; k < K; k += 256 * 8) {
         float v[8];
         if (PRO == PRO_POOL && k < zdim) {
-            const int which = k / (g.nkv * g.hd), gg = (k / g.hd) % g.nkv, e = k % g.hd;
-            const float* pp = g.pool_part +
-                (((size_t)b * g.nkv + gg) * g.pool_max_splits) * 2 * g.hd + which * g.hd + e;
-#pragma unroll
-            for (int q = 0; q < 8; ++q) v[q] = 0.f;
-            for (int s = 0; s < g.pool_splits; ++s) {
-                const float4 t0 = *reinterpret_cast<const float4*>(pp + (size_t)s * 2 * g.hd);
-                const float4 t1 = *reinterpret_cast<const float4*>(pp + (size_t)s * 2 * g.hd + 4);
-                v[0] += t0.x; v[1] += t0.y; v[2] += t0.z; v[3] += t0.w;
-                v[4] += t1.x; v[5] += t1.y; v[6] += t1.z; v[7] += t1.w;
-            }
-#pragma unroll
-            for (int q = 0; q < 8; ++q) v[q] *= inv_n;
+            const float4 t0 = pooled_feature4(g, b, k, inv_n), t1 = pooled_feature4(g, b, k + 4, inv_n);
+            v[0] = t0.x; v[1] = t0.y; v[2] = t0.z; v[3] = t0.w;
+            v[4] = t1.x; v[5] = t1.y; v[6] = t1.z; v[7] = t1.w;
         } else {
             const float* x = PRO == PRO_POOL ? g.h + (size_t)b * g.d + (k - zdim)
                                              : g.X + (size_t)b * g.ldx + k;

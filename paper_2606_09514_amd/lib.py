@@ -18,6 +18,8 @@ OK, EINVAL, ESHAPE, ECAPACITY, ENOMEM, EDEVICE, EUNSUPPORTED = range(7)
 F32, BF16 = 0, 1
 ACT_SILU, ACT_GELU_ERF = 0, 1
 SKIP_KV_ZERO, SKIP_KV_MASK = 0, 1
+CTX_KV, CTX_K, CTX_V, CTX_K_PLUS_V = 0, 1, 2, 3
+CTX_BY_NAME = {"kv": CTX_KV, "k": CTX_K, "v": CTX_V, "k+v": CTX_K_PLUS_V}
 LAUNCH_AUTO, LAUNCH_DEVICE_ROUTED, LAUNCH_HOST_ROUTED = 0, 1, 2
 KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN = range(5)
 
@@ -27,7 +29,7 @@ class Config(C.Structure):
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ffn", C.c_int32),
                 ("dm_hidden", C.c_int32), ("dm_act", C.c_int32), ("dtype", C.c_int32),
                 ("max_batch", C.c_int32), ("max_ctx", C.c_int32),
-                ("rms_eps", C.c_float), ("rope_theta", C.c_float)]
+                ("rms_eps", C.c_float), ("rope_theta", C.c_float), ("router_ctx", C.c_int32)]
 
 
 class LayerWeights(C.Structure):
@@ -136,7 +138,7 @@ class Model:
     """A model handle over caller-owned device weights.
 
     cfg: dict with the buddy_config fields (dm_act 'silu'|'gelu', dtype
-    'f32'|'bf16').  weights: {'layers': [dict of tensors], 'dm': {...}} as
+    'f32'|'bf16', router_ctx 'kv'|'k'|'v'|'k+v', default 'kv').  weights: {'layers': [dict of tensors], 'dm': {...}} as
     produced by paper_2606_09514_amd.synth.model_weights on the device.
     """
 
@@ -147,7 +149,8 @@ class Model:
                    cfg["head_dim"], cfg["d_ffn"], cfg["dm_hidden"],
                    ACT_GELU_ERF if cfg["dm_act"] == "gelu" else ACT_SILU,
                    BF16 if cfg["dtype"] == "bf16" else F32, int(max_batch), cfg["max_ctx"],
-                   float(cfg["rms_eps"]), float(cfg["rope_theta"]))
+                   float(cfg["rms_eps"]), float(cfg["rope_theta"]),
+                   CTX_BY_NAME[cfg.get("router_ctx", "kv")])
         self._c = c
         self._keep = weights
         L = cfg["n_layers"]

@@ -60,6 +60,14 @@ WORKLOADS = {
 }
 
 
+def context_dim(cfg: dict) -> int:
+    """Number of router-context inputs (the Decision Module's first-layer
+    width) for the configured variant: 'kv' pools K and V side by side, 'k',
+    'v' and 'k+v' one head-major vector; the newest hidden state follows."""
+    n = cfg["n_kv_heads"] * cfg["head_dim"]
+    return (2 * n if cfg.get("router_ctx", "kv") == "kv" else n) + cfg["d_model"]
+
+
 def model_config(shape: str | dict, dtype: str, max_ctx: int) -> dict:
     s = SHAPES[shape] if isinstance(shape, str) else shape
     c = dict(s)
@@ -100,7 +108,7 @@ def model_weights(cfg: dict, seed: int, device="cpu", omega: float = 0.1,
             wdown=_normal((d, f), std, 0.0, gen, device, dt),
         ))
     H, Lm = cfg["dm_hidden"], cfg["n_layers"] - 2
-    din = 2 * nkv * hd + d
+    din = context_dim(cfg)
     dm = dict(
         w1=_normal((H, din), std, 0.0, gen, device, dt),
         b1=_normal((H,), std, 0.0, gen, device, dt),

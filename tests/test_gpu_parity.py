@@ -66,6 +66,35 @@ def test_pool_route_scores(dtype, shape):
         assert np.max(np.abs(got[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref))))
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("ctx", ["k", "v", "k+v"])
+def test_router_context_variants(ctx, dtype):
+    """Router contexts from K, V or K + V of the first-layer cache (Sec. 4.3
+    features, the value states being the paper's default): scores of the
+    planner entry point and one decode step at B = 3 (GEMV) and B = 20 (MFMA
+    for bf16), against the oracle."""
+    T = 80
+    for B in (3, 20):
+        shape = dict(synth.SHAPES["tiny"], router_ctx=ctx)
+        P = Pair(shape, dtype, T, B, seed=80, omega=0.1)
+        g = torch.Generator().manual_seed(81)
+        hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        rng = np.random.default_rng(82)
+        pos = rng.integers(0, T, size=B).tolist()
+        h = synth.hidden_inputs(B, P.cfg["d_model"], seed=83)
+        scores = torch.zeros((B, P.L_mid), device="cuda")
+        P.gpu.pool_route(P.upload(hk), P.upload(hv), pos, h.cuda(), scores)
+        got = scores.cpu().numpy()
+        for b in range(B):
+            ref = P.orc.dm_scores(P.orc.context(hk[0, b], hv[0, b], pos[b], h[b].numpy()))
+            assert np.max(np.abs(got[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref))))
+        ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+        x = synth.hidden_inputs(B, P.cfg["d_model"], seed=84).numpy()
+        rep = one_step_all(P, hk, hv, pos, ks, x)
+        print(ctx, dtype, B, rep)
+
+
 # ------------------------------------------------ multi-step decode parity
 
 def run_teacher_forced(P, prompt, n_decode, ks, report):

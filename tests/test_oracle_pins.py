@@ -247,6 +247,36 @@ def test_dm_constant_scores_select_lowest_indices():
         assert margin == (math.inf if k in (0, orc.L_mid) else 0.0)
 
 
+@pytest.mark.parametrize("ctx", ["kv", "k", "v", "k+v"])
+def test_router_context_variants_brute_force(ctx):
+    """Sec. 4.3 features G_t in {K, V, K + V} (and the [K | V] default of
+    this implementation): head-major means of the stored first-layer rows
+    over 0..pos, computed here by a plain numpy mean, followed by h; the
+    Decision Module takes that many inputs."""
+    shape = dict(SMALL, router_ctx=ctx)
+    cfg, layers, dm, orc = make(shape=shape, dtype="bf16")
+    n = cfg["n_kv_heads"] * cfg["head_dim"]
+    assert dm["w1"].shape[1] == synth.context_dim(cfg) == (2 * n if ctx == "kv" else n) + cfg["d_model"]
+    rng = np.random.default_rng(9)
+    shp = (cfg["n_kv_heads"], cfg["max_ctx"], cfg["head_dim"])
+    mk = lambda: torch.from_numpy(rng.standard_normal(shp).astype(np.float32)).to(
+        torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    up = lambda a: (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    kc, vc = mk(), mk()
+    h = rng.standard_normal(cfg["d_model"])
+    for pos in (0, 3, 11):
+        mk_ = up(kc[:, :pos + 1]).mean(axis=1).reshape(-1)      # head-major [n_kv * hd]
+        mv_ = up(vc[:, :pos + 1]).mean(axis=1).reshape(-1)
+        feat = {"kv": np.concatenate([mk_, mv_]), "k": mk_, "v": mv_, "k+v": mk_ + mv_}[ctx]
+        ref = np.concatenate([feat, h])
+        z = orc.context(kc, vc, pos, h)
+        assert z.shape == ref.shape
+        assert np.allclose(z, ref, rtol=1e-14, atol=1e-14)
+    # the scores use the variant's context: a different variant gives others
+    s = orc.dm_scores(orc.context(kc, vc, 11, h))
+    assert s.shape == (orc.L_mid,) and np.all(np.isfinite(s))
+
+
 def test_omega_zero_ignores_prior():
     cfg, layers, dm, _ = make(omega=0.1)
     z = np.random.default_rng(10).standard_normal(2 * 2 * 16 + 64)
