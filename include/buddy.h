@@ -231,6 +231,30 @@ typedef enum {
 buddy_status buddy_set_timing_events(buddy_model* m, int32_t kernel, int32_t layer,
                                      void* const* start, void* const* stop, int32_t n);
 
+/* Kinds of raw per-layer importance indicator (App. B, direction
+ * unification): the skip-induced perplexity increase PPL_skip - PPL_full,
+ * a Taylor / Fisher / gradient-norm score, or the cosine similarity of a
+ * block's input and output. */
+typedef enum {
+    BUDDY_PRIOR_DELTA_PPL = 0,
+    BUDDY_PRIOR_TAYLOR = 1,
+    BUDDY_PRIOR_COSINE = 2
+} buddy_prior_kind;
+
+/* Offline prior normalisation (App. B, then Eq. 2), host code.  raw: host
+ * [n] indicator values of the n routable layers (finite); prior_out: host
+ * [n] fp32, the prior p~ for buddy_dm_weights.prior (copy it to the device).
+ * Steps over the n layers: larger-is-more-important (max(0, x) for the
+ * perplexity and Taylor kinds, 1 - x for cosine), log(1 + x) for the
+ * perplexity and Taylor kinds, robust z = (x - median) / (IQR + 1e-6) with
+ * linearly interpolated quartiles, clipped to [-winsor, winsor] when winsor
+ * > 0, rank normalisation u = (1 + rank) / (n + 1) with 0-based ranks and
+ * ties at their mean rank, and p~ = (u - mean u) / (population std + 1e-6).
+ * Errors: BUDDY_EINVAL for null pointers, n < 1, an unknown kind, a negative
+ * or non-finite winsor, or a non-finite raw value (nothing written). */
+buddy_status buddy_prior_normalize(const float* raw, int32_t n, int32_t kind, float winsor,
+                                   float* prior_out);
+
 /* Budget to routable-block count, k = round(b L) - 2 (Eq. 2), halves away
  * from zero, limited to [0, L-2]; -1 when b is outside (0, 1]. */
 int32_t buddy_budget_to_k(float b, int32_t n_layers);

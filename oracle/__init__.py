@@ -76,6 +76,7 @@ def lib():
                                      vp, vp, i32, i32, vp, vp, vp, vp, vp, dp,
                                      C.POINTER(C.c_int32)]
         L.orc_decode_seq.restype = C.c_int
+        L.orc_prior_normalize.argtypes = [vp, i32, i32, C.c_double, vp]
         L.orc_context_dim.argtypes = [C.POINTER(_Config)]
         L.orc_context_dim.restype = C.c_int
         L.orc_router_context.argtypes = [C.POINTER(_Config), vp, vp, i32, vp, vp]
@@ -101,6 +102,15 @@ def _need(a, dtype, name):
 
 def bf16_from_double(x: float) -> int:
     return int(lib().orc_bf16_from_double(float(x)))
+
+
+def prior_normalize(raw, kind: int, winsor: float = 0.0):
+    """App. B prior normalisation then Eq. 2 (kind 0 perplexity increase,
+    1 Taylor/Fisher, 2 cosine similarity); float64."""
+    r = np.ascontiguousarray(raw, dtype=np.float64)
+    out = np.empty(r.shape[0], dtype=np.float64)
+    lib().orc_prior_normalize(_ptr(r), int(r.shape[0]), int(kind), float(winsor), _ptr(out))
+    return out
 
 
 def num_threads() -> int:

@@ -79,6 +79,80 @@ static void st(void* p, size_t i, int dtype, double v)
         ((float*)p)[i] = (float)v;
 }
 
+
+/* ------------------------------------------------------------ prior (App. B) */
+
+static int cmp_double(const void* a, const void* b)
+{
+    const double x = *(const double*)a, y = *(const double*)b;
+    return (x > y) - (x < y);
+}
+
+/* Percentile at fraction q of n sorted values: the order statistic at
+ * q (n - 1), interpolated linearly between its two neighbours. */
+static double percentile_sorted(const double* s, int32_t n, double q)
+{
+    double at = q * (double)(n - 1);
+    int32_t i = (int32_t)at;
+    if (i >= n - 1) return s[n - 1];
+    return s[i] + (at - (double)i) * (s[i + 1] - s[i]);
+}
+
+typedef struct { double v; int32_t i; } orc_keyed;
+
+static int cmp_keyed(const void* a, const void* b)
+{
+    const orc_keyed* x = (const orc_keyed*)a;
+    const orc_keyed* y = (const orc_keyed*)b;
+    if (x->v != y->v) return (x->v > y->v) - (x->v < y->v);
+    return (x->i > y->i) - (x->i < y->i);
+}
+
+void orc_prior_normalize(const double* raw, int32_t n, int32_t kind, double winsor,
+                         double* out)
+{
+    double* x = malloc(sizeof(double) * n);
+    double* s = malloc(sizeof(double) * n);
+    orc_keyed* kz = malloc(sizeof(orc_keyed) * n);
+    /* (i) direction: larger means more important; (ii) heavy tails */
+    for (int32_t l = 0; l < n; ++l) {
+        if (kind == 2) {
+            x[l] = 1.0 - raw[l];                  /* cosine dissimilarity, identity */
+        } else {
+            double v = raw[l] > 0.0 ? raw[l] : 0.0; /* max{0, .} / clip to >= 0 */
+            x[l] = log(1.0 + v);
+        }
+    }
+    /* (iii) robust z-score with median and interquartile range */
+    memcpy(s, x, sizeof(double) * n);
+    qsort(s, n, sizeof(double), cmp_double);
+    double med = percentile_sorted(s, n, 0.5);
+    double iqr = percentile_sorted(s, n, 0.75) - percentile_sorted(s, n, 0.25);
+    for (int32_t l = 0; l < n; ++l) {
+        double z = (x[l] - med) / (iqr + 1e-6);
+        if (winsor > 0.0) z = z < -winsor ? -winsor : (z > winsor ? winsor : z);
+        kz[l].v = z;
+        kz[l].i = l;
+    }
+    /* (iv) rank normalisation: sort, each run of equal values gets the mean
+     * of the ranks it spans, u = (1 + rank) / (n + 1) */
+    qsort(kz, n, sizeof(orc_keyed), cmp_keyed);
+    for (int32_t a = 0; a < n;) {
+        int32_t b = a;
+        while (b + 1 < n && kz[b + 1].v == kz[a].v) ++b;
+        double rank = 0.5 * (double)(a + b);
+        for (int32_t t = a; t <= b; ++t) out[kz[t].i] = (1.0 + rank) / (double)(n + 1);
+        a = b + 1;
+    }
+    /* Eq. 2: p~ = (p - mu(p)) / (sigma(p) + eps) with p = u */
+    double mu = 0.0, var = 0.0;
+    for (int32_t l = 0; l < n; ++l) mu += out[l];
+    mu /= n;
+    for (int32_t l = 0; l < n; ++l) var += (out[l] - mu) * (out[l] - mu);
+    double sigma = sqrt(var / n);
+    for (int32_t l = 0; l < n; ++l) out[l] = (out[l] - mu) / (sigma + 1e-6);
+    free(x); free(s); free(kz);
+}
 int orc_num_threads(void)
 {
 #ifdef _OPENMP

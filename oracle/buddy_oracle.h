@@ -132,6 +132,17 @@ int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm
                       uint8_t* mask_out, float* scores_out, double* margin_out,
                       int32_t* n_exec_out);
 
+/* Offline prior normalisation, App. B steps (i)-(iv) over the n routable
+ * layers, then the standardisation of Eq. 2.  kind: 0 = perplexity increase
+ * (PPL_skip - PPL_full), 1 = Taylor/Fisher/gradient norm, 2 = cosine
+ * similarity.  winsor > 0 clips the robust z-scores to [-winsor, winsor].
+ * Readings (the paper leaves them open): quartiles interpolate linearly
+ * between order statistics, ranks are 0-based with tied values at their
+ * mean rank, the epsilons are 1e-6 and the standard deviation is the
+ * population one. */
+void orc_prior_normalize(const double* raw, int32_t n, int32_t kind, double winsor,
+                         double* out);
+
 /* Number of OpenMP threads the oracle uses. */
 int orc_num_threads(void);
 

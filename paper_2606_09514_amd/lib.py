@@ -19,6 +19,7 @@ F32, BF16 = 0, 1
 ACT_SILU, ACT_GELU_ERF = 0, 1
 SKIP_KV_ZERO, SKIP_KV_MASK = 0, 1
 CTX_KV, CTX_K, CTX_V, CTX_K_PLUS_V = 0, 1, 2, 3
+PRIOR_DELTA_PPL, PRIOR_TAYLOR, PRIOR_COSINE = 0, 1, 2
 CTX_BY_NAME = {"kv": CTX_KV, "k": CTX_K, "v": CTX_V, "k+v": CTX_K_PLUS_V}
 LAUNCH_AUTO, LAUNCH_DEVICE_ROUTED, LAUNCH_HOST_ROUTED = 0, 1, 2
 KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN = range(5)
@@ -78,6 +79,8 @@ def lib():
         L.buddy_set_launch_policy.restype = C.c_int
         L.buddy_set_timing_events.argtypes = [vp, i32, i32, vp, vp, i32]
         L.buddy_set_timing_events.restype = C.c_int
+        L.buddy_prior_normalize.argtypes = [vp, i32, i32, C.c_float, vp]
+        L.buddy_prior_normalize.restype = C.c_int
         L.buddy_budget_to_k.argtypes = [C.c_float, i32]
         L.buddy_budget_to_k.restype = i32
         L.buddy_status_string.argtypes = [C.c_int]
@@ -122,6 +125,19 @@ def _raise(rc: int, handle=None):
 
 def budget_to_k(b: float, n_layers: int) -> int:
     return int(lib().buddy_budget_to_k(float(b), int(n_layers)))
+
+
+def prior_normalize(raw, kind: int, winsor: float = 0.0, check: bool = True):
+    """Host wrapper of buddy_prior_normalize: raw indicator values of the
+    routable layers -> fp32 prior p~ (numpy)."""
+    import numpy as np
+    r = np.ascontiguousarray(raw, dtype=np.float32)
+    out = np.zeros(r.shape[0], dtype=np.float32)
+    rc = lib().buddy_prior_normalize(r.ctypes.data_as(C.c_void_p), int(r.shape[0]), int(kind),
+                                     C.c_float(winsor), out.ctypes.data_as(C.c_void_p))
+    if check:
+        _raise(rc, None)
+    return out if rc == OK else rc
 
 
 def select_topk(scores: torch.Tensor, k, mask_out: torch.Tensor, stream=None,

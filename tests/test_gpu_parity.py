@@ -307,6 +307,28 @@ def test_launch_policies_agree_bitwise():
     assert outs[0] == outs[1]
 
 
+# --------------------------------------------------- prior normalisation
+
+@pytest.mark.parametrize("kind", [blib.PRIOR_DELTA_PPL, blib.PRIOR_TAYLOR, blib.PRIOR_COSINE])
+@pytest.mark.parametrize("winsor", [0.0, 1.5])
+def test_prior_normalize_matches_oracle(kind, winsor):
+    """Host entry point of the App. B prior normalisation against the oracle
+    (fp32 output within 1e-6), and its argument checks."""
+    from oracle import prior_normalize as orc_prior
+    rng = np.random.default_rng(90 + kind)
+    for n in (1, 2, 6, 30, 38):
+        raw = (rng.standard_normal(n) * 2.0).astype(np.float32)
+        if n > 5:
+            raw[3] = raw[1]
+        got = blib.prior_normalize(raw, kind, winsor)
+        ref = orc_prior(raw.astype(np.float64), kind, winsor)
+        assert np.max(np.abs(got - ref)) <= 1e-6 * max(1.0, float(np.max(np.abs(ref))))
+    bad = np.array([1.0, np.nan], np.float32)
+    assert blib.prior_normalize(bad, kind, check=False) == blib.EINVAL
+    assert blib.prior_normalize(raw, 7, check=False) == blib.EINVAL
+    assert blib.prior_normalize(raw, kind, -1.0, check=False) == blib.EINVAL
+
+
 # ------------------------------------------------------- timing hook
 
 @pytest.mark.parametrize("B", [2, 40])

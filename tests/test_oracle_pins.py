@@ -391,3 +391,52 @@ def test_masked_routes_equal_per_block_subsequence_forward():
                    for t in range(T)])
     assert relerr(zf, ref) > 1e-3
 
+
+# -------------------------------------------- prior normalisation (App. B)
+
+def test_prior_normalize_hand_case():
+    """Four Taylor scores 1..4: log(1 + x) and the robust z keep the order, so
+    u = (1 + rank) / 5 = 0.2 .. 0.8, and Eq. 2 standardises it: mean 0.5,
+    population std sqrt(0.05)."""
+    from oracle import prior_normalize
+    got = prior_normalize([1.0, 2.0, 3.0, 4.0], 1)
+    u = np.array([0.2, 0.4, 0.6, 0.8])
+    assert np.allclose(got, (u - 0.5) / (np.sqrt(0.05) + 1e-6), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("kind", [0, 1, 2])
+def test_prior_normalize_depends_only_on_order(kind):
+    """Without winsorising, steps (ii) and (iii) are increasing maps, so u is
+    the rank transform of the direction-unified indicator: scipy's average
+    ranks give the same prior (ties from clipping at 0 included)."""
+    from scipy.stats import rankdata
+    from oracle import prior_normalize
+    rng = np.random.default_rng(40 + kind)
+    raw = rng.standard_normal(30) * 3.0
+    raw[[4, 9]] = -1.0                      # clipped to 0 together (kinds 0 and 1)
+    raw[[11, 20]] = raw[5]                  # exact ties
+    x = 1.0 - raw if kind == 2 else np.maximum(raw, 0.0)
+    u = rankdata(x, method="average") / (raw.size + 1)      # 1-based ranks: 1 + rank0
+    ref = (u - u.mean()) / (u.std() + 1e-6)
+    assert np.allclose(prior_normalize(raw, kind), ref, rtol=0, atol=1e-12)
+    # cosine: a more similar block (smaller change) is less important
+    if kind == 2:
+        p = prior_normalize([0.9, 0.5, 0.1], 2)
+        assert p[0] < p[1] < p[2]
+
+
+def test_prior_normalize_winsor_ties():
+    """Winsorising clips the robust z-scores: values beyond the clip share the
+    clipped value and therefore one mean rank (numpy percentile and scipy
+    ranks as the reference for this special case)."""
+    from scipy.stats import rankdata
+    from oracle import prior_normalize
+    raw = np.array([0.0, 0.1, 0.2, 0.3, 0.4, 50.0, 80.0, 200.0])
+    x = np.log1p(raw)
+    q25, q50, q75 = np.percentile(x, [25, 50, 75])
+    z = np.clip((x - q50) / (q75 - q25 + 1e-6), -1.0, 1.0)
+    assert np.sum(z == 1.0) >= 2
+    u = rankdata(z, method="average") / (raw.size + 1)
+    ref = (u - u.mean()) / (u.std() + 1e-6)
+    assert np.allclose(prior_normalize(raw, 1, winsor=1.0), ref, rtol=0, atol=1e-12)
+
