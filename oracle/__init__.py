@@ -53,6 +53,11 @@ class _DM(C.Structure):
                 ("b2", C.c_void_p), ("prior", C.c_void_p), ("omega", C.c_double)]
 
 
+class _Pred(C.Structure):
+    _fields_ = [("w1", C.c_void_p), ("b1", C.c_void_p), ("w2", C.c_void_p),
+                ("b2", C.c_void_p), ("hidden", C.c_int32)]
+
+
 _lib = None
 
 
@@ -76,6 +81,13 @@ def lib():
                                      vp, vp, i32, i32, vp, vp, vp, vp, vp, dp,
                                      C.POINTER(C.c_int32)]
         L.orc_decode_seq.restype = C.c_int
+        L.orc_predict_budget.argtypes = [C.POINTER(_Config), C.POINTER(_Pred), vp, vp, dp]
+        L.orc_predict_budget.restype = i32
+        L.orc_decode_seq_auto.argtypes = [C.POINTER(_Config), C.POINTER(_Layer), C.POINTER(_DM),
+                                          C.POINTER(_Pred), vp, vp, vp, i32, vp, vp,
+                                          C.POINTER(C.c_int32), vp, dp, vp, vp, dp,
+                                          C.POINTER(C.c_int32)]
+        L.orc_decode_seq_auto.restype = C.c_int
         L.orc_prior_normalize.argtypes = [vp, i32, i32, C.c_double, vp]
         L.orc_context_dim.argtypes = [C.POINTER(_Config)]
         L.orc_context_dim.restype = C.c_int
@@ -157,6 +169,56 @@ class Oracle:
                 d.prior = pr.ctypes.data
             d.omega = float(dm.get("omega", 0.0))
             self._dm = d
+        self._pred = None
+
+    def set_predictor(self, pred: dict | None):
+        """Budget Predictor weights {w1 [H][din], b1 [H], w2 [L-2][H], b2
+        [L-2]} as storage arrays, or None."""
+        if pred is None:
+            self._pred = None
+            return
+        p = _Pred()
+        for n in ("w1", "b1", "w2", "b2"):
+            a = _need(pred[n], self.sdt, n)
+            self._keep.append(a)
+            setattr(p, n, a.ctypes.data)
+        p.hidden = int(pred["w1"].shape[0])
+        self._pred = p
+
+    def predict_budget(self, z):
+        """(k_hat, logits [L-2] fp32, best - second best logit)."""
+        z = np.ascontiguousarray(z, dtype=np.float64)
+        lg = np.empty(self.L_mid, dtype=np.float32)
+        margin = C.c_double(0.0)
+        k = lib().orc_predict_budget(C.byref(self._c), C.byref(self._pred), _ptr(z), _ptr(lg),
+                                     C.byref(margin))
+        return int(k), lg, margin.value
+
+    def decode_seq_auto(self, kcs, vcs, pos: int, x, execs=None):
+        """Decode step without a budget (the predictor picks k).  Returns
+        (h, k, logits, predictor margin, mask, scores, margin, n_exec)."""
+        L = self.cfg["n_layers"]
+        kp = (C.c_void_p * L)(*[_need(a, self.sdt, "kc").ctypes.data for a in kcs])
+        vp = (C.c_void_p * L)(*[_need(a, self.sdt, "vc").ctypes.data for a in vcs])
+        ep = None
+        if execs is not None:
+            ep = (C.c_void_p * L)(*[_need(a, np.uint8, "exec").ctypes.data for a in execs])
+        x = np.ascontiguousarray(x, dtype=np.float32)
+        h = np.empty(self.cfg["d_model"], dtype=np.float64)
+        k = C.c_int32(0)
+        lg = np.zeros(self.L_mid, dtype=np.float32)
+        pm = C.c_double(0.0)
+        mask = np.zeros(self.L_mid, dtype=np.uint8)
+        scores = np.zeros(self.L_mid, dtype=np.float32)
+        margin = C.c_double(0.0)
+        n_exec = C.c_int32(0)
+        rc = lib().orc_decode_seq_auto(C.byref(self._c), self._layers, C.byref(self._dm),
+                                       C.byref(self._pred), kp, vp, ep, int(pos), _ptr(x),
+                                       _ptr(h), C.byref(k), _ptr(lg), C.byref(pm), _ptr(mask),
+                                       _ptr(scores), C.byref(margin), C.byref(n_exec))
+        if rc != 0:
+            raise ValueError("oracle rejected the arguments")
+        return h, k.value, lg, pm.value, mask, scores, margin.value, n_exec.value
 
     @property
     def L_mid(self) -> int:

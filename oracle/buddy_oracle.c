@@ -362,6 +362,36 @@ void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
     free(a); free(s);
 }
 
+/* Budget Predictor (Sec. 4.4): k_hat = argmax over k in {1..L-2} of the
+ * policy; the softmax of the policy is monotone, so the argmax of the
+ * logits is taken. */
+int32_t orc_predict_budget(const orc_config* c, const orc_predictor* p, const double* z,
+                           float* logits, double* margin)
+{
+    const int H = p->hidden, Lm = c->n_layers - 2;
+    const int din = orc_context_dim(c);
+    double* a = malloc(sizeof(double) * H);
+    double* s = malloc(sizeof(double) * Lm);
+    matvec(p->w1, c->dtype, 0, H, din, z, a);
+    for (int j = 0; j < H; ++j) {
+        double x = a[j] + ld(p->b1, j, c->dtype);
+        a[j] = c->dm_act == ORC_ACT_GELU_ERF ? act_gelu(x) : act_silu(x);
+    }
+    matvec(p->w2, c->dtype, 0, Lm, H, a, s);
+    int best = -1;
+    float top = 0.f, second = -INFINITY;
+    for (int i = 0; i < Lm; ++i) {
+        float v = (float)(s[i] + ld(p->b2, i, c->dtype));
+        if (logits) logits[i] = v;
+        if (v != v) continue;                            /* NaN never wins */
+        if (best < 0 || v > top) { second = best < 0 ? -INFINITY : top; top = v; best = i; }
+        else if (v > second) second = v;
+    }
+    if (margin) *margin = Lm > 1 ? (double)top - (double)second : INFINITY;
+    free(a); free(s);
+    return (best < 0 ? 0 : best) + 1;
+}
+
 /* Deterministic ordering for the hard top-k (Eq. 2): larger score first,
  * equal scores by lower layer index, NaN after every number. */
 static const float* g_cmp_scores;  /* set only under the single-threaded qsort below */
@@ -412,15 +442,18 @@ int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* d
                              mask_out, scores_out, margin_out, n_exec_out);
 }
 
-int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
-                      void* const* kc, void* const* vc, uint8_t* const* exec, int32_t pos,
-                      int32_t k_budget, const uint8_t* route, const float* x, double* h_out,
-                      uint8_t* mask_out, float* scores_out, double* margin_out,
-                      int32_t* n_exec_out)
+static int decode_core(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                       const orc_predictor* pred, void* const* kc, void* const* vc,
+                       uint8_t* const* exec, int32_t pos, int32_t k_budget,
+                       const uint8_t* route, const float* x, double* h_out,
+                       uint8_t* mask_out, float* scores_out, double* margin_out,
+                       int32_t* n_exec_out, int32_t* k_out, float* logits_out,
+                       double* pmargin_out)
 {
     const int L = c->n_layers, Lm = L - 2, d = c->d_model, dt = c->dtype;
     const int nkv = c->n_kv_heads, hd = c->head_dim, T = c->max_ctx;
-    if (L < 2 || pos < 0 || pos >= T || k_budget < 0 || k_budget > Lm) return -1;
+    if (L < 2 || pos < 0 || pos >= T) return -1;
+    if (pred ? (route || Lm < 1) : (k_budget < 0 || k_budget > Lm)) return -1;
     if (!route && !dm) return -1;
 
     double* h = malloc(sizeof(double) * d);
@@ -440,6 +473,10 @@ int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm
         /* router context: pooled first-layer features, newest hidden after block 0 */
         double* z = malloc(sizeof(double) * orc_context_dim(c));
         orc_router_context(c, kc[0], vc[0], pos, h, z);
+        if (pred) {   /* no budget given: the predictor's k from the same context */
+            k_budget = orc_predict_budget(c, pred, z, logits_out, pmargin_out);
+            if (k_out) *k_out = k_budget;
+        }
         orc_dm_scores(c, dm, z, sc);
         orc_topk(sc, Lm, k_budget, mask, &margin);
         free(z);
@@ -473,4 +510,26 @@ int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm
     if (n_exec_out) *n_exec_out = n_exec;
     free(h); free(mask); free(sc);
     return 0;
+}
+
+int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                      void* const* kc, void* const* vc, uint8_t* const* exec, int32_t pos,
+                      int32_t k_budget, const uint8_t* route, const float* x, double* h_out,
+                      uint8_t* mask_out, float* scores_out, double* margin_out,
+                      int32_t* n_exec_out)
+{
+    return decode_core(c, layers, dm, NULL, kc, vc, exec, pos, k_budget, route, x, h_out,
+                       mask_out, scores_out, margin_out, n_exec_out, NULL, NULL, NULL);
+}
+
+int orc_decode_seq_auto(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                        const orc_predictor* pred, void* const* kc, void* const* vc,
+                        uint8_t* const* exec, int32_t pos, const float* x, double* h_out,
+                        int32_t* k_out, float* logits_out, double* pmargin_out,
+                        uint8_t* mask_out, float* scores_out, double* margin_out,
+                        int32_t* n_exec_out)
+{
+    if (!pred) return -1;
+    return decode_core(c, layers, dm, pred, kc, vc, exec, pos, -1, NULL, x, h_out, mask_out,
+                       scores_out, margin_out, n_exec_out, k_out, logits_out, pmargin_out);
 }

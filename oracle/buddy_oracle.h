@@ -57,6 +57,15 @@ typedef struct {
     double omega;         /* prior weight; 0 disables the fusion */
 } orc_dm;
 
+/* Budget Predictor head (Sec. 4.4): a categorical policy over the actions
+ * k = 1..L-2 from the router context.  The paper does not give its layers;
+ * read here as the Decision Module's form, two linear layers with the
+ * Decision Module's activation in between. */
+typedef struct {
+    const void *w1, *b1, *w2, *b2;   /* [hidden][din], [hidden], [L-2][hidden], [L-2] */
+    int32_t hidden;
+} orc_predictor;
+
 /* bf16 bits nearest to x (round to nearest, ties to even; NaN -> quiet NaN). */
 uint16_t orc_bf16_from_double(double x);
 
@@ -98,6 +107,13 @@ void orc_router_context(const orc_config* c, const void* kc, const void* vc, int
 void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
                    float* scores);
 
+/* Budget Predictor: logits = W2 act(W1 z + b1) + b2 over k = 1..L-2, rounded
+ * to fp32 (the precision the argmax is taken in); returns k_hat = 1 + argmax
+ * (equal logits: the smaller k; NaN never wins).  logits[L-2] optional;
+ * *margin = best - second best logit (+inf with a single action). */
+int32_t orc_predict_budget(const orc_config* c, const orc_predictor* p, const double* z,
+                           float* logits, double* margin);
+
 /* Deterministic top-k over n scores: order by (score desc, index asc, NaN last).
  * mask[i] = 1 for the first k.  *margin = s(k-th) - s(k+1-th) in that order,
  * +inf when k == 0 or k == n.  Returns 0, or -1 for k outside [0, n]. */
@@ -131,6 +147,17 @@ int orc_decode_seq_ex(const orc_config* c, const orc_layer* layers, const orc_dm
                       int32_t k_budget, const uint8_t* route, const float* x, double* h_out,
                       uint8_t* mask_out, float* scores_out, double* margin_out,
                       int32_t* n_exec_out);
+
+/* orc_decode_seq_ex without a budget: the Budget Predictor picks k from the
+ * same router context as the Decision Module (Sec. 4.4, b = (k + 2) / L),
+ * then the step routes with it.  k_out, logits_out[L-2] and pmargin_out
+ * (the predictor's best - second best logit) are optional. */
+int orc_decode_seq_auto(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                        const orc_predictor* pred, void* const* kc, void* const* vc,
+                        uint8_t* const* exec, int32_t pos, const float* x, double* h_out,
+                        int32_t* k_out, float* logits_out, double* pmargin_out,
+                        uint8_t* mask_out, float* scores_out, double* margin_out,
+                        int32_t* n_exec_out);
 
 /* Offline prior normalisation, App. B steps (i)-(iv) over the n routable
  * layers, then the standardisation of Eq. 2.  kind: 0 = perplexity increase

@@ -120,6 +120,19 @@ def model_weights(cfg: dict, seed: int, device="cpu", omega: float = 0.1,
     return dict(layers=layers, dm=dm)
 
 
+def predictor_weights(cfg: dict, hidden: int, seed: int, device="cpu", std: float = 0.02) -> dict:
+    """Random-init Budget Predictor head: w1 [hidden][din], b1, w2 [L-2][hidden],
+    b2, all N(0, std) in the storage dtype (no trained predictor exists)."""
+    gen = torch.Generator(device=device).manual_seed(seed)
+    dt, Lm = cfg["dtype"], cfg["n_layers"] - 2
+    return dict(
+        w1=_normal((hidden, context_dim(cfg)), std, 0.0, gen, device, dt),
+        b1=_normal((hidden,), std, 0.0, gen, device, dt),
+        w2=_normal((Lm, hidden), std, 0.0, gen, device, dt),
+        b2=_normal((Lm,), std, 0.0, gen, device, dt),
+    )
+
+
 def kv_cache(cfg: dict, batch: int, ctx: int, seed: int, device="cpu",
              fill_std: float = 1.0) -> tuple:
     """K and V caches [L][B][n_kv][max_ctx][hd]; positions < ctx hold

@@ -440,3 +440,71 @@ def test_prior_normalize_winsor_ties():
     ref = (u - u.mean()) / (u.std() + 1e-6)
     assert np.allclose(prior_normalize(raw, 1, winsor=1.0), ref, rtol=0, atol=1e-12)
 
+
+# --------------------------------------------------- Budget Predictor
+
+def _predictor(cfg, hidden=16, seed=3):
+    return {k: synth.storage_numpy(v) for k, v in synth.predictor_weights(cfg, hidden, seed).items()}
+
+
+def test_predictor_argmax_and_ties():
+    """Sec. 4.4: k_hat = argmax over k in {1..L-2}; with W2 = 0 the logits are
+    b2, so a one-hot b2 picks its action, equal logits pick the smaller k and
+    a NaN logit never wins."""
+    cfg, layers, dm, orc = make()
+    pred = _predictor(cfg)
+    pred["w2"][...] = 0
+    z = np.random.default_rng(1).standard_normal(synth.context_dim(cfg))
+    for j in range(orc.L_mid):
+        pred["b2"][...] = 0
+        pred["b2"][j] = 0.5
+        orc.set_predictor(pred)
+        k, lg, margin = orc.predict_budget(z)
+        assert k == j + 1 and margin == pytest.approx(0.5)
+    pred["b2"][...] = 0.25
+    orc.set_predictor(pred)
+    assert orc.predict_budget(z)[0] == 1
+    pred["b2"][0] = np.nan
+    pred["b2"][2] = 0.5
+    orc.set_predictor(pred)
+    assert orc.predict_budget(z)[0] == 3
+
+
+@pytest.mark.parametrize("act", ["silu", "gelu"])
+def test_predictor_mlp_matches_torch(act):
+    """The head's two linear layers and activation reduce to torch's linear
+    and SiLU / exact GELU (float64), rounded to fp32."""
+    shape = dict(SMALL, dm_act=act)
+    cfg, layers, dm, orc = make(shape=shape)
+    pred = _predictor(cfg, hidden=24, seed=5)
+    orc.set_predictor(pred)
+    z = np.random.default_rng(2).standard_normal(synth.context_dim(cfg))
+    t = {k: torch.from_numpy(v.astype(np.float64)) for k, v in pred.items()}
+    a = torch.nn.functional.linear(torch.from_numpy(z), t["w1"], t["b1"])
+    a = torch.nn.functional.silu(a) if act == "silu" else torch.nn.functional.gelu(a)
+    ref = torch.nn.functional.linear(a, t["w2"], t["b2"]).numpy()
+    k, lg, _ = orc.predict_budget(z)
+    assert np.allclose(lg, ref.astype(np.float32), rtol=1e-6, atol=1e-7)
+    assert k == int(np.argmax(ref.astype(np.float32))) + 1
+
+
+def test_auto_budget_step_equals_budgeted_step():
+    """Without a budget the step runs exactly k_hat + 2 blocks, as the
+    budgeted step with k = k_hat does, and b_hat = (k_hat + 2) / L maps back
+    to k_hat through the Eq. 2 rounding."""
+    from paper_2606_09514_amd import costmodel
+    cfg, layers, dm, orc = make(omega=0.1)
+    orc.set_predictor(_predictor(cfg, hidden=32, seed=7))
+    xs = synth.hidden_inputs(6, cfg["d_model"], seed=11).numpy()
+    kc, vc = empty_cache(cfg, orc)
+    kc2, vc2 = empty_cache(cfg, orc)
+    seen = set()
+    for t, x in enumerate(xs):
+        h, k, lg, pm, mask, sc, margin, n_exec = orc.decode_seq_auto(kc, vc, t, x)
+        h2, m2, s2, _, n2 = orc.decode_seq(kc2, vc2, t, k, x)
+        assert 1 <= k <= orc.L_mid and n_exec == k + 2 and int(mask.sum()) == k
+        assert np.array_equal(h, h2) and np.array_equal(mask, m2) and np.array_equal(sc, s2)
+        b_hat = (k + 2) / cfg["n_layers"]
+        assert costmodel.budget_to_k(b_hat, cfg["n_layers"]) == k
+        seen.add(k)
+
