@@ -187,6 +187,41 @@ buddy_status buddy_decode_step(buddy_model* m, const buddy_kv* kv, float* hidden
                                int32_t skip_kv, const uint8_t* route_override,
                                uint8_t* mask_out, float* scores_out, void* stream);
 
+/* Budget Predictor head (Sec. 4.4): a categorical policy over k = 1..L-2
+ * from the same router context as the Decision Module, read as the Decision
+ * Module's form (the paper does not give its layers): logits = w2 act(w1 z
+ * + b1) + b2 with the Decision Module's activation. */
+typedef struct {
+    const void *w1, *b1, *w2, *b2;  /* device, storage dtype: w1 [hidden][din],
+                                       b1 [hidden], w2 [L-2][hidden], b2 [L-2] */
+    int32_t hidden;                 /* multiple of 8                          */
+} buddy_predictor_weights;
+
+/* Attaches a Budget Predictor head to the handle (the pointers are copied,
+ * the weights are not; they must outlive the handle), or detaches it with
+ * p == NULL.  Waits for the device, then allocates the head's workspace.
+ * Errors: BUDDY_EINVAL (null pointers, hidden not a positive multiple of 8,
+ * fewer than three layers), BUDDY_ESHAPE (hidden too wide), BUDDY_ENOMEM. */
+buddy_status buddy_set_budget_predictor(buddy_model* m, const buddy_predictor_weights* p);
+
+/* Planner and Budget Predictor only (steps 3 and 4 with the predictor's
+ * output layer): k_out device [B] int32 receives k_hat = 1 + argmax of the
+ * logits (fp32; the smaller k on equal logits; the budget is b_hat =
+ * (k_hat + 2) / L); logits_out device [B][L-2] fp32 or NULL.  pos and h_new
+ * as for buddy_pool_route.  BUDDY_EINVAL without an attached predictor. */
+buddy_status buddy_predict_budget(buddy_model* m, const buddy_kv* kv, const int32_t* pos,
+                                  const float* h_new, int32_t B, int32_t* k_out,
+                                  float* logits_out, void* stream);
+
+/* buddy_decode_step without budgets: each sequence's k is the Budget
+ * Predictor's k_hat from the step's own router context, then the step runs
+ * as buddy_decode_step with that k.  k_out: device [B] int32 or NULL.
+ * BUDDY_EINVAL without an attached predictor. */
+buddy_status buddy_decode_step_auto(buddy_model* m, const buddy_kv* kv, float* hidden,
+                                    const int32_t* pos, int32_t B, int32_t skip_kv,
+                                    int32_t* k_out, uint8_t* mask_out, float* scores_out,
+                                    void* stream);
+
 /* How buddy_decode_step launches the routable blocks.
  *   BUDDY_LAUNCH_DEVICE_ROUTED: everything is enqueued without waiting; every
  *     routable block is launched and its kernels read the routed row count

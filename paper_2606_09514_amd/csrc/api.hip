@@ -202,7 +202,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
 // split sums of the first-layer cache, then the first Decision Module GEMV,
 // which folds them into z = [mean K | mean V | h] while staging its input.
 buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, int max_pos,
-                         int pos_u, hipStream_t s) {
+                         int pos_u, bool predict, hipStream_t s) {
     const buddy_config& c = M.cfg;
     hipError_t e;
     int splits = 1;
@@ -223,6 +223,13 @@ buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, in
     // are decided on these scores
     if ((e = launch_gemv(c.dtype, PRO_POOL, EPI_BIAS_ACT, g, s)) != hipSuccess)
         return fail_device(M, e, "dm_hidden");
+    // the Budget Predictor's first layer on the same router context
+    if (predict) {
+        g.W = M.pred.w1; g.N = M.pred.hidden; g.bias = M.pred.b1;
+        g.Y = M.pred_a; g.ldy = M.pred.hidden;
+        if ((e = launch_gemv(c.dtype, PRO_POOL, EPI_BIAS_ACT, g, s)) != hipSuccess)
+            return fail_device(M, e, "predictor_hidden");
+    }
     return BUDDY_OK;
 }
 
@@ -376,6 +383,7 @@ void buddy_model_destroy(buddy_model* h) {
     if (!h) return;
     (void)hipDeviceSynchronize();
     (void)hipFree(h->M.ws_base);
+    (void)hipFree(h->M.pred_a);
     (void)hipHostFree(h->M.h_cnt);
     free(h->M.layers);
     free(h->M.timing.start);
@@ -398,11 +406,55 @@ buddy_status buddy_pool_route(buddy_model* h, const buddy_kv* kv, const int32_t*
     StepArgs a;
     int pos_u;
     if ((st = prepare_step(M, pos, nullptr, B, &a, &pos_u, s)) != BUDDY_OK) return st;
-    if ((st = run_planner(M, kv, h_new, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
+    if ((st = run_planner(M, kv, h_new, B, max_pos, pos_u, false, s)) != BUDDY_OK) return st;
     hipError_t e;
-    if ((e = launch_route(M, kv->k, kv->v, nullptr, a, nullptr, nullptr, scores_out, true, -1, s)) !=
-        hipSuccess)
+    if ((e = launch_route(M, kv->k, kv->v, nullptr, false, nullptr, nullptr, a, nullptr, nullptr,
+                          scores_out, true, -1, s)) != hipSuccess)
         return fail_device(M, e, "scores");
+    return BUDDY_OK;
+}
+
+buddy_status buddy_predict_budget(buddy_model* h, const buddy_kv* kv, const int32_t* pos,
+                                  const float* h_new, int32_t B, int32_t* k_out,
+                                  float* logits_out, void* stream) {
+    if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
+    if (B == 0) return BUDDY_OK;
+    if (B < 0) return BUDDY_EINVAL;
+    Model& M = h->M;
+    if (B > M.cfg.max_batch) return BUDDY_ECAPACITY;
+    if (!pos || !h_new || !k_out || M.pred.hidden == 0) return BUDDY_EINVAL;
+    int max_pos;
+    buddy_status st = check_step_host(M, pos, B, &max_pos);
+    if (st != BUDDY_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    StepArgs a;
+    int pos_u;
+    if ((st = prepare_step(M, pos, nullptr, B, &a, &pos_u, s)) != BUDDY_OK) return st;
+    if ((st = run_planner(M, kv, h_new, B, max_pos, pos_u, true, s)) != BUDDY_OK) return st;
+    hipError_t e;
+    if ((e = launch_route(M, kv->k, kv->v, nullptr, true, k_out, logits_out, a, nullptr, nullptr,
+                          nullptr, true, -1, s)) != hipSuccess)
+        return fail_device(M, e, "predictor");
+    return BUDDY_OK;
+}
+
+buddy_status buddy_set_budget_predictor(buddy_model* h, const buddy_predictor_weights* p) {
+    if (!h) return BUDDY_EINVAL;
+    Model& M = h->M;
+    if (p && (!p->w1 || !p->b1 || !p->w2 || !p->b2 || p->hidden <= 0 || p->hidden % 8 ||
+              M.cfg.n_layers < 3))
+        return BUDDY_EINVAL;
+    if (p && (size_t)p->hidden > (size_t)64 * 64 * (M.cfg.dtype == BUDDY_BF16 ? 8 : 4))
+        return BUDDY_ESHAPE;                       // output-layer rows of at most 64 k-steps
+    hipError_t e = hipDeviceSynchronize();         // no step may still read the old head
+    if (e != hipSuccess) return fail_device(M, e, "set_budget_predictor");
+    (void)hipFree(M.pred_a);
+    M.pred_a = nullptr;
+    memset(&M.pred, 0, sizeof(M.pred));
+    if (!p) return BUDDY_OK;
+    e = hipMalloc((void**)&M.pred_a, (size_t)M.cfg.max_batch * p->hidden * sizeof(float));
+    if (e != hipSuccess) { M.pred_a = nullptr; return BUDDY_ENOMEM; }
+    M.pred = *p;
     return BUDDY_OK;
 }
 
@@ -416,10 +468,14 @@ buddy_status buddy_select_topk(const float* scores, const int32_t* k, int32_t B,
     return e == hipSuccess ? BUDDY_OK : BUDDY_EDEVICE;
 }
 
-buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden,
-                               const int32_t* pos, const int32_t* k, int32_t B,
-                               int32_t skip_kv, const uint8_t* route_override,
-                               uint8_t* mask_out, float* scores_out, void* stream) {
+namespace {
+
+// One decode step: budgets from k, or from the Budget Predictor (predict),
+// or a given route.
+buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, const int32_t* pos,
+                         const int32_t* k, int32_t B, int32_t skip_kv,
+                         const uint8_t* route_override, bool predict, int32_t* k_out,
+                         uint8_t* mask_out, float* scores_out, void* stream) {
     if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
     if (skip_kv != BUDDY_SKIP_KV_ZERO && skip_kv != BUDDY_SKIP_KV_MASK) return BUDDY_EINVAL;
     if (B == 0) return BUDDY_OK;
@@ -427,13 +483,14 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     Model& M = h->M;
     const buddy_config& c = M.cfg;
     if (B > c.max_batch) return BUDDY_ECAPACITY;
-    if (!hidden || !pos || (!k && !route_override)) return BUDDY_EINVAL;
+    if (!hidden || !pos || (!k && !route_override && !predict)) return BUDDY_EINVAL;
+    if (predict && M.pred.hidden == 0) return BUDDY_EINVAL;
     tl_launch_events = {nullptr, nullptr};   // nothing armed by a failed earlier step
     int max_pos;
     buddy_status st = check_step_host(M, pos, B, &max_pos);
     if (st != BUDDY_OK) return st;
     const int Lm = c.n_layers - 2;
-    if (!route_override)
+    if (!route_override && !predict)
         for (int b = 0; b < B; ++b)
             if (k[b] < 0 || k[b] > Lm) return BUDDY_EINVAL;
     // masking needs the caller's execution map
@@ -443,7 +500,8 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     hipStream_t s = (hipStream_t)stream;
     StepArgs a;
     int pos_u;
-    if ((st = prepare_step(M, pos, route_override ? nullptr : k, B, &a, &pos_u, s)) != BUDDY_OK)
+    if ((st = prepare_step(M, pos, route_override || predict ? nullptr : k, B, &a, &pos_u, s)) !=
+        BUDDY_OK)
         return st;
     hipError_t e;
 
@@ -452,21 +510,21 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     if ((st = run_block(M, kv, exec, hidden, 0, all, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
     // KV-aware planner and Decision Module, unless the route is given
     if (!route_override)
-        if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
+        if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, predict, s)) != BUDDY_OK) return st;
     // Launch policy.  Device-routed: every routable block is launched and its
     // kernels read the routed row count on the device (an unused block costs
     // only empty launches).  Host-routed: the compaction kernel publishes the
     // per-block counts to mapped host memory; the host waits for them and
     // launches only the blocks some sequence runs, with exact grids.
-    bool all_used = !route_override;
+    bool all_used = !route_override && !predict;
     for (int b = 0; all_used && b < B; ++b) all_used = k[b] == Lm;
     bool host_routed = false;
     if (M.policy == BUDDY_LAUNCH_HOST_ROUTED) host_routed = true;
     else if (M.policy == BUDDY_LAUNCH_AUTO) host_routed = !all_used && B <= kHostRoutedMaxBatch;
     host_routed = host_routed && Lm > 0;
     const int32_t seq = host_routed ? (M.seq = (M.seq + 1) & 0x3fffffff) : -1;
-    if ((e = launch_route(M, kv->k, kv->v, exec, a, route_override, mask_out, scores_out, false, seq,
-                          s)) != hipSuccess)
+    if ((e = launch_route(M, kv->k, kv->v, exec, predict && !route_override, k_out, nullptr, a,
+                          route_override, mask_out, scores_out, false, seq, s)) != hipSuccess)
         return fail_device(M, e, "route");
     if (host_routed && (st = wait_route(M, seq, s)) != BUDDY_OK) return st;
     // routable blocks on their compacted sub-batches
@@ -492,6 +550,24 @@ buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden
     st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, B, max_pos, pos_u, s);
     if (M.timing.n > 0 && M.timing.next < M.timing.n) ++M.timing.next;
     return st;
+}
+
+}  // namespace
+
+buddy_status buddy_decode_step(buddy_model* h, const buddy_kv* kv, float* hidden,
+                               const int32_t* pos, const int32_t* k, int32_t B,
+                               int32_t skip_kv, const uint8_t* route_override,
+                               uint8_t* mask_out, float* scores_out, void* stream) {
+    return decode_impl(h, kv, hidden, pos, k, B, skip_kv, route_override, false, nullptr,
+                       mask_out, scores_out, stream);
+}
+
+buddy_status buddy_decode_step_auto(buddy_model* h, const buddy_kv* kv, float* hidden,
+                                    const int32_t* pos, int32_t B, int32_t skip_kv,
+                                    int32_t* k_out, uint8_t* mask_out, float* scores_out,
+                                    void* stream) {
+    return decode_impl(h, kv, hidden, pos, nullptr, B, skip_kv, nullptr, true, k_out, mask_out,
+                       scores_out, stream);
 }
 
 buddy_status buddy_set_launch_policy(buddy_model* h, int32_t policy) {

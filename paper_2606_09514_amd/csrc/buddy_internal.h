@@ -142,6 +142,8 @@ struct Model {
     int32_t seq;                  // sequence number of the last published route
     buddy_layer_weights* layers;  // host array of device pointers
     buddy_dm_weights dm;
+    buddy_predictor_weights pred;  // Budget Predictor head (pred.hidden == 0: none)
+    float* pred_a;                 // [max_batch][pred.hidden] its hidden activations
     Workspace ws;
     void* ws_base;                // one allocation holding the workspace
     int device;
@@ -191,7 +193,10 @@ hipError_t launch_pool(const Model& M, const void* k0, const void* v0, int B, in
 // publish_seq >= 0: also publish the per-block counts and then publish_seq
 // to the mapped host buffer (host-routed launches wait for it).  Budgets and
 // positions travel in `a`.
-hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t* exec, const StepArgs& a,
+// predict: the Budget Predictor's logits (from M.pred_a) pick each
+// sequence's k instead of a.k; k_out / logits_out receive them (nullable).
+hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t* exec, bool predict,
+                        int32_t* k_out, float* logits_out, const StepArgs& a,
                         const uint8_t* route_override, uint8_t* mask_out,
                         float* scores_out, bool scores_only, int32_t publish_seq,
                         hipStream_t s);

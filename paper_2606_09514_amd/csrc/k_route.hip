@@ -136,6 +136,10 @@ struct RouteParams {
     int32_t* idx; int32_t* cnt;       // compaction outputs (single-sequence launch)
     volatile int32_t* host_cnt; int32_t seq;
     uint8_t* exec;                    // execution map [L][bcap][T] (masking), or null
+    // Budget Predictor: hidden activations [B][Hp] (null: budgets from the
+    // step arguments), output layer, and the optional outputs
+    const float* pa; int Hp; const void* pw2; const void* pb2;
+    int32_t* k_out; float* logits_out;
 };
 
 // Groups by mask the routed blocks of a one-sequence batch and publishes the
@@ -145,36 +149,67 @@ __device__ __forceinline__ void publish_counts(volatile int32_t* host_cnt, int L
     host_cnt[Lm] = seq;
 }
 
+// One output layer row per wavefront: v[i] = W[i] . a + bias[i] (fp32).
+template <typename T>
+__device__ __forceinline__ void output_layer(const void* w, const void* bias, const float* a,
+                                             int H, int Lm, int wave, int lane, float* v) {
+    constexpr int V = St<T>::V;
+    const int nv = H / V;              // 16-byte vectors per row
+    for (int i = wave; i < Lm; i += 16) {
+        float acc = 0.f;
+        for (int q = lane; q < nv; q += kWave) {
+            float wv[V];
+            St<T>::vec((const T*)w + (size_t)i * H + q * V, wv);
+#pragma unroll
+            for (int e = 0; e < V; ++e) acc += wv[e] * a[q * V + e];
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) v[i] = acc + St<T>::get((const T*)bias, i);
+    }
+}
+
 template <typename T>
 __global__ __launch_bounds__(1024) void route_kernel(RouteParams p, StepArgs sa) {
     __shared__ float s_sc[256];
     __shared__ uint8_t s_mask[256];
+    __shared__ int s_k;
     const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int Lm = p.Lm;
 
+    // Budget Predictor (Sec. 4.4): k = 1 + argmax of the policy logits (the
+    // softmax is monotone), smaller k on equal logits, NaN never chosen
+    if (p.pa) {
+        output_layer<T>(p.pw2, p.pb2, p.pa + (size_t)b * p.Hp, p.Hp, Lm, wave, lane, s_sc);
+        __syncthreads();
+        if (tid < Lm && p.logits_out) p.logits_out[(size_t)b * Lm + tid] = s_sc[tid];
+        if (wave == 0) {
+            float bv = 0.f;
+            int bi = Lm;                                  // none yet
+            for (int i = lane; i < Lm; i += kWave) {
+                const float v = s_sc[i];
+                if (v == v && (bi == Lm || v > bv)) { bv = v; bi = i; }
+            }
+            for (int o = kWave / 2; o > 0; o >>= 1) {
+                const float ov = __shfl_xor(bv, o, kWave);
+                const int oi = __shfl_xor(bi, o, kWave);
+                if (oi != Lm && (bi == Lm || ov > bv || (ov == bv && oi < bi))) { bv = ov; bi = oi; }
+            }
+            if (lane == 0) {
+                s_k = (bi == Lm ? 0 : bi) + 1;
+                if (p.k_out) p.k_out[b] = s_k;
+            }
+        }
+        __syncthreads();   // s_sc is reused for the scores below
+    }
+    const int kb = p.pa ? s_k : (int)sa.k[b];
+
     if (p.route_override) {
         if (tid < Lm) s_mask[tid] = p.route_override[(size_t)b * Lm + tid] != 0;
     } else {
-        constexpr int V = St<T>::V;
-        const T* w2 = (const T*)p.w2;
-        const float* a = p.a + (size_t)b * p.H;
-        const int nv = p.H / V;        // 16-byte vectors per output-layer row
-        for (int i = wave; i < Lm; i += 16) {
-            float acc = 0.f;
-            for (int v = lane; v < nv; v += kWave) {
-                float wv[V];
-                St<T>::vec(w2 + (size_t)i * p.H + v * V, wv);
-#pragma unroll
-                for (int e = 0; e < V; ++e) acc += wv[e] * a[v * V + e];
-            }
-            acc = wave_sum(acc);
-            if (lane == 0) {
-                float v = acc + St<T>::get((const T*)p.b2, i);
-                if (p.prior) v += p.omega * p.prior[i];
-                s_sc[i] = v;
-            }
-        }
+        output_layer<T>(p.w2, p.b2, p.a + (size_t)b * p.H, p.H, Lm, wave, lane, s_sc);
+        __syncthreads();
+        if (p.prior && tid < Lm) s_sc[tid] += p.omega * p.prior[tid];
         __syncthreads();
         if (tid < Lm) {
             p.scores[(size_t)b * Lm + tid] = s_sc[tid];
@@ -185,7 +220,7 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteParams p, StepArgs sa)
             const float si = s_sc[tid];
             int rank = 0;
             for (int j = 0; j < Lm; ++j) rank += (j != tid) && beats(s_sc[j], j, si, tid);
-            s_mask[tid] = rank < (int)sa.k[b];
+            s_mask[tid] = rank < kb;
         }
     }
     __syncthreads();
@@ -255,7 +290,8 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint8_t* mask, int L
     }
 }
 
-hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t* exec, const StepArgs& a,
+hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t* exec, bool predict,
+                        int32_t* k_out, float* logits_out, const StepArgs& a,
                         const uint8_t* route_override, uint8_t* mask_out,
                         float* scores_out, bool scores_only, int32_t publish_seq,
                         hipStream_t s) {
@@ -275,6 +311,9 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t*
     p.host_cnt = publish_seq >= 0 ? M.d_host_cnt : nullptr;
     p.seq = publish_seq;
     p.exec = exec;
+    p.pa = predict ? M.pred_a : nullptr; p.Hp = M.pred.hidden;
+    p.pw2 = M.pred.w2; p.pb2 = M.pred.b2;
+    p.k_out = k_out; p.logits_out = logits_out;
     if (c.dtype == BUDDY_BF16) route_kernel<bf16_t><<<B, 1024, 0, s>>>(p, a);
     else route_kernel<float><<<B, 1024, 0, s>>>(p, a);
     hipError_t e = hipGetLastError();

@@ -43,6 +43,11 @@ class DMWeights(C.Structure):
                 ("b2", C.c_void_p), ("prior", C.c_void_p), ("omega", C.c_float)]
 
 
+class PredictorWeights(C.Structure):
+    _fields_ = [("w1", C.c_void_p), ("b1", C.c_void_p), ("w2", C.c_void_p),
+                ("b2", C.c_void_p), ("hidden", C.c_int32)]
+
+
 class KV(C.Structure):
     _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("exec", C.c_void_p)]
 
@@ -79,6 +84,9 @@ def lib():
         L.buddy_set_launch_policy.restype = C.c_int
         L.buddy_set_timing_events.argtypes = [vp, i32, i32, vp, vp, i32]
         L.buddy_set_timing_events.restype = C.c_int
+        L.buddy_set_budget_predictor.argtypes = [vp, P(PredictorWeights)]
+        L.buddy_predict_budget.argtypes = [vp, P(KV), vp, vp, i32, vp, vp, vp]
+        L.buddy_decode_step_auto.argtypes = [vp, P(KV), vp, vp, i32, i32, vp, vp, vp, vp]
         L.buddy_prior_normalize.argtypes = [vp, i32, i32, C.c_float, vp]
         L.buddy_prior_normalize.restype = C.c_int
         L.buddy_budget_to_k.argtypes = [C.c_float, i32]
@@ -212,6 +220,44 @@ class Model:
             _dev(route_override, "route_override", torch.uint8),
             _dev(mask_out, "mask_out", torch.uint8),
             _dev(scores_out, "scores_out", torch.float32), _stream(stream))
+        if check:
+            _raise(rc, self._h)
+        return rc
+
+    def set_budget_predictor(self, weights: dict | None) -> None:
+        """Budget Predictor head {w1, b1, w2, b2} (device tensors kept alive
+        by the handle), or None to detach."""
+        if weights is None:
+            _raise(lib().buddy_set_budget_predictor(self._h, None), self._h)
+            self._pred = None
+            return
+        p = PredictorWeights(*[_dev(weights[n], n, self.dtype) for n in ("w1", "b1", "w2", "b2")],
+                             int(weights["w1"].shape[0]))
+        _raise(lib().buddy_set_budget_predictor(self._h, C.byref(p)), self._h)
+        self._pred = weights
+
+    def predict_budget(self, k_cache, v_cache, pos, h_new, k_out, logits_out=None, stream=None,
+                       check: bool = True) -> int:
+        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype))
+        rc = lib().buddy_predict_budget(self._h, C.byref(kv), _host_i32(pos),
+                                        _dev(h_new, "h_new", torch.float32), len(pos),
+                                        _dev(k_out, "k_out", torch.int32),
+                                        _dev(logits_out, "logits_out", torch.float32),
+                                        _stream(stream))
+        if check:
+            _raise(rc, self._h)
+        return rc
+
+    def decode_step_auto(self, k_cache, v_cache, hidden, pos, k_out=None, mask_out=None,
+                         scores_out=None, skip_kv: int = SKIP_KV_ZERO, stream=None,
+                         check: bool = True, exec_map=None) -> int:
+        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype),
+                _dev(exec_map, "exec_map", torch.uint8))
+        rc = lib().buddy_decode_step_auto(
+            self._h, C.byref(kv), _dev(hidden, "hidden", torch.float32), _host_i32(pos),
+            len(pos), int(skip_kv), _dev(k_out, "k_out", torch.int32),
+            _dev(mask_out, "mask_out", torch.uint8), _dev(scores_out, "scores_out", torch.float32),
+            _stream(stream))
         if check:
             _raise(rc, self._h)
         return rc

@@ -14,7 +14,7 @@ from oracle import Oracle
 from paper_2606_09514_amd import lib as blib
 from paper_2606_09514_amd import synth
 
-from _gpu import Pair, compare_step, f32, gpu_step, oracle_step, relerr
+from _gpu import TOL, Pair, compare_step, f32, gpu_step, oracle_step, relerr
 
 pytestmark = pytest.mark.gpu
 
@@ -305,6 +305,105 @@ def test_launch_policies_agree_bitwise():
         outs.append((h.tobytes(), m.tobytes(), s.tobytes(), P.download(dk).tobytes(),
                      P.download(dv).tobytes()))
     assert outs[0] == outs[1]
+
+
+# --------------------------------------------------- Budget Predictor
+
+def attach_predictor(P, hidden=32, seed=95):
+    pw = synth.predictor_weights(P.cfg, hidden, seed)
+    P.orc.set_predictor({k: synth.storage_numpy(v) for k, v in pw.items()})
+    P.gpu.set_budget_predictor({k: v.cuda() for k, v in pw.items()})
+
+
+@pytest.mark.parametrize("dtype,shape", [("f32", "tiny"), ("bf16", "tiny"), ("bf16", "llama3_8b")])
+def test_predict_budget_matches_oracle(dtype, shape):
+    """Sec. 4.4 head on the router context: logits within 1e-5 and k_hat
+    exact except where the oracle's best and second best logits are closer
+    than 1e-3."""
+    B, T = 5, 300
+    P = Pair(shape, dtype, T, B, seed=96, omega=0.1, device_gen=(shape != "tiny"))
+    pw = synth.predictor_weights(P.cfg, 64, 97, device="cuda" if shape != "tiny" else "cpu")
+    P.orc.set_predictor({k: synth.storage_numpy(v) for k, v in pw.items()})
+    P.gpu.set_budget_predictor({k: v.cuda() for k, v in pw.items()})
+    hk, hv = P.empty_host_cache()
+    g = torch.Generator().manual_seed(98)
+    hk[0] = synth.storage_numpy(torch.randn(hk[0].shape, generator=g).to(P.tdt))
+    hv[0] = synth.storage_numpy(torch.randn(hk[0].shape, generator=g).to(P.tdt))
+    pos = [0, 1, 17, 63, T - 1]
+    h = synth.hidden_inputs(B, P.cfg["d_model"], seed=99)
+    k_out = torch.zeros(B, dtype=torch.int32, device="cuda")
+    logits = torch.zeros((B, P.L_mid), device="cuda")
+    P.gpu.predict_budget(P.upload(hk), P.upload(hv), pos, h.cuda(), k_out, logits)
+    kg, lg = k_out.cpu().numpy(), logits.cpu().numpy()
+    for b in range(B):
+        k, ref, margin = P.orc.predict_budget(P.orc.context(hk[0, b], hv[0, b], pos[b], h[b].numpy()))
+        assert np.max(np.abs(lg[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref))))
+        assert 1 <= kg[b] <= P.L_mid
+        assert kg[b] == k or margin < 1e-3
+
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+@pytest.mark.parametrize("dtype,B", [("f32", 4), ("bf16", 4), ("bf16", 20)])
+def test_decode_step_auto_teacher_forced(dtype, B, policy):
+    """Budget-free decode: the predictor's k per sequence and step, then the
+    routed step, teacher-forced against the oracle for 12 steps (k exact up
+    to the logit-margin rule; routes, hidden states and new K/V rows under
+    the usual rules)."""
+    T = 16
+    P = Pair("tiny", dtype, T, B, seed=100, omega=0.1, policy=policy)
+    attach_predictor(P, hidden=48, seed=101)
+    hk, hv = P.empty_host_cache()
+    dk, dv = P.upload(hk), P.upload(hv)
+    xs = synth.hidden_inputs(B * 12, P.cfg["d_model"], seed=102).numpy().reshape(B, 12, -1)
+    tol = TOL[dtype]
+    rep = new_report()
+    ks_seen = set()
+    L = P.cfg["n_layers"]
+    for t in range(12):
+        dk.copy_(P.upload(hk))
+        dv.copy_(P.upload(hv))
+        hidden = torch.from_numpy(np.ascontiguousarray(xs[:, t])).cuda()
+        k_out = torch.zeros(B, dtype=torch.int32, device="cuda")
+        mask = torch.zeros((B, P.L_mid), dtype=torch.uint8, device="cuda")
+        P.gpu.decode_step_auto(dk, dv, hidden, [t] * B, k_out=k_out, mask_out=mask)
+        torch.cuda.synchronize()
+        hg, kg, mg = hidden.cpu().numpy(), k_out.cpu().numpy(), mask.cpu().numpy()
+        for b in range(B):
+            pre = ([hk[l, b].copy() for l in range(L)], [hv[l, b].copy() for l in range(L)])
+            kcs, vcs = [hk[l, b] for l in range(L)], [hv[l, b] for l in range(L)]
+            h, k, lgt, pm, m, sc, margin, n_exec = P.orc.decode_seq_auto(kcs, vcs, t, xs[b, t])
+            if kg[b] != k or not np.array_equal(m, mg[b]):
+                assert (kg[b] != k and pm < 1e-3) or (kg[b] == k and margin < 1e-3), \
+                    f"seq {b} step {t}: k {kg[b]} vs {k} (logit margin {pm}), route margin {margin}"
+                rep["margin_mismatches"] += 1
+                for l in range(L):
+                    hk[l, b], hv[l, b] = pre[0][l], pre[1][l]
+                h, *_ = P.orc.decode_seq(kcs, vcs, t, int(kg[b]), xs[b, t], route=mg[b])
+            assert int(mg[b].sum()) == kg[b] and n_exec == k + 2
+            err = relerr(hg[b], h)
+            rep["max_hidden_err"] = max(rep["max_hidden_err"], err)
+            assert err < tol
+            ks_seen.add(int(kg[b]))
+    print(dtype, B, rep, sorted(ks_seen))
+
+
+def test_budget_predictor_argument_checks():
+    P = Pair("tiny", "f32", 8, 2, seed=103)
+    hk, hv = P.empty_host_cache()
+    dk, dv = P.upload(hk), P.upload(hv)
+    hidden = torch.ones((2, P.cfg["d_model"]), device="cuda")
+    k_out = torch.zeros(2, dtype=torch.int32, device="cuda")
+    assert P.gpu.decode_step_auto(dk, dv, hidden, [0, 0], k_out=k_out, check=False) == blib.EINVAL
+    assert P.gpu.predict_budget(dk, dv, [0, 0], hidden, k_out, check=False) == blib.EINVAL
+    pw = {k: v.cuda() for k, v in synth.predictor_weights(P.cfg, 12, 1).items()}
+    with pytest.raises(blib.BuddyError):               # hidden not a multiple of 8
+        P.gpu.set_budget_predictor(pw)
+    attach_predictor(P, hidden=16)
+    assert P.gpu.decode_step_auto(dk, dv, hidden, [0, 0], k_out=k_out, check=False) == blib.OK
+    torch.cuda.synchronize()
+    assert torch.all((k_out >= 1) & (k_out <= P.L_mid))
+    P.gpu.set_budget_predictor(None)
+    assert P.gpu.predict_budget(dk, dv, [0, 0], hidden, k_out, check=False) == blib.EINVAL
 
 
 # --------------------------------------------------- prior normalisation
