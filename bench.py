@@ -20,7 +20,6 @@ Prints one JSON line on stdout; progress goes to stderr.
 from __future__ import annotations
 
 import argparse
-import ctypes as C
 import json
 import os
 import sys
@@ -59,7 +58,11 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer):
+def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, exec_map=None):
+    """ks: budgets per sequence, or None for budget-free steps (the attached
+    Budget Predictor picks them); exec_map: execution map for skipped-KV
+    masking, or None for zero-filled skipped KV."""
+    import numpy as np
     import torch
     from paper_2606_09514_amd import costmodel
     from paper_2606_09514_amd import lib as blib
@@ -67,9 +70,21 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer):
     B, Lm = w.batch, cfg["n_layers"] - 2
     hidden = x0.clone()
     masks = torch.zeros((steps, B, Lm), dtype=torch.uint8, device="cuda")
+    k_pred = torch.zeros((steps, B), dtype=torch.int32, device="cuda")
+    skip = blib.SKIP_KV_ZERO if exec_map is None else blib.SKIP_KV_MASK
+
+    def step(pos, t=None):
+        mo = None if t is None else masks[t]
+        if ks is None:
+            model.decode_step_auto(dk, dv, hidden, [pos] * B, k_out=k_pred[t or 0], mask_out=mo,
+                                   skip_kv=skip, exec_map=exec_map)
+        else:
+            model.decode_step(dk, dv, hidden, [pos] * B, ks, mask_out=mo, skip_kv=skip,
+                              exec_map=exec_map)
+
     pos = w.ctx
     for _ in range(warmup):
-        model.decode_step(dk, dv, hidden, [pos] * B, ks)
+        step(pos)
         pos += 1
     starts, stops = hip.create(steps), hip.create(steps)
     model.set_timing_events(blib.KERNEL_GATE_UP, kernel_layer, starts, stops)
@@ -78,7 +93,7 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer):
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0.record()
     for t in range(steps):
-        model.decode_step(dk, dv, hidden, [pos] * B, ks, mask_out=masks[t])
+        step(pos, t)
         positions.append([pos] * B)
         pos += 1
     t1.record()
@@ -88,9 +103,10 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer):
     kern_ms = [hip.elapsed_ms(a, b) for a, b in zip(starts, stops)]
     hip.destroy(starts + stops)
     m = masks.cpu().numpy()
+    kk = k_pred.cpu().numpy() if ks is None else np.array([ks] * steps)
     step_bytes = [costmodel.step_bytes(cfg, m[t], positions[t]) for t in range(steps)]
     total_bytes = sum(s["total"] for s in step_bytes)
-    assert all(int(m[t, b].sum()) == ks[b] for t in range(steps) for b in range(B))
+    assert all(int(m[t, b].sum()) == kk[t, b] for t in range(steps) for b in range(B))
     distinct = len({m[t].tobytes() for t in range(steps)})
     return dict(ks=ks, total_ms=total_ms, ms_per_step=total_ms / steps,
                 tokens_per_s=B * steps / (total_ms / 1e3),
@@ -98,7 +114,7 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer):
                 step_hbm_frac=total_bytes / (total_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
                 layers_used=sum(s["layers_used"] for s in step_bytes) / steps,
                 distinct_routes=distinct, kernel_ms=sum(kern_ms) / len(kern_ms),
-                hidden=hidden, end_pos=pos)
+                mean_k=float(kk.mean()), hidden=hidden, end_pos=pos)
 
 
 def cpu_baseline(cfg, W, dk, dv, x0, k, ctx, budget_s=12.0):
@@ -136,6 +152,12 @@ def cpu_baseline(cfg, W, dk, dv, x0, k, ctx, budget_s=12.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--skip-kv", choices=["zero", "mask"], default="zero",
+                    help="KV of skipped blocks: zero-filled (the paper's) or masked")
+    ap.add_argument("--router-ctx", choices=["kv", "k", "v", "k+v"], default="kv",
+                    help="router context features")
+    ap.add_argument("--auto-budget", action="store_true",
+                    help="budget-free steps: a random-init Budget Predictor picks k")
     ap.add_argument("--steps", type=int, default=128)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="llama3_8b_b1_ctx2048")
@@ -162,6 +184,7 @@ def main():
     w = synth.WORKLOADS[args.workload]
     budgets = [int(b) for b in args.budgets.split(",")] if args.budgets else list(w.budgets)
     cfg = synth.model_config(w.shape, w.dtype, w.ctx + args.warmup + args.steps + 1)
+    cfg["router_ctx"] = args.router_ctx
 
     if args.copy_calibration:
         a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
@@ -181,18 +204,29 @@ def main():
     model.set_launch_policy({"auto": blib.LAUNCH_AUTO, "device": blib.LAUNCH_DEVICE_ROUTED,
                              "host": blib.LAUNCH_HOST_ROUTED}[args.policy])
     hip = blib.HipEvents()
+    exec_map = None
+    if args.skip_kv == "mask":
+        # every cached position ran every block (a dense prefill)
+        exec_map = torch.zeros((cfg["n_layers"], w.batch, cfg["max_ctx"]), dtype=torch.uint8,
+                               device="cuda")
+        exec_map[:, :, :w.ctx] = 1
+    if args.auto_budget:
+        pw = synth.predictor_weights(cfg, cfg["dm_hidden"], seed=3, device="cuda")
+        model.set_budget_predictor(pw)
 
     runs = {}
-    for i, k in enumerate(budgets if not w.mixed else [None]):
+    for i, k in enumerate(budgets if not (w.mixed or args.auto_budget) else [None]):
         ks = synth.budgets(w, seed=1) if w.mixed else [k] * w.batch
-        r = run_budget(model, cfg, w, dk, dv, x0, ks, args.steps, args.warmup, hip, 0)
-        name = "mixed" if w.mixed else str(k)
+        if args.auto_budget:
+            ks = None
+        r = run_budget(model, cfg, w, dk, dv, x0, ks, args.steps, args.warmup, hip, 0, exec_map)
+        name = "auto" if args.auto_budget else "mixed" if w.mixed else str(k)
         runs[name] = r
         log(f"k={name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step, "
             f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline, gate_up {r['kernel_ms'] * 1e3:.1f} us")
 
     head = runs[next(iter(runs))]
-    head_k = budgets[0] if not w.mixed else None
+    head_k = budgets[0] if not (w.mixed or args.auto_budget) else None
     for r in runs.values():
         r.pop("hidden", None)
     d, f = cfg["d_model"], cfg["d_ffn"]
@@ -202,7 +236,7 @@ def main():
     achieved = gate_up_bytes / (head["kernel_ms"] / 1e3) / 1e9
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and head["ks"] is not None and args.skip_kv == "zero":
         cpu = cpu_baseline(cfg, W, dk, dv, x0, head["ks"][0], w.ctx)
 
     out = {
@@ -219,7 +253,9 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "shape": w.shape, "batch": w.batch, "ctx": w.ctx,
-                   "k": head_k if head_k is not None else "mixed",
+                   "k": head_k if head_k is not None else ("predicted" if args.auto_budget
+                                                              else "mixed"),
+                   "skip_kv": args.skip_kv, "router_ctx": args.router_ctx,
                    "weights_kv": w.dtype, "accumulate": "f32", "omega": w.omega,
                    "launch_policy": args.policy,
                    "parallelism": "none (1 GPU)"},
@@ -229,6 +265,7 @@ def main():
                            "step_hbm_frac": round(r["step_hbm_frac"], 4),
                            "layers_used": r["layers_used"],
                            "distinct_routes": r["distinct_routes"],
+                           "mean_k": round(r["mean_k"], 2),
                            "gate_up_us": round(r["kernel_ms"] * 1e3, 2)}
                        for n, r in runs.items()},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
