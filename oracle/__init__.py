@@ -88,6 +88,9 @@ def lib():
                                           C.POINTER(C.c_int32), vp, dp, vp, vp, dp,
                                           C.POINTER(C.c_int32)]
         L.orc_decode_seq_auto.restype = C.c_int
+        L.orc_prefill_seq.argtypes = [C.POINTER(_Config), C.POINTER(_Layer), C.POINTER(_DM),
+                                      vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, dp]
+        L.orc_prefill_seq.restype = C.c_int
         L.orc_prior_normalize.argtypes = [vp, i32, i32, C.c_double, vp]
         L.orc_context_dim.argtypes = [C.POINTER(_Config)]
         L.orc_context_dim.restype = C.c_int
@@ -193,6 +196,34 @@ class Oracle:
         k = lib().orc_predict_budget(C.byref(self._c), C.byref(self._pred), _ptr(z), _ptr(lg),
                                      C.byref(margin))
         return int(k), lg, margin.value
+
+    def prefill_seq(self, kcs, vcs, x, k: int, route=None, execs=None):
+        """Routed prefill of one prompt x [len][d] into rows 0..len-1 of the
+        per-layer caches (modified in place).  Returns (h [len][d], mask,
+        scores, margin)."""
+        L = self.cfg["n_layers"]
+        kp = (C.c_void_p * L)(*[_need(a, self.sdt, "kc").ctypes.data for a in kcs])
+        vp = (C.c_void_p * L)(*[_need(a, self.sdt, "vc").ctypes.data for a in vcs])
+        ep = None
+        if execs is not None:
+            ep = (C.c_void_p * L)(*[_need(a, np.uint8, "exec").ctypes.data for a in execs])
+        x = np.ascontiguousarray(x, dtype=np.float32)
+        n = x.shape[0]
+        h = np.empty((n, self.cfg["d_model"]), dtype=np.float64)
+        mask = np.zeros(self.L_mid, dtype=np.uint8)
+        scores = np.zeros(self.L_mid, dtype=np.float32)
+        margin = C.c_double(0.0)
+        r = None
+        if route is not None:
+            r = np.ascontiguousarray(route, dtype=np.uint8)
+            mask[:] = r
+        rc = lib().orc_prefill_seq(C.byref(self._c), self._layers,
+                                   C.byref(self._dm) if self._dm is not None else None,
+                                   kp, vp, ep, int(n), int(k), _ptr(r), _ptr(x), _ptr(h),
+                                   _ptr(mask), _ptr(scores), C.byref(margin))
+        if rc != 0:
+            raise ValueError("oracle rejected the arguments")
+        return h, mask, scores, margin.value
 
     def decode_seq_auto(self, kcs, vcs, pos: int, x, execs=None):
         """Decode step without a budget (the predictor picks k).  Returns

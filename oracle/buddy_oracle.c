@@ -80,6 +80,65 @@ static void st(void* p, size_t i, int dtype, double v)
 }
 
 
+/* Routed prefill, one route per prompt: the Reuse setting of Sec. 5 keeps
+ * the decode path at the prefill's decision, so the prefill itself is
+ * routed.  Within a block the tokens run in order, each attending to the
+ * rows its predecessors appended, which is the causal prefill of that
+ * block. */
+int orc_prefill_seq(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                    void* const* kc, void* const* vc, uint8_t* const* exec, int32_t len,
+                    int32_t k_budget, const uint8_t* route, const float* x, double* h_out,
+                    uint8_t* mask_out, float* scores_out, double* margin_out)
+{
+    const int L = c->n_layers, Lm = L - 2, d = c->d_model, dt = c->dtype;
+    const int nkv = c->n_kv_heads, hd = c->head_dim, T = c->max_ctx;
+    if (L < 2 || len < 1 || len > T || k_budget < 0 || k_budget > Lm) return -1;
+    if (!route && !dm) return -1;
+    uint8_t* mask = malloc((size_t)(Lm > 0 ? Lm : 1));
+    float* sc = malloc(sizeof(float) * (Lm > 0 ? Lm : 1));
+    double margin = INFINITY;
+    for (size_t i = 0; i < (size_t)len * d; ++i) h_out[i] = (double)x[i];
+
+    /* first block over the prompt */
+    for (int t = 0; t < len; ++t) {
+        if (exec) exec[0][t] = 1;
+        orc_block_ex(c, &layers[0], kc[0], vc[0], t, h_out + (size_t)t * d, exec ? exec[0] : NULL);
+    }
+    /* one route for the prompt: planner at the last token */
+    if (route) {
+        for (int i = 0; i < Lm; ++i) mask[i] = route[i] ? 1 : 0;
+    } else {
+        double* z = malloc(sizeof(double) * orc_context_dim(c));
+        orc_router_context(c, kc[0], vc[0], len - 1, h_out + (size_t)(len - 1) * d, z);
+        orc_dm_scores(c, dm, z, sc);
+        orc_topk(sc, Lm, k_budget, mask, &margin);
+        free(z);
+        if (scores_out) memcpy(scores_out, sc, sizeof(float) * Lm);
+        if (mask_out) memcpy(mask_out, mask, (size_t)Lm);
+    }
+    /* selected blocks causally over the prompt, skipped ones zero-filled */
+    for (int l = 1; l < L; ++l) {
+        const int run = l == L - 1 || mask[l - 1];
+        for (int t = 0; t < len; ++t) {
+            if (exec) exec[l][t] = (uint8_t)run;
+            if (run) {
+                orc_block_ex(c, &layers[l], kc[l], vc[l], t, h_out + (size_t)t * d,
+                             exec ? exec[l] : NULL);
+            } else {
+                for (int g = 0; g < nkv; ++g)
+                    for (int i = 0; i < hd; ++i) {
+                        size_t at = ((size_t)g * T + t) * hd + i;
+                        st(kc[l], at, dt, 0.0);
+                        st(vc[l], at, dt, 0.0);
+                    }
+            }
+        }
+    }
+    if (margin_out) *margin_out = margin;
+    free(mask); free(sc);
+    return 0;
+}
+
 /* ------------------------------------------------------------ prior (App. B) */
 
 static int cmp_double(const void* a, const void* b)

@@ -159,6 +159,20 @@ int orc_decode_seq_auto(const orc_config* c, const orc_layer* layers, const orc_
                         uint8_t* mask_out, float* scores_out, double* margin_out,
                         int32_t* n_exec_out);
 
+/* Routed prefill of one sequence's prompt x[len][d] (rows 0..len-1 of the
+ * cache; len <= max_ctx).  The first block runs over every token; the route
+ * is decided once, from the pooled first-layer cache of the prompt and the
+ * last token's hidden state after the first block (the planner at position
+ * len - 1), unless `route` fixes it; then each selected block runs causally
+ * over all prompt tokens and every skipped block's K/V rows 0..len-1 are
+ * zero-filled (with exec maps: marked 0, selected and always-run blocks 1).
+ * h_out[len][d]: every token's output of the last block.  mask_out,
+ * scores_out, margin_out: as orc_decode_seq (optional).  Returns 0 or -1. */
+int orc_prefill_seq(const orc_config* c, const orc_layer* layers, const orc_dm* dm,
+                    void* const* kc, void* const* vc, uint8_t* const* exec, int32_t len,
+                    int32_t k_budget, const uint8_t* route, const float* x, double* h_out,
+                    uint8_t* mask_out, float* scores_out, double* margin_out);
+
 /* Offline prior normalisation, App. B steps (i)-(iv) over the n routable
  * layers, then the standardisation of Eq. 2.  kind: 0 = perplexity increase
  * (PPL_skip - PPL_full), 1 = Taylor/Fisher/gradient norm, 2 = cosine

@@ -508,3 +508,67 @@ def test_auto_budget_step_equals_budgeted_step():
         assert costmodel.budget_to_k(b_hat, cfg["n_layers"]) == k
         seen.add(k)
 
+
+# ------------------------------------------------------------ routed prefill
+
+def prefill(cfg, orc, xs, k, route=None, execs=None):
+    kc, vc = empty_cache(cfg, orc)
+    h, mask, sc, margin = orc.prefill_seq(kc, vc, xs, k, route=route, execs=execs)
+    return h, mask, sc, (kc, vc)
+
+
+def test_prefill_all_blocks_equals_dense_forward():
+    """k = L - 2: the prefill of every prompt token is the dense causal
+    forward (Eq. 1 with M = 1)."""
+    cfg, layers, dm, orc = make()
+    xs = synth.hidden_inputs(11, cfg["d_model"], seed=51).numpy()
+    h, mask, _, _ = prefill(cfg, orc, xs, orc.L_mid)
+    ref = hf_forward(hf_model(cfg, layers, list(range(cfg["n_layers"]))), xs)
+    assert relerr(h, ref) < 1e-5 and mask.sum() == orc.L_mid
+
+
+def test_prefill_route_and_sub_model():
+    """The prompt's route is the planner's decision at the last token: the
+    first-layer cache pooled over the prompt and the last token's hidden
+    state after the first block (here from a one-block Hugging Face forward);
+    every token's output is the dense forward of {first} + S + {last}, and
+    the skipped blocks hold zeros over the prompt."""
+    cfg, layers, dm, orc = make(omega=0.1)
+    n, k, L = 13, 2, cfg["n_layers"]
+    xs = synth.hidden_inputs(n, cfg["d_model"], seed=52).numpy()
+    h, mask, sc, (kc, vc) = prefill(cfg, orc, xs, k)
+    h0 = hf_forward(hf_model(cfg, layers, [0]), xs)[-1]
+    s_ref = orc.dm_scores(orc.context(kc[0], vc[0], n - 1, h0))
+    assert np.allclose(sc, s_ref, rtol=1e-6, atol=1e-7)
+    assert np.array_equal(mask, Oracle.topk(s_ref, k)[0])
+    keep = [0] + [l for l in range(1, L - 1) if mask[l - 1]] + [L - 1]
+    assert relerr(h, hf_forward(hf_model(cfg, layers, keep), xs)) < 1e-5
+    for l in range(1, L - 1):
+        if not mask[l - 1]:
+            assert np.all(kc[l][:, :n] == 0) and np.all(vc[l][:, :n] == 0)
+
+
+@pytest.mark.parametrize("masked", [False, True])
+def test_prefill_then_decode_equals_token_by_token(masked):
+    """Prefill then decode under the prompt's route is, bit for bit, the
+    decode of every token one by one under that route (the same arithmetic
+    in the same order; caches and, with masking, execution maps equal)."""
+    cfg, layers, dm, orc = make(dtype="bf16", omega=0.1)
+    n, L = 9, cfg["n_layers"]
+    xs = synth.hidden_inputs(n + 3, cfg["d_model"], seed=53).numpy()
+    ex1 = [np.zeros(cfg["max_ctx"], np.uint8) for _ in range(L)] if masked else None
+    ex2 = [np.zeros(cfg["max_ctx"], np.uint8) for _ in range(L)] if masked else None
+    h, mask, _, (kc, vc) = prefill(cfg, orc, xs[:n], 2, execs=ex1)
+    kc2, vc2 = empty_cache(cfg, orc)
+    for t in range(n):
+        h2, *_ = orc.decode_seq(kc2, vc2, t, 2, xs[t], route=mask, execs=ex2)
+        assert np.array_equal(h[t], h2)
+    for t in range(n, n + 3):
+        a, *_ = orc.decode_seq(kc, vc, t, 2, xs[t], route=mask, execs=ex1)
+        b, *_ = orc.decode_seq(kc2, vc2, t, 2, xs[t], route=mask, execs=ex2)
+        assert np.array_equal(a, b)
+    for l in range(L):
+        assert np.array_equal(kc[l], kc2[l]) and np.array_equal(vc[l], vc2[l])
+        if masked:
+            assert np.array_equal(ex1[l], ex2[l])
+
