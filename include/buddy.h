@@ -222,6 +222,28 @@ buddy_status buddy_decode_step_auto(buddy_model* m, const buddy_kv* kv, float* h
                                     int32_t* k_out, uint8_t* mask_out, float* scores_out,
                                     void* stream);
 
+/* Routed prefill of B prompts into cache rows 0..len[b]-1 (one route per
+ * prompt; the Reuse setting of Sec. 5 keeps decoding on the prefill's
+ * decision, so the prefill itself is routed).  The first block runs over
+ * every prompt token; the planner and Decision Module decide the route once
+ * per prompt at its last token (as a decode step at position len[b]-1
+ * would), unless route_override gives it; each selected block then runs
+ * causally over the prompt, and every skipped block's K/V rows 0..len[b]-1
+ * are zero-filled (with BUDDY_SKIP_KV_MASK also marked in kv->exec).
+ *   hidden: device [B][t_stride][d] fp32, the prompt tokens' inputs,
+ *           overwritten with their last-block outputs (rows t >= len[b]
+ *           untouched).
+ *   len:    host [B], 1 <= len[b] <= min(t_stride, max_ctx).
+ *   k:      host [B] budgets 0..L-2 (ignored with route_override).
+ *   route_override, mask_out, scores_out: as buddy_decode_step.
+ * Rows of all prompts together: B * t_stride <= 65535.  Grows the handle's
+ * prefill workspace when needed and returns after the device has finished
+ * (the host waits for the route to build the per-block token lists). */
+buddy_status buddy_prefill(buddy_model* m, const buddy_kv* kv, float* hidden, int32_t t_stride,
+                           const int32_t* len, const int32_t* k, int32_t B, int32_t skip_kv,
+                           const uint8_t* route_override, uint8_t* mask_out, float* scores_out,
+                           void* stream);
+
 /* How buddy_decode_step launches the routable blocks.
  *   BUDDY_LAUNCH_DEVICE_ROUTED: everything is enqueued without waiting; every
  *     routable block is launched and its kernels read the routed row count

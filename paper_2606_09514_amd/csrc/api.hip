@@ -11,6 +11,8 @@
 #include <chrono>
 #include <new>
 
+#include <vector>
+
 #include "buddy_internal.h"
 
 using namespace buddy;
@@ -105,12 +107,21 @@ void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chun
 // not on how many sequences a block routes, so a sequence's arithmetic does
 // not depend on the routes of the others or on the launch policy.
 hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, hipStream_t s) {
-    if (M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && g.K % 128 == 0) {
-        g.XB = M.ws.xb;
-        g.ldxb = M.ws.xb_ld;
+    if (M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && g.K % 128 == 0)
         return launch_mfma(pro, epi, g, s);
-    }
     return launch_gemv(M.cfg.dtype, pro, epi, g, s);
+}
+
+// Activation buffers of a block's launches and the meaning of a row id: a
+// sequence (decode, tok_T = 0) or a flattened prompt token (prefill).
+struct BlockBufs {
+    float* q; float* o; float* m;
+    bf16_t* xb; int xb_ld;
+    int tok_T;
+};
+
+BlockBufs decode_bufs(const Model& M) {
+    return BlockBufs{M.ws.q, M.ws.o, M.ws.m, M.ws.xb, M.ws.xb_ld, 0};
 }
 
 // Timing hook: event around kernel `kind` of block l, if asked for.
@@ -135,7 +146,8 @@ hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
 }
 
 buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float* hidden, int l,
-                       Rows rows, int batch, int max_pos, int pos_u, hipStream_t s) {
+                       Rows rows, int batch, int max_pos, int pos_u, const BlockBufs& bf,
+                       hipStream_t s) {
     const buddy_config& c = M.cfg;
     const buddy_layer_weights& w = M.layers[l];
     const int qdim = c.n_heads * c.head_dim;
@@ -149,11 +161,13 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
     g.bcap = c.max_batch; g.pos = M.ws.pos; g.pos_u = pos_u; g.rope = M.ws.rope;
     g.kc = (void*)layer_base(M, kv->k, l);
     g.vc = (void*)layer_base(M, kv->v, l);
+    g.tok_T = bf.tok_T;
+    g.XB = bf.xb; g.ldxb = bf.xb_ld;
 
     // RMSNorm + QKV projection + rotary + KV append
     g.W = w.wqkv; g.N = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; g.K = c.d_model;
     g.X = hidden; g.ldx = c.d_model; g.gain = w.attn_norm;
-    g.Y = M.ws.q; g.ldy = qdim;
+    g.Y = bf.q; g.ldy = qdim;
     if ((e = mark(M, BUDDY_KERNEL_QKV, l, false, s)) != hipSuccess ||
         (e = launch_proj(M, batch, PRO_RMSNORM, EPI_QKV, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_QKV, l, true, s)) != hipSuccess)
@@ -161,10 +175,20 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
 
     // attention over rows 0..pos
     AttnArgs a;
-    a.q = M.ws.q; a.o = M.ws.o; a.kc = g.kc; a.vc = g.vc;
+    memset(&a, 0, sizeof(a));
+    a.q = bf.q; a.o = bf.o; a.kc = g.kc; a.vc = g.vc;
     a.T = c.max_ctx; a.hd = c.head_dim; a.nq = c.n_heads; a.nkv = c.n_kv_heads;
     a.bcap = c.max_batch; a.pos = M.ws.pos; a.pos_u = pos_u; a.rows = rows;
-    attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
+    a.tok_T = bf.tok_T;
+    if (bf.tok_T > 0) {
+        // prompt tokens: one chunk per row (no merge; the partials are
+        // sized for decode rows only)
+        const int r = attention_rows_per_wg(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads);
+        a.chunks = 1;
+        a.chunk_len = (max_pos + 1 + r - 1) / r * r;
+    } else {
+        attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
+    }
     a.part = M.ws.part; a.max_chunks = M.ws.max_chunks;
     a.exec = exec ? exec + (size_t)l * c.max_batch * c.max_ctx : nullptr;
     if ((e = mark(M, BUDDY_KERNEL_ATTENTION, l, false, s)) != hipSuccess ||
@@ -173,7 +197,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
         return fail_device(M, e, "attention");
 
     // h += Wo o
-    g.W = w.wo; g.N = c.d_model; g.K = qdim; g.X = M.ws.o; g.ldx = qdim; g.gain = nullptr;
+    g.W = w.wo; g.N = c.d_model; g.K = qdim; g.X = bf.o; g.ldx = qdim; g.gain = nullptr;
     g.Y = hidden; g.ldy = c.d_model;
     if ((e = mark(M, BUDDY_KERNEL_O_PROJ, l, false, s)) != hipSuccess ||
         (e = launch_proj(M, batch, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
@@ -182,14 +206,14 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
 
     // m = SiLU(Wg u2) * (Wu u2), u2 = RMSNorm(h)
     g.W = w.wgate_up; g.N = 2 * c.d_ffn; g.K = c.d_model; g.X = hidden; g.ldx = c.d_model;
-    g.gain = w.mlp_norm; g.f = c.d_ffn; g.Y = M.ws.m; g.ldy = c.d_ffn;
+    g.gain = w.mlp_norm; g.f = c.d_ffn; g.Y = bf.m; g.ldy = c.d_ffn;
     if ((e = mark(M, BUDDY_KERNEL_GATE_UP, l, false, s)) != hipSuccess ||
         (e = launch_proj(M, batch, PRO_RMSNORM, EPI_SWIGLU, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_GATE_UP, l, true, s)) != hipSuccess)
         return fail_device(M, e, "gate_up");
 
     // h += Wdown m
-    g.W = w.wdown; g.N = c.d_model; g.K = c.d_ffn; g.X = M.ws.m; g.ldx = c.d_ffn;
+    g.W = w.wdown; g.N = c.d_model; g.K = c.d_ffn; g.X = bf.m; g.ldx = c.d_ffn;
     g.gain = nullptr; g.Y = hidden; g.ldy = c.d_model;
     if ((e = mark(M, BUDDY_KERNEL_DOWN, l, false, s)) != hipSuccess ||
         (e = launch_proj(M, batch, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
@@ -384,6 +408,8 @@ void buddy_model_destroy(buddy_model* h) {
     (void)hipDeviceSynchronize();
     (void)hipFree(h->M.ws_base);
     (void)hipFree(h->M.pred_a);
+    (void)hipFree(h->M.pf_base);
+    free(h->M.pf_hlists);
     (void)hipHostFree(h->M.h_cnt);
     free(h->M.layers);
     free(h->M.timing.start);
@@ -507,7 +533,9 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
 
     const Rows all{M.ws.idx_all, M.ws.n_all, B, true, true};
     // first block on every sequence (appends the first-layer K/V row)
-    if ((st = run_block(M, kv, exec, hidden, 0, all, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
+    if ((st = run_block(M, kv, exec, hidden, 0, all, B, max_pos, pos_u, decode_bufs(M), s)) !=
+        BUDDY_OK)
+        return st;
     // KV-aware planner and Decision Module, unless the route is given
     if (!route_override)
         if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, predict, s)) != BUDDY_OK) return st;
@@ -544,10 +572,12 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
         // every sequence routed (known on the host): the rows are the batch in order
         const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), n_max,
                      host_routed, host_routed && n_max == B};
-        if ((st = run_block(M, kv, exec, hidden, l, r, B, max_pos, pos_u, s)) != BUDDY_OK) return st;
+        if ((st = run_block(M, kv, exec, hidden, l, r, B, max_pos, pos_u, decode_bufs(M), s)) !=
+            BUDDY_OK)
+            return st;
     }
     // last block on every sequence
-    st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, B, max_pos, pos_u, s);
+    st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, B, max_pos, pos_u, decode_bufs(M), s);
     if (M.timing.n > 0 && M.timing.next < M.timing.n) ++M.timing.next;
     return st;
 }
@@ -568,6 +598,145 @@ buddy_status buddy_decode_step_auto(buddy_model* h, const buddy_kv* kv, float* h
                                     void* stream) {
     return decode_impl(h, kv, hidden, pos, nullptr, B, skip_kv, nullptr, true, k_out, mask_out,
                        scores_out, stream);
+}
+
+namespace {
+
+// Grows the prefill workspace to `rows` prompt-token rows (contents are not
+// kept).  Waits for the device before freeing the old one.
+buddy_status ensure_prefill_ws(Model& M, size_t rows) {
+    if (rows <= M.pf_rows) return BUDDY_OK;
+    const buddy_config& c = M.cfg;
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return fail_device(M, e, "prefill workspace");
+    (void)hipFree(M.pf_base);
+    free(M.pf_hlists);
+    M.pf_base = nullptr; M.pf_hlists = nullptr; M.pf_rows = 0;
+    const size_t qdim = (size_t)c.n_heads * c.head_dim;
+    const size_t L = c.n_layers, r16 = (rows + 15) / 16 * 16;
+    struct Part { void** p; size_t bytes; } parts[] = {
+        {(void**)&M.pf_q, rows * qdim * 4}, {(void**)&M.pf_o, rows * qdim * 4},
+        {(void**)&M.pf_m, rows * (size_t)c.d_ffn * 4},
+        {(void**)&M.pf_hlast, (size_t)c.max_batch * c.d_model * 4},
+        {(void**)&M.pf_xb, r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
+        {(void**)&M.pf_lists, L * rows * 4}, {(void**)&M.pf_len, (size_t)c.max_batch * 4},
+    };
+    size_t total = 0;
+    for (auto& q : parts) total += (q.bytes + 255) / 256 * 256;
+    if ((e = hipMalloc(&M.pf_base, total)) != hipSuccess) { M.pf_base = nullptr; return BUDDY_ENOMEM; }
+    M.pf_hlists = (int32_t*)malloc(L * rows * 4);
+    if (!M.pf_hlists) { (void)hipFree(M.pf_base); M.pf_base = nullptr; return BUDDY_ENOMEM; }
+    size_t off = 0;
+    for (auto& q : parts) {
+        *q.p = (char*)M.pf_base + off;
+        off += (q.bytes + 255) / 256 * 256;
+    }
+    M.pf_rows = rows;
+    return BUDDY_OK;
+}
+
+}  // namespace
+
+buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, int32_t t_stride,
+                           const int32_t* len, const int32_t* k, int32_t B, int32_t skip_kv,
+                           const uint8_t* route_override, uint8_t* mask_out, float* scores_out,
+                           void* stream) {
+    if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
+    if (skip_kv != BUDDY_SKIP_KV_ZERO && skip_kv != BUDDY_SKIP_KV_MASK) return BUDDY_EINVAL;
+    if (B == 0) return BUDDY_OK;
+    if (B < 0) return BUDDY_EINVAL;
+    Model& M = h->M;
+    const buddy_config& c = M.cfg;
+    if (B > c.max_batch) return BUDDY_ECAPACITY;
+    if (!hidden || !len || (!k && !route_override) || t_stride < 1) return BUDDY_EINVAL;
+    if ((size_t)B * t_stride > kMaxPrefillRows) return BUDDY_ECAPACITY;
+    const int Lm = c.n_layers - 2;
+    int max_len = 0;
+    bool full = true;
+    for (int b = 0; b < B; ++b) {
+        if (len[b] < 1 || len[b] > t_stride || len[b] > c.max_ctx) return BUDDY_EINVAL;
+        if (!route_override && (k[b] < 0 || k[b] > Lm)) return BUDDY_EINVAL;
+        if (len[b] > max_len) max_len = len[b];
+        full = full && len[b] == t_stride;
+    }
+    uint8_t* exec = skip_kv == BUDDY_SKIP_KV_MASK ? kv->exec : nullptr;
+    if (skip_kv == BUDDY_SKIP_KV_MASK && !exec) return BUDDY_EINVAL;
+    tl_launch_events = {nullptr, nullptr};
+    buddy_status st;
+    if ((st = ensure_prefill_ws(M, (size_t)B * t_stride)) != BUDDY_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    const size_t R = M.pf_rows;
+    const BlockBufs bf{M.pf_q, M.pf_o, M.pf_m, M.pf_xb, M.ws.xb_ld, t_stride};
+
+    // every prompt token (list 0) for the first and last blocks
+    int32_t* hl = M.pf_hlists;
+    int n_all = 0;
+    for (int b = 0; b < B; ++b)
+        for (int t = 0; t < len[b]; ++t) hl[n_all++] = b * t_stride + t;
+    if ((e = hipMemcpyAsync(M.pf_lists, hl, (size_t)n_all * 4, hipMemcpyHostToDevice, s)) !=
+            hipSuccess ||
+        (e = hipMemcpyAsync(M.pf_len, len, (size_t)B * 4, hipMemcpyHostToDevice, s)) != hipSuccess)
+        return fail_device(M, e, "prefill lists");
+    const Rows all{M.pf_lists, nullptr, n_all, true, full};
+    if ((st = run_block(M, kv, nullptr, hidden, 0, all, n_all, max_len - 1, -1, bf, s)) != BUDDY_OK)
+        return st;
+
+    // one route per prompt: the planner and Decision Module at the last token
+    std::vector<uint8_t> mask((size_t)B * (Lm > 0 ? Lm : 1));
+    if (route_override) {
+        if ((e = hipMemcpyAsync(mask.data(), route_override, (size_t)B * Lm, hipMemcpyDeviceToHost,
+                                s)) != hipSuccess ||
+            (e = hipMemcpyAsync(M.ws.mask, route_override, (size_t)B * Lm,
+                                hipMemcpyDeviceToDevice, s)) != hipSuccess)
+            return fail_device(M, e, "prefill route");
+        if (mask_out && (e = hipMemcpyAsync(mask_out, route_override, (size_t)B * Lm,
+                                            hipMemcpyDeviceToDevice, s)) != hipSuccess)
+            return fail_device(M, e, "prefill route");
+    } else {
+        std::vector<int32_t> last(B);
+        for (int b = 0; b < B; ++b) last[b] = len[b] - 1;
+        StepArgs a;
+        int pos_u;
+        if ((st = prepare_step(M, last.data(), k, B, &a, &pos_u, s)) != BUDDY_OK) return st;
+        if ((e = launch_gather_last(hidden, t_stride, c.d_model, M.pf_len, B, M.pf_hlast, s)) !=
+            hipSuccess)
+            return fail_device(M, e, "prefill gather");
+        if ((st = run_planner(M, kv, M.pf_hlast, B, max_len - 1, pos_u, false, s)) != BUDDY_OK)
+            return st;
+        if ((e = launch_route(M, kv->k, kv->v, nullptr, false, nullptr, nullptr, a, nullptr,
+                              mask_out, scores_out, false, -1, s)) != hipSuccess ||
+            (e = hipMemcpyAsync(mask.data(), M.ws.mask, (size_t)B * Lm, hipMemcpyDeviceToHost,
+                                s)) != hipSuccess)
+            return fail_device(M, e, "prefill route");
+    }
+    // zero-filled rows (and execution-map entries) of the skipped blocks
+    if ((e = launch_prefill_fill(M, kv->k, kv->v, exec, M.ws.mask, M.pf_len, B, max_len, s)) !=
+        hipSuccess)
+        return fail_device(M, e, "prefill fill");
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return fail_device(M, e, "prefill route");
+
+    // token lists of the routable blocks, then the blocks over their tokens
+    std::vector<int> n_l(Lm + 1, 0);
+    for (int l = 1; l <= Lm; ++l) {
+        int32_t* dst = hl + (size_t)l * R;
+        for (int b = 0; b < B; ++b)
+            if (mask[(size_t)b * Lm + (l - 1)])
+                for (int t = 0; t < len[b]; ++t) dst[n_l[l]++] = b * t_stride + t;
+    }
+    if (Lm > 0 && (e = hipMemcpyAsync(M.pf_lists + R, hl + R, (size_t)Lm * R * 4,
+                                      hipMemcpyHostToDevice, s)) != hipSuccess)
+        return fail_device(M, e, "prefill lists");
+    for (int l = 1; l <= Lm; ++l) {
+        if (n_l[l] == 0) continue;
+        const Rows r{M.pf_lists + (size_t)l * R, nullptr, n_l[l], true, full && n_l[l] == n_all};
+        if ((st = run_block(M, kv, exec, hidden, l, r, n_l[l], max_len - 1, -1, bf, s)) != BUDDY_OK)
+            return st;
+    }
+    st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, n_all, max_len - 1, -1, bf, s);
+    if (st == BUDDY_OK && (e = hipStreamSynchronize(s)) != hipSuccess)
+        return fail_device(M, e, "prefill");   // the host token lists are reused next call
+    return st;
 }
 
 buddy_status buddy_set_launch_policy(buddy_model* h, int32_t policy) {

@@ -14,6 +14,7 @@ namespace buddy {
 typedef uint16_t bf16_t;
 
 constexpr int kMaxBatch = 256;     // batch capacity limit (one WG scans a column)
+constexpr int kMaxPrefillRows = 65535;  // prompt-token rows of one prefill call (grid z)
 constexpr int kMaxGroup = 8;       // query heads per KV head held in registers
 constexpr int kWave = 64;
 constexpr int kAttnMaxChunks = 256;  // position chunks per (sequence, KV head)
@@ -144,6 +145,14 @@ struct Model {
     buddy_dm_weights dm;
     buddy_predictor_weights pred;  // Budget Predictor head (pred.hidden == 0: none)
     float* pred_a;                 // [max_batch][pred.hidden] its hidden activations
+    // prefill workspace, grown on demand to pf_rows prompt-token rows (one
+    // allocation): queries, attention outputs, SwiGLU outputs, MFMA staging,
+    // per-block token lists [L][rows], prompt lengths, last-token hidden rows
+    void* pf_base; size_t pf_rows;
+    float *pf_q, *pf_o, *pf_m, *pf_hlast;
+    bf16_t* pf_xb;
+    int32_t *pf_lists, *pf_len;
+    int32_t* pf_hlists;            // host copy of the token lists
     Workspace ws;
     void* ws_base;                // one allocation holding the workspace
     int device;
@@ -180,6 +189,15 @@ __device__ __forceinline__ int seq_pos(const int32_t* pos, int pos_u, int b) {
     return pos_u >= 0 ? pos_u : pos[b];
 }
 
+// Cache slot and position of row id b: in a decode step the row is a
+// sequence at its step position; in a prefill (tok_T > 0) it is a flattened
+// prompt token, slot b / tok_T at position b % tok_T.
+__device__ __forceinline__ void slot_pos(int b, int tok_T, const int32_t* pos, int pos_u,
+                                         int& slot, int& p) {
+    if (tok_T > 0) { slot = b / tok_T; p = b - slot * tok_T; }
+    else { slot = b; p = seq_pos(pos, pos_u, b); }
+}
+
 hipError_t launch_setup(const StepArgs& a, const Workspace& ws, hipStream_t s);
 
 // Split sums of the first layer's K/V rows 0..pos; returns the number of
@@ -201,6 +219,16 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t*
                         float* scores_out, bool scores_only, int32_t publish_seq,
                         hipStream_t s);
 
+// Prefill: zero-fills the K/V rows 0..len[b]-1 of every block sequence b
+// skips (mask [B][L-2]) and, with an execution map, writes its entries for
+// those rows in every block.
+hipError_t launch_prefill_fill(const Model& M, void* kc, void* vc, uint8_t* exec,
+                               const uint8_t* mask, const int32_t* len, int B, int max_len,
+                               hipStream_t s);
+// Prefill: the last prompt token's hidden row of every sequence, compacted
+// to [B][d].
+hipError_t launch_gather_last(const float* hidden, int t_stride, int d, const int32_t* len, int B,
+                              float* out, hipStream_t s);
 hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B, int n,
                               uint8_t* mask_out, hipStream_t s);
 
@@ -215,9 +243,10 @@ struct GemvArgs {
     float* Y; int ldy;                 // output rows, indexed by sequence
     const void* bias; int act;         // EPI_BIAS_ACT
     int f;                             // EPI_SWIGLU: rows j and f + j
-    // EPI_QKV: rotary + cache append of this block
+    // EPI_QKV: rotary + cache append of this block (tok_T > 0: rows are
+    // prompt tokens, see slot_pos)
     void* kc; void* vc; int T; int hd; int nq; int nkv; int bcap;
-    const int32_t* pos; int pos_u; const float2* rope;
+    const int32_t* pos; int pos_u; const float2* rope; int tok_T;
     // PRO_POOL: X is unused; row b of the input is the router context,
     // pooled first-layer features of variant ctx (buddy_router_ctx) built
     // from the pool's split partial sums, then h
@@ -268,6 +297,7 @@ struct AttnArgs {
     int chunks, chunk_len;
     float* part; int max_chunks;
     const uint8_t* exec;                // this block's execution map [bcap][T], or null
+    int tok_T;                          // > 0: rows are prompt tokens (slot_pos)
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // Cache rows one attention workgroup reads per block (chunk lengths are

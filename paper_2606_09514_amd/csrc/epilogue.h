@@ -48,7 +48,8 @@ __device__ __forceinline__ void epilogue(const GemvArgs& g, int b, int u, int r0
     } else {  // EPI_QKV
         const int half = g.hd >> 1;
         const int hg = u / half, i = u - hg * half;
-        const int pos = seq_pos(g.pos, g.pos_u, b);
+        int slot, pos;
+        slot_pos(b, g.tok_T, g.pos, g.pos_u, slot, pos);
         if (hg < g.nq + g.nkv) {
             const float2 cs = g.rope[(size_t)pos * half + i];
             const float a0 = v0 * cs.x - v1 * cs.y;
@@ -63,7 +64,7 @@ __device__ __forceinline__ void epilogue(const GemvArgs& g, int b, int u, int r0
             const bool is_k = hg < g.nq + g.nkv;
             const int kvh = is_k ? hg - g.nq : hg - g.nq - g.nkv;
             TW* dst = (TW*)(is_k ? g.kc : g.vc) +
-                      (((size_t)b * g.nkv + kvh) * g.T + pos) * g.hd;
+                      (((size_t)slot * g.nkv + kvh) * g.T + pos) * g.hd;
             St<TW>::put(dst, i, v0);
             St<TW>::put(dst, i + half, v1);
         }

@@ -72,7 +72,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     if (!a.rows.exact && i >= *a.rows.cnt) return;
     const int b = row_seq(a.rows, i);
     const int g = blockIdx.y, c = blockIdx.x;
-    const int pos = seq_pos(a.pos, a.pos_u, b);
+    int slot, pos;
+    slot_pos(b, a.tok_T, a.pos, a.pos_u, slot, pos);
     const int G = a.nq / a.nkv;
     constexpr int lpr = LPR;           // lanes per cache row (hd / V)
     constexpr int rpw = kWave / LPR;   // rows per wavefront pass
@@ -82,13 +83,13 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int j0 = c * a.chunk_len;
     const int j1 = min(j0 + a.chunk_len, pos + 1);
 
-    const size_t base = ((size_t)b * a.nkv + g) * a.T * a.hd + col * V;
+    const size_t base = ((size_t)slot * a.nkv + g) * a.T * a.hd + col * V;
     const T* Kb = (const T*)a.kc + base;
     const T* Vb = (const T*)a.vc + base;
     const int rows_wg = kAttnPasses * 4 * rpw;
     uint4 kr[kAttnPasses], vr[kAttnPasses];
     uint8_t er[kAttnPasses];
-    const uint8_t* exr = a.exec ? a.exec + (size_t)b * a.T : nullptr;
+    const uint8_t* exr = a.exec ? a.exec + (size_t)slot * a.T : nullptr;
     // every K/V row of a block is loaded before any arithmetic on it; rows
     // past the end are clamped to a valid row and masked below
     auto load_block = [&](int jb) {
@@ -250,13 +251,14 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     if (!a.rows.exact && i >= *a.rows.cnt) return;
     const int b = row_seq(a.rows, i);
     const int g = blockIdx.y, c = blockIdx.x;
-    const int pos = seq_pos(a.pos, a.pos_u, b);
+    int slot, pos;
+    slot_pos(b, a.tok_T, a.pos, a.pos_u, slot, pos);
     const int G = a.nq / a.nkv;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int j0 = c * a.chunk_len;
     const int j1 = min(j0 + a.chunk_len, pos + 1);
-    const size_t base = ((size_t)b * a.nkv + g) * a.T * HD;
+    const size_t base = ((size_t)slot * a.nkv + g) * a.T * HD;
     const bf16_t* Kb = (const bf16_t*)a.kc + base;
     const uint32_t* Vb = (const uint32_t*)((const bf16_t*)a.vc + base);   // bf16 pairs
 
@@ -307,7 +309,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         if (a.exec) {
 #pragma unroll
             for (int v = 0; v < 4; ++v)
-                ex[v] = a.exec[(size_t)b * a.T + min(jb + 4 * (lane >> 4) + v, j1 - 1)];
+                ex[v] = a.exec[(size_t)slot * a.T + min(jb + 4 * (lane >> 4) + v, j1 - 1)];
         }
 
         f32x4_t d = {0.f, 0.f, 0.f, 0.f};

@@ -323,6 +323,63 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t*
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- prefill
+
+// One workgroup per (sequence, block): zero rows 0..len-1 of a skipped
+// block (16-byte stores) and, with an execution map, its entries.
+template <typename T>
+__global__ __launch_bounds__(256) void prefill_fill_kernel(void* kc, void* vc, uint8_t* exec,
+                                                           const uint8_t* mask, const int32_t* len,
+                                                           int Lm, int T_cap, int bcap, int nkv,
+                                                           int hd) {
+    const int b = blockIdx.y, l = blockIdx.x;      // block l of 0..Lm+1
+    const int n = len[b];
+    const bool run = l == 0 || l == Lm + 1 || mask[(size_t)b * Lm + (l - 1)];
+    if (exec)
+        for (int t = threadIdx.x; t < n; t += 256) exec[((size_t)l * bcap + b) * T_cap + t] = run;
+    if (run) return;
+    constexpr int V = St<T>::V;
+    const int per_row = hd / V;
+    const size_t layer = (size_t)l * bcap * nkv * T_cap * hd;
+    for (int t = threadIdx.x; t < nkv * n * per_row; t += 256) {
+        const int g = t / (n * per_row), r = t - g * n * per_row;
+        const int row = r / per_row, e = (r - row * per_row) * V;
+        const size_t at = layer + (((size_t)b * nkv + g) * T_cap + row) * hd + e;
+        *reinterpret_cast<uint4*>((T*)kc + at) = make_uint4(0u, 0u, 0u, 0u);
+        *reinterpret_cast<uint4*>((T*)vc + at) = make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+hipError_t launch_prefill_fill(const Model& M, void* kc, void* vc, uint8_t* exec,
+                               const uint8_t* mask, const int32_t* len, int B, int max_len,
+                               hipStream_t s) {
+    const buddy_config& c = M.cfg;
+    (void)max_len;
+    const dim3 grid(c.n_layers, B);
+    if (c.dtype == BUDDY_BF16)
+        prefill_fill_kernel<bf16_t><<<grid, 256, 0, s>>>(kc, vc, exec, mask, len, c.n_layers - 2,
+                                                         c.max_ctx, c.max_batch, c.n_kv_heads,
+                                                         c.head_dim);
+    else
+        prefill_fill_kernel<float><<<grid, 256, 0, s>>>(kc, vc, exec, mask, len, c.n_layers - 2,
+                                                        c.max_ctx, c.max_batch, c.n_kv_heads,
+                                                        c.head_dim);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void gather_last_kernel(const float* hidden, int t_stride, int d,
+                                                          const int32_t* len, float* out) {
+    const int b = blockIdx.x;
+    const float* src = hidden + ((size_t)b * t_stride + len[b] - 1) * d;
+    for (int i = threadIdx.x; i < d; i += 256) out[(size_t)b * d + i] = src[i];
+}
+
+hipError_t launch_gather_last(const float* hidden, int t_stride, int d, const int32_t* len, int B,
+                              float* out, hipStream_t s) {
+    gather_last_kernel<<<B, 256, 0, s>>>(hidden, t_stride, d, len, out);
+    return hipGetLastError();
+}
+
 // ----------------------------------------------------------- select_topk
 
 struct TopkArgs {

@@ -87,6 +87,7 @@ def lib():
         L.buddy_set_budget_predictor.argtypes = [vp, P(PredictorWeights)]
         L.buddy_predict_budget.argtypes = [vp, P(KV), vp, vp, i32, vp, vp, vp]
         L.buddy_decode_step_auto.argtypes = [vp, P(KV), vp, vp, i32, i32, vp, vp, vp, vp]
+        L.buddy_prefill.argtypes = [vp, P(KV), vp, i32, vp, vp, i32, i32, vp, vp, vp, vp]
         L.buddy_prior_normalize.argtypes = [vp, i32, i32, C.c_float, vp]
         L.buddy_prior_normalize.restype = C.c_int
         L.buddy_budget_to_k.argtypes = [C.c_float, i32]
@@ -256,6 +257,25 @@ class Model:
         rc = lib().buddy_decode_step_auto(
             self._h, C.byref(kv), _dev(hidden, "hidden", torch.float32), _host_i32(pos),
             len(pos), int(skip_kv), _dev(k_out, "k_out", torch.int32),
+            _dev(mask_out, "mask_out", torch.uint8), _dev(scores_out, "scores_out", torch.float32),
+            _stream(stream))
+        if check:
+            _raise(rc, self._h)
+        return rc
+
+    def prefill(self, k_cache, v_cache, hidden, lens, k, route_override=None, mask_out=None,
+                scores_out=None, skip_kv: int = SKIP_KV_ZERO, stream=None, check: bool = True,
+                exec_map=None) -> int:
+        """hidden: device [B][t_stride][d] fp32 (in: prompt inputs, out: last
+        block outputs); lens: host prompt lengths; k: host budgets or None
+        with route_override."""
+        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype),
+                _dev(exec_map, "exec_map", torch.uint8))
+        B = len(lens)
+        rc = lib().buddy_prefill(
+            self._h, C.byref(kv), _dev(hidden, "hidden", torch.float32), int(hidden.shape[1]),
+            _host_i32(lens), _host_i32(k) if k is not None else None, B, int(skip_kv),
+            _dev(route_override, "route_override", torch.uint8),
             _dev(mask_out, "mask_out", torch.uint8), _dev(scores_out, "scores_out", torch.float32),
             _stream(stream))
         if check:

@@ -307,6 +307,97 @@ def test_launch_policies_agree_bitwise():
     assert outs[0] == outs[1]
 
 
+# ------------------------------------------------------ routed prefill
+
+def check_prefill(P, lens, ks, t_stride, masked=False, route=None, seed=110):
+    """GPU prefill of B ragged prompts against the oracle's prefill per
+    sequence: routes (margin rule), every prompt token's output, the new K/V
+    rows of every block (zero for skipped blocks), untouched padding rows,
+    and the execution maps with masking.  Returns the oracle's state."""
+    B, L, d = len(lens), P.cfg["n_layers"], P.cfg["d_model"]
+    tol = TOL[P.cfg["dtype"]]
+    hk, hv = P.empty_host_cache()
+    hk[...] = synth.storage_numpy(torch.full((1,), 7.0).to(P.tdt))[0]   # stale contents
+    hv[...] = hk[0, 0, 0, 0, 0]
+    T = P.cfg["max_ctx"]
+    hx = np.full((L, B, T), 7, np.uint8) if masked else None
+    x = synth.hidden_inputs(B * t_stride, d, seed=seed).numpy().reshape(B, t_stride, d)
+    dk, dv = P.upload(hk), P.upload(hv)
+    dx = torch.from_numpy(hx).cuda() if masked else None
+    hidden = torch.from_numpy(x.copy()).cuda()
+    mask = torch.zeros((B, P.L_mid), dtype=torch.uint8, device="cuda")
+    ro = None if route is None else torch.from_numpy(np.asarray(route, np.uint8)).cuda()
+    P.gpu.prefill(dk, dv, hidden, lens, ks, route_override=ro, mask_out=mask,
+                  skip_kv=blib.SKIP_KV_MASK if masked else blib.SKIP_KV_ZERO, exec_map=dx)
+    torch.cuda.synchronize()
+    hg, mg, gk, gv = hidden.cpu().numpy(), mask.cpu().numpy(), P.download(dk), P.download(dv)
+    gx = dx.cpu().numpy() if masked else None
+    rep = dict(margin_mismatches=0, max_hidden_err=0.0)
+    for b in range(B):
+        n = lens[b]
+        pre = (hk[:, b].copy(), hv[:, b].copy(), None if hx is None else hx[:, b].copy())
+        kcs, vcs = [hk[l, b] for l in range(L)], [hv[l, b] for l in range(L)]
+        ex = None if hx is None else [hx[l, b] for l in range(L)]
+        r = None if route is None else route[b]
+        h, m, sc, margin = P.orc.prefill_seq(kcs, vcs, x[b, :n], ks[b] if ks else 0, route=r,
+                                             execs=ex)
+        if not np.array_equal(m, mg[b]):
+            assert margin < MARGIN, f"prefill route mismatch at margin {margin} (seq {b})"
+            rep["margin_mismatches"] += 1
+            hk[:, b], hv[:, b] = pre[0], pre[1]
+            if hx is not None:
+                hx[:, b] = pre[2]
+            h, *_ = P.orc.prefill_seq(kcs, vcs, x[b, :n], 0, route=mg[b], execs=ex)
+        for t in range(n):
+            err = relerr(hg[b, t], h[t])
+            rep["max_hidden_err"] = max(rep["max_hidden_err"], err)
+            assert err < tol, f"seq {b} token {t}: {err}"
+        assert np.array_equal(hg[b, n:], x[b, n:])            # padding rows untouched
+        run = np.concatenate([[1], mg[b], [1]])
+        for l in range(L):
+            for ref, got in ((hk, gk), (hv, gv)):
+                rr, gg = f32(ref[l, b, :, :n], P.sdt), f32(got[l, b, :, :n], P.sdt)
+                if run[l]:
+                    assert relerr(gg, rr) < tol, f"KV rows of block {l}, seq {b}"
+                else:
+                    assert np.all(gg == 0) and np.all(rr == 0)
+            assert np.array_equal(got[l, b, :, n:], ref[l, b, :, n:])   # later rows untouched
+        if masked:
+            assert np.array_equal(gx[:, b, :n], hx[:, b, :n])
+    print(P.cfg["dtype"], lens, rep)
+    return hk, hv, hx, mg, x
+
+
+@pytest.mark.parametrize("masked", [False, True])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_prefill_matches_oracle(dtype, masked):
+    """Routed prefill of three ragged prompts (17, 40 and 5 tokens) with
+    budgets 2, 5 and 0, then one decode step that reuses each prompt's
+    route (Reuse, Sec. 5) teacher-forced against the oracle."""
+    P = Pair("tiny", dtype, 48, 3, seed=111, omega=0.1)
+    lens, ks = [17, 40, 5], [2, 5, 0]
+    hk, hv, hx, mg, x = check_prefill(P, lens, ks, 40, masked=masked)
+    dk, dv = P.upload(hk), P.upload(hv)
+    dx = torch.from_numpy(hx).cuda() if masked else None
+    xd = synth.hidden_inputs(3, P.cfg["d_model"], seed=112).numpy()
+    rep = new_report()
+    compare_step(P, hk, hv, dk, dv, xd, lens, ks, rep, hx=hx, dx=dx)
+
+
+@pytest.mark.parametrize("G", [1, 4])
+def test_prefill_head_dim_128(G):
+    """Prompts of 150 and 64 tokens on head_dim 128 (MFMA attention for
+    G = 4, the vector kernel for G = 1), bf16 MFMA projections."""
+    P = Pair(gqa_shape(G), "bf16", 160, 2, seed=113 + G, omega=0.1)
+    check_prefill(P, [150, 64], [1, 2], 150, seed=114)
+
+
+def test_prefill_route_override():
+    P = Pair("tiny", "bf16", 32, 2, seed=115, omega=0.1)
+    route = np.array([[1, 0, 0, 1, 1, 0], [0, 0, 0, 0, 0, 0]], np.uint8)
+    check_prefill(P, [20, 9], None, 24, route=route, seed=116)
+
+
 # --------------------------------------------------- Budget Predictor
 
 def attach_predictor(P, hidden=32, seed=95):
