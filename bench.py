@@ -117,6 +117,32 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
                 mean_k=float(kk.mean()), hidden=hidden, end_pos=pos)
 
 
+def run_prefill(model, cfg, w, dk, dv, ks_list, reps, warmup):
+    """Routed prefill of a prompt of w.ctx tokens per sequence at each
+    budget: prompt tokens per second (the call returns after the device)."""
+    import torch
+    from paper_2606_09514_amd import synth
+
+    B, n = w.batch, w.ctx
+    x = synth.hidden_inputs(B * n, cfg["d_model"], seed=5, device="cuda").reshape(B, n, -1)
+    out = {}
+    for k in ks_list:
+        hidden = torch.empty_like(x)
+        times = []
+        for r in range(warmup + reps):
+            hidden.copy_(x)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            model.prefill(dk, dv, hidden, [n] * B, [k] * B)
+            torch.cuda.synchronize()
+            if r >= warmup:
+                times.append(time.perf_counter() - t0)
+        ms = 1e3 * sorted(times)[len(times) // 2]
+        out[str(k)] = dict(ms_per_prefill=round(ms, 3), tokens_per_s=round(B * n / (ms / 1e3), 1))
+        log(f"prefill k={k}: {ms:.2f} ms for {B} x {n} tokens, {B * n / (ms / 1e3):.0f} tokens/s")
+    return out
+
+
 def cpu_baseline(cfg, W, dk, dv, x0, k, ctx, budget_s=12.0):
     """The oracle on the host cores: decode steps of sequence 0 of the same
     workload until about budget_s seconds of CPU work (at least one)."""
@@ -158,6 +184,9 @@ def main():
                     help="router context features")
     ap.add_argument("--auto-budget", action="store_true",
                     help="budget-free steps: a random-init Budget Predictor picks k")
+    ap.add_argument("--prefill", action="store_true",
+                    help="time the routed prefill of a prompt of the workload's context length "
+                         "at each budget and the dense one, instead of decode steps")
     ap.add_argument("--steps", type=int, default=128)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="llama3_8b_b1_ctx2048")
@@ -213,6 +242,24 @@ def main():
     if args.auto_budget:
         pw = synth.predictor_weights(cfg, cfg["dm_hidden"], seed=3, device="cuda")
         model.set_budget_predictor(pw)
+
+    if args.prefill:
+        Lm = cfg["n_layers"] - 2
+        ks_list = sorted(set(budgets) | {Lm}) if not w.mixed else [Lm]
+        pf = run_prefill(model, cfg, w, dk, dv, ks_list, reps=3, warmup=1)
+        dense = pf[str(Lm)]["ms_per_prefill"]
+        for r in pf.values():
+            r["speedup_vs_dense"] = round(dense / r["ms_per_prefill"], 3)
+        head_k = ks_list[0]
+        print(json.dumps({
+            "metric": "routed prefill tokens/s at budget k (1 GPU)",
+            "value": pf[str(head_k)]["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1,
+            "higher_is_better": True, "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": w.name, "prompt_tokens": w.ctx, "batch": w.batch, "k": head_k,
+                       "router_ctx": args.router_ctx},
+            "per_budget": pf}), flush=True)
+        model.close()
+        return
 
     runs = {}
     for i, k in enumerate(budgets if not (w.mixed or args.auto_budget) else [None]):
