@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 SO = os.path.join(HERE, "libbuddy.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["api.hip", "k_route.hip", "k_gemv.hip", "k_attn.hip", "k_mfma.hip", "prior.hip"]
+SOURCES = ["api.hip", "k_route.hip", "k_gemv.hip", "k_attn.hip", "k_mfma.hip", "k_gemm.hip", "prior.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 

@@ -107,6 +107,10 @@ void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chun
 // not on how many sequences a block routes, so a sequence's arithmetic does
 // not depend on the routes of the others or on the launch policy.
 hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, hipStream_t s) {
+    // prompt tokens of a prefill: the tiled GEMM
+    if (M.cfg.dtype == BUDDY_BF16 && g.tok_T > 0 && g.rows.exact && batch >= kGemmMinRows &&
+        g.K % 64 == 0)
+        return launch_gemm(pro, epi, g, s);
     if (M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && g.K % 128 == 0)
         return launch_mfma(pro, epi, g, s);
     return launch_gemv(M.cfg.dtype, pro, epi, g, s);

@@ -285,6 +285,13 @@ hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream
 // MFMA path (bf16 weights, K a multiple of 128): prep of the compact bf16
 // rows, then the MFMA projection with the same epilogues.
 hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s);
+// The activation staging of the MFMA paths: routed rows as bf16 in B-operand
+// fragment order (g.XB), RMSNorm / router context folded in per pro.
+hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s);
+// Tiled MFMA GEMM for many rows (prompt tokens): exact row counts, bf16
+// weights, K a multiple of 64.
+hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, hipStream_t s);
+constexpr int kGemmMinRows = 64;
 // Routed rows above which a bf16 projection takes the MFMA path.
 constexpr int kGemvMaxRows = 4;
 

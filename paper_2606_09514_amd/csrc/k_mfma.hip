@@ -246,12 +246,17 @@ static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, hipS
     }
 }
 
-hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s) {
+hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s) {
     const int n_host = g.rows.exact ? g.rows.n_max : -1;
     if (pro == PRO_RMSNORM) prep_kernel<PRO_RMSNORM><<<g.rows.n_max, 256, 0, s>>>(g, n_host);
     else if (pro == PRO_POOL) prep_kernel<PRO_POOL><<<g.rows.n_max, 256, 0, s>>>(g, n_host);
     else prep_kernel<PRO_NONE><<<g.rows.n_max, 256, 0, s>>>(g, n_host);
-    hipError_t e = hipGetLastError();
+    return hipGetLastError();
+}
+
+hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s) {
+    const int n_host = g.rows.exact ? g.rows.n_max : -1;
+    hipError_t e = launch_prep(pro, g, s);
     if (e != hipSuccess) return e;
     if (epi == EPI_QKV) return launch_mfma_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), n_host, s);
     if (epi == EPI_SWIGLU) return launch_mfma_epi<EPI_SWIGLU>(g, g.f, n_host, s);
