@@ -151,7 +151,7 @@ hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
 
 buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float* hidden, int l,
                        Rows rows, int batch, int max_pos, int pos_u, const BlockBufs& bf,
-                       hipStream_t s) {
+                       hipStream_t s, const int32_t* groups = nullptr, int n_groups = 0) {
     const buddy_config& c = M.cfg;
     const buddy_layer_weights& w = M.layers[l];
     const int qdim = c.n_heads * c.head_dim;
@@ -190,6 +190,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
         const int r = attention_rows_per_wg(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads);
         a.chunks = 1;
         a.chunk_len = (max_pos + 1 + r - 1) / r * r;
+        a.groups = groups; a.n_groups = n_groups;
     } else {
         attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
     }
@@ -624,11 +625,12 @@ buddy_status ensure_prefill_ws(Model& M, size_t rows) {
         {(void**)&M.pf_hlast, (size_t)c.max_batch * c.d_model * 4},
         {(void**)&M.pf_xb, r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
         {(void**)&M.pf_lists, L * rows * 4}, {(void**)&M.pf_len, (size_t)c.max_batch * 4},
+        {(void**)&M.pf_groups, L * rows * 8},
     };
     size_t total = 0;
     for (auto& q : parts) total += (q.bytes + 255) / 256 * 256;
     if ((e = hipMalloc(&M.pf_base, total)) != hipSuccess) { M.pf_base = nullptr; return BUDDY_ENOMEM; }
-    M.pf_hlists = (int32_t*)malloc(L * rows * 4);
+    M.pf_hlists = (int32_t*)malloc(L * rows * 12);   // token lists, then group pairs
     if (!M.pf_hlists) { (void)hipFree(M.pf_base); M.pf_base = nullptr; return BUDDY_ENOMEM; }
     size_t off = 0;
     for (auto& q : parts) {
@@ -637,6 +639,23 @@ buddy_status ensure_prefill_ws(Model& M, size_t rows) {
     }
     M.pf_rows = rows;
     return BUDDY_OK;
+}
+
+// Attention groups of a token list (tokens of one prompt contiguous and in
+// order): runs of up to qt consecutive entries of one prompt, as (first
+// entry, count) pairs in out; returns how many.
+int token_groups(const int32_t* list, int n, int t_stride, int qt, int32_t* out) {
+    int ng = 0;
+    for (int i = 0; i < n;) {
+        const int b = list[i] / t_stride;
+        int cnt = 1;
+        while (cnt < qt && i + cnt < n && list[i + cnt] / t_stride == b) ++cnt;
+        out[2 * ng] = i;
+        out[2 * ng + 1] = cnt;
+        ++ng;
+        i += cnt;
+    }
+    return ng;
 }
 
 }  // namespace
@@ -673,17 +692,27 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
     const size_t R = M.pf_rows;
     const BlockBufs bf{M.pf_q, M.pf_o, M.pf_m, M.pf_xb, M.ws.xb_ld, t_stride};
 
-    // every prompt token (list 0) for the first and last blocks
+    // every prompt token (list 0) for the first and last blocks; with more
+    // than one token per attention group, the group pairs of list l at
+    // [L R + 2 l R] (host) and [2 l R] (device)
     int32_t* hl = M.pf_hlists;
+    int32_t* hg = hl + (size_t)c.n_layers * R;
+    const int qt = attention_prefill_group(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads);
+    std::vector<int> n_g(Lm + 1, 0);
     int n_all = 0;
     for (int b = 0; b < B; ++b)
         for (int t = 0; t < len[b]; ++t) hl[n_all++] = b * t_stride + t;
+    if (qt > 1) n_g[0] = token_groups(hl, n_all, t_stride, qt, hg);
     if ((e = hipMemcpyAsync(M.pf_lists, hl, (size_t)n_all * 4, hipMemcpyHostToDevice, s)) !=
             hipSuccess ||
+        (qt > 1 && (e = hipMemcpyAsync(M.pf_groups, hg, (size_t)n_g[0] * 8,
+                                       hipMemcpyHostToDevice, s)) != hipSuccess) ||
         (e = hipMemcpyAsync(M.pf_len, len, (size_t)B * 4, hipMemcpyHostToDevice, s)) != hipSuccess)
         return fail_device(M, e, "prefill lists");
+    auto groups_of = [&](int l) { return qt > 1 ? M.pf_groups + (size_t)2 * l * R : nullptr; };
     const Rows all{M.pf_lists, nullptr, n_all, true, full};
-    if ((st = run_block(M, kv, nullptr, hidden, 0, all, n_all, max_len - 1, -1, bf, s)) != BUDDY_OK)
+    if ((st = run_block(M, kv, nullptr, hidden, 0, all, n_all, max_len - 1, -1, bf, s, groups_of(0),
+                        n_g[0])) != BUDDY_OK)
         return st;
 
     // one route per prompt: the planner and Decision Module at the last token
@@ -727,17 +756,23 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
         for (int b = 0; b < B; ++b)
             if (mask[(size_t)b * Lm + (l - 1)])
                 for (int t = 0; t < len[b]; ++t) dst[n_l[l]++] = b * t_stride + t;
+        if (qt > 1) n_g[l] = token_groups(dst, n_l[l], t_stride, qt, hg + (size_t)2 * l * R);
     }
-    if (Lm > 0 && (e = hipMemcpyAsync(M.pf_lists + R, hl + R, (size_t)Lm * R * 4,
-                                      hipMemcpyHostToDevice, s)) != hipSuccess)
+    if (Lm > 0 && ((e = hipMemcpyAsync(M.pf_lists + R, hl + R, (size_t)Lm * R * 4,
+                                       hipMemcpyHostToDevice, s)) != hipSuccess ||
+                   (qt > 1 && (e = hipMemcpyAsync(M.pf_groups + 2 * R, hg + 2 * R,
+                                                  (size_t)Lm * R * 8, hipMemcpyHostToDevice,
+                                                  s)) != hipSuccess)))
         return fail_device(M, e, "prefill lists");
     for (int l = 1; l <= Lm; ++l) {
         if (n_l[l] == 0) continue;
         const Rows r{M.pf_lists + (size_t)l * R, nullptr, n_l[l], true, full && n_l[l] == n_all};
-        if ((st = run_block(M, kv, exec, hidden, l, r, n_l[l], max_len - 1, -1, bf, s)) != BUDDY_OK)
+        if ((st = run_block(M, kv, exec, hidden, l, r, n_l[l], max_len - 1, -1, bf, s, groups_of(l),
+                            n_g[l])) != BUDDY_OK)
             return st;
     }
-    st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, n_all, max_len - 1, -1, bf, s);
+    st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, n_all, max_len - 1, -1, bf, s,
+                   groups_of(0), n_g[0]);
     if (st == BUDDY_OK && (e = hipStreamSynchronize(s)) != hipSuccess)
         return fail_device(M, e, "prefill");   // the host token lists are reused next call
     return st;

@@ -151,8 +151,8 @@ struct Model {
     void* pf_base; size_t pf_rows;
     float *pf_q, *pf_o, *pf_m, *pf_hlast;
     bf16_t* pf_xb;
-    int32_t *pf_lists, *pf_len;
-    int32_t* pf_hlists;            // host copy of the token lists
+    int32_t *pf_lists, *pf_len, *pf_groups;
+    int32_t* pf_hlists;            // host copy of the token lists, then of the groups
     Workspace ws;
     void* ws_base;                // one allocation holding the workspace
     int device;
@@ -305,10 +305,16 @@ struct AttnArgs {
     float* part; int max_chunks;
     const uint8_t* exec;                // this block's execution map [bcap][T], or null
     int tok_T;                          // > 0: rows are prompt tokens (slot_pos)
+    // prompt tokens on the MFMA score kernel: groups of up to 16 / G
+    // consecutive tokens of one prompt, (first row index, count) pairs; one
+    // workgroup per group (null: one per row)
+    const int32_t* groups; int n_groups;
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // Cache rows one attention workgroup reads per block (chunk lengths are
 // multiples of it).
 int attention_rows_per_wg(int dtype, int hd, int G);
+// Prompt tokens per attention workgroup of a prefill (1: no grouping).
+int attention_prefill_group(int dtype, int hd, int G);
 
 }  // namespace buddy

@@ -241,21 +241,40 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t bf16_bits(float x) { return (uint32_t)f2bf(x); }
 
-template <int GM>
+// MQ (prompt tokens): the 16 MFMA columns are (token, head) pairs of a group
+// of up to 16 / G consecutive tokens of one prompt, column j = token j / G,
+// head j % G, so a slab of K/V rows is read once for the group; each column
+// attends to the rows up to its own token's position (causal).
+template <int GM, bool MQ>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     constexpr int HD = 128, KS = HD / 32;
-    __shared__ float s_p[4][16][16];          // per wave: p[head][slab row]
-    __shared__ float s_al[4][16];             // per wave: rescale of each head
+    __shared__ float s_p[4][16][16];          // per wave: p[column][slab row]
+    __shared__ float s_al[4][16];             // per wave: rescale of each column
     __shared__ float s_acc[4][GM][HD + 2];
     const int i = blockIdx.z;
-    if (!a.rows.exact && i >= *a.rows.cnt) return;
-    const int b = row_seq(a.rows, i);
-    const int g = blockIdx.y, c = blockIdx.x;
-    int slot, pos;
-    slot_pos(b, a.tok_T, a.pos, a.pos_u, slot, pos);
+    if (!MQ && !a.rows.exact && i >= *a.rows.cnt) return;
     const int G = a.nq / a.nkv;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = blockIdx.y, c = blockIdx.x;
+    // this lane's column: token qt of the group (always 0 without MQ), head hq
+    const int first = MQ ? a.groups[2 * i] : i;
+    const int count = MQ ? a.groups[2 * i + 1] : 1;
+    const int qt = MQ ? (lane & 15) / G : 0, hq = MQ ? (lane & 15) % G : (lane & 15);
+    const bool col_ok = MQ ? qt < count : hq < G;
+    const int b = row_seq(a.rows, first);                     // first token: the group's slot
+    const int bq = MQ ? row_seq(a.rows, first + min(qt, count - 1)) : b;
+    int slot, pos, posq;
+    slot_pos(b, a.tok_T, a.pos, a.pos_u, slot, pos);
+    if (MQ) {
+        int sq;
+        slot_pos(bq, a.tok_T, a.pos, a.pos_u, sq, posq);
+        int sl, pl;
+        slot_pos(row_seq(a.rows, first + count - 1), a.tok_T, a.pos, a.pos_u, sl, pl);
+        pos = pl;                                             // the group's last position
+    } else {
+        posq = pos;
+    }
     const int j0 = c * a.chunk_len;
     const int j1 = min(j0 + a.chunk_len, pos + 1);
     const size_t base = ((size_t)slot * a.nkv + g) * a.T * HD;
@@ -266,9 +285,9 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     // softmax weight, as bf16 high + low parts; heads past G are zero
     bf16x8_t qh[KS], ql[KS];
     {
-        const int h = lane & 15, q8 = 8 * (lane >> 4);
+        const int q8 = 8 * (lane >> 4);
         const float qs = 1.4426950408889634f / sqrtf((float)HD);
-        const float* qp = a.q + ((size_t)b * a.nq + g * G + min(h, G - 1)) * HD + q8;
+        const float* qp = a.q + ((size_t)bq * a.nq + g * G + min(hq, G - 1)) * HD + q8;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             const float4 x0 = *reinterpret_cast<const float4*>(qp + 32 * s);
@@ -277,7 +296,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
             uint32_t hi[4], lo[4];
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const float v0 = h < G ? xv[e] * qs : 0.f, v1 = h < G ? xv[e + 1] * qs : 0.f;
+                const float v0 = col_ok ? xv[e] * qs : 0.f, v1 = col_ok ? xv[e + 1] * qs : 0.f;
                 const uint32_t h0 = bf16_bits(v0), h1 = bf16_bits(v1);
                 const float r0 = v0 - __uint_as_float(h0 << 16), r1 = v1 - __uint_as_float(h1 << 16);
                 hi[e / 2] = h0 | (h1 << 16);
@@ -323,7 +342,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int jrow = jb + 4 * (lane >> 4) + v;
-            sc[v] = jrow < j1 && (ex[v] != 0 || jrow == pos) ? d[v] : -INFINITY;
+            sc[v] = jrow < j1 && jrow <= posq && (ex[v] != 0 || jrow == posq) ? d[v] : -INFINITY;
         }
         float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
         mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
@@ -378,9 +397,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     }
     __syncthreads();
 
-    // merge the four wavefronts and write this chunk's partial
+    // merge the four wavefronts and write this chunk's partial (MQ: one
+    // chunk, the output rows of the group's tokens)
     const size_t pstride = (size_t)HD + 2;
-    for (int t = tid; t < G * HD; t += 256) {
+    for (int t = tid; t < (MQ ? count * G : G) * HD; t += 256) {
         const int h = t / HD, e = t % HD;
         float M = -INFINITY;
         for (int w = 0; w < 4; ++w) M = fmaxf(M, s_acc[w][h][HD]);
@@ -390,7 +410,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
             L += s_acc[w][h][HD + 1] * sw;
             A += s_acc[w][h][e] * sw;
         }
-        if (a.chunks == 1) {
+        if (MQ) {
+            const int bt = row_seq(a.rows, first + h / G);
+            a.o[((size_t)bt * a.nq + g * G + h % G) * HD + e] = A / L;
+        } else if (a.chunks == 1) {
             a.o[((size_t)b * a.nq + g * G + h) * HD + e] = A / L;
         } else {
             float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
@@ -438,6 +461,10 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 
 static bool attn_uses_mfma(int dtype, int hd, int G) { return dtype == BUDDY_BF16 && hd == 128 && G >= 3 && G <= kMaxGroup; }
 
+int attention_prefill_group(int dtype, int hd, int G) {
+    return attn_uses_mfma(dtype, hd, G) ? 16 / G : 1;
+}
+
 int attention_rows_per_wg(int dtype, int hd, int G) {
     if (attn_uses_mfma(dtype, hd, G)) return 64;
     // G rounded up to the register class the launcher picks
@@ -449,9 +476,14 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     dim3 grid(a.chunks, a.nkv, a.rows.n_max);
     const int G = a.nq / a.nkv;   // query heads per KV head, held in registers
     // lanes per cache row: hd / 8 (bf16) or hd / 4 (fp32); head_dim is 64 or 128
+    if (a.groups) {               // prompt-token groups (one chunk)
+        if (!attn_uses_mfma(dtype, a.hd, G) || a.chunks != 1) return hipErrorInvalidValue;
+        launch_main(attn_mfma_kernel<16, true>, dim3(1, a.nkv, a.n_groups), dim3(256), 0, s, a);
+        return hipGetLastError();
+    }
     if (attn_uses_mfma(dtype, a.hd, G)) {
-        if (G <= 4) launch_main(attn_mfma_kernel<4>, grid, dim3(256), 0, s, a);
-        else launch_main(attn_mfma_kernel<kMaxGroup>, grid, dim3(256), 0, s, a);
+        if (G <= 4) launch_main(attn_mfma_kernel<4, false>, grid, dim3(256), 0, s, a);
+        else launch_main(attn_mfma_kernel<kMaxGroup, false>, grid, dim3(256), 0, s, a);
     } else if (dtype == BUDDY_BF16) {
         if (a.hd == 128) {
             if (G == 1) launch_main(attn_kernel<bf16_t, 1, 16>, grid, dim3(256), 0, s, a);

@@ -384,12 +384,15 @@ def test_prefill_matches_oracle(dtype, masked):
     compare_step(P, hk, hv, dk, dv, xd, lens, ks, rep, hx=hx, dx=dx)
 
 
-@pytest.mark.parametrize("G", [1, 4])
-def test_prefill_head_dim_128(G):
-    """Prompts of 150 and 64 tokens on head_dim 128 (MFMA attention for
-    G = 4, the vector kernel for G = 1), bf16 MFMA projections."""
+@pytest.mark.parametrize("G,masked", [(1, False), (3, False), (4, False), (4, True), (5, False),
+                                      (8, False)])
+def test_prefill_head_dim_128(G, masked):
+    """Prompts of 150 and 61 tokens on head_dim 128, bf16 projections.  For
+    G >= 3 the MFMA score kernel takes groups of 16 / G consecutive tokens
+    of one prompt per workgroup (ragged last groups: 150 and 61 are not
+    multiples of 2, 3, 4 or 5); G = 1 uses the vector kernel."""
     P = Pair(gqa_shape(G), "bf16", 160, 2, seed=113 + G, omega=0.1)
-    check_prefill(P, [150, 64], [1, 2], 150, seed=114)
+    check_prefill(P, [150, 61], [1, 2], 150, masked=masked, seed=114)
 
 
 def test_prefill_route_override():
