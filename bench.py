@@ -58,10 +58,13 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, exec_map=None):
+def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, exec_map=None,
+               running_pool=False):
     """ks: budgets per sequence, or None for budget-free steps (the attached
     Budget Predictor picks them); exec_map: execution map for skipped-KV
-    masking, or None for zero-filled skipped KV."""
+    masking, or None for zero-filled skipped KV; running_pool: the planner
+    keeps running sums of the first block's rows (fresh state per budget,
+    so the first warm-up step sums the whole cache)."""
     import numpy as np
     import torch
     from paper_2606_09514_amd import costmodel
@@ -72,15 +75,16 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     masks = torch.zeros((steps, B, Lm), dtype=torch.uint8, device="cuda")
     k_pred = torch.zeros((steps, B), dtype=torch.int32, device="cuda")
     skip = blib.SKIP_KV_ZERO if exec_map is None else blib.SKIP_KV_MASK
+    pool = model.pool_state() if running_pool else None
 
     def step(pos, t=None):
         mo = None if t is None else masks[t]
         if ks is None:
             model.decode_step_auto(dk, dv, hidden, [pos] * B, k_out=k_pred[t or 0], mask_out=mo,
-                                   skip_kv=skip, exec_map=exec_map)
+                                   skip_kv=skip, exec_map=exec_map, pool=pool)
         else:
             model.decode_step(dk, dv, hidden, [pos] * B, ks, mask_out=mo, skip_kv=skip,
-                              exec_map=exec_map)
+                              exec_map=exec_map, pool=pool)
 
     pos = w.ctx
     for _ in range(warmup):
@@ -104,7 +108,8 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     hip.destroy(starts + stops)
     m = masks.cpu().numpy()
     kk = k_pred.cpu().numpy() if ks is None else np.array([ks] * steps)
-    step_bytes = [costmodel.step_bytes(cfg, m[t], positions[t]) for t in range(steps)]
+    step_bytes = [costmodel.step_bytes(cfg, m[t], positions[t], running_pool)
+                  for t in range(steps)]
     total_bytes = sum(s["total"] for s in step_bytes)
     assert all(int(m[t, b].sum()) == kk[t, b] for t in range(steps) for b in range(B))
     distinct = len({m[t].tobytes() for t in range(steps)})
@@ -182,6 +187,9 @@ def main():
                     help="KV of skipped blocks: zero-filled (the paper's) or masked")
     ap.add_argument("--router-ctx", choices=["kv", "k", "v", "k+v"], default="kv",
                     help="router context features")
+    ap.add_argument("--pool", choices=["scan", "running"], default="scan",
+                    help="router pool: sum the first block's rows every step, or keep "
+                         "running sums across steps")
     ap.add_argument("--auto-budget", action="store_true",
                     help="budget-free steps: a random-init Budget Predictor picks k")
     ap.add_argument("--prefill", action="store_true",
@@ -266,7 +274,8 @@ def main():
         ks = synth.budgets(w, seed=1) if w.mixed else [k] * w.batch
         if args.auto_budget:
             ks = None
-        r = run_budget(model, cfg, w, dk, dv, x0, ks, args.steps, args.warmup, hip, 0, exec_map)
+        r = run_budget(model, cfg, w, dk, dv, x0, ks, args.steps, args.warmup, hip, 0, exec_map,
+                       running_pool=args.pool == "running")
         name = "auto" if args.auto_budget else "mixed" if w.mixed else str(k)
         runs[name] = r
         log(f"k={name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step, "
@@ -302,7 +311,7 @@ def main():
         "config": {"workload": w.name, "shape": w.shape, "batch": w.batch, "ctx": w.ctx,
                    "k": head_k if head_k is not None else ("predicted" if args.auto_budget
                                                               else "mixed"),
-                   "skip_kv": args.skip_kv, "router_ctx": args.router_ctx,
+                   "skip_kv": args.skip_kv, "router_ctx": args.router_ctx, "pool": args.pool,
                    "weights_kv": w.dtype, "accumulate": "f32", "omega": w.omega,
                    "launch_policy": args.policy,
                    "parallelism": "none (1 GPU)"},

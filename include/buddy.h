@@ -138,6 +138,24 @@ typedef struct {
                        dense prefill), each step writes every block's entry
                        at its position.  Blocks 0 and L-1 run for every
                        token, so their maps are all ones.                  */
+    /* Running-sum pool (optional; both NULL or both set).  The KV-aware
+     * planner's context is the mean of the first block's K and V rows
+     * 0..pos (Sec. 4.3).  With these arrays the planner keeps, per sequence
+     * and KV head, the fp32 sums of rows 0..pool_rows-1 and adds only the
+     * rows it has not seen, instead of summing all pos + 1 rows each call:
+     *   pool_sum:  device fp32 [max_batch][n_kv][2][hd], K sums then V sums
+     *   pool_rows: device int32 [max_batch][n_kv], rows held in pool_sum
+     * A call at position p adds rows pool_rows..p-1 (rows older than the
+     * step, which the step does not rewrite) and sets pool_rows = p; row p
+     * enters that call's mean without entering the sums, so repeating a step
+     * at the same position stays exact.  pool_rows > p starts the sums over;
+     * where pool_rows is 0 the contents of pool_sum are not read.
+     * The caller zeroes pool_rows before first use and again for a slot
+     * whenever it rewrites that slot's cached rows below pool_rows;
+     * buddy_prefill does so itself for the slots it fills.  Sums are in a
+     * different order than a fresh scan: equal up to fp32 rounding.       */
+    float* pool_sum;
+    int32_t* pool_rows;
 } buddy_kv;
 
 typedef struct buddy_model buddy_model;

@@ -68,10 +68,12 @@ def dm_weight_bytes(cfg: dict) -> int:
     return (H * din + H + Lm * H + Lm) * _s(cfg["dtype"])
 
 
-def step_bytes(cfg: dict, masks, positions) -> dict:
+def step_bytes(cfg: dict, masks, positions, running_pool: bool = False) -> dict:
     """Algorithmic bytes of one step given the realised per-sequence masks
     (each a sequence of L-2 zeros/ones) and the positions written this step.
-    Attention of a sequence at position p reads p + 1 cached rows."""
+    Attention of a sequence at position p reads p + 1 cached rows; the pool
+    reads the first block's rows 0..p, or with running sums (steady state)
+    the previous row, the new row and the kept fp32 sums."""
     L = cfg["n_layers"]
     s = _s(cfg["dtype"])
     row = 2 * cfg["n_kv_heads"] * cfg["head_dim"] * s          # one K row + one V row
@@ -82,7 +84,11 @@ def step_bytes(cfg: dict, masks, positions) -> dict:
         kv += n_exec * row * (p + 1)
         used.update(l + 1 for l, v in enumerate(m) if v)
     weights = len(used) * layer_weight_bytes(cfg)
-    pool = sum(row * (p + 1) for p in positions)
+    if running_pool:
+        sums = 2 * cfg["n_kv_heads"] * cfg["head_dim"] * 4
+        pool = len(positions) * (2 * row + 2 * sums)
+    else:
+        pool = sum(row * (p + 1) for p in positions)
     dmw = dm_weight_bytes(cfg)
     writes = len(positions) * L * row
     return dict(weights=weights, kv=kv, pool=pool, dm=dmw, kv_writes=writes,

@@ -32,6 +32,11 @@ buddy_status fail_device(Model& M, hipError_t e, const char* where) {
     return BUDDY_EDEVICE;
 }
 
+// Caches present; the running-sum pool arrays both given or both absent.
+bool kv_ok(const buddy_kv* kv) {
+    return kv && kv->k && kv->v && (kv->pool_sum == nullptr) == (kv->pool_rows == nullptr);
+}
+
 buddy_status check_config(const buddy_config* c) {
     if (!c) return BUDDY_EINVAL;
     if (c->n_layers < 2 || c->n_layers - 2 > 255) return BUDDY_ESHAPE;
@@ -235,8 +240,13 @@ buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, in
     const buddy_config& c = M.cfg;
     hipError_t e;
     int splits = 1;
-    if ((e = launch_pool(M, kv->k, kv->v, B, max_pos, pos_u, &splits, s)) != hipSuccess)
+    if (kv->pool_sum) {
+        if ((e = launch_pool_running(M, kv->k, kv->v, kv->pool_sum, kv->pool_rows, B, pos_u, s)) !=
+            hipSuccess)
+            return fail_device(M, e, "pool");
+    } else if ((e = launch_pool(M, kv->k, kv->v, B, max_pos, pos_u, &splits, s)) != hipSuccess) {
         return fail_device(M, e, "pool");
+    }
     GemvArgs g;
     memset(&g, 0, sizeof(g));
     g.W = M.dm.w1; g.N = c.dm_hidden;
@@ -424,7 +434,7 @@ void buddy_model_destroy(buddy_model* h) {
 
 buddy_status buddy_pool_route(buddy_model* h, const buddy_kv* kv, const int32_t* pos,
                               const float* h_new, int32_t B, float* scores_out, void* stream) {
-    if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
+    if (!h || !kv_ok(kv)) return BUDDY_EINVAL;
     if (B == 0) return BUDDY_OK;
     if (B < 0) return BUDDY_EINVAL;
     Model& M = h->M;
@@ -448,7 +458,7 @@ buddy_status buddy_pool_route(buddy_model* h, const buddy_kv* kv, const int32_t*
 buddy_status buddy_predict_budget(buddy_model* h, const buddy_kv* kv, const int32_t* pos,
                                   const float* h_new, int32_t B, int32_t* k_out,
                                   float* logits_out, void* stream) {
-    if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
+    if (!h || !kv_ok(kv)) return BUDDY_EINVAL;
     if (B == 0) return BUDDY_OK;
     if (B < 0) return BUDDY_EINVAL;
     Model& M = h->M;
@@ -507,7 +517,7 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
                          const int32_t* k, int32_t B, int32_t skip_kv,
                          const uint8_t* route_override, bool predict, int32_t* k_out,
                          uint8_t* mask_out, float* scores_out, void* stream) {
-    if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
+    if (!h || !kv_ok(kv)) return BUDDY_EINVAL;
     if (skip_kv != BUDDY_SKIP_KV_ZERO && skip_kv != BUDDY_SKIP_KV_MASK) return BUDDY_EINVAL;
     if (B == 0) return BUDDY_OK;
     if (B < 0) return BUDDY_EINVAL;
@@ -664,7 +674,7 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
                            const int32_t* len, const int32_t* k, int32_t B, int32_t skip_kv,
                            const uint8_t* route_override, uint8_t* mask_out, float* scores_out,
                            void* stream) {
-    if (!h || !kv || !kv->k || !kv->v) return BUDDY_EINVAL;
+    if (!h || !kv_ok(kv)) return BUDDY_EINVAL;
     if (skip_kv != BUDDY_SKIP_KV_ZERO && skip_kv != BUDDY_SKIP_KV_MASK) return BUDDY_EINVAL;
     if (B == 0) return BUDDY_OK;
     if (B < 0) return BUDDY_EINVAL;
@@ -689,6 +699,11 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
     if ((st = ensure_prefill_ws(M, (size_t)B * t_stride)) != BUDDY_OK) return st;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e;
+    // the prompt rewrites the first block's rows of slots 0..B-1: their
+    // running pool sums start over
+    if (kv->pool_rows && (e = hipMemsetAsync(kv->pool_rows, 0, (size_t)B * c.n_kv_heads * 4, s)) !=
+                             hipSuccess)
+        return fail_device(M, e, "prefill pool");
     const size_t R = M.pf_rows;
     const BlockBufs bf{M.pf_q, M.pf_o, M.pf_m, M.pf_xb, M.ws.xb_ld, t_stride};
 

@@ -205,6 +205,11 @@ hipError_t launch_setup(const StepArgs& a, const Workspace& ws, hipStream_t s);
 // them, PRO_POOL).
 hipError_t launch_pool(const Model& M, const void* k0, const void* v0, int B, int max_pos,
                        int pos_u, int* splits, hipStream_t s);
+// The same context from running sums (buddy_kv.pool_sum / pool_rows): adds
+// the rows not yet summed, writes one split of partial sums (row pos
+// included) for the fold.
+hipError_t launch_pool_running(const Model& M, const void* k0, const void* v0, float* pool_sum,
+                               int32_t* pool_rows, int B, int pos_u, hipStream_t s);
 
 // Decision Module second layer + prior + top-k (or the override mask), then
 // zero-fill of skipped K/V rows and per-block compaction.

@@ -7,6 +7,9 @@
 //                 ranges; the Decision Module's first GEMV folds the splits
 //                 into the means and joins the newest hidden state,
 //                 z = [mean K | mean V | h] (PRO_POOL in k_gemv.hip).
+//  pool_running_kernel  the same sums kept across steps in caller memory:
+//                 only rows not yet summed are read (normally one per
+//                 sequence and step).
 //  route_kernel   Decision Module output layer plus prior fusion (Eq. 2),
 //                 deterministic top-k by rank counting, zero-fill of the K/V
 //                 row of every skipped block (Conclusion: non-executed states
@@ -109,6 +112,81 @@ hipError_t launch_pool(const Model& M, const void* k0, const void* v0, int B, in
     dim3 grid(splits, c.n_kv_heads, B);
     if (c.dtype == BUDDY_BF16) pool_kernel<bf16_t><<<grid, 256, 0, s>>>(p);
     else pool_kernel<float><<<grid, 256, 0, s>>>(p);
+    return hipGetLastError();
+}
+
+// Running sums: one workgroup per (KV head, sequence) owns its record, so
+// the sums and the row count need no synchronisation between workgroups.
+// Rows n0..pos-1 join the kept sums (n0 = pool_rows; a count of 0 or above
+// pos starts over from empty sums); row pos joins only this call's split.
+template <typename T>
+__global__ __launch_bounds__(1024) void pool_running_kernel(PoolParams p, float* sum,
+                                                            int32_t* rows) {
+    constexpr int V = St<T>::V;
+    __shared__ float red[2][16][128];   // [K|V][wavefront][hd] partial sums
+    const int g = blockIdx.x, b = blockIdx.y;
+    const int tid = threadIdx.x;
+    const int pos = seq_pos(p.pos, p.pos_u, b);
+    int32_t* cnt = rows + (size_t)b * p.nkv + g;
+    float* rec = sum + ((size_t)b * p.nkv + g) * 2 * p.hd;
+    int n0 = *cnt;
+    const bool restart = n0 <= 0 || n0 > pos;   // count 0: the kept sums are not read
+    if (restart) n0 = 0;
+    const int cpr = p.hd / V, rpp = 1024 / cpr;
+    const int col = tid % cpr, slot = tid / cpr;
+    const size_t base = ((size_t)b * p.nkv + g) * p.T * p.hd;
+    const T* K = (const T*)p.k0 + base;
+    const T* Vc = (const T*)p.v0 + base;
+    float ak[V], av[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) ak[e] = av[e] = 0.f;
+    for (int j = n0 + slot; j < pos; j += rpp) {
+        float kr[V], vr[V];
+        St<T>::vec(K + (size_t)j * p.hd + col * V, kr);
+        St<T>::vec(Vc + (size_t)j * p.hd + col * V, vr);
+#pragma unroll
+        for (int e = 0; e < V; ++e) { ak[e] += kr[e]; av[e] += vr[e]; }
+    }
+    // rows of one wavefront first (lanes cpr apart share a column), then
+    // the 16 wavefronts through LDS
+    const int lane = tid & 63, wave = tid >> 6;
+    for (int o = cpr; o < kWave; o <<= 1) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            ak[e] += __shfl_xor(ak[e], o, kWave);
+            av[e] += __shfl_xor(av[e], o, kWave);
+        }
+    }
+    if (lane < cpr) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            red[0][wave][col * V + e] = ak[e];
+            red[1][wave][col * V + e] = av[e];
+        }
+    }
+    __syncthreads();   // every thread has also read *cnt before it is replaced
+    float* part = p.part + ((size_t)b * p.nkv + g) * p.max_splits * 2 * p.hd;
+    for (int t = tid; t < 2 * p.hd; t += 1024) {
+        const int which = t / p.hd, e = t % p.hd;
+        float acc = restart ? 0.f : rec[t];
+        for (int w = 0; w < 16; ++w) acc += red[which][w][e];
+        rec[t] = acc;
+        part[t] = acc + St<T>::get(which ? Vc : K, (size_t)pos * p.hd + e);
+    }
+    if (tid == 0) *cnt = pos;
+}
+
+hipError_t launch_pool_running(const Model& M, const void* k0, const void* v0, float* pool_sum,
+                               int32_t* pool_rows, int B, int pos_u, hipStream_t s) {
+    const buddy_config& c = M.cfg;
+    PoolParams p;
+    p.k0 = k0; p.v0 = v0; p.pos = M.ws.pos; p.pos_u = pos_u;
+    p.part = M.ws.pool_part;
+    p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.max_splits = M.ws.max_pool_splits;
+    p.splits = 1;
+    dim3 grid(c.n_kv_heads, B);
+    if (c.dtype == BUDDY_BF16) pool_running_kernel<bf16_t><<<grid, 1024, 0, s>>>(p, pool_sum, pool_rows);
+    else pool_running_kernel<float><<<grid, 1024, 0, s>>>(p, pool_sum, pool_rows);
     return hipGetLastError();
 }
 

@@ -49,7 +49,8 @@ class PredictorWeights(C.Structure):
 
 
 class KV(C.Structure):
-    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("exec", C.c_void_p)]
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("exec", C.c_void_p),
+                ("pool_sum", C.c_void_p), ("pool_rows", C.c_void_p)]
 
 
 class BuddyError(RuntimeError):
@@ -207,13 +208,27 @@ class Model:
         except Exception:
             pass
 
+    def pool_state(self, device="cuda"):
+        """Zeroed running-sum pool state (sums fp32 [max_batch][n_kv][2][hd],
+        row counts int32 [max_batch][n_kv]) for the `pool` argument."""
+        c = self.cfg
+        shape = (self._c.max_batch, c["n_kv_heads"])
+        return (torch.zeros(shape + (2, c["head_dim"]), dtype=torch.float32, device=device),
+                torch.zeros(shape, dtype=torch.int32, device=device))
+
+    def _kv(self, k_cache, v_cache, exec_map=None, pool=None):
+        ps, pr = pool if pool is not None else (None, None)
+        return KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype),
+                  _dev(exec_map, "exec_map", torch.uint8), _dev(ps, "pool_sum", torch.float32),
+                  _dev(pr, "pool_rows", torch.int32))
+
     def decode_step(self, k_cache, v_cache, hidden, pos, k, route_override=None,
                     mask_out=None, scores_out=None, skip_kv: int = SKIP_KV_ZERO,
-                    stream=None, check: bool = True, exec_map=None) -> int:
+                    stream=None, check: bool = True, exec_map=None, pool=None) -> int:
         """exec_map: device uint8 [L][max_batch][max_ctx] execution map, for
-        skip_kv = SKIP_KV_MASK."""
-        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype),
-                _dev(exec_map, "exec_map", torch.uint8))
+        skip_kv = SKIP_KV_MASK; pool: running-sum pool state (pool_state())
+        or None to sum the first block's rows afresh."""
+        kv = self._kv(k_cache, v_cache, exec_map, pool)
         B = len(pos)
         rc = lib().buddy_decode_step(
             self._h, C.byref(kv), _dev(hidden, "hidden", torch.float32), _host_i32(pos),
@@ -238,8 +253,8 @@ class Model:
         self._pred = weights
 
     def predict_budget(self, k_cache, v_cache, pos, h_new, k_out, logits_out=None, stream=None,
-                       check: bool = True) -> int:
-        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype))
+                       check: bool = True, pool=None) -> int:
+        kv = self._kv(k_cache, v_cache, None, pool)
         rc = lib().buddy_predict_budget(self._h, C.byref(kv), _host_i32(pos),
                                         _dev(h_new, "h_new", torch.float32), len(pos),
                                         _dev(k_out, "k_out", torch.int32),
@@ -251,9 +266,8 @@ class Model:
 
     def decode_step_auto(self, k_cache, v_cache, hidden, pos, k_out=None, mask_out=None,
                          scores_out=None, skip_kv: int = SKIP_KV_ZERO, stream=None,
-                         check: bool = True, exec_map=None) -> int:
-        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype),
-                _dev(exec_map, "exec_map", torch.uint8))
+                         check: bool = True, exec_map=None, pool=None) -> int:
+        kv = self._kv(k_cache, v_cache, exec_map, pool)
         rc = lib().buddy_decode_step_auto(
             self._h, C.byref(kv), _dev(hidden, "hidden", torch.float32), _host_i32(pos),
             len(pos), int(skip_kv), _dev(k_out, "k_out", torch.int32),
@@ -265,12 +279,11 @@ class Model:
 
     def prefill(self, k_cache, v_cache, hidden, lens, k, route_override=None, mask_out=None,
                 scores_out=None, skip_kv: int = SKIP_KV_ZERO, stream=None, check: bool = True,
-                exec_map=None) -> int:
+                exec_map=None, pool=None) -> int:
         """hidden: device [B][t_stride][d] fp32 (in: prompt inputs, out: last
         block outputs); lens: host prompt lengths; k: host budgets or None
         with route_override."""
-        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype),
-                _dev(exec_map, "exec_map", torch.uint8))
+        kv = self._kv(k_cache, v_cache, exec_map, pool)
         B = len(lens)
         rc = lib().buddy_prefill(
             self._h, C.byref(kv), _dev(hidden, "hidden", torch.float32), int(hidden.shape[1]),
@@ -294,8 +307,8 @@ class Model:
                                              a if n else None, b if n else None, n), self._h)
 
     def pool_route(self, k_cache, v_cache, pos, h_new, scores_out, stream=None,
-                   check: bool = True) -> int:
-        kv = KV(_dev(k_cache, "k_cache", self.dtype), _dev(v_cache, "v_cache", self.dtype))
+                   check: bool = True, pool=None) -> int:
+        kv = self._kv(k_cache, v_cache, None, pool)
         rc = lib().buddy_pool_route(self._h, C.byref(kv), _host_i32(pos),
                                     _dev(h_new, "h_new", torch.float32), len(pos),
                                     _dev(scores_out, "scores_out", torch.float32),

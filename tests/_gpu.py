@@ -81,21 +81,22 @@ def oracle_step(P, hk, hv, b, pos, k, x, route=None, hx=None):
     return P.orc.decode_seq(kcs, vcs, pos, k, x, route=route, execs=execs)
 
 
-def gpu_step(P, dk, dv, x, pos, ks, route=None, dx=None):
-    """One GPU step; dx: device execution map (skipped-KV masking) or None."""
+def gpu_step(P, dk, dv, x, pos, ks, route=None, dx=None, pool=None):
+    """One GPU step; dx: device execution map (skipped-KV masking) or None;
+    pool: running-sum pool state or None."""
     B = len(pos)
     hidden = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
     mask = torch.zeros((B, P.L_mid), dtype=torch.uint8, device="cuda")
     scores = torch.zeros((B, P.L_mid), dtype=torch.float32, device="cuda")
     ro = None if route is None else torch.from_numpy(np.asarray(route, np.uint8)).cuda()
     P.gpu.decode_step(dk, dv, hidden, pos, ks, route_override=ro, mask_out=mask,
-                      scores_out=scores, exec_map=dx,
+                      scores_out=scores, exec_map=dx, pool=pool,
                       skip_kv=blib.SKIP_KV_ZERO if dx is None else blib.SKIP_KV_MASK)
     torch.cuda.synchronize()
     return hidden.cpu().numpy(), mask.cpu().numpy(), scores.cpu().numpy()
 
 
-def compare_step(P, hk, hv, dk, dv, x, pos, ks, report, hx=None, dx=None):
+def compare_step(P, hk, hv, dk, dv, x, pos, ks, report, hx=None, dx=None, pool=None):
     """Teacher-forced step: the GPU caches (and execution maps hx/dx, with
     masking) hold the oracle's state on entry.  Runs both sides, applies the
     parity rules, and leaves the oracle's post-step state in hk/hv/hx (re-run
@@ -103,7 +104,7 @@ def compare_step(P, hk, hv, dk, dv, x, pos, ks, report, hx=None, dx=None):
     oracle outputs [B][d]."""
     B = len(pos)
     tol = TOL[P.cfg["dtype"]]
-    hg, mg, sg = gpu_step(P, dk, dv, x, pos, ks, dx=dx)
+    hg, mg, sg = gpu_step(P, dk, dv, x, pos, ks, dx=dx, pool=pool)
     gk, gv = P.download(dk), P.download(dv)
     gx = None if dx is None else dx.cpu().numpy()
     out = np.zeros((B, P.cfg["d_model"]))

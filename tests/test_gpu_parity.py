@@ -14,7 +14,7 @@ from oracle import Oracle
 from paper_2606_09514_amd import lib as blib
 from paper_2606_09514_amd import synth
 
-from _gpu import TOL, Pair, compare_step, f32, gpu_step, oracle_step, relerr
+from _gpu import MARGIN, TOL, Pair, compare_step, f32, gpu_step, oracle_step, relerr
 
 pytestmark = pytest.mark.gpu
 
@@ -97,10 +97,10 @@ def test_router_context_variants(ctx, dtype):
 
 # ------------------------------------------------ multi-step decode parity
 
-def run_teacher_forced(P, prompt, n_decode, ks, report):
+def run_teacher_forced(P, prompt, n_decode, ks, report, pool=None):
     """Prompt tokens go through the decode step one by one, then n_decode
     steps feed back the final hidden state; every step starts from the
-    oracle's state (teacher forcing)."""
+    oracle's state (teacher forcing).  pool: running-sum pool state."""
     B = P.batch
     hk, hv = P.empty_host_cache()
     dk, dv = P.upload(hk), P.upload(hv)
@@ -110,7 +110,7 @@ def run_teacher_forced(P, prompt, n_decode, ks, report):
         dk.copy_(P.upload(hk))
         dv.copy_(P.upload(hv))
         x_t = prompt[:, t] if t < prompt.shape[1] else x
-        out, mg = compare_step(P, hk, hv, dk, dv, x_t, [t] * B, ks, report)
+        out, mg = compare_step(P, hk, hv, dk, dv, x_t, [t] * B, ks, report, pool=pool)
         masks.append(mg)
         x = out.astype(np.float32)
     return masks
@@ -673,10 +673,11 @@ def test_masked_attention_random_history(G, B):
     print(G, B, rep)
 
 
-def sampled_full_size(name, samples, seed=0):
+def sampled_full_size(name, samples, seed=0, running_pool=False):
     """One step of a full-size workload on the GPU; the sampled sequences
     are checked against the oracle (their caches and the weights are copied
-    to the host)."""
+    to the host).  running_pool: the planner starts zeroed running sums (a
+    cold start over every cached row)."""
     w = synth.WORKLOADS[name]
     P = Pair(w.shape, w.dtype, w.ctx + 2, w.batch, seed=seed, omega=w.omega, device_gen=True)
     dk, dv = synth.kv_cache(P.cfg, w.batch, w.ctx, seed=1, device="cuda")
@@ -686,7 +687,10 @@ def sampled_full_size(name, samples, seed=0):
     L = P.cfg["n_layers"]
     pre = {b: (synth.storage_numpy(dk[:, b]).copy(), synth.storage_numpy(dv[:, b]).copy())
            for b in samples}
-    hg, mg, _ = gpu_step(P, dk, dv, x, pos, ks)
+    pool = P.gpu.pool_state() if running_pool else None
+    hg, mg, _ = gpu_step(P, dk, dv, x, pos, ks, pool=pool)
+    if running_pool:
+        assert torch.all(pool[1] == w.ctx)
     tol = 2e-2
     report = new_report()
     for b in samples:
@@ -730,3 +734,105 @@ def test_qwen2_7b_b64_ctx8192_sampled():
 
 def test_mha_13b_b96_ctx2048_mixed_sampled():
     sampled_full_size("mha_13b_b96_ctx2048_mixed", samples=[0, 95])
+
+
+def test_llama3_8b_b32_ctx4096_running_pool_sampled():
+    sampled_full_size("llama3_8b_b32_ctx4096_mixed", samples=[5, 30], running_pool=True)
+
+
+# ------------------------------------------------ running-sum pool (Sec. 4.3)
+
+@pytest.mark.parametrize("dtype,shape", [("f32", "tiny"), ("bf16", "tiny"),
+                                         ("bf16", "llama3_8b")])
+def test_running_pool_scores(dtype, shape):
+    """Planner scores from running sums across calls: positions that advance
+    by one and by several rows, a repeated position whose newest row has
+    changed, a position below the kept count (start over), and a slot reset
+    by the caller; every call against the oracle's fresh means, and the kept
+    sums against numpy sums of rows 0..pos-1."""
+    B, T = 4, 300
+    P = Pair(shape, dtype, T, B, seed=3, omega=0.1, device_gen=(shape != "tiny"))
+    hk, hv = P.empty_host_cache()
+    g = torch.Generator().manual_seed(6)
+    hk[0] = synth.storage_numpy(torch.randn(hk[0].shape, generator=g).to(P.tdt))
+    hv[0] = synth.storage_numpy(torch.randn(hk[0].shape, generator=g).to(P.tdt))
+    h = synth.hidden_inputs(B, P.cfg["d_model"], seed=7)
+    pool = P.gpu.pool_state()
+    schedule = [[0, 5, 40, 298], [1, 6, 41, 299], [4, 9, 60, 299], [4, 9, 60, 299],
+                [2, 9, 10, 100], [3, 10, 11, 101]]
+    for call, pos in enumerate(schedule):
+        if call == 3:   # the newest rows change between two calls at one position
+            for b in range(B):
+                hk[0, b, :, pos[b]] = hk[0, b, :, pos[b] + 1 if pos[b] + 1 < T else 0]
+        if call == 5:   # the caller resets slot 1 (its rows "replaced")
+            pool[1][1].zero_()
+            hv[0, 1, :, :4] = hv[0, 1, :, 4:8]
+        scores = torch.zeros((B, P.L_mid), device="cuda")
+        P.gpu.pool_route(P.upload(hk), P.upload(hv), pos, h.cuda(), scores, pool=pool)
+        got = scores.cpu().numpy()
+        rows = pool[1].cpu().numpy()
+        sums = pool[0].cpu().numpy()
+        for b in range(B):
+            z = np.concatenate([P.orc.pool(hk[0, b], hv[0, b], pos[b]),
+                                h[b].numpy().astype(np.float64)])
+            ref = P.orc.dm_scores(z)
+            assert np.max(np.abs(got[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref)))), \
+                (call, b)
+            assert np.all(rows[b] == pos[b])
+            for which, c in ((0, hk), (1, hv)):
+                ref_sum = f32(c[0, b, :, :pos[b]], P.sdt).astype(np.float64).sum(axis=1)
+                scale = max(1.0, float(np.max(np.abs(ref_sum))))
+                assert np.max(np.abs(sums[b, :, which] - ref_sum)) <= 1e-5 * scale * \
+                    max(1, pos[b]) ** 0.5, (call, b, which)
+
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_running_pool_decode_teacher_forced(dtype, policy):
+    """Decode steps with the running-sum pool against the oracle's fresh
+    means: 24 prompt tokens one by one, then 8 fed-back steps, B = 4, k = 3,
+    teacher-forced."""
+    w = synth.WORKLOADS["tiny_b4_prompt64"]
+    P = Pair(w.shape, dtype, 40, w.batch, seed=0, omega=w.omega, policy=policy)
+    prompt = synth.hidden_inputs(w.batch * 24, P.cfg["d_model"], seed=1).numpy() \
+        .reshape(w.batch, 24, -1)
+    rep = new_report()
+    pool = P.gpu.pool_state()
+    run_teacher_forced(P, prompt, 8, [3] * w.batch, rep, pool=pool)
+    assert torch.all(pool[1] == 31)
+    print(dtype, rep)
+
+
+def test_running_pool_prefill_then_decode():
+    """The prefill restarts the sums of the slots it fills (stale counts
+    planted), its planner leaves rows 0..len-2 summed, and a decode step
+    after it adds row len-1; both against the oracle."""
+    P = Pair("tiny", "bf16", 48, 3, seed=111, omega=0.1)
+    pool = P.gpu.pool_state()
+    pool[1].fill_(2)     # stale sums that a missed restart would keep
+    pool[0].fill_(3.0)
+    lens, ks = [17, 40, 5], [2, 5, 0]
+    B, L, d, T = 3, P.cfg["n_layers"], P.cfg["d_model"], 48
+    x = synth.hidden_inputs(B * 40, d, seed=110).numpy().reshape(B, 40, d)
+    hk, hv = P.empty_host_cache()
+    dk, dv = P.upload(hk), P.upload(hv)
+    hidden = torch.from_numpy(x.copy()).cuda()
+    mask = torch.zeros((B, P.L_mid), dtype=torch.uint8, device="cuda")
+    P.gpu.prefill(dk, dv, hidden, lens, ks, mask_out=mask, pool=pool)
+    torch.cuda.synchronize()
+    assert pool[1].cpu().numpy().tolist() == [[n - 1] * P.cfg["n_kv_heads"] for n in lens]
+    mg = mask.cpu().numpy()
+    for b in range(B):
+        kcs, vcs = [hk[l, b] for l in range(L)], [hv[l, b] for l in range(L)]
+        h, m, sc, margin = P.orc.prefill_seq(kcs, vcs, x[b, :lens[b]], ks[b])
+        if not np.array_equal(m, mg[b]):
+            assert margin < MARGIN
+            hk[:, b], hv[:, b] = 0, 0
+            P.orc.prefill_seq(kcs, vcs, x[b, :lens[b]], 0, route=mg[b])
+    dk.copy_(P.upload(hk))
+    dv.copy_(P.upload(hv))
+    rep = new_report()
+    xd = synth.hidden_inputs(3, d, seed=112).numpy()
+    compare_step(P, hk, hv, dk, dv, xd, lens, [1, 2, 3], rep, pool=pool)
+    assert pool[1].cpu().numpy().tolist() == [[n] * P.cfg["n_kv_heads"] for n in lens]
+    print(rep)
