@@ -40,7 +40,7 @@ class _Config(C.Structure):
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ffn", C.c_int32),
                 ("dm_hidden", C.c_int32), ("dm_act", C.c_int32), ("dtype", C.c_int32),
                 ("max_ctx", C.c_int32), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
-                ("router_ctx", C.c_int32)]
+                ("router_ctx", C.c_int32), ("start_layer", C.c_int32)]
 
 
 class _Layer(C.Structure):
@@ -137,7 +137,8 @@ class Oracle:
 
     cfg keys: n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn,
     dm_hidden, dm_act ('silu'|'gelu'), dtype ('f32'|'bf16'), max_ctx,
-    rms_eps, rope_theta, router_ctx ('kv'|'k'|'v'|'k+v', default 'kv').  layers: list of dicts with attn_norm, wqkv, wo,
+    rms_eps, rope_theta, router_ctx ('kv'|'k'|'v'|'k+v', default 'kv'),
+    start_layer (default 1).  layers: list of dicts with attn_norm, wqkv, wo,
     mlp_norm, wgate_up, wdown.  dm: dict with w1, b1, w2, b2, prior (float32
     or None) and omega.
     """
@@ -149,7 +150,7 @@ class Oracle:
                           cfg["head_dim"], cfg["d_ffn"], cfg.get("dm_hidden", 0),
                           ACTS[cfg.get("dm_act", "silu")], DTYPES[cfg["dtype"]],
                           cfg["max_ctx"], float(cfg["rms_eps"]), float(cfg["rope_theta"]),
-                          CTXS[cfg.get("router_ctx", "kv")])
+                          CTXS[cfg.get("router_ctx", "kv")], int(cfg.get("start_layer", 1)))
         self._keep = []
         arr = (_Layer * len(layers))()
         for i, lw in enumerate(layers):
@@ -175,8 +176,8 @@ class Oracle:
         self._pred = None
 
     def set_predictor(self, pred: dict | None):
-        """Budget Predictor weights {w1 [H][din], b1 [H], w2 [L-2][H], b2
-        [L-2]} as storage arrays, or None."""
+        """Budget Predictor weights {w1 [H][din], b1 [H], w2 [L_mid][H], b2
+        [L_mid]} as storage arrays, or None."""
         if pred is None:
             self._pred = None
             return
@@ -189,7 +190,7 @@ class Oracle:
         self._pred = p
 
     def predict_budget(self, z):
-        """(k_hat, logits [L-2] fp32, best - second best logit)."""
+        """(k_hat, logits [L_mid] fp32, best - second best logit)."""
         z = np.ascontiguousarray(z, dtype=np.float64)
         lg = np.empty(self.L_mid, dtype=np.float32)
         margin = C.c_double(0.0)
@@ -252,8 +253,13 @@ class Oracle:
         return h, k.value, lg, pm.value, mask, scores, margin.value, n_exec.value
 
     @property
+    def start_layer(self) -> int:
+        return int(self.cfg.get("start_layer", 1))
+
+    @property
     def L_mid(self) -> int:
-        return self.cfg["n_layers"] - 2
+        """Routable blocks S..L-2 (S = start_layer)."""
+        return self.cfg["n_layers"] - 1 - self.start_layer
 
     # -- pieces ---------------------------------------------------------
     def rmsnorm(self, h, g):

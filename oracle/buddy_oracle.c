@@ -11,7 +11,8 @@
  * Paper passages followed (section / equation of the paper):
  *   - layer skipping, Sec. 3.1 Eq. (1): a skipped block is the identity on H;
  *   - first and last blocks always run, k = round(b L) - 2 routable blocks,
- *     Sec. 4.2.1 and Eq. (2);
+ *     Sec. 4.2.1 and Eq. (2); the start-layer ablation of Sec. 4.3 moves the
+ *     router after the first S blocks, which then all run;
  *   - score fusion s' = s + omega p~ and top-k selection, Eq. (2);
  *   - two-layer MLP scorer over pooled context, Sec. 4.2.3 and App. C.1;
  *   - KV-aware planner: the first layer's KV cache plus the newest token as
@@ -31,6 +32,18 @@
 #ifdef _OPENMP
 #include <omp.h>
 #endif
+
+/* ------------------------------------------------------------ start layer */
+
+int orc_start_layer(const orc_config* c)
+{
+    return c->start_layer > 0 ? c->start_layer : 1;
+}
+
+int orc_n_mid(const orc_config* c)
+{
+    return c->n_layers - 1 - orc_start_layer(c);
+}
 
 /* ---------------------------------------------------------------- storage */
 
@@ -90,26 +103,29 @@ int orc_prefill_seq(const orc_config* c, const orc_layer* layers, const orc_dm* 
                     int32_t k_budget, const uint8_t* route, const float* x, double* h_out,
                     uint8_t* mask_out, float* scores_out, double* margin_out)
 {
-    const int L = c->n_layers, Lm = L - 2, d = c->d_model, dt = c->dtype;
+    const int L = c->n_layers, S = orc_start_layer(c), Lm = orc_n_mid(c);
+    const int d = c->d_model, dt = c->dtype;
     const int nkv = c->n_kv_heads, hd = c->head_dim, T = c->max_ctx;
-    if (L < 2 || len < 1 || len > T || k_budget < 0 || k_budget > Lm) return -1;
+    if (L < 2 || Lm < 0 || len < 1 || len > T || k_budget < 0 || k_budget > Lm) return -1;
     if (!route && !dm) return -1;
     uint8_t* mask = malloc((size_t)(Lm > 0 ? Lm : 1));
     float* sc = malloc(sizeof(float) * (Lm > 0 ? Lm : 1));
     double margin = INFINITY;
     for (size_t i = 0; i < (size_t)len * d; ++i) h_out[i] = (double)x[i];
 
-    /* first block over the prompt */
-    for (int t = 0; t < len; ++t) {
-        if (exec) exec[0][t] = 1;
-        orc_block_ex(c, &layers[0], kc[0], vc[0], t, h_out + (size_t)t * d, exec ? exec[0] : NULL);
-    }
+    /* the always-run leading blocks over the prompt */
+    for (int l = 0; l < S; ++l)
+        for (int t = 0; t < len; ++t) {
+            if (exec) exec[l][t] = 1;
+            orc_block_ex(c, &layers[l], kc[l], vc[l], t, h_out + (size_t)t * d,
+                         exec ? exec[l] : NULL);
+        }
     /* one route for the prompt: planner at the last token */
     if (route) {
         for (int i = 0; i < Lm; ++i) mask[i] = route[i] ? 1 : 0;
     } else {
         double* z = malloc(sizeof(double) * orc_context_dim(c));
-        orc_router_context(c, kc[0], vc[0], len - 1, h_out + (size_t)(len - 1) * d, z);
+        orc_router_context(c, kc[S - 1], vc[S - 1], len - 1, h_out + (size_t)(len - 1) * d, z);
         orc_dm_scores(c, dm, z, sc);
         orc_topk(sc, Lm, k_budget, mask, &margin);
         free(z);
@@ -117,8 +133,8 @@ int orc_prefill_seq(const orc_config* c, const orc_layer* layers, const orc_dm* 
         if (mask_out) memcpy(mask_out, mask, (size_t)Lm);
     }
     /* selected blocks causally over the prompt, skipped ones zero-filled */
-    for (int l = 1; l < L; ++l) {
-        const int run = l == L - 1 || mask[l - 1];
+    for (int l = S; l < L; ++l) {
+        const int run = l == L - 1 || mask[l - S];
         for (int t = 0; t < len; ++t) {
             if (exec) exec[l][t] = (uint8_t)run;
             if (run) {
@@ -348,8 +364,9 @@ void orc_block_ex(const orc_config* c, const orc_layer* w, void* kc, void* vc,
 
 /* ----------------------------------------------------------------- router */
 
-/* KV-aware planner (Sec. 4.3): the first layer's cache, with the newest
- * token's row already appended, is averaged over positions 0..pos. */
+/* KV-aware planner (Sec. 4.3): the first layer's cache (block S-1's under
+ * the start-layer ablation), with the newest token's row already appended,
+ * is averaged over positions 0..pos. */
 void orc_pool(const orc_config* c, const void* kc, const void* vc, int32_t pos,
               double* z)
 {
@@ -403,7 +420,7 @@ void orc_router_context(const orc_config* c, const void* kc, const void* vc, int
 void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
                    float* scores)
 {
-    const int H = c->dm_hidden, Lm = c->n_layers - 2;
+    const int H = c->dm_hidden, Lm = orc_n_mid(c);
     const int din = orc_context_dim(c);
     double* a = malloc(sizeof(double) * H);
     double* s = malloc(sizeof(double) * Lm);
@@ -427,7 +444,7 @@ void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
 int32_t orc_predict_budget(const orc_config* c, const orc_predictor* p, const double* z,
                            float* logits, double* margin)
 {
-    const int H = p->hidden, Lm = c->n_layers - 2;
+    const int H = p->hidden, Lm = orc_n_mid(c);
     const int din = orc_context_dim(c);
     double* a = malloc(sizeof(double) * H);
     double* s = malloc(sizeof(double) * Lm);
@@ -509,9 +526,10 @@ static int decode_core(const orc_config* c, const orc_layer* layers, const orc_d
                        int32_t* n_exec_out, int32_t* k_out, float* logits_out,
                        double* pmargin_out)
 {
-    const int L = c->n_layers, Lm = L - 2, d = c->d_model, dt = c->dtype;
+    const int L = c->n_layers, S = orc_start_layer(c), Lm = orc_n_mid(c);
+    const int d = c->d_model, dt = c->dtype;
     const int nkv = c->n_kv_heads, hd = c->head_dim, T = c->max_ctx;
-    if (L < 2 || pos < 0 || pos >= T) return -1;
+    if (L < 2 || Lm < 0 || pos < 0 || pos >= T) return -1;
     if (pred ? (route || Lm < 1) : (k_budget < 0 || k_budget > Lm)) return -1;
     if (!route && !dm) return -1;
 
@@ -521,17 +539,21 @@ static int decode_core(const orc_config* c, const orc_layer* layers, const orc_d
     double margin = INFINITY;
     for (int i = 0; i < d; ++i) h[i] = (double)x[i];
 
-    /* first block always runs (Sec. 4.2.1); it appends the newest token's
-     * first-layer K/V, which the planner then sees */
-    if (exec) exec[0][pos] = 1;
-    orc_block_ex(c, &layers[0], kc[0], vc[0], pos, h, exec ? exec[0] : NULL);
+    /* the first block always runs (Sec. 4.2.1), and so do the blocks before
+     * the start layer; they append the newest token's K/V, which the planner
+     * then sees */
+    for (int l = 0; l < S; ++l) {
+        if (exec) exec[l][pos] = 1;
+        orc_block_ex(c, &layers[l], kc[l], vc[l], pos, h, exec ? exec[l] : NULL);
+    }
 
     if (route) {
         for (int i = 0; i < Lm; ++i) mask[i] = route[i] ? 1 : 0;
     } else {
-        /* router context: pooled first-layer features, newest hidden after block 0 */
+        /* router context: pooled features of block S-1's cache, newest
+         * hidden after block S-1 */
         double* z = malloc(sizeof(double) * orc_context_dim(c));
-        orc_router_context(c, kc[0], vc[0], pos, h, z);
+        orc_router_context(c, kc[S - 1], vc[S - 1], pos, h, z);
         if (pred) {   /* no budget given: the predictor's k from the same context */
             k_budget = orc_predict_budget(c, pred, z, logits_out, pmargin_out);
             if (k_out) *k_out = k_budget;
@@ -543,12 +565,12 @@ static int decode_core(const orc_config* c, const orc_layer* layers, const orc_d
         if (mask_out) memcpy(mask_out, mask, (size_t)Lm);
     }
 
-    /* routable blocks 1..L-2, Eq. (1): run when selected; when skipped, h is
+    /* routable blocks S..L-2, Eq. (1): run when selected; when skipped, h is
      * unchanged and the layer's K/V slot at pos is zero-filled (Sec. 6) */
-    int n_exec = 1;
-    for (int l = 1; l <= Lm; ++l) {
-        if (exec) exec[l][pos] = mask[l - 1] ? 1 : 0;
-        if (mask[l - 1]) {
+    int n_exec = S;
+    for (int l = S; l < L - 1; ++l) {
+        if (exec) exec[l][pos] = mask[l - S] ? 1 : 0;
+        if (mask[l - S]) {
             orc_block_ex(c, &layers[l], kc[l], vc[l], pos, h, exec ? exec[l] : NULL);
             ++n_exec;
         } else {

@@ -45,7 +45,15 @@ typedef struct {
     int32_t dm_hidden, dm_act, dtype, max_ctx;
     double rms_eps, rope_theta;
     int32_t router_ctx;   /* ORC_CTX_* */
+    /* Start layer of the Decision Module (Sec. 4.3 ablation): blocks
+     * 0..S-1 always run and block S-1's cache is the router context; the
+     * routable blocks are S..L-2.  0 reads as 1, the paper's default. */
+    int32_t start_layer;
 } orc_config;
+
+/* First routable block S and the number of routable blocks L - 1 - S. */
+int orc_start_layer(const orc_config* c);
+int orc_n_mid(const orc_config* c);
 
 typedef struct {
     const void *attn_norm, *wqkv, *wo, *mlp_norm, *wgate_up, *wdown;
@@ -58,11 +66,11 @@ typedef struct {
 } orc_dm;
 
 /* Budget Predictor head (Sec. 4.4): a categorical policy over the actions
- * k = 1..L-2 from the router context.  The paper does not give its layers;
+ * k = 1..L_mid from the router context (L_mid = orc_n_mid, L-2 by default).  The paper does not give its layers;
  * read here as the Decision Module's form, two linear layers with the
  * Decision Module's activation in between. */
 typedef struct {
-    const void *w1, *b1, *w2, *b2;   /* [hidden][din], [hidden], [L-2][hidden], [L-2] */
+    const void *w1, *b1, *w2, *b2;   /* [hidden][din], [hidden], [L_mid][hidden], [L_mid] */
     int32_t hidden;
 } orc_predictor;
 
@@ -107,9 +115,9 @@ void orc_router_context(const orc_config* c, const void* kc, const void* vc, int
 void orc_dm_scores(const orc_config* c, const orc_dm* dm, const double* z,
                    float* scores);
 
-/* Budget Predictor: logits = W2 act(W1 z + b1) + b2 over k = 1..L-2, rounded
+/* Budget Predictor: logits = W2 act(W1 z + b1) + b2 over k = 1..L_mid, rounded
  * to fp32 (the precision the argmax is taken in); returns k_hat = 1 + argmax
- * (equal logits: the smaller k; NaN never wins).  logits[L-2] optional;
+ * (equal logits: the smaller k; NaN never wins).  logits[L_mid] optional;
  * *margin = best - second best logit (+inf with a single action). */
 int32_t orc_predict_budget(const orc_config* c, const orc_predictor* p, const double* z,
                            float* logits, double* margin);
@@ -123,12 +131,14 @@ int orc_topk(const float* scores, int32_t n, int32_t k, uint8_t* mask,
 /* One full decode step for one sequence.
  *   kc[l], vc[l]: this sequence's cache of layer l ([n_kv][max_ctx][hd]).
  *   pos: cached positions before the step (the new token is written at pos).
- *   k_budget: number of routable layers to run (0..L-2).
- *   route: optional fixed mask over the L-2 routable layers (skips the
+ *   k_budget: number of routable layers to run (0..L_mid; L_mid = L-2
+ *          by default, L-1-S with start layer S: blocks S..L-2).
+ *   route: optional fixed mask over the L_mid routable layers (skips the
  *          Decision Module); NULL routes with the Decision Module.
  *   x: input hidden [d]; h_out: output hidden [d].
- *   mask_out[L-2], scores_out[L-2] (left untouched when route != NULL),
- *   margin_out, n_exec_out (blocks executed, including first and last):
+ *   mask_out[L_mid], scores_out[L_mid] (left untouched when route != NULL),
+ *   margin_out, n_exec_out (blocks executed, including the S leading ones
+ *   and the last):
  *   all optional.
  * Returns 0, or -1 on invalid arguments (nothing written). */
 int orc_decode_seq(const orc_config* c, const orc_layer* layers, const orc_dm* dm,

@@ -62,7 +62,7 @@ def layer_weight_bytes(cfg: dict) -> int:
 
 
 def dm_weight_bytes(cfg: dict) -> int:
-    H, Lm = cfg["dm_hidden"], cfg["n_layers"] - 2
+    H, Lm = cfg["dm_hidden"], cfg["n_layers"] - 1 - int(cfg.get("start_layer", 1))
     n = cfg["n_kv_heads"] * cfg["head_dim"]
     din = (2 * n if cfg.get("router_ctx", "kv") == "kv" else n) + cfg["d_model"]
     return (H * din + H + Lm * H + Lm) * _s(cfg["dtype"])
@@ -70,19 +70,21 @@ def dm_weight_bytes(cfg: dict) -> int:
 
 def step_bytes(cfg: dict, masks, positions, running_pool: bool = False) -> dict:
     """Algorithmic bytes of one step given the realised per-sequence masks
-    (each a sequence of L-2 zeros/ones) and the positions written this step.
+    (each a sequence of L_mid zeros/ones for blocks S..L-2) and the positions
+    written this step.
     Attention of a sequence at position p reads p + 1 cached rows; the pool
     reads the first block's rows 0..p, or with running sums (steady state)
     the previous row, the new row and the kept fp32 sums."""
     L = cfg["n_layers"]
     s = _s(cfg["dtype"])
     row = 2 * cfg["n_kv_heads"] * cfg["head_dim"] * s          # one K row + one V row
-    used = {0, L - 1}
+    S = int(cfg.get("start_layer", 1))
+    used = set(range(S)) | {L - 1}
     kv = 0
     for m, p in zip(masks, positions):
-        n_exec = 2 + sum(int(v) for v in m)
+        n_exec = S + 1 + sum(int(v) for v in m)
         kv += n_exec * row * (p + 1)
-        used.update(l + 1 for l, v in enumerate(m) if v)
+        used.update(l + S for l, v in enumerate(m) if v)
     weights = len(used) * layer_weight_bytes(cfg)
     if running_pool:
         sums = 2 * cfg["n_kv_heads"] * cfg["head_dim"] * 4

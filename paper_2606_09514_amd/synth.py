@@ -68,6 +68,11 @@ def context_dim(cfg: dict) -> int:
     return (2 * n if cfg.get("router_ctx", "kv") == "kv" else n) + cfg["d_model"]
 
 
+def n_mid(cfg: dict) -> int:
+    """Routable blocks S..L-2 for start layer S (default 1): L - 1 - S."""
+    return cfg["n_layers"] - 1 - int(cfg.get("start_layer", 1))
+
+
 def model_config(shape: str | dict, dtype: str, max_ctx: int) -> dict:
     s = SHAPES[shape] if isinstance(shape, str) else shape
     c = dict(s)
@@ -107,7 +112,7 @@ def model_weights(cfg: dict, seed: int, device="cpu", omega: float = 0.1,
             wgate_up=_normal((2 * f, d), std, 0.0, gen, device, dt),
             wdown=_normal((d, f), std, 0.0, gen, device, dt),
         ))
-    H, Lm = cfg["dm_hidden"], cfg["n_layers"] - 2
+    H, Lm = cfg["dm_hidden"], n_mid(cfg)
     din = context_dim(cfg)
     dm = dict(
         w1=_normal((H, din), std, 0.0, gen, device, dt),
@@ -121,10 +126,10 @@ def model_weights(cfg: dict, seed: int, device="cpu", omega: float = 0.1,
 
 
 def predictor_weights(cfg: dict, hidden: int, seed: int, device="cpu", std: float = 0.02) -> dict:
-    """Random-init Budget Predictor head: w1 [hidden][din], b1, w2 [L-2][hidden],
+    """Random-init Budget Predictor head: w1 [hidden][din], b1, w2 [L_mid][hidden],
     b2, all N(0, std) in the storage dtype (no trained predictor exists)."""
     gen = torch.Generator(device=device).manual_seed(seed)
-    dt, Lm = cfg["dtype"], cfg["n_layers"] - 2
+    dt, Lm = cfg["dtype"], n_mid(cfg)
     return dict(
         w1=_normal((hidden, context_dim(cfg)), std, 0.0, gen, device, dt),
         b1=_normal((hidden,), std, 0.0, gen, device, dt),

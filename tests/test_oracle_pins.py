@@ -572,3 +572,79 @@ def test_prefill_then_decode_equals_token_by_token(masked):
         if masked:
             assert np.array_equal(ex1[l], ex2[l])
 
+
+
+# ------------------------------------------ start layer of the router (Sec. 4.3)
+
+def _up(a):
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("S", [2, 3])
+def test_start_layer_router_context_and_budget(S, dtype):
+    """Start layer S: the router reads block S-1's cache (numpy means of its
+    stored rows 0..pos) and the hidden state after block S-1 (a Hugging
+    Face forward of blocks 0..S-1, which always run); the budget counts the
+    blocks S..L-2, so S + 1 + k blocks execute."""
+    shape = dict(SMALL, start_layer=S)
+    cfg, layers, dm, orc = make(shape=shape, dtype=dtype, omega=0.1)
+    L, n = cfg["n_layers"], 8
+    assert orc.L_mid == L - 1 - S and dm["w2"].shape[0] == L - 1 - S
+    xs = synth.hidden_inputs(n, cfg["d_model"], seed=60 + S).numpy()
+    hS = hf_forward(hf_model(cfg, layers, list(range(S))), xs)
+    kc, vc = empty_cache(cfg, orc)
+    for t in range(n):
+        k = t % (orc.L_mid + 1)
+        _, mask, sc, _, n_exec = orc.decode_seq(kc, vc, t, k, xs[t])
+        assert n_exec == S + 1 + k and int(mask.sum()) == k
+        z = np.concatenate([_up(kc[S - 1][:, :t + 1]).mean(axis=1).reshape(-1),
+                            _up(vc[S - 1][:, :t + 1]).mean(axis=1).reshape(-1), hS[t]])
+        s_ref = orc.dm_scores(z)
+        tol = 1e-5 if dtype == "f32" else 2e-3
+        assert np.max(np.abs(sc - s_ref)) <= tol * max(1.0, float(np.max(np.abs(s_ref)))), t
+
+
+@pytest.mark.parametrize("S", [2, 3])
+def test_start_layer_fixed_route_is_sub_model(S):
+    """Under a fixed route over blocks S..L-2 the decode (and the prefill) is
+    the dense forward of blocks 0..S-1, the selected ones and L-1; skipped
+    blocks hold zeros.  With S = L-1 nothing is routable: the dense model."""
+    shape = dict(SMALL, start_layer=S)
+    cfg, layers, dm, orc = make(shape=shape)
+    L = cfg["n_layers"]
+    route = np.zeros(orc.L_mid, np.uint8)
+    route[-1] = 1
+    keep = list(range(S)) + [S + i for i in range(orc.L_mid) if route[i]] + [L - 1]
+    xs = synth.hidden_inputs(10, cfg["d_model"], seed=70 + S).numpy()
+    ref = hf_forward(hf_model(cfg, layers, keep), xs)
+    got, execs, _, (kc, vc) = run_sequence(cfg, orc, xs, k=1, route=route)
+    assert relerr(got, ref) < 1e-5 and all(e == len(keep) for e in execs)
+    h, _, _, (pk, pv) = prefill(cfg, orc, xs, 1, route=route)
+    assert relerr(h, ref) < 1e-5
+    for i in range(orc.L_mid):
+        if not route[i]:
+            assert np.all(kc[S + i][:, :10] == 0) and np.all(pk[S + i][:, :10] == 0)
+    full = dict(SMALL, start_layer=L - 1)
+    cfg2, layers2, _, orc2 = make(shape=full)
+    assert orc2.L_mid == 0
+    got2, execs2, _, _ = run_sequence(cfg2, orc2, xs, k=0)
+    assert relerr(got2, hf_forward(hf_model(cfg2, layers2, list(range(L))), xs)) < 1e-5
+    assert all(e == L for e in execs2)
+
+
+def test_start_layer_prefill_route_from_block_s_minus_1():
+    """Prefill at start layer 2: the prompt's route comes from block 1's
+    cache over the prompt and the last token after blocks 0 and 1."""
+    shape = dict(SMALL, start_layer=2)
+    cfg, layers, dm, orc = make(shape=shape, omega=0.1)
+    n, k, L = 12, 1, cfg["n_layers"]
+    xs = synth.hidden_inputs(n, cfg["d_model"], seed=75).numpy()
+    h, mask, sc, (kc, vc) = prefill(cfg, orc, xs, k)
+    h1 = hf_forward(hf_model(cfg, layers, [0, 1]), xs)[-1]
+    s_ref = orc.dm_scores(orc.context(kc[1], vc[1], n - 1, h1))
+    assert np.allclose(sc, s_ref, rtol=1e-6, atol=1e-7)
+    keep = [0, 1] + [2 + i for i in range(orc.L_mid) if mask[i]] + [L - 1]
+    assert relerr(h, hf_forward(hf_model(cfg, layers, keep), xs)) < 1e-5
