@@ -69,8 +69,9 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     import torch
     from paper_2606_09514_amd import costmodel
     from paper_2606_09514_amd import lib as blib
+    from paper_2606_09514_amd import synth
 
-    B, Lm = w.batch, cfg["n_layers"] - 2
+    B, Lm = w.batch, synth.n_mid(cfg)
     hidden = x0.clone()
     masks = torch.zeros((steps, B, Lm), dtype=torch.uint8, device="cuda")
     k_pred = torch.zeros((steps, B), dtype=torch.int32, device="cuda")
@@ -187,6 +188,8 @@ def main():
                     help="KV of skipped blocks: zero-filled (the paper's) or masked")
     ap.add_argument("--router-ctx", choices=["kv", "k", "v", "k+v"], default="kv",
                     help="router context features")
+    ap.add_argument("--start-layer", type=int, default=1,
+                    help="router start layer S: blocks 0..S-1 always run, S..L-2 are routable")
     ap.add_argument("--pool", choices=["scan", "running"], default="scan",
                     help="router pool: sum the first block's rows every step, or keep "
                          "running sums across steps")
@@ -222,6 +225,7 @@ def main():
     budgets = [int(b) for b in args.budgets.split(",")] if args.budgets else list(w.budgets)
     cfg = synth.model_config(w.shape, w.dtype, w.ctx + args.warmup + args.steps + 1)
     cfg["router_ctx"] = args.router_ctx
+    cfg["start_layer"] = args.start_layer
 
     if args.copy_calibration:
         a = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
@@ -252,7 +256,7 @@ def main():
         model.set_budget_predictor(pw)
 
     if args.prefill:
-        Lm = cfg["n_layers"] - 2
+        Lm = synth.n_mid(cfg)
         ks_list = sorted(set(budgets) | {Lm}) if not w.mixed else [Lm]
         pf = run_prefill(model, cfg, w, dk, dv, ks_list, reps=3, warmup=1)
         dense = pf[str(Lm)]["ms_per_prefill"]
@@ -312,6 +316,7 @@ def main():
                    "k": head_k if head_k is not None else ("predicted" if args.auto_budget
                                                               else "mixed"),
                    "skip_kv": args.skip_kv, "router_ctx": args.router_ctx, "pool": args.pool,
+                   "start_layer": args.start_layer,
                    "weights_kv": w.dtype, "accumulate": "f32", "omega": w.omega,
                    "launch_policy": args.policy,
                    "parallelism": "none (1 GPU)"},

@@ -18,6 +18,11 @@
  *      (grouping by mask, App. C.1); a skipped block leaves h unchanged
  *      (Eq. 1) and gets a zero-filled K/V row at pos (Sec. 6, limitations);
  *   6. the last block runs for every sequence.
+ * Start layer (the Decision Module placement ablation of Sec. 4.3):
+ * with buddy_config.start_layer = S > 1, step 1 runs blocks 0..S-1, the
+ * planner reads block S-1's cache and the hidden state after block S-1, and
+ * the routable blocks are S..L-2.  L_mid = L - 1 - S routable blocks (L-2
+ * for the default S = 1) size every mask, score and budget below.
  * The decoder block is Llama-style (App. C.2): RMSNorm, Q/K/V projection,
  * rotary embedding (rotate-half pairing, angle pos * theta^(-2i/hd)), grouped
  * query attention over the cache including the new row (App. "Background",
@@ -39,8 +44,8 @@
  *       wdown    [d][d_ffn]
  *       attn_norm, mlp_norm [d]
  *       Decision Module: w1 [dm_hidden][din], b1 [dm_hidden],
- *                        w2 [L-2][dm_hidden], b2 [L-2]  (storage dtype),
- *                        prior [L-2] fp32 (already normalised p~) or NULL.
+ *                        w2 [L_mid][dm_hidden], b2 [L_mid]  (storage dtype),
+ *                        prior [L_mid] fp32 (already normalised p~) or NULL.
  *     KV cache: K and V each [n_layers][max_batch][n_kv_heads][max_ctx][hd].
  *   - Positions: pos[b] (host array) is the number of cached rows of
  *     sequence b before the step; the step writes row pos[b] of every layer
@@ -115,6 +120,9 @@ typedef struct {
     float rms_eps;        /* RMSNorm epsilon                               */
     float rope_theta;     /* rotary base                                   */
     int32_t router_ctx;   /* buddy_router_ctx                              */
+    int32_t start_layer;  /* S: blocks 0..S-1 always run, the router reads
+                             block S-1; 1 <= S <= n_layers - 1, 0 reads as
+                             1 (the paper's default)                       */
 } buddy_config;
 
 typedef struct {
@@ -123,7 +131,7 @@ typedef struct {
 
 typedef struct {
     const void *w1, *b1, *w2, *b2;  /* device, storage dtype              */
-    const float* prior;             /* device [L-2] fp32, or NULL         */
+    const float* prior;             /* device [L_mid] fp32, or NULL       */
     float omega;                    /* prior weight of Eq. 2 (paper: 0.1) */
 } buddy_dm_weights;
 
@@ -173,7 +181,7 @@ void buddy_model_destroy(buddy_model* m);
 /* KV-aware planner plus Decision Module (Sec. 4.3, Sec. 4.2.3, Eq. 2 fusion)
  * without routing: for b < B, pools the first layer's K/V rows 0..pos[b] of
  * kv (the newest token's row already written) with h_new[b] (device
- * [B][d] fp32) and writes s' to scores_out (device [B][L-2] fp32).
+ * [B][d] fp32) and writes s' to scores_out (device [B][L_mid] fp32).
  * pos: host [B].  B = 0 is a no-op. */
 buddy_status buddy_pool_route(buddy_model* m, const buddy_kv* kv, const int32_t* pos,
                               const float* h_new, int32_t B, float* scores_out,
@@ -191,27 +199,27 @@ buddy_status buddy_select_topk(const float* scores, const int32_t* k, int32_t B,
  *   hidden: device [B][d] fp32; input H_0 of the new token, overwritten
  *           with the last block's output H_L (no final norm).
  *   pos:    host [B]; 0 <= pos[b] < max_ctx.
- *   k:      host [B]; 0 <= k[b] <= L-2 routable blocks to run.
+ *   k:      host [B]; 0 <= k[b] <= L_mid routable blocks to run.
  *   skip_kv: buddy_skip_kv; BUDDY_SKIP_KV_MASK needs kv->exec
  *           (BUDDY_EINVAL otherwise).
- *   route_override: device [B][L-2] uint8 (nonzero = run) or NULL; when
+ *   route_override: device [B][L_mid] uint8 (nonzero = run) or NULL; when
  *           given, the planner and Decision Module are not run, k is
  *           ignored and scores_out is left untouched.
- *   mask_out: device [B][L-2] uint8 or NULL: the mask that was executed.
- *   scores_out: device [B][L-2] fp32 or NULL: s' of step 3.
+ *   mask_out: device [B][L_mid] uint8 or NULL: the mask that was executed.
+ *   scores_out: device [B][L_mid] fp32 or NULL: s' of step 3.
  * B = 0 is a no-op; B > max_batch gives BUDDY_ECAPACITY. */
 buddy_status buddy_decode_step(buddy_model* m, const buddy_kv* kv, float* hidden,
                                const int32_t* pos, const int32_t* k, int32_t B,
                                int32_t skip_kv, const uint8_t* route_override,
                                uint8_t* mask_out, float* scores_out, void* stream);
 
-/* Budget Predictor head (Sec. 4.4): a categorical policy over k = 1..L-2
+/* Budget Predictor head (Sec. 4.4): a categorical policy over k = 1..L_mid
  * from the same router context as the Decision Module, read as the Decision
  * Module's form (the paper does not give its layers): logits = w2 act(w1 z
  * + b1) + b2 with the Decision Module's activation. */
 typedef struct {
     const void *w1, *b1, *w2, *b2;  /* device, storage dtype: w1 [hidden][din],
-                                       b1 [hidden], w2 [L-2][hidden], b2 [L-2] */
+                                       b1 [hidden], w2 [L_mid][hidden], b2 [L_mid] */
     int32_t hidden;                 /* multiple of 8                          */
 } buddy_predictor_weights;
 
@@ -219,13 +227,13 @@ typedef struct {
  * the weights are not; they must outlive the handle), or detaches it with
  * p == NULL.  Waits for the device, then allocates the head's workspace.
  * Errors: BUDDY_EINVAL (null pointers, hidden not a positive multiple of 8,
- * fewer than three layers), BUDDY_ESHAPE (hidden too wide), BUDDY_ENOMEM. */
+ * no routable block), BUDDY_ESHAPE (hidden too wide), BUDDY_ENOMEM. */
 buddy_status buddy_set_budget_predictor(buddy_model* m, const buddy_predictor_weights* p);
 
 /* Planner and Budget Predictor only (steps 3 and 4 with the predictor's
  * output layer): k_out device [B] int32 receives k_hat = 1 + argmax of the
  * logits (fp32; the smaller k on equal logits; the budget is b_hat =
- * (k_hat + 2) / L); logits_out device [B][L-2] fp32 or NULL.  pos and h_new
+ * (k_hat + 2) / L); logits_out device [B][L_mid] fp32 or NULL.  pos and h_new
  * as for buddy_pool_route.  BUDDY_EINVAL without an attached predictor. */
 buddy_status buddy_predict_budget(buddy_model* m, const buddy_kv* kv, const int32_t* pos,
                                   const float* h_new, int32_t B, int32_t* k_out,
@@ -242,7 +250,8 @@ buddy_status buddy_decode_step_auto(buddy_model* m, const buddy_kv* kv, float* h
 
 /* Routed prefill of B prompts into cache rows 0..len[b]-1 (one route per
  * prompt; the Reuse setting of Sec. 5 keeps decoding on the prefill's
- * decision, so the prefill itself is routed).  The first block runs over
+ * decision, so the prefill itself is routed).  The first block (blocks
+ * 0..S-1 with a start layer S) runs over
  * every prompt token; the planner and Decision Module decide the route once
  * per prompt at its last token (as a decode step at position len[b]-1
  * would), unless route_override gives it; each selected block then runs
@@ -252,7 +261,7 @@ buddy_status buddy_decode_step_auto(buddy_model* m, const buddy_kv* kv, float* h
  *           overwritten with their last-block outputs (rows t >= len[b]
  *           untouched).
  *   len:    host [B], 1 <= len[b] <= min(t_stride, max_ctx).
- *   k:      host [B] budgets 0..L-2 (ignored with route_override).
+ *   k:      host [B] budgets 0..L_mid (ignored with route_override).
  *   route_override, mask_out, scores_out: as buddy_decode_step.
  * Rows of all prompts together: B * t_stride <= 65535.  Grows the handle's
  * prefill workspace when needed and returns after the device has finished
@@ -331,7 +340,9 @@ buddy_status buddy_prior_normalize(const float* raw, int32_t n, int32_t kind, fl
                                    float* prior_out);
 
 /* Budget to routable-block count, k = round(b L) - 2 (Eq. 2), halves away
- * from zero, limited to [0, L-2]; -1 when b is outside (0, 1]. */
+ * from zero, limited to [0, L-2]; -1 when b is outside (0, 1].  This is the
+ * default start layer's count; with start layer S the blocks 0..S-1 and
+ * L-1 always run and k = round(b L) - (S + 1), which callers compute. */
 int32_t buddy_budget_to_k(float b, int32_t n_layers);
 
 const char* buddy_status_string(buddy_status s);

@@ -39,7 +39,9 @@ bool kv_ok(const buddy_kv* kv) {
 
 buddy_status check_config(const buddy_config* c) {
     if (!c) return BUDDY_EINVAL;
-    if (c->n_layers < 2 || c->n_layers - 2 > 255) return BUDDY_ESHAPE;
+    if (c->n_layers < 2 || c->n_layers > 1024) return BUDDY_ESHAPE;
+    if (c->start_layer < 0 || c->start_layer > c->n_layers - 1) return BUDDY_EINVAL;
+    if (n_mid(*c) > 255) return BUDDY_ESHAPE;
     if (c->d_model <= 0 || c->d_model % 8) return BUDDY_ESHAPE;
     if (c->n_kv_heads <= 0 || c->n_heads <= 0 || c->n_heads % c->n_kv_heads) return BUDDY_ESHAPE;
     if (c->n_heads / c->n_kv_heads > kMaxGroup) return BUDDY_ESHAPE;
@@ -240,11 +242,14 @@ buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, in
     const buddy_config& c = M.cfg;
     hipError_t e;
     int splits = 1;
+    // the router's cache: the first block's, block S-1's with a start layer
+    const void* k0 = layer_base(M, kv->k, start_layer(c) - 1);
+    const void* v0 = layer_base(M, kv->v, start_layer(c) - 1);
     if (kv->pool_sum) {
-        if ((e = launch_pool_running(M, kv->k, kv->v, kv->pool_sum, kv->pool_rows, B, pos_u, s)) !=
+        if ((e = launch_pool_running(M, k0, v0, kv->pool_sum, kv->pool_rows, B, pos_u, s)) !=
             hipSuccess)
             return fail_device(M, e, "pool");
-    } else if ((e = launch_pool(M, kv->k, kv->v, B, max_pos, pos_u, &splits, s)) != hipSuccess) {
+    } else if ((e = launch_pool(M, k0, v0, B, max_pos, pos_u, &splits, s)) != hipSuccess) {
         return fail_device(M, e, "pool");
     }
     GemvArgs g;
@@ -296,7 +301,7 @@ buddy_status prepare_step(Model& M, const int32_t* pos, const int32_t* k, int B,
 // counts of step `seq` to mapped host memory.  A device error, or no answer
 // within a minute, ends the wait with BUDDY_EDEVICE.
 buddy_status wait_route(Model& M, int32_t seq, hipStream_t s) {
-    volatile int32_t* flag = M.h_cnt + (M.cfg.n_layers - 2);
+    volatile int32_t* flag = M.h_cnt + n_mid(M.cfg);
     const auto t0 = std::chrono::steady_clock::now();
     auto next_check = t0 + std::chrono::milliseconds(1);
     while (*flag != seq) {
@@ -353,7 +358,7 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
     (void)hipGetDevice(&M.device);
 
     const buddy_config& c = M.cfg;
-    const size_t Bc = c.max_batch, Lm = c.n_layers - 2, hd = c.head_dim;
+    const size_t Bc = c.max_batch, Lm = n_mid(c), hd = c.head_dim;
     const size_t din = pooled_dim(c.router_ctx, c.n_kv_heads, hd) + c.d_model;
     const size_t qdim = (size_t)c.n_heads * hd;
     const int max_chunks = kAttnMaxChunks;
@@ -483,7 +488,7 @@ buddy_status buddy_set_budget_predictor(buddy_model* h, const buddy_predictor_we
     if (!h) return BUDDY_EINVAL;
     Model& M = h->M;
     if (p && (!p->w1 || !p->b1 || !p->w2 || !p->b2 || p->hidden <= 0 || p->hidden % 8 ||
-              M.cfg.n_layers < 3))
+              n_mid(M.cfg) < 1))
         return BUDDY_EINVAL;
     if (p && (size_t)p->hidden > (size_t)64 * 64 * (M.cfg.dtype == BUDDY_BF16 ? 8 : 4))
         return BUDDY_ESHAPE;                       // output-layer rows of at most 64 k-steps
@@ -530,7 +535,7 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
     int max_pos;
     buddy_status st = check_step_host(M, pos, B, &max_pos);
     if (st != BUDDY_OK) return st;
-    const int Lm = c.n_layers - 2;
+    const int Lm = n_mid(c), S = start_layer(c);
     if (!route_override && !predict)
         for (int b = 0; b < B; ++b)
             if (k[b] < 0 || k[b] > Lm) return BUDDY_EINVAL;
@@ -547,10 +552,12 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
     hipError_t e;
 
     const Rows all{M.ws.idx_all, M.ws.n_all, B, true, true};
-    // first block on every sequence (appends the first-layer K/V row)
-    if ((st = run_block(M, kv, exec, hidden, 0, all, B, max_pos, pos_u, decode_bufs(M), s)) !=
-        BUDDY_OK)
-        return st;
+    // first block (blocks 0..S-1) on every sequence; block S-1 appends the
+    // K/V row the planner pools
+    for (int l = 0; l < S; ++l)
+        if ((st = run_block(M, kv, exec, hidden, l, all, B, max_pos, pos_u, decode_bufs(M), s)) !=
+            BUDDY_OK)
+            return st;
     // KV-aware planner and Decision Module, unless the route is given
     if (!route_override)
         if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, predict, s)) != BUDDY_OK) return st;
@@ -570,11 +577,12 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
                           route_override, mask_out, scores_out, false, seq, s)) != hipSuccess)
         return fail_device(M, e, "route");
     if (host_routed && (st = wait_route(M, seq, s)) != BUDDY_OK) return st;
-    // routable blocks on their compacted sub-batches
-    for (int l = 1; l <= Lm; ++l) {
+    // routable blocks S..L-2 (list i = l - S) on their compacted sub-batches
+    for (int l = S; l < S + Lm; ++l) {
+        const int i = l - S;
         int n_max = B;
         if (host_routed) {
-            n_max = M.h_cnt[l - 1];
+            n_max = M.h_cnt[i];
             if (n_max == 0) {
                 // a timed kernel of a block that does not run: an empty interval
                 if (M.timing.n > 0 && M.timing.next < M.timing.n && M.timing.layer == l &&
@@ -585,7 +593,7 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
             }
         }
         // every sequence routed (known on the host): the rows are the batch in order
-        const Rows r{M.ws.idx + (size_t)(l - 1) * c.max_batch, M.ws.cnt + (l - 1), n_max,
+        const Rows r{M.ws.idx + (size_t)i * c.max_batch, M.ws.cnt + i, n_max,
                      host_routed, host_routed && n_max == B};
         if ((st = run_block(M, kv, exec, hidden, l, r, B, max_pos, pos_u, decode_bufs(M), s)) !=
             BUDDY_OK)
@@ -683,7 +691,7 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
     if (B > c.max_batch) return BUDDY_ECAPACITY;
     if (!hidden || !len || (!k && !route_override) || t_stride < 1) return BUDDY_EINVAL;
     if ((size_t)B * t_stride > kMaxPrefillRows) return BUDDY_ECAPACITY;
-    const int Lm = c.n_layers - 2;
+    const int Lm = n_mid(c), S = start_layer(c);
     int max_len = 0;
     bool full = true;
     for (int b = 0; b < B; ++b) {
@@ -713,7 +721,7 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
     int32_t* hl = M.pf_hlists;
     int32_t* hg = hl + (size_t)c.n_layers * R;
     const int qt = attention_prefill_group(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads);
-    std::vector<int> n_g(Lm + 1, 0);
+    std::vector<int> n_g(c.n_layers, 0);
     int n_all = 0;
     for (int b = 0; b < B; ++b)
         for (int t = 0; t < len[b]; ++t) hl[n_all++] = b * t_stride + t;
@@ -726,9 +734,12 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
         return fail_device(M, e, "prefill lists");
     auto groups_of = [&](int l) { return qt > 1 ? M.pf_groups + (size_t)2 * l * R : nullptr; };
     const Rows all{M.pf_lists, nullptr, n_all, true, full};
-    if ((st = run_block(M, kv, nullptr, hidden, 0, all, n_all, max_len - 1, -1, bf, s, groups_of(0),
-                        n_g[0])) != BUDDY_OK)
-        return st;
+    // blocks 0..S-1 over every token, unmasked: their map entries are
+    // written with the route, and every prompt token runs them
+    for (int l = 0; l < S; ++l)
+        if ((st = run_block(M, kv, nullptr, hidden, l, all, n_all, max_len - 1, -1, bf, s,
+                            groups_of(0), n_g[0])) != BUDDY_OK)
+            return st;
 
     // one route per prompt: the planner and Decision Module at the last token
     std::vector<uint8_t> mask((size_t)B * (Lm > 0 ? Lm : 1));
@@ -764,22 +775,23 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
         return fail_device(M, e, "prefill fill");
     if ((e = hipStreamSynchronize(s)) != hipSuccess) return fail_device(M, e, "prefill route");
 
-    // token lists of the routable blocks, then the blocks over their tokens
-    std::vector<int> n_l(Lm + 1, 0);
-    for (int l = 1; l <= Lm; ++l) {
+    // token lists of the routable blocks S..L-2 (list l), then the blocks
+    // over their tokens
+    std::vector<int> n_l(c.n_layers, 0);
+    for (int l = S; l < S + Lm; ++l) {
         int32_t* dst = hl + (size_t)l * R;
         for (int b = 0; b < B; ++b)
-            if (mask[(size_t)b * Lm + (l - 1)])
+            if (mask[(size_t)b * Lm + (l - S)])
                 for (int t = 0; t < len[b]; ++t) dst[n_l[l]++] = b * t_stride + t;
         if (qt > 1) n_g[l] = token_groups(dst, n_l[l], t_stride, qt, hg + (size_t)2 * l * R);
     }
-    if (Lm > 0 && ((e = hipMemcpyAsync(M.pf_lists + R, hl + R, (size_t)Lm * R * 4,
+    if (Lm > 0 && ((e = hipMemcpyAsync(M.pf_lists + S * R, hl + S * R, (size_t)Lm * R * 4,
                                        hipMemcpyHostToDevice, s)) != hipSuccess ||
-                   (qt > 1 && (e = hipMemcpyAsync(M.pf_groups + 2 * R, hg + 2 * R,
+                   (qt > 1 && (e = hipMemcpyAsync(M.pf_groups + 2 * S * R, hg + 2 * S * R,
                                                   (size_t)Lm * R * 8, hipMemcpyHostToDevice,
                                                   s)) != hipSuccess)))
         return fail_device(M, e, "prefill lists");
-    for (int l = 1; l <= Lm; ++l) {
+    for (int l = S; l < S + Lm; ++l) {
         if (n_l[l] == 0) continue;
         const Rows r{M.pf_lists + (size_t)l * R, nullptr, n_l[l], true, full && n_l[l] == n_all};
         if ((st = run_block(M, kv, exec, hidden, l, r, n_l[l], max_len - 1, -1, bf, s, groups_of(l),

@@ -31,6 +31,11 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
     return (bf16_t)(u >> 16);
 }
 
+// Start layer S of the router (0 in the config reads as 1): blocks 0..S-1
+// always run, blocks S..L-2 are routable (n_mid of them).
+inline int start_layer(const buddy_config& c) { return c.start_layer > 0 ? c.start_layer : 1; }
+inline int n_mid(const buddy_config& c) { return c.n_layers - 1 - start_layer(c); }
+
 template <typename T> struct St;
 template <> struct St<float> {
     static constexpr int V = 4;  // elements per 16-byte vector

@@ -205,6 +205,7 @@ struct RouteParams {
     const float* a; int H;
     const void* w2; const void* b2; const float* prior; float omega;
     int Lm, B;
+    int S, L;                         // start layer (routable blocks S..L-2), blocks
     const uint8_t* route_override;
     uint8_t* mask; uint8_t* mask_out;
     float* scores; float* scores_out;
@@ -317,11 +318,11 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteParams p, StepArgs sa)
     }
 
     // with masking, every block's entry of the execution map at this step's
-    // position: 1 for the first and last blocks and the selected ones
+    // position: 1 for blocks 0..S-1, the last block and the selected ones
     const int pos = sa.pos[b];
-    if (p.exec && tid < Lm + 2)
+    if (p.exec && tid < p.L)
         p.exec[((size_t)tid * p.bcap + b) * p.T + pos] =
-            (tid == 0 || tid == Lm + 1) ? 1 : s_mask[tid - 1];
+            (tid < p.S || tid == p.L - 1) ? 1 : s_mask[tid - p.S];
 
     // zero-filled K/V row at this step's position for every skipped block,
     // written as 16-byte vectors
@@ -332,7 +333,7 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteParams p, StepArgs sa)
         const int i = t / per_layer, r = t % per_layer;
         if (s_mask[i]) continue;
         const int g = r / (p.hd / VZ), e = (r % (p.hd / VZ)) * VZ;
-        const size_t at = (size_t)(i + 1) * layer_stride +
+        const size_t at = (size_t)(i + p.S) * layer_stride +
                           (((size_t)b * p.nkv + g) * p.T + pos) * p.hd + e;
         *reinterpret_cast<uint4*>((T*)p.kc + at) = make_uint4(0u, 0u, 0u, 0u);
         *reinterpret_cast<uint4*>((T*)p.vc + at) = make_uint4(0u, 0u, 0u, 0u);
@@ -378,7 +379,8 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t*
     RouteParams p;
     p.a = M.ws.a; p.H = c.dm_hidden;
     p.w2 = M.dm.w2; p.b2 = M.dm.b2; p.prior = M.dm.prior; p.omega = M.dm.omega;
-    p.Lm = c.n_layers - 2; p.B = B;
+    p.Lm = n_mid(c); p.B = B;
+    p.S = start_layer(c); p.L = c.n_layers;
     p.route_override = route_override;
     p.mask = M.ws.mask; p.mask_out = mask_out;
     p.scores = M.ws.scores; p.scores_out = scores_out;
@@ -408,11 +410,12 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t*
 template <typename T>
 __global__ __launch_bounds__(256) void prefill_fill_kernel(void* kc, void* vc, uint8_t* exec,
                                                            const uint8_t* mask, const int32_t* len,
-                                                           int Lm, int T_cap, int bcap, int nkv,
-                                                           int hd) {
-    const int b = blockIdx.y, l = blockIdx.x;      // block l of 0..Lm+1
+                                                           int S, int L, int T_cap, int bcap,
+                                                           int nkv, int hd) {
+    const int b = blockIdx.y, l = blockIdx.x;      // block l of 0..L-1
     const int n = len[b];
-    const bool run = l == 0 || l == Lm + 1 || mask[(size_t)b * Lm + (l - 1)];
+    const int Lm = L - 1 - S;
+    const bool run = l < S || l == L - 1 || mask[(size_t)b * Lm + (l - S)];
     if (exec)
         for (int t = threadIdx.x; t < n; t += 256) exec[((size_t)l * bcap + b) * T_cap + t] = run;
     if (run) return;
@@ -435,13 +438,13 @@ hipError_t launch_prefill_fill(const Model& M, void* kc, void* vc, uint8_t* exec
     (void)max_len;
     const dim3 grid(c.n_layers, B);
     if (c.dtype == BUDDY_BF16)
-        prefill_fill_kernel<bf16_t><<<grid, 256, 0, s>>>(kc, vc, exec, mask, len, c.n_layers - 2,
-                                                         c.max_ctx, c.max_batch, c.n_kv_heads,
-                                                         c.head_dim);
+        prefill_fill_kernel<bf16_t><<<grid, 256, 0, s>>>(kc, vc, exec, mask, len, start_layer(c),
+                                                         c.n_layers, c.max_ctx, c.max_batch,
+                                                         c.n_kv_heads, c.head_dim);
     else
-        prefill_fill_kernel<float><<<grid, 256, 0, s>>>(kc, vc, exec, mask, len, c.n_layers - 2,
-                                                        c.max_ctx, c.max_batch, c.n_kv_heads,
-                                                        c.head_dim);
+        prefill_fill_kernel<float><<<grid, 256, 0, s>>>(kc, vc, exec, mask, len, start_layer(c),
+                                                        c.n_layers, c.max_ctx, c.max_batch,
+                                                        c.n_kv_heads, c.head_dim);
     return hipGetLastError();
 }
 

@@ -30,7 +30,8 @@ class Config(C.Structure):
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_ffn", C.c_int32),
                 ("dm_hidden", C.c_int32), ("dm_act", C.c_int32), ("dtype", C.c_int32),
                 ("max_batch", C.c_int32), ("max_ctx", C.c_int32),
-                ("rms_eps", C.c_float), ("rope_theta", C.c_float), ("router_ctx", C.c_int32)]
+                ("rms_eps", C.c_float), ("rope_theta", C.c_float), ("router_ctx", C.c_int32),
+                ("start_layer", C.c_int32)]
 
 
 class LayerWeights(C.Structure):
@@ -164,7 +165,8 @@ class Model:
     """A model handle over caller-owned device weights.
 
     cfg: dict with the buddy_config fields (dm_act 'silu'|'gelu', dtype
-    'f32'|'bf16', router_ctx 'kv'|'k'|'v'|'k+v', default 'kv').  weights: {'layers': [dict of tensors], 'dm': {...}} as
+    'f32'|'bf16', router_ctx 'kv'|'k'|'v'|'k+v', default 'kv', start_layer,
+    default 1).  weights: {'layers': [dict of tensors], 'dm': {...}} as
     produced by paper_2606_09514_amd.synth.model_weights on the device.
     """
 
@@ -176,7 +178,7 @@ class Model:
                    ACT_GELU_ERF if cfg["dm_act"] == "gelu" else ACT_SILU,
                    BF16 if cfg["dtype"] == "bf16" else F32, int(max_batch), cfg["max_ctx"],
                    float(cfg["rms_eps"]), float(cfg["rope_theta"]),
-                   CTX_BY_NAME[cfg.get("router_ctx", "kv")])
+                   CTX_BY_NAME[cfg.get("router_ctx", "kv")], int(cfg.get("start_layer", 1)))
         self._c = c
         self._keep = weights
         L = cfg["n_layers"]
@@ -195,7 +197,8 @@ class Model:
 
     @property
     def L_mid(self) -> int:
-        return self.cfg["n_layers"] - 2
+        """Routable blocks S..L-2 (S = start_layer, default 1)."""
+        return self.cfg["n_layers"] - 1 - int(self.cfg.get("start_layer", 1))
 
     def close(self):
         if getattr(self, "_h", None):

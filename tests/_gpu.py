@@ -48,7 +48,7 @@ class Pair:
 
     @property
     def L_mid(self):
-        return self.cfg["n_layers"] - 2
+        return self.orc.L_mid
 
     def empty_host_cache(self):
         return (np.zeros(self.shape5, dtype=self.sdt), np.zeros(self.shape5, dtype=self.sdt))
@@ -113,7 +113,7 @@ def compare_step(P, hk, hv, dk, dv, x, pos, ks, report, hx=None, dx=None, pool=N
         pre_v = [hv[l, b].copy() for l in range(P.cfg["n_layers"])]
         pre_x = None if hx is None else [hx[l, b].copy() for l in range(P.cfg["n_layers"])]
         h, m, s, margin, n_exec = oracle_step(P, hk, hv, b, pos[b], ks[b], x[b], hx=hx)
-        assert n_exec == ks[b] + 2 and int(m.sum()) == ks[b]
+        assert n_exec == ks[b] + P.orc.start_layer + 1 and int(m.sum()) == ks[b]
         if not np.array_equal(m, mg[b]):
             assert margin < MARGIN, f"route mismatch at margin {margin} (seq {b})"
             report["margin_mismatches"] += 1
@@ -130,7 +130,7 @@ def compare_step(P, hk, hv, dk, dv, x, pos, ks, report, hx=None, dx=None, pool=N
         report["max_hidden_err"] = max(report["max_hidden_err"], err)
         assert err < tol, f"hidden rel err {err} (seq {b}, pos {pos[b]})"
         # new K/V rows of every block, same rule; skipped blocks exactly zero
-        run = np.concatenate([[1], mg[b], [1]])
+        run = np.concatenate([[1] * P.orc.start_layer, mg[b], [1]])
         for l in range(P.cfg["n_layers"]):
             for ref, got in ((hk, gk), (hv, gv)):
                 r = f32(ref[l, b, :, pos[b]], P.sdt)

@@ -353,7 +353,7 @@ def check_prefill(P, lens, ks, t_stride, masked=False, route=None, seed=110):
             rep["max_hidden_err"] = max(rep["max_hidden_err"], err)
             assert err < tol, f"seq {b} token {t}: {err}"
         assert np.array_equal(hg[b, n:], x[b, n:])            # padding rows untouched
-        run = np.concatenate([[1], mg[b], [1]])
+        run = np.concatenate([[1] * P.orc.start_layer, mg[b], [1]])
         for l in range(L):
             for ref, got in ((hk, gk), (hv, gv)):
                 rr, gg = f32(ref[l, b, :, :n], P.sdt), f32(got[l, b, :, :n], P.sdt)
@@ -711,7 +711,7 @@ def sampled_full_size(name, samples, seed=0, running_pool=False):
         # new K/V rows of the sampled sequence against the oracle's
         gk = synth.storage_numpy(dk[:, b, :, w.ctx])
         gv = synth.storage_numpy(dv[:, b, :, w.ctx])
-        run = np.concatenate([[1], mg[b], [1]])
+        run = np.concatenate([[1] * P.orc.start_layer, mg[b], [1]])
         for l in range(L):
             for ref, got in ((hk[l][:, w.ctx], gk[l]), (hv[l][:, w.ctx], gv[l])):
                 r, gg = f32(ref, P.sdt), f32(got, P.sdt)
@@ -836,3 +836,66 @@ def test_running_pool_prefill_then_decode():
     compare_step(P, hk, hv, dk, dv, xd, lens, [1, 2, 3], rep, pool=pool)
     assert pool[1].cpu().numpy().tolist() == [[n] * P.cfg["n_kv_heads"] for n in lens]
     print(rep)
+
+
+# ----------------------------------- start layer of the router (Sec. 4.3 ablation)
+
+def start_shape(S, base="tiny"):
+    return dict(synth.SHAPES[base], start_layer=S)
+
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+@pytest.mark.parametrize("dtype,S", [("f32", 2), ("bf16", 3)])
+def test_start_layer_teacher_forced(dtype, S, policy):
+    """Start layer S: blocks 0..S-1 on every sequence, the planner on block
+    S-1's cache, routes over blocks S..L-2 (budgets 0 to all of them);
+    12 prompt tokens then 6 fed-back steps, B = 4, teacher-forced."""
+    P = Pair(start_shape(S), dtype, 24, 4, seed=90 + S, omega=0.1, policy=policy)
+    assert P.L_mid == P.cfg["n_layers"] - 1 - S
+    prompt = synth.hidden_inputs(4 * 12, P.cfg["d_model"], seed=91).numpy().reshape(4, 12, -1)
+    rep = new_report()
+    masks = run_teacher_forced(P, prompt, 6, [0, 1, P.L_mid // 2, P.L_mid], rep)
+    assert all(m.shape == (4, P.L_mid) for m in masks)
+    print(dtype, S, rep)
+
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+def test_start_layer_batched_masked(policy):
+    """Start layer 2 on the MFMA path (B = 24, bf16) with skipped-KV
+    masking: the execution map marks blocks 0, 1 and L-1 and the selected
+    ones exactly, random caches and positions, mixed budgets; and the
+    planner entry point's scores from block 1's cache."""
+    B, T = 24, 40
+    P = Pair(start_shape(2), "bf16", T, B, seed=93, omega=0.1, policy=policy)
+    g = torch.Generator().manual_seed(94)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    L = P.cfg["n_layers"]
+    rng = np.random.default_rng(95)
+    hx = (rng.random((L, B, T)) < 0.7).astype(np.uint8)
+    pos = rng.integers(1, T, size=B).tolist()
+    ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=96).numpy()
+    h = synth.hidden_inputs(B, P.cfg["d_model"], seed=97)
+    scores = torch.zeros((B, P.L_mid), device="cuda")
+    P.gpu.pool_route(P.upload(hk), P.upload(hv), pos, h.cuda(), scores)
+    got = scores.cpu().numpy()
+    for b in range(B):
+        ref = P.orc.dm_scores(P.orc.context(hk[1, b], hv[1, b], pos[b], h[b].numpy()))
+        assert np.max(np.abs(got[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref))))
+    dk, dv = P.upload(hk), P.upload(hv)
+    dx = torch.from_numpy(hx).cuda()
+    rep = new_report()
+    compare_step(P, hk, hv, dk, dv, x, pos, ks, rep, hx=hx, dx=dx)
+    print(rep)
+
+
+@pytest.mark.parametrize("masked", [False, True])
+def test_start_layer_prefill(masked):
+    """Prefill at start layer 3 (head_dim 128, G = 4, MFMA attention
+    groups): blocks 0..2 over every prompt token, the route from block 2's
+    cache at each prompt's last token, ragged prompts."""
+    shape = dict(gqa_shape(4), start_layer=3, n_layers=6)
+    P = Pair(shape, "bf16", 96, 3, seed=98, omega=0.1)
+    assert P.L_mid == 2
+    check_prefill(P, [90, 33, 7], [1, 2, 0], 90, masked=masked, seed=99)
