@@ -292,6 +292,22 @@ typedef enum {
 /* Sets the launch policy of a handle; BUDDY_EINVAL for an unknown policy. */
 buddy_status buddy_set_launch_policy(buddy_model* m, int32_t policy);
 
+/* Output tile of the prefill's tiled projections (bf16 weights, many prompt
+ * tokens).  Every tile accumulates each output over K in the same order, so
+ * the choice changes speed, never results.
+ *   BUDDY_GEMM_TILE_AUTO (default): 256 x 256 where that still gives every
+ *     CU two workgroups, else 128 x 128;
+ *   BUDDY_GEMM_TILE_128, BUDDY_GEMM_TILE_256: always that tile (weight
+ *     rows x token rows). */
+typedef enum {
+    BUDDY_GEMM_TILE_AUTO = 0,
+    BUDDY_GEMM_TILE_128 = 1,
+    BUDDY_GEMM_TILE_256 = 2
+} buddy_gemm_tile;
+
+/* Sets the tile choice of a handle; BUDDY_EINVAL for an unknown value. */
+buddy_status buddy_set_gemm_tile(buddy_model* m, int32_t tile);
+
 /* Kernels of a decoder block, for buddy_set_timing_events. */
 typedef enum {
     BUDDY_KERNEL_QKV = 0,        /* RMSNorm + QKV projection + rotary + KV append */

@@ -117,7 +117,7 @@ hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, 
     // prompt tokens of a prefill: the tiled GEMM
     if (M.cfg.dtype == BUDDY_BF16 && g.tok_T > 0 && g.rows.exact && batch >= kGemmMinRows &&
         g.K % 64 == 0)
-        return launch_gemm(pro, epi, g, s);
+        return launch_gemm(pro, epi, g, M.gemm_tile, s);
     if (M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && g.K % 128 == 0)
         return launch_mfma(pro, epi, g, s);
     return launch_gemv(M.cfg.dtype, pro, epi, g, s);
@@ -808,6 +808,12 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
 buddy_status buddy_set_launch_policy(buddy_model* h, int32_t policy) {
     if (!h || policy < BUDDY_LAUNCH_AUTO || policy > BUDDY_LAUNCH_HOST_ROUTED) return BUDDY_EINVAL;
     h->M.policy = policy;
+    return BUDDY_OK;
+}
+
+buddy_status buddy_set_gemm_tile(buddy_model* h, int32_t tile) {
+    if (!h || tile < BUDDY_GEMM_TILE_AUTO || tile > BUDDY_GEMM_TILE_256) return BUDDY_EINVAL;
+    h->M.gemm_tile = tile;
     return BUDDY_OK;
 }
 

@@ -143,6 +143,7 @@ struct Model {
     buddy_config cfg;
     TimingHook timing;
     int policy;                   // buddy_launch_policy
+    int gemm_tile;                // buddy_gemm_tile
     int32_t* h_cnt;               // mapped pinned host memory: [L-2] counts, then a sequence number
     int32_t* d_host_cnt;          // device address of h_cnt
     int32_t seq;                  // sequence number of the last published route
@@ -300,7 +301,7 @@ hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s);
 hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s);
 // Tiled MFMA GEMM for many rows (prompt tokens): exact row counts, bf16
 // weights, K a multiple of 64.
-hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, hipStream_t s);
+hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, hipStream_t s);
 constexpr int kGemmMinRows = 64;
 // Routed rows above which a bf16 projection takes the MFMA path.
 constexpr int kGemvMaxRows = 4;

@@ -2,21 +2,25 @@
 // routed prefill): Y = W X^T with v_mfma_f32_16x16x32_bf16, fp32 accumulate,
 // and the fused epilogues of the decode paths.
 //
-// A workgroup computes a 128-weight-row x 128-row tile (for the two-row
-// kinds: 64 units, their first rows in tile rows 0..63 and their second rows
-// in 64..127), stepping K by 64.  Both operands pass through LDS in MFMA
-// fragment order, so each wavefront reads a fragment as one conflict-free
-// 16-byte read per lane:
-//   A fragment (row tile rt, k-step s): 1 KB at (rt * 2 + s) KB, lane
-//     i + 16 q holding tile row 16 rt + i, k = 32 s + 8 q .. + 7;
-//   B fragment (column tile ct, k-step s): 1 KB at (ct * 2 + s) KB, copied
-//     as is from the activations, which the staging kernel already wrote in
+// A workgroup of WM x WN wavefronts computes a (16 WM TI weight rows) x
+// (16 WN TJ rows) tile, each wavefront TI x TJ accumulator tiles of 16 x 16,
+// stepping K by 32.  For the two-row kinds (SwiGLU, QKV) the weight rows of
+// a tile are 8 WM TI units: their first rows in the upper half of the row
+// tiles and their second rows in the lower half, and each wavefront holds
+// the first and second rows of the same units.  Two shapes:
+//   128 x 128 (2 x 2 wavefronts of 64 x 64), two workgroups per CU;
+//   256 x 256 (2 x 4 wavefronts of 128 x 64), one workgroup per CU, which
+//     halves the bytes each CU fetches per flop (the loads through the
+//     texture path, not the MFMA, bound the smaller tile).
+// Both operands pass through LDS in MFMA fragment order, so each wavefront
+// reads a fragment as one conflict-free 16-byte read per lane:
+//   A fragment (row tile rt): 1 KB at rt KB of the step's buffer, lane
+//     i + 16 q holding tile row 16 rt + i, k = 8 q .. + 7 of the step;
+//   B fragment (column tile ct): 1 KB after the A fragments, copied as is
+//     from the activations, which the staging kernel already wrote in
 //     B-operand order (16 rows x 32 k per contiguous KB).
-// The next K step's tiles travel straight from memory to the idle LDS
-// buffer (global_load_lds) while the current one is multiplied (two
-// buffers, one barrier per step).  Wavefront w takes
-// tile rows of half w / 2 (for two-row kinds: its 32 units' first and second
-// rows) and tile columns of half w % 2: 4 x 4 accumulator tiles.
+// Tiles travel straight from memory to LDS (global_load_lds) three K steps
+// ahead of the multiply (four buffers, one barrier per step).
 //   D[i][j] (16 x 16): lane j + 16 (i / 4), element i % 4.
 #include "buddy_internal.h"
 #include "epilogue.h"
@@ -25,133 +29,195 @@ namespace buddy {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-constexpr int kTileM = 128, kTileN = 128, kTileK = 64;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 typedef __attribute__((address_space(1))) const void* gptr_t;
 typedef __attribute__((address_space(3))) void* lptr_t;
 
-// Two workgroups per CU (64 KB of LDS each): registers for two wavefronts
-// per SIMD.
-template <int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+constexpr int kTileK = 32;
+constexpr int kFragBytes = 1024;                 // one 16 x 32 bf16 fragment
+constexpr int kBufs = 4;                         // K steps in LDS, three ahead
+
+// s_waitcnt operand: at most n vector-memory operations outstanding, other
+// counters unconstrained (gfx9 encoding: vmcnt low bits 3:0 and high bits
+// 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int vmcnt_at_most(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// LDS reads of 16 bytes at address a (and b) plus immediate offsets, then a
+// wait for them.  Written as asm so that the compiler, which cannot tell the
+// direct-to-LDS loads into the other buffers from these reads, does not make
+// them wait for every load in flight.
+template <int O0, int O1, int O2, int O3>
+__device__ __forceinline__ void lds_read4(uint32_t a, u32x4_t* x) {
+    asm volatile(
+        "ds_read_b128 %0, %4 offset:%5\n\t"
+        "ds_read_b128 %1, %4 offset:%6\n\t"
+        "ds_read_b128 %2, %4 offset:%7\n\t"
+        "ds_read_b128 %3, %4 offset:%8\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3])
+        : "v"(a), "i"(O0), "i"(O1), "i"(O2), "i"(O3)
+        : "memory");
+}
+template <int O0, int O1, int O2, int O3, int P0, int P1, int P2, int P3>
+__device__ __forceinline__ void lds_read8(uint32_t a, uint32_t b, u32x4_t* x, u32x4_t* y) {
+    asm volatile(
+        "ds_read_b128 %0, %8 offset:%10\n\t"
+        "ds_read_b128 %1, %8 offset:%11\n\t"
+        "ds_read_b128 %2, %8 offset:%12\n\t"
+        "ds_read_b128 %3, %8 offset:%13\n\t"
+        "ds_read_b128 %4, %9 offset:%14\n\t"
+        "ds_read_b128 %5, %9 offset:%15\n\t"
+        "ds_read_b128 %6, %9 offset:%16\n\t"
+        "ds_read_b128 %7, %9 offset:%17\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(y[0]), "=&v"(y[1]),
+          "=&v"(y[2]), "=&v"(y[3])
+        : "v"(a), "v"(b), "i"(O0), "i"(O1), "i"(O2), "i"(O3), "i"(P0), "i"(P1), "i"(P2),
+          "i"(P3)
+        : "memory");
+}
+
+template <int WM, int WN, int TI, int TJ>
+struct GemmShape {
+    static constexpr int kWaves = WM * WN, kThreads = 64 * kWaves;
+    static constexpr int kRowTiles = WM * TI, kColTiles = WN * TJ;
+    static constexpr int kRows = 16 * kRowTiles, kCols = 16 * kColTiles;
+    static constexpr int kBufBytes = (kRowTiles + kColTiles) * kFragBytes;
+    // fragments each wavefront loads per K step
+    static constexpr int kALoads = kRowTiles / kWaves, kBLoads = kColTiles / kWaves;
+    static_assert(kRowTiles % kWaves == 0 && kColTiles % kWaves == 0, "even load split");
+    static_assert(kBufs * kBufBytes <= 128 * 1024, "LDS");
+    static_assert(TJ == 4 && (TI == 4 || TI == 8), "wavefront tile");
+};
+
+template <int EPI, int WM, int WN, int TI, int TJ>
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_kernel(GemvArgs g, int units, int n) {
+    using Sh = GemmShape<WM, WN, TI, TJ>;
     constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
-    // two buffers as separate arrays, so that the compiler can tell the loads
-    // into one from the reads of the other and keep the loads in flight
-    __shared__ uint4 s_a0[kTileM * kTileK / 8], s_a1[kTileM * kTileK / 8];   // 16 A fragments
-    __shared__ uint4 s_b0[kTileN * kTileK / 8], s_b1[kTileN * kTileK / 8];   // 16 B fragments
+    __shared__ __attribute__((aligned(16))) char s_buf[kBufs * Sh::kBufBytes];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int K = g.K, S = K >> 5, nk = K / kTileK;
-    const int u0 = blockIdx.x * (kPaired ? kTileM / 2 : kTileM);   // first unit or row
-    const int t0 = blockIdx.y * kTileN;                             // first row (token)
-    const int last_tile = (n - 1) >> 4;                             // last 16-row column tile
+    const int u0 = blockIdx.x * (kPaired ? Sh::kRows / 2 : Sh::kRows);   // first unit or row
+    const int t0 = blockIdx.y * Sh::kCols;                               // first row (token)
+    const int last_tile = (n - 1) >> 4;                                   // last 16-row column tile
 
     // Direct global -> LDS loads (each lane's 16 bytes land at the wave's LDS
-    // base + 16 lane): wavefront w loads the A fragments of row tiles 2w and
-    // 2w + 1 and the B fragments of column tiles 2w and 2w + 1, both k-steps.
-    // A fragment lane i + 16 q: tile row 16 rt + i, k = 32 s + 8 q.
-    const bf16_t* arow[2];
+    // base + 16 lane): wavefront w loads row tiles kALoads w .. and column
+    // tiles kBLoads w .. of every step.
+    // A fragment lane i + 16 q: tile row 16 rt + i, k = 8 q of the step.
+    const bf16_t* arow[Sh::kALoads];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int r = 16 * (2 * wave + t) + (lane & 15);
+    for (int t = 0; t < Sh::kALoads; ++t) {
+        const int r = 16 * (Sh::kALoads * wave + t) + (lane & 15);
         int row;
         if (kPaired) {
-            const int u = min(u0 + (r & 63), units - 1);
+            const int half = Sh::kRows / 2;
+            const int u = min(u0 + (r % half), units - 1);
             int r0, r1;
             unit_rows<EPI>(g, u, r0, r1);
-            row = r < 64 ? r0 : r1;
+            row = r < half ? r0 : r1;
         } else {
             row = min(u0 + r, units - 1);
         }
         arow[t] = (const bf16_t*)g.W + (size_t)row * K + 8 * (lane >> 4);
     }
-    const bf16_t* bfrag[2];
+    const bf16_t* bfrag[Sh::kBLoads];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int c = min((t0 >> 4) + 2 * wave + t, last_tile);   // repeats of the last tile are discarded
+    for (int t = 0; t < Sh::kBLoads; ++t) {
+        const int c = min((t0 >> 4) + Sh::kBLoads * wave + t, last_tile);   // repeats of the last tile are discarded
         bfrag[t] = g.XB + ((size_t)c * S * 64 + lane) * 8;
     }
-    auto issue = [&](int kb, uint4* sa, uint4* sb) {
+    // one load per fragment; steps past the end reload the last one into a
+    // buffer that is not read again
+    auto issue = [&](int kb) {
+        const int kc = min(kb, nk - 1);
+        char* base = s_buf + (kb % kBufs) * Sh::kBufBytes;
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < Sh::kALoads; ++t)
+            __builtin_amdgcn_global_load_lds((gptr_t)(arow[t] + kc * kTileK),
+                                             (lptr_t)(base + (Sh::kALoads * wave + t) * kFragBytes),
+                                             16, 0, 0);
 #pragma unroll
-            for (int s = 0; s < 2; ++s) {
-                __builtin_amdgcn_global_load_lds((gptr_t)(arow[t] + kb * kTileK + 32 * s),
-                                                 (lptr_t)&sa[((2 * wave + t) * 2 + s) * 64], 16, 0, 0);
-                __builtin_amdgcn_global_load_lds((gptr_t)(bfrag[t] + (size_t)(2 * kb + s) * 512),
-                                                 (lptr_t)&sb[((2 * wave + t) * 2 + s) * 64], 16, 0, 0);
-            }
+        for (int t = 0; t < Sh::kBLoads; ++t)
+            __builtin_amdgcn_global_load_lds(
+                (gptr_t)(bfrag[t] + (size_t)kc * 512),
+                (lptr_t)(base + (Sh::kRowTiles + Sh::kBLoads * wave + t) * kFragBytes), 16, 0, 0);
     };
+    constexpr int kLoads = Sh::kALoads + Sh::kBLoads;   // per wavefront and step
 
-    f32x4_t acc[4][4];
+    f32x4_t acc[TI][TJ];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-    // this wavefront's row tiles: its units' first rows then second rows, or 4 row tiles
-    int rts[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) rts[i] = kPaired ? (i < 2 ? 2 * wm + i : 4 + 2 * wm + (i - 2)) : 4 * wm + i;
+        for (int j = 0; j < TJ; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    // this wavefront's fragments within a buffer.  Row tiles: paired, its
+    // units' first rows (TI/2 tiles from wm TI/2) and second rows (the same
+    // TI/2 tiles of the lower half); otherwise TI tiles from wm TI.  Column
+    // tiles: TJ from wn TJ.
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lptr_t)s_buf;
+    const uint32_t a_off = lds0 + lane * 16 + (kPaired ? wm * TI / 2 : wm * TI) * kFragBytes;
+    const uint32_t b_off = lds0 + lane * 16 + (Sh::kRowTiles + wn * TJ) * kFragBytes;
+    constexpr int kSecond = kPaired ? Sh::kRowTiles / 2 - TI / 2 : 0;   // gap to the second rows
+    constexpr int F = kFragBytes;
 
-    auto compute = [&](const uint4* sa, const uint4* sb) {
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            bf16x8_t a[4], bv[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                a[i] = __builtin_bit_cast(bf16x8_t, sa[(rts[i] * 2 + s) * 64 + lane]);
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                bv[j] = __builtin_bit_cast(bf16x8_t, sb[((4 * wn + j) * 2 + s) * 64 + lane]);
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], bv[j], acc[i][j], 0, 0, 0);
+    // At step kb: wait until only the loads of steps kb + 1 and kb + 2 are
+    // outstanding, barrier (every wavefront's loads of step kb have landed
+    // and every wavefront has read step kb - 1's buffer), refill that buffer
+    // with step kb + 3, multiply step kb.
+    issue(0);
+    issue(1);
+    issue(2);
+    for (int kb = 0; kb < nk; ++kb) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_at_most(2 * kLoads));
+        // a plain barrier: __syncthreads() would also wait for every load in
+        // flight (its fence covers the direct-to-LDS writes)
+        asm volatile("s_barrier" ::: "memory");
+        issue(kb + 3);
+        const uint32_t sb = (kb % kBufs) * Sh::kBufBytes;
+        u32x4_t a[TI], bv[TJ];
+        if constexpr (TI == 4) {
+            lds_read8<0, F, (2 + kSecond) * F, (3 + kSecond) * F, 0, F, 2 * F, 3 * F>(
+                a_off + sb, b_off + sb, a, bv);
+        } else {
+            lds_read8<0, F, 2 * F, 3 * F, 0, F, 2 * F, 3 * F>(a_off + sb, b_off + sb, a, bv);
+            lds_read4<(4 + kSecond) * F, (5 + kSecond) * F, (6 + kSecond) * F, (7 + kSecond) * F>(
+                a_off + sb, a + 4);
         }
-    };
-
-    // Two K steps per trip, one per buffer.  At each step: this step's tiles
-    // have landed (own loads, then everyone's at the barrier) and every
-    // wavefront is done reading the other buffer, which then receives the
-    // next step's tiles while this one is multiplied.
-    issue(0, s_a0, s_b0);
-    for (int kb = 0; kb < nk; kb += 2) {
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (kb + 1 < nk) issue(kb + 1, s_a1, s_b1);
-        compute(s_a0, s_b0);
-        if (kb + 1 >= nk) break;
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (kb + 2 < nk) issue(kb + 2, s_a0, s_b0);
-        compute(s_a1, s_b1);
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(bf16x8_t, a[i]), __builtin_bit_cast(bf16x8_t, bv[j]),
+                    acc[i][j], 0, 0, 0);
     }
+    __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));   // the reloads past the end
 
     // epilogue from the accumulators: rows 4 (lane / 16) + e of each tile
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int col = t0 + 64 * wn + 16 * j + (lane & 15);
+    for (int j = 0; j < TJ; ++j) {
+        const int col = t0 + 16 * (wn * TJ + j) + (lane & 15);
         if (col >= n) continue;
         const int b = row_seq(g.rows, col);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             if (kPaired) {
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const int u = u0 + 32 * wm + 16 * i + 4 * (lane >> 4) + e;
+                for (int i = 0; i < TI / 2; ++i) {
+                    const int u = u0 + 16 * (wm * TI / 2 + i) + 4 * (lane >> 4) + e;
                     if (u >= units) continue;
                     int r0, r1;
                     unit_rows<EPI>(g, u, r0, r1);
-                    epilogue<bf16_t, EPI>(g, b, u, r0, r1, acc[i][j][e], acc[2 + i][j][e]);
+                    epilogue<bf16_t, EPI>(g, b, u, r0, r1, acc[i][j][e], acc[TI / 2 + i][j][e]);
                 }
             } else {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int r = u0 + 64 * wm + 16 * i + 4 * (lane >> 4) + e;
+                for (int i = 0; i < TI; ++i) {
+                    const int r = u0 + 16 * (wm * TI + i) + 4 * (lane >> 4) + e;
                     if (r < units) epilogue1<bf16_t, EPI>(g, b, r, acc[i][j][e]);
                 }
             }
@@ -159,22 +225,43 @@ void gemm_kernel(GemvArgs g, int units, int n) {
     }
 }
 
+template <int EPI, int WM, int WN, int TI, int TJ>
+static dim3 gemm_grid(int units, int n) {
+    using Sh = GemmShape<WM, WN, TI, TJ>;
+    constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
+    const int per = kPaired ? Sh::kRows / 2 : Sh::kRows;
+    return dim3((units + per - 1) / per, (n + Sh::kCols - 1) / Sh::kCols);
+}
+
+template <int EPI, int WM, int WN, int TI, int TJ>
+static void gemm_launch(const GemvArgs& g, int units, int n, hipStream_t s) {
+    launch_main(gemm_kernel<EPI, WM, WN, TI, TJ>, gemm_grid<EPI, WM, WN, TI, TJ>(units, n),
+                dim3(GemmShape<WM, WN, TI, TJ>::kThreads), 0, s, g, units, n);
+}
+
+// Tile choice (automatic): 256 x 256 where it still gives the CUs two
+// rounds of workgroups, else 128 x 128 (two per CU).  A 256 x 128 tile with
+// one wavefront per SIMD was slower than 128 x 128 on the 4096-row
+// projections (measured).
 template <int EPI>
-static hipError_t launch_gemm_epi(const GemvArgs& g, int units, hipStream_t s) {
-    constexpr int per = EPI == EPI_SWIGLU || EPI == EPI_QKV ? kTileM / 2 : kTileM;
+static hipError_t launch_gemm_epi(const GemvArgs& g, int units, int tile, hipStream_t s) {
     const int n = g.rows.n_max;
-    const dim3 grid((units + per - 1) / per, (n + kTileN - 1) / kTileN);
-    launch_main(gemm_kernel<EPI>, grid, dim3(256), 0, s, g, units, n);
+    const dim3 big = gemm_grid<EPI, 2, 4, 8, 4>(units, n);
+    if (tile == BUDDY_GEMM_TILE_256 || (tile == BUDDY_GEMM_TILE_AUTO && big.x * big.y >= 512))
+        gemm_launch<EPI, 2, 4, 8, 4>(g, units, n, s);
+    else
+        gemm_launch<EPI, 2, 2, 4, 4>(g, units, n, s);
     return hipGetLastError();
 }
 
-hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, hipStream_t s) {
+hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, hipStream_t s) {
     hipError_t e = launch_prep(pro, g, s);
     if (e != hipSuccess) return e;
-    if (epi == EPI_QKV) return launch_gemm_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), s);
-    if (epi == EPI_SWIGLU) return launch_gemm_epi<EPI_SWIGLU>(g, g.f, s);
-    if (epi == EPI_BIAS_ACT) return launch_gemm_epi<EPI_BIAS_ACT>(g, g.N, s);
-    return launch_gemm_epi<EPI_ADD>(g, g.N, s);
+    if (epi == EPI_QKV)
+        return launch_gemm_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), tile, s);
+    if (epi == EPI_SWIGLU) return launch_gemm_epi<EPI_SWIGLU>(g, g.f, tile, s);
+    if (epi == EPI_BIAS_ACT) return launch_gemm_epi<EPI_BIAS_ACT>(g, g.N, tile, s);
+    return launch_gemm_epi<EPI_ADD>(g, g.N, tile, s);
 }
 
 }  // namespace buddy

@@ -22,6 +22,7 @@ CTX_KV, CTX_K, CTX_V, CTX_K_PLUS_V = 0, 1, 2, 3
 PRIOR_DELTA_PPL, PRIOR_TAYLOR, PRIOR_COSINE = 0, 1, 2
 CTX_BY_NAME = {"kv": CTX_KV, "k": CTX_K, "v": CTX_V, "k+v": CTX_K_PLUS_V}
 LAUNCH_AUTO, LAUNCH_DEVICE_ROUTED, LAUNCH_HOST_ROUTED = 0, 1, 2
+GEMM_TILE_AUTO, GEMM_TILE_128, GEMM_TILE_256 = 0, 1, 2
 KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN = range(5)
 
 
@@ -84,6 +85,8 @@ def lib():
         L.buddy_decode_step.restype = C.c_int
         L.buddy_set_launch_policy.argtypes = [vp, i32]
         L.buddy_set_launch_policy.restype = C.c_int
+        L.buddy_set_gemm_tile.argtypes = [vp, i32]
+        L.buddy_set_gemm_tile.restype = C.c_int
         L.buddy_set_timing_events.argtypes = [vp, i32, i32, vp, vp, i32]
         L.buddy_set_timing_events.restype = C.c_int
         L.buddy_set_budget_predictor.argtypes = [vp, P(PredictorWeights)]
@@ -300,6 +303,9 @@ class Model:
 
     def set_launch_policy(self, policy: int) -> None:
         _raise(lib().buddy_set_launch_policy(self._h, int(policy)), self._h)
+
+    def set_gemm_tile(self, tile: int) -> None:
+        _raise(lib().buddy_set_gemm_tile(self._h, int(tile)), self._h)
 
     def set_timing_events(self, kernel: int, layer: int, starts, stops) -> None:
         """starts/stops: sequences of raw hipEvent_t handles (ints)."""

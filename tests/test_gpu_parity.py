@@ -395,6 +395,38 @@ def test_prefill_head_dim_128(G, masked):
     check_prefill(P, [150, 61], [1, 2], 150, masked=masked, seed=114)
 
 
+def gpu_prefill(P, lens, ks, t_stride, seed):
+    """GPU prefill from zeroed caches: hidden outputs, route, K and V."""
+    B, d = len(lens), P.cfg["d_model"]
+    hk, hv = P.empty_host_cache()
+    x = synth.hidden_inputs(B * t_stride, d, seed=seed).numpy().reshape(B, t_stride, d)
+    dk, dv = P.upload(hk), P.upload(hv)
+    hidden = torch.from_numpy(x.copy()).cuda()
+    mask = torch.zeros((B, P.L_mid), dtype=torch.uint8, device="cuda")
+    P.gpu.prefill(dk, dv, hidden, lens, ks, mask_out=mask)
+    torch.cuda.synchronize()
+    return hidden.cpu().numpy(), mask.cpu().numpy(), P.download(dk), P.download(dv)
+
+
+@pytest.mark.parametrize("G", [4, 8])
+def test_prefill_gemm_tiles(G):
+    """The 256 x 256 tile of the prefill projections (forced on a small
+    model) against the oracle, and bit for bit equal to the 128 x 128 tile
+    (every output accumulates over K in the same order): 211 prompt rows
+    fill one partial column tile; paired (QKV, SwiGLU) and single-row
+    (O, down) epilogues."""
+    P = Pair(gqa_shape(G), "bf16", 160, 2, seed=117 + G, omega=0.1)
+    P.gpu.set_gemm_tile(blib.GEMM_TILE_256)
+    check_prefill(P, [150, 61], [1, 2], 150, seed=118)
+    outs = []
+    for tile in (blib.GEMM_TILE_128, blib.GEMM_TILE_256):
+        P.gpu.set_gemm_tile(tile)
+        outs.append(gpu_prefill(P, [150, 61], [1, 2], 150, seed=118))
+    for other in outs[1:]:
+        for a, b in zip(outs[0], other):
+            assert np.array_equal(a, b)
+
+
 def test_prefill_route_override():
     P = Pair("tiny", "bf16", 32, 2, seed=115, omega=0.1)
     route = np.array([[1, 0, 0, 1, 1, 0], [0, 0, 0, 0, 0, 0]], np.uint8)
