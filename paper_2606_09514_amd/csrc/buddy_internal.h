@@ -316,9 +316,9 @@ struct AttnArgs {
     float* part; int max_chunks;
     const uint8_t* exec;                // this block's execution map [bcap][T], or null
     int tok_T;                          // > 0: rows are prompt tokens (slot_pos)
-    // prompt tokens on the MFMA score kernel: groups of up to 16 / G
+    // prompt tokens on the prefill attention kernel: groups of up to 64 / G
     // consecutive tokens of one prompt, (first row index, count) pairs; one
-    // workgroup per group (null: one per row)
+    // workgroup per (KV head, group) (null: one per row)
     const int32_t* groups; int n_groups;
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);

@@ -24,6 +24,8 @@
 //  attn_mfma_kernel  bf16, head_dim 128, three to eight query heads per KV
 //                    head: the scores of 16 rows against the group are one
 //                    MFMA product, P V stays on the vector ALUs.
+// The prompt tokens of a prefill (bf16, head_dim 128) take a third kernel,
+// attn_prefill_kernel, with both products on the MFMA (below).
 #include "buddy_internal.h"
 
 namespace buddy {
@@ -241,40 +243,21 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t bf16_bits(float x) { return (uint32_t)f2bf(x); }
 
-// MQ (prompt tokens): the 16 MFMA columns are (token, head) pairs of a group
-// of up to 16 / G consecutive tokens of one prompt, column j = token j / G,
-// head j % G, so a slab of K/V rows is read once for the group; each column
-// attends to the rows up to its own token's position (causal).
-template <int GM, bool MQ>
+template <int GM>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     constexpr int HD = 128, KS = HD / 32;
-    __shared__ float s_p[4][16][16];          // per wave: p[column][slab row]
-    __shared__ float s_al[4][16];             // per wave: rescale of each column
+    __shared__ float s_p[4][16][16];          // per wave: p[head][slab row]
+    __shared__ float s_al[4][16];             // per wave: rescale of each head
     __shared__ float s_acc[4][GM][HD + 2];
     const int i = blockIdx.z;
-    if (!MQ && !a.rows.exact && i >= *a.rows.cnt) return;
+    if (!a.rows.exact && i >= *a.rows.cnt) return;
+    const int b = row_seq(a.rows, i);
+    const int g = blockIdx.y, c = blockIdx.x;
+    int slot, pos;
+    slot_pos(b, a.tok_T, a.pos, a.pos_u, slot, pos);
     const int G = a.nq / a.nkv;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int g = blockIdx.y, c = blockIdx.x;
-    // this lane's column: token qt of the group (always 0 without MQ), head hq
-    const int first = MQ ? a.groups[2 * i] : i;
-    const int count = MQ ? a.groups[2 * i + 1] : 1;
-    const int qt = MQ ? (lane & 15) / G : 0, hq = MQ ? (lane & 15) % G : (lane & 15);
-    const bool col_ok = MQ ? qt < count : hq < G;
-    const int b = row_seq(a.rows, first);                     // first token: the group's slot
-    const int bq = MQ ? row_seq(a.rows, first + min(qt, count - 1)) : b;
-    int slot, pos, posq;
-    slot_pos(b, a.tok_T, a.pos, a.pos_u, slot, pos);
-    if (MQ) {
-        int sq;
-        slot_pos(bq, a.tok_T, a.pos, a.pos_u, sq, posq);
-        int sl, pl;
-        slot_pos(row_seq(a.rows, first + count - 1), a.tok_T, a.pos, a.pos_u, sl, pl);
-        pos = pl;                                             // the group's last position
-    } else {
-        posq = pos;
-    }
     const int j0 = c * a.chunk_len;
     const int j1 = min(j0 + a.chunk_len, pos + 1);
     const size_t base = ((size_t)slot * a.nkv + g) * a.T * HD;
@@ -285,9 +268,9 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     // softmax weight, as bf16 high + low parts; heads past G are zero
     bf16x8_t qh[KS], ql[KS];
     {
-        const int q8 = 8 * (lane >> 4);
+        const int h = lane & 15, q8 = 8 * (lane >> 4);
         const float qs = 1.4426950408889634f / sqrtf((float)HD);
-        const float* qp = a.q + ((size_t)bq * a.nq + g * G + min(hq, G - 1)) * HD + q8;
+        const float* qp = a.q + ((size_t)b * a.nq + g * G + min(h, G - 1)) * HD + q8;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             const float4 x0 = *reinterpret_cast<const float4*>(qp + 32 * s);
@@ -296,7 +279,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
             uint32_t hi[4], lo[4];
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const float v0 = col_ok ? xv[e] * qs : 0.f, v1 = col_ok ? xv[e + 1] * qs : 0.f;
+                const float v0 = h < G ? xv[e] * qs : 0.f, v1 = h < G ? xv[e + 1] * qs : 0.f;
                 const uint32_t h0 = bf16_bits(v0), h1 = bf16_bits(v1);
                 const float r0 = v0 - __uint_as_float(h0 << 16), r1 = v1 - __uint_as_float(h1 << 16);
                 hi[e / 2] = h0 | (h1 << 16);
@@ -342,7 +325,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int jrow = jb + 4 * (lane >> 4) + v;
-            sc[v] = jrow < j1 && jrow <= posq && (ex[v] != 0 || jrow == posq) ? d[v] : -INFINITY;
+            sc[v] = jrow < j1 && (ex[v] != 0 || jrow == pos) ? d[v] : -INFINITY;
         }
         float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
         mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
@@ -397,10 +380,9 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     }
     __syncthreads();
 
-    // merge the four wavefronts and write this chunk's partial (MQ: one
-    // chunk, the output rows of the group's tokens)
+    // merge the four wavefronts and write this chunk's partial
     const size_t pstride = (size_t)HD + 2;
-    for (int t = tid; t < (MQ ? count * G : G) * HD; t += 256) {
+    for (int t = tid; t < G * HD; t += 256) {
         const int h = t / HD, e = t % HD;
         float M = -INFINITY;
         for (int w = 0; w < 4; ++w) M = fmaxf(M, s_acc[w][h][HD]);
@@ -410,10 +392,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
             L += s_acc[w][h][HD + 1] * sw;
             A += s_acc[w][h][e] * sw;
         }
-        if (MQ) {
-            const int bt = row_seq(a.rows, first + h / G);
-            a.o[((size_t)bt * a.nq + g * G + h % G) * HD + e] = A / L;
-        } else if (a.chunks == 1) {
+        if (a.chunks == 1) {
             a.o[((size_t)b * a.nq + g * G + h) * HD + e] = A / L;
         } else {
             float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
@@ -422,6 +401,267 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         }
     }
 }
+
+// ------------------------------------------------------ prefill attention
+
+// Causal attention of the prompt tokens of a prefill (bf16 cache, head_dim
+// 128): one workgroup per (KV head, group of up to 64 / G consecutive tokens
+// of one prompt); its 64 query rows are (token, head) pairs, 16 per
+// wavefront.  K and V tiles of 64 rows pass through LDS (two buffers, the
+// next tile's direct-to-LDS loads in flight while the current one is used),
+// each row's 16-byte chunks stored at chunk ^ (row % 16) so that both reads
+// below are free of bank conflicts.  Per tile and wavefront:
+//   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = K rows from LDS, B = the
+//                 queries (held as bf16 high and low parts, as in the decode
+//                 kernel); D: lane q + 16 r holds rows 4 r .. 4 r + 3 of q;
+//   softmax       online per query row (exp2 of prescaled scores), causal
+//                 through each row's own position;
+//   O += P V      v_mfma_f32_16x16x16_bf16: the A operand (4 consecutive
+//                 rows per lane) is the softmax of S^T in place, the B
+//                 operand V[4 rows][d] comes from ds_read_b64_tr_b16, whose
+//                 16-lane groups return element l % 4 of the 8-byte block
+//                 addressed by lane l / 4 + 4 e (checked on the device).
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(1))) const void* pf_gptr_t;
+typedef __attribute__((address_space(3))) void* pf_lptr_t;
+
+constexpr int kPfRows = 64;                      // K/V rows per tile
+constexpr int kPfTile = kPfRows * 128 * 2;       // bytes of a K or V tile
+
+// Four 16-byte LDS reads at per-lane addresses plus one immediate, then a
+// wait; asm so that the compiler does not wait for the direct-to-LDS loads
+// into the other buffer first.
+template <int OFF>
+__device__ __forceinline__ void pf_read_k(const uint32_t* ad, uint32_t base, bf16x8_t* x) {
+    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+    u4 r0, r1, r2, r3;
+    asm volatile(
+        "ds_read_b128 %0, %4 offset:%8\n\t"
+        "ds_read_b128 %1, %5 offset:%8\n\t"
+        "ds_read_b128 %2, %6 offset:%8\n\t"
+        "ds_read_b128 %3, %7 offset:%8\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r0), "=&v"(r1), "=&v"(r2), "=&v"(r3)
+        : "v"(ad[0] + base), "v"(ad[1] + base), "v"(ad[2] + base), "v"(ad[3] + base), "i"(OFF)
+        : "memory");
+    x[0] = __builtin_bit_cast(bf16x8_t, r0);
+    x[1] = __builtin_bit_cast(bf16x8_t, r1);
+    x[2] = __builtin_bit_cast(bf16x8_t, r2);
+    x[3] = __builtin_bit_cast(bf16x8_t, r3);
+}
+// Eight transposing 8-byte reads (the V fragments of the 8 column tiles).
+template <int OFF>
+__device__ __forceinline__ void pf_read_v(const uint32_t* ad, uint32_t base, s16x4_t* x) {
+    i32x2_t r[8];
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %8 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %1, %9 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %2, %10 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %3, %11 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %4, %12 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %5, %13 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %6, %14 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %7, %15 offset:%16\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]),
+          "=&v"(r[6]), "=&v"(r[7])
+        : "v"(ad[0] + base), "v"(ad[1] + base), "v"(ad[2] + base), "v"(ad[3] + base),
+          "v"(ad[4] + base), "v"(ad[5] + base), "v"(ad[6] + base), "v"(ad[7] + base), "i"(OFF)
+        : "memory");
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = __builtin_bit_cast(s16x4_t, r[i]);
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_prefill_kernel(AttnArgs a) {
+    constexpr int HD = 128;
+    __shared__ __attribute__((aligned(16))) char s_kv[2][2][kPfTile];   // [buffer][K | V]
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = blockIdx.y;
+    const int gi = a.n_groups - 1 - blockIdx.z;            // the longest groups first
+    const int first = a.groups[2 * gi], count = a.groups[2 * gi + 1];
+    const int G = a.nq / a.nkv;
+    int slot, pos0;
+    slot_pos(row_seq(a.rows, first), a.tok_T, a.pos, a.pos_u, slot, pos0);
+    const int pos_last = pos0 + count - 1;
+    const int ntiles = pos_last / kPfRows + 1;
+
+    // this lane's query row (S^T column, softmax row): 16 wave + lane % 16
+    const int qr = 16 * wave + (lane & 15);
+    const int qt = qr / G, hq = qr - qt * G;
+    const bool q_ok = qt < count;
+    const int q_pos = pos0 + qt;
+    bf16x8_t qh[4], ql[4];
+    {
+        const int bq = row_seq(a.rows, first + min(qt, count - 1));
+        const float qs = 1.4426950408889634f / sqrtf((float)HD);
+        const float* qp = a.q + ((size_t)bq * a.nq + g * G + hq) * HD + 8 * (lane >> 4);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const float4 x0 = *reinterpret_cast<const float4*>(qp + 32 * s);
+            const float4 x1 = *reinterpret_cast<const float4*>(qp + 32 * s + 4);
+            const float xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+            uint32_t hi[4], lo[4];
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+                const float v0 = q_ok ? xv[e] * qs : 0.f, v1 = q_ok ? xv[e + 1] * qs : 0.f;
+                const uint32_t h0 = bf16_bits(v0), h1 = bf16_bits(v1);
+                const float r0 = v0 - __uint_as_float(h0 << 16), r1 = v1 - __uint_as_float(h1 << 16);
+                hi[e / 2] = h0 | (h1 << 16);
+                lo[e / 2] = bf16_bits(r0) | (bf16_bits(r1) << 16);
+            }
+            qh[s] = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+            ql[s] = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+        }
+    }
+
+    // Tile loads: wavefront w moves rows 16 w .. 16 w + 15 of K and of V, four
+    // rows (1 KB) per load; lane L lands at 16 L of the load's block, i.e. row
+    // L / 16 of it and stored chunk L % 16, which holds source chunk
+    // (L % 16) ^ (row % 16).  Rows past the last position repeat it (masked).
+    const size_t cbase = ((size_t)slot * a.nkv + g) * a.T * HD;
+    const bf16_t* Kg = (const bf16_t*)a.kc + cbase;
+    const bf16_t* Vg = (const bf16_t*)a.vc + cbase;
+    auto issue = [&](int kt, int buf) {
+#pragma unroll
+        for (int ld = 0; ld < 4; ++ld) {
+            const int rl = 16 * wave + 4 * ld + (lane >> 4);          // row within the tile
+            const int row = min(kt * kPfRows + rl, pos_last);
+            const size_t src = (size_t)row * HD + (((lane & 15) ^ (rl & 15)) * 8);
+            const int dst = (16 * wave + 4 * ld) * 256;
+            __builtin_amdgcn_global_load_lds((pf_gptr_t)(Kg + src), (pf_lptr_t)(s_kv[buf][0] + dst),
+                                             16, 0, 0);
+            __builtin_amdgcn_global_load_lds((pf_gptr_t)(Vg + src), (pf_lptr_t)(s_kv[buf][1] + dst),
+                                             16, 0, 0);
+        }
+    };
+
+    // K fragment addresses (A operand: lane i + 16 dg holds row 16 t + i,
+    // d = 32 s + 8 dg .. + 7): stored chunk (4 s + dg) ^ i; the tile t of 16
+    // rows is an immediate 4 KB t.
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(pf_lptr_t)&s_kv[0][0][0];
+    const int li = lane & 15, lg = lane >> 4;
+    uint32_t kad[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) kad[s] = lds0 + li * 256 + (((4 * s + lg) ^ li) * 16);
+    // V addresses for ds_read_b64_tr_b16 (B operand: lane d + 16 r holds
+    // V[4 r .. 4 r + 3][d] of a 16-row tile): source lane s = lane % 16
+    // addresses row 4 r + s / 4, columns 16 dt + 4 (s % 4) .. + 3.
+    uint32_t vad[8];
+    {
+        const int rr = 4 * lg + (li >> 2);                          // row within a 16-row tile
+        const int cin = 4 * (li & 3);                                // column within the 16-column tile
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) {
+            const int col = 16 * dt + cin;
+            vad[dt] = lds0 + kPfTile + rr * 256 + (((col >> 3) ^ rr) * 16) + (col & 7) * 2;
+        }
+    }
+
+    float m_run = -INFINITY, l_run = 0.f;                           // query row lane % 16
+    f32x4_t o[8];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[dt] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+
+    issue(0, 0);
+    for (int kt = 0; kt < ntiles; ++kt) {
+        const int buf = kt & 1;
+        __builtin_amdgcn_s_waitcnt(0);                                 // this tile's loads
+        asm volatile("s_barrier" ::: "memory");                        // everyone's, and buffer buf ^ 1 is free
+        if (kt + 1 < ntiles) issue(kt + 1, buf ^ 1);
+        const uint32_t bb = buf * 2 * kPfTile;
+
+        // S^T for the 4 row tiles of the K tile
+        f32x4_t st[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            bf16x8_t kf[4];
+            switch (t) {
+                case 0: pf_read_k<0>(kad, bb, kf); break;
+                case 1: pf_read_k<4096>(kad, bb, kf); break;
+                case 2: pf_read_k<8192>(kad, bb, kf); break;
+                default: pf_read_k<12288>(kad, bb, kf); break;
+            }
+            f32x4_t d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qh[s], d, 0, 0, 0);
+                d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], ql[s], d, 0, 0, 0);
+            }
+            st[t] = d;
+        }
+        // causal mask and online softmax of query row lane % 16
+        const int r0 = kt * kPfRows + 4 * lg;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int row = r0 + 16 * t + e;
+                st[t][e] = q_ok && row <= q_pos ? st[t][e] : -INFINITY;
+                mx = fmaxf(mx, st[t][e]);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        const float mn = fmaxf(m_run, mx);
+        const float al = scale_of(m_run, mn);
+        float ls = 0.f;
+        s16x4_t pa[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            float p[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                p[e] = scale_of(st[t][e], mn);
+                ls += p[e];
+            }
+            pa[t] = __builtin_bit_cast(s16x4_t, make_uint2(bf16_bits(p[0]) | (bf16_bits(p[1]) << 16),
+                                                           bf16_bits(p[2]) | (bf16_bits(p[3]) << 16)));
+        }
+        ls += __shfl_xor(ls, 16, kWave);
+        ls += __shfl_xor(ls, 32, kWave);
+        l_run = l_run * al + ls;
+        m_run = mn;
+        // rescale O: lane d + 16 r holds query rows 4 r .. 4 r + 3
+        float ar[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ar[e] = __shfl(al, 4 * lg + e, kWave);
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[dt][e] *= ar[e];
+        // O += P V, 16 rows at a time
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            s16x4_t vf[8];
+            switch (t) {
+                case 0: pf_read_v<0>(vad, bb, vf); break;
+                case 1: pf_read_v<4096>(vad, bb, vf); break;
+                case 2: pf_read_v<8192>(vad, bb, vf); break;
+                default: pf_read_v<12288>(vad, bb, vf); break;
+            }
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt)
+                o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vf[dt], o[dt], 0, 0, 0);
+        }
+    }
+
+    // O / l, query rows 4 r + e of this lane
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float le = __shfl(l_run, 4 * lg + e, kWave);
+        const int r = 16 * wave + 4 * lg + e;
+        const int t = r / G, h = r - t * G;
+        if (t >= count) continue;
+        float* op = a.o + ((size_t)row_seq(a.rows, first + t) * a.nq + g * G + h) * HD + li;
+        const float inv = 1.f / le;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) op[16 * dt] = o[dt][e] * inv;
+    }
+}
+
 
 // Merge of the chunk partials of one (routed sequence, query head): the
 // chunk maxima and sums go through LDS once, then every thread folds one
@@ -462,7 +702,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 static bool attn_uses_mfma(int dtype, int hd, int G) { return dtype == BUDDY_BF16 && hd == 128 && G >= 3 && G <= kMaxGroup; }
 
 int attention_prefill_group(int dtype, int hd, int G) {
-    return attn_uses_mfma(dtype, hd, G) ? 16 / G : 1;
+    return dtype == BUDDY_BF16 && hd == 128 && G <= kMaxGroup ? 64 / G : 1;
 }
 
 int attention_rows_per_wg(int dtype, int hd, int G) {
@@ -477,13 +717,13 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     const int G = a.nq / a.nkv;   // query heads per KV head, held in registers
     // lanes per cache row: hd / 8 (bf16) or hd / 4 (fp32); head_dim is 64 or 128
     if (a.groups) {               // prompt-token groups (one chunk)
-        if (!attn_uses_mfma(dtype, a.hd, G) || a.chunks != 1) return hipErrorInvalidValue;
-        launch_main(attn_mfma_kernel<16, true>, dim3(1, a.nkv, a.n_groups), dim3(256), 0, s, a);
+        if (attention_prefill_group(dtype, a.hd, G) < 2 || a.chunks != 1) return hipErrorInvalidValue;
+        launch_main(attn_prefill_kernel, dim3(1, a.nkv, a.n_groups), dim3(256), 0, s, a);
         return hipGetLastError();
     }
     if (attn_uses_mfma(dtype, a.hd, G)) {
-        if (G <= 4) launch_main(attn_mfma_kernel<4, false>, grid, dim3(256), 0, s, a);
-        else launch_main(attn_mfma_kernel<kMaxGroup, false>, grid, dim3(256), 0, s, a);
+        if (G <= 4) launch_main(attn_mfma_kernel<4>, grid, dim3(256), 0, s, a);
+        else launch_main(attn_mfma_kernel<kMaxGroup>, grid, dim3(256), 0, s, a);
     } else if (dtype == BUDDY_BF16) {
         if (a.hd == 128) {
             if (G == 1) launch_main(attn_kernel<bf16_t, 1, 16>, grid, dim3(256), 0, s, a);
