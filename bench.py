@@ -31,7 +31,8 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0   # MI355X HBM3E peak
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic_llama3_8b_b1_ctx2048.md")
-KERNEL_SOURCES = ["paper_2606_09514_amd/csrc/k_gemv.hip", "paper_2606_09514_amd/csrc/buddy_internal.h"]
+KERNEL_SOURCES = ["paper_2606_09514_amd/csrc/k_gemv.hip", "paper_2606_09514_amd/csrc/epilogue.h",
+                  "paper_2606_09514_amd/csrc/buddy_internal.h"]
 
 
 def measured_traffic():
