@@ -296,23 +296,35 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int h = 0; h < GM; ++h) acc[h][0] = acc[h][1] = 0.f;
 
-    for (int jb = j0 + 16 * wave; jb < j1; jb += 64) {
-        // K fragments of the slab (rows clamped to a valid row, masked below)
-        // and its V rows, all issued before any arithmetic
-        bf16x8_t kf[KS];
+    // K fragments of a slab (rows clamped to a valid row, masked below) and
+    // its V rows and map entries; the next slab's are issued before the
+    // current one's arithmetic
+    bf16x8_t kn[KS];
+    uint32_t vn[16];
+    uint8_t en[4];
+    auto load_slab = [&](int jb) {
         const int jr = min(jb + (lane & 15), j1 - 1);
 #pragma unroll
         for (int s = 0; s < KS; ++s)
-            kf[s] = *reinterpret_cast<const bf16x8_t*>(Kb + (size_t)jr * HD + 32 * s + 8 * (lane >> 4));
+            kn[s] = *reinterpret_cast<const bf16x8_t*>(Kb + (size_t)jr * HD + 32 * s + 8 * (lane >> 4));
+#pragma unroll
+        for (int r = 0; r < 16; ++r) vn[r] = Vb[(size_t)min(jb + r, j1 - 1) * (HD / 2) + lane];
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            en[v] = a.exec ? a.exec[(size_t)slot * a.T + min(jb + 4 * (lane >> 4) + v, j1 - 1)] : 1;
+    };
+    if (j0 + 16 * wave < j1) load_slab(j0 + 16 * wave);
+    for (int jb = j0 + 16 * wave; jb < j1; jb += 64) {
+        bf16x8_t kf[KS];
         uint32_t vw[16];
+        uint8_t ex[4];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) vw[r] = Vb[(size_t)min(jb + r, j1 - 1) * (HD / 2) + lane];
-        uint8_t ex[4] = {1, 1, 1, 1};
-        if (a.exec) {
+        for (int s = 0; s < KS; ++s) kf[s] = kn[s];
 #pragma unroll
-            for (int v = 0; v < 4; ++v)
-                ex[v] = a.exec[(size_t)slot * a.T + min(jb + 4 * (lane >> 4) + v, j1 - 1)];
-        }
+        for (int r = 0; r < 16; ++r) vw[r] = vn[r];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) ex[v] = en[v];
+        if (jb + 64 < j1) load_slab(jb + 64);
 
         f32x4_t d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
