@@ -225,6 +225,86 @@ void gemm_kernel(GemvArgs g, int units, int n) {
     }
 }
 
+// ----------------------------------------------------------- staging
+
+// Activation staging for the tiled GEMM: the rows of a 16-row column tile
+// as bf16 in B-operand fragment order, with the RMSNorm folded in
+// (PRO_RMSNORM) or a plain conversion (PRO_NONE).  One workgroup of 16
+// wavefronts per tile (and, for PRO_NONE, per chunk of kPrepChunk columns):
+// wavefront w converts row w of the tile into LDS (rows padded by 16 bytes,
+// so the fragment reads below are conflict-free), then every thread writes
+// whole 16-byte pieces of the tile's fragments, consecutive threads to
+// consecutive addresses.  For the RMSNorm the row's sum of squares comes
+// first, over all of K.
+constexpr int kPrepChunk = 2048;                 // columns per LDS pass
+constexpr int kPrepPitch = kPrepChunk * 2 + 16;  // bytes per LDS row
+
+template <int PRO>
+__global__ __launch_bounds__(1024) void prep_tile_kernel(GemvArgs g, int n) {
+    __shared__ __attribute__((aligned(16))) char s_rows[16 * kPrepPitch];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int tile = blockIdx.x, K = g.K, S = K >> 5;
+    const int i = 16 * tile + w;                      // this wavefront's row (list index)
+    const bool live = i < n;
+    const float* x = g.X + (size_t)(live ? row_seq(g.rows, i) : 0) * g.ldx;
+    float inv = 1.f;
+    if (PRO == PRO_RMSNORM) {
+        float ss = 0.f;
+        if (live)
+            for (int k = 4 * lane; k < K; k += 256) {
+                const float4 v = *reinterpret_cast<const float4*>(x + k);
+                ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+            }
+        ss = wave_sum(ss);
+        inv = 1.0f / sqrtf(ss / (float)K + g.eps);
+    }
+    const int c_first = PRO == PRO_RMSNORM ? 0 : blockIdx.y * kPrepChunk;
+    const int c_end = PRO == PRO_RMSNORM ? K : min(K, c_first + kPrepChunk);
+    for (int c0 = c_first; c0 < c_end; c0 += kPrepChunk) {
+        const int kc = min(kPrepChunk, K - c0);
+        char* row = s_rows + w * kPrepPitch;
+        for (int k = 4 * lane; k < kc; k += 256) {
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (live) {
+                v = *reinterpret_cast<const float4*>(x + c0 + k);
+                if (PRO == PRO_RMSNORM) {
+                    const bf16_t* gp = (const bf16_t*)g.gain + c0 + k;
+                    v.x *= inv * bf2f(gp[0]); v.y *= inv * bf2f(gp[1]);
+                    v.z *= inv * bf2f(gp[2]); v.w *= inv * bf2f(gp[3]);
+                }
+            }
+            *reinterpret_cast<uint2*>(row + 2 * k) =
+                make_uint2((uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16),
+                           (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+        }
+        __syncthreads();
+        // fragment (k-step s, lane L): row L % 16, columns 32 s + 8 (L / 16) .. + 7
+        const int nfrag = (kc >> 5) * 64;
+        for (int f = tid; f < nfrag; f += 1024) {
+            const int sl = f >> 6, L = f & 63;
+            const uint4 v = *reinterpret_cast<const uint4*>(s_rows + (L & 15) * kPrepPitch +
+                                                           2 * (32 * sl + 8 * (L >> 4)));
+            const size_t frag = ((size_t)tile * S + (c0 >> 5) + sl) * 64 + L;
+            *reinterpret_cast<uint4*>(g.XB + frag * 8) = v;
+        }
+        __syncthreads();
+    }
+}
+
+static hipError_t launch_prep_tiles(int pro, const GemvArgs& g, hipStream_t s) {
+    const int n = g.rows.n_max, tiles = (n + 15) / 16;
+    if (pro == PRO_RMSNORM) {
+        prep_tile_kernel<PRO_RMSNORM><<<dim3(tiles, 1), 1024, 0, s>>>(g, n);
+    } else if (pro == PRO_NONE) {
+        const int chunks = (g.K + kPrepChunk - 1) / kPrepChunk;
+        prep_tile_kernel<PRO_NONE><<<dim3(tiles, chunks), 1024, 0, s>>>(g, n);
+    } else {
+        return launch_prep(pro, g, s);
+    }
+    return hipGetLastError();
+}
+
 template <int EPI, int WM, int WN, int TI, int TJ>
 static dim3 gemm_grid(int units, int n) {
     using Sh = GemmShape<WM, WN, TI, TJ>;
@@ -255,7 +335,7 @@ static hipError_t launch_gemm_epi(const GemvArgs& g, int units, int tile, hipStr
 }
 
 hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, hipStream_t s) {
-    hipError_t e = launch_prep(pro, g, s);
+    hipError_t e = launch_prep_tiles(pro, g, s);
     if (e != hipSuccess) return e;
     if (epi == EPI_QKV)
         return launch_gemm_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), tile, s);
