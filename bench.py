@@ -210,7 +210,7 @@ def main():
                     help="run a 1 GiB device copy first (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs the decode step on one GPU; "
+        print("bench.py: the library runs the decode step on one GPU; "
               f"--gpus {args.gpus} is not supported (sharding is design-only)", file=sys.stderr)
         sys.exit(2)
 

@@ -76,7 +76,7 @@ typedef enum {
     BUDDY_ECAPACITY = 3,    /* batch above max_batch */
     BUDDY_ENOMEM = 4,       /* workspace allocation failed */
     BUDDY_EDEVICE = 5,      /* HIP error (see buddy_last_error) */
-    BUDDY_EUNSUPPORTED = 6  /* valid request this build does not implement */
+    BUDDY_EUNSUPPORTED = 6  /* valid request the library does not implement  */
 } buddy_status;
 
 typedef enum { BUDDY_F32 = 0, BUDDY_BF16 = 1 } buddy_dtype;
