@@ -109,15 +109,20 @@ void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chun
     *chunks = (max_pos + 1 + *chunk_len - 1) / *chunk_len;
 }
 
+// Whether a projection of K inputs over `batch` rows takes the tiled GEMM.
+bool uses_gemm(const Model& M, const Rows& rows, int batch, int K, int tok_T) {
+    return M.cfg.dtype == BUDDY_BF16 && tok_T > 0 && rows.exact && batch >= kGemmMinRows &&
+           K % 64 == 0;
+}
+
 // A routed projection: the GEMV for batches of up to kGemvMaxRows sequences
 // (or fp32 weights), the MFMA path beyond.  The choice depends on the batch,
 // not on how many sequences a block routes, so a sequence's arithmetic does
 // not depend on the routes of the others or on the launch policy.
 hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, hipStream_t s) {
     // prompt tokens of a prefill: the tiled GEMM
-    if (M.cfg.dtype == BUDDY_BF16 && g.tok_T > 0 && g.rows.exact && batch >= kGemmMinRows &&
-        g.K % 64 == 0)
-        return launch_gemm(pro, epi, g, M.gemm_tile, s);
+    if (uses_gemm(M, g.rows, batch, g.K, g.tok_T)) return launch_gemm(pro, epi, g, M.gemm_tile, s);
+    if (pro == PRO_STAGED) return hipErrorInvalidValue;   // staged inputs only feed the GEMM
     if (M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && g.K % 128 == 0)
         return launch_mfma(pro, epi, g, s);
     return launch_gemv(M.cfg.dtype, pro, epi, g, s);
@@ -129,11 +134,13 @@ struct BlockBufs {
     float* q; float* o; float* m;
     bf16_t* xb; int xb_ld;
     int tok_T;
+    bf16_t* xb2;          // second staging buffer (prefill: the down projection's input)
 };
 
 BlockBufs decode_bufs(const Model& M) {
-    return BlockBufs{M.ws.q, M.ws.o, M.ws.m, M.ws.xb, M.ws.xb_ld, 0};
+    return BlockBufs{M.ws.q, M.ws.o, M.ws.m, M.ws.xb, M.ws.xb_ld, 0, nullptr};
 }
+
 
 // Timing hook: event around kernel `kind` of block l, if asked for.
 bool timed(const Model& M, int kind, int l) {
@@ -198,6 +205,9 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
         a.chunks = 1;
         a.chunk_len = (max_pos + 1 + r - 1) / r * r;
         a.groups = groups; a.n_groups = n_groups;
+        // the prefill kernel writes o straight into the O projection's
+        // staging when that projection takes the tiled GEMM
+        if (groups && uses_gemm(M, rows, batch, qdim, bf.tok_T)) a.xb_out = bf.xb;
     } else {
         attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
     }
@@ -212,23 +222,30 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
     g.W = w.wo; g.N = c.d_model; g.K = qdim; g.X = bf.o; g.ldx = qdim; g.gain = nullptr;
     g.Y = hidden; g.ldy = c.d_model;
     if ((e = mark(M, BUDDY_KERNEL_O_PROJ, l, false, s)) != hipSuccess ||
-        (e = launch_proj(M, batch, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
+        (e = launch_proj(M, batch, a.xb_out ? PRO_STAGED : PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_O_PROJ, l, true, s)) != hipSuccess)
         return fail_device(M, e, "o_proj");
 
-    // m = SiLU(Wg u2) * (Wu u2), u2 = RMSNorm(h)
+    // m = SiLU(Wg u2) * (Wu u2), u2 = RMSNorm(h); when both MLP projections
+    // take the tiled GEMM, m goes straight to the down projection's staging
+    // (bf16 fragments in the second buffer)
+    const bool m_staged = bf.xb2 && uses_gemm(M, rows, batch, c.d_model, bf.tok_T) &&
+                          uses_gemm(M, rows, batch, c.d_ffn, bf.tok_T);
     g.W = w.wgate_up; g.N = 2 * c.d_ffn; g.K = c.d_model; g.X = hidden; g.ldx = c.d_model;
     g.gain = w.mlp_norm; g.f = c.d_ffn; g.Y = bf.m; g.ldy = c.d_ffn;
+    g.xb_out = m_staged ? bf.xb2 : nullptr;
     if ((e = mark(M, BUDDY_KERNEL_GATE_UP, l, false, s)) != hipSuccess ||
         (e = launch_proj(M, batch, PRO_RMSNORM, EPI_SWIGLU, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_GATE_UP, l, true, s)) != hipSuccess)
         return fail_device(M, e, "gate_up");
+    g.xb_out = nullptr;
 
     // h += Wdown m
     g.W = w.wdown; g.N = c.d_model; g.K = c.d_ffn; g.X = bf.m; g.ldx = c.d_ffn;
     g.gain = nullptr; g.Y = hidden; g.ldy = c.d_model;
+    if (m_staged) g.XB = bf.xb2;
     if ((e = mark(M, BUDDY_KERNEL_DOWN, l, false, s)) != hipSuccess ||
-        (e = launch_proj(M, batch, PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
+        (e = launch_proj(M, batch, m_staged ? PRO_STAGED : PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_DOWN, l, true, s)) != hipSuccess)
         return fail_device(M, e, "down");
     return BUDDY_OK;
@@ -642,6 +659,7 @@ buddy_status ensure_prefill_ws(Model& M, size_t rows) {
         {(void**)&M.pf_m, rows * (size_t)c.d_ffn * 4},
         {(void**)&M.pf_hlast, (size_t)c.max_batch * c.d_model * 4},
         {(void**)&M.pf_xb, r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
+        {(void**)&M.pf_xb2, r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
         {(void**)&M.pf_lists, L * rows * 4}, {(void**)&M.pf_len, (size_t)c.max_batch * 4},
         {(void**)&M.pf_groups, L * rows * 8},
     };
@@ -713,7 +731,7 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
                              hipSuccess)
         return fail_device(M, e, "prefill pool");
     const size_t R = M.pf_rows;
-    const BlockBufs bf{M.pf_q, M.pf_o, M.pf_m, M.pf_xb, M.ws.xb_ld, t_stride};
+    const BlockBufs bf{M.pf_q, M.pf_o, M.pf_m, M.pf_xb, M.ws.xb_ld, t_stride, M.pf_xb2};
 
     // every prompt token (list 0) for the first and last blocks; with more
     // than one token per attention group, the group pairs of list l at

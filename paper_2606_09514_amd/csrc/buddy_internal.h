@@ -156,7 +156,7 @@ struct Model {
     // per-block token lists [L][rows], prompt lengths, last-token hidden rows
     void* pf_base; size_t pf_rows;
     float *pf_q, *pf_o, *pf_m, *pf_hlast;
-    bf16_t* pf_xb;
+    bf16_t* pf_xb, *pf_xb2;
     int32_t *pf_lists, *pf_len, *pf_groups;
     int32_t* pf_hlists;            // host copy of the token lists, then of the groups
     Workspace ws;
@@ -243,7 +243,9 @@ hipError_t launch_gather_last(const float* hidden, int t_stride, int d, const in
 hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B, int n,
                               uint8_t* mask_out, hipStream_t s);
 
-enum Pro { PRO_NONE = 0, PRO_RMSNORM = 1, PRO_POOL = 2 };
+enum Pro { PRO_NONE = 0, PRO_RMSNORM = 1, PRO_POOL = 2, PRO_STAGED = 3 };
+// PRO_STAGED (tiled GEMM only): the input rows are already in XB, written
+// there in fragment order by the producing kernel.
 enum Epi { EPI_ADD = 0, EPI_BIAS_ACT = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 
 struct GemvArgs {
@@ -264,7 +266,18 @@ struct GemvArgs {
     const float* pool_part; int pool_splits, pool_max_splits; const float* h; int d; int ctx;
     // MFMA path: compact bf16 activation rows [round16(max_batch)][ldxb]
     bf16_t* XB; int ldxb;
+    // tiled GEMM, EPI_SWIGLU: the outputs as bf16 in B-operand fragment
+    // order with K = f (the next projection's staged input) instead of Y
+    bf16_t* xb_out;
 };
+
+// Element (row i, column k) of activations in B-operand fragment order for
+// a K-column input: 16 rows x 32 columns per contiguous 1 KB fragment, lane
+// (i % 16) + 16 ((k / 8) % 4) holding columns 8 (k / 8) .. + 7.
+__host__ __device__ inline size_t xb_index(int i, int k, int K) {
+    return ((((size_t)(i >> 4) * (K >> 5) + (k >> 5)) * 64 + (i & 15) + 16 * ((k >> 3) & 3)) << 3) +
+           (k & 7);
+}
 
 // Pooled inputs of the router context: 2 n_kv hd for [mean K | mean V],
 // n_kv hd for the single-feature variants.
@@ -316,6 +329,9 @@ struct AttnArgs {
     float* part; int max_chunks;
     const uint8_t* exec;                // this block's execution map [bcap][T], or null
     int tok_T;                          // > 0: rows are prompt tokens (slot_pos)
+    // prefill attention: o of list row i as bf16 in fragment order
+    // (xb_index with K = nq hd) instead of fp32 o, or null
+    bf16_t* xb_out;
     // prompt tokens on the prefill attention kernel: groups of up to 64 / G
     // consecutive tokens of one prompt, (first row index, count) pairs; one
     // workgroup per (KV head, group) (null: one per row)

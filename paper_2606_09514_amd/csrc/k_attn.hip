@@ -667,10 +667,17 @@ void attn_prefill_kernel(AttnArgs a) {
         const int r = 16 * wave + 4 * lg + e;
         const int t = r / G, h = r - t * G;
         if (t >= count) continue;
-        float* op = a.o + ((size_t)row_seq(a.rows, first + t) * a.nq + g * G + h) * HD + li;
         const float inv = 1.f / le;
+        if (a.xb_out) {   // bf16, straight into the O projection's staging
+            const int k0 = (g * G + h) * HD + li;
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) op[16 * dt] = o[dt][e] * inv;
+            for (int dt = 0; dt < 8; ++dt)
+                a.xb_out[xb_index(first + t, k0 + 16 * dt, a.nq * HD)] = f2bf(o[dt][e] * inv);
+        } else {
+            float* op = a.o + ((size_t)row_seq(a.rows, first + t) * a.nq + g * G + h) * HD + li;
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) op[16 * dt] = o[dt][e] * inv;
+        }
     }
 }
 

@@ -203,6 +203,24 @@ void gemm_kernel(GemvArgs g, int units, int n) {
         const int col = t0 + 16 * (wn * TJ + j) + (lane & 15);
         if (col >= n) continue;
         const int b = row_seq(g.rows, col);
+        if (EPI == EPI_SWIGLU && g.xb_out) {
+            // SiLU(gate) * up of 4 consecutive units as bf16 into the next
+            // projection's staging: one 8-byte store (f % 8 == 0)
+#pragma unroll
+            for (int i = 0; i < TI / 2; ++i) {
+                const int ub = u0 + 16 * (wm * TI / 2 + i) + 4 * (lane >> 4);
+                if (ub >= units) continue;
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float v0 = acc[i][j][e], v1 = acc[TI / 2 + i][j][e];
+                    h[e] = f2bf(v0 / (1.0f + expf(-v0)) * v1);
+                }
+                *reinterpret_cast<uint2*>(g.xb_out + xb_index(col, ub, units)) =
+                    make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+            }
+            continue;
+        }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             if (kPaired) {
@@ -335,8 +353,10 @@ static hipError_t launch_gemm_epi(const GemvArgs& g, int units, int tile, hipStr
 }
 
 hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, hipStream_t s) {
-    hipError_t e = launch_prep_tiles(pro, g, s);
-    if (e != hipSuccess) return e;
+    if (pro != PRO_STAGED) {
+        hipError_t e = launch_prep_tiles(pro, g, s);
+        if (e != hipSuccess) return e;
+    }
     if (epi == EPI_QKV)
         return launch_gemm_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), tile, s);
     if (epi == EPI_SWIGLU) return launch_gemm_epi<EPI_SWIGLU>(g, g.f, tile, s);
