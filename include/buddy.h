@@ -293,16 +293,22 @@ typedef enum {
 buddy_status buddy_set_launch_policy(buddy_model* m, int32_t policy);
 
 /* Output tile of the prefill's tiled projections (bf16 weights, many prompt
- * tokens).  Every tile accumulates each output over K in the same order, so
- * the choice changes speed, never results.
+ * tokens).
  *   BUDDY_GEMM_TILE_AUTO (default): 256 x 256 where that still gives every
- *     CU two workgroups, else 128 x 128;
+ *     CU two workgroups; for the residual-add projections (O, down) whose
+ *     256 x 256 grid is smaller, 256 x 256 with K split in two halves whose
+ *     sums are added to the residual in a fixed order; else 128 x 128;
  *   BUDDY_GEMM_TILE_128, BUDDY_GEMM_TILE_256: always that tile (weight
- *     rows x token rows). */
+ *     rows x token rows), K never split;
+ *   BUDDY_GEMM_TILE_256_SPLIT: 256 x 256, K split for the residual-add
+ *     projections.
+ * The tiles without a split give the same results bit for bit; a split
+ * adds the two half sums, a different rounding order. */
 typedef enum {
     BUDDY_GEMM_TILE_AUTO = 0,
     BUDDY_GEMM_TILE_128 = 1,
-    BUDDY_GEMM_TILE_256 = 2
+    BUDDY_GEMM_TILE_256 = 2,
+    BUDDY_GEMM_TILE_256_SPLIT = 3
 } buddy_gemm_tile;
 
 /* Sets the tile choice of a handle; BUDDY_EINVAL for an unknown value. */

@@ -121,7 +121,8 @@ bool uses_gemm(const Model& M, const Rows& rows, int batch, int K, int tok_T) {
 // not depend on the routes of the others or on the launch policy.
 hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, hipStream_t s) {
     // prompt tokens of a prefill: the tiled GEMM
-    if (uses_gemm(M, g.rows, batch, g.K, g.tok_T)) return launch_gemm(pro, epi, g, M.gemm_tile, s);
+    if (uses_gemm(M, g.rows, batch, g.K, g.tok_T))
+        return launch_gemm(pro, epi, g, M.gemm_tile, M.pf_split, s);
     if (pro == PRO_STAGED) return hipErrorInvalidValue;   // staged inputs only feed the GEMM
     if (M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && g.K % 128 == 0)
         return launch_mfma(pro, epi, g, s);
@@ -660,6 +661,7 @@ buddy_status ensure_prefill_ws(Model& M, size_t rows) {
         {(void**)&M.pf_hlast, (size_t)c.max_batch * c.d_model * 4},
         {(void**)&M.pf_xb, r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
         {(void**)&M.pf_xb2, r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
+        {(void**)&M.pf_split, 2 * rows * (size_t)c.d_model * 4},
         {(void**)&M.pf_lists, L * rows * 4}, {(void**)&M.pf_len, (size_t)c.max_batch * 4},
         {(void**)&M.pf_groups, L * rows * 8},
     };
@@ -830,7 +832,7 @@ buddy_status buddy_set_launch_policy(buddy_model* h, int32_t policy) {
 }
 
 buddy_status buddy_set_gemm_tile(buddy_model* h, int32_t tile) {
-    if (!h || tile < BUDDY_GEMM_TILE_AUTO || tile > BUDDY_GEMM_TILE_256) return BUDDY_EINVAL;
+    if (!h || tile < BUDDY_GEMM_TILE_AUTO || tile > BUDDY_GEMM_TILE_256_SPLIT) return BUDDY_EINVAL;
     h->M.gemm_tile = tile;
     return BUDDY_OK;
 }

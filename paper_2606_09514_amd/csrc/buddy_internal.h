@@ -157,6 +157,7 @@ struct Model {
     void* pf_base; size_t pf_rows;
     float *pf_q, *pf_o, *pf_m, *pf_hlast;
     bf16_t* pf_xb, *pf_xb2;
+    float* pf_split;               // split-K partial sums [2][rows][d_model]
     int32_t *pf_lists, *pf_len, *pf_groups;
     int32_t* pf_hlists;            // host copy of the token lists, then of the groups
     Workspace ws;
@@ -314,7 +315,9 @@ hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s);
 hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s);
 // Tiled MFMA GEMM for many rows (prompt tokens): exact row counts, bf16
 // weights, K a multiple of 64.
-hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, hipStream_t s);
+// part: fp32 workspace of 2 x rows x N for the split-K residual-add
+// projections (null: no split).
+hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, float* part, hipStream_t s);
 constexpr int kGemmMinRows = 64;
 // Routed rows above which a bf16 projection takes the MFMA path.
 constexpr int kGemvMaxRows = 4;

@@ -93,14 +93,16 @@ struct GemmShape {
 
 template <int EPI, int WM, int WN, int TI, int TJ>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void gemm_kernel(GemvArgs g, int units, int n) {
+void gemm_kernel(GemvArgs g, int units, int n, float* part) {
     using Sh = GemmShape<WM, WN, TI, TJ>;
     constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
     __shared__ __attribute__((aligned(16))) char s_buf[kBufs * Sh::kBufBytes];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WN, wn = wave % WN;
-    const int K = g.K, S = K >> 5, nk = K / kTileK;
+    // split K (part != null): workgroup z takes K steps [z nk, (z + 1) nk)
+    // and writes its fp32 sums to part[z][row][unit] for a separate add
+    const int K = g.K, S = K >> 5, nk = K / kTileK / gridDim.z, k0 = blockIdx.z * nk;
     const int u0 = blockIdx.x * (kPaired ? Sh::kRows / 2 : Sh::kRows);   // first unit or row
     const int t0 = blockIdx.y * Sh::kCols;                               // first row (token)
     const int last_tile = (n - 1) >> 4;                                   // last 16-row column tile
@@ -134,7 +136,7 @@ void gemm_kernel(GemvArgs g, int units, int n) {
     // one load per fragment; steps past the end reload the last one into a
     // buffer that is not read again
     auto issue = [&](int kb) {
-        const int kc = min(kb, nk - 1);
+        const int kc = k0 + min(kb, nk - 1);
         char* base = s_buf + (kb % kBufs) * Sh::kBufBytes;
 #pragma unroll
         for (int t = 0; t < Sh::kALoads; ++t)
@@ -196,6 +198,23 @@ void gemm_kernel(GemvArgs g, int units, int n) {
                     acc[i][j], 0, 0, 0);
     }
     __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));   // the reloads past the end
+
+    if (part) {   // split K (single-row kinds): 4 consecutive units per lane, one 16-byte store
+        float* pz = part + (size_t)blockIdx.z * n * units;
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
+            const int col = t0 + 16 * (wn * TJ + j) + (lane & 15);
+            if (col >= n) continue;
+#pragma unroll
+            for (int i = 0; i < TI; ++i) {
+                const int r = u0 + 16 * (wm * TI + i) + 4 * (lane >> 4);
+                if (r < units)
+                    *reinterpret_cast<float4*>(pz + (size_t)col * units + r) =
+                        make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
+        }
+        return;
+    }
 
     // epilogue from the accumulators: rows 4 (lane / 16) + e of each tile
 #pragma unroll
@@ -332,9 +351,29 @@ static dim3 gemm_grid(int units, int n) {
 }
 
 template <int EPI, int WM, int WN, int TI, int TJ>
-static void gemm_launch(const GemvArgs& g, int units, int n, hipStream_t s) {
-    launch_main(gemm_kernel<EPI, WM, WN, TI, TJ>, gemm_grid<EPI, WM, WN, TI, TJ>(units, n),
-                dim3(GemmShape<WM, WN, TI, TJ>::kThreads), 0, s, g, units, n);
+static void gemm_launch(const GemvArgs& g, int units, int n, hipStream_t s, float* part = nullptr,
+                        int splits = 1) {
+    dim3 grid = gemm_grid<EPI, WM, WN, TI, TJ>(units, n);
+    grid.z = splits;
+    launch_main(gemm_kernel<EPI, WM, WN, TI, TJ>, grid, dim3(GemmShape<WM, WN, TI, TJ>::kThreads),
+                0, s, g, units, n, part);
+}
+
+// Residual add of the split-K partial sums: Y[row] += part[0] + part[1]
+// (fixed order), four units per thread.
+__global__ __launch_bounds__(256) void splitk_add_kernel(GemvArgs g, int units, int n,
+                                                         const float* part) {
+    const int q = units >> 2;
+    for (size_t t = (size_t)blockIdx.x * 256 + threadIdx.x; t < (size_t)n * q;
+         t += (size_t)gridDim.x * 256) {
+        const int col = (int)(t / q), r = 4 * (int)(t - (size_t)col * q);
+        const float4 a = *reinterpret_cast<const float4*>(part + (size_t)col * units + r);
+        const float4 b = *reinterpret_cast<const float4*>(part + ((size_t)n + col) * units + r);
+        float* y = g.Y + (size_t)row_seq(g.rows, col) * g.ldy + r;
+        float4 v = *reinterpret_cast<float4*>(y);
+        v.x += a.x + b.x; v.y += a.y + b.y; v.z += a.z + b.z; v.w += a.w + b.w;
+        *reinterpret_cast<float4*>(y) = v;
+    }
 }
 
 // Tile choice (automatic): 256 x 256 where it still gives the CUs two
@@ -342,26 +381,42 @@ static void gemm_launch(const GemvArgs& g, int units, int n, hipStream_t s) {
 // one wavefront per SIMD was slower than 128 x 128 on the 4096-row
 // projections (measured).
 template <int EPI>
-static hipError_t launch_gemm_epi(const GemvArgs& g, int units, int tile, hipStream_t s) {
+static hipError_t launch_gemm_epi(const GemvArgs& g, int units, int tile, float* part,
+                                  hipStream_t s) {
     const int n = g.rows.n_max;
     const dim3 big = gemm_grid<EPI, 2, 4, 8, 4>(units, n);
-    if (tile == BUDDY_GEMM_TILE_256 || (tile == BUDDY_GEMM_TILE_AUTO && big.x * big.y >= 512))
+    // split K in two for residual-add projections whose 256 x 256 grid would
+    // leave CUs idle but fills them when doubled (O and down at prefill sizes)
+    const bool split_ok = EPI == EPI_ADD && part && (g.K / kTileK) % 2 == 0 && units % 4 == 0;
+    const bool split = split_ok && (tile == BUDDY_GEMM_TILE_256_SPLIT ||
+                                    (tile == BUDDY_GEMM_TILE_AUTO && big.x * big.y < 512 &&
+                                     2 * big.x * big.y >= 256));
+    if (split) {
+        gemm_launch<EPI, 2, 4, 8, 4>(g, units, n, s, part, 2);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const size_t work = (size_t)n * (units / 4);
+        const int grid = (int)((work + 255) / 256 < 4096 ? (work + 255) / 256 : 4096);
+        splitk_add_kernel<<<grid, 256, 0, s>>>(g, units, n, part);
+    } else if (tile == BUDDY_GEMM_TILE_256 || tile == BUDDY_GEMM_TILE_256_SPLIT ||
+               (tile == BUDDY_GEMM_TILE_AUTO && big.x * big.y >= 512)) {
         gemm_launch<EPI, 2, 4, 8, 4>(g, units, n, s);
-    else
+    } else {
         gemm_launch<EPI, 2, 2, 4, 4>(g, units, n, s);
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, hipStream_t s) {
+hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, float* part, hipStream_t s) {
     if (pro != PRO_STAGED) {
         hipError_t e = launch_prep_tiles(pro, g, s);
         if (e != hipSuccess) return e;
     }
     if (epi == EPI_QKV)
-        return launch_gemm_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), tile, s);
-    if (epi == EPI_SWIGLU) return launch_gemm_epi<EPI_SWIGLU>(g, g.f, tile, s);
-    if (epi == EPI_BIAS_ACT) return launch_gemm_epi<EPI_BIAS_ACT>(g, g.N, tile, s);
-    return launch_gemm_epi<EPI_ADD>(g, g.N, tile, s);
+        return launch_gemm_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), tile, nullptr, s);
+    if (epi == EPI_SWIGLU) return launch_gemm_epi<EPI_SWIGLU>(g, g.f, tile, nullptr, s);
+    if (epi == EPI_BIAS_ACT) return launch_gemm_epi<EPI_BIAS_ACT>(g, g.N, tile, nullptr, s);
+    return launch_gemm_epi<EPI_ADD>(g, g.N, tile, part, s);
 }
 
 }  // namespace buddy

@@ -411,12 +411,17 @@ def gpu_prefill(P, lens, ks, t_stride, seed):
 @pytest.mark.parametrize("G", [4, 8])
 def test_prefill_gemm_tiles(G):
     """The 256 x 256 tile of the prefill projections (forced on a small
-    model) against the oracle, and bit for bit equal to the 128 x 128 tile
-    (every output accumulates over K in the same order): 211 prompt rows
+    model), with and without K split in two for the residual-add
+    projections, against the oracle; without the split bit for bit equal
+    to the 128 x 128 tile (every output accumulates over K in the same
+    order): 211 prompt rows
     fill one partial column tile; paired (QKV, SwiGLU) and single-row
     (O, down) epilogues."""
     P = Pair(gqa_shape(G), "bf16", 160, 2, seed=117 + G, omega=0.1)
     P.gpu.set_gemm_tile(blib.GEMM_TILE_256)
+    check_prefill(P, [150, 61], [1, 2], 150, seed=118)
+    # K split in two for O and down, half sums added to the residual
+    P.gpu.set_gemm_tile(blib.GEMM_TILE_256_SPLIT)
     check_prefill(P, [150, 61], [1, 2], 150, seed=118)
     outs = []
     for tile in (blib.GEMM_TILE_128, blib.GEMM_TILE_256):
