@@ -255,6 +255,18 @@ def test_abi_validation_writes_nothing():
     m = torch.zeros((2, 4), dtype=torch.uint8, device="cuda")
     assert blib.select_topk(s, [5, 0], m, check=False) == blib.EINVAL
     assert blib.select_topk(s, [4, 0], m, check=False) == blib.OK
+    # running-sum pool arrays must come together
+    ps, pr = P.gpu.pool_state()
+    rc = P.gpu.decode_step(dk, dv, hidden, [0, 0], [1, 1], pool=(ps, None), check=False)
+    assert rc == blib.EINVAL
+    # handle settings
+    lib = blib.lib()
+    for bad_tile in (-1, 4):
+        assert lib.buddy_set_gemm_tile(P.gpu._h, bad_tile) == blib.EINVAL
+    for bad_policy in (-1, 3):
+        assert lib.buddy_set_launch_policy(P.gpu._h, bad_policy) == blib.EINVAL
+    torch.cuda.synchronize()
+    assert torch.all(hidden == 1) and torch.all(mask == 9)
 
 
 def test_model_create_rejects_bad_shapes():
@@ -936,3 +948,23 @@ def test_start_layer_prefill(masked):
     P = Pair(shape, "bf16", 96, 3, seed=98, omega=0.1)
     assert P.L_mid == 2
     check_prefill(P, [90, 33, 7], [1, 2, 0], 90, masked=masked, seed=99)
+
+
+def test_running_pool_at_start_layer():
+    """Running sums at start layer 2 pool block 1's cache: scores over a
+    call schedule against the oracle's fresh means of block 1's rows."""
+    B, T = 3, 64
+    P = Pair(start_shape(2), "bf16", T, B, seed=120, omega=0.1)
+    g = torch.Generator().manual_seed(121)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    h = synth.hidden_inputs(B, P.cfg["d_model"], seed=122)
+    pool = P.gpu.pool_state()
+    for pos in ([3, 10, 40], [4, 11, 41], [9, 30, 63]):
+        scores = torch.zeros((B, P.L_mid), device="cuda")
+        P.gpu.pool_route(P.upload(hk), P.upload(hv), pos, h.cuda(), scores, pool=pool)
+        got = scores.cpu().numpy()
+        for b in range(B):
+            ref = P.orc.dm_scores(P.orc.context(hk[1, b], hv[1, b], pos[b], h[b].numpy()))
+            assert np.max(np.abs(got[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref))))
+        assert pool[1].cpu().numpy().tolist() == [[p] * P.cfg["n_kv_heads"] for p in pos]
