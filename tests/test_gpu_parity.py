@@ -968,3 +968,39 @@ def test_running_pool_at_start_layer():
             ref = P.orc.dm_scores(P.orc.context(hk[1, b], hv[1, b], pos[b], h[b].numpy()))
             assert np.max(np.abs(got[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref))))
         assert pool[1].cpu().numpy().tolist() == [[p] * P.cfg["n_kv_heads"] for p in pos]
+
+
+# ------------------------------------------------------------ size limits
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+def test_max_batch_256(policy):
+    """The largest batch a handle takes (256 sequences): MFMA projections
+    over two 128-row column groups, the compaction of 256 sequences per
+    block, mixed positions and budgets, one teacher-forced step."""
+    B, T = 256, 24
+    P = Pair("tiny", "bf16", T, B, seed=130, omega=0.1, policy=policy)
+    g = torch.Generator().manual_seed(131)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    rng = np.random.default_rng(132)
+    pos = rng.integers(0, T, size=B).tolist()
+    ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=133).numpy()
+    rep = one_step_all(P, hk, hv, pos, ks, x)
+    print(rep)
+
+
+@pytest.mark.parametrize("G", [1, 4])
+def test_long_context_many_chunks(G):
+    """Positions near 20 000 at B = 2: the split attention runs on ~80-160
+    position chunks per (sequence, KV head) and the merge folds them all
+    (MFMA score kernel for G = 4, vector kernel for G = 1)."""
+    B, T = 2, 20000
+    P = Pair(gqa_shape(G), "bf16", T, B, seed=134 + G, omega=0.1)
+    g = torch.Generator().manual_seed(136)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    pos, ks = [T - 1, 12345], [1, 2]
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=137).numpy()
+    rep = one_step_all(P, hk, hv, pos, ks, x)
+    print(G, rep)
