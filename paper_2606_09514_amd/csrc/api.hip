@@ -115,6 +115,12 @@ bool uses_gemm(const Model& M, const Rows& rows, int batch, int K, int tok_T) {
            K % 64 == 0;
 }
 
+// Whether a projection of K inputs over `batch` rows takes the MFMA path.
+bool uses_mfma(const Model& M, const Rows& rows, int batch, int K, int tok_T) {
+    return M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && K % 128 == 0 &&
+           !uses_gemm(M, rows, batch, K, tok_T);
+}
+
 // A routed projection: the GEMV for batches of up to kGemvMaxRows sequences
 // (or fp32 weights), the MFMA path beyond.  The choice depends on the batch,
 // not on how many sequences a block routes, so a sequence's arithmetic does
@@ -123,9 +129,9 @@ hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, 
     // prompt tokens of a prefill: the tiled GEMM
     if (uses_gemm(M, g.rows, batch, g.K, g.tok_T))
         return launch_gemm(pro, epi, g, M.gemm_tile, M.pf_split, s);
-    if (pro == PRO_STAGED) return hipErrorInvalidValue;   // staged inputs only feed the GEMM
-    if (M.cfg.dtype == BUDDY_BF16 && batch > kGemvMaxRows && g.K % 128 == 0)
-        return launch_mfma(pro, epi, g, s);
+    if (uses_mfma(M, g.rows, batch, g.K, g.tok_T))
+        return launch_mfma(pro, epi, g, g.rows.n_max <= M.ws.mfma_part_rows ? M.ws.mfma_part : nullptr, s);
+    if (pro == PRO_STAGED) return hipErrorInvalidValue;   // staged inputs feed the MFMA paths only
     return launch_gemv(M.cfg.dtype, pro, epi, g, s);
 }
 
@@ -135,11 +141,11 @@ struct BlockBufs {
     float* q; float* o; float* m;
     bf16_t* xb; int xb_ld;
     int tok_T;
-    bf16_t* xb2;          // second staging buffer (prefill: the down projection's input)
+    bf16_t* xb2;          // second staging buffer: the down projection's input
 };
 
 BlockBufs decode_bufs(const Model& M) {
-    return BlockBufs{M.ws.q, M.ws.o, M.ws.m, M.ws.xb, M.ws.xb_ld, 0, nullptr};
+    return BlockBufs{M.ws.q, M.ws.o, M.ws.m, M.ws.xb, M.ws.xb_ld, 0, M.ws.xb2};
 }
 
 
@@ -211,6 +217,9 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
         if (groups && uses_gemm(M, rows, batch, qdim, bf.tok_T)) a.xb_out = bf.xb;
     } else {
         attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
+        // decode rows on the MFMA path: o goes straight to the O
+        // projection's staging, rounded to bf16 as its staging would
+        if (uses_mfma(M, rows, batch, qdim, 0)) a.xb_out = bf.xb;
     }
     a.part = M.ws.part; a.max_chunks = M.ws.max_chunks;
     a.exec = exec ? exec + (size_t)l * c.max_batch * c.max_ctx : nullptr;
@@ -228,10 +237,12 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
         return fail_device(M, e, "o_proj");
 
     // m = SiLU(Wg u2) * (Wu u2), u2 = RMSNorm(h); when both MLP projections
-    // take the tiled GEMM, m goes straight to the down projection's staging
-    // (bf16 fragments in the second buffer)
-    const bool m_staged = bf.xb2 && uses_gemm(M, rows, batch, c.d_model, bf.tok_T) &&
-                          uses_gemm(M, rows, batch, c.d_ffn, bf.tok_T);
+    // take the tiled GEMM, or both the MFMA path, m goes straight to the down
+    // projection's staging (bf16 fragments in the second buffer)
+    const bool m_staged = bf.xb2 && ((uses_gemm(M, rows, batch, c.d_model, bf.tok_T) &&
+                                      uses_gemm(M, rows, batch, c.d_ffn, bf.tok_T)) ||
+                                     (bf.tok_T == 0 && uses_mfma(M, rows, batch, c.d_model, 0) &&
+                                      uses_mfma(M, rows, batch, c.d_ffn, 0)));
     g.W = w.wgate_up; g.N = 2 * c.d_ffn; g.K = c.d_model; g.X = hidden; g.ldx = c.d_model;
     g.gain = w.mlp_norm; g.f = c.d_ffn; g.Y = bf.m; g.ldy = c.d_ffn;
     g.xb_out = m_staged ? bf.xb2 : nullptr;
@@ -390,6 +401,18 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
     if (din > xb_ld) xb_ld = din;
     M.ws.xb_ld = (int)xb_ld;
 
+    // K-split partials of the MFMA path (the FFN down projection), for the
+    // batch or a short prompt's tokens
+    size_t part_elems = 0;
+    const int part_rows = Bc > kGemmMinRows ? (int)Bc : kGemmMinRows;
+    if (c.dtype == BUDDY_BF16 && Bc > (size_t)kGemvMaxRows) {
+        size_t splits = mfma_splits(EPI_ADD, c.d_model, c.d_ffn);
+        const size_t so = mfma_splits(EPI_ADD, c.d_model, (int)qdim);
+        if (so > splits) splits = so;
+        if (splits > 1) part_elems = splits * c.d_model * part_rows;
+    }
+    M.ws.mfma_part_rows = part_elems ? part_rows : 0;
+
     struct Piece { void** dst; size_t bytes; };
     Workspace& W = M.ws;
     Piece pieces[] = {
@@ -403,6 +426,8 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
         {(void**)&W.pool_part, Bc * c.n_kv_heads * max_splits * 2 * hd * 4},
         {(void**)&W.rope, (size_t)c.max_ctx * (hd / 2) * sizeof(float2)},
         {(void**)&W.xb, ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
+        {(void**)&W.xb2, ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
+        {(void**)&W.mfma_part, part_elems * 4},
     };
     size_t total = 0;
     for (const Piece& p : pieces) total += align_up(p.bytes);

@@ -103,6 +103,9 @@ struct Workspace {
     float* pool_part;    // pool partials [max_batch][n_kv][max_pool_splits][2 hd]
     float2* rope;        // [max_ctx][hd/2] (cos, sin) of pos * theta^(-2i/hd)
     bf16_t* xb;          // [round16(max_batch)][xb_ld] compact bf16 rows (MFMA path)
+    bf16_t* xb2;         // the same, for the down projection's input
+    float* mfma_part;    // K-split partial sums of the MFMA path (see mfma_splits)
+    int mfma_part_rows;  // routed rows the partial buffer holds (0: no buffer)
     int xb_ld;
     int max_chunks;
     int max_pool_splits;
@@ -245,8 +248,8 @@ hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B,
                               uint8_t* mask_out, hipStream_t s);
 
 enum Pro { PRO_NONE = 0, PRO_RMSNORM = 1, PRO_POOL = 2, PRO_STAGED = 3 };
-// PRO_STAGED (tiled GEMM only): the input rows are already in XB, written
-// there in fragment order by the producing kernel.
+// PRO_STAGED (tiled GEMM and MFMA paths): the input rows are already in XB,
+// written there in fragment order by the producing kernel.
 enum Epi { EPI_ADD = 0, EPI_BIAS_ACT = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 
 struct GemvArgs {
@@ -267,8 +270,9 @@ struct GemvArgs {
     const float* pool_part; int pool_splits, pool_max_splits; const float* h; int d; int ctx;
     // MFMA path: compact bf16 activation rows [round16(max_batch)][ldxb]
     bf16_t* XB; int ldxb;
-    // tiled GEMM, EPI_SWIGLU: the outputs as bf16 in B-operand fragment
-    // order with K = f (the next projection's staged input) instead of Y
+    // EPI_SWIGLU (tiled GEMM and MFMA paths): the outputs as bf16 in
+    // B-operand fragment order with K = f (the next projection's staged
+    // input) instead of Y
     bf16_t* xb_out;
 };
 
@@ -308,8 +312,9 @@ __device__ __forceinline__ float4 pooled_feature4(const GemvArgs& g, int b, int 
 }
 hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream_t s);
 // MFMA path (bf16 weights, K a multiple of 128): prep of the compact bf16
-// rows, then the MFMA projection with the same epilogues.
-hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s);
+// rows, then the MFMA projection with the same epilogues.  part: fp32
+// workspace of mfma_part_elems for the K-split projections.
+hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, float* part, hipStream_t s);
 // The activation staging of the MFMA paths: routed rows as bf16 in B-operand
 // fragment order (g.XB), RMSNorm / router context folded in per pro.
 hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s);
@@ -321,6 +326,34 @@ hipError_t launch_gemm(int pro, int epi, const GemvArgs& g, int tile, float* par
 constexpr int kGemmMinRows = 64;
 // Routed rows above which a bf16 projection takes the MFMA path.
 constexpr int kGemvMaxRows = 4;
+// MFMA path: workgroups below which a launch takes smaller weight tiles per
+// workgroup or splits K; the most K splits.
+constexpr int kMfmaMinGrid = 384;
+constexpr int kMfmaMaxSplits = 8;
+
+// K splits of an MFMA projection of `units` output rows over K inputs
+// (residual-add kinds).  A workgroup reads every routed activation row of
+// its K range for its weight rows, so the activation bytes a CU fetches per
+// weight byte are n / (rows per workgroup): long-K projections (K >= 2
+// units, the FFN down projection) whose 64-row tiles give fewer than
+// kMfmaMinGrid workgroups split K over up to kMfmaMaxSplits workgroups
+// instead of shrinking the tile; a second kernel adds the split sums in a
+// fixed order.  Their partial sums (splits x n x units) stay small next to
+// the weights because K is long.  Fixed by the shape alone: a sequence's
+// sums never depend on the batch or its routes.
+inline int mfma_splits(int epi, int units, int K) {
+    if (epi != EPI_ADD || K % 32 != 0 || K < 2 * units) return 1;
+    const int grid = (units + 63) / 64;
+    if (grid >= kMfmaMinGrid) return 1;
+    const int S = K / 32;
+    int splits = 1;
+    for (int c = 2; c <= kMfmaMaxSplits; c *= 2) {
+        if (S % (4 * c) != 0) break;
+        splits = c;
+        if (grid * c >= 256) break;
+    }
+    return splits;
+}
 
 struct AttnArgs {
     const float* q; float* o;
@@ -332,8 +365,8 @@ struct AttnArgs {
     float* part; int max_chunks;
     const uint8_t* exec;                // this block's execution map [bcap][T], or null
     int tok_T;                          // > 0: rows are prompt tokens (slot_pos)
-    // prefill attention: o of list row i as bf16 in fragment order
-    // (xb_index with K = nq hd) instead of fp32 o, or null
+    // o of launch row i as bf16 in fragment order (xb_index with K = nq hd),
+    // the O projection's staged input, instead of fp32 o; or null
     bf16_t* xb_out;
     // prompt tokens on the prefill attention kernel: groups of up to 64 / G
     // consecutive tokens of one prompt, (first row index, count) pairs; one

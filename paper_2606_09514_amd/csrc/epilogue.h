@@ -23,6 +23,9 @@ __device__ __forceinline__ float act_fn(float x, int act) {
     return x / (1.0f + expf(-x));
 }
 
+// SwiGLU of a gate sum v0 and an up sum v1: SiLU(v0) v1.
+__device__ __forceinline__ float swiglu(float v0, float v1) { return v0 / (1.0f + expf(-v0)) * v1; }
+
 // Epilogue of one finished row for the single-row kinds.
 template <typename TW, int EPI>
 __device__ __forceinline__ void epilogue1(const GemvArgs& g, int b, int row, float v) {
@@ -44,7 +47,7 @@ __device__ __forceinline__ void epilogue(const GemvArgs& g, int b, int u, int r0
         y[r0] = act_fn(v0 + St<TW>::get(bias, r0), g.act);
         y[r1] = act_fn(v1 + St<TW>::get(bias, r1), g.act);
     } else if (EPI == EPI_SWIGLU) {
-        g.Y[(size_t)b * g.ldy + u] = v0 / (1.0f + expf(-v0)) * v1;
+        g.Y[(size_t)b * g.ldy + u] = swiglu(v0, v1);
     } else {  // EPI_QKV
         const int half = g.hd >> 1;
         const int hg = u / half, i = u - hg * half;

@@ -9,7 +9,8 @@
 // A second kernel merges the chunk partials of (b, g) in chunk order and
 // writes o[b] for the group's heads (no cross-workgroup synchronisation
 // inside a kernel: device-wide fences are costly across the XCDs); with a
-// single chunk the first kernel writes o itself.  Zero-filled rows of skipped
+// single chunk the first kernel writes o itself (fp32, or as bf16 straight
+// into the O projection's staged input).  Zero-filled rows of skipped
 // steps are ordinary cache rows here (logit 0, value 0), unless the block's
 // execution map is given: then rows at which the block did not run are left
 // out of the softmax (the new row at pos always counts: the block runs for
@@ -220,7 +221,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             A += s_acc[w][h][e] * sw;
         }
         if (a.chunks == 1) {
-            a.o[((size_t)b * a.nq + g * G + h) * a.hd + e] = A / L;
+            const int col = (g * G + h) * a.hd + e;
+            if (a.xb_out) a.xb_out[xb_index(i, col, a.nq * a.hd)] = f2bf(A / L);
+            else a.o[(size_t)b * a.nq * a.hd + col] = A / L;
         } else {
             float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
             pp[e] = A;
@@ -405,7 +408,9 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
             A += s_acc[w][h][e] * sw;
         }
         if (a.chunks == 1) {
-            a.o[((size_t)b * a.nq + g * G + h) * HD + e] = A / L;
+            const int col = (g * G + h) * HD + e;
+            if (a.xb_out) a.xb_out[xb_index(i, col, a.nq * HD)] = f2bf(A / L);
+            else a.o[(size_t)b * a.nq * HD + col] = A / L;
         } else {
             float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
             pp[e] = A;
@@ -714,7 +719,9 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
         float A = 0.f;
 #pragma unroll 8
         for (int q = 0; q < a.chunks; ++q) A += pp[q * pstride + e] * s_w[q];
-        a.o[(size_t)b * a.nq * a.hd + (size_t)head * a.hd + e] = A / L;
+        const int col = head * a.hd + e;
+        if (a.xb_out) a.xb_out[xb_index(i, col, a.nq * a.hd)] = f2bf(A / L);
+        else a.o[(size_t)b * a.nq * a.hd + col] = A / L;
     }
 }
 

@@ -233,7 +233,7 @@ void gemm_kernel(GemvArgs g, int units, int n, float* part) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float v0 = acc[i][j][e], v1 = acc[TI / 2 + i][j][e];
-                    h[e] = f2bf(v0 / (1.0f + expf(-v0)) * v1);
+                    h[e] = f2bf(swiglu(v0, v1));
                 }
                 *reinterpret_cast<uint2*>(g.xb_out + xb_index(col, ub, units)) =
                     make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));

@@ -5,13 +5,19 @@
 //  prep_kernel  writes the routed rows as bf16 in MFMA operand order (row i
 //               of the launch is sequence idx[i]): RMSNorm and gain folded in
 //               (PRO_RMSNORM), the router context built from the pool's split
-//               sums (PRO_POOL), or a plain conversion (PRO_NONE).
+//               sums (PRO_POOL), or a plain conversion (PRO_NONE).  Inputs
+//               staged by their producer (PRO_STAGED: the attention output,
+//               the SwiGLU output) skip it.
 //  mfma_kernel  Y = W XB^T with v_mfma_f32_16x16x32_bf16 (fp32 accumulate).
 //               A workgroup owns RT 16-row weight tiles (16 RT rows, or 8 RT
 //               two-row units) and all routed rows; its four wavefronts take
-//               a quarter of K each, their sums are reduced through LDS one
-//               epilogue group at a time, and the fused epilogues of the GEMV
-//               path run on the finished sums.
+//               a quarter of K each (of the workgroup's K range when K is
+//               split over gridDim.y workgroups), their sums are reduced
+//               through LDS one epilogue group at a time, and the fused
+//               epilogues of the GEMV path run on the finished sums, or the
+//               sums go to a partial buffer when K is split.
+//  split_add_kernel  adds the K-split partial sums in split order to the
+//               residual rows.
 //
 // Operand layouts of v_mfma_f32_16x16x32_bf16 (checked on the device):
 //   A[i][k] (16 x 32): lane i + 16 (k / 8), element k % 8
@@ -96,8 +102,15 @@ __host__ __device__ constexpr int mfma_round(int rt, int nt) {
     return 16 / (rt + nt) < 1 ? 1 : 16 / (rt + nt) > 8 ? 8 : 16 / (rt + nt);
 }
 
+// Partial sums of K split `ks`, weight tile t of a unit (0, or 1 for the
+// second row of the two-row kinds), unit u, routed row j: index
+// ((ks GT + t) units + u) n_cap + j, n_cap = the launch's row capacity.
+__device__ __forceinline__ size_t part_index(int ks, int GT, int t, int units, int u, int n_cap, int j) {
+    return ((size_t)(ks * GT + t) * units + u) * n_cap + j;
+}
+
 template <int EPI, int NT, int RT>
-__global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_host) {
+__global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_host, float* part) {
     constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
     constexpr int GT = kPaired ? 2 : 1;       // weight tiles per epilogue group
     constexpr int NG = RT / GT;               // epilogue groups (16 units or rows each)
@@ -109,7 +122,8 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int K = g.K;
     const int S = K >> 5;                     // k-steps of a row
-    const int sw = S >> 2;                    // k-steps of a wavefront (K % 128 == 0)
+    const int sw = S / (4 * gridDim.y);       // k-steps of a wavefront (exact)
+    const int kw = (blockIdx.y * 4 + wave) * sw;   // its first k-step
     const int u0 = blockIdx.x * 16 * NG;      // first unit (two-row kinds) or row
 
     // A rows of this lane (lane % 16 within each tile); past the end the
@@ -120,8 +134,8 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
         const int u = min(u0 + 16 * q + (lane & 15), units - 1);
         int r0 = u, r1 = u;
         if (kPaired) unit_rows<EPI>(g, u, r0, r1);
-        Ap[q] = (const bf16_t*)g.W + (size_t)r0 * K + wave * (K >> 2) + 8 * (lane >> 4);
-        if (kPaired) Ap[NG + q] = (const bf16_t*)g.W + (size_t)r1 * K + wave * (K >> 2) + 8 * (lane >> 4);
+        Ap[q] = (const bf16_t*)g.W + (size_t)r0 * K + kw * 32 + 8 * (lane >> 4);
+        if (kPaired) Ap[NG + q] = (const bf16_t*)g.W + (size_t)r1 * K + kw * 32 + 8 * (lane >> 4);
     }
 
     for (int j0 = 0; j0 < n; j0 += NT * 16) {   // column groups of NT tiles
@@ -131,7 +145,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
         const bf16_t* Bp[NT];
 #pragma unroll
         for (int c = 0; c < NT; ++c)
-            Bp[c] = g.XB + (((size_t)((j0 >> 4) + min(c, nct - 1)) * S + wave * sw) * 64 + lane) * 8;
+            Bp[c] = g.XB + (((size_t)((j0 >> 4) + min(c, nct - 1)) * S + kw) * 64 + lane) * 8;
 
         f32x4_t acc[RT][NT];
 #pragma unroll
@@ -188,6 +202,19 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
                     for (int v = 0; v < 4; ++v)
                         s_red[wave][t][4 * (lane >> 4) + v][c * 16 + (lane & 15)] = acc[q + t * NG][c][v];
             __syncthreads();
+            if (part) {   // K split: the workgroup's sums, row j fastest
+                for (int p = tid; p < 16 * ncols; p += 256) {
+                    const int il = p / ncols, j = p - il * ncols;
+                    const int uu = u0 + 16 * q + il;
+                    if (uu >= units) continue;
+#pragma unroll
+                    for (int t = 0; t < GT; ++t)
+                        part[part_index(blockIdx.y, GT, t, units, uu, g.rows.n_max, j0 + j)] =
+                            (s_red[0][t][il][j] + s_red[1][t][il][j]) +
+                            (s_red[2][t][il][j] + s_red[3][t][il][j]);
+                }
+                continue;
+            }
             for (int p = tid; p < 16 * ncols; p += 256) {
                 const int il = p / ncols, j = p - il * ncols;
                 const int uu = u0 + 16 * q + il;
@@ -198,6 +225,10 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
                 if (kPaired) {
                     const float v1 = (s_red[0][GT - 1][il][j] + s_red[1][GT - 1][il][j]) +
                                      (s_red[2][GT - 1][il][j] + s_red[3][GT - 1][il][j]);
+                    if (EPI == EPI_SWIGLU && g.xb_out) {   // the down projection's staged input
+                        g.xb_out[xb_index(j0 + j, uu, g.f)] = f2bf(swiglu(v0, v1));
+                        continue;
+                    }
                     int r0, r1;
                     unit_rows<EPI>(g, uu, r0, r1);
                     epilogue<bf16_t, EPI>(g, b, uu, r0, r1, v0, v1);
@@ -209,40 +240,87 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
     }
 }
 
-// Workgroups below which a launch takes smaller weight tiles per workgroup
-constexpr int kMfmaMinGrid = 384;
+// Sum of the K-split partials in split order, then the residual add.  A
+// workgroup takes 64 rows x 16 routed rows: every partial of a thread is
+// loaded before the first add, the routed row runs fastest in the reads,
+// and a transpose through LDS lets the writes run along the output rows.
+template <int SPLITS>
+__global__ __launch_bounds__(256) void split_add_kernel(GemvArgs g, int units, int n_host,
+                                                        const float* part) {
+    __shared__ float s_v[16][65];
+    const int n = n_host >= 0 ? n_host : *g.rows.cnt;
+    const int u0 = blockIdx.x * 64, j0 = blockIdx.y * 16;
+    if (j0 >= n) return;
+    const int tid = threadIdx.x, n_cap = g.rows.n_max;
+    const int jl = tid & 15, j = min(j0 + jl, n - 1);
+    float v[4][SPLITS];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = min(u0 + (tid >> 4) + 16 * r, units - 1);
+#pragma unroll
+        for (int ks = 0; ks < SPLITS; ++ks) v[r][ks] = part[part_index(ks, 1, 0, units, u, n_cap, j)];
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float acc = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < SPLITS; ++ks) acc += v[r][ks];
+        s_v[jl][(tid >> 4) + 16 * r] = acc;
+    }
+    __syncthreads();
+    const int ul = tid & 63, u = u0 + ul;
+    if (u >= units) return;
+    for (int jj = tid >> 6; jj < 16 && j0 + jj < n; jj += 4)
+        epilogue1<bf16_t, EPI_ADD>(g, row_seq(g.rows, j0 + jj), u, s_v[jj][ul]);
+}
 
 template <int EPI, int RT>
-static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, hipStream_t s) {
+static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int splits, float* part,
+                                 hipStream_t s) {
     constexpr int per = 16 * (EPI == EPI_SWIGLU || EPI == EPI_QKV ? RT / 2 : RT);
-    const int grid = (units + per - 1) / per;
+    const dim3 grid((units + per - 1) / per, splits);
     const int tiles = (g.rows.n_max + 15) / 16;
-    if (tiles <= 1) launch_main(mfma_kernel<EPI, 1, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
-    else if (tiles <= 2) launch_main(mfma_kernel<EPI, 2, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
-    else if (tiles <= 3) launch_main(mfma_kernel<EPI, 3, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
-    else if (tiles <= 4) launch_main(mfma_kernel<EPI, 4, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
-    else if (tiles <= 5) launch_main(mfma_kernel<EPI, 5, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
-    else if (tiles <= 6) launch_main(mfma_kernel<EPI, 6, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
+    if (tiles <= 1) launch_main(mfma_kernel<EPI, 1, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
+    else if (tiles <= 2) launch_main(mfma_kernel<EPI, 2, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
+    else if (tiles <= 3) launch_main(mfma_kernel<EPI, 3, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
+    else if (tiles <= 4) launch_main(mfma_kernel<EPI, 4, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
+    else if (tiles <= 5) launch_main(mfma_kernel<EPI, 5, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
+    else if (tiles <= 6) launch_main(mfma_kernel<EPI, 6, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
     else if constexpr (RT <= 2) {
-        if (tiles <= 7) launch_main(mfma_kernel<EPI, 7, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
-        else launch_main(mfma_kernel<EPI, kMfmaMaxTiles, RT>, dim3(grid), dim3(256), 0, s, g, units, n_host);
+        if (tiles <= 7) launch_main(mfma_kernel<EPI, 7, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
+        else launch_main(mfma_kernel<EPI, kMfmaMaxTiles, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
     }
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    if constexpr (EPI == EPI_ADD) {
+        const dim3 sg((units + 63) / 64, (g.rows.n_max + 15) / 16);
+        if (splits == 2) split_add_kernel<2><<<sg, 256, 0, s>>>(g, units, n_host, part);
+        else if (splits == 4) split_add_kernel<4><<<sg, 256, 0, s>>>(g, units, n_host, part);
+        else split_add_kernel<kMfmaMaxSplits><<<sg, 256, 0, s>>>(g, units, n_host, part);
+        return hipGetLastError();
+    }
+    return hipErrorInvalidValue;   // only the residual-add kinds split K
 }
 
 // Largest weight tile per workgroup that still gives kMfmaMinGrid workgroups
 // (four tiles only up to six column tiles: beyond, their registers would
-// halve the occupancy)
+// halve the occupancy); K split per mfma_splits, with 64-row (or, beyond
+// six column tiles, 32-row) tiles
 template <int EPI>
-static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, hipStream_t s) {
+static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, float* part, hipStream_t s) {
     const bool wide = g.rows.n_max <= 16 * 6;
+    const int splits = part ? mfma_splits(EPI, units, g.K) : 1;
+    if (splits > 1) {
+        if (wide) return launch_mfma_nt<EPI, 4>(g, units, n_host, splits, part, s);
+        return launch_mfma_nt<EPI, 2>(g, units, n_host, splits, part, s);
+    }
     if constexpr (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
-        if (wide && units / 32 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, s);
-        return launch_mfma_nt<EPI, 2>(g, units, n_host, s);
+        if (wide && units / 32 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, 1, nullptr, s);
+        return launch_mfma_nt<EPI, 2>(g, units, n_host, 1, nullptr, s);
     } else {
-        if (wide && units / 64 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, s);
-        if (units / 32 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 2>(g, units, n_host, s);
-        return launch_mfma_nt<EPI, 1>(g, units, n_host, s);
+        if (wide && units / 64 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, 1, nullptr, s);
+        if (units / 32 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 2>(g, units, n_host, 1, nullptr, s);
+        return launch_mfma_nt<EPI, 1>(g, units, n_host, 1, nullptr, s);
     }
 }
 
@@ -254,14 +332,16 @@ hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, hipStream_t s) {
+hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, float* part, hipStream_t s) {
     const int n_host = g.rows.exact ? g.rows.n_max : -1;
-    hipError_t e = launch_prep(pro, g, s);
-    if (e != hipSuccess) return e;
-    if (epi == EPI_QKV) return launch_mfma_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), n_host, s);
-    if (epi == EPI_SWIGLU) return launch_mfma_epi<EPI_SWIGLU>(g, g.f, n_host, s);
-    if (epi == EPI_BIAS_ACT) return launch_mfma_epi<EPI_BIAS_ACT>(g, g.N, n_host, s);
-    return launch_mfma_epi<EPI_ADD>(g, g.N, n_host, s);
+    if (pro != PRO_STAGED) {
+        hipError_t e = launch_prep(pro, g, s);
+        if (e != hipSuccess) return e;
+    }
+    if (epi == EPI_QKV) return launch_mfma_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), n_host, part, s);
+    if (epi == EPI_SWIGLU) return launch_mfma_epi<EPI_SWIGLU>(g, g.f, n_host, part, s);
+    if (epi == EPI_BIAS_ACT) return launch_mfma_epi<EPI_BIAS_ACT>(g, g.N, n_host, part, s);
+    return launch_mfma_epi<EPI_ADD>(g, g.N, n_host, part, s);
 }
 
 }  // namespace buddy
