@@ -630,6 +630,31 @@ def test_batched_steps_mfma(B, policy):
     print(B, rep)
 
 
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+@pytest.mark.parametrize("B", [40, 150])
+def test_batched_split_k_mfma(B, policy):
+    """A decoder whose FFN down projection is long (K = 4 d): on the MFMA
+    path it splits K over eight workgroups and a fixed-order kernel adds the
+    split sums; the attention output and the SwiGLU output reach the O and
+    down projections as bf16 staged by their producers.  Positions up to
+    299 give several attention chunks (merge kernel) next to single-chunk
+    rows; B = 150 spans two 128-row column groups."""
+    T = 300
+    shape = dict(n_layers=5, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64, d_ffn=1024,
+                 dm_hidden=64, dm_act="silu", rope_theta=1e4, rms_eps=1e-5)
+    P = Pair(shape, "bf16", T, B, seed=25, omega=0.1, policy=policy)
+    g = torch.Generator().manual_seed(26)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    rng = np.random.default_rng(27)
+    pos = rng.integers(0, T, size=B).tolist()
+    pos[0] = T - 1
+    ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=28).numpy()
+    rep = one_step_all(P, hk, hv, pos, ks, x)
+    print(B, rep)
+
+
 # ------------------------------------- grouped-query attention on MFMA
 
 def gqa_shape(G):
