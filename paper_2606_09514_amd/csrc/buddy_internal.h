@@ -23,12 +23,25 @@ constexpr int kAttnMaxChunks = 256;  // position chunks per (sequence, KV head)
 
 __device__ __forceinline__ float bf2f(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
 
-// fp32 -> bf16, round to nearest, ties to even; NaN stays a quiet NaN.
+// fp32 -> bf16, round to nearest, ties to even; NaN becomes the quiet NaN
+// of its sign.  The conversion is gfx950's v_cvt_pk_bf16_f32, which gives
+// the same bits as adding 0x7fff plus the lowest kept bit and truncating, on
+// every non-NaN input (compared over all 2^32 inputs on the device); only
+// NaN payloads differ, hence the select.
 __device__ __forceinline__ bf16_t f2bf(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)(((u >> 16) & 0x8000u) | 0x7fc0u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (bf16_t)(u >> 16);
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t rounded = __builtin_bit_cast(unsigned short, (__bf16)f);
+    const uint32_t qnan = ((u >> 16) & 0x8000u) | 0x7fc0u;
+    return (bf16_t)((u & 0x7fffffffu) > 0x7f800000u ? qnan : rounded);
+}
+
+// Two fp32 values as packed bf16 (a in the low half), round to nearest
+// even, in one v_cvt_pk_bf16_f32; NaNs stay NaNs but keep a payload, so this
+// is for MFMA operands, and f2bf for values that are stored.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
 // Start layer S of the router (0 in the config reads as 1): blocks 0..S-1

@@ -244,7 +244,6 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint32_t bf16_bits(float x) { return (uint32_t)f2bf(x); }
 
 template <int GM>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
@@ -283,10 +282,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
                 const float v0 = h < G ? xv[e] * qs : 0.f, v1 = h < G ? xv[e + 1] * qs : 0.f;
-                const uint32_t h0 = bf16_bits(v0), h1 = bf16_bits(v1);
-                const float r0 = v0 - __uint_as_float(h0 << 16), r1 = v1 - __uint_as_float(h1 << 16);
-                hi[e / 2] = h0 | (h1 << 16);
-                lo[e / 2] = bf16_bits(r0) | (bf16_bits(r1) << 16);
+                const uint32_t hp = pack_bf16x2(v0, v1);
+                const float r0 = v0 - __uint_as_float(hp << 16), r1 = v1 - __uint_as_float(hp & 0xffff0000u);
+                hi[e / 2] = hp;
+                lo[e / 2] = pack_bf16x2(r0, r1);
             }
             qh[s] = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
             ql[s] = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
@@ -524,10 +523,10 @@ void attn_prefill_kernel(AttnArgs a) {
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
                 const float v0 = q_ok ? xv[e] * qs : 0.f, v1 = q_ok ? xv[e + 1] * qs : 0.f;
-                const uint32_t h0 = bf16_bits(v0), h1 = bf16_bits(v1);
-                const float r0 = v0 - __uint_as_float(h0 << 16), r1 = v1 - __uint_as_float(h1 << 16);
-                hi[e / 2] = h0 | (h1 << 16);
-                lo[e / 2] = bf16_bits(r0) | (bf16_bits(r1) << 16);
+                const uint32_t hp = pack_bf16x2(v0, v1);
+                const float r0 = v0 - __uint_as_float(hp << 16), r1 = v1 - __uint_as_float(hp & 0xffff0000u);
+                hi[e / 2] = hp;
+                lo[e / 2] = pack_bf16x2(r0, r1);
             }
             qh[s] = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
             ql[s] = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
@@ -634,8 +633,7 @@ void attn_prefill_kernel(AttnArgs a) {
                 p[e] = scale_of(st[t][e], mn);
                 ls += p[e];
             }
-            pa[t] = __builtin_bit_cast(s16x4_t, make_uint2(bf16_bits(p[0]) | (bf16_bits(p[1]) << 16),
-                                                           bf16_bits(p[2]) | (bf16_bits(p[3]) << 16)));
+            pa[t] = __builtin_bit_cast(s16x4_t, make_uint2(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])));
         }
         ls += __shfl_xor(ls, 16, kWave);
         ls += __shfl_xor(ls, 32, kWave);

@@ -229,14 +229,11 @@ void gemm_kernel(GemvArgs g, int units, int n, float* part) {
             for (int i = 0; i < TI / 2; ++i) {
                 const int ub = u0 + 16 * (wm * TI / 2 + i) + 4 * (lane >> 4);
                 if (ub >= units) continue;
-                uint32_t h[4];
+                float m[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float v0 = acc[i][j][e], v1 = acc[TI / 2 + i][j][e];
-                    h[e] = f2bf(swiglu(v0, v1));
-                }
+                for (int e = 0; e < 4; ++e) m[e] = swiglu(acc[i][j][e], acc[TI / 2 + i][j][e]);
                 *reinterpret_cast<uint2*>(g.xb_out + xb_index(col, ub, units)) =
-                    make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                    make_uint2(pack_bf16x2(m[0], m[1]), pack_bf16x2(m[2], m[3]));
             }
             continue;
         }
@@ -312,8 +309,7 @@ __global__ __launch_bounds__(1024) void prep_tile_kernel(GemvArgs g, int n) {
                 }
             }
             *reinterpret_cast<uint2*>(row + 2 * k) =
-                make_uint2((uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16),
-                           (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+                make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
         }
         __syncthreads();
         // fragment (k-step s, lane L): row L % 16, columns 32 s + 8 (L / 16) .. + 7

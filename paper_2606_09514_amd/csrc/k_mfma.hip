@@ -85,10 +85,10 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
             for (int q = 0; q < 8; ++q) v[q] *= inv * gv[q];
         }
         uint4 o;
-        o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-        o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-        o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-        o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+        o.x = pack_bf16x2(v[0], v[1]);
+        o.y = pack_bf16x2(v[2], v[3]);
+        o.z = pack_bf16x2(v[4], v[5]);
+        o.w = pack_bf16x2(v[6], v[7]);
         // B-operand order: tile i / 16, k-step k / 32, lane (i % 16) + 16 (k / 8 % 4)
         const size_t frag = ((size_t)(i >> 4) * (K >> 5) + (k >> 5)) * 64 + (i & 15) + 16 * ((k >> 3) & 3);
         *reinterpret_cast<uint4*>(g.XB + frag * 8) = o;
