@@ -23,8 +23,8 @@
 //                    products finish with a short DPP / shuffle tree.  Used
 //                    for fp32 caches, head_dim 64 and groups of one or two.
 //  attn_mfma_kernel  bf16, head_dim 128, three to eight query heads per KV
-//                    head: the scores of 16 rows against the group are one
-//                    MFMA product, P V stays on the vector ALUs.
+//                    head: the scores of 16 rows against the group and the
+//                    P V product of those rows are MFMA products.
 // The prompt tokens of a prefill (bf16, head_dim 128) take a third kernel,
 // attn_prefill_kernel, with both products on the MFMA (below).
 #include "buddy_internal.h"
@@ -232,24 +232,73 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     }
 }
 
-// Grouped-query attention for bf16 caches with head_dim 128 and three to
-// kMaxGroup query heads per KV head: the scores of a 16-row slab against the
-// group's heads are one 16 x 16 x 128 MFMA product (v_mfma_f32_16x16x32_bf16,
-// K rows as the A operand, the queries split into bf16 high and low parts as
-// the B operand, so the scores keep about 16 bits of the fp32 query), the
-// online softmax runs on the MFMA result, and P V runs on the vector ALUs
-// with each lane owning two output columns of every head.
+// Decode attention on MFMA: bf16 cache, head_dim 128, three to kMaxGroup
+// query heads per KV head.  Each wavefront takes 16-row slabs of the chunk
+// (every fourth slab) and keeps an online softmax per head:
+//   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = the slab's K rows (loaded
+//                 to registers one slab ahead), B = the group's queries as
+//                 bf16 high + low parts (heads past G are zero), so scores
+//                 keep about 16 bits of the fp32 query;
+//                 D: lane h + 16 r holds rows 4 r .. 4 r + 3 of head h;
+//   softmax       online per head (exp2 of prescaled scores);
+//   O += P V      v_mfma_f32_16x16x16_bf16 with the softmax weights in place
+//                 as the A operand, split into bf16 high + low parts (two
+//                 products, so P keeps about 16 bits), and V[4 rows][col] as
+//                 the B operand from ds_read_b64_tr_b16: the wavefront moves
+//                 its slab of V global -> LDS directly (two buffers, the next
+//                 slab's loads in flight), each 256-byte row's 16-byte chunks
+//                 stored at chunk ^ (row % 16); O: lane c + 16 r holds heads
+//                 4 r .. 4 r + 3 of column c of each 16-column tile.
+// The four wavefronts' (max, sum, O) are merged through LDS at the end.
 //   D[i][j] (16 x 16): lane j + 16 (i / 4), element i % 4
-//   A[i][k]: lane i + 16 (k / 8), element k % 8;  B[k][j]: lane j + 16 (k / 8)
+//   x32 A[i][k]: lane i + 16 (k / 8), element k % 8;  B[k][j]: lane j + 16 (k / 8)
+//   x16 A[i][k]: lane i + 16 (k / 4), element k % 4;  B[k][j]: lane j + 16 (k / 4)
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(1))) const void* attn_gptr_t;
+typedef __attribute__((address_space(3))) void* attn_lptr_t;
 
+// Eight transposing 8-byte LDS reads at per-lane addresses plus one
+// immediate (the V fragments of the 8 column tiles of a 16-row slab), then a
+// wait; asm so that the compiler does not first wait for the direct-to-LDS
+// loads in flight into the other buffer.
+template <int OFF>
+__device__ __forceinline__ void read_v_tr(const uint32_t* ad, uint32_t base, s16x4_t* x) {
+    i32x2_t r[8];
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %8 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %1, %9 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %2, %10 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %3, %11 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %4, %12 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %5, %13 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %6, %14 offset:%16\n\t"
+        "ds_read_b64_tr_b16 %7, %15 offset:%16\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]),
+          "=&v"(r[6]), "=&v"(r[7])
+        : "v"(ad[0] + base), "v"(ad[1] + base), "v"(ad[2] + base), "v"(ad[3] + base),
+          "v"(ad[4] + base), "v"(ad[5] + base), "v"(ad[6] + base), "v"(ad[7] + base), "i"(OFF)
+        : "memory");
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = __builtin_bit_cast(s16x4_t, r[i]);
+}
 
-template <int GM>
-__global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
+// s_waitcnt with at most n vector-memory operations outstanding (the other
+// counters left at their maxima).
+__device__ __forceinline__ constexpr int vmcnt_at_most(int n) {
+    return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8);
+}
+
+// Three workgroups per CU: 138 registers (accumulators in VGPRs) and at most
+// 49 KB of LDS each.
+template <int GM, bool MASKED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void attn_mfma_kernel(AttnArgs a) {
     constexpr int HD = 128, KS = HD / 32;
-    __shared__ float s_p[4][16][16];          // per wave: p[head][slab row]
-    __shared__ float s_al[4][16];             // per wave: rescale of each head
+    constexpr int kSlab = 16 * HD * 2;        // bytes of a 16-row V slab
+    __shared__ __attribute__((aligned(16))) char s_v[4][2][kSlab];   // [wave][buffer]
     __shared__ float s_acc[4][GM][HD + 2];
     const int i = blockIdx.z;
     if (!a.rows.exact && i >= *a.rows.cnt) return;
@@ -259,20 +308,20 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     slot_pos(b, a.tok_T, a.pos, a.pos_u, slot, pos);
     const int G = a.nq / a.nkv;
     const int tid = threadIdx.x, lane = tid & 63;
+    const int li = lane & 15, lg = lane >> 4;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int j0 = c * a.chunk_len;
     const int j1 = min(j0 + a.chunk_len, pos + 1);
     const size_t base = ((size_t)slot * a.nkv + g) * a.T * HD;
     const bf16_t* Kb = (const bf16_t*)a.kc + base;
-    const uint32_t* Vb = (const uint32_t*)((const bf16_t*)a.vc + base);   // bf16 pairs
+    const bf16_t* Vb = (const bf16_t*)a.vc + base;
 
-    // B operand: queries of the group, scaled so that exp2 of a score is the
-    // softmax weight, as bf16 high + low parts; heads past G are zero
+    // B operand of the scores: queries of the group, scaled so that exp2 of
+    // a score is the softmax weight, as bf16 high + low parts
     bf16x8_t qh[KS], ql[KS];
     {
-        const int h = lane & 15, q8 = 8 * (lane >> 4);
         const float qs = 1.4426950408889634f / sqrtf((float)HD);
-        const float* qp = a.q + ((size_t)b * a.nq + g * G + min(h, G - 1)) * HD + q8;
+        const float* qp = a.q + ((size_t)b * a.nq + g * G + min(li, G - 1)) * HD + 8 * lg;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             const float4 x0 = *reinterpret_cast<const float4*>(qp + 32 * s);
@@ -281,7 +330,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
             uint32_t hi[4], lo[4];
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-                const float v0 = h < G ? xv[e] * qs : 0.f, v1 = h < G ? xv[e + 1] * qs : 0.f;
+                const float v0 = li < G ? xv[e] * qs : 0.f, v1 = li < G ? xv[e + 1] * qs : 0.f;
                 const uint32_t hp = pack_bf16x2(v0, v1);
                 const float r0 = v0 - __uint_as_float(hp << 16), r1 = v1 - __uint_as_float(hp & 0xffff0000u);
                 hi[e / 2] = hp;
@@ -292,53 +341,87 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         }
     }
 
-    float mrun = -INFINITY;     // running max of head lane % 16 (same in its four lanes)
-    float lrun = 0.f;           // running sum over this lane's rows of that head
-    float acc[GM][2];           // columns 2 lane, 2 lane + 1 of every head
+    // V addresses of ds_read_b64_tr_b16 in a slab (B operand: lane c + 16 r
+    // holds V[4 r .. 4 r + 3][c]): source lane s = lane % 16 addresses row
+    // 4 r + s / 4, columns 16 dt + 4 (s % 4) .. + 3, stored in chunk
+    // (column / 8) ^ row
+    const uint32_t lds_w = (uint32_t)(uintptr_t)(attn_lptr_t)&s_v[wave][0][0];
+    uint32_t vad[8];
+    {
+        const int rr = 4 * lg + (li >> 2), cin = 4 * (li & 3);
 #pragma unroll
-    for (int h = 0; h < GM; ++h) acc[h][0] = acc[h][1] = 0.f;
+        for (int dt = 0; dt < 8; ++dt) {
+            const int col = 16 * dt + cin;
+            vad[dt] = lds_w + rr * 256 + (((col >> 3) ^ rr) * 16) + (col & 7) * 2;
+        }
+    }
 
-    // K fragments of a slab (rows clamped to a valid row, masked below) and
-    // its V rows and map entries; the next slab's are issued before the
-    // current one's arithmetic
-    bf16x8_t kn[KS];
-    uint32_t vn[16];
+    float mrun = -INFINITY;     // running max of head li (same in its four lanes)
+    float lrun = 0.f;           // running sum over this lane's rows of that head
+    f32x4_t o[8];               // O[4 lg + e][16 dt + li]
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[dt] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+
+    // a slab: its K fragments to registers (rows clamped to a valid row,
+    // masked below), with a map its map entries, then its V rows global ->
+    // LDS buffer `buf` (lane L of load ld lands at row 4 ld + L / 16, stored
+    // chunk L % 16, which holds source chunk (L % 16) ^ row).  The next
+    // slab's loads are issued once the current scores have used the K
+    // registers.  Without a map the K loads are asm, outside the compiler's
+    // load tracking, which with direct-to-LDS loads pending would wait for
+    // every load before the scores; the waits below cover them (in this
+    // issue order the scores need all but the slab's last 4 loads, its V,
+    // done).  With a map every register load is the compiler's, and so are
+    // their waits.
+    bf16x8_t kf[KS];
     uint8_t en[4];
-    auto load_slab = [&](int jb) {
-        const int jr = min(jb + (lane & 15), j1 - 1);
+    auto load_slab = [&](int jb, int buf) {
+        const int jr = min(jb + li, j1 - 1);
+        const bf16_t* kp = Kb + (size_t)jr * HD + 8 * lg;
+        if constexpr (MASKED) {
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-            kn[s] = *reinterpret_cast<const bf16x8_t*>(Kb + (size_t)jr * HD + 32 * s + 8 * (lane >> 4));
+            for (int s = 0; s < KS; ++s) kf[s] = *reinterpret_cast<const bf16x8_t*>(kp + 32 * s);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) vn[r] = Vb[(size_t)min(jb + r, j1 - 1) * (HD / 2) + lane];
+            for (int v = 0; v < 4; ++v) en[v] = a.exec[(size_t)slot * a.T + min(jb + 4 * lg + v, j1 - 1)];
+        } else {
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
-            en[v] = a.exec ? a.exec[(size_t)slot * a.T + min(jb + 4 * (lane >> 4) + v, j1 - 1)] : 1;
+            for (int s = 0; s < KS; ++s) {
+                typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+                u4 r;
+                asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(kp + 32 * s) : "memory");
+                kf[s] = __builtin_bit_cast(bf16x8_t, r);
+            }
+        }
+#pragma unroll
+        for (int ld = 0; ld < 4; ++ld) {
+            const int rl = 4 * ld + lg;
+            const size_t src = (size_t)min(jb + rl, j1 - 1) * HD + ((li ^ rl) * 8);
+            __builtin_amdgcn_global_load_lds((attn_gptr_t)(Vb + src),
+                                             (attn_lptr_t)(&s_v[wave][buf][ld * 1024]), 16, 0, 0);
+        }
     };
-    if (j0 + 16 * wave < j1) load_slab(j0 + 16 * wave);
-    for (int jb = j0 + 16 * wave; jb < j1; jb += 64) {
-        bf16x8_t kf[KS];
-        uint32_t vw[16];
+    int buf = 0;
+    if (j0 + 16 * wave < j1) load_slab(j0 + 16 * wave, 0);
+    for (int jb = j0 + 16 * wave; jb < j1; jb += 64, buf ^= 1) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_at_most(4));
+        __builtin_amdgcn_sched_barrier(0);   // nothing reads K before the wait
         uint8_t ex[4];
 #pragma unroll
-        for (int s = 0; s < KS; ++s) kf[s] = kn[s];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) vw[r] = vn[r];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) ex[v] = en[v];
-        if (jb + 64 < j1) load_slab(jb + 64);
-
+        for (int v = 0; v < 4; ++v) ex[v] = MASKED ? en[v] : 1;
         f32x4_t d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qh[s], d, 0, 0, 0);
             d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], ql[s], d, 0, 0, 0);
         }
-        // rows of this lane: jb + 4 (lane / 16) + v; head lane % 16
+        __builtin_amdgcn_sched_barrier(0);   // the K registers are free only now
+        const bool more = jb + 64 < j1;
+        if (more) load_slab(jb + 64, buf ^ 1);
+        // rows of this lane: jb + 4 lg + v; head li
         float sc[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int jrow = jb + 4 * (lane >> 4) + v;
+            const int jrow = jb + 4 * lg + v;
             sc[v] = jrow < j1 && (ex[v] != 0 || jrow == pos) ? d[v] : -INFINITY;
         }
         float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
@@ -351,42 +434,48 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         for (int v = 0; v < 4; ++v) p[v] = scale_of(sc[v], mn);
         lrun = lrun * al + ((p[0] + p[1]) + (p[2] + p[3]));
         mrun = mn;
-        *reinterpret_cast<float4*>(&s_p[wave][lane & 15][4 * (lane >> 4)]) = make_float4(p[0], p[1], p[2], p[3]);
-        if (lane < 16) s_al[wave][lane] = al;
-        __builtin_amdgcn_wave_barrier();
-
-        float vf[16][2];
+        // A operand (head li, rows 4 lg .. 4 lg + 3) as bf16 high + low parts
+        const uint32_t h01 = pack_bf16x2(p[0], p[1]), h23 = pack_bf16x2(p[2], p[3]);
+        const s16x4_t ph = __builtin_bit_cast(s16x4_t, make_uint2(h01, h23));
+        const s16x4_t pl = __builtin_bit_cast(s16x4_t, make_uint2(
+            pack_bf16x2(p[0] - __uint_as_float(h01 << 16), p[1] - __uint_as_float(h01 & 0xffff0000u)),
+            pack_bf16x2(p[2] - __uint_as_float(h23 << 16), p[3] - __uint_as_float(h23 & 0xffff0000u))));
+        // rescale O (lane c + 16 r holds heads 4 r .. 4 r + 3) unless no
+        // head's running max moved; a multiply by 1 would change nothing
+        if (__any(al != 1.f)) {
+            float ar[4];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            vf[r][0] = __uint_as_float(vw[r] << 16);
-            vf[r][1] = __uint_as_float(vw[r] & 0xffff0000u);
+            for (int e = 0; e < 4; ++e) ar[e] = __shfl(al, 4 * lg + e, kWave);
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[dt][e] *= ar[e];
         }
+        // this slab's V is in LDS once its four loads are done (the next
+        // slab's K and V loads, 8, and with a map its 4 map loads, may still
+        // be in flight)
+        if (more) __builtin_amdgcn_s_waitcnt(vmcnt_at_most(8));
+        else __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));
+        s16x4_t vf[8];
+        if (buf == 0) read_v_tr<0>(vad, 0, vf);
+        else read_v_tr<kSlab>(vad, 0, vf);
 #pragma unroll
-        for (int h = 0; h < GM; ++h) {
-            const float sa = s_al[wave][h];
-            acc[h][0] *= sa;
-            acc[h][1] *= sa;
-#pragma unroll
-            for (int rq = 0; rq < 4; ++rq) {
-                const float4 p4 = *reinterpret_cast<const float4*>(&s_p[wave][h][4 * rq]);
-                const float pv[4] = {p4.x, p4.y, p4.z, p4.w};
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    acc[h][0] += pv[v] * vf[4 * rq + v][0];
-                    acc[h][1] += pv[v] * vf[4 * rq + v][1];
-                }
-            }
+        for (int dt = 0; dt < 8; ++dt) {
+            o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ph, vf[dt], o[dt], 0, 0, 0);
+            o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pl, vf[dt], o[dt], 0, 0, 0);
         }
-        __builtin_amdgcn_wave_barrier();   // s_p / s_al reads done before the next slab's writes
     }
 
     // per wave: total of each head's running sum over its four lanes
     lrun += __shfl_xor(lrun, 16, kWave);
     lrun += __shfl_xor(lrun, 32, kWave);
 #pragma unroll
-    for (int h = 0; h < GM; ++h) {
-        s_acc[wave][h][2 * lane] = acc[h][0];
-        s_acc[wave][h][2 * lane + 1] = acc[h][1];
+    for (int e = 0; e < 4; ++e) {
+        const int hh = 4 * lg + e;
+        if (hh < GM) {
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) s_acc[wave][hh][16 * dt + li] = o[dt][e];
+        }
     }
     if (lane < GM) {
         s_acc[wave][lane][HD] = mrun;
@@ -437,10 +526,6 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
 //                 operand V[4 rows][d] comes from ds_read_b64_tr_b16, whose
 //                 16-lane groups return element l % 4 of the 8-byte block
 //                 addressed by lane l / 4 + 4 e (checked on the device).
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-typedef int i32x2_t __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(1))) const void* pf_gptr_t;
-typedef __attribute__((address_space(3))) void* pf_lptr_t;
 
 constexpr int kPfRows = 64;                      // K/V rows per tile
 constexpr int kPfTile = kPfRows * 128 * 2;       // bytes of a K or V tile
@@ -466,29 +551,6 @@ __device__ __forceinline__ void pf_read_k(const uint32_t* ad, uint32_t base, bf1
     x[2] = __builtin_bit_cast(bf16x8_t, r2);
     x[3] = __builtin_bit_cast(bf16x8_t, r3);
 }
-// Eight transposing 8-byte reads (the V fragments of the 8 column tiles).
-template <int OFF>
-__device__ __forceinline__ void pf_read_v(const uint32_t* ad, uint32_t base, s16x4_t* x) {
-    i32x2_t r[8];
-    asm volatile(
-        "ds_read_b64_tr_b16 %0, %8 offset:%16\n\t"
-        "ds_read_b64_tr_b16 %1, %9 offset:%16\n\t"
-        "ds_read_b64_tr_b16 %2, %10 offset:%16\n\t"
-        "ds_read_b64_tr_b16 %3, %11 offset:%16\n\t"
-        "ds_read_b64_tr_b16 %4, %12 offset:%16\n\t"
-        "ds_read_b64_tr_b16 %5, %13 offset:%16\n\t"
-        "ds_read_b64_tr_b16 %6, %14 offset:%16\n\t"
-        "ds_read_b64_tr_b16 %7, %15 offset:%16\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]),
-          "=&v"(r[6]), "=&v"(r[7])
-        : "v"(ad[0] + base), "v"(ad[1] + base), "v"(ad[2] + base), "v"(ad[3] + base),
-          "v"(ad[4] + base), "v"(ad[5] + base), "v"(ad[6] + base), "v"(ad[7] + base), "i"(OFF)
-        : "memory");
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = __builtin_bit_cast(s16x4_t, r[i]);
-}
-
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_prefill_kernel(AttnArgs a) {
     constexpr int HD = 128;
@@ -547,9 +609,9 @@ void attn_prefill_kernel(AttnArgs a) {
             const int row = min(kt * kPfRows + rl, pos_last);
             const size_t src = (size_t)row * HD + (((lane & 15) ^ (rl & 15)) * 8);
             const int dst = (16 * wave + 4 * ld) * 256;
-            __builtin_amdgcn_global_load_lds((pf_gptr_t)(Kg + src), (pf_lptr_t)(s_kv[buf][0] + dst),
+            __builtin_amdgcn_global_load_lds((attn_gptr_t)(Kg + src), (attn_lptr_t)(s_kv[buf][0] + dst),
                                              16, 0, 0);
-            __builtin_amdgcn_global_load_lds((pf_gptr_t)(Vg + src), (pf_lptr_t)(s_kv[buf][1] + dst),
+            __builtin_amdgcn_global_load_lds((attn_gptr_t)(Vg + src), (attn_lptr_t)(s_kv[buf][1] + dst),
                                              16, 0, 0);
         }
     };
@@ -557,7 +619,7 @@ void attn_prefill_kernel(AttnArgs a) {
     // K fragment addresses (A operand: lane i + 16 dg holds row 16 t + i,
     // d = 32 s + 8 dg .. + 7): stored chunk (4 s + dg) ^ i; the tile t of 16
     // rows is an immediate 4 KB t.
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(pf_lptr_t)&s_kv[0][0][0];
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(attn_lptr_t)&s_kv[0][0][0];
     const int li = lane & 15, lg = lane >> 4;
     uint32_t kad[4];
 #pragma unroll
@@ -652,10 +714,10 @@ void attn_prefill_kernel(AttnArgs a) {
         for (int t = 0; t < 4; ++t) {
             s16x4_t vf[8];
             switch (t) {
-                case 0: pf_read_v<0>(vad, bb, vf); break;
-                case 1: pf_read_v<4096>(vad, bb, vf); break;
-                case 2: pf_read_v<8192>(vad, bb, vf); break;
-                default: pf_read_v<12288>(vad, bb, vf); break;
+                case 0: read_v_tr<0>(vad, bb, vf); break;
+                case 1: read_v_tr<4096>(vad, bb, vf); break;
+                case 2: read_v_tr<8192>(vad, bb, vf); break;
+                default: read_v_tr<12288>(vad, bb, vf); break;
             }
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt)
@@ -746,8 +808,13 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
         return hipGetLastError();
     }
     if (attn_uses_mfma(dtype, a.hd, G)) {
-        if (G <= 4) launch_main(attn_mfma_kernel<4>, grid, dim3(256), 0, s, a);
-        else launch_main(attn_mfma_kernel<kMaxGroup>, grid, dim3(256), 0, s, a);
+        if (a.exec) {
+            if (G <= 4) launch_main(attn_mfma_kernel<4, true>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_mfma_kernel<kMaxGroup, true>, grid, dim3(256), 0, s, a);
+        } else {
+            if (G <= 4) launch_main(attn_mfma_kernel<4, false>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_mfma_kernel<kMaxGroup, false>, grid, dim3(256), 0, s, a);
+        }
     } else if (dtype == BUDDY_BF16) {
         if (a.hd == 128) {
             if (G == 1) launch_main(attn_kernel<bf16_t, 1, 16>, grid, dim3(256), 0, s, a);

@@ -19,6 +19,8 @@
 //             EPI_QKV      unit = rows (i, i + hd/2) of one head: rotary
 //                          embedding at pos[b] for q and k heads, q to Y,
 //                          k and v appended to the cache rounded to storage.
+#include <atomic>
+#include <cstdint>
 #include <type_traits>
 
 #include "buddy_internal.h"
@@ -242,15 +244,22 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
 template <typename TW, int NR, int PRO, int EPI, int S, int ML, int P, bool TAIL, bool MULTI>
 static hipError_t launch_one(const GemvArgs& g, int units, int n_host, hipStream_t s) {
     const size_t lds = (size_t)NR * g.K * sizeof(float);
-    static bool attr_set = false;
-    if (lds > 64 * 1024 && !attr_set) {
-        // dynamic LDS above the 64 KB default; the dispatcher never asks
-        // for more than kGemvLds
-        hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, kGemvLds);
+    // devices (one bit each, current device) on which this instantiation
+    // may take more than the 64 KB default of dynamic LDS
+    static std::atomic<uint64_t> attr_set{0};
+    if (lds > 64 * 1024) {
+        int dev = 0;
+        hipError_t e = hipGetDevice(&dev);
         if (e != hipSuccess) return e;
-        attr_set = true;
+        const uint64_t bit = 1ull << (dev & 63);
+        if (!(attr_set.load(std::memory_order_relaxed) & bit)) {
+            // the dispatcher never asks for more than kGemvLds
+            e = hipFuncSetAttribute(
+                reinterpret_cast<const void*>(&gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI>),
+                hipFuncAttributeMaxDynamicSharedMemorySize, kGemvLds);
+            if (e != hipSuccess) return e;
+            attr_set.fetch_or(bit, std::memory_order_relaxed);
+        }
     }
     constexpr int KS = kWave * St<TW>::V;
     const int nsteps = (g.K + KS - 1) / KS;
