@@ -96,16 +96,19 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     model.set_timing_events(blib.KERNEL_GATE_UP, kernel_layer, starts, stops)
     positions = []
     torch.cuda.synchronize()
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0.record()
+    # an event between consecutive steps on the launch stream: the first and
+    # last bracket the timed region, the others give per-step times
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    evs[0].record()
     for t in range(steps):
         step(pos, t)
+        evs[t + 1].record()
         positions.append([pos] * B)
         pos += 1
-    t1.record()
     torch.cuda.synchronize()
     model.set_timing_events(blib.KERNEL_GATE_UP, kernel_layer, [], [])
-    total_ms = t0.elapsed_time(t1)
+    total_ms = evs[0].elapsed_time(evs[steps])
+    step_ms = np.array([evs[t].elapsed_time(evs[t + 1]) for t in range(steps)])
     kern_ms = [hip.elapsed_ms(a, b) for a, b in zip(starts, stops)]
     hip.destroy(starts + stops)
     m = masks.cpu().numpy()
@@ -116,6 +119,8 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     assert all(int(m[t, b].sum()) == kk[t, b] for t in range(steps) for b in range(B))
     distinct = len({m[t].tobytes() for t in range(steps)})
     return dict(ks=ks, total_ms=total_ms, ms_per_step=total_ms / steps,
+                step_ms_p50=float(np.percentile(step_ms, 50)),
+                step_ms_p90=float(np.percentile(step_ms, 90)),
                 tokens_per_s=B * steps / (total_ms / 1e3),
                 bytes_per_step=total_bytes / steps,
                 step_hbm_frac=total_bytes / (total_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
@@ -283,7 +288,8 @@ def main():
                        running_pool=args.pool == "running")
         name = "auto" if args.auto_budget else "mixed" if w.mixed else str(k)
         runs[name] = r
-        log(f"k={name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step, "
+        log(f"k={name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step "
+            f"(p50 {r['step_ms_p50']:.3f}, p90 {r['step_ms_p90']:.3f}), "
             f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline, gate_up {r['kernel_ms'] * 1e3:.1f} us")
 
     head = runs[next(iter(runs))]
@@ -323,6 +329,8 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "per_budget": {n: {"tokens_per_s": round(r["tokens_per_s"], 2),
                            "ms_per_step": round(r["ms_per_step"], 4),
+                           "step_ms_p50": round(r["step_ms_p50"], 4),
+                           "step_ms_p90": round(r["step_ms_p90"], 4),
                            "bytes_per_step": int(r["bytes_per_step"]),
                            "step_hbm_frac": round(r["step_hbm_frac"], 4),
                            "layers_used": r["layers_used"],
