@@ -51,6 +51,21 @@ struct PoolParams {
     int T, hd, nkv, splits, max_splits;
 };
 
+typedef uint32_t pool_u4 __attribute__((ext_vector_type(4)));
+// 16 bytes of a cache row as fp32 (8 bf16 or 4 fp32 values), nontemporal
+__device__ __forceinline__ void nt_vec(const bf16_t* q, float* out) {
+    const pool_u4 w = __builtin_nontemporal_load(reinterpret_cast<const pool_u4*>(q));
+    out[0] = __uint_as_float(w.x << 16); out[1] = __uint_as_float(w.x & 0xffff0000u);
+    out[2] = __uint_as_float(w.y << 16); out[3] = __uint_as_float(w.y & 0xffff0000u);
+    out[4] = __uint_as_float(w.z << 16); out[5] = __uint_as_float(w.z & 0xffff0000u);
+    out[6] = __uint_as_float(w.w << 16); out[7] = __uint_as_float(w.w & 0xffff0000u);
+}
+__device__ __forceinline__ void nt_vec(const float* q, float* out) {
+    const pool_u4 w = __builtin_nontemporal_load(reinterpret_cast<const pool_u4*>(q));
+    out[0] = __uint_as_float(w.x); out[1] = __uint_as_float(w.y);
+    out[2] = __uint_as_float(w.z); out[3] = __uint_as_float(w.w);
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void pool_kernel(PoolParams p) {
     constexpr int V = St<T>::V;
@@ -70,11 +85,13 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolParams p) {
     float ak[V], av[V];
 #pragma unroll
     for (int e = 0; e < V; ++e) ak[e] = av[e] = 0.f;
+    // the rows are read once here (this step's first-block attention has
+    // already run): nontemporal 16-byte loads
 #pragma unroll 4
     for (int j = j0 + slot; j < j1; j += rpp) {
         float kr[V], vr[V];
-        St<T>::vec(K + (size_t)j * p.hd + col * V, kr);
-        St<T>::vec(Vc + (size_t)j * p.hd + col * V, vr);
+        nt_vec(K + (size_t)j * p.hd + col * V, kr);
+        nt_vec(Vc + (size_t)j * p.hd + col * V, vr);
 #pragma unroll
         for (int e = 0; e < V; ++e) { ak[e] += kr[e]; av[e] += vr[e]; }
     }
@@ -100,10 +117,11 @@ hipError_t launch_pool(const Model& M, const void* k0, const void* v0, int B, in
     p.k0 = k0; p.v0 = v0; p.pos = M.ws.pos; p.pos_u = pos_u;
     p.part = M.ws.pool_part;
     p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.max_splits = M.ws.max_pool_splits;
-    // a few position splits per (sequence, KV head): enough workgroups to
-    // stream the first-layer cache, few enough partials for the fold
-    int want = (256 + B * c.n_kv_heads - 1) / (B * c.n_kv_heads);
-    int by_len = (max_pos + 1 + 127) / 128;
+    // position splits per (sequence, KV head): about four workgroups per CU
+    // to stream the first-layer cache, at least 64 rows each, few enough
+    // partials for the fold
+    int want = (1024 + B * c.n_kv_heads - 1) / (B * c.n_kv_heads);
+    int by_len = (max_pos + 1 + 63) / 64;
     int splits = want < by_len ? want : by_len;
     if (splits < 1) splits = 1;
     if (splits > p.max_splits) splits = p.max_splits;
