@@ -97,11 +97,6 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
 
 // ----------------------------------------------------------------- MFMA
 
-// k-steps per load round: all loads of a round are issued before its MFMAs
-__host__ __device__ constexpr int mfma_round(int rt, int nt) {
-    return 16 / (rt + nt) < 1 ? 1 : 16 / (rt + nt) > 8 ? 8 : 16 / (rt + nt);
-}
-
 // Partial sums of K split `ks`, weight tile t of a unit (0, or 1 for the
 // second row of the two-row kinds), unit u, routed row j: index
 // ((ks GT + t) units + u) n_cap + j, n_cap = the launch's row capacity.
@@ -109,13 +104,39 @@ __device__ __forceinline__ size_t part_index(int ks, int GT, int t, int units, i
     return ((size_t)(ks * GT + t) * units + u) * n_cap + j;
 }
 
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const void* mfma_gptr_t;
+typedef __attribute__((address_space(3))) void* mfma_lptr_t;
+
+// s_waitcnt with at most n vector-memory operations outstanding
+__device__ __forceinline__ constexpr int mfma_vmcnt(int n) {
+    return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8);
+}
+
+// Bytes of LDS: the weight rounds (4 wavefronts x 2 buffers x RT tiles x 16
+// rows x 128 bytes), reused for the K-slice reduction afterwards.
+__host__ __device__ constexpr int mfma_lds_bytes(int rt, int nt, int gt) {
+    return 4 * 2 * rt * 2048 > 4 * gt * 16 * nt * 16 * 4 ? 4 * 2 * rt * 2048 : 4 * gt * 16 * nt * 16 * 4;
+}
+
+// Weight stream: a round is two k-steps, 128 bytes (one cache line) of each
+// of the wavefront's 16 RT rows.  The rows move global -> LDS directly with
+// 1 KB loads of whole lines (8 rows x 128 bytes), nontemporal (read once per
+// launch), into one of two buffers while the other is used; each row's
+// 16-byte chunk c is stored at c ^ (row % 8), so that the fragment reads
+// (16 rows, one chunk each) spread over the banks.  The activation
+// fragments of a round (1 KB contiguous each) are asm register loads issued
+// at the round's start, outside the compiler's load tracking: the waits are
+// explicit (the round's weights, issued a round earlier, and activations
+// are in once no more than the next round's 2 RT weight loads are pending).
 template <int EPI, int NT, int RT>
 __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_host, float* part) {
     constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
     constexpr int GT = kPaired ? 2 : 1;       // weight tiles per epilogue group
     constexpr int NG = RT / GT;               // epilogue groups (16 units or rows each)
-    constexpr int U = mfma_round(RT, NT);
-    __shared__ float s_red[4][GT][16][NT * 16];
+    constexpr int kBuf = RT * 2048;           // bytes of one wavefront's round
+    __shared__ __attribute__((aligned(16))) char s_lds[mfma_lds_bytes(RT, NT, GT)];
+    auto s_red = reinterpret_cast<float (*)[GT][16][NT * 16]>(s_lds);
     const int n = n_host >= 0 ? n_host : *g.rows.cnt;
     if (n <= 0) return;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -124,19 +145,49 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
     const int S = K >> 5;                     // k-steps of a row
     const int sw = S / (4 * gridDim.y);       // k-steps of a wavefront (exact)
     const int kw = (blockIdx.y * 4 + wave) * sw;   // its first k-step
+    const int nr = (sw + 1) >> 1;             // rounds; the last is half when sw is odd
     const int u0 = blockIdx.x * 16 * NG;      // first unit (two-row kinds) or row
 
-    // A rows of this lane (lane % 16 within each tile); past the end the
-    // last valid unit is read and its sums are discarded
-    const bf16_t* Ap[RT];
+    // weight rows of this lane's direct loads: tile t, half h covers rows
+    // 8 h + lane / 8 of the tile; past the end the last valid unit is read
+    // and its sums are discarded
+    const bf16_t* Ar[RT][2];
 #pragma unroll
-    for (int q = 0; q < NG; ++q) {
-        const int u = min(u0 + 16 * q + (lane & 15), units - 1);
-        int r0 = u, r1 = u;
-        if (kPaired) unit_rows<EPI>(g, u, r0, r1);
-        Ap[q] = (const bf16_t*)g.W + (size_t)r0 * K + kw * 32 + 8 * (lane >> 4);
-        if (kPaired) Ap[NG + q] = (const bf16_t*)g.W + (size_t)r1 * K + kw * 32 + 8 * (lane >> 4);
-    }
+    for (int q = 0; q < NG; ++q)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int u = min(u0 + 16 * q + 8 * h + (lane >> 3), units - 1);
+            int r0 = u, r1 = u;
+            if (kPaired) unit_rows<EPI>(g, u, r0, r1);
+            Ar[q][h] = (const bf16_t*)g.W + (size_t)r0 * K + kw * 32;
+            if (kPaired) Ar[NG + q][h] = (const bf16_t*)g.W + (size_t)r1 * K + kw * 32;
+        }
+    // this lane's 16-byte chunk of a row line: stored chunk lane % 8 holds
+    // source chunk (lane % 8) ^ row, row % 8 = (lane / 8) % 8; a half round
+    // (64 bytes per row) loads chunks 0..3 and fills the rest with copies
+    const int csrc = (lane & 7) ^ ((lane >> 3) & 7);
+    const uint32_t lds_w = (uint32_t)(uintptr_t)(mfma_lptr_t)(s_lds + wave * 2 * kBuf);
+    auto issue_a = [&](int r, int buf) {
+        const int c = (2 * r + 1 < sw) ? csrc : (csrc & 3);
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                __builtin_amdgcn_global_load_lds((mfma_gptr_t)(Ar[t][h] + 64 * r + 8 * c),
+                                                 (mfma_lptr_t)(s_lds + wave * 2 * kBuf + buf * kBuf +
+                                                               (16 * t + 8 * h) * 128),
+                                                 16, 0, 2 /* nontemporal */);
+    };
+    // fragment (tile t, k-step u of the round): row 16 t + lane % 16, chunk
+    // 4 u + lane / 16, stored at that chunk ^ (row % 8)
+    uint32_t ad[RT][2];
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int i = lane & 15;
+            ad[t][u] = lds_w + (16 * t + i) * 128 + (((4 * u + (lane >> 4)) ^ (i & 7)) * 16);
+        }
 
     for (int j0 = 0; j0 < n; j0 += NT * 16) {   // column groups of NT tiles
         // tiles past the last one re-read the last tile and their sums are
@@ -153,39 +204,51 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
 #pragma unroll
             for (int c = 0; c < NT; ++c) acc[t][c] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-        int s = 0;
-        for (; s + U <= sw; s += U) {
-            bf16x8_t a[U][RT], bv[U][NT];
+        if (j0 > 0) __syncthreads();   // the previous group's epilogue is done with the LDS
+        issue_a(0, 0);
+        for (int r = 0; r < nr; ++r) {
+            const int buf = r & 1;
+            const bool half = 2 * r + 1 >= sw;
+            u32x4_t bv[2][NT];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
+            for (int u = 0; u < 2; ++u)
 #pragma unroll
-                for (int t = 0; t < RT; ++t)
-                    a[u][t] = *reinterpret_cast<const bf16x8_t*>(Ap[t] + 32 * (s + u));
-#pragma unroll
-                for (int c = 0; c < NT; ++c)
-                    bv[u][c] = *reinterpret_cast<const bf16x8_t*>(Bp[c] + 512 * (s + u));
+                for (int c = 0; c < NT; ++c) {
+                    const bf16_t* bp = Bp[c] + 512 * (2 * r + (half ? 0 : u));
+                    // reads data no kernel writes while this one runs: no memory clobber
+                    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(bv[u][c]) : "v"(bp));
+                }
+            if (r + 1 < nr) {
+                issue_a(r + 1, buf ^ 1);
+                __builtin_amdgcn_s_waitcnt(mfma_vmcnt(2 * RT));
+            } else {
+                __builtin_amdgcn_s_waitcnt(mfma_vmcnt(0));
             }
-            __builtin_amdgcn_sched_barrier(0);   // keep every load of the round ahead
+            __builtin_amdgcn_sched_barrier(0);   // nothing reads bv or the LDS round before the wait
+            u32x4_t a[RT][2];
 #pragma unroll
-            for (int u = 0; u < U; ++u)
+            for (int t = 0; t < RT; ++t)
+                asm volatile(
+                    "ds_read_b128 %0, %2\n\t"
+                    "ds_read_b128 %1, %3\n\t"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=&v"(a[t][0]), "=&v"(a[t][1])
+                    : "v"(ad[t][0] + buf * kBuf), "v"(ad[t][1] + buf * kBuf)
+                    : "memory");
+            // a half round's second k-step multiplies zeros (adds exactly 0):
+            // the MFMAs stay unconditional
+            const uint32_t keep = half ? 0u : ~0u;
+#pragma unroll
+            for (int c = 0; c < NT; ++c) bv[1][c] &= keep;
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
 #pragma unroll
                 for (int t = 0; t < RT; ++t)
 #pragma unroll
                     for (int c = 0; c < NT; ++c)
-                        acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][t], bv[u][c],
-                                                                            acc[t][c], 0, 0, 0);
-        }
-        for (; s < sw; ++s) {
-            bf16x8_t a[RT], bv[NT];
-#pragma unroll
-            for (int t = 0; t < RT; ++t) a[t] = *reinterpret_cast<const bf16x8_t*>(Ap[t] + 32 * s);
-#pragma unroll
-            for (int c = 0; c < NT; ++c) bv[c] = *reinterpret_cast<const bf16x8_t*>(Bp[c] + 512 * s);
-#pragma unroll
-            for (int t = 0; t < RT; ++t)
-#pragma unroll
-                for (int c = 0; c < NT; ++c)
-                    acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[t], bv[c], acc[t][c], 0, 0, 0);
+                        acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(bf16x8_t, a[t][u]), __builtin_bit_cast(bf16x8_t, bv[u][c]),
+                            acc[t][c], 0, 0, 0);
         }
 
         // per epilogue group: reduce the four K-slices through LDS, then the
