@@ -239,8 +239,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // Decode attention on MFMA: bf16 cache, head_dim 128, three to kMaxGroup
 // query heads per KV head.  Each wavefront takes 16-row slabs of the chunk
 // (every fourth slab) and keeps an online softmax per head:
-//   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = the slab's K rows (read
-//                 from LDS, below), B = the group's queries as
+//   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = the slab's K rows (loaded
+//                 to registers one slab ahead), B = the group's queries as
 //                 bf16 high + low parts (heads past G are zero), so scores
 //                 keep about 16 bits of the fp32 query;
 //                 D: lane h + 16 r holds rows 4 r .. 4 r + 3 of head h;
@@ -248,12 +248,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 //   O += P V      v_mfma_f32_16x16x16_bf16 with the softmax weights in place
 //                 as the A operand, split into bf16 high + low parts (two
 //                 products, so P keeps about 16 bits), and V[4 rows][col] as
-//                 the B operand from ds_read_b64_tr_b16; O: lane c + 16 r holds heads
+//                 the B operand from ds_read_b64_tr_b16: the wavefront moves
+//                 its slab of V global -> LDS directly (two buffers, the next
+//                 slab's loads in flight), each 256-byte row's 16-byte chunks
+//                 stored at chunk ^ (row % 16); O: lane c + 16 r holds heads
 //                 4 r .. 4 r + 3 of column c of each 16-column tile.
-// The wavefront moves each slab's K and V rows global -> LDS directly, each
-// 256-byte row's 16-byte chunks stored at chunk ^ (row % 16) so that both
-// fragment reads are free of bank conflicts; once a slab's fragments are in
-// registers the next slab's loads go out into the same buffers.
 // The four wavefronts' (max, sum, O) are merged through LDS at the end.
 //   D[i][j] (16 x 16): lane j + 16 (i / 4), element i % 4
 //   x32 A[i][k]: lane i + 16 (k / 8), element k % 8;  B[k][j]: lane j + 16 (k / 8)
@@ -297,20 +296,20 @@ __device__ __forceinline__ constexpr int vmcnt_at_most(int n) {
     return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8);
 }
 
-// Three workgroups per CU: 127 registers (144 with a map; accumulators in
-// VGPRs) and at most 49 KB of LDS each.
+// Three workgroups per CU: 138 registers (accumulators in VGPRs) and at most
+// 49 KB of LDS each.
 // Cache policy of a load: nontemporal (the NT bit of the instruction).  The
-// slab's K and V rows arrive as whole 256-byte rows, 1 KB per instruction,
-// and are read once: loading V nontemporal made the Llama-8B B = 32 launch
-// 6 % faster.
+// slab's V rows arrive as whole 256-byte rows, 1 KB per instruction, and are
+// read once: loading them nontemporal made the Llama-8B B = 32 launch 6 %
+// faster; K, fetched 64 bytes of a row per instruction, stays cached (its
+// nontemporal loads were slower).
 constexpr int kCpolNontemporal = 2;
 
 template <int GM, bool MASKED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void attn_mfma_kernel(AttnArgs a) {
     constexpr int HD = 128, KS = HD / 32;
-    constexpr int kSlab = 16 * HD * 2;        // bytes of a 16-row K or V slab
-    __shared__ __attribute__((aligned(16))) char s_k[4][kSlab];   // [wave]
-    __shared__ __attribute__((aligned(16))) char s_v[4][kSlab];
+    constexpr int kSlab = 16 * HD * 2;        // bytes of a 16-row V slab
+    __shared__ __attribute__((aligned(16))) char s_v[4][2][kSlab];   // [wave][buffer]
     __shared__ float s_acc[4][GM][HD + 2];
     const int i = blockIdx.z;
     if (!a.rows.exact && i >= *a.rows.cnt) return;
@@ -357,7 +356,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     // holds V[4 r .. 4 r + 3][c]): source lane s = lane % 16 addresses row
     // 4 r + s / 4, columns 16 dt + 4 (s % 4) .. + 3, stored in chunk
     // (column / 8) ^ row
-    const uint32_t lds_w = (uint32_t)(uintptr_t)(attn_lptr_t)&s_v[wave][0];
+    const uint32_t lds_w = (uint32_t)(uintptr_t)(attn_lptr_t)&s_v[wave][0][0];
     uint32_t vad[8];
     {
         const int rr = 4 * lg + (li >> 2), cin = 4 * (li & 3);
@@ -374,74 +373,62 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) o[dt] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-    // a slab: its K and V rows global -> LDS, nontemporal (rows clamped to a
-    // valid row, masked below; lane L of load ld lands at row 4 ld + L / 16,
-    // stored chunk L % 16, which holds source chunk (L % 16) ^ row), and with
-    // a map its map entries.  One buffer each: the next slab's loads are
-    // issued once this slab's fragments are in registers, and overlap its
-    // arithmetic.  All slab loads are direct-to-LDS with explicit waits and
-    // the LDS reads are asm, so the compiler adds no waits of its own (with
-    // a map, its map loads are the compiler's).
+    // a slab: its K fragments to registers (rows clamped to a valid row,
+    // masked below), with a map its map entries, then its V rows global ->
+    // LDS buffer `buf` (lane L of load ld lands at row 4 ld + L / 16, stored
+    // chunk L % 16, which holds source chunk (L % 16) ^ row).  The next
+    // slab's loads are issued once the current scores have used the K
+    // registers.  Without a map the K loads are asm, outside the compiler's
+    // load tracking, which with direct-to-LDS loads pending would wait for
+    // every load before the scores; the waits below cover them (in this
+    // issue order the scores need all but the slab's last 4 loads, its V,
+    // done).  With a map every register load is the compiler's, and so are
+    // their waits.
+    bf16x8_t kf[KS];
     uint8_t en[4];
-    auto load_slab = [&](int jb) {
+    auto load_slab = [&](int jb, int buf) {
+        const int jr = min(jb + li, j1 - 1);
+        const bf16_t* kp = Kb + (size_t)jr * HD + 8 * lg;
+        if constexpr (MASKED) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s) kf[s] = *reinterpret_cast<const bf16x8_t*>(kp + 32 * s);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) en[v] = a.exec[(size_t)slot * a.T + min(jb + 4 * lg + v, j1 - 1)];
+        } else {
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+                u4 r;
+                asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(kp + 32 * s) : "memory");
+                kf[s] = __builtin_bit_cast(bf16x8_t, r);
+            }
+        }
 #pragma unroll
         for (int ld = 0; ld < 4; ++ld) {
             const int rl = 4 * ld + lg;
             const size_t src = (size_t)min(jb + rl, j1 - 1) * HD + ((li ^ rl) * 8);
-            __builtin_amdgcn_global_load_lds((attn_gptr_t)(Kb + src), (attn_lptr_t)(&s_k[wave][ld * 1024]),
-                                             16, 0, kCpolNontemporal);
-            __builtin_amdgcn_global_load_lds((attn_gptr_t)(Vb + src), (attn_lptr_t)(&s_v[wave][ld * 1024]),
-                                             16, 0, kCpolNontemporal);
-        }
-        if constexpr (MASKED) {
-#pragma unroll
-            for (int v = 0; v < 4; ++v) en[v] = a.exec[(size_t)slot * a.T + min(jb + 4 * lg + v, j1 - 1)];
+            __builtin_amdgcn_global_load_lds((attn_gptr_t)(Vb + src),
+                                             (attn_lptr_t)(&s_v[wave][buf][ld * 1024]), 16, 0,
+                                             kCpolNontemporal);
         }
     };
-    // K fragment s (A operand: lane i + 16 kg holds row i, 32 s + 8 kg ..):
-    // stored chunk (4 s + kg) ^ i
-    uint32_t kad[KS];
-    {
-        const uint32_t lds_k = (uint32_t)(uintptr_t)(attn_lptr_t)&s_k[wave][0];
-#pragma unroll
-        for (int s = 0; s < KS; ++s) kad[s] = lds_k + li * 256 + (((4 * s + lg) ^ li) * 16);
-    }
-    if (j0 + 16 * wave < j1) load_slab(j0 + 16 * wave);
-    for (int jb = j0 + 16 * wave; jb < j1; jb += 64) {
-        __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));   // this slab's K, V (and map entries)
-        bf16x8_t kf[KS];
-        {
-            typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-            u4 r0, r1, r2, r3;
-            asm volatile(
-                "ds_read_b128 %0, %4\n\t"
-                "ds_read_b128 %1, %5\n\t"
-                "ds_read_b128 %2, %6\n\t"
-                "ds_read_b128 %3, %7\n\t"
-                "s_waitcnt lgkmcnt(0)"
-                : "=&v"(r0), "=&v"(r1), "=&v"(r2), "=&v"(r3)
-                : "v"(kad[0]), "v"(kad[1]), "v"(kad[2]), "v"(kad[3])
-                : "memory");
-            kf[0] = __builtin_bit_cast(bf16x8_t, r0);
-            kf[1] = __builtin_bit_cast(bf16x8_t, r1);
-            kf[2] = __builtin_bit_cast(bf16x8_t, r2);
-            kf[3] = __builtin_bit_cast(bf16x8_t, r3);
-        }
-        s16x4_t vf[8];
-        read_v_tr<0>(vad, 0, vf);
+    int buf = 0;
+    if (j0 + 16 * wave < j1) load_slab(j0 + 16 * wave, 0);
+    for (int jb = j0 + 16 * wave; jb < j1; jb += 64, buf ^= 1) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_at_most(4));
+        __builtin_amdgcn_sched_barrier(0);   // nothing reads K before the wait
         uint8_t ex[4];
 #pragma unroll
         for (int v = 0; v < 4; ++v) ex[v] = MASKED ? en[v] : 1;
-        const bool more = jb + 64 < j1;
-        if (more) load_slab(jb + 64);
-        __builtin_amdgcn_sched_barrier(0);
-
         f32x4_t d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qh[s], d, 0, 0, 0);
             d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], ql[s], d, 0, 0, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);   // the K registers are free only now
+        const bool more = jb + 64 < j1;
+        if (more) load_slab(jb + 64, buf ^ 1);
         // rows of this lane: jb + 4 lg + v; head li
         float sc[4];
 #pragma unroll
@@ -476,6 +463,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
 #pragma unroll
                 for (int e = 0; e < 4; ++e) o[dt][e] *= ar[e];
         }
+        // this slab's V is in LDS once its four loads are done (the next
+        // slab's K and V loads, 8, and with a map its 4 map loads, may still
+        // be in flight)
+        if (more) __builtin_amdgcn_s_waitcnt(vmcnt_at_most(8));
+        else __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));
+        s16x4_t vf[8];
+        if (buf == 0) read_v_tr<0>(vad, 0, vf);
+        else read_v_tr<kSlab>(vad, 0, vf);
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
             o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ph, vf[dt], o[dt], 0, 0, 0);
