@@ -314,10 +314,21 @@ __device__ __forceinline__ float4 pooled_feature4(const GemvArgs& g, int b, int 
     const int gg = kk / g.hd, e = kk - gg * g.hd;
     const float* pp = g.pool_part + ((size_t)b * g.nkv + gg) * g.pool_max_splits * 2 * g.hd + e;
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int q = 0; q < g.pool_splits; ++q) {
-        for (int w = first; w <= last; ++w) {
-            const float4 t = *reinterpret_cast<const float4*>(pp + ((size_t)q * 2 + w) * g.hd);
+    if (first == last) {
+        // one feature row: the splits' loads are independent, so eight at a
+        // time are in flight; the sum keeps split order
+        const float* p1 = pp + (size_t)first * g.hd;
+#pragma unroll 8
+        for (int q = 0; q < g.pool_splits; ++q) {
+            const float4 t = *reinterpret_cast<const float4*>(p1 + (size_t)q * 2 * g.hd);
             v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
+        }
+    } else {
+        for (int q = 0; q < g.pool_splits; ++q) {
+            for (int w = first; w <= last; ++w) {
+                const float4 t = *reinterpret_cast<const float4*>(pp + ((size_t)q * 2 + w) * g.hd);
+                v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
+            }
         }
     }
     v.x *= inv_n; v.y *= inv_n; v.z *= inv_n; v.w *= inv_n;
