@@ -328,15 +328,18 @@ buddy_status prepare_step(Model& M, const int32_t* pos, const int32_t* k, int B,
 
 // Host-routed launches: spin until the compaction kernel has published the
 // counts of step `seq` to mapped host memory.  A device error, or no answer
-// within a minute, ends the wait with BUDDY_EDEVICE.
+// within a minute, ends the wait with BUDDY_EDEVICE.  The stream is queried
+// for errors every 100 ms only: a query leaves the next kernel launch on the
+// stream 15-20 us slower on the host, and that launch is the one the idle
+// device waits for (a step's route takes about a millisecond).
 buddy_status wait_route(Model& M, int32_t seq, hipStream_t s) {
     volatile int32_t* flag = M.h_cnt + n_mid(M.cfg);
     const auto t0 = std::chrono::steady_clock::now();
-    auto next_check = t0 + std::chrono::milliseconds(1);
+    auto next_check = t0 + std::chrono::milliseconds(100);
     while (*flag != seq) {
         const auto now = std::chrono::steady_clock::now();
         if (now < next_check) continue;
-        next_check = now + std::chrono::milliseconds(1);
+        next_check = now + std::chrono::milliseconds(100);
         hipError_t e = hipStreamQuery(s);
         if (e != hipSuccess && e != hipErrorNotReady) return fail_device(M, e, "route wait");
         if (now - t0 > std::chrono::seconds(60)) {
