@@ -324,8 +324,12 @@ __device__ __forceinline__ float4 pooled_feature4(const GemvArgs& g, int b, int 
             v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
         }
     } else {
+        // K + V: both rows of each split, in split order, four splits' loads
+        // in flight at a time
+#pragma unroll 4
         for (int q = 0; q < g.pool_splits; ++q) {
-            for (int w = first; w <= last; ++w) {
+#pragma unroll
+            for (int w = 0; w < 2; ++w) {
                 const float4 t = *reinterpret_cast<const float4*>(pp + ((size_t)q * 2 + w) * g.hd);
                 v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
             }
