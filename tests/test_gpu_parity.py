@@ -95,6 +95,28 @@ def test_router_context_variants(ctx, dtype):
         print(ctx, dtype, B, rep)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("ctx", ["kv", "k", "v", "k+v"])
+def test_router_context_many_pool_splits(ctx, dtype):
+    """Long contexts at B = 1 and 2: the pool scan splits each KV head's rows
+    into up to 18 position splits, so the router context folds whole groups
+    of splits and a remainder (positions 0, 63, 64, 515, 1023, T - 1)."""
+    T = 1100
+    for B, pos in ((1, [T - 1]), (2, [515, 1023]), (2, [0, 64]), (1, [63])):
+        shape = dict(synth.SHAPES["tiny"], router_ctx=ctx)
+        P = Pair(shape, dtype, T, B, seed=85, omega=0.1)
+        g = torch.Generator().manual_seed(86)
+        hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        h = synth.hidden_inputs(B, P.cfg["d_model"], seed=87)
+        scores = torch.zeros((B, P.L_mid), device="cuda")
+        P.gpu.pool_route(P.upload(hk), P.upload(hv), pos, h.cuda(), scores)
+        got = scores.cpu().numpy()
+        for b in range(B):
+            ref = P.orc.dm_scores(P.orc.context(hk[0, b], hv[0, b], pos[b], h[b].numpy()))
+            assert np.max(np.abs(got[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref)))), (ctx, B, pos)
+
+
 # ------------------------------------------------ multi-step decode parity
 
 def run_teacher_forced(P, prompt, n_decode, ks, report, pool=None):
