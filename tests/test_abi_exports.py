@@ -52,3 +52,13 @@ def test_entry_points_reject_null_handles_without_a_device():
     out = ctypes.c_void_p(1)
     assert L.buddy_model_create(None, None, None, ctypes.byref(out)) == blib.EINVAL
     assert out.value is None
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch, tmp_path):
+    """No fallback: with the shared library absent, the binding raises
+    instead of computing anything."""
+    from paper_2606_09514_amd import lib as blib
+    monkeypatch.setattr(blib, "_SO", str(tmp_path / "libbuddy.so"))
+    monkeypatch.setattr(blib, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        blib.lib()
