@@ -280,7 +280,9 @@ buddy_status buddy_prefill(buddy_model* m, const buddy_kv* kv, float* hidden, in
  *     per-block routed counts (written by the device to mapped pinned host
  *     memory owned by the handle) and launches only the blocks some sequence
  *     runs, with grids sized to the routed rows.  The host blocks until the
- *     first block and the router have run.
+ *     first block and the router have run; a device error during that wait
+ *     is reported (BUDDY_EDEVICE) within about 0.1 s, and no answer within a
+ *     minute also ends it with BUDDY_EDEVICE.
  *   BUDDY_LAUNCH_AUTO (default): host-routed when B <= 16 and not every
  *     sequence runs every block, device-routed otherwise. */
 typedef enum {
