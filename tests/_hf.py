@@ -81,3 +81,81 @@ def hf_routed_masked(model, x: np.ndarray, routes: np.ndarray) -> np.ndarray:
             out = out[0] if isinstance(out, tuple) else out
             h[idx] = out[0]
     return h.numpy()
+
+
+def bf16_round_f64(t: torch.Tensor) -> torch.Tensor:
+    """Round float64 values to the nearest bfloat16 (ties to even) in ONE
+    rounding, returned as float64.  torch converts float64 to bfloat16
+    through float32 (two roundings); the two differ only where the float32
+    value lands exactly halfway between two bfloat16 values although the
+    double did not, and there the side the double lay on decides.  Finite,
+    normal-range inputs only (what the tests feed it)."""
+    t = t.to(torch.float64)
+    f = t.to(torch.float32)
+    out = f.to(torch.bfloat16).to(torch.float64)
+    bits = f.view(torch.int32)
+    tie = ((bits & 0xFFFF) == 0x8000) & (f.to(torch.float64) != t)
+    if bool(tie.any()):
+        lo = (bits & ~0xFFFF).view(torch.float32).to(torch.float64)   # toward zero
+        hi = (bits + 0x8000).view(torch.float32).to(torch.float64)    # away from zero
+        away = t.abs() > f.to(torch.float64).abs()
+        out = torch.where(tie, torch.where(away, hi, lo), out)
+    return out
+
+
+def hf_model_exact(cfg: dict, layers: list, keep: list):
+    """hf_model with float64 arithmetic end to end: rotary angles computed in
+    float64 (HF computes them in float32), RMSNorm in float64 (HF's casts to
+    float32) and attention through torch's scaled_dot_product_attention,
+    whose softmax stays in float64 (HF's eager attention takes the softmax
+    in float32)."""
+    m = hf_model(cfg, layers, keep)
+    eps = float(cfg["rms_eps"])
+
+    def rms64(norm):
+        def fwd(x):
+            return norm.weight * (x * torch.rsqrt(x.pow(2).mean(-1, keepdim=True) + eps))
+        return fwd
+
+    for blk in m.layers:
+        blk.input_layernorm.forward = rms64(blk.input_layernorm)
+        blk.post_attention_layernorm.forward = rms64(blk.post_attention_layernorm)
+    m.config._attn_implementation = "sdpa"
+    for blk in m.layers:
+        blk.self_attn.config._attn_implementation = "sdpa"
+    hd, theta = cfg["head_dim"], float(cfg["rope_theta"])
+    inv = 1.0 / (theta ** (torch.arange(0, hd, 2, dtype=torch.float64) / hd))
+
+    def rope64(x, position_ids):
+        ang = position_ids[..., None].to(torch.float64) * inv
+        emb = torch.cat([ang, ang], dim=-1)
+        return emb.cos(), emb.sin()
+
+    m.rotary_emb.forward = rope64
+    return m
+
+
+def hf_decode_rounded_cache(model, x: np.ndarray, round_kv=bf16_round_f64):
+    """Token-by-token decode of x [T][d] through a KV cache whose new K/V
+    rows (after the rotary embedding) are rounded by round_kv before any
+    attention reads them, as a bf16 cache stores them.  Returns the last
+    block's outputs [T][d] and the cache (per block: K, V [n_kv][T][hd])."""
+    from transformers import DynamicCache
+
+    class RoundedCache(DynamicCache):
+        def update(self, key_states, value_states, layer_idx, *a, **kw):
+            return super().update(round_kv(key_states), round_kv(value_states), layer_idx,
+                                  *a, **kw)
+
+    cache = RoundedCache()
+    outs = []
+    with torch.no_grad():
+        for t in range(x.shape[0]):
+            xt = torch.from_numpy(x[t:t + 1].astype(np.float64))[None]
+            pid = torch.tensor([[t]])
+            out = model(inputs_embeds=xt, position_ids=pid, past_key_values=cache,
+                        use_cache=True, cache_position=torch.tensor([t]))
+            outs.append(out.last_hidden_state[0, 0].numpy())
+    kv = [(cache.layers[i].keys[0].numpy(), cache.layers[i].values[0].numpy())
+          for i in range(len(model.layers))]
+    return np.array(outs), kv

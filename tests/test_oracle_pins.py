@@ -17,7 +17,8 @@ import torch
 from oracle import Oracle, bf16_from_double
 from paper_2606_09514_amd import synth
 
-from _hf import hf_forward, hf_model, hf_routed_masked
+from _hf import (bf16_round_f64, hf_decode_rounded_cache, hf_forward, hf_model,
+                 hf_model_exact, hf_routed_masked)
 
 SMALL = dict(n_layers=6, d_model=64, n_heads=4, n_kv_heads=2, head_dim=16, d_ffn=96,
              dm_hidden=32, dm_act="gelu", rope_theta=1e4, rms_eps=1e-5)
@@ -57,6 +58,126 @@ def test_bf16_rounding_matches_torch():
     got = np.array([bf16_from_double(float(v)) for v in vals], dtype=np.uint16)
     assert np.array_equal(got, ref)
     assert bf16_from_double(float("nan")) & 0x7F80 == 0x7F80
+
+
+def test_single_rounding_helper_matches_oracle_on_doubles():
+    """The tests' double -> bf16 helper (torch's float32 path with the
+    double-rounding case decided by the double) and the oracle's direct
+    rounding agree, including doubles just off a bf16 midpoint, where a
+    float32 intermediate would round the wrong way."""
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(20000) * np.exp2(rng.integers(-20, 20, 20000))
+    # bf16 midpoints nudged by less than a float32 ulp either way
+    mid = (torch.from_numpy(rng.standard_normal(4000).astype(np.float32)).view(torch.int32)
+           & ~0xFFFF | 0x8000).view(torch.float32).to(torch.float64).numpy()
+    x = np.concatenate([x, mid, mid * (1 + 2.0 ** -40), mid * (1 - 2.0 ** -40)])
+    ref = np.array([bf16_from_double(float(v)) for v in x], dtype=np.uint16)
+    got = bf16_round_f64(torch.from_numpy(x)).to(torch.float32).view(torch.int32).numpy()
+    assert np.array_equal(((got >> 16) & 0xFFFF).astype(np.uint16), ref)
+
+
+# --------------------------------------------------------- bf16 KV storage
+#
+# In bf16 mode a block stores the new K row after the rotary embedding and
+# the new V row, each rounded once to bf16, and attention reads the stored
+# (rounded) rows back, the new row included (App. "Background", KV-cache
+# equation; Sec. 5 runs the model in bf16).  Pinned against Hugging Face's
+# projections and rotary embedding in float64.
+
+def _bf16_bits(a):
+    bits = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float64)).to(
+        torch.float32).view(torch.int32).numpy()
+    return ((bits >> 16) & 0xFFFF).astype(np.uint16)
+
+
+@pytest.mark.parametrize("pos", [0, 5])
+def test_bf16_new_kv_row_is_rounded_rotated_projection(pos):
+    from transformers.models.llama.modeling_llama import apply_rotary_pos_emb
+    cfg, layers, dm, orc = make(dtype="bf16")
+    nq, nkv, hd, d = cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"], cfg["d_model"]
+    rng = np.random.default_rng(21)
+    kc, vc = empty_cache(cfg, orc)
+    shp = (nkv, pos, hd)
+    to_bf = lambda a: torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16).view(
+        torch.int16).numpy().view(np.uint16)
+    kc[1][:, :pos], vc[1][:, :pos] = to_bf(rng.standard_normal(shp)), to_bf(rng.standard_normal(shp))
+    before_k, before_v = kc[1].copy(), vc[1].copy()
+    h = rng.standard_normal(d) * 2.0
+    orc.block(1, kc[1], vc[1], pos, h)
+
+    f64 = lambda a: torch.from_numpy((a.astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+    w = layers[1]
+    u = torch.nn.functional.rms_norm(torch.from_numpy(h)[None], (d,), f64(w["attn_norm"]),
+                                     eps=cfg["rms_eps"])
+    wqkv = f64(w["wqkv"])
+    k = torch.nn.functional.linear(u, wqkv[nq * hd:(nq + nkv) * hd]).view(1, nkv, 1, hd)
+    v = torch.nn.functional.linear(u, wqkv[(nq + nkv) * hd:]).view(nkv, hd)
+    inv = 1.0 / (cfg["rope_theta"] ** (torch.arange(0, hd, 2, dtype=torch.float64) / hd))
+    emb = torch.cat([pos * inv, pos * inv])[None, None]
+    _, k_rot = apply_rotary_pos_emb(k, k, emb.cos(), emb.sin())
+    k_rot = k_rot.view(nkv, hd)
+    assert np.array_equal(kc[1][:, pos], _bf16_bits(bf16_round_f64(k_rot).numpy()))
+    assert np.array_equal(vc[1][:, pos], _bf16_bits(bf16_round_f64(v).numpy()))
+    if pos > 0:
+        # rotating after rounding would store other bits for most entries
+        assert not np.array_equal(kc[1][:, pos], _bf16_bits(
+            apply_rotary_pos_emb(bf16_round_f64(k), k, emb.cos(), emb.sin())[0].view(nkv, hd)))
+    # no other row is touched
+    mask = np.ones(cfg["max_ctx"], dtype=bool)
+    mask[pos] = False
+    assert np.array_equal(kc[1][:, mask], before_k[:, mask])
+    assert np.array_equal(vc[1][:, mask], before_v[:, mask])
+
+
+def test_bf16_first_row_attention_returns_the_rounded_v():
+    """With one cached row (position 0) the softmax weight is 1, so each
+    query head's attention output is its KV group's stored V row: the
+    block's output equals Hugging Face's block fed the bf16-rounded V.  The
+    unrounded V is ~1e-3 relative away (bf16 has 8 significant bits), far
+    outside the tolerance."""
+    cfg, layers, dm, orc = make(dtype="bf16")
+    d = cfg["d_model"]
+    hf = hf_model_exact(cfg, layers, [1])
+    x = synth.hidden_inputs(1, d, seed=22).numpy().astype(np.float64) * 3.0
+    kc, vc = empty_cache(cfg, orc)
+    got = orc.block(1, kc[1], vc[1], 0, x[0])
+    ref_r, _ = hf_decode_rounded_cache(hf, x)
+    ref_u, _ = hf_decode_rounded_cache(hf, x, round_kv=lambda t: t)
+    assert relerr(got, ref_r[0]) < 1e-12, relerr(got, ref_r[0])
+    assert relerr(got, ref_u[0]) > 1e-6
+
+
+def _f32_round(t):
+    return t.to(torch.float32).to(torch.float64)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("route", [None, (1, 0, 1, 1)])
+def test_decode_equals_hf_with_storage_rounded_cache(dtype, route):
+    """A sequence (every routable block, or a fixed route, i.e. the dense
+    sub-model) against Hugging Face's float64 token-by-token decode whose
+    cache stores each new K/V row rounded to the storage dtype after the
+    rotary embedding: hidden states to 1e-10 and every stored cache row bit
+    for bit.  In bf16, rounding before the rotary embedding, or attending to
+    the unrounded new row, moves the hidden states by ~1e-6."""
+    cfg, layers, dm, orc = make(dtype=dtype)
+    rnd = bf16_round_f64 if dtype == "bf16" else _f32_round
+    bits = _bf16_bits if dtype == "bf16" else (lambda a: a.astype(np.float32))
+    L, T = cfg["n_layers"], 10
+    keep = list(range(L)) if route is None else [0] + [1 + i for i, r in enumerate(route) if r] + [L - 1]
+    xs = synth.hidden_inputs(T, cfg["d_model"], seed=23).numpy()
+    r = None if route is None else np.array(route, dtype=np.uint8)
+    got, execs, _, (kc, vc) = run_sequence(cfg, orc, xs, k=orc.L_mid if r is None else int(r.sum()),
+                                           route=r)
+    ref, kv = hf_decode_rounded_cache(hf_model_exact(cfg, layers, keep), xs, round_kv=rnd)
+    assert relerr(got, ref) < 1e-10, relerr(got, ref)
+    for j, li in enumerate(keep):
+        assert np.array_equal(kc[li][:, :T], bits(kv[j][0]))
+        assert np.array_equal(vc[li][:, :T], bits(kv[j][1]))
+    # the same sequence with an unrounded cache differs by far more
+    ref_u, _ = hf_decode_rounded_cache(hf_model_exact(cfg, layers, keep), xs,
+                                       round_kv=lambda t: t)
+    assert relerr(ref_u, ref) > (1e-7 if dtype == "bf16" else 1e-14)
 
 
 # ------------------------------------------------------------ block pieces
