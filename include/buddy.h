@@ -284,7 +284,14 @@ buddy_status buddy_prefill(buddy_model* m, const buddy_kv* kv, float* hidden, in
  *     is reported (BUDDY_EDEVICE) within about 0.1 s, and no answer within a
  *     minute also ends it with BUDDY_EDEVICE.
  *   BUDDY_LAUNCH_AUTO (default): host-routed when B <= 16 and not every
- *     sequence runs every block, device-routed otherwise. */
+ *     sequence runs every block, device-routed otherwise, and always
+ *     device-routed while the stream is being captured into a graph.
+ * Under stream capture (hipStreamBeginCapture) an explicit host-routed
+ * policy makes buddy_decode_step and buddy_decode_step_auto return
+ * BUDDY_EINVAL with nothing enqueued, and buddy_prefill, which waits for its
+ * route on the host, always returns BUDDY_EINVAL.  A captured step replays
+ * with the positions and budgets it was captured with (they are kernel
+ * arguments). */
 typedef enum {
     BUDDY_LAUNCH_AUTO = 0,
     BUDDY_LAUNCH_DEVICE_ROUTED = 1,

@@ -351,6 +351,15 @@ buddy_status wait_route(Model& M, int32_t seq, hipStream_t s) {
     return BUDDY_OK;
 }
 
+// Whether the stream is being captured into a graph.
+buddy_status stream_capturing(Model& M, hipStream_t s, bool* capturing) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    const hipError_t e = hipStreamIsCapturing(s, &cs);
+    if (e != hipSuccess) return fail_device(M, e, "capture status");
+    *capturing = cs != hipStreamCaptureStatusNone;
+    return BUDDY_OK;
+}
+
 buddy_status check_step_host(const Model& M, const int32_t* pos, int B, int* max_pos) {
     *max_pos = 0;
     for (int b = 0; b < B; ++b) {
@@ -590,6 +599,11 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
     if (skip_kv == BUDDY_SKIP_KV_MASK && !exec) return BUDDY_EINVAL;
 
     hipStream_t s = (hipStream_t)stream;
+    bool capturing;
+    if ((st = stream_capturing(M, s, &capturing)) != BUDDY_OK) return st;
+    // the host-routed policy waits for the device, which a captured stream
+    // never reaches: refused before anything is enqueued
+    if (choose_host_routed(M.policy, false, B, Lm, capturing) < 0) return BUDDY_EINVAL;
     StepArgs a;
     int pos_u;
     if ((st = prepare_step(M, pos, route_override || predict ? nullptr : k, B, &a, &pos_u, s)) !=
@@ -614,10 +628,8 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
     // launches only the blocks some sequence runs, with exact grids.
     bool all_used = !route_override && !predict;
     for (int b = 0; all_used && b < B; ++b) all_used = k[b] == Lm;
-    bool host_routed = false;
-    if (M.policy == BUDDY_LAUNCH_HOST_ROUTED) host_routed = true;
-    else if (M.policy == BUDDY_LAUNCH_AUTO) host_routed = !all_used && B <= kHostRoutedMaxBatch;
-    host_routed = host_routed && Lm > 0;
+    const int choice = choose_host_routed(M.policy, all_used, B, Lm, capturing);
+    const bool host_routed = choice == 1;
     const int32_t seq = host_routed ? (M.seq = (M.seq + 1) & 0x3fffffff) : -1;
     if ((e = launch_route(M, kv->k, kv->v, exec, predict && !route_override, k_out, nullptr, a,
                           route_override, mask_out, scores_out, false, seq, s)) != hipSuccess)
@@ -752,8 +764,11 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
     if (skip_kv == BUDDY_SKIP_KV_MASK && !exec) return BUDDY_EINVAL;
     tl_launch_events = {nullptr, nullptr};
     buddy_status st;
-    if ((st = ensure_prefill_ws(M, (size_t)B * t_stride)) != BUDDY_OK) return st;
     hipStream_t s = (hipStream_t)stream;
+    bool capturing;
+    if ((st = stream_capturing(M, s, &capturing)) != BUDDY_OK) return st;
+    if (capturing) return BUDDY_EINVAL;     // the prefill waits for its route on the host
+    if ((st = ensure_prefill_ws(M, (size_t)B * t_stride)) != BUDDY_OK) return st;
     hipError_t e;
     // the prompt rewrites the first block's rows of slots 0..B-1: their
     // running pool sums start over

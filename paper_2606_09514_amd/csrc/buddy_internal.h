@@ -155,6 +155,18 @@ inline void launch_main(void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_
 // is used by some sequence).
 constexpr int kHostRoutedMaxBatch = 16;
 
+// Launch policy of the routable blocks of one step: 1 host-routed (the host
+// waits for the route and launches only the blocks in use), 0 device-routed,
+// -1 refused.  A stream being captured into a graph never runs while the
+// host waits, so AUTO then takes the device-routed launches and an explicit
+// host-routed request is refused.  Lm: routable blocks (none: nothing to
+// wait for); all_used: every sequence runs every routable block.
+inline int choose_host_routed(int policy, bool all_used, int B, int Lm, bool capturing) {
+    if (Lm <= 0 || policy == BUDDY_LAUNCH_DEVICE_ROUTED) return 0;
+    if (policy == BUDDY_LAUNCH_HOST_ROUTED) return capturing ? -1 : 1;
+    return !all_used && B <= kHostRoutedMaxBatch && !capturing ? 1 : 0;
+}
+
 struct Model {
     buddy_config cfg;
     TimingHook timing;

@@ -50,6 +50,12 @@ class Pair:
     def L_mid(self):
         return self.orc.L_mid
 
+    @property
+    def path(self):
+        """Projection path the library takes at this batch: the GEMV (fp32
+        activations) up to four sequences or in fp32, the MFMA path beyond."""
+        return "mfma" if self.cfg["dtype"] == "bf16" and self.batch > 4 else "gemv"
+
     def empty_host_cache(self):
         return (np.zeros(self.shape5, dtype=self.sdt), np.zeros(self.shape5, dtype=self.sdt))
 
@@ -69,6 +75,30 @@ def f32(a, sdt):
 
 def relerr(got, ref):
     return float(np.max(np.abs(got - ref)) / max(float(np.max(np.abs(ref))), 1e-30))
+
+
+# New K/V rows in bf16 storage.  Both sides round their own fp32 / double
+# value of the row once to bf16, so where the two unrounded values differ by
+# little the stored values are equal or one bf16 ulp apart.  The unrounded
+# values differ by the hidden state's error carried into the projection,
+# which is a fraction of the row's scale, not of each entry: hence one ulp
+# of the entry plus `rel` times the row's largest magnitude.
+KV_ULP_REL = {"gemv": 1e-4, "mfma": TOL["bf16"]}
+
+
+def bf16_ulp(x):
+    """Spacing of bf16 values at |x| (2^(e-7) for |x| in [2^e, 2^(e+1)))."""
+    ax = np.maximum(np.abs(x).astype(np.float64), 2.0 ** -126)
+    return np.exp2(np.floor(np.log2(ax)) - 7)
+
+
+def kv_row_err(g, r, rel):
+    """Largest violation ratio of |g - r| <= ulp(max(|g|, |r|)) + rel max|r|
+    over a row (<= 1 passes)."""
+    g = g.astype(np.float64)
+    r = r.astype(np.float64)
+    bound = bf16_ulp(np.maximum(np.abs(g), np.abs(r))) + rel * max(float(np.max(np.abs(r))), 1e-30)
+    return float(np.max(np.abs(g - r) / bound))
 
 
 def oracle_step(P, hk, hv, b, pos, k, x, route=None, hx=None):
@@ -139,6 +169,10 @@ def compare_step(P, hk, hv, dk, dv, x, pos, ks, report, hx=None, dx=None, pool=N
                     e = relerr(g, r)
                     report["max_kv_err"] = max(report["max_kv_err"], e)
                     assert e < tol, f"new KV row err {e} (layer {l}, seq {b})"
+                    if P.sdt == np.uint16:
+                        v = kv_row_err(g, r, KV_ULP_REL[P.path])
+                        report["max_kv_ulp_ratio"] = max(report.get("max_kv_ulp_ratio", 0.0), v)
+                        assert v <= 1.0, f"new KV row beyond one bf16 ulp: {v} (layer {l}, seq {b})"
                 else:
                     assert np.all(g == 0) and np.all(r == 0)
         out[b] = h
