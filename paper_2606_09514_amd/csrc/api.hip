@@ -218,7 +218,8 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
     } else {
         attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
         // decode rows on the MFMA path: o goes straight to the O
-        // projection's staging, rounded to bf16 as its staging would
+        // projection's staging, split into bf16 high and low parts as its
+        // staging would
         if (uses_mfma(M, rows, batch, qdim, 0)) a.xb_out = bf.xb;
     }
     a.part = M.ws.part; a.max_chunks = M.ws.max_chunks;
@@ -403,8 +404,7 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
     const size_t din = pooled_dim(c.router_ctx, c.n_kv_heads, hd) + c.d_model;
     const size_t qdim = (size_t)c.n_heads * hd;
     const int max_chunks = kAttnMaxChunks;
-    int max_splits = (c.max_ctx + 63) / 64;
-    if (max_splits > 64) max_splits = 64;
+    const int max_splits = pool_max_splits(c.max_ctx);
     M.ws.max_chunks = max_chunks;
     M.ws.max_pool_splits = max_splits;
     size_t xb_ld = (size_t)c.d_model;
@@ -437,8 +437,9 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
         {(void**)&W.part, Bc * c.n_heads * max_chunks * (hd + 2) * 4},
         {(void**)&W.pool_part, Bc * c.n_kv_heads * max_splits * 2 * hd * 4},
         {(void**)&W.rope, (size_t)c.max_ctx * (hd / 2) * sizeof(float2)},
-        {(void**)&W.xb, ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
-        {(void**)&W.xb2, ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
+        // MFMA staging: high and low bf16 parts of every activation
+        {(void**)&W.xb, 2 * ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
+        {(void**)&W.xb2, 2 * ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
         {(void**)&W.mfma_part, part_elems * 4},
     };
     size_t total = 0;
@@ -699,8 +700,10 @@ buddy_status ensure_prefill_ws(Model& M, size_t rows) {
         {(void**)&M.pf_q, rows * qdim * 4}, {(void**)&M.pf_o, rows * qdim * 4},
         {(void**)&M.pf_m, rows * (size_t)c.d_ffn * 4},
         {(void**)&M.pf_hlast, (size_t)c.max_batch * c.d_model * 4},
-        {(void**)&M.pf_xb, r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
-        {(void**)&M.pf_xb2, r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
+        // staging of the tiled GEMM (bf16) or of the MFMA path for few
+        // prompt tokens (high and low parts)
+        {(void**)&M.pf_xb, 2 * r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
+        {(void**)&M.pf_xb2, 2 * r16 * (size_t)M.ws.xb_ld * sizeof(bf16_t)},
         {(void**)&M.pf_split, 2 * rows * (size_t)c.d_model * 4},
         {(void**)&M.pf_lists, L * rows * 4}, {(void**)&M.pf_len, (size_t)c.max_batch * 4},
         {(void**)&M.pf_groups, L * rows * 8},

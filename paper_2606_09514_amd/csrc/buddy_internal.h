@@ -115,7 +115,7 @@ struct Workspace {
     float* part;         // attention partials [max_batch][n_heads][max_chunks][hd + 2]
     float* pool_part;    // pool partials [max_batch][n_kv][max_pool_splits][2 hd]
     float2* rope;        // [max_ctx][hd/2] (cos, sin) of pos * theta^(-2i/hd)
-    bf16_t* xb;          // [round16(max_batch)][xb_ld] compact bf16 rows (MFMA path)
+    bf16_t* xb;          // [2][round16(max_batch)][xb_ld] MFMA staging, high and low parts
     bf16_t* xb2;         // the same, for the down projection's input
     float* mfma_part;    // K-split partial sums of the MFMA path (see mfma_splits)
     int mfma_part_rows;  // routed rows the partial buffer holds (0: no buffer)
@@ -235,6 +235,23 @@ __device__ __forceinline__ void slot_pos(int b, int tok_T, const int32_t* pos, i
 
 hipError_t launch_setup(const StepArgs& a, const Workspace& ws, hipStream_t s);
 
+// Position splits per (sequence, KV head) of the pool over rows 0..max_pos:
+// about four workgroups per CU to stream the first-layer cache, at least 64
+// rows each, at most max_splits (few enough partials for the fold).
+inline int pool_splits(int B, int nkv, int max_pos, int max_splits) {
+    const int want = (1024 + B * nkv - 1) / (B * nkv);
+    const int by_len = (max_pos + 1 + 63) / 64;
+    int splits = want < by_len ? want : by_len;
+    if (splits < 1) splits = 1;
+    if (splits > max_splits) splits = max_splits;
+    return splits;
+}
+// Most position splits per (sequence, KV head) for a cache of max_ctx rows.
+inline int pool_max_splits(int max_ctx) {
+    const int s = (max_ctx + 63) / 64;
+    return s > 64 ? 64 : s;
+}
+
 // Split sums of the first layer's K/V rows 0..pos; returns the number of
 // splits per (sequence, KV head) in *splits (the Decision Module GEMV folds
 // them, PRO_POOL).
@@ -293,11 +310,12 @@ struct GemvArgs {
     // pooled first-layer features of variant ctx (buddy_router_ctx) built
     // from the pool's split partial sums, then h
     const float* pool_part; int pool_splits, pool_max_splits; const float* h; int d; int ctx;
-    // MFMA path: compact bf16 activation rows [round16(max_batch)][ldxb]
+    // MFMA path: compact activation rows, split high / low bf16 fragments
+    // (xbs_index; the prefill's tiled GEMM: one bf16 fragment, xb_index)
     bf16_t* XB; int ldxb;
-    // EPI_SWIGLU (tiled GEMM and MFMA paths): the outputs as bf16 in
-    // B-operand fragment order with K = f (the next projection's staged
-    // input) instead of Y
+    // EPI_SWIGLU (tiled GEMM and MFMA paths): the outputs in the next
+    // projection's staging order with K = f (its staged input) instead of Y:
+    // xb_index bf16 for the tiled GEMM, xbs_index split for the MFMA path
     bf16_t* xb_out;
 };
 
@@ -307,6 +325,34 @@ struct GemvArgs {
 __host__ __device__ inline size_t xb_index(int i, int k, int K) {
     return ((((size_t)(i >> 4) * (K >> 5) + (k >> 5)) * 64 + (i & 15) + 16 * ((k >> 3) & 3)) << 3) +
            (k & 7);
+}
+
+// Split activations of the decode MFMA path: each value as its bf16
+// rounding (high part) plus the bf16 rounding of the remainder (low part),
+// about 16 significant bits together, so that the bf16 products see the
+// fp32 activations almost exactly (the weights are bf16 already).  Element
+// (row i, column k) of part p (0 high, 1 low) for a K-column input: tile
+// i / 16 and k-step k / 32 hold two contiguous 1 KB fragments, high then
+// low, each in B-operand order (lane (i % 16) + 16 ((k / 8) % 4), element
+// k % 8).
+__host__ __device__ inline size_t xbs_index(int i, int k, int K, int part) {
+    return (((((size_t)(i >> 4) * (K >> 5) + (k >> 5)) * 2 + part) * 64 + (i & 15) +
+             16 * ((k >> 3) & 3)) << 3) + (k & 7);
+}
+
+// Low part of v given its high part's bits: the exact remainder rounded to
+// bf16, 0 where v or its high part is not finite (they then decide alone).
+__device__ __forceinline__ float split_rest(float v, uint32_t hi_bits16) {
+    const float r = v - bf2f(hi_bits16);
+    return (r - r) == 0.f ? r : 0.f;
+}
+
+// Stores v at high-part index `at` (xbs_index with part 0) and its low part
+// one fragment (512 elements) further.
+__device__ __forceinline__ void store_split(bf16_t* xb, size_t at, float v) {
+    const bf16_t hi = f2bf(v);
+    xb[at] = hi;
+    xb[at + 512] = f2bf(split_rest(v, hi));
 }
 
 // Pooled inputs of the router context: 2 n_kv hd for [mean K | mean V],
@@ -405,8 +451,9 @@ struct AttnArgs {
     float* part; int max_chunks;
     const uint8_t* exec;                // this block's execution map [bcap][T], or null
     int tok_T;                          // > 0: rows are prompt tokens (slot_pos)
-    // o of launch row i as bf16 in fragment order (xb_index with K = nq hd),
-    // the O projection's staged input, instead of fp32 o; or null
+    // o of launch row i in the O projection's staging order instead of fp32
+    // o (decode rows: split high / low, xbs_index; prompt tokens of the
+    // prefill attention kernel: bf16, xb_index, with K = nq hd); or null
     bf16_t* xb_out;
     // prompt tokens on the prefill attention kernel: groups of up to 64 / G
     // consecutive tokens of one prompt, (first row index, count) pairs; one

@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         }
         if (a.chunks == 1) {
             const int col = (g * G + h) * a.hd + e;
-            if (a.xb_out) a.xb_out[xb_index(i, col, a.nq * a.hd)] = f2bf(A / L);
+            if (a.xb_out) store_split(a.xb_out, xbs_index(i, col, a.nq * a.hd, 0), A / L);
             else a.o[(size_t)b * a.nq * a.hd + col] = A / L;
         } else {
             float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
@@ -509,7 +509,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
         }
         if (a.chunks == 1) {
             const int col = (g * G + h) * HD + e;
-            if (a.xb_out) a.xb_out[xb_index(i, col, a.nq * HD)] = f2bf(A / L);
+            if (a.xb_out) store_split(a.xb_out, xbs_index(i, col, a.nq * HD, 0), A / L);
             else a.o[(size_t)b * a.nq * HD + col] = A / L;
         } else {
             float* pp = a.part + (((size_t)b * a.nq + g * G + h) * a.max_chunks + c) * pstride;
@@ -792,7 +792,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 #pragma unroll 8
         for (int q = 0; q < a.chunks; ++q) A += pp[q * pstride + e] * s_w[q];
         const int col = head * a.hd + e;
-        if (a.xb_out) a.xb_out[xb_index(i, col, a.nq * a.hd)] = f2bf(A / L);
+        if (a.xb_out) store_split(a.xb_out, xbs_index(i, col, a.nq * a.hd, 0), A / L);
         else a.o[(size_t)b * a.nq * a.hd + col] = A / L;
     }
 }

@@ -2,13 +2,17 @@
 // batches of more than four sequences: the projection is then a real dense
 // contraction over the routed rows.
 //
-//  prep_kernel  writes the routed rows as bf16 in MFMA operand order (row i
-//               of the launch is sequence idx[i]): RMSNorm and gain folded in
-//               (PRO_RMSNORM), the router context built from the pool's split
-//               sums (PRO_POOL), or a plain conversion (PRO_NONE).  Inputs
-//               staged by their producer (PRO_STAGED: the attention output,
-//               the SwiGLU output) skip it.
-//  mfma_kernel  Y = W XB^T with v_mfma_f32_16x16x32_bf16 (fp32 accumulate).
+//  prep_kernel  writes the routed rows in MFMA operand order (row i of the
+//               launch is sequence idx[i]) as bf16 high and low parts
+//               (xbs_index): RMSNorm and gain folded in (PRO_RMSNORM), the
+//               router context built from the pool's split sums (PRO_POOL), or
+//               a plain conversion (PRO_NONE).  Inputs staged by their
+//               producer (PRO_STAGED: the attention output, the SwiGLU output)
+//               skip it.
+//  mfma_kernel  Y = W XB^T with v_mfma_f32_16x16x32_bf16 (fp32 accumulate),
+//               each activation fragment as its high part times W plus its
+//               low part times W, so the fp32 activations enter with about 16
+//               significant bits instead of bf16's 8.
 //               A workgroup owns RT 16-row weight tiles (16 RT rows, or 8 RT
 //               two-row units) and all routed rows; its four wavefronts take
 //               a quarter of K each (of the workgroup's K range when K is
@@ -25,9 +29,10 @@
 //   D[i][j] (16 x 16): lane j + 16 (i / 4), element i % 4
 // One 16-byte load per lane fetches an A tile segment from the row-major
 // weights (16 rows x 64 bytes).  The activations are small and re-read by
-// every workgroup, so they are stored in B-operand order: the B tile of
-// column tile c and k-step s is 1 KB at ((c * K/32 + s) * 64 + lane) * 8
-// elements, one contiguous load per wavefront.
+// every workgroup, so they are stored in B-operand order: the B tiles of
+// column tile c and k-step s are 2 KB at ((c * K/32 + s) * 128 + lane) * 8
+// elements, the high part's 1 KB then the low part's, one contiguous load
+// per wavefront each.
 #include "buddy_internal.h"
 #include "epilogue.h"
 
@@ -84,14 +89,17 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
 #pragma unroll
             for (int q = 0; q < 8; ++q) v[q] *= inv * gv[q];
         }
-        uint4 o;
-        o.x = pack_bf16x2(v[0], v[1]);
-        o.y = pack_bf16x2(v[2], v[3]);
-        o.z = pack_bf16x2(v[4], v[5]);
-        o.w = pack_bf16x2(v[6], v[7]);
-        // B-operand order: tile i / 16, k-step k / 32, lane (i % 16) + 16 (k / 8 % 4)
-        const size_t frag = ((size_t)(i >> 4) * (K >> 5) + (k >> 5)) * 64 + (i & 15) + 16 * ((k >> 3) & 3);
-        *reinterpret_cast<uint4*>(g.XB + frag * 8) = o;
+        // high parts, then the low parts from the exact remainders
+        uint32_t hi[4], lo[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            hi[q] = pack_bf16x2(v[2 * q], v[2 * q + 1]);
+            lo[q] = pack_bf16x2(split_rest(v[2 * q], hi[q] & 0xffffu),
+                                split_rest(v[2 * q + 1], hi[q] >> 16));
+        }
+        const size_t at = xbs_index(i, k, K, 0);
+        *reinterpret_cast<uint4*>(g.XB + at) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+        *reinterpret_cast<uint4*>(g.XB + at + 512) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
     }
 }
 
@@ -196,7 +204,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
         const bf16_t* Bp[NT];
 #pragma unroll
         for (int c = 0; c < NT; ++c)
-            Bp[c] = g.XB + (((size_t)((j0 >> 4) + min(c, nct - 1)) * S + kw) * 64 + lane) * 8;
+            Bp[c] = g.XB + (((size_t)((j0 >> 4) + min(c, nct - 1)) * S + kw) * 128 + lane) * 8;
 
         f32x4_t acc[RT][NT];
 #pragma unroll
@@ -209,14 +217,16 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
         for (int r = 0; r < nr; ++r) {
             const int buf = r & 1;
             const bool half = 2 * r + 1 >= sw;
-            u32x4_t bv[2][NT];
+            u32x4_t bv[2][2][NT];   // [k-step u][high, low][column tile]
 #pragma unroll
             for (int u = 0; u < 2; ++u)
 #pragma unroll
                 for (int c = 0; c < NT; ++c) {
-                    const bf16_t* bp = Bp[c] + 512 * (2 * r + (half ? 0 : u));
+                    const bf16_t* bp = Bp[c] + 1024 * (2 * r + (half ? 0 : u));
                     // reads data no kernel writes while this one runs: no memory clobber
-                    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(bv[u][c]) : "v"(bp));
+                    asm volatile("global_load_dwordx4 %0, %2, off\n\t"
+                                 "global_load_dwordx4 %1, %2, off offset:1024"
+                                 : "=&v"(bv[u][0][c]), "=&v"(bv[u][1][c]) : "v"(bp));
                 }
             if (r + 1 < nr) {
                 issue_a(r + 1, buf ^ 1);
@@ -239,16 +249,21 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
             // the MFMAs stay unconditional
             const uint32_t keep = half ? 0u : ~0u;
 #pragma unroll
-            for (int c = 0; c < NT; ++c) bv[1][c] &= keep;
+            for (int c = 0; c < NT; ++c) {
+                bv[1][0][c] &= keep;
+                bv[1][1][c] &= keep;
+            }
 #pragma unroll
             for (int u = 0; u < 2; ++u)
 #pragma unroll
-                for (int t = 0; t < RT; ++t)
+                for (int p = 0; p < 2; ++p)
 #pragma unroll
-                    for (int c = 0; c < NT; ++c)
-                        acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            __builtin_bit_cast(bf16x8_t, a[t][u]), __builtin_bit_cast(bf16x8_t, bv[u][c]),
-                            acc[t][c], 0, 0, 0);
+                    for (int t = 0; t < RT; ++t)
+#pragma unroll
+                        for (int c = 0; c < NT; ++c)
+                            acc[t][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8_t, a[t][u]),
+                                __builtin_bit_cast(bf16x8_t, bv[u][p][c]), acc[t][c], 0, 0, 0);
         }
 
         // per epilogue group: reduce the four K-slices through LDS, then the
@@ -289,7 +304,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
                     const float v1 = (s_red[0][GT - 1][il][j] + s_red[1][GT - 1][il][j]) +
                                      (s_red[2][GT - 1][il][j] + s_red[3][GT - 1][il][j]);
                     if (EPI == EPI_SWIGLU && g.xb_out) {   // the down projection's staged input
-                        g.xb_out[xb_index(j0 + j, uu, g.f)] = f2bf(swiglu(v0, v1));
+                        store_split(g.xb_out, xbs_index(j0 + j, uu, g.f, 0), swiglu(v0, v1));
                         continue;
                     }
                     int r0, r1;

@@ -117,14 +117,7 @@ hipError_t launch_pool(const Model& M, const void* k0, const void* v0, int B, in
     p.k0 = k0; p.v0 = v0; p.pos = M.ws.pos; p.pos_u = pos_u;
     p.part = M.ws.pool_part;
     p.T = c.max_ctx; p.hd = c.head_dim; p.nkv = c.n_kv_heads; p.max_splits = M.ws.max_pool_splits;
-    // position splits per (sequence, KV head): about four workgroups per CU
-    // to stream the first-layer cache, at least 64 rows each, few enough
-    // partials for the fold
-    int want = (1024 + B * c.n_kv_heads - 1) / (B * c.n_kv_heads);
-    int by_len = (max_pos + 1 + 63) / 64;
-    int splits = want < by_len ? want : by_len;
-    if (splits < 1) splits = 1;
-    if (splits > p.max_splits) splits = p.max_splits;
+    const int splits = pool_splits(B, c.n_kv_heads, max_pos, p.max_splits);
     p.splits = splits;
     *splits_out = splits;
     dim3 grid(splits, c.n_kv_heads, B);
