@@ -187,6 +187,33 @@ buddy_status buddy_pool_route(buddy_model* m, const buddy_kv* kv, const int32_t*
                               const float* h_new, int32_t B, float* scores_out,
                               void* stream);
 
+/* buddy_pool_route for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same planner and Decision Module scores, bit for bit, with
+ * no model handle and no allocation of any kind.  The configuration and the
+ * Decision Module weights come as arguments (cfg as for buddy_model_create;
+ * cfg->max_batch is the batch capacity of the KV cache layout); kv, pos,
+ * h_new, B, scores_out and stream as for buddy_pool_route.  Every buffer
+ * the kernels need beyond the inputs and outputs (positions, pool partial
+ * sums, the Decision Module's hidden activations, scores) lives in a scratch
+ * array of 8 MiB that the library holds once per device for the life of the
+ * process; no part of it needs to start at zero.  That limits a call to
+ * pieces of 4 B bytes (three of them), 4, 4 B L_mid + 4, 4 B dm_hidden and
+ * 8 B n_kv_heads head_dim splits bytes, each rounded up to 256, totalling at
+ * most 8 MiB, where splits, the pool's position splits, is 1 with
+ * kv->pool_sum and otherwise min(ceil(1024 / (B n_kv_heads)),
+ * ceil((max pos + 1) / 64), ceil(max_ctx / 64), 64), at least 1 (e.g. a
+ * Llama-3-8B shape fits any batch up to 256; a 40-KV-head, head_dim 128
+ * shape fits batches up to about 190).  Beyond it the call returns
+ * BUDDY_ECAPACITY and writes nothing.  Calls on one GPU
+ * share its array: calls that overlap on a device (other streams or host
+ * threads) race and must be ordered by the caller.  Errors as for
+ * buddy_model_create and buddy_pool_route; BUDDY_EDEVICE when the scratch
+ * address cannot be obtained on the current device. */
+buddy_status buddy_pool_route_noalloc(const buddy_config* cfg, const buddy_dm_weights* dm,
+                                      const buddy_kv* kv, const int32_t* pos, const float* h_new,
+                                      int32_t B, float* scores_out, void* stream);
+
 /* Deterministic per-row top-k (Eq. 2): mask_out[b][i] = 1 iff layer i is
  * among the k[b] largest of scores[b][0..n) under (score desc, index asc,
  * NaN last).  scores: device [B][n] fp32; k: host [B], 0 <= k[b] <= n;

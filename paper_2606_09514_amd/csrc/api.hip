@@ -9,6 +9,7 @@
 
 #include <atomic>
 #include <chrono>
+#include <mutex>
 #include <new>
 
 #include <vector>
@@ -370,6 +371,36 @@ buddy_status check_step_host(const Model& M, const int32_t* pos, int B, int* max
     return BUDDY_OK;
 }
 
+// Scratch of buddy_pool_route_noalloc, in place of a handle's workspace:
+// one array per device (each device that loads the library holds its own
+// copy at its own address until the process ends).  Host code never uses
+// the array's name as an address; it takes the device address that
+// hipGetSymbolAddress returns for the current device.
+constexpr size_t kNoAllocScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices];
+
+// Device address of `scratch` on the current device, looked up on the first
+// call on that device.
+hipError_t scratch_address(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -513,6 +544,58 @@ buddy_status buddy_pool_route(buddy_model* h, const buddy_kv* kv, const int32_t*
     if ((e = launch_route(M, kv->k, kv->v, nullptr, false, nullptr, nullptr, a, nullptr, nullptr,
                           scores_out, true, -1, s)) != hipSuccess)
         return fail_device(M, e, "scores");
+    return BUDDY_OK;
+}
+
+buddy_status buddy_pool_route_noalloc(const buddy_config* cfg, const buddy_dm_weights* dm,
+                                      const buddy_kv* kv, const int32_t* pos, const float* h_new,
+                                      int32_t B, float* scores_out, void* stream) {
+    buddy_status st = check_config(cfg);
+    if (st != BUDDY_OK) return st;
+    if (!dm || !dm->w1 || !dm->b1 || !dm->w2 || !dm->b2 || !kv_ok(kv)) return BUDDY_EINVAL;
+    if (B == 0) return BUDDY_OK;
+    if (B < 0) return BUDDY_EINVAL;
+    if (B > cfg->max_batch) return BUDDY_ECAPACITY;
+    if (!pos || !h_new || !scores_out) return BUDDY_EINVAL;
+    tl_launch_events = {nullptr, nullptr};   // nothing armed by a failed earlier call
+    // a model without a workspace: the planner's buffers are carved from the
+    // device's scratch array, with the same split count as buddy_pool_route
+    Model M;
+    memset(&M, 0, sizeof(M));
+    M.cfg = *cfg;
+    M.dm = *dm;
+    int max_pos;
+    if ((st = check_step_host(M, pos, B, &max_pos)) != BUDDY_OK) return st;
+    const buddy_config& c = M.cfg;
+    const int max_splits = pool_max_splits(c.max_ctx);
+    // the running-sum pool writes one split
+    const int splits = kv->pool_sum ? 1 : pool_splits(B, c.n_kv_heads, max_pos, max_splits);
+    const size_t Bs = (size_t)B;
+    struct Piece { void** dst; size_t bytes; };
+    Workspace& W = M.ws;
+    Piece pieces[] = {
+        {(void**)&W.pos, Bs * 4}, {(void**)&W.kb, Bs * 4}, {(void**)&W.idx_all, Bs * 4},
+        {(void**)&W.n_all, 4}, {(void**)&W.scores, Bs * n_mid(c) * 4 + 4},
+        {(void**)&W.a, Bs * c.dm_hidden * 4},
+        {(void**)&W.pool_part, Bs * c.n_kv_heads * splits * 2 * c.head_dim * 4},
+    };
+    size_t total = 0;
+    for (const Piece& q : pieces) total += align_up(q.bytes);
+    if (total > kNoAllocScratchBytes) return BUDDY_ECAPACITY;
+    void* base = nullptr;
+    hipError_t e = scratch_address(&base);
+    if (e != hipSuccess) return BUDDY_EDEVICE;
+    size_t off = 0;
+    for (const Piece& q : pieces) { *q.dst = (char*)base + off; off += align_up(q.bytes); }
+    W.max_pool_splits = splits;          // partial stride: this call's split count
+    hipStream_t s = (hipStream_t)stream;
+    StepArgs a;
+    int pos_u;
+    if ((st = prepare_step(M, pos, nullptr, B, &a, &pos_u, s)) != BUDDY_OK) return st;
+    if ((st = run_planner(M, kv, h_new, B, max_pos, pos_u, false, s)) != BUDDY_OK) return st;
+    if (launch_route(M, kv->k, kv->v, nullptr, false, nullptr, nullptr, a, nullptr, nullptr,
+                     scores_out, true, -1, s) != hipSuccess)
+        return BUDDY_EDEVICE;
     return BUDDY_OK;
 }
 

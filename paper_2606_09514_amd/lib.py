@@ -79,6 +79,9 @@ def lib():
         L.buddy_model_destroy.restype = None
         L.buddy_pool_route.argtypes = [vp, P(KV), vp, vp, i32, vp, vp]
         L.buddy_pool_route.restype = C.c_int
+        L.buddy_pool_route_noalloc.argtypes = [P(Config), P(DMWeights), P(KV), vp, vp, i32, vp,
+                                               vp]
+        L.buddy_pool_route_noalloc.restype = C.c_int
         L.buddy_select_topk.argtypes = [vp, vp, i32, i32, vp, vp]
         L.buddy_select_topk.restype = C.c_int
         L.buddy_decode_step.argtypes = [vp, P(KV), vp, vp, vp, i32, i32, vp, vp, vp, vp]
@@ -164,6 +167,42 @@ def select_topk(scores: torch.Tensor, k, mask_out: torch.Tensor, stream=None,
     return rc
 
 
+def _config(cfg: dict, max_batch: int) -> Config:
+    return Config(cfg["n_layers"], cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"],
+                  cfg["head_dim"], cfg["d_ffn"], cfg["dm_hidden"],
+                  ACT_GELU_ERF if cfg["dm_act"] == "gelu" else ACT_SILU,
+                  BF16 if cfg["dtype"] == "bf16" else F32, int(max_batch), cfg["max_ctx"],
+                  float(cfg["rms_eps"]), float(cfg["rope_theta"]),
+                  CTX_BY_NAME[cfg.get("router_ctx", "kv")], int(cfg.get("start_layer", 1)))
+
+
+def _dm_weights(dm: dict, dtype) -> DMWeights:
+    return DMWeights(_dev(dm["w1"], "w1", dtype), _dev(dm["b1"], "b1", dtype),
+                     _dev(dm["w2"], "w2", dtype), _dev(dm["b2"], "b2", dtype),
+                     _dev(dm.get("prior"), "prior", torch.float32), float(dm.get("omega", 0.0)))
+
+
+def pool_route_noalloc(cfg: dict, dm: dict, max_batch: int, k_cache, v_cache, pos, h_new,
+                       scores_out, stream=None, check: bool = True, pool=None) -> int:
+    """buddy_pool_route_noalloc: planner scores without a model handle or any
+    allocation.  cfg as for Model; dm: the Decision Module's device tensors;
+    max_batch: batch capacity of the KV cache layout; pool: running-sum pool
+    state (sums, row counts) or None."""
+    dtype = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
+    c = _config(cfg, max_batch)
+    d = _dm_weights(dm, dtype)
+    ps, pr = pool if pool is not None else (None, None)
+    kv = KV(_dev(k_cache, "k_cache", dtype), _dev(v_cache, "v_cache", dtype), None,
+            _dev(ps, "pool_sum", torch.float32), _dev(pr, "pool_rows", torch.int32))
+    rc = lib().buddy_pool_route_noalloc(C.byref(c), C.byref(d), C.byref(kv), _host_i32(pos),
+                                        _dev(h_new, "h_new", torch.float32), len(pos),
+                                        _dev(scores_out, "scores_out", torch.float32),
+                                        _stream(stream))
+    if check:
+        _raise(rc)
+    return rc
+
+
 class Model:
     """A model handle over caller-owned device weights.
 
@@ -176,12 +215,7 @@ class Model:
     def __init__(self, cfg: dict, weights: dict, max_batch: int):
         self.cfg = dict(cfg)
         self.dtype = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
-        c = Config(cfg["n_layers"], cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"],
-                   cfg["head_dim"], cfg["d_ffn"], cfg["dm_hidden"],
-                   ACT_GELU_ERF if cfg["dm_act"] == "gelu" else ACT_SILU,
-                   BF16 if cfg["dtype"] == "bf16" else F32, int(max_batch), cfg["max_ctx"],
-                   float(cfg["rms_eps"]), float(cfg["rope_theta"]),
-                   CTX_BY_NAME[cfg.get("router_ctx", "kv")], int(cfg.get("start_layer", 1)))
+        c = _config(cfg, max_batch)
         self._c = c
         self._keep = weights
         L = cfg["n_layers"]
@@ -189,10 +223,7 @@ class Model:
         for i, lw in enumerate(weights["layers"]):
             for n, _ in LayerWeights._fields_:
                 setattr(arr[i], n, _dev(lw[n], n, self.dtype))
-        dm = weights["dm"]
-        d = DMWeights(_dev(dm["w1"], "w1", self.dtype), _dev(dm["b1"], "b1", self.dtype),
-                      _dev(dm["w2"], "w2", self.dtype), _dev(dm["b2"], "b2", self.dtype),
-                      _dev(dm.get("prior"), "prior", torch.float32), float(dm.get("omega", 0.0)))
+        d = _dm_weights(weights["dm"], self.dtype)
         h = C.c_void_p()
         rc = lib().buddy_model_create(C.byref(c), arr, C.byref(d), C.byref(h))
         _raise(rc)
