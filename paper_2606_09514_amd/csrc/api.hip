@@ -19,6 +19,7 @@
 using namespace buddy;
 
 thread_local LaunchEvents buddy::tl_launch_events = {nullptr, nullptr};
+thread_local LaunchEvents buddy::tl_merge_events = {nullptr, nullptr};
 
 struct buddy_model {
     Model M;
@@ -126,12 +127,16 @@ bool uses_mfma(const Model& M, const Rows& rows, int batch, int K, int tok_T) {
 // (or fp32 weights), the MFMA path beyond.  The choice depends on the batch,
 // not on how many sequences a block routes, so a sequence's arithmetic does
 // not depend on the routes of the others or on the launch policy.
-hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, hipStream_t s) {
+// fold: the MFMA path's residual add goes to the partial buffer for the next
+// staging to add (the caller has checked that the buffer holds the rows).
+hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, hipStream_t s,
+                       bool fold = false) {
     // prompt tokens of a prefill: the tiled GEMM
     if (uses_gemm(M, g.rows, batch, g.K, g.tok_T))
         return launch_gemm(pro, epi, g, M.gemm_tile, M.pf_split, s);
     if (uses_mfma(M, g.rows, batch, g.K, g.tok_T))
-        return launch_mfma(pro, epi, g, g.rows.n_max <= M.ws.mfma_part_rows ? M.ws.mfma_part : nullptr, s);
+        return launch_mfma(pro, epi, g, g.rows.n_max <= M.ws.mfma_part_rows ? M.ws.mfma_part : nullptr, s,
+                           fold);
     if (pro == PRO_STAGED) return hipErrorInvalidValue;   // staged inputs feed the MFMA paths only
     return launch_gemv(M.cfg.dtype, pro, epi, g, s);
 }
@@ -161,12 +166,13 @@ bool timed(const Model& M, int kind, int l) {
 hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
     if (!timed(M, kind, l)) return hipSuccess;
     const TimingHook& t = M.timing;
+    LaunchEvents& ev = kind == BUDDY_KERNEL_ATTN_MERGE ? tl_merge_events : tl_launch_events;
     if (!stop) {
-        tl_launch_events = {t.start[t.next], t.stop[t.next]};
+        ev = {t.start[t.next], t.stop[t.next]};
         return hipSuccess;
     }
-    if (!tl_launch_events.start) return hipSuccess;
-    tl_launch_events = {nullptr, nullptr};
+    if (!ev.start) return hipSuccess;
+    ev = {nullptr, nullptr};
     hipError_t e = hipEventRecord(t.start[t.next], s);
     return e != hipSuccess ? e : hipEventRecord(t.stop[t.next], s);
 }
@@ -226,15 +232,24 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
     a.part = M.ws.part; a.max_chunks = M.ws.max_chunks;
     a.exec = exec ? exec + (size_t)l * c.max_batch * c.max_ctx : nullptr;
     if ((e = mark(M, BUDDY_KERNEL_ATTENTION, l, false, s)) != hipSuccess ||
+        (e = mark(M, BUDDY_KERNEL_ATTN_MERGE, l, false, s)) != hipSuccess ||
         (e = launch_attention(c.dtype, a, s)) != hipSuccess ||
-        (e = mark(M, BUDDY_KERNEL_ATTENTION, l, true, s)) != hipSuccess)
+        (e = mark(M, BUDDY_KERNEL_ATTENTION, l, true, s)) != hipSuccess ||
+        (e = mark(M, BUDDY_KERNEL_ATTN_MERGE, l, true, s)) != hipSuccess)
         return fail_device(M, e, "attention");
 
-    // h += Wo o
+    // h += Wo o.  Decode rows on the MFMA path with an MFMA gate/up behind:
+    // K is split and the split sums go to the partial buffer, and the gate/up
+    // staging adds them into h before its RMSNorm (no add kernel, a quarter
+    // of the activation re-reads of unsplit 16-row tiles)
+    const bool o_fold = bf.tok_T == 0 && a.xb_out && uses_mfma(M, rows, batch, qdim, 0) &&
+                        uses_mfma(M, rows, batch, c.d_model, 0) && M.ws.mfma_part &&
+                        rows.n_max <= M.ws.mfma_part_rows;
     g.W = w.wo; g.N = c.d_model; g.K = qdim; g.X = bf.o; g.ldx = qdim; g.gain = nullptr;
     g.Y = hidden; g.ldy = c.d_model;
     if ((e = mark(M, BUDDY_KERNEL_O_PROJ, l, false, s)) != hipSuccess ||
-        (e = launch_proj(M, batch, a.xb_out ? PRO_STAGED : PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
+        (e = launch_proj(M, batch, a.xb_out ? PRO_STAGED : PRO_NONE, EPI_ADD, g, s, o_fold)) !=
+            hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_O_PROJ, l, true, s)) != hipSuccess)
         return fail_device(M, e, "o_proj");
 
@@ -248,11 +263,17 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
     g.W = w.wgate_up; g.N = 2 * c.d_ffn; g.K = c.d_model; g.X = hidden; g.ldx = c.d_model;
     g.gain = w.mlp_norm; g.f = c.d_ffn; g.Y = bf.m; g.ldy = c.d_ffn;
     g.xb_out = m_staged ? bf.xb2 : nullptr;
+    if (o_fold) {
+        g.addpart = M.ws.mfma_part;
+        g.addpart_splits = mfma_fold_splits(c.d_model, qdim);
+        g.addpart_cap = rows.n_max;
+    }
     if ((e = mark(M, BUDDY_KERNEL_GATE_UP, l, false, s)) != hipSuccess ||
         (e = launch_proj(M, batch, PRO_RMSNORM, EPI_SWIGLU, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_GATE_UP, l, true, s)) != hipSuccess)
         return fail_device(M, e, "gate_up");
     g.xb_out = nullptr;
+    g.addpart = nullptr;
 
     // h += Wdown m
     g.W = w.wdown; g.N = c.d_model; g.K = c.d_ffn; g.X = bf.m; g.ldx = c.d_ffn;
@@ -450,7 +471,7 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
     const int part_rows = Bc > kGemmMinRows ? (int)Bc : kGemmMinRows;
     if (c.dtype == BUDDY_BF16 && Bc > (size_t)kGemvMaxRows) {
         size_t splits = mfma_splits(EPI_ADD, c.d_model, c.d_ffn);
-        const size_t so = mfma_splits(EPI_ADD, c.d_model, (int)qdim);
+        const size_t so = mfma_fold_splits(c.d_model, (int)qdim);   // the O projection's
         if (so > splits) splits = so;
         if (splits > 1) part_elems = splits * c.d_model * part_rows;
     }
@@ -557,7 +578,7 @@ buddy_status buddy_pool_route_noalloc(const buddy_config* cfg, const buddy_dm_we
     if (B < 0) return BUDDY_EINVAL;
     if (B > cfg->max_batch) return BUDDY_ECAPACITY;
     if (!pos || !h_new || !scores_out) return BUDDY_EINVAL;
-    tl_launch_events = {nullptr, nullptr};   // nothing armed by a failed earlier call
+    tl_launch_events = tl_merge_events = {nullptr, nullptr};   // nothing armed by a failed earlier call
     // a model without a workspace: the planner's buffers are carved from the
     // device's scratch array, with the same split count as buddy_pool_route
     Model M;
@@ -670,7 +691,7 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
     if (B > c.max_batch) return BUDDY_ECAPACITY;
     if (!hidden || !pos || (!k && !route_override && !predict)) return BUDDY_EINVAL;
     if (predict && M.pred.hidden == 0) return BUDDY_EINVAL;
-    tl_launch_events = {nullptr, nullptr};   // nothing armed by a failed earlier step
+    tl_launch_events = tl_merge_events = {nullptr, nullptr};   // nothing armed by a failed earlier step
     int max_pos;
     buddy_status st = check_step_host(M, pos, B, &max_pos);
     if (st != BUDDY_OK) return st;
@@ -848,7 +869,7 @@ buddy_status buddy_prefill(buddy_model* h, const buddy_kv* kv, float* hidden, in
     }
     uint8_t* exec = skip_kv == BUDDY_SKIP_KV_MASK ? kv->exec : nullptr;
     if (skip_kv == BUDDY_SKIP_KV_MASK && !exec) return BUDDY_EINVAL;
-    tl_launch_events = {nullptr, nullptr};
+    tl_launch_events = tl_merge_events = {nullptr, nullptr};
     buddy_status st;
     hipStream_t s = (hipStream_t)stream;
     bool capturing;
@@ -968,7 +989,8 @@ buddy_status buddy_set_gemm_tile(buddy_model* h, int32_t tile) {
 
 buddy_status buddy_set_timing_events(buddy_model* h, int32_t kernel, int32_t layer,
                                      void* const* start, void* const* stop, int32_t n) {
-    if (!h || n < 0 || kernel < BUDDY_KERNEL_QKV || kernel > BUDDY_KERNEL_DOWN) return BUDDY_EINVAL;
+    if (!h || n < 0 || kernel < BUDDY_KERNEL_QKV || kernel > BUDDY_KERNEL_ATTN_MERGE)
+        return BUDDY_EINVAL;
     Model& M = h->M;
     if (layer < 0 || layer >= M.cfg.n_layers) return BUDDY_EINVAL;
     if (n > 0 && (!start || !stop)) return BUDDY_EINVAL;

@@ -137,6 +137,8 @@ struct TimingHook {
 // one launch and cleared by that launch.
 struct LaunchEvents { hipEvent_t start, stop; };
 extern thread_local LaunchEvents tl_launch_events;
+// The same for the attention's chunk-merge launch.
+extern thread_local LaunchEvents tl_merge_events;
 
 template <typename... KArgs, typename... Args>
 inline void launch_main(void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_t lds,
@@ -313,6 +315,11 @@ struct GemvArgs {
     // MFMA path: compact activation rows, split high / low bf16 fragments
     // (xbs_index; the prefill's tiled GEMM: one bf16 fragment, xb_index)
     bf16_t* XB; int ldxb;
+    // PRO_RMSNORM on the MFMA path: K-split partial sums of the preceding
+    // residual-add projection, [split][row capacity][K] by launch row, that
+    // the staging adds into X's rows (in split order, written back) before
+    // the norm; or null
+    const float* addpart; int addpart_splits; int addpart_cap;
     // EPI_SWIGLU (tiled GEMM and MFMA paths): the outputs in the next
     // projection's staging order with K = f (its staged input) instead of Y:
     // xb_index bf16 for the tiled GEMM, xbs_index split for the MFMA path
@@ -400,7 +407,11 @@ hipError_t launch_gemv(int dtype, int pro, int epi, const GemvArgs& g, hipStream
 // MFMA path (bf16 weights, K a multiple of 128): prep of the compact bf16
 // rows, then the MFMA projection with the same epilogues.  part: fp32
 // workspace of mfma_part_elems for the K-split projections.
-hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, float* part, hipStream_t s);
+// fold: for a residual-add projection, K is split per mfma_fold_splits and
+// the split sums go to part by launch row ([split][n_max][N]) for the next
+// staging to add (GemvArgs.addpart), instead of into Y.
+hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, float* part, hipStream_t s,
+                       bool fold = false);
 // The activation staging of the MFMA paths: routed rows as bf16 in B-operand
 // fragment order (g.XB), RMSNorm / router context folded in per pro.
 hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s);
@@ -432,6 +443,22 @@ inline int mfma_splits(int epi, int units, int K) {
     const int grid = (units + 63) / 64;
     if (grid >= kMfmaMinGrid) return 1;
     const int S = K / 32;
+    int splits = 1;
+    for (int c = 2; c <= kMfmaMaxSplits; c *= 2) {
+        if (S % (4 * c) != 0) break;
+        splits = c;
+        if (grid * c >= 256) break;
+    }
+    return splits;
+}
+
+// K splits of a residual-add MFMA projection whose split sums are added by
+// the next projection's staging (no add kernel): 64-row tiles, K split until
+// the grid has 256 workgroups (at most kMfmaMaxSplits, whole rounds of four
+// k-steps per wavefront).  Fixed by the shape alone.
+inline int mfma_fold_splits(int units, int K) {
+    if (K % 32 != 0) return 1;
+    const int grid = (units + 63) / 64, S = K / 32;
     int splits = 1;
     for (int c = 2; c <= kMfmaMaxSplits; c *= 2) {
         if (S % (4 * c) != 0) break;

@@ -56,11 +56,31 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
     const int K = g.K, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     float inv = 1.f;
     if (PRO == PRO_RMSNORM) {
-        const float* x = g.X + (size_t)b * g.ldx;
+        // each thread owns the same 8-element groups here and in the staging
+        // below, so it reads back its own residual writes
+        float* x = const_cast<float*>(g.X) + (size_t)b * g.ldx;   // written only with addpart
         float ss = 0.f;
-        for (int k = tid * 4; k < K; k += 1024) {
-            const float4 v = *reinterpret_cast<const float4*>(x + k);
-            ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        for (int k = tid * 8; k < K; k += 256 * 8) {
+            float4 v0 = *reinterpret_cast<const float4*>(x + k);
+            float4 v1 = *reinterpret_cast<const float4*>(x + k + 4);
+            if (g.addpart) {
+                // the preceding projection's K-split sums, in split order,
+                // then the residual add (as the split-add kernel does it)
+                float4 a0 = make_float4(0.f, 0.f, 0.f, 0.f), a1 = a0;
+                for (int q = 0; q < g.addpart_splits; ++q) {
+                    const float* pp = g.addpart + ((size_t)q * g.addpart_cap + i) * K + k;
+                    const float4 t0 = *reinterpret_cast<const float4*>(pp);
+                    const float4 t1 = *reinterpret_cast<const float4*>(pp + 4);
+                    a0.x += t0.x; a0.y += t0.y; a0.z += t0.z; a0.w += t0.w;
+                    a1.x += t1.x; a1.y += t1.y; a1.z += t1.z; a1.w += t1.w;
+                }
+                v0.x += a0.x; v0.y += a0.y; v0.z += a0.z; v0.w += a0.w;
+                v1.x += a1.x; v1.y += a1.y; v1.z += a1.z; v1.w += a1.w;
+                *reinterpret_cast<float4*>(x + k) = v0;
+                *reinterpret_cast<float4*>(x + k + 4) = v1;
+            }
+            ss += v0.x * v0.x + v0.y * v0.y + v0.z * v0.z + v0.w * v0.w;
+            ss += v1.x * v1.x + v1.y * v1.y + v1.z * v1.z + v1.w * v1.w;
         }
         ss = wave_sum(ss);
         if (lane == 0) s_ss[wave] = ss;
@@ -138,7 +158,8 @@ __host__ __device__ constexpr int mfma_lds_bytes(int rt, int nt, int gt) {
 // explicit (the round's weights, issued a round earlier, and activations
 // are in once no more than the next round's 2 RT weight loads are pending).
 template <int EPI, int NT, int RT>
-__global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_host, float* part) {
+__global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_host, float* part,
+                                                   int fold) {
     constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
     constexpr int GT = kPaired ? 2 : 1;       // weight tiles per epilogue group
     constexpr int NG = RT / GT;               // epilogue groups (16 units or rows each)
@@ -280,6 +301,17 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
                     for (int v = 0; v < 4; ++v)
                         s_red[wave][t][4 * (lane >> 4) + v][c * 16 + (lane & 15)] = acc[q + t * NG][c][v];
             __syncthreads();
+            if (part && fold) {   // K split, by launch row: [split][n_max][units]
+                for (int p = tid; p < 16 * ncols; p += 256) {
+                    const int il = p & 15, j = p >> 4;
+                    const int uu = u0 + 16 * q + il;
+                    if (uu >= units) continue;
+                    part[((size_t)blockIdx.y * g.rows.n_max + j0 + j) * units + uu] =
+                        (s_red[0][0][il][j] + s_red[1][0][il][j]) +
+                        (s_red[2][0][il][j] + s_red[3][0][il][j]);
+                }
+                continue;
+            }
             if (part) {   // K split: the workgroup's sums, row j fastest
                 for (int p = tid; p < 16 * ncols; p += 256) {
                     const int il = p / ncols, j = p - il * ncols;
@@ -354,22 +386,22 @@ __global__ __launch_bounds__(256) void split_add_kernel(GemvArgs g, int units, i
 
 template <int EPI, int RT>
 static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int splits, float* part,
-                                 hipStream_t s) {
+                                 hipStream_t s, int fold = 0) {
     constexpr int per = 16 * (EPI == EPI_SWIGLU || EPI == EPI_QKV ? RT / 2 : RT);
     const dim3 grid((units + per - 1) / per, splits);
     const int tiles = (g.rows.n_max + 15) / 16;
-    if (tiles <= 1) launch_main(mfma_kernel<EPI, 1, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
-    else if (tiles <= 2) launch_main(mfma_kernel<EPI, 2, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
-    else if (tiles <= 3) launch_main(mfma_kernel<EPI, 3, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
-    else if (tiles <= 4) launch_main(mfma_kernel<EPI, 4, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
-    else if (tiles <= 5) launch_main(mfma_kernel<EPI, 5, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
-    else if (tiles <= 6) launch_main(mfma_kernel<EPI, 6, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
+    if (tiles <= 1) launch_main(mfma_kernel<EPI, 1, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
+    else if (tiles <= 2) launch_main(mfma_kernel<EPI, 2, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
+    else if (tiles <= 3) launch_main(mfma_kernel<EPI, 3, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
+    else if (tiles <= 4) launch_main(mfma_kernel<EPI, 4, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
+    else if (tiles <= 5) launch_main(mfma_kernel<EPI, 5, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
+    else if (tiles <= 6) launch_main(mfma_kernel<EPI, 6, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
     else if constexpr (RT <= 2) {
-        if (tiles <= 7) launch_main(mfma_kernel<EPI, 7, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
-        else launch_main(mfma_kernel<EPI, kMfmaMaxTiles, RT>, grid, dim3(256), 0, s, g, units, n_host, part);
+        if (tiles <= 7) launch_main(mfma_kernel<EPI, 7, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
+        else launch_main(mfma_kernel<EPI, kMfmaMaxTiles, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
     }
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || splits == 1) return e;
+    if (e != hipSuccess || splits == 1 || fold) return e;
     if constexpr (EPI == EPI_ADD) {
         const dim3 sg((units + 63) / 64, (g.rows.n_max + 15) / 16);
         if (splits == 2) split_add_kernel<2><<<sg, 256, 0, s>>>(g, units, n_host, part);
@@ -385,8 +417,16 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
 // halve the occupancy); K split per mfma_splits, with 64-row (or, beyond
 // six column tiles, 32-row) tiles
 template <int EPI>
-static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, float* part, hipStream_t s) {
+static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, float* part, hipStream_t s,
+                                  bool fold = false) {
     const bool wide = g.rows.n_max <= 16 * 6;
+    if constexpr (EPI == EPI_ADD) {
+        if (fold) {   // split sums for the next staging to add
+            const int splits = mfma_fold_splits(units, g.K);
+            if (wide) return launch_mfma_nt<EPI, 4>(g, units, n_host, splits, part, s, 1);
+            return launch_mfma_nt<EPI, 2>(g, units, n_host, splits, part, s, 1);
+        }
+    }
     const int splits = part ? mfma_splits(EPI, units, g.K) : 1;
     if (splits > 1) {
         if (wide) return launch_mfma_nt<EPI, 4>(g, units, n_host, splits, part, s);
@@ -410,7 +450,7 @@ hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, float* part, hipStream_t s) {
+hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, float* part, hipStream_t s, bool fold) {
     const int n_host = g.rows.exact ? g.rows.n_max : -1;
     if (pro != PRO_STAGED) {
         hipError_t e = launch_prep(pro, g, s);
@@ -419,7 +459,8 @@ hipError_t launch_mfma(int pro, int epi, const GemvArgs& g, float* part, hipStre
     if (epi == EPI_QKV) return launch_mfma_epi<EPI_QKV>(g, (g.nq + 2 * g.nkv) * (g.hd / 2), n_host, part, s);
     if (epi == EPI_SWIGLU) return launch_mfma_epi<EPI_SWIGLU>(g, g.f, n_host, part, s);
     if (epi == EPI_BIAS_ACT) return launch_mfma_epi<EPI_BIAS_ACT>(g, g.N, n_host, part, s);
-    return launch_mfma_epi<EPI_ADD>(g, g.N, n_host, part, s);
+    if (fold && (!part || pro != PRO_STAGED)) return hipErrorInvalidValue;
+    return launch_mfma_epi<EPI_ADD>(g, g.N, n_host, part, s, fold);
 }
 
 }  // namespace buddy
