@@ -60,7 +60,7 @@ def log(*a):
 
 
 def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, exec_map=None,
-               running_pool=False):
+               running_pool=False, kernel=None):
     """ks: budgets per sequence, or None for budget-free steps (the attached
     Budget Predictor picks them); exec_map: execution map for skipped-KV
     masking, or None for zero-filled skipped KV; running_pool: the planner
@@ -92,8 +92,9 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     for _ in range(warmup):
         step(pos)
         pos += 1
+    kernel = blib.KERNEL_GATE_UP if kernel is None else kernel
     starts, stops = hip.create(steps), hip.create(steps)
-    model.set_timing_events(blib.KERNEL_GATE_UP, kernel_layer, starts, stops)
+    model.set_timing_events(kernel, kernel_layer, starts, stops)
     positions = []
     torch.cuda.synchronize()
     # an event between consecutive steps on the launch stream: the first and
@@ -106,7 +107,7 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
         positions.append([pos] * B)
         pos += 1
     torch.cuda.synchronize()
-    model.set_timing_events(blib.KERNEL_GATE_UP, kernel_layer, [], [])
+    model.set_timing_events(kernel, kernel_layer, [], [])
     total_ms = evs[0].elapsed_time(evs[steps])
     step_ms = np.array([evs[t].elapsed_time(evs[t + 1]) for t in range(steps)])
     kern_ms = [hip.elapsed_ms(a, b) for a, b in zip(starts, stops)]
@@ -153,6 +154,76 @@ def run_prefill(model, cfg, w, dk, dv, ks_list, reps, warmup):
         out[str(k)] = dict(ms_per_prefill=round(ms, 3), tokens_per_s=round(B * n / (ms / 1e3), 1))
         log(f"prefill k={k}: {ms:.2f} ms for {B} x {n} tokens, {B * n / (ms / 1e3):.0f} tokens/s")
     return out
+
+
+KERNEL_KINDS = [("qkv", "KERNEL_QKV"), ("attention", "KERNEL_ATTENTION"),
+                ("attn_merge", "KERNEL_ATTN_MERGE"), ("o_proj", "KERNEL_O_PROJ"),
+                ("gate_up", "KERNEL_GATE_UP"), ("down", "KERNEL_DOWN")]
+
+
+def per_kernel(model, cfg, w, dk, dv, x0, ks, hip, steps=24, warmup=2):
+    """Live launch durations of every kernel of block 0 (which runs every
+    step), from the timing hook's events on the library's stream, against
+    each kernel's algorithmic bytes per launch (attention: the score kernel
+    and the chunk merge together)."""
+    from paper_2606_09514_amd import costmodel
+    from paper_2606_09514_amd import lib as blib
+    us = {}
+    for name, attr in KERNEL_KINDS:
+        r = run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, 0,
+                       kernel=getattr(blib, attr))
+        us[name] = r["kernel_ms"] * 1e3
+    kb = costmodel.kernel_bytes(cfg, w.batch, w.ctx + warmup + steps // 2)
+    out = {}
+    for name in ("qkv", "attention", "o_proj", "gate_up", "down"):
+        t = us[name] + (us["attn_merge"] if name == "attention" else 0.0)
+        gbs = kb[name] / (t / 1e6) / 1e9
+        out[name] = {"us": round(t, 2), "bytes": int(kb[name]), "achieved_gbs": round(gbs, 1),
+                     "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    out["attention"]["score_us"] = round(us["attention"], 2)
+    out["attention"]["merge_us"] = round(us["attn_merge"], 2)
+    block_us = sum(v["us"] for v in out.values())
+    block_bytes = sum(v["bytes"] for v in out.values())
+    out["block"] = {"us": round(block_us, 2), "bytes": int(block_bytes),
+                    "frac": round(block_bytes / (block_us / 1e6) / 1e9 / PEAK_HBM_GBS, 4)}
+    return out
+
+
+def batched_workload(name, warmup, policy):
+    """One batched workload (rerouted every step): its own synthetic model,
+    cache and budgets; tokens/s and the step's HBM fraction."""
+    import torch
+    from paper_2606_09514_amd import lib as blib
+    from paper_2606_09514_amd import synth
+
+    w = synth.WORKLOADS[name]
+    cfg = synth.model_config(w.shape, w.dtype, w.ctx + warmup + w.steps + 1)
+    log(f"generating weights and KV cache for {w.name}")
+    W = synth.model_weights(cfg, seed=0, device="cuda", omega=w.omega)
+    dk, dv = synth.kv_cache(cfg, w.batch, w.ctx, seed=1, device="cuda")
+    x0 = synth.hidden_inputs(w.batch, cfg["d_model"], seed=2, device="cuda")
+    model = blib.Model(cfg, W, max_batch=w.batch)
+    model.set_launch_policy(policy)
+    hip = blib.HipEvents()
+    ks = synth.budgets(w, seed=1) if w.mixed else [w.budgets[0]] * w.batch
+    r = run_budget(model, cfg, w, dk, dv, x0, ks, w.steps, warmup, hip, 0)
+    log(f"{w.name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step "
+        f"(p50 {r['step_ms_p50']:.3f}, p90 {r['step_ms_p90']:.3f}), "
+        f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline")
+    model.close()
+    del model, W, dk, dv, x0
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return {"batch": w.batch, "ctx": w.ctx, "steps": w.steps, "warmup": warmup,
+            "k": "mixed " + "/".join(map(str, w.budgets)) if w.mixed else w.budgets[0],
+            "mean_k": round(r["mean_k"], 2), "tokens_per_s": round(r["tokens_per_s"], 2),
+            "ms_per_step": round(r["ms_per_step"], 4), "step_ms_p50": round(r["step_ms_p50"], 4),
+            "step_ms_p90": round(r["step_ms_p90"], 4), "bytes_per_step": int(r["bytes_per_step"]),
+            "step_hbm_frac": round(r["step_hbm_frac"], 4), "layers_used": r["layers_used"],
+            "distinct_routes": r["distinct_routes"]}
+
+
+BATCHED = ["llama3_8b_b32_ctx4096_mixed", "qwen2_7b_b64_ctx8192", "mha_13b_b96_ctx2048_mixed"]
 
 
 def cpu_baseline(cfg, W, dk, dv, x0, k, ctx, budget_s=12.0):
@@ -213,6 +284,11 @@ def main():
                     help="launch policy of the routable blocks")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a 1 GiB device copy first (HBM counter calibration)")
+    ap.add_argument("--batched", default="all",
+                    help="batched workloads timed after the headline for per_workload: 'all', "
+                         "'none' or a comma list of workload names")
+    ap.add_argument("--no-per-kernel", action="store_true",
+                    help="skip the live per-kernel timing passes of block 0")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: the library runs the decode step on one GPU; "
@@ -302,9 +378,31 @@ def main():
     gate_up_bytes = 2 * f * d * s + w.batch * d * 4 + w.batch * f * 4
     achieved = gate_up_bytes / (head["kernel_ms"] / 1e3) / 1e9
 
+    kernels = None
+    if not args.no_per_kernel and head["ks"] is not None:
+        kernels = per_kernel(model, cfg, w, dk, dv, x0, head["ks"], hip)
+        log("per-kernel (block 0): " + ", ".join(
+            f"{n} {v['us']:.1f} us {v['frac'] * 100:.0f}%" for n, v in kernels.items()))
+
     cpu = None
     if not args.no_cpu_baseline and head["ks"] is not None and args.skip_kv == "zero":
         cpu = cpu_baseline(cfg, W, dk, dv, x0, head["ks"][0], w.ctx)
+
+    policy = {"auto": blib.LAUNCH_AUTO, "device": blib.LAUNCH_DEVICE_ROUTED,
+              "host": blib.LAUNCH_HOST_ROUTED}[args.policy]
+    batched = []
+    if args.batched != "none" and w.name == "llama3_8b_b1_ctx2048" and args.skip_kv == "zero" \
+            and not args.auto_budget and args.router_ctx == "kv" and args.start_layer == 1 \
+            and args.pool == "scan":
+        batched = BATCHED if args.batched == "all" else args.batched.split(",")
+    per_workload = {}
+    if batched:
+        model.close()
+        del model, W, dk, dv, x0
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        for name in batched:
+            per_workload[name] = batched_workload(name, 4, policy)
 
     out = {
         "metric": "routed-decode tokens/s at budget k (1 GPU); % of HBM roofline",
@@ -344,9 +442,12 @@ def main():
                      "kernel": "gemv gate_up+SwiGLU (block 0)",
                      "bytes_per_launch": gate_up_bytes,
                      "launch_us": round(head["kernel_ms"] * 1e3, 2)},
+        "per_kernel": kernels,
+        "per_workload": per_workload or None,
         "cpu_baseline": cpu,
     }
-    model.close()
+    if not batched:
+        model.close()
     print(json.dumps(out), flush=True)
 
 

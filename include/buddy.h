@@ -356,7 +356,10 @@ typedef enum {
     BUDDY_KERNEL_ATTENTION = 1,  /* split-K decode attention                      */
     BUDDY_KERNEL_O_PROJ = 2,     /* output projection + residual                  */
     BUDDY_KERNEL_GATE_UP = 3,    /* RMSNorm + gate/up projection + SwiGLU         */
-    BUDDY_KERNEL_DOWN = 4        /* down projection + residual                    */
+    BUDDY_KERNEL_DOWN = 4,       /* down projection + residual                    */
+    BUDDY_KERNEL_ATTN_MERGE = 5  /* merge of the attention's position-chunk partials
+                                    (no launch when one chunk covers every row:
+                                    the events then mark an empty interval)      */
 } buddy_kernel;
 
 /* Measurement hook.  For the next n calls of buddy_decode_step on this

@@ -95,3 +95,23 @@ def step_bytes(cfg: dict, masks, positions, running_pool: bool = False) -> dict:
     writes = len(positions) * L * row
     return dict(weights=weights, kv=kv, pool=pool, dm=dmw, kv_writes=writes,
                 total=weights + kv + pool + dmw + writes, layers_used=len(used))
+
+
+def kernel_bytes(cfg: dict, n: int, pos: int) -> dict:
+    """Algorithmic bytes of one launch of each decoder-block kernel over n
+    routed rows at position pos: the weight matrix once, the activation rows
+    it reads and writes (fp32), the new K/V rows, and for attention the K/V
+    rows 0..pos of every routed sequence (with its fp32 queries in and
+    outputs out).  'attention' covers the score kernel and the chunk merge
+    together: the merge's partials are not algorithmic bytes."""
+    d, nq, nkv, hd, f = (cfg["d_model"], cfg["n_heads"], cfg["n_kv_heads"],
+                         cfg["head_dim"], cfg["d_ffn"])
+    s = _s(cfg["dtype"])
+    qdim = nq * hd
+    return dict(
+        qkv=(nq + 2 * nkv) * hd * d * s + n * d * 4 + n * qdim * 4 + n * 2 * nkv * hd * s,
+        attention=n * 2 * nkv * hd * (pos + 1) * s + 2 * n * qdim * 4,
+        o_proj=d * qdim * s + n * qdim * 4 + 2 * n * d * 4,
+        gate_up=2 * f * d * s + n * d * 4 + n * f * 4,
+        down=d * f * s + n * f * 4 + 2 * n * d * 4,
+    )

@@ -847,7 +847,14 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.chunks == 1) return hipSuccess;   // the score kernel wrote o
-    attn_combine_kernel<<<dim3(a.nq, a.rows.n_max), 256, 0, s>>>(a);
+    LaunchEvents& ev = tl_merge_events;
+    if (ev.start) {
+        hipExtLaunchKernelGGL(attn_combine_kernel, dim3(a.nq, a.rows.n_max), dim3(256), 0, s,
+                              ev.start, ev.stop, 0, a);
+        ev.start = ev.stop = nullptr;
+    } else {
+        attn_combine_kernel<<<dim3(a.nq, a.rows.n_max), 256, 0, s>>>(a);
+    }
     return hipGetLastError();
 }
 

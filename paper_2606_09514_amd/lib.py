@@ -23,7 +23,7 @@ PRIOR_DELTA_PPL, PRIOR_TAYLOR, PRIOR_COSINE = 0, 1, 2
 CTX_BY_NAME = {"kv": CTX_KV, "k": CTX_K, "v": CTX_V, "k+v": CTX_K_PLUS_V}
 LAUNCH_AUTO, LAUNCH_DEVICE_ROUTED, LAUNCH_HOST_ROUTED = 0, 1, 2
 GEMM_TILE_AUTO, GEMM_TILE_128, GEMM_TILE_256, GEMM_TILE_256_SPLIT = 0, 1, 2, 3
-KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN = range(5)
+KERNEL_QKV, KERNEL_ATTENTION, KERNEL_O_PROJ, KERNEL_GATE_UP, KERNEL_DOWN, KERNEL_ATTN_MERGE = range(6)
 
 
 class Config(C.Structure):

@@ -53,3 +53,17 @@ def test_step_bytes_counts_union_of_routes():
     # two sequences with disjoint routes use every layer once
     r2 = cm.step_bytes(cfg, [[1] * 15 + [0] * 15, [0] * 15 + [1] * 15], [10, 20])
     assert r2["layers_used"] == 32 and r2["weights"] == 32 * W
+
+
+def test_kernel_bytes_cover_the_block_weights():
+    """The per-kernel algorithmic bytes hold each weight matrix once: their
+    weight parts sum to a block's weights without the two norm gains, and
+    attention scales with the attended rows."""
+    cfg = synth.model_config("llama3_8b", "bf16", 4096)
+    kb0 = cm.kernel_bytes(cfg, 0, 0)
+    weights = kb0["qkv"] + kb0["o_proj"] + kb0["gate_up"] + kb0["down"]
+    assert weights == cm.layer_weight_bytes(cfg) - 2 * cfg["d_model"] * 2
+    a1 = cm.kernel_bytes(cfg, 1, 2047)["attention"]
+    a2 = cm.kernel_bytes(cfg, 2, 2047)["attention"]
+    assert a2 == 2 * a1
+    assert a1 == 2 * 8 * 128 * 2048 * 2 + 2 * 4096 * 4
