@@ -92,6 +92,8 @@ def lib():
                                       vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, dp]
         L.orc_prefill_seq.restype = C.c_int
         L.orc_prior_normalize.argtypes = [vp, i32, i32, C.c_double, vp]
+        L.orc_group_by_route.argtypes = [vp, i32, i32, vp, vp]
+        L.orc_group_by_route.restype = i32
         L.orc_context_dim.argtypes = [C.POINTER(_Config)]
         L.orc_context_dim.restype = C.c_int
         L.orc_router_context.argtypes = [C.POINTER(_Config), vp, vp, i32, vp, vp]
@@ -126,6 +128,19 @@ def prior_normalize(raw, kind: int, winsor: float = 0.0):
     out = np.empty(r.shape[0], dtype=np.float64)
     lib().orc_prior_normalize(_ptr(r), int(r.shape[0]), int(kind), float(winsor), _ptr(out))
     return out
+
+
+def group_by_route(mask):
+    """Batch-level path grouping of mask [B][n] (nonzero = run): (perm [B],
+    starts [n_groups + 1]) as int32 arrays."""
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    B, n = m.shape
+    perm = np.zeros(max(B, 1), dtype=np.int32)
+    starts = np.zeros(B + 1, dtype=np.int32)
+    g = lib().orc_group_by_route(_ptr(m), int(B), int(n), _ptr(perm), _ptr(starts))
+    if g < 0:
+        raise ValueError("oracle rejected the arguments")
+    return perm[:B], starts[:g + 1]
 
 
 def num_threads() -> int:

@@ -228,6 +228,49 @@ void orc_prior_normalize(const double* raw, int32_t n, int32_t kind, double wins
     for (int32_t l = 0; l < n; ++l) out[l] = (out[l] - mu) / (sigma + 1e-6);
     free(x); free(s); free(kz);
 }
+/* ------------------------------------------------------- path grouping */
+
+/* Batch-level path grouping (the Conclusion names grouping requests by their
+ * path among the open questions of path and KV handling): the sequences of a
+ * batch are ordered by route and those with identical routes form a group.
+ * A route is a sequence's mask row over the routable blocks, read as run
+ * (nonzero byte) or skip (zero); routes compare lexicographically in block
+ * order with skip before run, and sequences with equal routes keep their
+ * batch order (a stable sort).  Reading: the paper gives no order; this one
+ * is fixed so that the result is unique. */
+static int route_before(const uint8_t* mask, int32_t n, int32_t a, int32_t b)
+{
+    for (int32_t i = 0; i < n; ++i) {
+        const int ra = mask[(size_t)a * n + i] != 0, rb = mask[(size_t)b * n + i] != 0;
+        if (ra != rb) return ra < rb;
+    }
+    return a < b;
+}
+
+int32_t orc_group_by_route(const uint8_t* mask, int32_t B, int32_t n, int32_t* perm,
+                           int32_t* starts)
+{
+    if (B < 0 || n < 1) return -1;
+    /* insertion sort of the sequence indices: plain and stable */
+    for (int32_t b = 0; b < B; ++b) {
+        int32_t j = b;
+        while (j > 0 && route_before(mask, n, b, perm[j - 1])) {
+            perm[j] = perm[j - 1];
+            --j;
+        }
+        perm[j] = b;
+    }
+    int32_t groups = 0;
+    for (int32_t i = 0; i < B; ++i) {
+        int same = i > 0;
+        for (int32_t k = 0; same && k < n; ++k)
+            same = (mask[(size_t)perm[i] * n + k] != 0) == (mask[(size_t)perm[i - 1] * n + k] != 0);
+        if (!same) starts[groups++] = i;
+    }
+    starts[groups] = B;
+    return groups;
+}
+
 int orc_num_threads(void)
 {
 #ifdef _OPENMP

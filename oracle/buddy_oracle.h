@@ -195,6 +195,14 @@ void orc_prior_normalize(const double* raw, int32_t n, int32_t kind, double wins
                          double* out);
 
 /* Number of OpenMP threads the oracle uses. */
+/* Batch-level path grouping: perm [B] receives the sequences ordered by
+ * route (mask [B][n], nonzero = run; lexicographic over blocks, skip before
+ * run, ties in batch order); starts [B + 1] the first position of each group
+ * of identical routes, then B.  Returns the number of groups (-1 on bad
+ * arguments). */
+int32_t orc_group_by_route(const uint8_t* mask, int32_t B, int32_t n, int32_t* perm,
+                           int32_t* starts);
+
 int orc_num_threads(void);
 
 #ifdef __cplusplus

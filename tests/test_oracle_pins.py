@@ -769,3 +769,33 @@ def test_start_layer_prefill_route_from_block_s_minus_1():
     assert np.allclose(sc, s_ref, rtol=1e-6, atol=1e-7)
     keep = [0, 1] + [2 + i for i in range(orc.L_mid) if mask[i]] + [L - 1]
     assert relerr(h, hf_forward(hf_model(cfg, layers, keep), xs)) < 1e-5
+
+
+# ------------------------------------------------- batch-level path grouping
+
+def test_group_by_route_matches_sorted():
+    """Path grouping against Python's stable sort on (route, index), with
+    routes read as run / skip, and groups as maximal runs of equal routes;
+    many duplicate routes, bytes other than 0 and 1, one routable block."""
+    from oracle import group_by_route
+    rng = np.random.default_rng(31)
+    for trial in range(200):
+        B = int(rng.integers(1, 70))
+        n = int(rng.integers(1, 12)) if trial % 10 else 1
+        # few distinct routes so that groups have several members
+        pool = rng.integers(0, 2, size=(int(rng.integers(1, 6)), n)).astype(np.uint8)
+        m = pool[rng.integers(0, len(pool), size=B)].copy()
+        m[m == 1] = rng.choice(np.array([1, 7, 255], np.uint8), size=int((m == 1).sum()))
+        perm, starts = group_by_route(m)
+        key = lambda b: (tuple(int(v != 0) for v in m[b]), b)
+        ref = sorted(range(B), key=key)
+        assert perm.tolist() == ref
+        routes = [key(b)[0] for b in ref]
+        ref_starts = [i for i in range(B) if i == 0 or routes[i] != routes[i - 1]] + [B]
+        assert starts.tolist() == ref_starts
+    # degenerate cases: every route equal (one group), every route distinct
+    perm, starts = group_by_route(np.ones((5, 3), np.uint8))
+    assert perm.tolist() == [0, 1, 2, 3, 4] and starts.tolist() == [0, 5]
+    m = np.array([[1, 1], [0, 1], [1, 0], [0, 0]], np.uint8)
+    perm, starts = group_by_route(m)
+    assert perm.tolist() == [3, 1, 2, 0] and starts.tolist() == [0, 1, 2, 3, 4]
