@@ -119,6 +119,22 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     total_bytes = sum(s["total"] for s in step_bytes)
     assert all(int(m[t, b].sum()) == kk[t, b] for t in range(steps) for b in range(B))
     distinct = len({m[t].tobytes() for t in range(steps)})
+    # batch-level path grouping of every timed step's executed routes (after
+    # the timed region): groups of identical routes, and the block runs that
+    # serving each group as its own sub-batch would take (k + 2 blocks per
+    # group) against the blocks the per-block compaction runs
+    groups, per_path = [], []
+    if B > 1:
+        perm = torch.empty(B, dtype=torch.int32, device="cuda")
+        starts = torch.empty(B + 1, dtype=torch.int32, device="cuda")
+        ng = torch.empty(1, dtype=torch.int32, device="cuda")
+        for t in range(steps):
+            blib.group_by_route(masks[t], perm, starts, ng)
+            g = int(ng.item())
+            st = starts[:g + 1].cpu().numpy()
+            first = perm.cpu().numpy()[st[:-1]]
+            groups.append(g)
+            per_path.append(int(sum(int(m[t, b].sum()) + 2 for b in first)))
     return dict(ks=ks, total_ms=total_ms, ms_per_step=total_ms / steps,
                 step_ms_p50=float(np.percentile(step_ms, 50)),
                 step_ms_p90=float(np.percentile(step_ms, 90)),
@@ -127,7 +143,9 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
                 step_hbm_frac=total_bytes / (total_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
                 layers_used=sum(s["layers_used"] for s in step_bytes) / steps,
                 distinct_routes=distinct, kernel_ms=sum(kern_ms) / len(kern_ms),
-                mean_k=float(kk.mean()), hidden=hidden, end_pos=pos)
+                mean_k=float(kk.mean()), hidden=hidden, end_pos=pos,
+                route_groups=float(np.mean(groups)) if groups else None,
+                per_path_blocks=float(np.mean(per_path)) if per_path else None)
 
 
 def run_prefill(model, cfg, w, dk, dv, ks_list, reps, warmup):
@@ -220,7 +238,10 @@ def batched_workload(name, warmup, policy):
             "ms_per_step": round(r["ms_per_step"], 4), "step_ms_p50": round(r["step_ms_p50"], 4),
             "step_ms_p90": round(r["step_ms_p90"], 4), "bytes_per_step": int(r["bytes_per_step"]),
             "step_hbm_frac": round(r["step_hbm_frac"], 4), "layers_used": r["layers_used"],
-            "distinct_routes": r["distinct_routes"]}
+            "distinct_routes": r["distinct_routes"],
+            "path_grouping": {"route_groups_per_step": r["route_groups"],
+                              "block_runs_per_path_sub_batches": r["per_path_blocks"],
+                              "block_runs_per_block_compaction": r["layers_used"]}}
 
 
 BATCHED = ["llama3_8b_b32_ctx4096_mixed", "qwen2_7b_b64_ctx8192", "mha_13b_b96_ctx2048_mixed"]

@@ -222,6 +222,20 @@ buddy_status buddy_pool_route_noalloc(const buddy_config* cfg, const buddy_dm_we
 buddy_status buddy_select_topk(const float* scores, const int32_t* k, int32_t B, int32_t n,
                                uint8_t* mask_out, void* stream);
 
+/* Batch-level path grouping (the Conclusion names grouping requests by
+ * their path among its open questions): orders the B sequences of a batch
+ * by route and marks the groups of identical routes, e.g. to serve each
+ * group as one sub-batch with route_override.  mask: device [B][n] uint8,
+ * nonzero = the block runs (as buddy_decode_step's mask_out); routes
+ * compare lexicographically in block order with a skipped block before a
+ * run one, and equal routes keep their batch order, so the result is
+ * unique.  perm_out: device int32 [B], the sequence at each position;
+ * starts_out: device int32 [B + 1], the first position of group g at
+ * [g] and B after the last group; n_groups_out: device int32 [1].
+ * 1 <= n <= 255, B <= 1024; B = 0 is a no-op.  Needs no model handle. */
+buddy_status buddy_group_by_route(const uint8_t* mask, int32_t B, int32_t n, int32_t* perm_out,
+                                  int32_t* starts_out, int32_t* n_groups_out, void* stream);
+
 /* One budget-routed decode step for B sequences (steps 1-6 above).
  *   hidden: device [B][d] fp32; input H_0 of the new token, overwritten
  *           with the last block's output H_L (no final norm).

@@ -674,6 +674,17 @@ buddy_status buddy_select_topk(const float* scores, const int32_t* k, int32_t B,
     return e == hipSuccess ? BUDDY_OK : BUDDY_EDEVICE;
 }
 
+buddy_status buddy_group_by_route(const uint8_t* mask, int32_t B, int32_t n, int32_t* perm_out,
+                                  int32_t* starts_out, int32_t* n_groups_out, void* stream) {
+    if (B == 0) return BUDDY_OK;
+    if (!mask || !perm_out || !starts_out || !n_groups_out || B < 0 || B > kMaxGroupBatch ||
+        n < 1 || n > 255)
+        return BUDDY_EINVAL;
+    hipError_t e = launch_group_by_route(mask, B, n, perm_out, starts_out, n_groups_out,
+                                         (hipStream_t)stream);
+    return e == hipSuccess ? BUDDY_OK : BUDDY_EDEVICE;
+}
+
 namespace {
 
 // One decode step: budgets from k, or from the Budget Predictor (predict),

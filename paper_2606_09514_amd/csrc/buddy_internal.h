@@ -290,6 +290,11 @@ hipError_t launch_gather_last(const float* hidden, int t_stride, int d, const in
                               float* out, hipStream_t s);
 hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B, int n,
                               uint8_t* mask_out, hipStream_t s);
+// Batch-level path grouping (buddy_group_by_route), B <= kMaxGroupBatch,
+// 1 <= n <= 256.
+constexpr int kMaxGroupBatch = 1024;
+hipError_t launch_group_by_route(const uint8_t* mask, int B, int n, int32_t* perm, int32_t* starts,
+                                 int32_t* n_groups, hipStream_t s);
 
 enum Pro { PRO_NONE = 0, PRO_RMSNORM = 1, PRO_POOL = 2, PRO_STAGED = 3 };
 // PRO_STAGED (tiled GEMM and MFMA paths): the input rows are already in XB,

@@ -492,6 +492,80 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* scores, uint8_t*
     }
 }
 
+// ------------------------------------------------------- path grouping
+
+// One workgroup orders the batch by route: each sequence's route (mask row,
+// nonzero = run) is packed into four 64-bit words, block 0 in the top bit of
+// word 0, so that comparing the words as unsigned numbers in order compares
+// routes lexicographically with skip before run; a sequence's position is
+// the count of (route, index) keys below its own, which is unique.  Groups
+// start where the route differs from the previous position's (flags, then a
+// scan in LDS).
+__global__ __launch_bounds__(1024) void group_kernel(const uint8_t* mask, int B, int n, int32_t* perm,
+                                                     int32_t* starts, int32_t* n_groups) {
+    __shared__ uint64_t s_key[kMaxGroupBatch][4];
+    __shared__ int32_t s_perm[kMaxGroupBatch];
+    __shared__ int32_t s_scan[kMaxGroupBatch];
+    const int t = threadIdx.x;
+    if (t < B) {
+        uint64_t w[4] = {0, 0, 0, 0};
+        const uint8_t* row = mask + (size_t)t * n;
+        for (int i = 0; i < n; ++i)
+            if (row[i]) w[i >> 6] |= 1ull << (63 - (i & 63));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s_key[t][q] = w[q];
+    }
+    __syncthreads();
+    if (t < B) {
+        const uint64_t k0 = s_key[t][0], k1 = s_key[t][1], k2 = s_key[t][2], k3 = s_key[t][3];
+        int rank = 0;
+        for (int b = 0; b < B; ++b) {
+            const uint64_t o0 = s_key[b][0], o1 = s_key[b][1], o2 = s_key[b][2], o3 = s_key[b][3];
+            bool below;
+            if (o0 != k0) below = o0 < k0;
+            else if (o1 != k1) below = o1 < k1;
+            else if (o2 != k2) below = o2 < k2;
+            else if (o3 != k3) below = o3 < k3;
+            else below = b < t;
+            rank += below;
+        }
+        s_perm[rank] = t;
+        perm[rank] = t;
+    }
+    __syncthreads();
+    int flag = 0;
+    if (t < B) {
+        const int a = s_perm[t];
+        flag = t == 0;
+        if (t > 0) {
+            const int p = s_perm[t - 1];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) flag |= s_key[a][q] != s_key[p][q];
+        }
+    }
+    // inclusive scan of the flags: group index + 1 at each position
+    if (t < kMaxGroupBatch) s_scan[t] = flag;
+    __syncthreads();
+    for (int off = 1; off < kMaxGroupBatch; off <<= 1) {
+        const int v = t < kMaxGroupBatch && t >= off ? s_scan[t - off] : 0;
+        __syncthreads();
+        if (t < kMaxGroupBatch) s_scan[t] += v;
+        __syncthreads();
+    }
+    if (t < B && flag) starts[s_scan[t] - 1] = t;
+    if (t == 0) {
+        const int g = B > 0 ? s_scan[B - 1] : 0;
+        starts[g] = B;
+        *n_groups = g;
+    }
+}
+
+hipError_t launch_group_by_route(const uint8_t* mask, int B, int n, int32_t* perm, int32_t* starts,
+                                 int32_t* n_groups, hipStream_t s) {
+    group_kernel<<<1, kMaxGroupBatch, 0, s>>>(mask, B, n, perm, starts, n_groups);
+    return hipGetLastError();
+}
+
 hipError_t launch_select_topk(const float* scores, const int32_t* k_host, int B, int n,
                               uint8_t* mask_out, hipStream_t s) {
     for (int r0 = 0; r0 < B; r0 += kMaxBatch) {

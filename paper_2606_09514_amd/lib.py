@@ -84,6 +84,8 @@ def lib():
         L.buddy_pool_route_noalloc.restype = C.c_int
         L.buddy_select_topk.argtypes = [vp, vp, i32, i32, vp, vp]
         L.buddy_select_topk.restype = C.c_int
+        L.buddy_group_by_route.argtypes = [vp, i32, i32, vp, vp, vp, vp]
+        L.buddy_group_by_route.restype = C.c_int
         L.buddy_decode_step.argtypes = [vp, P(KV), vp, vp, vp, i32, i32, vp, vp, vp, vp]
         L.buddy_decode_step.restype = C.c_int
         L.buddy_set_launch_policy.argtypes = [vp, i32]
@@ -198,6 +200,20 @@ def pool_route_noalloc(cfg: dict, dm: dict, max_batch: int, k_cache, v_cache, po
                                         _dev(h_new, "h_new", torch.float32), len(pos),
                                         _dev(scores_out, "scores_out", torch.float32),
                                         _stream(stream))
+    if check:
+        _raise(rc)
+    return rc
+
+
+def group_by_route(mask: torch.Tensor, perm_out: torch.Tensor, starts_out: torch.Tensor,
+                   n_groups_out: torch.Tensor, stream=None, check: bool = True) -> int:
+    """buddy_group_by_route: mask uint8 [B][n] -> perm int32 [B], group starts
+    int32 [B + 1], group count int32 [1] (device tensors)."""
+    B, n = (mask.shape[0], mask.shape[1]) if mask.dim() == 2 else (0, 0)
+    rc = lib().buddy_group_by_route(_dev(mask, "mask", torch.uint8), B, n,
+                                    _dev(perm_out, "perm_out", torch.int32),
+                                    _dev(starts_out, "starts_out", torch.int32),
+                                    _dev(n_groups_out, "n_groups_out", torch.int32), _stream(stream))
     if check:
         _raise(rc)
     return rc

@@ -123,6 +123,13 @@ int main() {
     EXPECT(buddy_select_topk(&f, ks, 1, 0, mk, nullptr) == BUDDY_EINVAL, "topk n = 0");
     EXPECT(buddy_select_topk(&f, ks, 1, 256, mk, nullptr) == BUDDY_EINVAL, "topk n = 256");
     EXPECT(buddy_select_topk(&f, ks, 65536, 4, mk, nullptr) == BUDDY_EINVAL, "topk B");
+    int32_t pi[4];
+    EXPECT(buddy_group_by_route(mk, 0, 4, pi, pi, pi, nullptr) == BUDDY_OK, "group B = 0");
+    EXPECT(buddy_group_by_route(nullptr, 1, 4, pi, pi, pi, nullptr) == BUDDY_EINVAL, "group mask");
+    EXPECT(buddy_group_by_route(mk, 1, 0, pi, pi, pi, nullptr) == BUDDY_EINVAL, "group n = 0");
+    EXPECT(buddy_group_by_route(mk, 1, 256, pi, pi, pi, nullptr) == BUDDY_EINVAL, "group n");
+    EXPECT(buddy_group_by_route(mk, 1025, 4, pi, pi, pi, nullptr) == BUDDY_EINVAL, "group B");
+    EXPECT(buddy_group_by_route(mk, 1, 4, nullptr, pi, pi, nullptr) == BUDDY_EINVAL, "group perm");
     int32_t kbad[1] = {5};
     EXPECT(buddy_select_topk(&f, kbad, 1, 4, mk, nullptr) == BUDDY_EINVAL, "topk k > n");
 

@@ -172,6 +172,18 @@ int main(void)
             for (int i = 0; i < n; ++i) EXPECT(isfinite(out[i]) || i >= 1, "prior finite");
         }
     free(out);
+
+    /* batch-level path grouping: random masks with repeats, B = 1 and n = 1 */
+    for (int trial = 0; trial < 20; ++trial) {
+        const int32_t B = 1 + (int32_t)((rnd() + 1.0) * 40.0), n = trial % 5 == 0 ? 1 : 9;
+        uint8_t* m = malloc((size_t)B * n);
+        for (int32_t i = 0; i < B * n; ++i) m[i] = rnd() > 0.2 ? 1 : (rnd() > 0.5 ? 0 : 5);
+        int32_t* perm = malloc(sizeof(int32_t) * B);
+        int32_t* starts = malloc(sizeof(int32_t) * (B + 1));
+        const int32_t g = orc_group_by_route(m, B, n, perm, starts);
+        EXPECT(g >= 1 && g <= B && starts[g] == B, "path grouping");
+        free(m); free(perm); free(starts);
+    }
     if (failures) return 1;
     printf("oracle driver ok\n");
     return 0;

@@ -42,6 +42,63 @@ def test_select_topk_bit_exact(n):
         assert np.array_equal(got[b], ref), b
 
 
+# ------------------------------------------------ batch-level path grouping
+
+@pytest.mark.parametrize("B,n", [(1, 30), (5, 1), (96, 38), (256, 30), (1024, 255), (700, 6)])
+def test_group_by_route_bit_exact(B, n):
+    """Path grouping through the C ABI against the oracle: permutation,
+    group starts and group count exactly (integer outputs), on masks with
+    many repeated routes, bytes other than 1 meaning run, and all-run /
+    all-skip rows."""
+    from oracle import group_by_route
+    rng = np.random.default_rng(B * 1000 + n)
+    pool = rng.integers(0, 2, size=(max(1, B // 7), n)).astype(np.uint8)
+    m = pool[rng.integers(0, len(pool), size=B)].copy()
+    m[rng.random(m.shape) < 0.05] = 3
+    m[0, :] = 1
+    if B > 2:
+        m[1, :] = 0
+    perm = torch.full((B,), -1, dtype=torch.int32, device="cuda")
+    starts = torch.full((B + 1,), -1, dtype=torch.int32, device="cuda")
+    ng = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    blib.group_by_route(torch.from_numpy(m).cuda(), perm, starts, ng)
+    torch.cuda.synchronize()
+    ref_perm, ref_starts = group_by_route(m)
+    g = int(ng.item())
+    assert g == len(ref_starts) - 1
+    assert np.array_equal(perm.cpu().numpy(), ref_perm)
+    assert np.array_equal(starts.cpu().numpy()[:g + 1], ref_starts)
+
+
+def test_group_by_route_of_a_batched_step():
+    """The routes a batched decode step executed (mask_out), grouped: every
+    group holds sequences with one route, groups are in route order, and the
+    oracle gives the same grouping."""
+    from oracle import group_by_route
+    B = 40
+    P = Pair("tiny", "bf16", 40, B, seed=5, omega=0.1)
+    g = torch.Generator().manual_seed(6)
+    dk = P.upload(synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt)))
+    dv = P.upload(synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt)))
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=7).numpy()
+    ks = [int(v) for v in np.random.default_rng(8).integers(0, P.L_mid + 1, size=B)]
+    _, mg, _ = gpu_step(P, dk, dv, x, [30] * B, ks)
+    mask = torch.from_numpy(mg).cuda()
+    perm = torch.empty(B, dtype=torch.int32, device="cuda")
+    starts = torch.empty(B + 1, dtype=torch.int32, device="cuda")
+    ng = torch.empty(1, dtype=torch.int32, device="cuda")
+    blib.group_by_route(mask, perm, starts, ng)
+    torch.cuda.synchronize()
+    p, st, n_g = perm.cpu().numpy(), starts.cpu().numpy(), int(ng.item())
+    ref_perm, ref_starts = group_by_route(mg)
+    assert np.array_equal(p, ref_perm) and np.array_equal(st[:n_g + 1], ref_starts)
+    for q in range(n_g):
+        rows = mg[p[st[q]:st[q + 1]]]
+        assert np.all(rows == rows[0])
+        if q > 0:
+            assert tuple(mg[p[st[q - 1]]]) < tuple(rows[0])
+
+
 # ----------------------------------------------------- planner + scorer
 
 @pytest.mark.parametrize("dtype,shape", [("f32", "tiny"), ("bf16", "tiny"),
