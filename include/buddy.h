@@ -107,11 +107,13 @@ typedef enum { BUDDY_SKIP_KV_ZERO = 0, BUDDY_SKIP_KV_MASK = 1 } buddy_skip_kv;
 
 typedef struct {
     int32_t n_layers;     /* L >= 2; blocks 0 and L-1 always run          */
-    int32_t d_model;      /* multiple of 8                                 */
+    int32_t d_model;      /* multiple of 8; bf16: at most 8192, a multiple
+                             of 512 above 4096; fp32: at most 2048        */
     int32_t n_heads;      /* query heads, multiple of n_kv_heads           */
     int32_t n_kv_heads;   /* n_heads / n_kv_heads <= 8                     */
     int32_t head_dim;     /* 64 or 128                                     */
-    int32_t d_ffn;        /* multiple of 8                                 */
+    int32_t d_ffn;        /* multiple of 8; bf16: at most 32768, a multiple
+                             of 512 above 4096; fp32: at most 2048        */
     int32_t dm_hidden;    /* Decision Module hidden width, multiple of 8   */
     int32_t dm_act;       /* buddy_dm_act                                  */
     int32_t dtype;        /* buddy_dtype of weights and KV cache           */
@@ -171,7 +173,10 @@ typedef struct buddy_model buddy_model;
 /* Creates a model handle on the current HIP device.  `layers` holds
  * n_layers entries; the weight pointers are copied, the weights are not.
  * Allocates the handle's workspace (sized by max_batch and max_ctx).
- * Returns BUDDY_OK and *out, or an error status with *out = NULL. */
+ * Returns BUDDY_OK and *out, or an error status with *out = NULL:
+ * BUDDY_ESHAPE for a shape outside the limits of the fields above (the
+ * query width n_heads * head_dim within those of d_ffn, the router input
+ * of at most 20480 elements), BUDDY_ECAPACITY for max_batch or max_ctx. */
 buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weights* layers,
                                 const buddy_dm_weights* dm, buddy_model** out);
 

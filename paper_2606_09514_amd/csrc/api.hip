@@ -61,6 +61,7 @@ buddy_status check_config(const buddy_config* c) {
     // and a quarter of 64 k-steps of a single row
     const int ks = 64 * (c->dtype == BUDDY_BF16 ? 8 : 4);
     if (c->d_model > 16 * ks || c->d_ffn > 64 * ks) return BUDDY_ESHAPE;
+    if (c->n_heads * c->head_dim > 64 * ks) return BUDDY_ESHAPE;
     // every K the GEMVs see (d_model, d_ffn, n_heads * head_dim and the
     // router input) is a whole number of k-steps of 64 lanes x 16 bytes or at
     // most 8 k-steps; fp32 weights (small models) have rows of at most 8
@@ -74,9 +75,13 @@ buddy_status check_config(const buddy_config* c) {
     if (c->dtype == BUDDY_F32 &&
         (c->d_model > 8 * ks || c->d_ffn > 8 * ks || qdim > 8 * ks || din > 8 * ks))
         return BUDDY_ESHAPE;
-    // the activation rows of one GEMV pass must fit in LDS
-    const int kmax = c->d_ffn > c->d_model ? c->d_ffn : c->d_model;
-    if ((size_t)kmax * sizeof(float) > 80 * 1024) return BUDDY_ESHAPE;
+    // a GEMV stages an fp32 activation row in at most 80 KB of LDS, or a
+    // K-sliced row of whole k-steps in two halves of at most 64 KB; the
+    // router input is staged in one piece
+    auto staged_ok = [ks](int K) {
+        return (size_t)K * sizeof(float) <= 80 * 1024 || (K % ks == 0 && K <= 64 * ks);
+    };
+    if (!staged_ok(c->d_ffn) || !staged_ok(c->d_model) || !staged_ok(qdim)) return BUDDY_ESHAPE;
     if ((size_t)din * sizeof(float) > 80 * 1024) return BUDDY_ESHAPE;
     return BUDDY_OK;
 }

@@ -85,11 +85,17 @@ __device__ __forceinline__ int slot_row(const GemvArgs& g, int blk, int slot, in
 // When the host knows the routed row count (n_host >= 0) the weight loads
 // start before anything else; otherwise the device count is read first and
 // an empty launch returns without touching the weights.  PRO_RMSNORM stages
-// gain * x and applies 1/rms(x) to the finished sums.
-template <typename TW, int NR, int PRO, int EPI, int S, int ML, int P, bool TAIL, bool MULTI>
+// gain * x and applies 1/rms(x) to the finished sums.  NP = 2 (K-sliced rows
+// too long for one staging in LDS): the activation rows pass through LDS in
+// two halves, the first for the wavefronts of slices 0 .. S/2 - 1, the
+// second for the others.
+template <typename TW, int NR, int PRO, int EPI, int S, int ML, int P, bool TAIL, bool MULTI,
+          int NP = 1>
 __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int nsteps, int spw,
                                                     int n_host) {
-    extern __shared__ float xs[];   // [NR][K] staged activation rows
+    static_assert(NP == 1 || (NP == 2 && S % 2 == 0 && !TAIL && PRO != PRO_POOL),
+                  "two staging passes split the K-slices of whole k-steps");
+    extern __shared__ float xs[];   // [NR][Kp] staged activation rows (Kp = K when NP = 1)
     __shared__ float s_ss[P][NR];
     __shared__ float s_part[P][NR];
     constexpr int V = St<TW>::V;
@@ -131,11 +137,21 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
     // MULTI = false: the host guarantees n <= NR, and the single pass keeps
     // the weight registers out of a loop (half the VGPRs, twice the waves)
     const int groups = MULTI ? (n + NR - 1) / NR : 1;
+    // k-steps and elements of one staging pass
+    const int spp = NP == 1 ? nsteps : (S / NP) * spw;
+    const int Kp = NP == 1 ? K : spp * KS;
     for (int gi = 0; gi < groups; ++gi) {
         const int i0 = gi * NR;
         const int nr = min(NR, n - i0);
         if (MULTI) __syncthreads();  // the previous group is done with xs and s_part
         const TW* gain = (const TW*)g.gain;
+        float ssr[NR], acc[NR];
+#pragma unroll
+        for (int r = 0; r < NR; ++r) ssr[r] = acc[r] = 0.f;
+#pragma unroll
+        for (int pass = 0; pass < NP; ++pass) {
+        const int kb = pass * Kp, ke = NP == 1 ? K : min(K, kb + Kp);
+        if (pass > 0) __syncthreads();   // the previous pass is done with xs
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
             float ss = 0.f;
@@ -152,11 +168,11 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
                     } else {
                         v = *reinterpret_cast<const float4*>(g.h + (size_t)b * g.d + (k - zdim));
                     }
-                    *reinterpret_cast<float4*>(xs + r * K + k) = v;
+                    *reinterpret_cast<float4*>(xs + r * Kp + k) = v;
                 }
             } else if (r < nr) {
                 const float* xr = g.X + (size_t)row_seq(g.rows, i0 + r) * g.ldx;
-                for (int k = tid * V; k < K; k += NT * V) {
+                for (int k = kb + tid * V; k < ke; k += NT * V) {
                     float v[V];
 #pragma unroll
                     for (int e = 0; e < V; e += 4) {
@@ -171,30 +187,33 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
                     }
 #pragma unroll
                     for (int e = 0; e < V; e += 4)
-                        *reinterpret_cast<float4*>(xs + r * K + k + e) = make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
+                        *reinterpret_cast<float4*>(xs + r * Kp + (k - kb) + e) =
+                            make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
                 }
             } else {
-                for (int k = tid * 4; k < K; k += NT * 4)
-                    *reinterpret_cast<float4*>(xs + r * K + k) = make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int k = kb + tid * 4; k < ke; k += NT * 4)
+                    *reinterpret_cast<float4*>(xs + r * Kp + (k - kb)) = make_float4(0.f, 0.f, 0.f, 0.f);
             }
-            if (PRO == PRO_RMSNORM) {
-                ss = wave_sum(ss);
-                if (lane == 0) s_ss[wave][r] = ss;
+            ssr[r] += ss;
+            if (PRO == PRO_RMSNORM && pass == NP - 1) {
+                const float t = wave_sum(ssr[r]);
+                if (lane == 0) s_ss[wave][r] = t;
             }
         }
         __syncthreads();
 
-        float acc[NR];
+        // this pass's K-slices: the wavefronts whose slice it staged
+        if (NP == 1 || slice / (S / NP) == pass) {
+            const float* xw = xs + (st0 - pass * spp) * KS + lane * V;
 #pragma unroll
-        for (int r = 0; r < NR; ++r) acc[r] = 0.f;
-        const float* xw = xs + st0 * KS + lane * V;
+            for (int q = 0; q < ML; ++q) {
+                if (q < nl && (!TAIL || (st0 + q) * KS + lane * V < K)) {
 #pragma unroll
-        for (int q = 0; q < ML; ++q) {
-            if (q < nl && (!TAIL || (st0 + q) * KS + lane * V < K)) {
-#pragma unroll
-                for (int r = 0; r < NR; ++r) acc[r] += dot16(w[q], xw + r * K + q * KS, TW());
+                    for (int r = 0; r < NR; ++r) acc[r] += dot16(w[q], xw + r * Kp + q * KS, TW());
+                }
             }
         }
+        }   // staging passes
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
             const float v = wave_sum(acc[r]);
@@ -246,9 +265,13 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
     }
 }
 
-template <typename TW, int NR, int PRO, int EPI, int S, int ML, int P, bool TAIL, bool MULTI>
+template <typename TW, int NR, int PRO, int EPI, int S, int ML, int P, bool TAIL, bool MULTI,
+          int NP = 1>
 static hipError_t launch_one(const GemvArgs& g, int units, int n_host, hipStream_t s) {
-    const size_t lds = (size_t)NR * g.K * sizeof(float);
+    constexpr int KS0 = kWave * St<TW>::V;
+    const int nsteps0 = (g.K + KS0 - 1) / KS0;
+    const int kp = NP == 1 ? g.K : (S / NP) * ((nsteps0 + S - 1) / S) * KS0;
+    const size_t lds = (size_t)NR * kp * sizeof(float);
     // devices (one bit each, current device) on which this instantiation
     // may take more than the 64 KB default of dynamic LDS
     static std::atomic<uint64_t> attr_set{0};
@@ -260,7 +283,7 @@ static hipError_t launch_one(const GemvArgs& g, int units, int n_host, hipStream
         if (!(attr_set.load(std::memory_order_relaxed) & bit)) {
             // the dispatcher never asks for more than kGemvLds
             e = hipFuncSetAttribute(
-                reinterpret_cast<const void*>(&gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI>),
+                reinterpret_cast<const void*>(&gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI, NP>),
                 hipFuncAttributeMaxDynamicSharedMemorySize, kGemvLds);
             if (e != hipSuccess) return e;
             attr_set.fetch_or(bit, std::memory_order_relaxed);
@@ -272,7 +295,7 @@ static hipError_t launch_one(const GemvArgs& g, int units, int n_host, hipStream
     const int per_wg = (EPI == EPI_SWIGLU || EPI == EPI_QKV) ? P / 2 : P / S;
     const int items = (EPI == EPI_SWIGLU || EPI == EPI_QKV) ? units : g.N;
     const int grid = (items + per_wg - 1) / per_wg;
-    launch_main(gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI>, dim3(grid), dim3(64 * P),
+    launch_main(gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI, NP>, dim3(grid), dim3(64 * P),
                 (uint32_t)lds, s, g, units, nsteps, spw, n_host);
     return hipGetLastError();
 }
@@ -321,6 +344,22 @@ static hipError_t dispatch_tail(const GemvArgs& g, int units, int n_host, hipStr
     return dispatch_s<TW, NR, PRO, EPI, false, false>(g, units, n_host, s);
 }
 
+// Rows longer than one staging in kGemvLds (bf16 K-sliced rows of 41 to 64
+// k-steps: the FFN down projection of d_ffn up to 32768) pass through LDS in
+// two halves of at most 32 k-steps (64 KB), one routed row at a time.
+template <typename TW, int PRO, int EPI>
+static hipError_t dispatch_halves(const GemvArgs& g, int units, int n_host, hipStream_t s) {
+    if constexpr (std::is_same<TW, float>::value || PRO == PRO_POOL || EPI == EPI_SWIGLU ||
+                  EPI == EPI_QKV) {
+        return hipErrorInvalidValue;   // K of at most d_model or the router input (checked at create)
+    } else {
+        constexpr int KS = kWave * St<TW>::V;
+        if (g.K % KS || g.K > 64 * KS) return hipErrorInvalidValue;
+        if (g.rows.n_max > 1) return launch_one<TW, 1, PRO, EPI, 4, 16, 16, false, true, 2>(g, units, n_host, s);
+        return launch_one<TW, 1, PRO, EPI, 4, 16, 16, false, false, 2>(g, units, n_host, s);
+    }
+}
+
 template <typename TW, int PRO, int EPI>
 static hipError_t dispatch_nr(const GemvArgs& g, int units, hipStream_t s) {
     // rows staged per pass: as many as fit in kGemvLds, at most 4
@@ -328,6 +367,7 @@ static hipError_t dispatch_nr(const GemvArgs& g, int units, hipStream_t s) {
     const int fit = (int)(kGemvLds / row_bytes);
     const int nr = g.rows.n_max < fit ? g.rows.n_max : fit;
     const int n_host = g.rows.exact ? g.rows.n_max : -1;
+    if (fit == 0) return dispatch_halves<TW, PRO, EPI>(g, units, n_host, s);
     if (nr >= 4) return dispatch_tail<TW, 4, PRO, EPI>(g, units, n_host, s);
     if (nr >= 2) return dispatch_tail<TW, 2, PRO, EPI>(g, units, n_host, s);
     return dispatch_tail<TW, 1, PRO, EPI>(g, units, n_host, s);

@@ -82,7 +82,15 @@ def relerr(got, ref):
 # little the stored values are equal or one bf16 ulp apart.  The unrounded
 # values differ by the hidden state's error carried into the projection,
 # which is a fraction of the row's scale, not of each entry: hence one ulp
-# of the entry plus `rel` times the row's largest magnitude.
+# of the entry plus `rel` times the row's largest magnitude, `rel` the
+# larger of a floor per path and twice the sequence's measured hidden-state
+# error.  The second term matters at small positions: both sides round the
+# new V row to bf16, and where the unrounded values straddle a rounding
+# boundary the stored values differ by one ulp; at position 0 the attention
+# output is that row itself, so the flip passes whole into the O projection
+# and the hidden state entering the later blocks (measured: 6.9e-4 at
+# position 0 on the MFMA path, whose 16-bit activations flip more entries
+# than the GEMV's fp32 ones, 3.8e-5 at position 4, below 1e-5 beyond).
 KV_ULP_REL = {"gemv": 1e-4, "mfma": 1e-4}
 
 
@@ -170,7 +178,7 @@ def compare_step(P, hk, hv, dk, dv, x, pos, ks, report, hx=None, dx=None, pool=N
                     report["max_kv_err"] = max(report["max_kv_err"], e)
                     assert e < tol, f"new KV row err {e} (layer {l}, seq {b})"
                     if P.sdt == np.uint16:
-                        v = kv_row_err(g, r, KV_ULP_REL[P.path])
+                        v = kv_row_err(g, r, max(KV_ULP_REL[P.path], 2 * err))
                         report["max_kv_ulp_ratio"] = max(report.get("max_kv_ulp_ratio", 0.0), v)
                         assert v <= 1.0, f"new KV row beyond one bf16 ulp: {v} (layer {l}, seq {b})"
                 else:

@@ -360,6 +360,14 @@ def test_model_create_rejects_bad_shapes():
     with pytest.raises(blib.BuddyError) as e:
         blib.Model(cfg, W, max_batch=300)
     assert e.value.status == blib.ECAPACITY
+    # bf16 FFN rows: at most 64 k-steps of 512 elements, whole k-steps
+    # beyond eight
+    cfg16 = synth.model_config("tiny", "bf16", 8)
+    W16 = synth.model_weights(cfg16, 0, "cuda", omega=0.0)
+    for d_ffn in (65 * 512, 56 * 512 + 8):
+        with pytest.raises(blib.BuddyError) as e:
+            blib.Model(dict(cfg16, d_ffn=d_ffn), W16, max_batch=2)
+        assert e.value.status == blib.ESHAPE
 
 
 # ------------------------------------------- full-size sampled parity (bf16)
@@ -744,6 +752,33 @@ def test_timing_hook_times_the_kernel(B):
                 assert 0.0 < v < 50.0
 
 
+@pytest.mark.parametrize("d_ffn", [56 * 512, 64 * 512])
+@pytest.mark.parametrize("B", [1, 3, 8])
+def test_wide_ffn_rows(d_ffn, B):
+    """FFN rows too long to stage whole in the GEMV's LDS (d_ffn 28672, the
+    Llama-70B width, and the 32768 limit): the down projection stages the
+    SwiGLU output in two halves; B = 1 single row, B = 3 routed rows one at
+    a time, B = 8 the MFMA path with K split."""
+    T = 40
+    shape = dict(n_layers=4, d_model=1024, n_heads=8, n_kv_heads=2, head_dim=128, d_ffn=d_ffn,
+                 dm_hidden=64, dm_act="silu", rope_theta=5e5, rms_eps=1e-5)
+    P = Pair(shape, "bf16", T, B, seed=31, omega=0.1, device_gen=True)
+    g = torch.Generator().manual_seed(32)
+    rep = new_report()
+    for step in range(2):
+        hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        rng = np.random.default_rng(33 + step)
+        pos = rng.integers(0, T, size=B).tolist()
+        pos[0] = T - 1
+        ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+        x = synth.hidden_inputs(B, P.cfg["d_model"], seed=34 + step).numpy()
+        r = one_step_all(P, hk, hv, pos, ks, x)
+        for key in ("max_hidden_err", "max_kv_err"):
+            rep[key] = max(rep[key], r[key])
+    print(d_ffn, B, rep)
+
+
 # --------------------------------------------- batched (MFMA) projections
 
 def one_step_all(P, hk, hv, pos, ks, x):
@@ -947,7 +982,7 @@ def sampled_full_size(name, samples, steps=2, seed=0, running_pool=False):
                         e = relerr(gg, r)
                         report["max_kv_err"] = max(report["max_kv_err"], e)
                         assert e < tol, (b, t, l, e)
-                        v = kv_row_err(gg, r, KV_ULP_REL[P.path])
+                        v = kv_row_err(gg, r, max(KV_ULP_REL[P.path], 2 * err))
                         report["max_kv_ulp_ratio"] = max(report.get("max_kv_ulp_ratio", 0.0), v)
                         assert v <= 1.0, (b, t, l, v)
                     else:
