@@ -33,6 +33,8 @@
 // column tile c and k-step s are 2 KB at ((c * K/32 + s) * 128 + lane) * 8
 // elements, the high part's 1 KB then the low part's, one contiguous load
 // per wavefront each.
+#include <atomic>
+
 #include "buddy_internal.h"
 #include "epilogue.h"
 
@@ -164,7 +166,7 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
     constexpr int GT = kPaired ? 2 : 1;       // weight tiles per epilogue group
     constexpr int NG = RT / GT;               // epilogue groups (16 units or rows each)
     constexpr int kBuf = RT * 2048;           // bytes of one wavefront's round
-    __shared__ __attribute__((aligned(16))) char s_lds[mfma_lds_bytes(RT, NT, GT)];
+    extern __shared__ __attribute__((aligned(16))) char s_lds[];   // mfma_lds_bytes(RT, NT, GT)
     auto s_red = reinterpret_cast<float (*)[GT][16][NT * 16]>(s_lds);
     const int n = n_host >= 0 ? n_host : *g.rows.cnt;
     if (n <= 0) return;
@@ -384,21 +386,48 @@ __global__ __launch_bounds__(256) void split_add_kernel(GemvArgs g, int units, i
         epilogue1<bf16_t, EPI_ADD>(g, row_seq(g.rows, j0 + jj), u, s_v[jj][ul]);
 }
 
+// One instantiation's launch; LDS beyond the 64 KB default (eight weight
+// tiles per workgroup) is allowed once per device.
+template <int EPI, int NT, int RT>
+static void launch_tiles(dim3 grid, const GemvArgs& g, int units, int n_host, float* part, int fold,
+                         hipStream_t s) {
+    constexpr int kGT = EPI == EPI_SWIGLU || EPI == EPI_QKV ? 2 : 1;
+    constexpr int lds = mfma_lds_bytes(RT, NT, kGT);
+    static_assert(lds <= 160 * 1024, "LDS of one CU");
+    if constexpr (lds > 64 * 1024) {
+        static std::atomic<uint64_t> attr_set{0};
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess) return;   // the launch below reports the error
+        const uint64_t bit = 1ull << (dev & 63);
+        if (!(attr_set.load(std::memory_order_relaxed) & bit)) {
+            if (hipFuncSetAttribute(reinterpret_cast<const void*>(&mfma_kernel<EPI, NT, RT>),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
+                return;
+            attr_set.fetch_or(bit, std::memory_order_relaxed);
+        }
+    }
+    launch_main(mfma_kernel<EPI, NT, RT>, grid, dim3(256), (uint32_t)lds, s, g, units, n_host, part, fold);
+}
+
 template <int EPI, int RT>
 static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int splits, float* part,
                                  hipStream_t s, int fold = 0) {
     constexpr int per = 16 * (EPI == EPI_SWIGLU || EPI == EPI_QKV ? RT / 2 : RT);
     const dim3 grid((units + per - 1) / per, splits);
     const int tiles = (g.rows.n_max + 15) / 16;
-    if (tiles <= 1) launch_main(mfma_kernel<EPI, 1, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
-    else if (tiles <= 2) launch_main(mfma_kernel<EPI, 2, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
-    else if (tiles <= 3) launch_main(mfma_kernel<EPI, 3, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
-    else if (tiles <= 4) launch_main(mfma_kernel<EPI, 4, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
-    else if (tiles <= 5) launch_main(mfma_kernel<EPI, 5, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
-    else if (tiles <= 6) launch_main(mfma_kernel<EPI, 6, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
-    else if constexpr (RT <= 2) {
-        if (tiles <= 7) launch_main(mfma_kernel<EPI, 7, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
-        else launch_main(mfma_kernel<EPI, kMfmaMaxTiles, RT>, grid, dim3(256), 0, s, g, units, n_host, part, fold);
+    if (tiles <= 1) launch_tiles<EPI, 1, RT>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 2) launch_tiles<EPI, 2, RT>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 3) launch_tiles<EPI, 3, RT>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 4) launch_tiles<EPI, 4, RT>(grid, g, units, n_host, part, fold, s);
+    else if constexpr (RT == 8) {
+        return hipErrorInvalidValue;   // eight weight tiles: at most four column tiles (registers)
+    } else {
+        if (tiles <= 5) launch_tiles<EPI, 5, RT>(grid, g, units, n_host, part, fold, s);
+        else if (tiles <= 6) launch_tiles<EPI, 6, RT>(grid, g, units, n_host, part, fold, s);
+        else if constexpr (RT <= 2) {
+            if (tiles <= 7) launch_tiles<EPI, 7, RT>(grid, g, units, n_host, part, fold, s);
+            else launch_tiles<EPI, kMfmaMaxTiles, RT>(grid, g, units, n_host, part, fold, s);
+        }
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1 || fold) return e;
@@ -414,8 +443,9 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
 
 // Largest weight tile per workgroup that still gives kMfmaMinGrid workgroups
 // (four tiles only up to six column tiles: beyond, their registers would
-// halve the occupancy); K split per mfma_splits, with 64-row (or, beyond
-// six column tiles, 32-row) tiles
+// halve the occupancy; eight for a gate/up projection of up to 32 routed
+// rows whose grid then fills the chip once); K split per mfma_splits, with
+// 64-row (or, beyond six column tiles, 32-row) tiles
 template <int EPI>
 static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, float* part, hipStream_t s,
                                   bool fold = false) {
@@ -431,6 +461,14 @@ static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, floa
     if (splits > 1) {
         if (wide) return launch_mfma_nt<EPI, 4>(g, units, n_host, splits, part, s);
         return launch_mfma_nt<EPI, 2>(g, units, n_host, splits, part, s);
+    }
+    if constexpr (EPI == EPI_SWIGLU) {
+        // up to two column tiles and a grid that fits the chip in one round
+        // of workgroups (one per CU): eight weight tiles per workgroup halve
+        // the activation re-reads against four
+        const int wg8 = (units + 63) / 64;
+        if (g.rows.n_max <= 32 && wg8 >= 192 && wg8 <= 256)
+            return launch_mfma_nt<EPI, 8>(g, units, n_host, 1, nullptr, s);
     }
     if constexpr (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
         if (wide && units / 32 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, 1, nullptr, s);

@@ -781,6 +781,31 @@ def test_wide_ffn_rows(d_ffn, B):
 
 # --------------------------------------------- batched (MFMA) projections
 
+@pytest.mark.parametrize("B", [5, 32])
+def test_gate_up_eight_weight_tiles(B):
+    """A gate/up projection whose 64-unit tiles give between 192 and 256
+    workgroups (d_ffn 12800: 200) at up to 32 routed rows takes eight weight
+    tiles per workgroup; two steps, mixed positions and budgets."""
+    T = 40
+    shape = dict(n_layers=4, d_model=512, n_heads=4, n_kv_heads=1, head_dim=128, d_ffn=12800,
+                 dm_hidden=64, dm_act="silu", rope_theta=5e5, rms_eps=1e-5)
+    P = Pair(shape, "bf16", T, B, seed=41, omega=0.1, device_gen=True)
+    g = torch.Generator().manual_seed(42)
+    rep = new_report()
+    for step in range(2):
+        hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        rng = np.random.default_rng(43 + step)
+        pos = rng.integers(0, T, size=B).tolist()
+        pos[0] = T - 1
+        ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+        x = synth.hidden_inputs(B, P.cfg["d_model"], seed=44 + step).numpy()
+        r = one_step_all(P, hk, hv, pos, ks, x)
+        for key in ("max_hidden_err", "max_kv_err"):
+            rep[key] = max(rep[key], r[key])
+    print(B, rep)
+
+
 def one_step_all(P, hk, hv, pos, ks, x):
     """One teacher-forced step of every sequence from the given host caches."""
     dk, dv = P.upload(hk), P.upload(hv)
