@@ -92,7 +92,7 @@ __device__ __forceinline__ int slot_row(const GemvArgs& g, int blk, int slot, in
 template <typename TW, int NR, int PRO, int EPI, int S, int ML, int P, bool TAIL, bool MULTI,
           int NP = 1>
 __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int nsteps, int spw,
-                                                    int n_host) {
+                                                    int n_host, int rb) {
     static_assert(NP == 1 || (NP == 2 && S % 2 == 0 && !TAIL && PRO != PRO_POOL),
                   "two staging passes split the K-slices of whole k-steps");
     extern __shared__ float xs[];   // [NR][Kp] staged activation rows (Kp = K when NP = 1)
@@ -110,6 +110,9 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
         n = *g.rows.cnt;
         if (n <= 0) return;
     }
+    // MULTI: this workgroup's slice of rb routed rows (grid.y slices)
+    const int rbase = MULTI ? (int)blockIdx.y * rb : 0;
+    if (MULTI && rbase >= n) return;
     const int row = slot_row<EPI, S, P>(g, blockIdx.x, wave, units);
     const int st0 = slice * spw;
     const int nl = row < 0 ? 0 : max(0, min(spw, nsteps - st0));
@@ -136,13 +139,14 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
 
     // MULTI = false: the host guarantees n <= NR, and the single pass keeps
     // the weight registers out of a loop (half the VGPRs, twice the waves)
-    const int groups = MULTI ? (n + NR - 1) / NR : 1;
+    const int nloc = MULTI ? min(rb, n - rbase) : n;
+    const int groups = MULTI ? (nloc + NR - 1) / NR : 1;
     // k-steps and elements of one staging pass
     const int spp = NP == 1 ? nsteps : (S / NP) * spw;
     const int Kp = NP == 1 ? K : spp * KS;
     for (int gi = 0; gi < groups; ++gi) {
-        const int i0 = gi * NR;
-        const int nr = min(NR, n - i0);
+        const int i0 = rbase + gi * NR;
+        const int nr = min(NR, rbase + nloc - i0);
         if (MULTI) __syncthreads();  // the previous group is done with xs and s_part
         const TW* gain = (const TW*)g.gain;
         float ssr[NR], acc[NR];
@@ -295,8 +299,21 @@ static hipError_t launch_one(const GemvArgs& g, int units, int n_host, hipStream
     const int per_wg = (EPI == EPI_SWIGLU || EPI == EPI_QKV) ? P / 2 : P / S;
     const int items = (EPI == EPI_SWIGLU || EPI == EPI_QKV) ? units : g.N;
     const int grid = (items + per_wg - 1) / per_wg;
-    launch_main(gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI, NP>, dim3(grid), dim3(64 * P),
-                (uint32_t)lds, s, g, units, nsteps, spw, n_host);
+    // MULTI: the batch's staging groups split into slices over grid.y, so
+    // that the launch has about 512 workgroups (each slice loads its weight
+    // rows again, mostly from L2): at B = 32 on the Llama-8B shape the
+    // Decision Module layer's 128 column workgroups left half the CUs idle
+    // (92 us, 52 us with four slices)
+    int rb = 0, gy = 1;
+    if (MULTI) {
+        const int ng = (g.rows.n_max + NR - 1) / NR;   // staging groups of the batch
+        int slices = (512 + grid - 1) / grid;
+        if (slices > ng) slices = ng;
+        rb = (ng + slices - 1) / slices * NR;
+        gy = (g.rows.n_max + rb - 1) / rb;
+    }
+    launch_main(gemv_kernel<TW, NR, PRO, EPI, S, ML, P, TAIL, MULTI, NP>, dim3(grid, gy), dim3(64 * P),
+                (uint32_t)lds, s, g, units, nsteps, spw, n_host, rb);
     return hipGetLastError();
 }
 
