@@ -133,15 +133,18 @@ bool uses_mfma(const Model& M, const Rows& rows, int batch, int K, int tok_T) {
 // not on how many sequences a block routes, so a sequence's arithmetic does
 // not depend on the routes of the others or on the launch policy.
 // fold: the MFMA path's residual add goes to the partial buffer for the next
-// staging to add (the caller has checked that the buffer holds the rows).
+// staging to add (the caller has checked that the buffer holds the rows):
+// fold_part, or the handle's K-split buffer.
 hipError_t launch_proj(const Model& M, int batch, int pro, int epi, GemvArgs g, hipStream_t s,
-                       bool fold = false) {
+                       bool fold = false, float* fold_part = nullptr) {
     // prompt tokens of a prefill: the tiled GEMM
     if (uses_gemm(M, g.rows, batch, g.K, g.tok_T))
         return launch_gemm(pro, epi, g, M.gemm_tile, M.pf_split, s);
     if (uses_mfma(M, g.rows, batch, g.K, g.tok_T))
-        return launch_mfma(pro, epi, g, g.rows.n_max <= M.ws.mfma_part_rows ? M.ws.mfma_part : nullptr, s,
-                           fold);
+        return launch_mfma(pro, epi, g,
+                           fold_part ? fold_part
+                                     : g.rows.n_max <= M.ws.mfma_part_rows ? M.ws.mfma_part : nullptr,
+                           s, fold);
     if (pro == PRO_STAGED) return hipErrorInvalidValue;   // staged inputs feed the MFMA paths only
     return launch_gemv(M.cfg.dtype, pro, epi, g, s);
 }
@@ -182,9 +185,14 @@ hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
     return e != hipSuccess ? e : hipEventRecord(t.stop[t.next], s);
 }
 
+// d_upto > 0: the QKV staging first adds each sequence's deferred down sums
+// from the routable blocks before list index d_upto; d_out >= 0: this
+// block's down projection leaves its split sums deferred, as routable block
+// d_out (decode rows on the MFMA path, M.ws.down_part).
 buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float* hidden, int l,
                        Rows rows, int batch, int max_pos, int pos_u, const BlockBufs& bf,
-                       hipStream_t s, const int32_t* groups = nullptr, int n_groups = 0) {
+                       hipStream_t s, const int32_t* groups = nullptr, int n_groups = 0,
+                       int d_upto = -1, int d_out = -1) {
     const buddy_config& c = M.cfg;
     const buddy_layer_weights& w = M.layers[l];
     const int qdim = c.n_heads * c.head_dim;
@@ -205,10 +213,17 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
     g.W = w.wqkv; g.N = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim; g.K = c.d_model;
     g.X = hidden; g.ldx = c.d_model; g.gain = w.attn_norm;
     g.Y = bf.q; g.ldy = qdim;
+    const size_t down_block = (size_t)M.ws.down_splits * c.max_batch * c.d_model;
+    if (d_upto > 0 && M.ws.down_part) {
+        g.dpart = M.ws.down_part; g.dpart_block = down_block; g.dpart_splits = M.ws.down_splits;
+        g.dpart_cap = c.max_batch; g.dinv = M.ws.inv; g.dmask = M.ws.mask; g.dLm = n_mid(c);
+        g.d_upto = d_upto;
+    }
     if ((e = mark(M, BUDDY_KERNEL_QKV, l, false, s)) != hipSuccess ||
         (e = launch_proj(M, batch, PRO_RMSNORM, EPI_QKV, g, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_QKV, l, true, s)) != hipSuccess)
         return fail_device(M, e, "qkv");
+    g.dpart = nullptr;
 
     // attention over rows 0..pos
     AttnArgs a;
@@ -252,6 +267,7 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
                         rows.n_max <= M.ws.mfma_part_rows;
     g.W = w.wo; g.N = c.d_model; g.K = qdim; g.X = bf.o; g.ldx = qdim; g.gain = nullptr;
     g.Y = hidden; g.ldy = c.d_model;
+    g.part_cap = rows.n_max;
     if ((e = mark(M, BUDDY_KERNEL_O_PROJ, l, false, s)) != hipSuccess ||
         (e = launch_proj(M, batch, a.xb_out ? PRO_STAGED : PRO_NONE, EPI_ADD, g, s, o_fold)) !=
             hipSuccess ||
@@ -280,12 +296,19 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
     g.xb_out = nullptr;
     g.addpart = nullptr;
 
-    // h += Wdown m
+    // h += Wdown m, or (deferred) the split sums left for the sequence's
+    // next block to add while staging its input
     g.W = w.wdown; g.N = c.d_model; g.K = c.d_ffn; g.X = bf.m; g.ldx = c.d_ffn;
     g.gain = nullptr; g.Y = hidden; g.ldy = c.d_model;
     if (m_staged) g.XB = bf.xb2;
+    const bool defer = d_out >= 0 && M.ws.down_part && m_staged && bf.tok_T == 0;
+    // a later staging adds what a deferring block leaves: never a stale buffer
+    if (d_out >= 0 && !defer) return fail_device(M, hipErrorInvalidValue, "down (deferred sums)");
+    float* down_fold = defer ? M.ws.down_part + (size_t)d_out * down_block : nullptr;
+    g.part_cap = c.max_batch;
     if ((e = mark(M, BUDDY_KERNEL_DOWN, l, false, s)) != hipSuccess ||
-        (e = launch_proj(M, batch, m_staged ? PRO_STAGED : PRO_NONE, EPI_ADD, g, s)) != hipSuccess ||
+        (e = launch_proj(M, batch, m_staged ? PRO_STAGED : PRO_NONE, EPI_ADD, g, s, defer, down_fold)) !=
+            hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_DOWN, l, true, s)) != hipSuccess)
         return fail_device(M, e, "down");
     return BUDDY_OK;
@@ -481,6 +504,17 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
         if (splits > 1) part_elems = splits * c.d_model * part_rows;
     }
     M.ws.mfma_part_rows = part_elems ? part_rows : 0;
+    // deferred down-projection sums of the routable blocks (decode on the
+    // MFMA path with the down projection K-split): one buffer per block
+    size_t down_elems = 0;
+    M.ws.down_splits = 0;
+    if (c.dtype == BUDDY_BF16 && Bc > (size_t)kGemvMaxRows && Lm > 0) {
+        const int sd = mfma_splits(EPI_ADD, c.d_model, c.d_ffn);
+        if (sd > 1 && mfma_fold_splits(c.d_model, c.d_ffn) == sd) {
+            M.ws.down_splits = sd;
+            down_elems = (size_t)Lm * sd * Bc * c.d_model;
+        }
+    }
 
     struct Piece { void** dst; size_t bytes; };
     Workspace& W = M.ws;
@@ -498,6 +532,8 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
         {(void**)&W.xb, 2 * ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
         {(void**)&W.xb2, 2 * ((Bc + 15) / 16 * 16) * xb_ld * sizeof(bf16_t)},
         {(void**)&W.mfma_part, part_elems * 4},
+        {(void**)&W.inv, Lm * Bc * 4 + 4},
+        {(void**)&W.down_part, down_elems * 4},
     };
     size_t total = 0;
     for (const Piece& p : pieces) total += align_up(p.bytes);
@@ -506,6 +542,7 @@ buddy_status buddy_model_create(const buddy_config* cfg, const buddy_layer_weigh
     }
     size_t off = 0;
     for (const Piece& p : pieces) { *p.dst = (char*)M.ws_base + off; off += align_up(p.bytes); }
+    if (!down_elems) W.down_part = nullptr;
     hipError_t e = hipMemset(M.ws_base, 0, total);
     // rotary table: angle pos * theta^(-2i/hd) in double, cos and sin rounded to fp32
     const size_t half = hd / 2;
@@ -756,7 +793,12 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
                           route_override, mask_out, scores_out, false, seq, s)) != hipSuccess)
         return fail_device(M, e, "route");
     if (host_routed && (st = wait_route(M, seq, s)) != BUDDY_OK) return st;
-    // routable blocks S..L-2 (list i = l - S) on their compacted sub-batches
+    // routable blocks S..L-2 (list i = l - S) on their compacted sub-batches.
+    // On the MFMA path each one's down projection leaves its split sums to
+    // the staging of the sequence's next block (no add kernel per block);
+    // the sums, their order and the residual add are those of the add kernel
+    const bool defer = M.ws.down_part && uses_mfma(M, all, B, c.d_model, 0) &&
+                       uses_mfma(M, all, B, c.d_ffn, 0);
     for (int l = S; l < S + Lm; ++l) {
         const int i = l - S;
         int n_max = B;
@@ -774,12 +816,13 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
         // every sequence routed (known on the host): the rows are the batch in order
         const Rows r{M.ws.idx + (size_t)i * c.max_batch, M.ws.cnt + i, n_max,
                      host_routed, host_routed && n_max == B};
-        if ((st = run_block(M, kv, exec, hidden, l, r, B, max_pos, pos_u, decode_bufs(M), s)) !=
-            BUDDY_OK)
+        if ((st = run_block(M, kv, exec, hidden, l, r, B, max_pos, pos_u, decode_bufs(M), s, nullptr,
+                            0, defer ? i : -1, defer ? i : -1)) != BUDDY_OK)
             return st;
     }
-    // last block on every sequence
-    st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, B, max_pos, pos_u, decode_bufs(M), s);
+    // last block on every sequence (it adds what the routable blocks deferred)
+    st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, B, max_pos, pos_u, decode_bufs(M), s,
+                   nullptr, 0, defer ? Lm : -1, -1);
     if (M.timing.n > 0 && M.timing.next < M.timing.n) ++M.timing.next;
     return st;
 }

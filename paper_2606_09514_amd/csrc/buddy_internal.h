@@ -119,6 +119,12 @@ struct Workspace {
     bf16_t* xb2;         // the same, for the down projection's input
     float* mfma_part;    // K-split partial sums of the MFMA path (see mfma_splits)
     int mfma_part_rows;  // routed rows the partial buffer holds (0: no buffer)
+    int32_t* inv;        // [L-2][max_batch] launch row of sequence b in block i's list, or -1
+    // K-split sums of each routable block's down projection, added by the
+    // staging of the sequence's next block (decode on the MFMA path):
+    // [L-2][splits][max_batch][d], or null
+    float* down_part;
+    int down_splits;
     int xb_ld;
     int max_chunks;
     int max_pool_splits;
@@ -325,6 +331,18 @@ struct GemvArgs {
     // the staging adds into X's rows (in split order, written back) before
     // the norm; or null
     const float* addpart; int addpart_splits; int addpart_cap;
+    // PRO_RMSNORM on the MFMA path, decode rows: the deferred sums of the
+    // down projections.  Routable block i's down projection leaves its split
+    // sums at dpart + i dpart_block ([split][dpart_cap][K] by that block's
+    // launch row); the staging adds, for each of its sequences b, those of
+    // the last routable block before list index d_upto that b ran (dmask
+    // [B][dLm]), at row dinv[i dpart_cap + b], into X's row (in split order,
+    // written back) before the norm; or null
+    const float* dpart; size_t dpart_block; int dpart_splits; int dpart_cap;
+    const int32_t* dinv; const uint8_t* dmask; int dLm; int d_upto;
+    // MFMA residual-add projection with fold: the row capacity of its
+    // [split][row][N] partial sums
+    int part_cap;
     // EPI_SWIGLU (tiled GEMM and MFMA paths): the outputs in the next
     // projection's staging order with K = f (its staged input) instead of Y:
     // xb_index bf16 for the tiled GEMM, xbs_index split for the MFMA path

@@ -48,9 +48,14 @@ constexpr int kMfmaMaxTiles = 8;   // 16-row column tiles of routed rows per pas
 
 // ----------------------------------------------------------------- prep
 
+// Threads of a staging workgroup (one routed row): 512, so that a 4096-wide
+// row takes one pass of 8 elements per thread, its loads (the row and any
+// split sums) all in flight at once.
+constexpr int kPrepThreads = 512;
+
 template <int PRO>
-__global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
-    __shared__ float s_ss[4];
+__global__ __launch_bounds__(kPrepThreads) void prep_kernel(GemvArgs g, int n_host) {
+    __shared__ float s_ss[kPrepThreads / 64];
     const int i = blockIdx.x;
     const int n = n_host >= 0 ? n_host : *g.rows.cnt;
     if (i >= n) return;
@@ -60,17 +65,32 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
     if (PRO == PRO_RMSNORM) {
         // each thread owns the same 8-element groups here and in the staging
         // below, so it reads back its own residual writes
-        float* x = const_cast<float*>(g.X) + (size_t)b * g.ldx;   // written only with addpart
+        float* x = const_cast<float*>(g.X) + (size_t)b * g.ldx;   // written only with split sums
+        // split sums to add: the preceding projection's of this block (by
+        // launch row), or the down projection's of the last routable block
+        // this sequence ran (deferred)
+        const float* ap = g.addpart;
+        int an = g.addpart_splits, acap = g.addpart_cap, arow = i;
+        if (g.dpart) {
+            int last = -1;
+            for (int q = g.d_upto - 1; q >= 0; --q)
+                if (g.dmask[(size_t)b * g.dLm + q]) { last = q; break; }
+            if (last >= 0) {
+                ap = g.dpart + (size_t)last * g.dpart_block;
+                an = g.dpart_splits; acap = g.dpart_cap;
+                arow = g.dinv[(size_t)last * g.dpart_cap + b];
+            }
+        }
         float ss = 0.f;
-        for (int k = tid * 8; k < K; k += 256 * 8) {
+        for (int k = tid * 8; k < K; k += kPrepThreads * 8) {
             float4 v0 = *reinterpret_cast<const float4*>(x + k);
             float4 v1 = *reinterpret_cast<const float4*>(x + k + 4);
-            if (g.addpart) {
-                // the preceding projection's K-split sums, in split order,
-                // then the residual add (as the split-add kernel does it)
+            if (ap) {
+                // K-split sums in split order, then the residual add (as the
+                // split-add kernel does it)
                 float4 a0 = make_float4(0.f, 0.f, 0.f, 0.f), a1 = a0;
-                for (int q = 0; q < g.addpart_splits; ++q) {
-                    const float* pp = g.addpart + ((size_t)q * g.addpart_cap + i) * K + k;
+                for (int q = 0; q < an; ++q) {
+                    const float* pp = ap + ((size_t)q * acap + arow) * K + k;
                     const float4 t0 = *reinterpret_cast<const float4*>(pp);
                     const float4 t1 = *reinterpret_cast<const float4*>(pp + 4);
                     a0.x += t0.x; a0.y += t0.y; a0.z += t0.z; a0.w += t0.w;
@@ -87,11 +107,13 @@ __global__ __launch_bounds__(256) void prep_kernel(GemvArgs g, int n_host) {
         ss = wave_sum(ss);
         if (lane == 0) s_ss[wave] = ss;
         __syncthreads();
-        inv = 1.0f / sqrtf((s_ss[0] + s_ss[1] + s_ss[2] + s_ss[3]) / (float)K + g.eps);
+        const float ss_all = ((s_ss[0] + s_ss[1]) + (s_ss[2] + s_ss[3])) +
+                             ((s_ss[4] + s_ss[5]) + (s_ss[6] + s_ss[7]));
+        inv = 1.0f / sqrtf(ss_all / (float)K + g.eps);
     }
     const float inv_n = PRO == PRO_POOL ? 1.0f / (float)(seq_pos(g.pos, g.pos_u, b) + 1) : 0.f;
     const int zdim = pooled_dim(g.ctx, g.nkv, g.hd);
-    for (int k = tid * 8; k < K; k += 256 * 8) {
+    for (int k = tid * 8; k < K; k += kPrepThreads * 8) {
         float v[8];
         if (PRO == PRO_POOL && k < zdim) {
             const float4 t0 = pooled_feature4(g, b, k, inv_n), t1 = pooled_feature4(g, b, k + 4, inv_n);
@@ -303,12 +325,12 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
                     for (int v = 0; v < 4; ++v)
                         s_red[wave][t][4 * (lane >> 4) + v][c * 16 + (lane & 15)] = acc[q + t * NG][c][v];
             __syncthreads();
-            if (part && fold) {   // K split, by launch row: [split][n_max][units]
+            if (part && fold) {   // K split, by launch row: [split][part_cap][units]
                 for (int p = tid; p < 16 * ncols; p += 256) {
                     const int il = p & 15, j = p >> 4;
                     const int uu = u0 + 16 * q + il;
                     if (uu >= units) continue;
-                    part[((size_t)blockIdx.y * g.rows.n_max + j0 + j) * units + uu] =
+                    part[((size_t)blockIdx.y * g.part_cap + j0 + j) * units + uu] =
                         (s_red[0][0][il][j] + s_red[1][0][il][j]) +
                         (s_red[2][0][il][j] + s_red[3][0][il][j]);
                 }
@@ -482,9 +504,9 @@ static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, floa
 
 hipError_t launch_prep(int pro, const GemvArgs& g, hipStream_t s) {
     const int n_host = g.rows.exact ? g.rows.n_max : -1;
-    if (pro == PRO_RMSNORM) prep_kernel<PRO_RMSNORM><<<g.rows.n_max, 256, 0, s>>>(g, n_host);
-    else if (pro == PRO_POOL) prep_kernel<PRO_POOL><<<g.rows.n_max, 256, 0, s>>>(g, n_host);
-    else prep_kernel<PRO_NONE><<<g.rows.n_max, 256, 0, s>>>(g, n_host);
+    if (pro == PRO_RMSNORM) prep_kernel<PRO_RMSNORM><<<g.rows.n_max, kPrepThreads, 0, s>>>(g, n_host);
+    else if (pro == PRO_POOL) prep_kernel<PRO_POOL><<<g.rows.n_max, kPrepThreads, 0, s>>>(g, n_host);
+    else prep_kernel<PRO_NONE><<<g.rows.n_max, kPrepThreads, 0, s>>>(g, n_host);
     return hipGetLastError();
 }
 

@@ -17,7 +17,8 @@
 //                 entries of the execution map; with a single sequence it
 //                 also does the compaction below.
 //  compact_kernel grouping by mask (App. C.1): for every routable block the
-//                 ascending list of sequences that run it and their count.
+//                 ascending list of sequences that run it, their count and
+//                 each sequence's row in the list (-1 if absent).
 //  topk_kernel    the standalone top-k entry point.
 // Partial results always travel through a kernel boundary; no kernel here
 // synchronises workgroups (device-wide fences are costly across the XCDs).
@@ -352,11 +353,11 @@ __global__ __launch_bounds__(1024) void route_kernel(RouteParams p, StepArgs sa)
 }
 
 // One workgroup: each wavefront scans the mask columns of every fourth
-// routable block over the batch.  When host_cnt (mapped pinned host memory)
+// routable block over the batch (inv: [Lm][bcap] rows).  When host_cnt (mapped pinned host memory)
 // is given, the counts are also published there, followed by the step's
 // sequence number once they are visible to the host.
 __global__ __launch_bounds__(256) void compact_kernel(const uint8_t* mask, int Lm, int B, int bcap,
-                                                      int32_t* idx, int32_t* cnt,
+                                                      int32_t* idx, int32_t* cnt, int32_t* inv,
                                                       volatile int32_t* host_cnt, int32_t seq) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int i = wave; i < Lm; i += 4) {
@@ -367,6 +368,7 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint8_t* mask, int L
             const uint64_t bal = __ballot(sel);
             const int before = __popcll(bal & ((1ull << lane) - 1ull));
             if (sel) idx[(size_t)i * bcap + base + before] = bb;
+            if (bb < B) inv[(size_t)i * bcap + bb] = sel ? base + before : -1;
             base += __popcll(bal);
         }
         if (lane == 0) {
@@ -410,7 +412,7 @@ hipError_t launch_route(const Model& M, const void* kc, const void* vc, uint8_t*
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || scores_only || p.Lm == 0 || B == 1) return e;
     compact_kernel<<<1, 256, 0, s>>>(M.ws.mask, p.Lm, B, c.max_batch, M.ws.idx, M.ws.cnt,
-                                     p.host_cnt, publish_seq);
+                                     M.ws.inv, p.host_cnt, publish_seq);
     return hipGetLastError();
 }
 
