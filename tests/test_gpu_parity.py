@@ -834,6 +834,43 @@ def test_batched_steps_mfma(B, policy):
 
 
 @pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+def test_deferred_down_sums_fixed_routes(policy):
+    """MFMA path with the down projection's split sums deferred to each
+    sequence's next block: fixed routes in which a routable block runs no
+    sequence (host-routed: not launched), one runs all sequences but the
+    one that skips every routable block, and the others skip one or several,
+    so the sums wait
+    across skipped blocks and the last block adds them; six fed-back steps
+    against the oracle with the same routes."""
+    T = 12
+    shape = dict(n_layers=7, d_model=256, n_heads=4, n_kv_heads=1, head_dim=128, d_ffn=1024,
+                 dm_hidden=64, dm_act="silu", rope_theta=1e4, rms_eps=1e-5)
+    B = 8
+    P = Pair(shape, "bf16", T, B, seed=51, policy=policy)
+    routes = np.array([[1, 0, 1, 0, 1], [0, 0, 0, 0, 0], [1, 0, 1, 1, 1], [0, 0, 1, 0, 0],
+                       [1, 0, 1, 0, 0], [0, 0, 1, 0, 1], [1, 0, 1, 0, 1], [0, 0, 1, 0, 0]], np.uint8)
+    assert routes[:, 1].sum() == 0 and routes[1].sum() == 0 and routes[:, 2].sum() == B - 1
+    hk, hv = P.empty_host_cache()
+    dk, dv = P.upload(hk), P.upload(hv)
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=52).numpy()
+    worst = 0.0
+    for t in range(6):
+        dk.copy_(P.upload(hk))
+        dv.copy_(P.upload(hv))
+        hg, mg, _ = gpu_step(P, dk, dv, x, [t] * B, None, route=routes)
+        assert np.array_equal(mg, routes)
+        outs = []
+        for b in range(B):
+            h, *_ = oracle_step(P, hk, hv, b, t, 0, x[b], route=routes[b])
+            err = relerr(hg[b], h)
+            worst = max(worst, err)
+            assert err < TOL["bf16"], (t, b, err)
+            outs.append(h)
+        x = np.array(outs).astype(np.float32)
+    print("deferred down sums", worst)
+
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
 @pytest.mark.parametrize("B", [40, 150])
 def test_batched_split_k_mfma(B, policy):
     """A decoder whose FFN down projection is long (K = 4 d): on the MFMA
