@@ -815,11 +815,12 @@ def one_step_all(P, hk, hv, pos, ks, x):
 
 
 @pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
-@pytest.mark.parametrize("B", [40, 150])
+@pytest.mark.parametrize("B", [40, 150, 256])
 def test_batched_steps_mfma(B, policy):
     """More routed rows than the GEMV stages per pass: the bf16 projections
     run on MFMA (compact bf16 rows, fp32 accumulation).  Mixed positions and
-    budgets; B = 150 spans two 128-row column groups."""
+    budgets; B = 150 spans two 128-row column groups, B = 256 is the largest
+    batch a handle takes."""
     T = 48
     P = Pair("tiny", "bf16", T, B, seed=21, omega=0.1, policy=policy)
     g = torch.Generator().manual_seed(22)
