@@ -442,7 +442,10 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
     else if (tiles <= 3) launch_tiles<EPI, 3, RT>(grid, g, units, n_host, part, fold, s);
     else if (tiles <= 4) launch_tiles<EPI, 4, RT>(grid, g, units, n_host, part, fold, s);
     else if constexpr (RT == 8) {
-        return hipErrorInvalidValue;   // eight weight tiles: at most four column tiles (registers)
+        // eight weight tiles: at most six column tiles (registers)
+        if (tiles <= 5) launch_tiles<EPI, 5, RT>(grid, g, units, n_host, part, fold, s);
+        else if (tiles <= 6) launch_tiles<EPI, 6, RT>(grid, g, units, n_host, part, fold, s);
+        else return hipErrorInvalidValue;
     } else {
         if (tiles <= 5) launch_tiles<EPI, 5, RT>(grid, g, units, n_host, part, fold, s);
         else if (tiles <= 6) launch_tiles<EPI, 6, RT>(grid, g, units, n_host, part, fold, s);
@@ -463,11 +466,13 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
     return hipErrorInvalidValue;   // only the residual-add kinds split K
 }
 
-// Largest weight tile per workgroup that still gives kMfmaMinGrid workgroups
-// (four tiles only up to six column tiles: beyond, their registers would
-// halve the occupancy; eight for a gate/up projection of up to 32 routed
-// rows whose grid then fills the chip once); K split per mfma_splits, with
-// 64-row (or, beyond six column tiles, 32-row) tiles
+// Weight tiles per workgroup (up to six column tiles of routed rows; beyond,
+// the registers of four or eight tiles would halve the occupancy): for the
+// two-row kinds eight (gate/up) or four when that grid still has 192 to 256
+// (eight) or at least 192 (four) workgroups, since every workgroup re-reads
+// all routed rows; for the others the largest that keeps kMfmaMinGrid
+// workgroups.  K split per mfma_splits, with 64-row (or, beyond six column
+// tiles, 32-row) tiles.
 template <int EPI>
 static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, float* part, hipStream_t s,
                                   bool fold = false) {
@@ -485,15 +490,19 @@ static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, floa
         return launch_mfma_nt<EPI, 2>(g, units, n_host, splits, part, s);
     }
     if constexpr (EPI == EPI_SWIGLU) {
-        // up to two column tiles and a grid that fits the chip in one round
-        // of workgroups (one per CU): eight weight tiles per workgroup halve
-        // the activation re-reads against four
+        // a grid that fits the chip in one round of workgroups (one per CU):
+        // eight weight tiles per workgroup halve the activation re-reads
+        // against four (Llama-8B shape B = 32: 47.3 -> 44.0 us; 13B MHA shape
+        // B = 96: 97.9 -> 77.6 us; a second round of workgroups, Qwen-7B B = 64,
+        // 82 -> 94 us)
         const int wg8 = (units + 63) / 64;
-        if (g.rows.n_max <= 32 && wg8 >= 192 && wg8 <= 256)
-            return launch_mfma_nt<EPI, 8>(g, units, n_host, 1, nullptr, s);
+        if (wide && wg8 >= 192 && wg8 <= 256) return launch_mfma_nt<EPI, 8>(g, units, n_host, 1, nullptr, s);
     }
     if constexpr (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
-        if (wide && units / 32 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, 1, nullptr, s);
+        // four tiles once they still give 192 workgroups: with many routed
+        // rows the activation re-reads outweigh the weights (13B MHA shape,
+        // B = 96: QKV 78.1 -> 61.8 us)
+        if (wide && units / 32 >= 192) return launch_mfma_nt<EPI, 4>(g, units, n_host, 1, nullptr, s);
         return launch_mfma_nt<EPI, 2>(g, units, n_host, 1, nullptr, s);
     } else {
         if (wide && units / 64 >= kMfmaMinGrid) return launch_mfma_nt<EPI, 4>(g, units, n_host, 1, nullptr, s);
