@@ -473,6 +473,14 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
 // all routed rows; for the others the largest that keeps kMfmaMinGrid
 // workgroups.  K split per mfma_splits, with 64-row (or, beyond six column
 // tiles, 32-row) tiles.
+// A K-split launch takes 128-row tiles (the same splits) where 64-row tiles
+// would need a second round of workgroups on part of the chip and 128-row
+// ones still give 128 workgroups: the busiest CU then moves one workgroup's
+// bytes, not two (13B MHA shape, B = 96: O and down projections).
+static bool split_rows128(int units, int splits) {
+    return (units + 63) / 64 * splits > 256 && (units + 127) / 128 * splits >= 128;
+}
+
 template <int EPI>
 static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, float* part, hipStream_t s,
                                   bool fold = false) {
@@ -480,12 +488,18 @@ static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, floa
     if constexpr (EPI == EPI_ADD) {
         if (fold) {   // split sums for the next staging to add
             const int splits = mfma_fold_splits(units, g.K);
+            if (wide && split_rows128(units, splits))
+                return launch_mfma_nt<EPI, 8>(g, units, n_host, splits, part, s, 1);
             if (wide) return launch_mfma_nt<EPI, 4>(g, units, n_host, splits, part, s, 1);
             return launch_mfma_nt<EPI, 2>(g, units, n_host, splits, part, s, 1);
         }
     }
     const int splits = part ? mfma_splits(EPI, units, g.K) : 1;
     if (splits > 1) {
+        if constexpr (EPI == EPI_ADD) {
+            if (wide && split_rows128(units, splits))
+                return launch_mfma_nt<EPI, 8>(g, units, n_host, splits, part, s);
+        }
         if (wide) return launch_mfma_nt<EPI, 4>(g, units, n_host, splits, part, s);
         return launch_mfma_nt<EPI, 2>(g, units, n_host, splits, part, s);
     }

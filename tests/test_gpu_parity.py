@@ -834,6 +834,32 @@ def test_batched_steps_mfma(B, policy):
     print(B, rep)
 
 
+@pytest.mark.parametrize("B", [8, 40])
+def test_split_down_128_row_tiles(B):
+    """A K-split down projection whose 64-row tiles would need more than 256
+    workgroups (d 2560, FFN 10240: 40 x 8 splits) takes 128-row tiles with
+    the same splits; its split sums stay deferred to each sequence's next
+    block.  Two steps, mixed positions and budgets."""
+    T = 40
+    shape = dict(n_layers=4, d_model=2560, n_heads=20, n_kv_heads=4, head_dim=128, d_ffn=10240,
+                 dm_hidden=64, dm_act="silu", rope_theta=5e5, rms_eps=1e-5)
+    P = Pair(shape, "bf16", T, B, seed=61, omega=0.1, device_gen=True)
+    g = torch.Generator().manual_seed(62)
+    rep = new_report()
+    for step in range(2):
+        hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+        rng = np.random.default_rng(63 + step)
+        pos = rng.integers(0, T, size=B).tolist()
+        pos[0] = T - 1
+        ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+        x = synth.hidden_inputs(B, P.cfg["d_model"], seed=64 + step).numpy()
+        r = one_step_all(P, hk, hv, pos, ks, x)
+        for key in ("max_hidden_err", "max_kv_err"):
+            rep[key] = max(rep[key], r[key])
+    print(B, rep)
+
+
 @pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
 def test_deferred_down_sums_fixed_routes(policy):
     """MFMA path with the down projection's split sums deferred to each
