@@ -958,6 +958,31 @@ def test_gqa_attention_mfma(G, B):
     print(G, B, rep)
 
 
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+@pytest.mark.parametrize("B", [9, 24])
+def test_fp32_batches_beyond_one_staging(B, policy):
+    """fp32 weights keep the GEMV at every batch size: more routed rows than
+    one LDS staging holds loop over staging groups, split into slices over
+    the grid's second dimension (with device-read counts under the
+    device-routed policy).  Three teacher-forced steps, mixed positions and
+    budgets, fp32 tolerance."""
+    T = 24
+    P = Pair("tiny", "f32", T, B, seed=91, omega=0.1, policy=policy)
+    g = torch.Generator().manual_seed(92)
+    hk = (torch.randn(P.shape5, generator=g) * 0.5).numpy().astype(np.float32)
+    hv = (torch.randn(P.shape5, generator=g) * 0.5).numpy().astype(np.float32)
+    rng = np.random.default_rng(93)
+    pos = rng.integers(0, T - 3, size=B)
+    ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=94).numpy()
+    rep = new_report()
+    for t in range(3):
+        dk, dv = P.upload(hk), P.upload(hv)
+        out, _ = compare_step(P, hk, hv, dk, dv, x, (pos + t).tolist(), ks, rep)
+        x = out.astype(np.float32)
+    print(B, rep)
+
+
 # ------------------------------------------------ skipped-KV masking
 
 @pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
