@@ -154,69 +154,69 @@ __global__ __launch_bounds__(64 * P) void gemv_kernel(GemvArgs g, int units, int
         for (int r = 0; r < NR; ++r) ssr[r] = acc[r] = 0.f;
 #pragma unroll
         for (int pass = 0; pass < NP; ++pass) {
-        const int kb = pass * Kp, ke = NP == 1 ? K : min(K, kb + Kp);
-        if (pass > 0) __syncthreads();   // the previous pass is done with xs
+            const int kb = pass * Kp, ke = NP == 1 ? K : min(K, kb + Kp);
+            if (pass > 0) __syncthreads();   // the previous pass is done with xs
 #pragma unroll
-        for (int r = 0; r < NR; ++r) {
-            float ss = 0.f;
-            if (PRO == PRO_POOL && r < nr) {
-                // router context of sequence b: means of the pool's split sums,
-                // then the newest hidden state
-                const int b = row_seq(g.rows, i0 + r);
-                const int zdim = pooled_dim(g.ctx, g.nkv, g.hd);
-                const float inv_n = 1.0f / (float)(seq_pos(g.pos, g.pos_u, b) + 1);
-                for (int k = tid * 4; k < K; k += NT * 4) {
-                    float4 v;
-                    if (k < zdim) {
-                        v = pooled_feature4(g, b, k, inv_n);
-                    } else {
-                        v = *reinterpret_cast<const float4*>(g.h + (size_t)b * g.d + (k - zdim));
+            for (int r = 0; r < NR; ++r) {
+                float ss = 0.f;
+                if (PRO == PRO_POOL && r < nr) {
+                    // router context of sequence b: means of the pool's split sums,
+                    // then the newest hidden state
+                    const int b = row_seq(g.rows, i0 + r);
+                    const int zdim = pooled_dim(g.ctx, g.nkv, g.hd);
+                    const float inv_n = 1.0f / (float)(seq_pos(g.pos, g.pos_u, b) + 1);
+                    for (int k = tid * 4; k < K; k += NT * 4) {
+                        float4 v;
+                        if (k < zdim) {
+                            v = pooled_feature4(g, b, k, inv_n);
+                        } else {
+                            v = *reinterpret_cast<const float4*>(g.h + (size_t)b * g.d + (k - zdim));
+                        }
+                        *reinterpret_cast<float4*>(xs + r * Kp + k) = v;
                     }
-                    *reinterpret_cast<float4*>(xs + r * Kp + k) = v;
+                } else if (r < nr) {
+                    const float* xr = g.X + (size_t)row_seq(g.rows, i0 + r) * g.ldx;
+                    for (int k = kb + tid * V; k < ke; k += NT * V) {
+                        float v[V];
+#pragma unroll
+                        for (int e = 0; e < V; e += 4) {
+                            const float4 t = *reinterpret_cast<const float4*>(xr + k + e);
+                            v[e] = t.x; v[e + 1] = t.y; v[e + 2] = t.z; v[e + 3] = t.w;
+                        }
+                        if (PRO == PRO_RMSNORM) {
+                            float gv[V];
+                            St<TW>::vec(gain + k, gv);
+#pragma unroll
+                            for (int e = 0; e < V; ++e) { ss += v[e] * v[e]; v[e] *= gv[e]; }
+                        }
+#pragma unroll
+                        for (int e = 0; e < V; e += 4)
+                            *reinterpret_cast<float4*>(xs + r * Kp + (k - kb) + e) =
+                                make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
+                    }
+                } else {
+                    for (int k = kb + tid * 4; k < ke; k += NT * 4)
+                        *reinterpret_cast<float4*>(xs + r * Kp + (k - kb)) = make_float4(0.f, 0.f, 0.f, 0.f);
                 }
-            } else if (r < nr) {
-                const float* xr = g.X + (size_t)row_seq(g.rows, i0 + r) * g.ldx;
-                for (int k = kb + tid * V; k < ke; k += NT * V) {
-                    float v[V];
-#pragma unroll
-                    for (int e = 0; e < V; e += 4) {
-                        const float4 t = *reinterpret_cast<const float4*>(xr + k + e);
-                        v[e] = t.x; v[e + 1] = t.y; v[e + 2] = t.z; v[e + 3] = t.w;
-                    }
-                    if (PRO == PRO_RMSNORM) {
-                        float gv[V];
-                        St<TW>::vec(gain + k, gv);
-#pragma unroll
-                        for (int e = 0; e < V; ++e) { ss += v[e] * v[e]; v[e] *= gv[e]; }
-                    }
-#pragma unroll
-                    for (int e = 0; e < V; e += 4)
-                        *reinterpret_cast<float4*>(xs + r * Kp + (k - kb) + e) =
-                            make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
+                ssr[r] += ss;
+                if (PRO == PRO_RMSNORM && pass == NP - 1) {
+                    const float t = wave_sum(ssr[r]);
+                    if (lane == 0) s_ss[wave][r] = t;
                 }
-            } else {
-                for (int k = kb + tid * 4; k < ke; k += NT * 4)
-                    *reinterpret_cast<float4*>(xs + r * Kp + (k - kb)) = make_float4(0.f, 0.f, 0.f, 0.f);
             }
-            ssr[r] += ss;
-            if (PRO == PRO_RMSNORM && pass == NP - 1) {
-                const float t = wave_sum(ssr[r]);
-                if (lane == 0) s_ss[wave][r] = t;
-            }
-        }
-        __syncthreads();
+            __syncthreads();
 
-        // this pass's K-slices: the wavefronts whose slice it staged
-        if (NP == 1 || slice / (S / NP) == pass) {
-            const float* xw = xs + (st0 - pass * spp) * KS + lane * V;
+            // this pass's K-slices: the wavefronts whose slice it staged
+            if (NP == 1 || slice / (S / NP) == pass) {
+                const float* xw = xs + (st0 - pass * spp) * KS + lane * V;
 #pragma unroll
-            for (int q = 0; q < ML; ++q) {
-                if (q < nl && (!TAIL || (st0 + q) * KS + lane * V < K)) {
+                for (int q = 0; q < ML; ++q) {
+                    if (q < nl && (!TAIL || (st0 + q) * KS + lane * V < K)) {
 #pragma unroll
-                    for (int r = 0; r < NR; ++r) acc[r] += dot16(w[q], xw + r * Kp + q * KS, TW());
+                        for (int r = 0; r < NR; ++r) acc[r] += dot16(w[q], xw + r * Kp + q * KS, TW());
+                    }
                 }
             }
-        }
         }   // staging passes
 #pragma unroll
         for (int r = 0; r < NR; ++r) {

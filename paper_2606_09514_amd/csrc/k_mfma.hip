@@ -411,24 +411,26 @@ __global__ __launch_bounds__(256) void split_add_kernel(GemvArgs g, int units, i
 // One instantiation's launch; LDS beyond the 64 KB default (eight weight
 // tiles per workgroup) is allowed once per device.
 template <int EPI, int NT, int RT>
-static void launch_tiles(dim3 grid, const GemvArgs& g, int units, int n_host, float* part, int fold,
-                         hipStream_t s) {
+static hipError_t launch_tiles(dim3 grid, const GemvArgs& g, int units, int n_host, float* part,
+                               int fold, hipStream_t s) {
     constexpr int kGT = EPI == EPI_SWIGLU || EPI == EPI_QKV ? 2 : 1;
     constexpr int lds = mfma_lds_bytes(RT, NT, kGT);
     static_assert(lds <= 160 * 1024, "LDS of one CU");
     if constexpr (lds > 64 * 1024) {
         static std::atomic<uint64_t> attr_set{0};
         int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess) return;   // the launch below reports the error
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return e;
         const uint64_t bit = 1ull << (dev & 63);
         if (!(attr_set.load(std::memory_order_relaxed) & bit)) {
-            if (hipFuncSetAttribute(reinterpret_cast<const void*>(&mfma_kernel<EPI, NT, RT>),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
-                return;
+            e = hipFuncSetAttribute(reinterpret_cast<const void*>(&mfma_kernel<EPI, NT, RT>),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+            if (e != hipSuccess) return e;
             attr_set.fetch_or(bit, std::memory_order_relaxed);
         }
     }
     launch_main(mfma_kernel<EPI, NT, RT>, grid, dim3(256), (uint32_t)lds, s, g, units, n_host, part, fold);
+    return hipGetLastError();
 }
 
 template <int EPI, int RT>
@@ -437,24 +439,19 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
     constexpr int per = 16 * (EPI == EPI_SWIGLU || EPI == EPI_QKV ? RT / 2 : RT);
     const dim3 grid((units + per - 1) / per, splits);
     const int tiles = (g.rows.n_max + 15) / 16;
-    if (tiles <= 1) launch_tiles<EPI, 1, RT>(grid, g, units, n_host, part, fold, s);
-    else if (tiles <= 2) launch_tiles<EPI, 2, RT>(grid, g, units, n_host, part, fold, s);
-    else if (tiles <= 3) launch_tiles<EPI, 3, RT>(grid, g, units, n_host, part, fold, s);
-    else if (tiles <= 4) launch_tiles<EPI, 4, RT>(grid, g, units, n_host, part, fold, s);
-    else if constexpr (RT == 8) {
-        // eight weight tiles: at most six column tiles (registers)
-        if (tiles <= 5) launch_tiles<EPI, 5, RT>(grid, g, units, n_host, part, fold, s);
-        else if (tiles <= 6) launch_tiles<EPI, 6, RT>(grid, g, units, n_host, part, fold, s);
-        else return hipErrorInvalidValue;
+    hipError_t e;
+    if (tiles <= 1) e = launch_tiles<EPI, 1, RT>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 2) e = launch_tiles<EPI, 2, RT>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 3) e = launch_tiles<EPI, 3, RT>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 4) e = launch_tiles<EPI, 4, RT>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 5) e = launch_tiles<EPI, 5, RT>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 6) e = launch_tiles<EPI, 6, RT>(grid, g, units, n_host, part, fold, s);
+    else if constexpr (RT <= 2) {
+        if (tiles <= 7) e = launch_tiles<EPI, 7, RT>(grid, g, units, n_host, part, fold, s);
+        else e = launch_tiles<EPI, kMfmaMaxTiles, RT>(grid, g, units, n_host, part, fold, s);
     } else {
-        if (tiles <= 5) launch_tiles<EPI, 5, RT>(grid, g, units, n_host, part, fold, s);
-        else if (tiles <= 6) launch_tiles<EPI, 6, RT>(grid, g, units, n_host, part, fold, s);
-        else if constexpr (RT <= 2) {
-            if (tiles <= 7) launch_tiles<EPI, 7, RT>(grid, g, units, n_host, part, fold, s);
-            else launch_tiles<EPI, kMfmaMaxTiles, RT>(grid, g, units, n_host, part, fold, s);
-        }
+        return hipErrorInvalidValue;   // four or eight weight tiles: at most six column tiles
     }
-    hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1 || fold) return e;
     if constexpr (EPI == EPI_ADD) {
         const dim3 sg((units + 63) / 64, (g.rows.n_max + 15) / 16);
@@ -466,13 +463,6 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
     return hipErrorInvalidValue;   // only the residual-add kinds split K
 }
 
-// Weight tiles per workgroup (up to six column tiles of routed rows; beyond,
-// the registers of four or eight tiles would halve the occupancy): for the
-// two-row kinds eight (gate/up) or four when that grid still has 192 to 256
-// (eight) or at least 192 (four) workgroups, since every workgroup re-reads
-// all routed rows; for the others the largest that keeps kMfmaMinGrid
-// workgroups.  K split per mfma_splits, with 64-row (or, beyond six column
-// tiles, 32-row) tiles.
 // A K-split launch takes 128-row tiles (the same splits) where 64-row tiles
 // would need a second round of workgroups on part of the chip and 128-row
 // ones still give 128 workgroups: the busiest CU then moves one workgroup's
@@ -480,6 +470,14 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
 static bool split_rows128(int units, int splits) {
     return (units + 63) / 64 * splits > 256 && (units + 127) / 128 * splits >= 128;
 }
+
+// Weight tiles per workgroup (up to six column tiles of routed rows; beyond,
+// the registers of four or eight tiles would halve the occupancy): for the
+// two-row kinds eight (gate/up) or four when that grid still has 192 to 256
+// (eight) or at least 192 (four) workgroups, since every workgroup re-reads
+// all routed rows; for the others the largest that keeps kMfmaMinGrid
+// workgroups.  K split per mfma_splits, with 64-row (or, beyond six column
+// tiles, 32-row) tiles, or 128-row ones per split_rows128.
 
 template <int EPI>
 static hipError_t launch_mfma_epi(const GemvArgs& g, int units, int n_host, float* part, hipStream_t s,
