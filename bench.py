@@ -114,7 +114,10 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     hip.destroy(starts + stops)
     m = masks.cpu().numpy()
     kk = k_pred.cpu().numpy() if ks is None else np.array([ks] * steps)
-    step_bytes = [costmodel.step_bytes(cfg, m[t], positions[t], running_pool)
+    # the router block's attention sums the pooled rows unless masking or
+    # running sums take the pool kernel
+    fused = exec_map is None and not running_pool
+    step_bytes = [costmodel.step_bytes(cfg, m[t], positions[t], running_pool, fused)
                   for t in range(steps)]
     total_bytes = sum(s["total"] for s in step_bytes)
     assert all(int(m[t, b].sum()) == kk[t, b] for t in range(steps) for b in range(B))

@@ -68,13 +68,16 @@ def dm_weight_bytes(cfg: dict) -> int:
     return (H * din + H + Lm * H + Lm) * _s(cfg["dtype"])
 
 
-def step_bytes(cfg: dict, masks, positions, running_pool: bool = False) -> dict:
+def step_bytes(cfg: dict, masks, positions, running_pool: bool = False,
+               pool_fused: bool = False) -> dict:
     """Algorithmic bytes of one step given the realised per-sequence masks
     (each a sequence of L_mid zeros/ones for blocks S..L-2) and the positions
     written this step.
     Attention of a sequence at position p reads p + 1 cached rows; the pool
     reads the first block's rows 0..p, or with running sums (steady state)
-    the previous row, the new row and the kept fp32 sums."""
+    the previous row, the new row and the kept fp32 sums, or nothing of its
+    own when the router block's attention sums those rows as it reads them
+    (pool_fused: decode steps without skipped-KV masking or running sums)."""
     L = cfg["n_layers"]
     s = _s(cfg["dtype"])
     row = 2 * cfg["n_kv_heads"] * cfg["head_dim"] * s          # one K row + one V row
@@ -89,6 +92,8 @@ def step_bytes(cfg: dict, masks, positions, running_pool: bool = False) -> dict:
     if running_pool:
         sums = 2 * cfg["n_kv_heads"] * cfg["head_dim"] * 4
         pool = len(positions) * (2 * row + 2 * sums)
+    elif pool_fused:
+        pool = 0
     else:
         pool = sum(row * (p + 1) for p in positions)
     dmw = dm_weight_bytes(cfg)

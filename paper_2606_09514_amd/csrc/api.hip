@@ -97,8 +97,10 @@ const char* layer_base(const Model& M, const void* kv, int l) {
 
 // Position chunks per (sequence, KV head): enough workgroups to cover the
 // chip (about 2048 over the launch), chunk lengths a multiple of the rows one
-// workgroup block reads, at most kAttnMaxChunks chunks.
-void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chunk_len) {
+// workgroup block reads, at most kAttnMaxChunks chunks, or `cap` (at least
+// 1) when that is smaller.
+void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chunk_len,
+                 int cap = kAttnMaxChunks) {
     const buddy_config& c = M.cfg;
     const int rows = attention_rows_per_wg(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads);
     const int blocks = (max_pos + 1 + rows - 1) / rows;
@@ -114,6 +116,7 @@ void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chun
     int want = (2048 + pairs - 1) / pairs;
     if (want > blocks) want = blocks;
     if (want > kAttnMaxChunks) want = kAttnMaxChunks;
+    if (want > cap) want = cap;
     if (want < 1) want = 1;
     // at most kAttnMaxChunks chunks (max_ctx is bounded at create so that
     // min_chunks itself stays within it)
@@ -196,11 +199,15 @@ hipError_t mark(const Model& M, int kind, int l, bool stop, hipStream_t s) {
 // d_upto > 0: the QKV staging first adds each sequence's deferred down sums
 // from the routable blocks before list index d_upto; d_out >= 0: this
 // block's down projection leaves its split sums deferred, as routable block
-// d_out (decode rows on the MFMA path, M.ws.down_part).
+// d_out (decode rows on the MFMA path, M.ws.down_part).  pooled: for the
+// router's block, decode rows without an execution map, the attention also
+// writes the planner's pool sums (its chunks as the splits) when the chunks
+// fit the pool's split capacity; *pooled receives that split count, 0 if
+// it did not.
 buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float* hidden, int l,
                        Rows rows, int batch, int max_pos, int pos_u, const BlockBufs& bf,
                        hipStream_t s, const int32_t* groups = nullptr, int n_groups = 0,
-                       int d_upto = -1, int d_out = -1) {
+                       int d_upto = -1, int d_out = -1, int* pooled = nullptr) {
     const buddy_config& c = M.cfg;
     const buddy_layer_weights& w = M.layers[l];
     const int qdim = c.n_heads * c.head_dim;
@@ -251,7 +258,10 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
         // staging when that projection takes the tiled GEMM
         if (groups && uses_gemm(M, rows, batch, qdim, bf.tok_T)) a.xb_out = bf.xb;
     } else {
-        attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len);
+        // the router's block writing the pool's sums: no more chunks than
+        // the pool has splits
+        attn_chunks(M, rows.n_max, max_pos, &a.chunks, &a.chunk_len,
+                    pooled && !exec ? M.ws.max_pool_splits : kAttnMaxChunks);
         // decode rows on the MFMA path: o goes straight to the O
         // projection's staging, split into bf16 high and low parts as its
         // staging would
@@ -259,6 +269,14 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
     }
     a.part = M.ws.part; a.max_chunks = M.ws.max_chunks;
     a.exec = exec ? exec + (size_t)l * c.max_batch * c.max_ctx : nullptr;
+    if (pooled) {
+        *pooled = 0;
+        if (bf.tok_T == 0 && !a.exec && a.chunks <= M.ws.max_pool_splits) {
+            a.pool_part = M.ws.pool_part;
+            a.pool_max_splits = M.ws.max_pool_splits;
+            *pooled = a.chunks;
+        }
+    }
     if ((e = mark(M, BUDDY_KERNEL_ATTENTION, l, false, s)) != hipSuccess ||
         (e = mark(M, BUDDY_KERNEL_ATTN_MERGE, l, false, s)) != hipSuccess ||
         (e = launch_attention(c.dtype, a, s)) != hipSuccess ||
@@ -325,15 +343,19 @@ buddy_status run_block(Model& M, const buddy_kv* kv, const uint8_t* exec, float*
 // Router context and the Decision Module's hidden layer for every sequence:
 // split sums of the first-layer cache, then the first Decision Module GEMV,
 // which folds them into z = [mean K | mean V | h] while staging its input.
+// pooled > 0: that block's attention has already written the split sums
+// (that many splits), and the cache is not read again.
 buddy_status run_planner(Model& M, const buddy_kv* kv, const float* h, int B, int max_pos,
-                         int pos_u, bool predict, hipStream_t s) {
+                         int pos_u, bool predict, hipStream_t s, int pooled = 0) {
     const buddy_config& c = M.cfg;
     hipError_t e;
     int splits = 1;
     // the router's cache: the first block's, block S-1's with a start layer
     const void* k0 = layer_base(M, kv->k, start_layer(c) - 1);
     const void* v0 = layer_base(M, kv->v, start_layer(c) - 1);
-    if (kv->pool_sum) {
+    if (pooled > 0) {
+        splits = pooled;
+    } else if (kv->pool_sum) {
         if ((e = launch_pool_running(M, k0, v0, kv->pool_sum, kv->pool_rows, B, pos_u, s)) !=
             hipSuccess)
             return fail_device(M, e, "pool");
@@ -779,14 +801,20 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
 
     const Rows all{M.ws.idx_all, M.ws.n_all, B, true, true};
     // first block (blocks 0..S-1) on every sequence; block S-1 appends the
-    // K/V row the planner pools
+    // K/V row the planner pools, and its attention, which reads every row
+    // the pool needs, writes the pool's split sums on the way (unless the
+    // route is given, the caller keeps running sums, or the attention
+    // leaves rows out by the execution map)
+    const bool fuse_pool = !route_override && !kv->pool_sum && !exec;
+    int pooled = 0;
     for (int l = 0; l < S; ++l)
-        if ((st = run_block(M, kv, exec, hidden, l, all, B, max_pos, pos_u, decode_bufs(M), s)) !=
-            BUDDY_OK)
+        if ((st = run_block(M, kv, exec, hidden, l, all, B, max_pos, pos_u, decode_bufs(M), s, nullptr,
+                            0, -1, -1, fuse_pool && l == S - 1 ? &pooled : nullptr)) != BUDDY_OK)
             return st;
     // KV-aware planner and Decision Module, unless the route is given
     if (!route_override)
-        if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, predict, s)) != BUDDY_OK) return st;
+        if ((st = run_planner(M, kv, hidden, B, max_pos, pos_u, predict, s, pooled)) != BUDDY_OK)
+            return st;
     // Launch policy.  Device-routed: every routable block is launched and its
     // kernels read the routed row count on the device (an unused block costs
     // only empty launches).  Host-routed: the compaction kernel publishes the

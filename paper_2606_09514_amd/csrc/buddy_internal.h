@@ -509,6 +509,11 @@ struct AttnArgs {
     // consecutive tokens of one prompt, (first row index, count) pairs; one
     // workgroup per (KV head, group) (null: one per row)
     const int32_t* groups; int n_groups;
+    // decode rows of the router's block, no execution map: each workgroup
+    // also writes the column sums of the K and V rows of its chunk to the
+    // pool's partial sums, split c at pool_part [b][nkv][pool_max_splits]
+    // [K | V][hd] (the pool kernel's layout); or null
+    float* pool_part; int pool_max_splits;
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 // Cache rows one attention workgroup reads per block (chunk lengths are

@@ -66,11 +66,14 @@ __host__ __device__ constexpr int attn_rows_per_wg(int hd, int G) {
     return attn_passes(G) * 4 * (kWave / (hd / St<T>::V));
 }
 
-template <typename T, int GM, int LPR>
+// POOL: the workgroup also sums the chunk's K and V rows per column (the
+// router's pooled context, written to a.pool_part; rows past pos excluded).
+template <typename T, int GM, int LPR, bool POOL = false>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     constexpr int V = St<T>::V;
     constexpr int kAttnPasses = attn_passes(GM);
     __shared__ float s_acc[4][GM][128 + 2];
+    __shared__ float s_pool[POOL ? 4 : 1][2][128];
     const int i = blockIdx.z;
     if (!a.rows.exact && i >= *a.rows.cnt) return;
     const int b = row_seq(a.rows, i);
@@ -132,6 +135,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < V; ++e) acc[h][e] = 0.f;
     }
+    float pk[V], pv[V];   // POOL: this lane's column sums of its K and V rows
+#pragma unroll
+    for (int e = 0; e < V; ++e) pk[e] = pv[e] = 0.f;
     for (int jb = j0; jb < j1; jb += rows_wg) {
         if (jb != j0) load_block(jb);
         // all scores of the block first: the row reductions are independent
@@ -141,6 +147,14 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             float kf[V];
             unpack<T>(kr[p], kf);
             const int jrow = jb + (p * 4 + wave) * rpw + sub;
+            if constexpr (POOL) {
+                // rows past the chunk were clamped to a valid row: left out
+                const float w = jrow < j1 ? 1.f : 0.f;
+                float vv[V];
+                unpack<T>(vr[p], vv);
+#pragma unroll
+                for (int e = 0; e < V; ++e) { pk[e] += w * kf[e]; pv[e] += w * vv[e]; }
+            }
             const bool live = jrow < j1 && (er[p] != 0 || jrow == pos);
 #pragma unroll
             for (int h = 0; h < GM; ++h) {
@@ -210,7 +224,29 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             }
         }
     }
+    if constexpr (POOL) {
+        // the wavefront's row slots (lanes with equal col), then per wave
+        for (int o = lpr; o < kWave; o <<= 1)
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                pk[e] += __shfl_xor(pk[e], o, kWave);
+                pv[e] += __shfl_xor(pv[e], o, kWave);
+            }
+        if (sub == 0)
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                s_pool[wave][0][col * V + e] = pk[e];
+                s_pool[wave][1][col * V + e] = pv[e];
+            }
+    }
     __syncthreads();
+    if constexpr (POOL) {
+        float* pp = a.pool_part + (((size_t)b * a.nkv + g) * a.pool_max_splits + c) * 2 * a.hd;
+        for (int t = tid; t < 2 * a.hd; t += 256) {
+            const int which = t / a.hd, e = t - which * a.hd;
+            pp[t] = (s_pool[0][which][e] + s_pool[1][which][e]) + (s_pool[2][which][e] + s_pool[3][which][e]);
+        }
+    }
 
     // merge the four wavefronts and write this chunk's partial
     const size_t pstride = (size_t)a.hd + 2;
@@ -305,8 +341,19 @@ __device__ __forceinline__ constexpr int vmcnt_at_most(int n) {
 // nontemporal loads were slower).
 constexpr int kCpolNontemporal = 2;
 
-template <int GM, bool MASKED>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void attn_mfma_kernel(AttnArgs a) {
+// POOL (no execution map): the workgroup also sums the chunk's K and V rows
+// per column, the router's pooled context (a.pool_part).  The V sums come
+// from the P V product itself: a query head past G has q = 0, so its scores
+// are 0 and its softmax weights exactly 1 on every row of the chunk, and its
+// row of O accumulates the plain sum of the V rows.  The K sums are vector
+// adds of the K fragments already in registers.
+// (The pooling variant runs only for the router's block, one launch per
+// step; its 32 K sums per lane would spill within three waves' registers,
+// so it takes two.)
+template <int GM, bool MASKED, bool POOL = false>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(POOL ? 2 : 3))) void attn_mfma_kernel(AttnArgs a) {
+    static_assert(!(POOL && MASKED), "the pooled sums take every row of the chunk");
+    static_assert(GM < 16, "a padded query head carries the V sums");
     constexpr int HD = 128, KS = HD / 32;
     constexpr int kSlab = 16 * HD * 2;        // bytes of a 16-row V slab
     __shared__ __attribute__((aligned(16))) char s_v[4][2][kSlab];   // [wave][buffer]
@@ -382,18 +429,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
     // load tracking, which with direct-to-LDS loads pending would wait for
     // every load before the scores; the waits below cover them (in this
     // issue order the scores need all but the slab's last 4 loads, its V,
-    // done).  With a map every register load is the compiler's, and so are
-    // their waits.
+    // done).  With a map, and in the pooling variant, every register load
+    // is the compiler's, and so are their waits: the asm loads are sound
+    // only while the compiler keeps their results in place until the wait,
+    // and with the pooling variant's 32 more live registers it copied the
+    // next slab's K registers at the loop's back edge, before the wait.
     bf16x8_t kf[KS];
     uint8_t en[4];
+    // POOL: sums of this lane's K rows (row li of each slab), columns
+    // 32 s + 8 lg + e
+    float ks[KS][8];
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ks[s][e] = 0.f;
     auto load_slab = [&](int jb, int buf) {
         const int jr = min(jb + li, j1 - 1);
         const bf16_t* kp = Kb + (size_t)jr * HD + 8 * lg;
-        if constexpr (MASKED) {
+        if constexpr (MASKED || POOL) {
 #pragma unroll
             for (int s = 0; s < KS; ++s) kf[s] = *reinterpret_cast<const bf16x8_t*>(kp + 32 * s);
+            if constexpr (MASKED) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) en[v] = a.exec[(size_t)slot * a.T + min(jb + 4 * lg + v, j1 - 1)];
+                for (int v = 0; v < 4; ++v)
+                    en[v] = a.exec[(size_t)slot * a.T + min(jb + 4 * lg + v, j1 - 1)];
+            }
         } else {
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
@@ -425,6 +485,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
         for (int s = 0; s < KS; ++s) {
             d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qh[s], d, 0, 0, 0);
             d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], ql[s], d, 0, 0, 0);
+        }
+        if constexpr (POOL) {
+            // row jb + li (clamped past the chunk's end: left out)
+            const uint32_t keep = jb + li < j1 ? ~0u : 0u;
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                const uint4 w = __builtin_bit_cast(uint4, kf[s]);
+                const uint32_t x[4] = {w.x & keep, w.y & keep, w.z & keep, w.w & keep};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    ks[s][2 * e] += __uint_as_float(x[e] << 16);
+                    ks[s][2 * e + 1] += __uint_as_float(x[e] & 0xffff0000u);
+                }
+            }
         }
         __builtin_amdgcn_sched_barrier(0);   // the K registers are free only now
         const bool more = jb + 64 < j1;
@@ -493,7 +567,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void a
         s_acc[wave][lane][HD] = mrun;
         s_acc[wave][lane][HD + 1] = lrun;
     }
+    // POOL: the wave's K sums (over the 16 lanes of a row group) and V sums
+    // (O's row of head G) in its own V buffers, idle now: its last slab's
+    // loads and LDS reads are done
+    float* s_pool = reinterpret_cast<float*>(&s_v[wave][0][0]);
+    if constexpr (POOL) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ks[s][e] = row_sum16(ks[s][e]);
+        if (li == 0)
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) s_pool[32 * s + 8 * lg + e] = ks[s][e];
+        if (lg == (G >> 2)) {
+            const int eg = G & 3;
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt)
+                s_pool[HD + 16 * dt + li] = eg == 0 ? o[dt][0] : eg == 1 ? o[dt][1] : eg == 2 ? o[dt][2] : o[dt][3];
+        }
+    }
     __syncthreads();
+    if constexpr (POOL) {
+        float* pp = a.pool_part + (((size_t)b * a.nkv + g) * a.pool_max_splits + c) * 2 * HD;
+        const float* p0 = reinterpret_cast<const float*>(&s_v[0][0][0]);
+        const float* p1 = reinterpret_cast<const float*>(&s_v[1][0][0]);
+        const float* p2 = reinterpret_cast<const float*>(&s_v[2][0][0]);
+        const float* p3 = reinterpret_cast<const float*>(&s_v[3][0][0]);
+        pp[tid] = (p0[tid] + p1[tid]) + (p2[tid] + p3[tid]);   // 256 threads = 2 HD sums
+    }
 
     // merge the four wavefronts and write this chunk's partial
     const size_t pstride = (size_t)HD + 2;
@@ -810,6 +913,28 @@ int attention_rows_per_wg(int dtype, int hd, int G) {
     return dtype == BUDDY_BF16 ? attn_rows_per_wg<bf16_t>(hd, gm) : attn_rows_per_wg<float>(hd, gm);
 }
 
+// The vector score kernel for a cache dtype, head_dim and group size.
+template <bool POOL>
+static void launch_vector_attention(int dtype, int G, dim3 grid, const AttnArgs& a, hipStream_t s) {
+    if (dtype == BUDDY_BF16) {
+        if (a.hd == 128) {
+            if (G == 1) launch_main(attn_kernel<bf16_t, 1, 16, POOL>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_kernel<bf16_t, 2, 16, POOL>, grid, dim3(256), 0, s, a);
+        } else {
+            if (G <= 2) launch_main(attn_kernel<bf16_t, 2, 8, POOL>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_kernel<bf16_t, 8, 8, POOL>, grid, dim3(256), 0, s, a);
+        }
+    } else {
+        if (a.hd == 128) {
+            if (G <= 2) launch_main(attn_kernel<float, 2, 32, POOL>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_kernel<float, 8, 32, POOL>, grid, dim3(256), 0, s, a);
+        } else {
+            if (G <= 2) launch_main(attn_kernel<float, 2, 16, POOL>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_kernel<float, 8, 16, POOL>, grid, dim3(256), 0, s, a);
+        }
+    }
+}
+
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     dim3 grid(a.chunks, a.nkv, a.rows.n_max);
     const int G = a.nq / a.nkv;   // query heads per KV head, held in registers
@@ -819,30 +944,22 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
         launch_main(attn_prefill_kernel, dim3(1, a.nkv, a.n_groups), dim3(256), 0, s, a);
         return hipGetLastError();
     }
+    if (a.pool_part && (a.exec || a.tok_T > 0)) return hipErrorInvalidValue;
     if (attn_uses_mfma(dtype, a.hd, G)) {
-        if (a.exec) {
+        if (a.pool_part) {
+            if (G <= 4) launch_main(attn_mfma_kernel<4, false, true>, grid, dim3(256), 0, s, a);
+            else launch_main(attn_mfma_kernel<kMaxGroup, false, true>, grid, dim3(256), 0, s, a);
+        } else if (a.exec) {
             if (G <= 4) launch_main(attn_mfma_kernel<4, true>, grid, dim3(256), 0, s, a);
             else launch_main(attn_mfma_kernel<kMaxGroup, true>, grid, dim3(256), 0, s, a);
         } else {
             if (G <= 4) launch_main(attn_mfma_kernel<4, false>, grid, dim3(256), 0, s, a);
             else launch_main(attn_mfma_kernel<kMaxGroup, false>, grid, dim3(256), 0, s, a);
         }
-    } else if (dtype == BUDDY_BF16) {
-        if (a.hd == 128) {
-            if (G == 1) launch_main(attn_kernel<bf16_t, 1, 16>, grid, dim3(256), 0, s, a);
-            else launch_main(attn_kernel<bf16_t, 2, 16>, grid, dim3(256), 0, s, a);
-        } else {
-            if (G <= 2) launch_main(attn_kernel<bf16_t, 2, 8>, grid, dim3(256), 0, s, a);
-            else launch_main(attn_kernel<bf16_t, 8, 8>, grid, dim3(256), 0, s, a);
-        }
+    } else if (a.pool_part) {
+        launch_vector_attention<true>(dtype, G, grid, a, s);
     } else {
-        if (a.hd == 128) {
-            if (G <= 2) launch_main(attn_kernel<float, 2, 32>, grid, dim3(256), 0, s, a);
-            else launch_main(attn_kernel<float, 8, 32>, grid, dim3(256), 0, s, a);
-        } else {
-            if (G <= 2) launch_main(attn_kernel<float, 2, 16>, grid, dim3(256), 0, s, a);
-            else launch_main(attn_kernel<float, 8, 16>, grid, dim3(256), 0, s, a);
-        }
+        launch_vector_attention<false>(dtype, G, grid, a, s);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

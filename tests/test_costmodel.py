@@ -53,6 +53,9 @@ def test_step_bytes_counts_union_of_routes():
     # two sequences with disjoint routes use every layer once
     r2 = cm.step_bytes(cfg, [[1] * 15 + [0] * 15, [0] * 15 + [1] * 15], [10, 20])
     assert r2["layers_used"] == 32 and r2["weights"] == 32 * W
+    # the router block's attention summing the pooled rows: no pool reads
+    r3 = cm.step_bytes(cfg, m, [2048], pool_fused=True)
+    assert r3["pool"] == 0 and r3["total"] == r["total"] - r["pool"]
 
 
 def test_kernel_bytes_cover_the_block_weights():

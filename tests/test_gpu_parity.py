@@ -175,6 +175,57 @@ def test_router_context_many_pool_splits(ctx, dtype):
             assert np.max(np.abs(got[b] - ref)) <= 1e-5 * max(1.0, float(np.max(np.abs(ref)))), (ctx, B, pos)
 
 
+# ------------------------------------ pool sums written by the attention
+
+@pytest.mark.parametrize("case", ["tiny-f32", "tiny-bf16", "G1", "G4", "G8", "G4-long", "tiny-bf16-mfma"])
+def test_decode_step_pool_from_attention(case):
+    """In a decode step the router block's attention writes the pool's split
+    sums (its position chunks) and the planner reads no cache rows of its
+    own.  The step's scores must equal the Decision Module of the oracle's
+    context: the mean of the router block's rows 0..pos after the oracle's
+    own block-0 step, joined with its hidden state.  Cases: the vector
+    attention in fp32 and bf16 (head_dim 64), bf16 head_dim 128 with one
+    query head per KV head (vector) and four or eight (MFMA); ragged
+    positions, so that short sequences leave chunks empty; a B = 1 context
+    whose chunks are capped at the pool's split capacity (64); and a batch
+    on the MFMA projections."""
+    T, B, pos = 700, 3, [699, 37, 300]
+    if case.startswith("tiny"):
+        dtype = "f32" if case == "tiny-f32" else "bf16"
+        shape = "tiny"
+        if case == "tiny-bf16-mfma":
+            B, pos = 20, None
+    else:
+        dtype = "bf16"
+        shape = gqa_shape(int(case[1]))
+        if case == "G4-long":
+            T, B, pos = 5000, 1, [4999]
+    P = Pair(shape, dtype, T, B, seed=140, omega=0.1)
+    g = torch.Generator().manual_seed(141)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    rng = np.random.default_rng(142)
+    if pos is None:
+        pos = rng.integers(0, T, size=B).tolist()
+    ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=143).numpy()
+    _, _, sg = gpu_step(P, P.upload(hk), P.upload(hv), x, pos, ks)
+    # the oracle's hidden state after block 0 carries the projection path's
+    # error into the context: 1e-5 on the GEMV (fp32 activations), more on
+    # the MFMA path (16-bit activations); a lost or doubled chunk moves the
+    # scores by far more
+    tol = 1e-5 if P.path == "gemv" else 2e-4
+    worst = 0.0
+    for b in range(B):
+        kc, vc = hk[0, b].copy(), hv[0, b].copy()
+        h0 = P.orc.block(0, kc, vc, pos[b], x[b].astype(np.float64))
+        ref = P.orc.dm_scores(P.orc.context(kc, vc, pos[b], h0))
+        e = float(np.max(np.abs(sg[b] - ref))) / max(1.0, float(np.max(np.abs(ref))))
+        worst = max(worst, e)
+        assert e <= tol, (case, b, pos[b], e)
+    print(case, worst)
+
+
 # ------------------------------------------------ multi-step decode parity
 
 def run_teacher_forced(P, prompt, n_decode, ks, report, pool=None):
