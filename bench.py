@@ -183,15 +183,17 @@ KERNEL_KINDS = [("qkv", "KERNEL_QKV"), ("attention", "KERNEL_ATTENTION"),
 
 
 def per_kernel(model, cfg, w, dk, dv, x0, ks, hip, steps=24, warmup=2):
-    """Live launch durations of every kernel of block 0 (which runs every
-    step), from the timing hook's events on the library's stream, against
-    each kernel's algorithmic bytes per launch (attention: the score kernel
-    and the chunk merge together)."""
+    """Live launch durations of every kernel of the last block (which runs
+    every step and takes the same kernels as a routed block; the first
+    block's attention also sums the planner's pool), from the timing hook's
+    events on the library's stream, against each kernel's algorithmic bytes
+    per launch (attention: the score kernel and the chunk merge together)."""
     from paper_2606_09514_amd import costmodel
     from paper_2606_09514_amd import lib as blib
     us = {}
+    last = cfg["n_layers"] - 1
     for name, attr in KERNEL_KINDS:
-        r = run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, 0,
+        r = run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, last,
                        kernel=getattr(blib, attr))
         us[name] = r["kernel_ms"] * 1e3
     kb = costmodel.kernel_bytes(cfg, w.batch, w.ctx + warmup + steps // 2)
@@ -312,7 +314,7 @@ def main():
                     help="batched workloads timed after the headline for per_workload: 'all', "
                          "'none' or a comma list of workload names")
     ap.add_argument("--no-per-kernel", action="store_true",
-                    help="skip the live per-kernel timing passes of block 0")
+                    help="skip the live per-kernel timing passes of the last block")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: the library runs the decode step on one GPU; "
@@ -405,7 +407,7 @@ def main():
     kernels = None
     if not args.no_per_kernel and head["ks"] is not None:
         kernels = per_kernel(model, cfg, w, dk, dv, x0, head["ks"], hip)
-        log("per-kernel (block 0): " + ", ".join(
+        log("per-kernel (last block): " + ", ".join(
             f"{n} {v['us']:.1f} us {v['frac'] * 100:.0f}%" for n, v in kernels.items()))
 
     cpu = None

@@ -166,29 +166,40 @@ __device__ __forceinline__ constexpr int mfma_vmcnt(int n) {
 }
 
 // Bytes of LDS: the weight rounds (4 wavefronts x 2 buffers x RT tiles x 16
-// rows x 128 bytes), reused for the K-slice reduction afterwards.
-__host__ __device__ constexpr int mfma_lds_bytes(int rt, int nt, int gt) {
-    return 4 * 2 * rt * 2048 > 4 * gt * 16 * nt * 16 * 4 ? 4 * 2 * rt * 2048 : 4 * gt * 16 * nt * 16 * 4;
+// rows x 64 KR bytes), reused for the K-slice reduction afterwards.
+__host__ __device__ constexpr int mfma_lds_bytes(int rt, int nt, int gt, int kr = 2) {
+    return 4 * 2 * rt * 1024 * kr > 4 * gt * 16 * nt * 16 * 4 ? 4 * 2 * rt * 1024 * kr
+                                                               : 4 * gt * 16 * nt * 16 * 4;
 }
 
-// Weight stream: a round is two k-steps, 128 bytes (one cache line) of each
-// of the wavefront's 16 RT rows.  The rows move global -> LDS directly with
-// 1 KB loads of whole lines (8 rows x 128 bytes), nontemporal (read once per
-// launch), into one of two buffers while the other is used; each row's
-// 16-byte chunk c is stored at c ^ (row % 8), so that the fragment reads
-// (16 rows, one chunk each) spread over the banks.  The activation
-// fragments of a round (1 KB contiguous each) are asm register loads issued
-// at the round's start, outside the compiler's load tracking: the waits are
-// explicit (the round's weights, issued a round earlier, and activations
-// are in once no more than the next round's 2 RT weight loads are pending).
-template <int EPI, int NT, int RT>
+// Weight stream: a round is KR k-steps, 64 KR bytes of each of the
+// wavefront's 16 RT rows (KR = 2: one cache line of each row; KR = 4: two,
+// which the small grids stream markedly faster -- the longer run of each
+// row per round suits the DRAM pages better).  The rows move global -> LDS
+// directly with 1 KB loads of whole lines (1024 / (64 KR) rows each),
+// nontemporal (read once per launch), into one of two buffers while the
+// other is used; each row's 16-byte chunk c is stored at c ^ (row % (4 KR)),
+// so that the fragment reads (16 rows, one chunk each) spread over the banks.
+// The activation fragments of a round (1 KB contiguous each) are asm
+// register loads issued at the round's start, outside the compiler's load
+// tracking: the waits are explicit (the round's weights, issued a round
+// earlier, and activations are in once no more than the next round's RT KR
+// weight loads are pending).  The k-steps enter the accumulators in the
+// same order for either round length, so the sums are identical bit for bit.
+// KR = 4 needs a multiple of four k-steps per wavefront (no partial round).
+template <int EPI, int NT, int RT, int KR = 2>
 __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_host, float* part,
                                                    int fold) {
+    static_assert(KR == 2 || KR == 4, "rounds of two or four k-steps");
     constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
     constexpr int GT = kPaired ? 2 : 1;       // weight tiles per epilogue group
     constexpr int NG = RT / GT;               // epilogue groups (16 units or rows each)
-    constexpr int kBuf = RT * 2048;           // bytes of one wavefront's round
-    extern __shared__ __attribute__((aligned(16))) char s_lds[];   // mfma_lds_bytes(RT, NT, GT)
+    constexpr int kRow = 64 * KR;             // bytes of a weight row per round
+    constexpr int kCpr = kRow / 16;           // its 16-byte chunks (8 or 16)
+    constexpr int kRpi = 64 / kCpr;           // rows of one 1 KB load (8 or 4)
+    constexpr int kIpt = 16 / kRpi;           // loads per 16-row tile (2 or 4)
+    constexpr int kBuf = RT * 16 * kRow;      // bytes of one wavefront's round
+    extern __shared__ __attribute__((aligned(16))) char s_lds[];   // mfma_lds_bytes(RT, NT, GT, KR)
     auto s_red = reinterpret_cast<float (*)[GT][16][NT * 16]>(s_lds);
     const int n = n_host >= 0 ? n_host : *g.rows.cnt;
     if (n <= 0) return;
@@ -198,48 +209,54 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
     const int S = K >> 5;                     // k-steps of a row
     const int sw = S / (4 * gridDim.y);       // k-steps of a wavefront (exact)
     const int kw = (blockIdx.y * 4 + wave) * sw;   // its first k-step
-    const int nr = (sw + 1) >> 1;             // rounds; the last is half when sw is odd
+    // rounds; with KR = 2 the last is half when sw is odd
+    const int nr = (sw + KR - 1) / KR;
     const int u0 = blockIdx.x * 16 * NG;      // first unit (two-row kinds) or row
 
-    // weight rows of this lane's direct loads: tile t, half h covers rows
-    // 8 h + lane / 8 of the tile; past the end the last valid unit is read
-    // and its sums are discarded
-    const bf16_t* Ar[RT][2];
+    // weight rows of this lane's direct loads: tile t, load h covers rows
+    // kRpi h + lane / kCpr of the tile; past the end the last valid unit is
+    // read and its sums are discarded
+    const bf16_t* Ar[RT][kIpt];
 #pragma unroll
     for (int q = 0; q < NG; ++q)
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int u = min(u0 + 16 * q + 8 * h + (lane >> 3), units - 1);
+        for (int h = 0; h < kIpt; ++h) {
+            const int u = min(u0 + 16 * q + kRpi * h + lane / kCpr, units - 1);
             int r0 = u, r1 = u;
             if (kPaired) unit_rows<EPI>(g, u, r0, r1);
             Ar[q][h] = (const bf16_t*)g.W + (size_t)r0 * K + kw * 32;
             if (kPaired) Ar[NG + q][h] = (const bf16_t*)g.W + (size_t)r1 * K + kw * 32;
         }
-    // this lane's 16-byte chunk of a row line: stored chunk lane % 8 holds
-    // source chunk (lane % 8) ^ row, row % 8 = (lane / 8) % 8; a half round
-    // (64 bytes per row) loads chunks 0..3 and fills the rest with copies
-    const int csrc = (lane & 7) ^ ((lane >> 3) & 7);
+    // this lane's 16-byte chunk of a row: stored position lane % kCpr of
+    // tile row kRpi h + lane / kCpr holds source chunk position ^ row; a
+    // half round (KR = 2, 64 bytes per row) loads chunks 0..3 and fills the
+    // rest with copies
+    int csrc[kIpt];
+#pragma unroll
+    for (int h = 0; h < kIpt; ++h) csrc[h] = (lane % kCpr) ^ ((kRpi * h + lane / kCpr) % kCpr);
     const uint32_t lds_w = (uint32_t)(uintptr_t)(mfma_lptr_t)(s_lds + wave * 2 * kBuf);
     auto issue_a = [&](int r, int buf) {
-        const int c = (2 * r + 1 < sw) ? csrc : (csrc & 3);
+        const bool part_round = KR == 2 && 2 * r + 1 >= sw;
 #pragma unroll
         for (int t = 0; t < RT; ++t)
 #pragma unroll
-            for (int h = 0; h < 2; ++h)
-                __builtin_amdgcn_global_load_lds((mfma_gptr_t)(Ar[t][h] + 64 * r + 8 * c),
+            for (int h = 0; h < kIpt; ++h) {
+                const int c = part_round ? (csrc[h] & 3) : csrc[h];
+                __builtin_amdgcn_global_load_lds((mfma_gptr_t)(Ar[t][h] + 32 * KR * r + 8 * c),
                                                  (mfma_lptr_t)(s_lds + wave * 2 * kBuf + buf * kBuf +
-                                                               (16 * t + 8 * h) * 128),
+                                                               (16 * t + kRpi * h) * kRow),
                                                  16, 0, 2 /* nontemporal */);
+            }
     };
     // fragment (tile t, k-step u of the round): row 16 t + lane % 16, chunk
-    // 4 u + lane / 16, stored at that chunk ^ (row % 8)
-    uint32_t ad[RT][2];
+    // 4 u + lane / 16, stored at that chunk ^ (row % kCpr)
+    uint32_t ad[RT][KR];
 #pragma unroll
     for (int t = 0; t < RT; ++t)
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
+        for (int u = 0; u < KR; ++u) {
             const int i = lane & 15;
-            ad[t][u] = lds_w + (16 * t + i) * 128 + (((4 * u + (lane >> 4)) ^ (i & 7)) * 16);
+            ad[t][u] = lds_w + (16 * t + i) * kRow + (((4 * u + (lane >> 4)) ^ (i % kCpr)) * 16);
         }
 
     for (int j0 = 0; j0 < n; j0 += NT * 16) {   // column groups of NT tiles
@@ -261,13 +278,13 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
         issue_a(0, 0);
         for (int r = 0; r < nr; ++r) {
             const int buf = r & 1;
-            const bool half = 2 * r + 1 >= sw;
-            u32x4_t bv[2][2][NT];   // [k-step u][high, low][column tile]
+            const bool half = KR == 2 && 2 * r + 1 >= sw;
+            u32x4_t bv[KR][2][NT];   // [k-step u][high, low][column tile]
 #pragma unroll
-            for (int u = 0; u < 2; ++u)
+            for (int u = 0; u < KR; ++u)
 #pragma unroll
                 for (int c = 0; c < NT; ++c) {
-                    const bf16_t* bp = Bp[c] + 1024 * (2 * r + (half ? 0 : u));
+                    const bf16_t* bp = Bp[c] + 1024 * (KR * r + (half ? 0 : u));
                     // reads data no kernel writes while this one runs: no memory clobber
                     asm volatile("global_load_dwordx4 %0, %2, off\n\t"
                                  "global_load_dwordx4 %1, %2, off offset:1024"
@@ -275,31 +292,47 @@ __global__ __launch_bounds__(256) void mfma_kernel(GemvArgs g, int units, int n_
                 }
             if (r + 1 < nr) {
                 issue_a(r + 1, buf ^ 1);
-                __builtin_amdgcn_s_waitcnt(mfma_vmcnt(2 * RT));
+                __builtin_amdgcn_s_waitcnt(mfma_vmcnt(kIpt * RT));
             } else {
                 __builtin_amdgcn_s_waitcnt(mfma_vmcnt(0));
             }
             __builtin_amdgcn_sched_barrier(0);   // nothing reads bv or the LDS round before the wait
-            u32x4_t a[RT][2];
+            u32x4_t a[RT][KR];
 #pragma unroll
-            for (int t = 0; t < RT; ++t)
-                asm volatile(
-                    "ds_read_b128 %0, %2\n\t"
-                    "ds_read_b128 %1, %3\n\t"
-                    "s_waitcnt lgkmcnt(0)"
-                    : "=&v"(a[t][0]), "=&v"(a[t][1])
-                    : "v"(ad[t][0] + buf * kBuf), "v"(ad[t][1] + buf * kBuf)
-                    : "memory");
+            for (int t = 0; t < RT; ++t) {
+                if constexpr (KR == 2) {
+                    asm volatile(
+                        "ds_read_b128 %0, %2\n\t"
+                        "ds_read_b128 %1, %3\n\t"
+                        "s_waitcnt lgkmcnt(0)"
+                        : "=&v"(a[t][0]), "=&v"(a[t][1])
+                        : "v"(ad[t][0] + buf * kBuf), "v"(ad[t][1] + buf * kBuf)
+                        : "memory");
+                } else {
+                    asm volatile(
+                        "ds_read_b128 %0, %4\n\t"
+                        "ds_read_b128 %1, %5\n\t"
+                        "ds_read_b128 %2, %6\n\t"
+                        "ds_read_b128 %3, %7\n\t"
+                        "s_waitcnt lgkmcnt(0)"
+                        : "=&v"(a[t][0]), "=&v"(a[t][1]), "=&v"(a[t][2]), "=&v"(a[t][3])
+                        : "v"(ad[t][0] + buf * kBuf), "v"(ad[t][1] + buf * kBuf),
+                          "v"(ad[t][2] + buf * kBuf), "v"(ad[t][3] + buf * kBuf)
+                        : "memory");
+                }
+            }
             // a half round's second k-step multiplies zeros (adds exactly 0):
             // the MFMAs stay unconditional
-            const uint32_t keep = half ? 0u : ~0u;
+            if constexpr (KR == 2) {
+                const uint32_t keep = half ? 0u : ~0u;
 #pragma unroll
-            for (int c = 0; c < NT; ++c) {
-                bv[1][0][c] &= keep;
-                bv[1][1][c] &= keep;
+                for (int c = 0; c < NT; ++c) {
+                    bv[1][0][c] &= keep;
+                    bv[1][1][c] &= keep;
+                }
             }
 #pragma unroll
-            for (int u = 0; u < 2; ++u)
+            for (int u = 0; u < KR; ++u)
 #pragma unroll
                 for (int p = 0; p < 2; ++p)
 #pragma unroll
@@ -409,12 +442,12 @@ __global__ __launch_bounds__(256) void split_add_kernel(GemvArgs g, int units, i
 }
 
 // One instantiation's launch; LDS beyond the 64 KB default (eight weight
-// tiles per workgroup) is allowed once per device.
-template <int EPI, int NT, int RT>
+// tiles per workgroup, or four-k-step rounds) is allowed once per device.
+template <int EPI, int NT, int RT, int KR>
 static hipError_t launch_tiles(dim3 grid, const GemvArgs& g, int units, int n_host, float* part,
                                int fold, hipStream_t s) {
     constexpr int kGT = EPI == EPI_SWIGLU || EPI == EPI_QKV ? 2 : 1;
-    constexpr int lds = mfma_lds_bytes(RT, NT, kGT);
+    constexpr int lds = mfma_lds_bytes(RT, NT, kGT, KR);
     static_assert(lds <= 160 * 1024, "LDS of one CU");
     if constexpr (lds > 64 * 1024) {
         static std::atomic<uint64_t> attr_set{0};
@@ -423,34 +456,36 @@ static hipError_t launch_tiles(dim3 grid, const GemvArgs& g, int units, int n_ho
         if (e != hipSuccess) return e;
         const uint64_t bit = 1ull << (dev & 63);
         if (!(attr_set.load(std::memory_order_relaxed) & bit)) {
-            e = hipFuncSetAttribute(reinterpret_cast<const void*>(&mfma_kernel<EPI, NT, RT>),
+            e = hipFuncSetAttribute(reinterpret_cast<const void*>(&mfma_kernel<EPI, NT, RT, KR>),
                                     hipFuncAttributeMaxDynamicSharedMemorySize, lds);
             if (e != hipSuccess) return e;
             attr_set.fetch_or(bit, std::memory_order_relaxed);
         }
     }
-    launch_main(mfma_kernel<EPI, NT, RT>, grid, dim3(256), (uint32_t)lds, s, g, units, n_host, part, fold);
+    launch_main(mfma_kernel<EPI, NT, RT, KR>, grid, dim3(256), (uint32_t)lds, s, g, units, n_host,
+                part, fold);
     return hipGetLastError();
 }
 
-template <int EPI, int RT>
-static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int splits, float* part,
-                                 hipStream_t s, int fold = 0) {
+// The launch of a tile configuration with rounds of KR k-steps.
+template <int EPI, int RT, int KR>
+static hipError_t launch_mfma_rounds(const GemvArgs& g, int units, int n_host, int splits, float* part,
+                                     hipStream_t s, int fold) {
     constexpr int per = 16 * (EPI == EPI_SWIGLU || EPI == EPI_QKV ? RT / 2 : RT);
     const dim3 grid((units + per - 1) / per, splits);
     const int tiles = (g.rows.n_max + 15) / 16;
     hipError_t e;
-    if (tiles <= 1) e = launch_tiles<EPI, 1, RT>(grid, g, units, n_host, part, fold, s);
-    else if (tiles <= 2) e = launch_tiles<EPI, 2, RT>(grid, g, units, n_host, part, fold, s);
-    else if (tiles <= 3) e = launch_tiles<EPI, 3, RT>(grid, g, units, n_host, part, fold, s);
-    else if (tiles <= 4) e = launch_tiles<EPI, 4, RT>(grid, g, units, n_host, part, fold, s);
-    else if (tiles <= 5) e = launch_tiles<EPI, 5, RT>(grid, g, units, n_host, part, fold, s);
-    else if (tiles <= 6) e = launch_tiles<EPI, 6, RT>(grid, g, units, n_host, part, fold, s);
-    else if constexpr (RT <= 2) {
-        if (tiles <= 7) e = launch_tiles<EPI, 7, RT>(grid, g, units, n_host, part, fold, s);
-        else e = launch_tiles<EPI, kMfmaMaxTiles, RT>(grid, g, units, n_host, part, fold, s);
+    if (tiles <= 1) e = launch_tiles<EPI, 1, RT, KR>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 2) e = launch_tiles<EPI, 2, RT, KR>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 3) e = launch_tiles<EPI, 3, RT, KR>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 4) e = launch_tiles<EPI, 4, RT, KR>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 5) e = launch_tiles<EPI, 5, RT, KR>(grid, g, units, n_host, part, fold, s);
+    else if (tiles <= 6) e = launch_tiles<EPI, 6, RT, KR>(grid, g, units, n_host, part, fold, s);
+    else if constexpr (RT <= 2 && KR == 2) {
+        if (tiles <= 7) e = launch_tiles<EPI, 7, RT, KR>(grid, g, units, n_host, part, fold, s);
+        else e = launch_tiles<EPI, kMfmaMaxTiles, RT, KR>(grid, g, units, n_host, part, fold, s);
     } else {
-        return hipErrorInvalidValue;   // four or eight weight tiles: at most six column tiles
+        return hipErrorInvalidValue;   // four or eight weight tiles, or long rounds: at most six column tiles
     }
     if (e != hipSuccess || splits == 1 || fold) return e;
     if constexpr (EPI == EPI_ADD) {
@@ -461,6 +496,26 @@ static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int s
         return hipGetLastError();
     }
     return hipErrorInvalidValue;   // only the residual-add kinds split K
+}
+
+// Rounds of four k-steps (two cache lines of each weight row) where the
+// tile keeps the LDS of a workgroup within 64 KB (at most two weight tiles),
+// the batch within four column tiles (beyond, the round's activation
+// registers push the compiler into spilling, and a spill of an untracked
+// load's registers before its wait would read data not yet arrived), and
+// every wavefront's k-steps split into whole rounds.
+inline bool mfma_long_rounds(int rt, int K, int splits, int n_max) {
+    return rt <= 2 && (n_max + 15) / 16 <= 4 && (K / 32) % (16 * splits) == 0;
+}
+
+template <int EPI, int RT>
+static hipError_t launch_mfma_nt(const GemvArgs& g, int units, int n_host, int splits, float* part,
+                                 hipStream_t s, int fold = 0) {
+    if constexpr (RT <= 2) {
+        if (mfma_long_rounds(RT, g.K, splits, g.rows.n_max))
+            return launch_mfma_rounds<EPI, RT, 4>(g, units, n_host, splits, part, s, fold);
+    }
+    return launch_mfma_rounds<EPI, RT, 2>(g, units, n_host, splits, part, s, fold);
 }
 
 // A K-split launch takes 128-row tiles (the same splits) where 64-row tiles

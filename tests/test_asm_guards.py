@@ -1,16 +1,24 @@
-"""Static check of the gfx950 code hipcc emits for the decode attention's
-MFMA score kernel (no GPU needed).
+"""Static check of the gfx950 code hipcc emits for the kernels that load
+through inline asm (no GPU needed).
 
-Without an execution map the kernel loads each slab's K fragments with
-inline-asm loads that the compiler does not track, and waits for them
-itself (s_waitcnt) just before the score MFMAs.  That is sound only while
-the compiler leaves the loaded registers where the asm put them until the
-wait: a copy of them (for instance at the loop's back edge, when the next
-slab's loads went to other registers) would read data that has not arrived.
-So every asm K load must write registers that the score MFMAs read as their
-A operand directly.  A variant with 32 more live registers broke exactly
-this (NaN scores once a wavefront took two slabs), which is why that variant
-uses compiler-tracked loads instead."""
+The decode attention's MFMA score kernel (K fragments) and the MFMA
+projection kernel (activation fragments) issue some vector-memory loads as
+inline asm, outside the compiler's load tracking, and wait for them with
+their own s_waitcnt.  That is sound only while the compiler leaves the
+loaded registers alone until the wait: an instruction that reads such a
+register earlier -- a copy at a loop's back edge, a spill into an
+accumulation register -- takes data that has not arrived, and one that
+writes it is overwritten when the load lands.  So in every instantiation,
+from each asm load to the next s_waitcnt with a vmcnt (the kernels' own
+waits cover their asm loads), no instruction may touch its destination
+registers.  The walk is linear through the function, which matches these
+kernels, whose loads and waits share a basic block.
+
+Two earlier builds that gave wrong results both fail this check: a pooling
+variant of the attention whose compiler copied the next slab's K at the
+loop's back edge (NaN once a wavefront took two slabs), and four-k-step
+projection rounds with six column tiles, whose registers spilled into
+accumulation registers before the wait."""
 import os
 import re
 import subprocess
@@ -20,49 +28,129 @@ import pytest
 
 from paper_2606_09514_amd import build as hip_build
 
-SRC = os.path.join(hip_build.CSRC, "k_attn.hip")
-KERNELS = [f"_ZN5buddy16attn_mfma_kernelILi{g}ELb0ELb0EEEvNS_8AttnArgsE" for g in (4, 8)]
+SOURCES = {"k_attn.hip": "_ZN5buddy16attn_mfma_kernel", "k_mfma.hip": "_ZN5buddy11mfma_kernel"}
+REG = re.compile(r"\bv(\d+)\b|\bv\[(\d+):(\d+)\]")
 
 
-@pytest.fixture(scope="module")
-def device_asm():
-    if not os.path.exists(hip_build.HIPCC):
-        pytest.skip("hipcc not available")
+def device_asm(src: str) -> str:
     flags = [f for f in hip_build.FLAGS if f != "-fPIC"]
     with tempfile.TemporaryDirectory() as d:
-        out = os.path.join(d, "k_attn.s")
-        subprocess.run([hip_build.HIPCC, *flags, "--cuda-device-only", "-S", SRC, "-o", out],
+        out = os.path.join(d, "k.s")
+        subprocess.run([hip_build.HIPCC, *flags, "--cuda-device-only", "-S",
+                        os.path.join(hip_build.CSRC, src), "-o", out],
                        check=True, capture_output=True)
         with open(out) as f:
             return f.read()
 
 
-def function_body(asm: str, name: str) -> list:
-    start = asm.index(f"\n{name}:")
-    end = asm.index(".Lfunc_end", start)
-    return asm[start:end].splitlines()
-
-
-@pytest.mark.parametrize("name", KERNELS)
-def test_asm_k_loads_feed_the_score_mfma_directly(device_asm, name):
-    lines = function_body(device_asm, name)
-    in_asm, k_dst, a_ops = False, [], set()
-    for ln in lines:
-        s = ln.strip()
-        if s.startswith(";;#ASMSTART"):
-            in_asm = True
-        elif s.startswith(";;#ASMEND"):
-            in_asm = False
-        elif in_asm:
-            m = re.match(r"global_load_dwordx4 (v\[\d+:\d+\]),", s)
-            if m:
-                k_dst.append(m.group(1))
+def vregs(operand: str) -> set:
+    out = set()
+    for m in REG.finditer(operand):
+        if m.group(1):
+            out.add(int(m.group(1)))
         else:
-            m = re.match(r"v_mfma_f32_16x16x32_bf16 v\[\d+:\d+\], (v\[\d+:\d+\]),", s)
-            if m:
-                a_ops.add(m.group(1))
-    # the first slab's four loads and the loop's four
-    assert len(k_dst) >= 8, k_dst
-    assert len(a_ops) == 4, a_ops
-    stray = [r for r in k_dst if r not in a_ops]
-    assert not stray, f"asm K loads into {stray}, score MFMAs read {sorted(a_ops)}"
+            out.update(range(int(m.group(2)), int(m.group(3)) + 1))
+    return out
+
+
+def operands(text: str):
+    parts = text.split(None, 1)
+    if len(parts) == 1:
+        return parts[0], []
+    ops, depth, cur = [], 0, ""
+    for ch in parts[1]:
+        depth += ch == "["
+        depth -= ch == "]"
+        if ch == "," and depth == 0:
+            ops.append(cur.strip())
+            cur = ""
+        else:
+            cur += ch
+    if cur.strip():
+        ops.append(cur.strip())
+    return parts[0], ops
+
+
+def hazards(lines) -> list:
+    """Instructions that read or write an asm load's registers before the
+    next vmcnt wait."""
+    in_asm, pending, bad = False, set(), []
+    for ln in lines:
+        raw = ln.strip()
+        if raw.startswith(";;#ASMSTART"):
+            in_asm = True
+            continue
+        if raw.startswith(";;#ASMEND"):
+            in_asm = False
+            continue
+        text = ln.split(";")[0].strip()
+        if not text or text.endswith(":") or text.startswith("."):
+            continue
+        op, ops = operands(text)
+        if op == "s_waitcnt" and "vmcnt" in text:
+            pending.clear()
+            continue
+        if in_asm and op == "global_load_dwordx4":
+            pending |= vregs(ops[0])
+            continue
+        if op.startswith("s_") or not ops:
+            continue
+        store = not op.startswith("v_") and any(k in op for k in ("store", "ds_write", "atomic"))
+        touched = set().union(*[vregs(o) for o in ops])
+        if not store:
+            touched |= vregs(ops[0])
+        if touched & pending:
+            bad.append(text)
+    return bad
+
+
+@pytest.fixture(scope="module")
+def kernels():
+    if not os.path.exists(hip_build.HIPCC):
+        pytest.skip("hipcc not available")
+    out = {}
+    for src, prefix in SOURCES.items():
+        asm = device_asm(src)
+        for m in re.finditer(r"^(" + re.escape(prefix) + r"\S*):", asm, re.M):
+            start = m.end()
+            out[m.group(1)] = asm[start:asm.index(".Lfunc_end", start)].splitlines()
+    return out
+
+
+def test_every_asm_load_instantiation_is_checked(kernels):
+    # the attention's four instantiations (two group sizes, masked and not,
+    # pooling) and every MFMA projection tiling
+    assert sum(k.startswith(SOURCES["k_attn.hip"]) for k in kernels) >= 4
+    assert sum(k.startswith(SOURCES["k_mfma.hip"]) for k in kernels) >= 60
+    asm_loads = sum(1 for body in kernels.values() for ln in body
+                    if ln.strip().startswith("global_load_dwordx4") and "off" in ln)
+    assert asm_loads > 0
+
+
+def test_no_register_of_an_untracked_load_is_touched_before_its_wait(kernels):
+    bad = {name: h[:3] for name, body in kernels.items() if (h := hazards(body))}
+    assert not bad, bad
+
+
+def test_attention_k_loads_feed_the_score_mfma_directly(kernels):
+    # the unmasked score kernels: the asm K loads write the score MFMA's A
+    # operands themselves (no copy at all)
+    for g in (4, 8):
+        body = kernels[f"_ZN5buddy16attn_mfma_kernelILi{g}ELb0ELb0EEEvNS_8AttnArgsE"]
+        in_asm, k_dst, a_ops = False, [], set()
+        for ln in body:
+            s = ln.strip()
+            if s.startswith(";;#ASMSTART"):
+                in_asm = True
+            elif s.startswith(";;#ASMEND"):
+                in_asm = False
+            elif in_asm:
+                m = re.match(r"global_load_dwordx4 (v\[\d+:\d+\]),", s)
+                if m:
+                    k_dst.append(m.group(1))
+            else:
+                m = re.match(r"v_mfma_f32_16x16x32_bf16 v\[\d+:\d+\], (v\[\d+:\d+\]),", s)
+                if m:
+                    a_ops.add(m.group(1))
+        assert len(k_dst) >= 8 and len(a_ops) == 4, (k_dst, a_ops)
+        assert set(k_dst) <= a_ops, (k_dst, sorted(a_ops))
