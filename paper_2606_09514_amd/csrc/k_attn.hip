@@ -15,6 +15,11 @@
 // execution map is given: then rows at which the block did not run are left
 // out of the softmax (the new row at pos always counts: the block runs for
 // it, and the first block's entry is written only after its attention).
+// In a decode step the router's block (the first, or the one before the
+// start layer) reads exactly the rows the planner pools (Sec. 4.3: the mean
+// of that block's K and V rows 0..pos), so its workgroups also write the
+// column sums of their chunk's K and V rows in the pool's partial-sum
+// layout, and the cache is not read a second time (the pooling variants).
 //
 // Two score kernels:
 //  attn_kernel       vector ALUs: a cache row of hd elements is read by hd/V
