@@ -885,6 +885,40 @@ def test_batched_steps_mfma(B, policy):
     print(B, rep)
 
 
+def long_round_shape():
+    """A small bf16 decoder whose QKV and gate/up projections (K = 512, two
+    weight tiles per workgroup) stream four k-steps of weights per round on
+    the MFMA path; the K-split O and down projections keep two-k-step rounds.
+    Head_dim 128 with four query heads per KV head puts the attention on the
+    MFMA score kernel (and its pooling variant for block 0)."""
+    return dict(n_layers=5, d_model=512, n_heads=4, n_kv_heads=1, head_dim=128, d_ffn=1536,
+                dm_hidden=64, dm_act="silu", rope_theta=1e4, rms_eps=1e-5)
+
+
+@pytest.mark.parametrize("policy", [p for _, p in POLICIES], ids=[n for n, _ in POLICIES])
+@pytest.mark.parametrize("B", [24, 60, 70])
+def test_mfma_four_step_rounds(B, policy):
+    """Two and four column tiles of routed rows take the four-k-step weight
+    rounds (whose sums equal the two-k-step rounds' bit for bit), five
+    column tiles the two-k-step ones; both against the oracle, with mixed
+    positions and budgets over two teacher-forced steps."""
+    T = 96
+    P = Pair(long_round_shape(), "bf16", T, B, seed=150, omega=0.1, policy=policy)
+    g = torch.Generator().manual_seed(151)
+    hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    hv = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
+    rng = np.random.default_rng(152)
+    pos = rng.integers(0, T - 2, size=B).tolist()
+    ks = rng.integers(0, P.L_mid + 1, size=B).tolist()
+    x = synth.hidden_inputs(B, P.cfg["d_model"], seed=153).numpy()
+    dk, dv = P.upload(hk), P.upload(hv)
+    rep = new_report()
+    for step in range(2):
+        x = compare_step(P, hk, hv, dk, dv, x, [p + step for p in pos], ks, rep)[0]
+        dk.copy_(P.upload(hk)); dv.copy_(P.upload(hv))
+    print(B, rep)
+
+
 @pytest.mark.parametrize("B", [8, 40])
 def test_split_down_128_row_tiles(B):
     """A K-split down projection whose 64-row tiles would need more than 256
