@@ -100,6 +100,9 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     # an event between consecutive steps on the launch stream: the first and
     # last bracket the timed region, the others give per-step times
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    # host CPU time of the process over the timed steps (the host-routed
+    # launch policy waits for each step's route)
+    cpu0 = time.process_time()
     evs[0].record()
     for t in range(steps):
         step(pos, t)
@@ -107,6 +110,7 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
         positions.append([pos] * B)
         pos += 1
     torch.cuda.synchronize()
+    cpu_ms = (time.process_time() - cpu0) * 1e3
     model.set_timing_events(kernel, kernel_layer, [], [])
     total_ms = evs[0].elapsed_time(evs[steps])
     step_ms = np.array([evs[t].elapsed_time(evs[t + 1]) for t in range(steps)])
@@ -142,6 +146,7 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
                 step_ms_p50=float(np.percentile(step_ms, 50)),
                 step_ms_p90=float(np.percentile(step_ms, 90)),
                 tokens_per_s=B * steps / (total_ms / 1e3),
+                host_cpu_ms_per_step=cpu_ms / steps,
                 bytes_per_step=total_bytes / steps,
                 step_hbm_frac=total_bytes / (total_ms / 1e3) / 1e9 / PEAK_HBM_GBS,
                 layers_used=sum(s["layers_used"] for s in step_bytes) / steps,
@@ -392,7 +397,8 @@ def main():
         runs[name] = r
         log(f"k={name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step "
             f"(p50 {r['step_ms_p50']:.3f}, p90 {r['step_ms_p90']:.3f}), "
-            f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline, gate_up {r['kernel_ms'] * 1e3:.1f} us")
+            f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline, gate_up {r['kernel_ms'] * 1e3:.1f} us, "
+            f"host CPU {r['host_cpu_ms_per_step']:.3f} ms/step")
 
     head = runs[next(iter(runs))]
     head_k = budgets[0] if not (w.mixed or args.auto_budget) else None
@@ -460,7 +466,8 @@ def main():
                            "layers_used": r["layers_used"],
                            "distinct_routes": r["distinct_routes"],
                            "mean_k": round(r["mean_k"], 2),
-                           "gate_up_us": round(r["kernel_ms"] * 1e3, 2)}
+                           "gate_up_us": round(r["kernel_ms"] * 1e3, 2),
+                           "host_cpu_ms_per_step": round(r["host_cpu_ms_per_step"], 3)}
                        for n, r in runs.items()},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),

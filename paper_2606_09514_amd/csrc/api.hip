@@ -11,6 +11,7 @@
 #include <chrono>
 #include <mutex>
 #include <new>
+#include <thread>
 
 #include <vector>
 
@@ -407,15 +408,40 @@ buddy_status prepare_step(Model& M, const int32_t* pos, const int32_t* k, int B,
     return BUDDY_OK;
 }
 
-// Host-routed launches: spin until the compaction kernel has published the
+// Host-routed launches: wait until the compaction kernel has published the
 // counts of step `seq` to mapped host memory.  A device error, or no answer
 // within a minute, ends the wait with BUDDY_EDEVICE.  The stream is queried
 // for errors every 100 ms only: a query leaves the next kernel launch on the
 // stream 15-20 us slower on the host, and that launch is the one the idle
-// device waits for (a step's route takes about a millisecond).
+// device waits for (a step's route takes about a millisecond).  The host
+// does not spin for the whole wait: when a step follows the previous one
+// back to back (the device is still running that step's blocks), its route
+// comes about as long after the call as the previous step's did, so the
+// thread sleeps until a margin before that time and spins from there.  A
+// route already published on waking halves the next expected wait;
+// otherwise the measured wait becomes the next one's expectation.  After a
+// pause between steps the device has drained and the route comes at once:
+// no sleep.
+constexpr int64_t kRouteSpinMarginNs = 150000;
+constexpr int64_t kBackToBackNs = 300000;
+
+int64_t steady_ns() {
+    return std::chrono::duration_cast<std::chrono::nanoseconds>(
+               std::chrono::steady_clock::now().time_since_epoch()).count();
+}
+
 buddy_status wait_route(Model& M, int32_t seq, hipStream_t s) {
     volatile int32_t* flag = M.h_cnt + n_mid(M.cfg);
     const auto t0 = std::chrono::steady_clock::now();
+    const bool back_to_back = M.step_end_ns > 0 && steady_ns() - M.step_end_ns < kBackToBackNs;
+    if (back_to_back && M.route_wait_ns > 2 * kRouteSpinMarginNs && *flag != seq) {
+        std::this_thread::sleep_for(std::chrono::nanoseconds(M.route_wait_ns - kRouteSpinMarginNs));
+        if (*flag == seq) {
+            M.route_wait_ns /= 2;   // woke late: expect less next time
+            std::atomic_thread_fence(std::memory_order_acquire);
+            return BUDDY_OK;
+        }
+    }
     auto next_check = t0 + std::chrono::milliseconds(100);
     while (*flag != seq) {
         const auto now = std::chrono::steady_clock::now();
@@ -429,6 +455,8 @@ buddy_status wait_route(Model& M, int32_t seq, hipStream_t s) {
         }
     }
     std::atomic_thread_fence(std::memory_order_acquire);
+    M.route_wait_ns = std::chrono::duration_cast<std::chrono::nanoseconds>(
+                          std::chrono::steady_clock::now() - t0).count();
     return BUDDY_OK;
 }
 
@@ -860,6 +888,7 @@ buddy_status decode_impl(buddy_model* h, const buddy_kv* kv, float* hidden, cons
     st = run_block(M, kv, exec, hidden, c.n_layers - 1, all, B, max_pos, pos_u, decode_bufs(M), s,
                    nullptr, 0, defer ? Lm : -1, -1);
     if (M.timing.n > 0 && M.timing.next < M.timing.n) ++M.timing.next;
+    M.step_end_ns = steady_ns();
     return st;
 }
 

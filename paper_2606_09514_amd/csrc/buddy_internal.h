@@ -183,6 +183,8 @@ struct Model {
     int32_t* h_cnt;               // mapped pinned host memory: [L-2] counts, then a sequence number
     int32_t* d_host_cnt;          // device address of h_cnt
     int32_t seq;                  // sequence number of the last published route
+    int64_t route_wait_ns;        // how long the host-routed wait is expected to take (0: unknown)
+    int64_t step_end_ns;          // steady-clock time the last decode step's enqueue ended (0: none)
     buddy_layer_weights* layers;  // host array of device pointers
     buddy_dm_weights dm;
     buddy_predictor_weights pred;  // Budget Predictor head (pred.hidden == 0: none)
