@@ -177,7 +177,8 @@ def test_router_context_many_pool_splits(ctx, dtype):
 
 # ------------------------------------ pool sums written by the attention
 
-@pytest.mark.parametrize("case", ["tiny-f32", "tiny-bf16", "G1", "G4", "G8", "G4-long", "tiny-bf16-mfma"])
+@pytest.mark.parametrize("case", ["tiny-f32", "tiny-bf16", "G1", "G4", "G8", "G4-long", "tiny-bf16-mfma",
+                                  "tiny-bf16-S2", "G4-S3"])
 def test_decode_step_pool_from_attention(case):
     """In a decode step the router block's attention writes the pool's split
     sums (its position chunks) and the planner reads no cache rows of its
@@ -187,19 +188,24 @@ def test_decode_step_pool_from_attention(case):
     attention in fp32 and bf16 (head_dim 64), bf16 head_dim 128 with one
     query head per KV head (vector) and four or eight (MFMA); ragged
     positions, so that short sequences leave chunks empty; a B = 1 context
-    whose chunks are capped at the pool's split capacity (64); and a batch
-    on the MFMA projections."""
+    whose chunks are capped at the pool's split capacity (64); a batch on
+    the MFMA projections; and start layers 2 and 3, where the router's block
+    is block 1 or 2 (vector and MFMA attention)."""
     T, B, pos = 700, 3, [699, 37, 300]
     if case.startswith("tiny"):
         dtype = "f32" if case == "tiny-f32" else "bf16"
         shape = "tiny"
         if case == "tiny-bf16-mfma":
             B, pos = 20, None
+        if case == "tiny-bf16-S2":
+            shape = dict(synth.SHAPES["tiny"], start_layer=2)
     else:
         dtype = "bf16"
         shape = gqa_shape(int(case[1]))
         if case == "G4-long":
             T, B, pos = 5000, 1, [4999]
+        if case == "G4-S3":
+            shape = dict(shape, start_layer=3, n_layers=6)
     P = Pair(shape, dtype, T, B, seed=140, omega=0.1)
     g = torch.Generator().manual_seed(141)
     hk = synth.storage_numpy(torch.randn(P.shape5, generator=g).to(P.tdt))
@@ -216,9 +222,14 @@ def test_decode_step_pool_from_attention(case):
     # scores by far more
     tol = 1e-5 if P.path == "gemv" else 2e-4
     worst = 0.0
+    S = P.orc.start_layer
     for b in range(B):
-        kc, vc = hk[0, b].copy(), hv[0, b].copy()
-        h0 = P.orc.block(0, kc, vc, pos[b], x[b].astype(np.float64))
+        # the oracle's blocks 0..S-1 on this sequence, then the context from
+        # block S-1's rows (its new row included) and hidden state
+        h0 = x[b].astype(np.float64)
+        for l in range(S):
+            kc, vc = hk[l, b].copy(), hv[l, b].copy()
+            h0 = P.orc.block(l, kc, vc, pos[b], h0)
         ref = P.orc.dm_scores(P.orc.context(kc, vc, pos[b], h0))
         e = float(np.max(np.abs(sg[b] - ref))) / max(1.0, float(np.max(np.abs(ref))))
         worst = max(worst, e)
