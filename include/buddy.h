@@ -350,7 +350,9 @@ buddy_status buddy_set_launch_policy(buddy_model* m, int32_t policy);
 /* Output tile of the prefill's tiled projections (bf16 weights, many prompt
  * tokens).
  *   BUDDY_GEMM_TILE_AUTO (default): 256 x 256 where that still gives every
- *     CU two workgroups; for the residual-add projections (O, down) whose
+ *     CU two workgroups (when the last round of such a grid would leave CUs
+ *     idle, its weight rows go to a second launch of 128 x 128 tiles that
+ *     fits one round); for the residual-add projections (O, down) whose
  *     256 x 256 grid is smaller, 256 x 256 with K split in two halves whose
  *     sums are added to the residual in a fixed order; else 128 x 128;
  *   BUDDY_GEMM_TILE_128, BUDDY_GEMM_TILE_256: always that tile (weight

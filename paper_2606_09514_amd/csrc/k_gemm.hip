@@ -20,7 +20,8 @@
 //     from the activations, which the staging kernel already wrote in
 //     B-operand order (16 rows x 32 k per contiguous KB).
 // Tiles travel straight from memory to LDS (global_load_lds) three K steps
-// ahead of the multiply (four buffers, one barrier per step).
+// ahead of the multiply (four buffers, one barrier per step); each row
+// tile's MFMAs start as soon as its own fragment read has landed.
 //   D[i][j] (16 x 16): lane j + 16 (i / 4), element i % 4.
 #include "buddy_internal.h"
 #include "epilogue.h"
@@ -43,39 +44,73 @@ constexpr int kBufs = 4;                         // K steps in LDS, three ahead
 // 15:14, expcnt 6:4, lgkmcnt 11:8).
 constexpr int vmcnt_at_most(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-// LDS reads of 16 bytes at address a (and b) plus immediate offsets, then a
-// wait for them.  Written as asm so that the compiler, which cannot tell the
-// direct-to-LDS loads into the other buffers from these reads, does not make
-// them wait for every load in flight.
+// Fragment reads from LDS: 16 bytes at address a (or b) plus immediate
+// offsets, issued without a wait.  Written as asm so that the compiler, which
+// cannot tell the direct-to-LDS loads into the other buffers from these
+// reads, does not make them wait for every load in flight.  LDS reads return
+// in issue order, so after a step's reads (the B fragments, then the A
+// fragments in row-tile order) lgkmcnt(n) means that all but the last n have
+// landed, and the MFMAs of row tile i can start once TI - 1 - i reads remain
+// (lds_wait): the first MFMAs wait for 4 + 1 reads, not for all of them.
+// Other counted operations the compiler issues only make such a wait longer.
+// Until its wait, the compiler believes a read's registers written: the wait
+// takes them as operands it modifies, so that nothing reads them earlier.
 template <int O0, int O1, int O2, int O3>
-__device__ __forceinline__ void lds_read4(uint32_t a, u32x4_t* x) {
+__device__ __forceinline__ void lds_issue4(uint32_t a, u32x4_t* x) {
     asm volatile(
         "ds_read_b128 %0, %4 offset:%5\n\t"
         "ds_read_b128 %1, %4 offset:%6\n\t"
         "ds_read_b128 %2, %4 offset:%7\n\t"
-        "ds_read_b128 %3, %4 offset:%8\n\t"
-        "s_waitcnt lgkmcnt(0)"
+        "ds_read_b128 %3, %4 offset:%8"
         : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3])
         : "v"(a), "i"(O0), "i"(O1), "i"(O2), "i"(O3)
         : "memory");
 }
-template <int O0, int O1, int O2, int O3, int P0, int P1, int P2, int P3>
-__device__ __forceinline__ void lds_read8(uint32_t a, uint32_t b, u32x4_t* x, u32x4_t* y) {
+// B fragments at b + 0, 1, 2, 3 KB, then A fragments at a + O0 .. O3
+template <int O0, int O1, int O2, int O3>
+__device__ __forceinline__ void lds_issue8(uint32_t a, uint32_t b, u32x4_t* x, u32x4_t* y) {
     asm volatile(
+        "ds_read_b128 %4, %9 offset:0\n\t"
+        "ds_read_b128 %5, %9 offset:1024\n\t"
+        "ds_read_b128 %6, %9 offset:2048\n\t"
+        "ds_read_b128 %7, %9 offset:3072\n\t"
         "ds_read_b128 %0, %8 offset:%10\n\t"
         "ds_read_b128 %1, %8 offset:%11\n\t"
         "ds_read_b128 %2, %8 offset:%12\n\t"
-        "ds_read_b128 %3, %8 offset:%13\n\t"
-        "ds_read_b128 %4, %9 offset:%14\n\t"
-        "ds_read_b128 %5, %9 offset:%15\n\t"
-        "ds_read_b128 %6, %9 offset:%16\n\t"
-        "ds_read_b128 %7, %9 offset:%17\n\t"
-        "s_waitcnt lgkmcnt(0)"
+        "ds_read_b128 %3, %8 offset:%13"
         : "=&v"(x[0]), "=&v"(x[1]), "=&v"(x[2]), "=&v"(x[3]), "=&v"(y[0]), "=&v"(y[1]),
           "=&v"(y[2]), "=&v"(y[3])
-        : "v"(a), "v"(b), "i"(O0), "i"(O1), "i"(O2), "i"(O3), "i"(P0), "i"(P1), "i"(P2),
-          "i"(P3)
+        : "v"(a), "v"(b), "i"(O0), "i"(O1), "i"(O2), "i"(O3)
         : "memory");
+}
+template <int N>
+__device__ __forceinline__ void lds_wait(u32x4_t& r) {
+    asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(r) : "i"(N));
+}
+template <int N>
+__device__ __forceinline__ void lds_wait(u32x4_t& r, u32x4_t* y) {
+    asm volatile("s_waitcnt lgkmcnt(%5)"
+                 : "+v"(r), "+v"(y[0]), "+v"(y[1]), "+v"(y[2]), "+v"(y[3])
+                 : "i"(N));
+}
+
+// One K step's MFMAs, row tile I onwards: each row tile after its own read
+// (and, for the first, the B fragments') has landed.
+template <int I, int TI, int TJ>
+__device__ __forceinline__ void mfma_rows(f32x4_t (&acc)[TI][TJ], u32x4_t* a, u32x4_t* bv) {
+    if constexpr (I == 0)
+        lds_wait<TI - 1>(a[0], bv);
+    else
+        lds_wait<TI - 1 - I>(a[I]);
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+        acc[I][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8_t, a[I]), __builtin_bit_cast(bf16x8_t, bv[j]), acc[I][j], 0,
+            0, 0);
+    // keep the next row tile's wait behind these MFMAs (the scheduler would
+    // otherwise gather the waits ahead of them)
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (I + 1 < TI) mfma_rows<I + 1>(acc, a, bv);
 }
 
 template <int WM, int WN, int TI, int TJ>
@@ -93,7 +128,7 @@ struct GemmShape {
 
 template <int EPI, int WM, int WN, int TI, int TJ>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void gemm_kernel(GemvArgs g, int units, int n, float* part) {
+void gemm_kernel(GemvArgs g, int units, int n, float* part, int ubase) {
     using Sh = GemmShape<WM, WN, TI, TJ>;
     constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
     __shared__ __attribute__((aligned(16))) char s_buf[kBufs * Sh::kBufBytes];
@@ -103,7 +138,7 @@ void gemm_kernel(GemvArgs g, int units, int n, float* part) {
     // split K (part != null): workgroup z takes K steps [z nk, (z + 1) nk)
     // and writes its fp32 sums to part[z][row][unit] for a separate add
     const int K = g.K, S = K >> 5, nk = K / kTileK / gridDim.z, k0 = blockIdx.z * nk;
-    const int u0 = blockIdx.x * (kPaired ? Sh::kRows / 2 : Sh::kRows);   // first unit or row
+    const int u0 = ubase + blockIdx.x * (kPaired ? Sh::kRows / 2 : Sh::kRows);   // first unit or row
     const int t0 = blockIdx.y * Sh::kCols;                               // first row (token)
     const int last_tile = (n - 1) >> 4;                                   // last 16-row column tile
 
@@ -182,20 +217,13 @@ void gemm_kernel(GemvArgs g, int units, int n, float* part) {
         const uint32_t sb = (kb % kBufs) * Sh::kBufBytes;
         u32x4_t a[TI], bv[TJ];
         if constexpr (TI == 4) {
-            lds_read8<0, F, (2 + kSecond) * F, (3 + kSecond) * F, 0, F, 2 * F, 3 * F>(
-                a_off + sb, b_off + sb, a, bv);
+            lds_issue8<0, F, (2 + kSecond) * F, (3 + kSecond) * F>(a_off + sb, b_off + sb, a, bv);
         } else {
-            lds_read8<0, F, 2 * F, 3 * F, 0, F, 2 * F, 3 * F>(a_off + sb, b_off + sb, a, bv);
-            lds_read4<(4 + kSecond) * F, (5 + kSecond) * F, (6 + kSecond) * F, (7 + kSecond) * F>(
+            lds_issue8<0, F, 2 * F, 3 * F>(a_off + sb, b_off + sb, a, bv);
+            lds_issue4<(4 + kSecond) * F, (5 + kSecond) * F, (6 + kSecond) * F, (7 + kSecond) * F>(
                 a_off + sb, a + 4);
         }
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-#pragma unroll
-            for (int j = 0; j < TJ; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(bf16x8_t, a[i]), __builtin_bit_cast(bf16x8_t, bv[j]),
-                    acc[i][j], 0, 0, 0);
+        mfma_rows<0>(acc, a, bv);
     }
     __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));   // the reloads past the end
 
@@ -338,21 +366,49 @@ static hipError_t launch_prep_tiles(int pro, const GemvArgs& g, hipStream_t s) {
     return hipGetLastError();
 }
 
+constexpr int kCUs = 256;   // compute units of the MI355X: one round of 256 x 256 tiles
+
+// units (weight rows, or row pairs for the two-row kinds) per row tile
 template <int EPI, int WM, int WN, int TI, int TJ>
-static dim3 gemm_grid(int units, int n) {
-    using Sh = GemmShape<WM, WN, TI, TJ>;
-    constexpr bool kPaired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
-    const int per = kPaired ? Sh::kRows / 2 : Sh::kRows;
-    return dim3((units + per - 1) / per, (n + Sh::kCols - 1) / Sh::kCols);
+constexpr int tile_units() {
+    return EPI == EPI_SWIGLU || EPI == EPI_QKV ? GemmShape<WM, WN, TI, TJ>::kRows / 2
+                                               : GemmShape<WM, WN, TI, TJ>::kRows;
 }
 
 template <int EPI, int WM, int WN, int TI, int TJ>
+static dim3 gemm_grid(int units, int n) {
+    constexpr int per = tile_units<EPI, WM, WN, TI, TJ>();
+    return dim3((units + per - 1) / per, (n + GemmShape<WM, WN, TI, TJ>::kCols - 1) /
+                                             GemmShape<WM, WN, TI, TJ>::kCols);
+}
+
+// Units [ubase, uend) of the projection (uend = -1: to the last one).
+template <int EPI, int WM, int WN, int TI, int TJ>
 static void gemm_launch(const GemvArgs& g, int units, int n, hipStream_t s, float* part = nullptr,
-                        int splits = 1) {
-    dim3 grid = gemm_grid<EPI, WM, WN, TI, TJ>(units, n);
+                        int splits = 1, int ubase = 0, int uend = -1) {
+    dim3 grid = gemm_grid<EPI, WM, WN, TI, TJ>((uend < 0 ? units : uend) - ubase, n);
     grid.z = splits;
     launch_main(gemm_kernel<EPI, WM, WN, TI, TJ>, grid, dim3(GemmShape<WM, WN, TI, TJ>::kThreads),
-                0, s, g, units, n, part);
+                0, s, g, units, n, part, ubase);
+}
+
+// The last round of a 256 x 256 grid that does not fill the CUs: the units
+// of the row tiles that fill whole rounds stay on 256 x 256 tiles, and the
+// rest go to a second launch of 128 x 128 tiles when those take one round
+// of two workgroups per CU (half the flops of a large round, at about 0.8
+// of the large tile's rate per flop measured on the MI355X: some 0.6 of its
+// time) instead of a partly idle round of the large one.  Returns the
+// first unit of the 128 x 128 launch, or units for none.  The outputs are
+// the same bit for bit: every output sums its K steps in the same order in
+// either tile.
+template <int EPI>
+static int gemm_tail_units(int units, int n) {
+    const dim3 big = gemm_grid<EPI, 2, 4, 8, 4>(units, n);
+    const int tiles = big.x * big.y, whole = tiles / kCUs * kCUs;
+    if (whole == tiles || whole == 0) return units;
+    const int ubig = whole / big.y * tile_units<EPI, 2, 4, 8, 4>();
+    const dim3 small = gemm_grid<EPI, 2, 2, 4, 4>(units - ubig, n);
+    return small.x * small.y <= 2 * kCUs ? ubig : units;
 }
 
 // Residual add of the split-K partial sums: Y[row] += part[0] + part[1]
@@ -385,8 +441,8 @@ static hipError_t launch_gemm_epi(const GemvArgs& g, int units, int tile, float*
     // leave CUs idle but fills them when doubled (O and down at prefill sizes)
     const bool split_ok = EPI == EPI_ADD && part && (g.K / kTileK) % 2 == 0 && units % 4 == 0;
     const bool split = split_ok && (tile == BUDDY_GEMM_TILE_256_SPLIT ||
-                                    (tile == BUDDY_GEMM_TILE_AUTO && big.x * big.y < 512 &&
-                                     2 * big.x * big.y >= 256));
+                                    (tile == BUDDY_GEMM_TILE_AUTO && big.x * big.y < 2 * kCUs &&
+                                     2 * big.x * big.y >= kCUs));
     if (split) {
         gemm_launch<EPI, 2, 4, 8, 4>(g, units, n, s, part, 2);
         hipError_t e = hipGetLastError();
@@ -394,9 +450,12 @@ static hipError_t launch_gemm_epi(const GemvArgs& g, int units, int tile, float*
         const size_t work = (size_t)n * (units / 4);
         const int grid = (int)((work + 255) / 256 < 4096 ? (work + 255) / 256 : 4096);
         splitk_add_kernel<<<grid, 256, 0, s>>>(g, units, n, part);
-    } else if (tile == BUDDY_GEMM_TILE_256 || tile == BUDDY_GEMM_TILE_256_SPLIT ||
-               (tile == BUDDY_GEMM_TILE_AUTO && big.x * big.y >= 512)) {
+    } else if (tile == BUDDY_GEMM_TILE_256 || tile == BUDDY_GEMM_TILE_256_SPLIT) {
         gemm_launch<EPI, 2, 4, 8, 4>(g, units, n, s);
+    } else if (tile == BUDDY_GEMM_TILE_AUTO && big.x * big.y >= 2 * kCUs) {
+        const int ubig = gemm_tail_units<EPI>(units, n);
+        gemm_launch<EPI, 2, 4, 8, 4>(g, units, n, s, nullptr, 1, 0, ubig);
+        if (ubig < units) gemm_launch<EPI, 2, 2, 4, 4>(g, units, n, s, nullptr, 1, ubig);
     } else {
         gemm_launch<EPI, 2, 2, 4, 4>(g, units, n, s);
     }

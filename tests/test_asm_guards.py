@@ -28,7 +28,8 @@ import pytest
 
 from paper_2606_09514_amd import build as hip_build
 
-SOURCES = {"k_attn.hip": "_ZN5buddy16attn_mfma_kernel", "k_mfma.hip": "_ZN5buddy11mfma_kernel"}
+SOURCES = {"k_attn.hip": "_ZN5buddy16attn_mfma_kernel", "k_mfma.hip": "_ZN5buddy11mfma_kernel",
+           "k_gemm.hip": "_ZN5buddy11gemm_kernel"}
 REG = re.compile(r"\bv(\d+)\b|\bv\[(\d+):(\d+)\]")
 
 
@@ -71,10 +72,16 @@ def operands(text: str):
     return parts[0], ops
 
 
+LGKM = re.compile(r"lgkmcnt\((\d+)\)")
+
+
 def hazards(lines) -> list:
     """Instructions that read or write an asm load's registers before the
-    next vmcnt wait."""
+    wait that covers it: the next vmcnt wait for a global load; for an LDS
+    read, the first lgkmcnt(n) wait with at most n asm LDS reads issued after
+    it (LDS reads return in issue order)."""
     in_asm, pending, bad = False, set(), []
+    lds = []   # destination register sets of asm LDS reads, in issue order
     for ln in lines:
         raw = ln.strip()
         if raw.startswith(";;#ASMSTART"):
@@ -87,8 +94,13 @@ def hazards(lines) -> list:
         if not text or text.endswith(":") or text.startswith("."):
             continue
         op, ops = operands(text)
-        if op == "s_waitcnt" and "vmcnt" in text:
-            pending.clear()
+        if op == "s_waitcnt":
+            if "vmcnt" in text:
+                pending.clear()
+            m = LGKM.search(text)
+            if m:
+                n = int(m.group(1))
+                lds = lds[len(lds) - n:] if n < len(lds) else lds
             continue
         if in_asm and op == "global_load_dwordx4":
             pending |= vregs(ops[0])
@@ -99,8 +111,10 @@ def hazards(lines) -> list:
         touched = set().union(*[vregs(o) for o in ops])
         if not store:
             touched |= vregs(ops[0])
-        if touched & pending:
+        if touched & (pending.union(*lds) if lds else pending):
             bad.append(text)
+        if in_asm and op == "ds_read_b128":
+            lds.append(vregs(ops[0]))
     return bad
 
 

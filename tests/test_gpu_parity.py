@@ -657,6 +657,27 @@ def test_prefill_gemm_tiles(G):
             assert np.array_equal(a, b)
 
 
+def test_prefill_gemm_tail_round():
+    """A gate/up grid two rounds and a bit of 256 x 256 tiles on 256 CUs
+    (8704 units x 2000 prompt rows: 68 x 8 = 544 tiles): the automatic
+    choice keeps 512 of them on 256 x 256 tiles and sends the last 512 units
+    to a 128 x 128 launch.  Every output accumulates over K in the same order
+    in both tiles, so the prefill equals the all-128 x 128 and all-256 x 256
+    runs bit for bit (outputs, routes and caches); both of those are held to
+    the oracle by the tests above."""
+    shape = dict(n_layers=4, d_model=256, n_heads=4, n_kv_heads=1, head_dim=128, d_ffn=8704,
+                 dm_hidden=64, dm_act="silu", rope_theta=1e4, rms_eps=1e-5)
+    P = Pair(shape, "bf16", 2048, 1, seed=131, omega=0.1, device_gen=True)
+    outs = []
+    for tile in (blib.GEMM_TILE_AUTO, blib.GEMM_TILE_128, blib.GEMM_TILE_256):
+        P.gpu.set_gemm_tile(tile)
+        outs.append(gpu_prefill(P, [2000], [1], 2000, seed=132))
+    assert np.all(np.isfinite(outs[0][0])) and np.any(outs[0][0] != 0)
+    for other in outs[1:]:
+        for a, b in zip(outs[0], other):
+            assert np.array_equal(a, b)
+
+
 def test_prefill_route_override():
     P = Pair("tiny", "bf16", 32, 2, seed=115, omega=0.1)
     route = np.array([[1, 0, 0, 1, 1, 0], [0, 0, 0, 0, 0, 0]], np.uint8)
