@@ -60,12 +60,15 @@ def log(*a):
 
 
 def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, exec_map=None,
-               running_pool=False, kernel=None):
+               running_pool=False, kernel=None, repeats=1):
     """ks: budgets per sequence, or None for budget-free steps (the attached
     Budget Predictor picks them); exec_map: execution map for skipped-KV
     masking, or None for zero-filled skipped KV; running_pool: the planner
     keeps running sums of the first block's rows (fresh state per budget,
-    so the first warm-up step sums the whole cache)."""
+    so the first warm-up step sums the whole cache).  The first timed run of
+    `steps` steps gives every figure; repeats - 1 further runs over the same
+    positions, after it, give only their tokens/s (run_tokens_per_s, and the
+    median over all runs)."""
     import numpy as np
     import torch
     from paper_2606_09514_amd import costmodel
@@ -92,6 +95,7 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
     for _ in range(warmup):
         step(pos)
         pos += 1
+    pos0 = pos
     kernel = blib.KERNEL_GATE_UP if kernel is None else kernel
     starts, stops = hip.create(steps), hip.create(steps)
     model.set_timing_events(kernel, kernel_layer, starts, stops)
@@ -142,7 +146,19 @@ def run_budget(model, cfg, w, dk, dv, x0, ks, steps, warmup, hip, kernel_layer, 
             first = perm.cpu().numpy()[st[:-1]]
             groups.append(g)
             per_path.append(int(sum(int(m[t, b].sum()) + 2 for b in first)))
+    # further timed runs over the same positions: tokens/s only
+    runs = [B * steps / (total_ms / 1e3)]
+    for _ in range(repeats - 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for t in range(steps):
+            step(pos0 + t, t)
+        e1.record()
+        torch.cuda.synchronize()
+        runs.append(B * steps / (e0.elapsed_time(e1) / 1e3))
     return dict(ks=ks, total_ms=total_ms, ms_per_step=total_ms / steps,
+                run_tokens_per_s=runs, median_tokens_per_s=float(np.median(runs)),
                 step_ms_p50=float(np.percentile(step_ms, 50)),
                 step_ms_p90=float(np.percentile(step_ms, 90)),
                 tokens_per_s=B * steps / (total_ms / 1e3),
@@ -217,7 +233,7 @@ def per_kernel(model, cfg, w, dk, dv, x0, ks, hip, steps=24, warmup=2):
     return out
 
 
-def batched_workload(name, warmup, policy):
+def batched_workload(name, warmup, policy, repeats=1):
     """One batched workload (rerouted every step): its own synthetic model,
     cache and budgets; tokens/s and the step's HBM fraction."""
     import torch
@@ -234,10 +250,11 @@ def batched_workload(name, warmup, policy):
     model.set_launch_policy(policy)
     hip = blib.HipEvents()
     ks = synth.budgets(w, seed=1) if w.mixed else [w.budgets[0]] * w.batch
-    r = run_budget(model, cfg, w, dk, dv, x0, ks, w.steps, warmup, hip, 0)
+    r = run_budget(model, cfg, w, dk, dv, x0, ks, w.steps, warmup, hip, 0, repeats=repeats)
     log(f"{w.name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step "
         f"(p50 {r['step_ms_p50']:.3f}, p90 {r['step_ms_p90']:.3f}), "
-        f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline")
+        f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline; runs "
+        + ", ".join(f"{v:.1f}" for v in r["run_tokens_per_s"]) + " tokens/s")
     model.close()
     del model, W, dk, dv, x0
     torch.cuda.synchronize()
@@ -249,6 +266,8 @@ def batched_workload(name, warmup, policy):
             "step_ms_p90": round(r["step_ms_p90"], 4), "bytes_per_step": int(r["bytes_per_step"]),
             "step_hbm_frac": round(r["step_hbm_frac"], 4), "layers_used": r["layers_used"],
             "distinct_routes": r["distinct_routes"],
+            "run_tokens_per_s": [round(v, 2) for v in r["run_tokens_per_s"]],
+            "median_tokens_per_s": round(r["median_tokens_per_s"], 2),
             "path_grouping": {"route_groups_per_step": r["route_groups"],
                               "block_runs_per_path_sub_batches": r["per_path_blocks"],
                               "block_runs_per_block_compaction": r["layers_used"]}}
@@ -307,6 +326,9 @@ def main():
                     help="time the routed prefill of a prompt of the workload's context length "
                          "at each budget and the dense one, instead of decode steps")
     ap.add_argument("--steps", type=int, default=128)
+    ap.add_argument("--repeats", type=int, default=3,
+                    help="timed runs per budget: the first gives every figure, all of them the "
+                         "median tokens/s (median_tokens_per_s)")
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="llama3_8b_b1_ctx2048")
     ap.add_argument("--budgets", default=None, help="comma list of k (default: the workload's)")
@@ -391,14 +413,17 @@ def main():
         ks = synth.budgets(w, seed=1) if w.mixed else [k] * w.batch
         if args.auto_budget:
             ks = None
+        # the running pool's sums follow the positions forward: one run
         r = run_budget(model, cfg, w, dk, dv, x0, ks, args.steps, args.warmup, hip, 0, exec_map,
-                       running_pool=args.pool == "running")
+                       running_pool=args.pool == "running",
+                       repeats=1 if args.pool == "running" else args.repeats)
         name = "auto" if args.auto_budget else "mixed" if w.mixed else str(k)
         runs[name] = r
         log(f"k={name}: {r['tokens_per_s']:.1f} tokens/s, {r['ms_per_step']:.3f} ms/step "
             f"(p50 {r['step_ms_p50']:.3f}, p90 {r['step_ms_p90']:.3f}), "
             f"{r['step_hbm_frac'] * 100:.1f}% of HBM roofline, gate_up {r['kernel_ms'] * 1e3:.1f} us, "
-            f"host CPU {r['host_cpu_ms_per_step']:.3f} ms/step")
+            f"host CPU {r['host_cpu_ms_per_step']:.3f} ms/step; runs "
+            + ", ".join(f"{v:.1f}" for v in r["run_tokens_per_s"]) + " tokens/s")
 
     head = runs[next(iter(runs))]
     head_k = budgets[0] if not (w.mixed or args.auto_budget) else None
@@ -434,7 +459,7 @@ def main():
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
         for name in batched:
-            per_workload[name] = batched_workload(name, 4, policy)
+            per_workload[name] = batched_workload(name, 4, policy, args.repeats)
 
     out = {
         "metric": "routed-decode tokens/s at budget k (1 GPU); % of HBM roofline",
@@ -467,6 +492,8 @@ def main():
                            "distinct_routes": r["distinct_routes"],
                            "mean_k": round(r["mean_k"], 2),
                            "gate_up_us": round(r["kernel_ms"] * 1e3, 2),
+                           "run_tokens_per_s": [round(v, 2) for v in r["run_tokens_per_s"]],
+                           "median_tokens_per_s": round(r["median_tokens_per_s"], 2),
                            "host_cpu_ms_per_step": round(r["host_cpu_ms_per_step"], 3)}
                        for n, r in runs.items()},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
