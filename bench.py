@@ -459,7 +459,7 @@ def main():
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
         for name in batched:
-            per_workload[name] = batched_workload(name, 4, policy, args.repeats)
+            per_workload[name] = batched_workload(name, args.warmup, policy, args.repeats)
 
     out = {
         "metric": "routed-decode tokens/s at budget k (1 GPU); % of HBM roofline",
