@@ -4,7 +4,8 @@ through inline asm (no GPU needed).
 The decode attention's MFMA score kernel (K fragments) and the MFMA
 projection kernel (activation fragments) issue some vector-memory loads as
 inline asm, outside the compiler's load tracking, and wait for them with
-their own s_waitcnt.  That is sound only while the compiler leaves the
+their own s_waitcnt; the prefill GEMM does the same with its fragment reads
+from LDS, waiting for each row tile's read with a partial lgkmcnt.  That is sound only while the compiler leaves the
 loaded registers alone until the wait: an instruction that reads such a
 register earlier -- a copy at a loop's back edge, a spill into an
 accumulation register -- takes data that has not arrived, and one that
@@ -136,6 +137,11 @@ def test_every_asm_load_instantiation_is_checked(kernels):
     # pooling) and every MFMA projection tiling
     assert sum(k.startswith(SOURCES["k_attn.hip"]) for k in kernels) >= 4
     assert sum(k.startswith(SOURCES["k_mfma.hip"]) for k in kernels) >= 60
+    # the prefill GEMM's eight (epilogue x tile) instantiations, each with
+    # its fragment reads from LDS as asm
+    gemm = [b for k, b in kernels.items() if k.startswith(SOURCES["k_gemm.hip"])]
+    assert len(gemm) >= 8
+    assert all(sum(ln.strip().startswith("ds_read_b128") for ln in b) >= 8 for b in gemm)
     asm_loads = sum(1 for body in kernels.values() for ln in body
                     if ln.strip().startswith("global_load_dwordx4") and "off" in ln)
     assert asm_loads > 0
@@ -168,3 +174,31 @@ def test_attention_k_loads_feed_the_score_mfma_directly(kernels):
                     a_ops.add(m.group(1))
         assert len(k_dst) >= 8 and len(a_ops) == 4, (k_dst, a_ops)
         assert set(k_dst) <= a_ops, (k_dst, sorted(a_ops))
+
+
+def test_the_walk_flags_what_it_should():
+    """The checker itself, on hand-written instruction streams: registers of
+    an asm load read or overwritten before the wait that covers it are
+    flagged; after that wait they are free.  For LDS reads, lgkmcnt(n)
+    covers all but the last n asm reads issued."""
+    A, E = ";;#ASMSTART", ";;#ASMEND"
+    glob = [A, "global_load_dwordx4 v[4:7], v2, off", E]
+    assert hazards(glob + ["v_mov_b32_e32 v9, v5"]) == ["v_mov_b32_e32 v9, v5"]
+    assert hazards(glob + ["v_mov_b32_e32 v6, v9"]) == ["v_mov_b32_e32 v6, v9"]
+    assert hazards(glob + ["s_waitcnt vmcnt(0)", "v_mov_b32_e32 v9, v5"]) == []
+    assert hazards(glob + ["v_mov_b32_e32 v9, v8"]) == []
+    lds = [A, "ds_read_b128 v[10:13], v1 offset:0", "ds_read_b128 v[14:17], v1 offset:1024",
+           "ds_read_b128 v[18:21], v1 offset:2048", E]
+    mfma = "v_mfma_f32_16x16x32_bf16 v[30:33], v[{}], v[40:43], v[30:33]"
+    # after lgkmcnt(2) only the first read has landed
+    assert hazards(lds + ["s_waitcnt lgkmcnt(2)", mfma.format("10:13")]) == []
+    assert hazards(lds + ["s_waitcnt lgkmcnt(2)", mfma.format("14:17")]) == [mfma.format("14:17")]
+    assert hazards(lds + ["s_waitcnt lgkmcnt(1)", mfma.format("14:17")]) == []
+    assert hazards(lds + ["s_waitcnt lgkmcnt(1)", mfma.format("18:21")]) == [mfma.format("18:21")]
+    assert hazards(lds + ["s_waitcnt lgkmcnt(0)", mfma.format("18:21")]) == []
+    # a copy of a pending register, and a second read into it, are flagged
+    assert hazards(lds + ["v_mov_b32_e32 v50, v19"]) == ["v_mov_b32_e32 v50, v19"]
+    again = "ds_read_b128 v[18:21], v1 offset:4096"
+    assert hazards(lds + [A, again, E]) == [again]
+    # compiler-issued LDS reads (outside asm) are the compiler's to track
+    assert hazards(["ds_read_b128 v[10:13], v1", mfma.format("10:13")]) == []
