@@ -507,7 +507,7 @@ struct AttnArgs {
     // o (decode rows: split high / low, xbs_index; prompt tokens of the
     // prefill attention kernel: bf16, xb_index, with K = nq hd); or null
     bf16_t* xb_out;
-    // prompt tokens on the prefill attention kernel: groups of up to 64 / G
+    // prompt tokens on the prefill attention kernel: groups of up to 128 / G
     // consecutive tokens of one prompt, (first row index, count) pairs; one
     // workgroup per (KV head, group) (null: one per row)
     const int32_t* groups; int n_groups;

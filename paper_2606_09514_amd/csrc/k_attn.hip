@@ -630,10 +630,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(POOL ? 2 : 
 // ------------------------------------------------------ prefill attention
 
 // Causal attention of the prompt tokens of a prefill (bf16 cache, head_dim
-// 128): one workgroup per (KV head, group of up to 64 / G consecutive tokens
-// of one prompt); its 64 query rows are (token, head) pairs, 16 per
-// wavefront.  K and V tiles of 64 rows pass through LDS (two buffers, the
-// next tile's direct-to-LDS loads in flight while the current one is used),
+// 128): one workgroup per (KV head, group of up to 128 / G consecutive
+// tokens of one prompt); its 128 query rows are (token, head) pairs, 16 per
+// wavefront, eight wavefronts sharing every K/V tile.  K and V tiles of 64
+// rows pass through LDS (four buffers, the next three tiles' direct-to-LDS
+// loads in flight while the current one is used; one workgroup per CU),
 // each row's 16-byte chunks stored at chunk ^ (row % 16) so that both reads
 // below are free of bank conflicts.  Per tile and wavefront:
 //   S^T = K Q^T   v_mfma_f32_16x16x32_bf16, A = K rows from LDS, B = the
@@ -649,6 +650,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(POOL ? 2 : 
 
 constexpr int kPfRows = 64;                      // K/V rows per tile
 constexpr int kPfTile = kPfRows * 128 * 2;       // bytes of a K or V tile
+constexpr int kPfWaves = 8;                      // wavefronts (16 query rows each)
+constexpr int kPfBufs = 4;                       // tiles in LDS: three loading ahead
 
 // Four 16-byte LDS reads at per-lane addresses plus one immediate, then a
 // wait; asm so that the compiler does not wait for the direct-to-LDS loads
@@ -671,10 +674,10 @@ __device__ __forceinline__ void pf_read_k(const uint32_t* ad, uint32_t base, bf1
     x[2] = __builtin_bit_cast(bf16x8_t, r2);
     x[3] = __builtin_bit_cast(bf16x8_t, r3);
 }
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_prefill_kernel(AttnArgs a) {
     constexpr int HD = 128;
-    __shared__ __attribute__((aligned(16))) char s_kv[2][2][kPfTile];   // [buffer][K | V]
+    __shared__ __attribute__((aligned(16))) char s_kv[kPfBufs][2][kPfTile];   // [buffer][K | V]
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = blockIdx.y;
@@ -715,20 +718,21 @@ void attn_prefill_kernel(AttnArgs a) {
         }
     }
 
-    // Tile loads: wavefront w moves rows 16 w .. 16 w + 15 of K and of V, four
+    // Tile loads: wavefront w moves rows 8 w .. 8 w + 7 of K and of V, four
     // rows (1 KB) per load; lane L lands at 16 L of the load's block, i.e. row
     // L / 16 of it and stored chunk L % 16, which holds source chunk
     // (L % 16) ^ (row % 16).  Rows past the last position repeat it (masked).
     const size_t cbase = ((size_t)slot * a.nkv + g) * a.T * HD;
     const bf16_t* Kg = (const bf16_t*)a.kc + cbase;
     const bf16_t* Vg = (const bf16_t*)a.vc + cbase;
+    constexpr int kWaveRows = kPfRows / kPfWaves;                   // 8 rows of each
     auto issue = [&](int kt, int buf) {
 #pragma unroll
-        for (int ld = 0; ld < 4; ++ld) {
-            const int rl = 16 * wave + 4 * ld + (lane >> 4);          // row within the tile
+        for (int ld = 0; ld < kWaveRows / 4; ++ld) {
+            const int rl = kWaveRows * wave + 4 * ld + (lane >> 4);   // row within the tile
             const int row = min(kt * kPfRows + rl, pos_last);
             const size_t src = (size_t)row * HD + (((lane & 15) ^ (rl & 15)) * 8);
-            const int dst = (16 * wave + 4 * ld) * 256;
+            const int dst = (kWaveRows * wave + 4 * ld) * 256;
             __builtin_amdgcn_global_load_lds((attn_gptr_t)(Kg + src), (attn_lptr_t)(s_kv[buf][0] + dst),
                                              16, 0, 0);
             __builtin_amdgcn_global_load_lds((attn_gptr_t)(Vg + src), (attn_lptr_t)(s_kv[buf][1] + dst),
@@ -763,12 +767,22 @@ void attn_prefill_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) o[dt] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 
-    issue(0, 0);
+    // Tile kt sits in buffer kt % 4, its loads issued three tiles ahead: at
+    // tile kt, wait until only the loads of the tiles after it that have been
+    // issued (kt + 1 and kt + 2, those that exist; kWaveRows / 2 loads each)
+    // are in flight, barrier (everyone's loads of tile kt have landed, and
+    // everyone has read tile kt - 1's buffer), refill that buffer with tile
+    // kt + 3.
+    constexpr int kTileLoads = kWaveRows / 2;                      // K and V loads per wavefront
+    for (int j = 0; j < kPfBufs - 1 && j < ntiles; ++j) issue(j, j);
     for (int kt = 0; kt < ntiles; ++kt) {
-        const int buf = kt & 1;
-        __builtin_amdgcn_s_waitcnt(0);                                 // this tile's loads
-        asm volatile("s_barrier" ::: "memory");                        // everyone's, and buffer buf ^ 1 is free
-        if (kt + 1 < ntiles) issue(kt + 1, buf ^ 1);
+        const int buf = kt % kPfBufs;
+        const int later = min(ntiles - 1, kt + kPfBufs - 2) - kt;      // tiles issued after kt
+        if (later >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_at_most(2 * kTileLoads));
+        else if (later == 1) __builtin_amdgcn_s_waitcnt(vmcnt_at_most(kTileLoads));
+        else __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));
+        asm volatile("s_barrier" ::: "memory");
+        if (kt + kPfBufs - 1 < ntiles) issue(kt + kPfBufs - 1, (kt + kPfBufs - 1) % kPfBufs);
         const uint32_t bb = buf * 2 * kPfTile;
 
         // S^T for the 4 row tiles of the K tile
@@ -908,7 +922,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 static bool attn_uses_mfma(int dtype, int hd, int G) { return dtype == BUDDY_BF16 && hd == 128 && G >= 3 && G <= kMaxGroup; }
 
 int attention_prefill_group(int dtype, int hd, int G) {
-    return dtype == BUDDY_BF16 && hd == 128 && G <= kMaxGroup ? 64 / G : 1;
+    return dtype == BUDDY_BF16 && hd == 128 && G <= kMaxGroup ? 16 * kPfWaves / G : 1;
 }
 
 int attention_rows_per_wg(int dtype, int hd, int G) {
@@ -946,7 +960,7 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
     // lanes per cache row: hd / 8 (bf16) or hd / 4 (fp32); head_dim is 64 or 128
     if (a.groups) {               // prompt-token groups (one chunk)
         if (attention_prefill_group(dtype, a.hd, G) < 2 || a.chunks != 1) return hipErrorInvalidValue;
-        launch_main(attn_prefill_kernel, dim3(1, a.nkv, a.n_groups), dim3(256), 0, s, a);
+        launch_main(attn_prefill_kernel, dim3(1, a.nkv, a.n_groups), dim3(64 * kPfWaves), 0, s, a);
         return hipGetLastError();
     }
     if (a.pool_part && (a.exec || a.tok_T > 0)) return hipErrorInvalidValue;
