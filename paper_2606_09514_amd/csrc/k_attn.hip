@@ -331,6 +331,29 @@ __device__ __forceinline__ void read_v_tr(const uint32_t* ad, uint32_t base, s16
     for (int i = 0; i < 8; ++i) x[i] = __builtin_bit_cast(s16x4_t, r[i]);
 }
 
+// Max and sum of a value and its copy 16 (or 32) lanes away, by the gfx950
+// lane swaps: with both operands the same register, v_permlane16_swap
+// (v_permlane32_swap) leaves each lane's own value in one result and its
+// partner's in the other, so their max or sum is the pair's -- the same
+// operands as a cross-lane shuffle (so the same result bit for bit), without
+// its round trip through the LDS unit.
+__device__ __forceinline__ float max_xor16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // s_waitcnt with at most n vector-memory operations outstanding (the other
 // counters left at their maxima).
 __device__ __forceinline__ constexpr int vmcnt_at_most(int n) {
@@ -516,8 +539,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(POOL ? 2 : 
             sc[v] = jrow < j1 && (ex[v] != 0 || jrow == pos) ? d[v] : -INFINITY;
         }
         float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        mx = max_xor32(max_xor16(mx));
         const float mn = fmaxf(mrun, mx);
         const float al = scale_of(mrun, mn);
         float p[4];
@@ -558,8 +580,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(POOL ? 2 : 
     }
 
     // per wave: total of each head's running sum over its four lanes
-    lrun += __shfl_xor(lrun, 16, kWave);
-    lrun += __shfl_xor(lrun, 32, kWave);
+    lrun = sum_xor32(sum_xor16(lrun));
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         const int hh = 4 * lg + e;
@@ -815,8 +836,7 @@ void attn_prefill_kernel(AttnArgs a) {
                 st[t][e] = q_ok && row <= q_pos ? st[t][e] : -INFINITY;
                 mx = fmaxf(mx, st[t][e]);
             }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+        mx = max_xor32(max_xor16(mx));
         const float mn = fmaxf(m_run, mx);
         const float al = scale_of(m_run, mn);
         float ls = 0.f;
@@ -831,8 +851,7 @@ void attn_prefill_kernel(AttnArgs a) {
             }
             pa[t] = __builtin_bit_cast(s16x4_t, make_uint2(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])));
         }
-        ls += __shfl_xor(ls, 16, kWave);
-        ls += __shfl_xor(ls, 32, kWave);
+        ls = sum_xor32(sum_xor16(ls));
         l_run = l_run * al + ls;
         m_run = mn;
         // rescale O: lane d + 16 r holds query rows 4 r .. 4 r + 3
