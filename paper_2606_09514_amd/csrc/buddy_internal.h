@@ -90,9 +90,24 @@ __device__ __forceinline__ void unpack<float>(const uint4& w, float* out) {
 
 // ------------------------------------------------------------- reductions
 
+// Sum over the wavefront, every lane receiving it: the butterfly of lane
+// pairs 32, 16, 8, 4, 2 and 1 apart.  The first two steps take the partner
+// from the gfx950 lane swaps (v_permlane32_swap / v_permlane16_swap: a lane's
+// own value and its partner's in the two results), the last four from DPP
+// rotations within 16-lane rows (by 8, 4, 2, 1): after the wider steps the
+// lane a rotation reaches holds the same value as the partner, so every sum
+// has the operands of the shuffle butterfly (bit-identical results) without
+// a round trip through the LDS unit per step.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    constexpr int kRowRor = 0x120;   // DPP control: rotate right within each row
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kRowRor + 8, 0xf, 0xf, true));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kRowRor + 4, 0xf, 0xf, true));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kRowRor + 2, 0xf, 0xf, true));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kRowRor + 1, 0xf, 0xf, true));
     return v;
 }
 
