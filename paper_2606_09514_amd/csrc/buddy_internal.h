@@ -111,6 +111,20 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// Maximum over the wavefront, every lane receiving it, by the same steps.
+__device__ __forceinline__ float wave_max(float v) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    constexpr int kRowRor = 0x120;
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kRowRor + 8, 0xf, 0xf, true)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kRowRor + 4, 0xf, 0xf, true)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kRowRor + 2, 0xf, 0xf, true)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kRowRor + 1, 0xf, 0xf, true)));
+    return v;
+}
+
 // --------------------------------------------------------------- workspace
 
 struct Workspace {

@@ -914,9 +914,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
     const size_t pstride = (size_t)a.hd + 2;
     const float* pp = a.part + ((size_t)b * a.nq + head) * a.max_chunks * pstride;
     const float mc = tid < a.chunks ? pp[tid * pstride + a.hd] : -INFINITY;
-    float M = mc;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, kWave));
+    float M = wave_max(mc);
     if (lane == 0) s_red[wave] = M;
     __syncthreads();
     M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
