@@ -97,9 +97,11 @@ const char* layer_base(const Model& M, const void* kv, int l) {
 }
 
 // Position chunks per (sequence, KV head): enough workgroups to cover the
-// chip (about 2048 over the launch), chunk lengths a multiple of the rows one
-// workgroup block reads, at most kAttnMaxChunks chunks, or `cap` (at least
-// 1) when that is smaller.
+// chip (about 2048 over the launch), chunk lengths a multiple (at least two)
+// of the rows one workgroup block reads, at most kAttnMaxChunks chunks, or
+// `cap` (at least 1) when that is smaller.
+constexpr int kAttnMinBlocks = 2;   // workgroup blocks per chunk, at least
+
 void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chunk_len,
                  int cap = kAttnMaxChunks) {
     const buddy_config& c = M.cfg;
@@ -122,8 +124,12 @@ void attn_chunks(const Model& M, int n_rows, int max_pos, int* chunks, int* chun
     // at most kAttnMaxChunks chunks (max_ctx is bounded at create so that
     // min_chunks itself stays within it)
     const int min_chunks = (blocks + kAttnMaxChunks - 1) / kAttnMaxChunks;
-    const int per = (blocks + (want > min_chunks ? want : min_chunks) - 1) /
-                    (want > min_chunks ? want : min_chunks);
+    int per = (blocks + (want > min_chunks ? want : min_chunks) - 1) /
+              (want > min_chunks ? want : min_chunks);
+    // at least two blocks per chunk: at B = 1 (2049 rows, Llama-8B shape) 17
+    // chunks instead of 33 keep the score kernel at its time (a launch of 136
+    // workgroups is no slower than one of 264) and halve the merge's partials
+    if (per < kAttnMinBlocks) per = kAttnMinBlocks;
     *chunk_len = per * rows;
     *chunks = (max_pos + 1 + *chunk_len - 1) / *chunk_len;
 }
