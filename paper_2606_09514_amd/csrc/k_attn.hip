@@ -913,14 +913,16 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const size_t pstride = (size_t)a.hd + 2;
     const float* pp = a.part + ((size_t)b * a.nq + head) * a.max_chunks * pstride;
+    // each chunk's max and sum, both loaded before the first reduction
     const float mc = tid < a.chunks ? pp[tid * pstride + a.hd] : -INFINITY;
+    const float lc = tid < a.chunks ? pp[tid * pstride + a.hd + 1] : 0.f;
     float M = wave_max(mc);
     if (lane == 0) s_red[wave] = M;
     __syncthreads();
     M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
     const float wc = scale_of(mc, M);
     if (tid < a.chunks) s_w[tid] = wc;
-    float L = tid < a.chunks ? pp[tid * pstride + a.hd + 1] * wc : 0.f;
+    float L = tid < a.chunks ? lc * wc : 0.f;
     L = wave_sum(L);
     __syncthreads();                      // s_red reads above are done
     if (lane == 0) s_red[wave] = L;
