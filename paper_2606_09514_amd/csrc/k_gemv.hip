@@ -321,20 +321,25 @@ static hipError_t launch_one(const GemvArgs& g, int units, int n_host, hipStream
 // the activations.
 // Shape classes (k-steps of 64 lanes x 16 bytes per weight row):
 //   <= 8 steps: one wavefront per row, 8 loads per lane, 8 wavefronts per
-//   workgroup (16 for plain rows without a prologue); two-row units with
-//   <= 16 steps: 16 loads per lane; single rows
-//   with <= 32 (<= 64) steps: quarter rows of <= 8 (16) loads per lane, 16
+//   workgroup (16 for plain rows without a prologue, 12 for QKV units);
+//   two-row units with <= 16 steps: 16 loads per lane; single rows with
+//   <= 32 (<= 64) steps: quarter rows of <= 8 (16) loads per lane, 16
 //   wavefronts per workgroup so four rows share one activation staging.
 template <typename TW, int NR, int PRO, int EPI, bool TAIL, bool MULTI>
 static hipError_t dispatch_s(const GemvArgs& g, int units, int n_host, hipStream_t s) {
     constexpr int KS = kWave * St<TW>::V;
     const int nsteps = (g.K + KS - 1) / KS;
     if (nsteps <= 8) {
-        // plain rows (the attention output projection): 16 rows share one
-        // staging (Llama-8B O at B = 1: 9.5 -> 8.9 us); the two-row units
-        // and RMSNorm rows keep 8 wavefronts (QKV with 16: 12.2 -> 12.8 us)
+        // workgroup widths that keep the Llama-8B grids whole multiples of
+        // the 256 CUs at B = 1: plain rows (the attention output projection)
+        // 16 rows per workgroup, 256 workgroups (9.5 -> 8.9 us against 8);
+        // QKV units six per workgroup, 512 workgroups (12.2 -> 11.8 us; with
+        // 16 wavefronts, 384 workgroups: 12.8 us); SwiGLU units keep four
+        // (3584 workgroups; seven per workgroup, 2048: 37 -> 70 us)
         if (EPI == EPI_ADD && PRO == PRO_NONE)
             return launch_one<TW, NR, PRO, EPI, 1, 8, 16, TAIL, MULTI>(g, units, n_host, s);
+        if (EPI == EPI_QKV)
+            return launch_one<TW, NR, PRO, EPI, 1, 8, 12, TAIL, MULTI>(g, units, n_host, s);
         return launch_one<TW, NR, PRO, EPI, 1, 8, 8, TAIL, MULTI>(g, units, n_host, s);
     }
     if constexpr (std::is_same<TW, float>::value) {
